@@ -1,0 +1,110 @@
+"""CPU oracle for the batched dataflow replay -- TEST INFRASTRUCTURE ONLY.
+
+Python side of ``oracle.c`` (ctypes, host numpy arrays).  Only ``tests/``,
+``__graft_entry__.smoke()`` and the benchmark's CPU-baseline leg use it; the
+library never imports it.  See ``oracle.h`` for the semantics.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB = os.path.join(HERE, "liboracle.so")
+
+OK, E_INVAL, E_RANGE, E_CYCLE, E_NOMEM = 0, -1, -2, -3, -4
+ST_BAD_DUR, ST_BAD_RES, ST_OVERFLOW = 1, 2, 4
+
+
+def build() -> str:
+    """Compile ``oracle.c`` with gcc into ``liboracle.so`` (always rebuilds)."""
+    tmp = LIB + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
+                           "-pthread", os.path.join(HERE, "oracle.c"), "-o", tmp])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+_lib = None
+
+
+def lib(path: Optional[str] = None):
+    """The loaded oracle library (``path`` loads another build of oracle.c)."""
+    global _lib
+    if path is not None or _lib is None:
+        if path is None and not os.path.exists(LIB):
+            build()
+        L = ctypes.CDLL(path or LIB)
+        P = ctypes.c_void_p
+        L.oracle_run_batch.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, ctypes.c_int64,
+                                       P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
+                                       P, ctypes.c_int32]
+        L.oracle_run_batch.restype = ctypes.c_int
+        L.oracle_critical_path.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, P, ctypes.c_int64,
+                                           P, ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
+        L.oracle_critical_path.restype = ctypes.c_int
+        if path is not None:
+            return L
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle error {code}")
+        self.code = code
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dt):
+    return None if a is None else np.ascontiguousarray(a, dtype=dt)
+
+
+def _threads(n_threads: Optional[int]) -> int:
+    return n_threads if n_threads else len(os.sched_getaffinity(0))
+
+
+def run_batch(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None,
+              want_finish: bool = True, n_threads: Optional[int] = None, library=None):
+    """Replay every scenario column of ``dur`` ([n_ops, n_scen] int32).
+
+    Returns ``(makespan [S], finish [n_ops, S] or None, status [S])``.
+    """
+    succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
+    op_res, prio = _c(op_res, np.int32), _c(prio, np.int32)
+    dur, place = _c(dur, np.int32), _c(place, np.uint16)
+    n = op_res.size
+    S = dur.shape[1] if dur.ndim == 2 else 0
+    makespan = np.empty(S, np.int32)
+    status = np.empty(S, np.int32)
+    finish = np.empty((n, S), np.int32) if want_finish else None
+    rc = (library or lib()).oracle_run_batch(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
+                                S, _ptr(dur), S, _ptr(place), S, _ptr(makespan), _ptr(finish), S,
+                                _ptr(status), _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return makespan, finish, status
+
+
+def critical_path(succ_ptr, succ_idx, n_ops: int, dur, path_scen: int = -1,
+                  n_threads: Optional[int] = None, library=None):
+    """Longest path per scenario; returns ``(cp_len [S], path or None)``."""
+    succ_ptr, succ_idx, dur = _c(succ_ptr, np.int64), _c(succ_idx, np.int32), _c(dur, np.int32)
+    S = dur.shape[1] if dur.ndim == 2 else 0
+    cp = np.empty(S, np.int32)
+    cap = max(n_ops, 1)
+    path = np.empty(cap, np.int32)
+    plen = np.zeros(1, np.int32)
+    rc = (library or lib()).oracle_critical_path(n_ops, _ptr(succ_ptr), _ptr(succ_idx), S, _ptr(dur), S,
+                                    _ptr(cp), path_scen, _ptr(path), cap, _ptr(plen),
+                                    _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return cp, (path[: int(plen[0])].copy() if path_scen >= 0 else None)

@@ -1,0 +1,418 @@
+/*
+ * CPU oracle for the batched dataflow replay -- TEST INFRASTRUCTURE ONLY.
+ * Only the tests and the benchmark's CPU-baseline leg load this library.
+ *
+ * It is a direct discrete-event simulation of the paper's simulation module
+ * (Sec. 2, "Dataflow based simulation"), one scenario at a time, with no
+ * blocking, fusion or reordering beyond what that loop states.  The global
+ * ready list is a binary min-heap of ops whose dependency counters reached
+ * zero, keyed by (ready time, priority, op id).  Popping it in key order
+ * serves every device's queue first-in-first-out by ready time: an op that
+ * becomes ready when its last predecessor finishes at time t is pushed with
+ * key t, strictly later than the key just popped because durations are at
+ * least 1 ns, so pops come out in nondecreasing key order, and everything
+ * that finishes at t is on the heap before the first op keyed t is popped.
+ * A popped op starts when both it is ready and its device has finished the
+ * previous op (the device's "finish time"), and the iteration time is the
+ * largest finish time of any device.
+ *
+ * The critical path (longest path, devices ignored) is a plain topological
+ * sweep; it is the iteration time with unlimited devices (Sec. 1: finding the
+ * performance bottleneck).
+ */
+#include "oracle.h"
+
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+  int32_t n, nres;
+  const int64_t *sp;
+  const int32_t *si;
+  const int32_t *res;
+  const int32_t *prio;
+  int32_t *indeg; /* number of incoming edge occurrences */
+} graph_t;
+
+/* Kahn's algorithm on the edge multiset: returns 1 if every op is ordered. */
+static int topo_order(const graph_t *g, int32_t *order) {
+  int32_t *cnt = (int32_t *)malloc(sizeof(int32_t) * (size_t)(g->n ? g->n : 1));
+  if (!cnt) return -1;
+  memcpy(cnt, g->indeg, sizeof(int32_t) * (size_t)g->n);
+  int32_t head = 0, tail = 0;
+  for (int32_t v = 0; v < g->n; ++v)
+    if (cnt[v] == 0) order[tail++] = v;
+  while (head < tail) {
+    int32_t v = order[head++];
+    for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e)
+      if (--cnt[g->si[e]] == 0) order[tail++] = g->si[e];
+  }
+  free(cnt);
+  return tail == g->n;
+}
+
+static int check_graph(graph_t *g, int need_res) {
+  if (g->n < 0 || (g->n > 0 && (!g->sp || (need_res && (!g->res || g->nres < 1)))))
+    return ORC_E_INVAL;
+  if (g->n == 0) return ORC_OK;
+  if (g->sp[0] != 0) return ORC_E_INVAL;
+  for (int32_t v = 0; v < g->n; ++v)
+    if (g->sp[v + 1] < g->sp[v]) return ORC_E_INVAL;
+  if (g->sp[g->n] > 0 && !g->si) return ORC_E_INVAL;
+  for (int64_t e = 0; e < g->sp[g->n]; ++e)
+    if (g->si[e] < 0 || g->si[e] >= g->n) return ORC_E_RANGE;
+  if (need_res)
+    for (int32_t v = 0; v < g->n; ++v)
+      if (g->res[v] < 0 || g->res[v] >= g->nres) return ORC_E_RANGE;
+  return ORC_OK;
+}
+
+static int build_indeg(graph_t *g) {
+  g->indeg = (int32_t *)calloc((size_t)(g->n ? g->n : 1), sizeof(int32_t));
+  if (!g->indeg) return ORC_E_NOMEM;
+  for (int64_t e = 0; e < (g->n ? g->sp[g->n] : 0); ++e) g->indeg[g->si[e]]++;
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------- replay */
+
+typedef struct {
+  int64_t *ready; /* [n] ready time of each op (max finish of its predecessors) */
+  int32_t *cnt;   /* [n] predecessors not yet finished */
+  int64_t *fin;   /* [n] finish time */
+  int64_t *rfree; /* [nres] time each device finishes its last op */
+  int32_t *heap;  /* [n] the ready list */
+  int32_t hsize;
+} sim_ws;
+
+/* key order of the ready list: ready time, then priority, then op id */
+static int key_less(const graph_t *g, const sim_ws *w, int32_t a, int32_t b) {
+  if (w->ready[a] != w->ready[b]) return w->ready[a] < w->ready[b];
+  int32_t pa = g->prio ? g->prio[a] : a, pb = g->prio ? g->prio[b] : b;
+  if (pa != pb) return pa < pb;
+  return a < b;
+}
+
+static void heap_push(const graph_t *g, sim_ws *w, int32_t v) {
+  int32_t i = w->hsize++;
+  w->heap[i] = v;
+  while (i > 0) {
+    int32_t p = (i - 1) / 2;
+    if (!key_less(g, w, w->heap[i], w->heap[p])) break;
+    int32_t t = w->heap[i];
+    w->heap[i] = w->heap[p];
+    w->heap[p] = t;
+    i = p;
+  }
+}
+
+static int32_t heap_pop(const graph_t *g, sim_ws *w) {
+  int32_t top = w->heap[0];
+  w->heap[0] = w->heap[--w->hsize];
+  int32_t i = 0;
+  for (;;) {
+    int32_t l = 2 * i + 1, r = l + 1, m = i;
+    if (l < w->hsize && key_less(g, w, w->heap[l], w->heap[m])) m = l;
+    if (r < w->hsize && key_less(g, w, w->heap[r], w->heap[m])) m = r;
+    if (m == i) break;
+    int32_t t = w->heap[i];
+    w->heap[i] = w->heap[m];
+    w->heap[m] = t;
+    i = m;
+  }
+  return top;
+}
+
+typedef struct {
+  const graph_t *g;
+  int64_t s0, s1;
+  const int32_t *dur;
+  int64_t ld_dur;
+  const uint16_t *place;
+  int64_t ld_place;
+  int32_t *makespan, *finish, *status;
+  int64_t ld_fin;
+  int rc;
+} run_job;
+
+static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
+  const graph_t *g = J->g;
+  int32_t st = 0;
+  /* per-scenario input checks */
+  for (int32_t v = 0; v < g->n; ++v) {
+    if (J->dur[(int64_t)v * J->ld_dur + s] < 1) st |= ORC_ST_BAD_DUR;
+    if (J->place && J->place[(int64_t)v * J->ld_place + s] >= (uint32_t)g->nres) st |= ORC_ST_BAD_RES;
+  }
+  int64_t span = 0;
+  if (!st) {
+    for (int32_t v = 0; v < g->n; ++v) {
+      w->ready[v] = 0;
+      w->cnt[v] = g->indeg[v];
+    }
+    for (int32_t r = 0; r < g->nres; ++r) w->rfree[r] = 0;
+    w->hsize = 0;
+    /* (1) every op with no predecessors is ready at t = 0 */
+    for (int32_t v = 0; v < g->n; ++v)
+      if (w->cnt[v] == 0) heap_push(g, w, v);
+    while (w->hsize > 0) {
+      int32_t v = heap_pop(g, w);
+      int32_t r = J->place ? (int32_t)J->place[(int64_t)v * J->ld_place + s] : g->res[v];
+      int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];
+      int64_t f = start + J->dur[(int64_t)v * J->ld_dur + s];
+      if (f > INT32_MAX) {
+        st |= ORC_ST_OVERFLOW;
+        break;
+      }
+      w->fin[v] = f;
+      w->rfree[r] = f;
+      /* (2) the finished op updates its successors' dependency counters */
+      for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e) {
+        int32_t x = g->si[e];
+        if (f > w->ready[x]) w->ready[x] = f;
+        if (--w->cnt[x] == 0) heap_push(g, w, x);
+      }
+    }
+    if (!st) /* the finish time of the last device */
+      for (int32_t r = 0; r < g->nres; ++r)
+        if (w->rfree[r] > span) span = w->rfree[r];
+  }
+  if (J->status) J->status[s] = st;
+  J->makespan[s] = st ? -1 : (int32_t)span;
+  if (J->finish && !st)
+    for (int32_t v = 0; v < g->n; ++v) J->finish[(int64_t)v * J->ld_fin + s] = (int32_t)w->fin[v];
+}
+
+static void *run_range(void *arg) {
+  run_job *J = (run_job *)arg;
+  const graph_t *g = J->g;
+  size_t n = (size_t)(g->n ? g->n : 1), R = (size_t)g->nres;
+  sim_ws w;
+  w.ready = (int64_t *)malloc(n * sizeof(int64_t));
+  w.cnt = (int32_t *)malloc(n * sizeof(int32_t));
+  w.fin = (int64_t *)malloc(n * sizeof(int64_t));
+  w.rfree = (int64_t *)malloc((R ? R : 1) * sizeof(int64_t));
+  w.heap = (int32_t *)malloc(n * sizeof(int32_t));
+  if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap) {
+    J->rc = ORC_E_NOMEM;
+  } else {
+    for (int64_t s = J->s0; s < J->s1; ++s) replay_one(J, &w, s);
+  }
+  free(w.ready);
+  free(w.cnt);
+  free(w.fin);
+  free(w.rfree);
+  free(w.heap);
+  return NULL;
+}
+
+static int run_threads(void *(*fn)(void *), void *jobs, size_t job_size, int64_t n_scen,
+                       int32_t n_threads, void (*set_range)(void *, int64_t, int64_t)) {
+  if (n_threads < 1) n_threads = 1;
+  if (n_scen < n_threads) n_threads = (int32_t)(n_scen > 0 ? n_scen : 1);
+  pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
+  if (!th) return ORC_E_NOMEM;
+  for (int32_t t = 0; t < n_threads; ++t) {
+    void *job = (char *)jobs + job_size * (size_t)t;
+    set_range(job, n_scen * t / n_threads, n_scen * (t + 1) / n_threads);
+  }
+  int32_t started = 0;
+  for (int32_t t = 1; t < n_threads; ++t) {
+    if (pthread_create(&th[t], NULL, fn, (char *)jobs + job_size * (size_t)t) != 0) break;
+    started = t;
+  }
+  fn(jobs);
+  for (int32_t t = 1; t <= started; ++t) pthread_join(th[t], NULL);
+  /* threads that could not be started run here */
+  for (int32_t t = started + 1; t < n_threads; ++t) fn((char *)jobs + job_size * (size_t)t);
+  free(th);
+  return ORC_OK;
+}
+
+static void set_run_range(void *p, int64_t a, int64_t b) {
+  ((run_job *)p)->s0 = a;
+  ((run_job *)p)->s1 = b;
+}
+
+int oracle_run_batch(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                     const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                     int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, int32_t *makespan,
+                     int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
+  graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL};
+  int rc = check_graph(&g, 1);
+  if (rc) return rc;
+  if (n_scen < 0 || (n_scen > 0 && !makespan)) return ORC_E_INVAL;
+  if (n_scen > 0 && n_ops > 0) {
+    if (!dur || ld_dur < n_scen) return ORC_E_INVAL;
+    if (place && ld_place < n_scen) return ORC_E_INVAL;
+    if (finish && ld_fin < n_scen) return ORC_E_INVAL;
+  }
+  if ((rc = build_indeg(&g))) return rc;
+  int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_ops ? n_ops : 1));
+  if (!order) {
+    free(g.indeg);
+    return ORC_E_NOMEM;
+  }
+  int acyclic = topo_order(&g, order);
+  free(order);
+  if (acyclic != 1) {
+    free(g.indeg);
+    return acyclic < 0 ? ORC_E_NOMEM : ORC_E_CYCLE;
+  }
+  if (n_threads < 1) n_threads = 1;
+  run_job *jobs = (run_job *)calloc((size_t)n_threads, sizeof(run_job));
+  if (!jobs) {
+    free(g.indeg);
+    return ORC_E_NOMEM;
+  }
+  for (int32_t t = 0; t < n_threads; ++t) {
+    run_job J = {&g, 0, 0, dur, ld_dur, place, ld_place, makespan, finish, status, ld_fin, 0};
+    jobs[t] = J;
+  }
+  rc = run_threads(run_range, jobs, sizeof(run_job), n_scen, n_threads, set_run_range);
+  for (int32_t t = 0; t < n_threads && !rc; ++t) rc = jobs[t].rc;
+  free(jobs);
+  free(g.indeg);
+  return rc;
+}
+
+/* --------------------------------------------------------- critical path */
+
+typedef struct {
+  const graph_t *g;
+  const int32_t *order;
+  int64_t s0, s1;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *cp_len;
+  int rc;
+} cp_job;
+
+/* dist(v) = d(v) + max over predecessors of dist, in topological order.
+ * Returns 0 on success, 1 on a bad duration or a path above INT32_MAX. */
+static int longest_paths(const graph_t *g, const int32_t *order, const int32_t *dur,
+                         int64_t ld_dur, int64_t s, int64_t *best, int64_t *dist) {
+  for (int32_t v = 0; v < g->n; ++v) best[v] = 0;
+  for (int32_t k = 0; k < g->n; ++k) {
+    int32_t v = order[k];
+    int32_t d = dur[(int64_t)v * ld_dur + s];
+    if (d < 1) return 1;
+    dist[v] = best[v] + d;
+    if (dist[v] > INT32_MAX) return 1;
+    for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e)
+      if (dist[v] > best[g->si[e]]) best[g->si[e]] = dist[v];
+  }
+  return 0;
+}
+
+static void *cp_range(void *arg) {
+  cp_job *J = (cp_job *)arg;
+  size_t n = (size_t)(J->g->n ? J->g->n : 1);
+  int64_t *best = (int64_t *)malloc(n * sizeof(int64_t));
+  int64_t *dist = (int64_t *)malloc(n * sizeof(int64_t));
+  if (!best || !dist) {
+    J->rc = ORC_E_NOMEM;
+  } else {
+    for (int64_t s = J->s0; s < J->s1; ++s) {
+      if (longest_paths(J->g, J->order, J->dur, J->ld_dur, s, best, dist)) {
+        J->cp_len[s] = -1;
+        continue;
+      }
+      int64_t m = 0;
+      for (int32_t v = 0; v < J->g->n; ++v)
+        if (dist[v] > m) m = dist[v];
+      J->cp_len[s] = (int32_t)m;
+    }
+  }
+  free(best);
+  free(dist);
+  return NULL;
+}
+
+static void set_cp_range(void *p, int64_t a, int64_t b) {
+  ((cp_job *)p)->s0 = a;
+  ((cp_job *)p)->s1 = b;
+}
+
+int oracle_critical_path(int32_t n_ops, const int64_t *succ_ptr, const int32_t *succ_idx,
+                         int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         int32_t *cp_len, int64_t path_scen, int32_t *path_ops,
+                         int32_t path_cap, int32_t *path_len, int32_t n_threads) {
+  graph_t g = {n_ops, 1, succ_ptr, succ_idx, NULL, NULL, NULL};
+  int rc = check_graph(&g, 0);
+  if (rc) return rc;
+  if (n_scen < 0 || (n_scen > 0 && !cp_len)) return ORC_E_INVAL;
+  if (n_scen > 0 && n_ops > 0 && (!dur || ld_dur < n_scen)) return ORC_E_INVAL;
+  if (path_scen >= n_scen || (path_scen >= 0 && (!path_len || (path_cap > 0 && !path_ops))))
+    return ORC_E_INVAL;
+  if ((rc = build_indeg(&g))) return rc;
+  int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_ops ? n_ops : 1));
+  if (!order) {
+    free(g.indeg);
+    return ORC_E_NOMEM;
+  }
+  int acyclic = topo_order(&g, order);
+  if (acyclic != 1) {
+    free(order);
+    free(g.indeg);
+    return acyclic < 0 ? ORC_E_NOMEM : ORC_E_CYCLE;
+  }
+  if (n_threads < 1) n_threads = 1;
+  cp_job *jobs = (cp_job *)calloc((size_t)n_threads, sizeof(cp_job));
+  if (!jobs) rc = ORC_E_NOMEM;
+  for (int32_t t = 0; t < n_threads && !rc; ++t) {
+    cp_job J = {&g, order, 0, 0, dur, ld_dur, cp_len, 0};
+    jobs[t] = J;
+  }
+  if (!rc) rc = run_threads(cp_range, jobs, sizeof(cp_job), n_scen, n_threads, set_cp_range);
+  for (int32_t t = 0; t < n_threads && !rc; ++t) rc = jobs[t].rc;
+  free(jobs);
+
+  if (!rc && path_scen >= 0) {
+    size_t n = (size_t)(n_ops ? n_ops : 1);
+    int64_t *best = (int64_t *)malloc(n * sizeof(int64_t));
+    int64_t *dist = (int64_t *)malloc(n * sizeof(int64_t));
+    int32_t *pred_ptr = (int32_t *)calloc(n + 1, sizeof(int32_t));
+    int32_t *pred_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_ops ? succ_ptr[n_ops] + 1 : 1));
+    int32_t *rev = (int32_t *)malloc(n * sizeof(int32_t));
+    if (!best || !dist || !pred_ptr || !pred_idx || !rev) {
+      rc = ORC_E_NOMEM;
+    } else if (n_ops == 0 || longest_paths(&g, order, dur, ld_dur, path_scen, best, dist)) {
+      *path_len = 0;
+    } else {
+      /* predecessor lists, for stepping back */
+      for (int32_t v = 0; v < n_ops; ++v) pred_ptr[v + 1] = g.indeg[v];
+      for (int32_t v = 0; v < n_ops; ++v) pred_ptr[v + 1] += pred_ptr[v];
+      int32_t *fill = rev; /* reuse as a cursor array first */
+      for (int32_t v = 0; v < n_ops; ++v) fill[v] = pred_ptr[v];
+      for (int32_t u = 0; u < n_ops; ++u)
+        for (int64_t e = succ_ptr[u]; e < succ_ptr[u + 1]; ++e) pred_idx[fill[succ_idx[e]]++] = u;
+      int32_t v = 0;
+      for (int32_t x = 1; x < n_ops; ++x)
+        if (dist[x] > dist[v]) v = x;
+      int32_t len = 0;
+      for (;;) {
+        rev[len++] = v;
+        int64_t want = dist[v] - dur[(int64_t)v * ld_dur + path_scen];
+        if (want == 0) break;
+        int32_t nxt = -1;
+        for (int32_t k = pred_ptr[v]; k < pred_ptr[v + 1]; ++k) {
+          int32_t p = pred_idx[k];
+          if (dist[p] == want && (nxt < 0 || p < nxt)) nxt = p;
+        }
+        v = nxt;
+      }
+      *path_len = len;
+      for (int32_t k = 0; k < len && k < path_cap; ++k) path_ops[k] = rev[len - 1 - k];
+    }
+    free(best);
+    free(dist);
+    free(pred_ptr);
+    free(pred_idx);
+    free(rev);
+  }
+  free(order);
+  free(g.indeg);
+  return rc;
+}

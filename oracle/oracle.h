@@ -1,0 +1,88 @@
+/*
+ * CPU oracle for the batched dataflow replay -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow discrete-event simulator written from the paper's
+ * description of its simulation module (Sec. 2, "Dataflow based
+ * simulation"): every device or link runs in parallel and keeps a job queue
+ * and its finish time; ready nodes are queued on their device; a finished
+ * op decrements its successors' dependency counters and a counter reaching
+ * zero makes the successor ready; the iteration time is the finish time of
+ * the last device.  It is used only by tests and by the benchmark's CPU
+ * baseline; nothing in the library calls it, links it or includes this
+ * header.
+ *
+ * Readings of points the paper leaves open (listed in the design notes):
+ *  - each device serves its queue first-in-first-out by ready time, one op
+ *    at a time, without preemption; equal ready times are served by lower
+ *    priority value, then lower op id;
+ *  - all ops that finish at time t are applied before anything starts at t;
+ *  - sources are ready at t = 0, every device is free at t = 0, edges add no
+ *    latency, durations are integer nanoseconds >= 1;
+ *  - a finish time above INT32_MAX is reported as an overflow, never wrapped.
+ *
+ * All functions take host pointers.  Graphs are given as successor CSR;
+ * repeated edges are allowed and behave like a single edge.
+ */
+#ifndef MLSIM_ORACLE_H
+#define MLSIM_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes (same numbering as the library's, by interface contract) */
+#define ORC_OK 0
+#define ORC_E_INVAL (-1)
+#define ORC_E_RANGE (-2)
+#define ORC_E_CYCLE (-3)
+#define ORC_E_NOMEM (-4)
+
+/* per-scenario status bits */
+#define ORC_ST_BAD_DUR 1
+#define ORC_ST_BAD_RES 2
+#define ORC_ST_OVERFLOW 4
+
+/*
+ * Replay every scenario s in [0, n_scen).
+ *   succ_ptr [n_ops+1], succ_idx [succ_ptr[n_ops]]: successor CSR.
+ *   op_res   [n_ops]: resource of each op, in [0, n_res).
+ *   prio     [n_ops] or NULL (NULL means prio[v] = v).
+ *   dur      [n_ops][ld_dur]: duration of op v in scenario s is dur[v*ld_dur+s].
+ *   place    [n_ops][ld_place] or NULL: if given, resource of v in s is
+ *            place[v*ld_place+s] instead of op_res[v].
+ * Outputs: makespan[s]; finish[v*ld_fin+s] if finish != NULL; status[s] if
+ * status != NULL.  A scenario with a bad duration (< 1), a bad placement or
+ * an overflow gets its status bits and makespan -1 (its finish values are
+ * then unspecified).  n_threads <= 0 means 1.
+ */
+int oracle_run_batch(int32_t n_ops, int32_t n_res,
+                     const int64_t *succ_ptr, const int32_t *succ_idx,
+                     const int32_t *op_res, const int32_t *prio,
+                     int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place,
+                     int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                     int32_t *status, int32_t n_threads);
+
+/*
+ * Longest path through the DAG, resources ignored: dist(v) = d(v) + max over
+ * predecessors p of dist(p) (0 without predecessors); cp_len[s] = max_v
+ * dist(v), 0 for an empty graph, -1 if a duration is < 1 or a path exceeds
+ * INT32_MAX.  If path_scen >= 0, the path of that scenario is written to
+ * path_ops (host, capacity path_cap) from its first op to its last, and its
+ * length to *path_len (the length is written even if it exceeds path_cap):
+ * the last op is the lowest-id op of maximum dist; each step back goes to
+ * the lowest-id predecessor p with dist(p) = dist(v) - d(v).
+ */
+int oracle_critical_path(int32_t n_ops,
+                         const int64_t *succ_ptr, const int32_t *succ_idx,
+                         int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         int32_t *cp_len, int64_t path_scen,
+                         int32_t *path_ops, int32_t path_cap, int32_t *path_len,
+                         int32_t n_threads);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,135 @@
+"""Independent brute-force replays used to pin the CPU oracle.
+
+Neither shares code with the oracle (which is C): they restate the paper's
+simulation loop (Sec. 2, "Dataflow based simulation") in two other ways.
+
+``tick_sim`` advances time one nanosecond at a time.  At each tick it first
+retires every op that finishes at that tick (decrementing its successors'
+dependency counters and appending newly ready ops to their device's job
+queue), then every idle device starts the op at the head of its queue.  Ops
+that become ready at the same tick enter a queue in (priority, id) order.
+
+``enumerate_orders`` tries every per-device order of the ops, computes the
+start times that order implies (an op starts when its predecessors and the
+previous op on its device have finished), and keeps the orders in which every
+device's sequence is sorted by (ready time, priority, id), i.e. a
+first-in-first-out queue by ready time.
+"""
+from __future__ import annotations
+
+import itertools
+from collections import deque
+
+import numpy as np
+
+
+def preds_of(n, succ_ptr, succ_idx):
+    P = [set() for _ in range(n)]
+    for u in range(n):
+        for e in range(int(succ_ptr[u]), int(succ_ptr[u + 1])):
+            P[int(succ_idx[e])].add(u)
+    return P
+
+
+def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
+    """One scenario: returns finish times (list) by 1-ns time stepping."""
+    prio = list(range(n)) if prio is None else [int(x) for x in prio]
+    P = preds_of(n, succ_ptr, succ_idx)
+    S = [set() for _ in range(n)]
+    for v in range(n):
+        for u in P[v]:
+            S[u].add(v)
+    cnt = [len(P[v]) for v in range(n)]
+    queue = [deque() for _ in range(n_res)]
+    running = [None] * n_res  # (op, finish)
+    finish = [None] * n
+    done = 0
+    arrivals = sorted((v for v in range(n) if cnt[v] == 0), key=lambda v: (prio[v], v))
+    for v in arrivals:
+        queue[int(res[v])].append(v)
+    t = 0
+    limit = int(np.sum(dur)) + 1
+    while done < n:
+        # retire everything finishing now
+        newly = []
+        for r in range(n_res):
+            if running[r] is not None and running[r][1] == t:
+                v = running[r][0]
+                running[r] = None
+                done += 1
+                for w in S[v]:
+                    cnt[w] -= 1
+                    if cnt[w] == 0:
+                        newly.append(w)
+        for w in sorted(newly, key=lambda v: (prio[v], v)):
+            queue[int(res[w])].append(w)
+        # idle devices start their queue heads
+        for r in range(n_res):
+            if running[r] is None and queue[r]:
+                v = queue[r].popleft()
+                finish[v] = t + int(dur[v])
+                running[r] = (v, finish[v])
+        t += 1
+        if t > limit:
+            raise RuntimeError("tick simulation did not terminate")
+    return finish
+
+
+def _times_for_order(n, P, res, dur, orders):
+    """Start/finish/ready times implied by per-device orders, or None if the
+    orders contradict the DAG (a cycle through device and data edges)."""
+    prev_on_dev = {}
+    for seq in orders:
+        for a, b in zip(seq, seq[1:]):
+            prev_on_dev[b] = a
+    finish = [None] * n
+    ready = [None] * n
+    remaining = set(range(n))
+    while remaining:
+        progress = False
+        for v in sorted(remaining):
+            if all(finish[u] is not None for u in P[v]) and (
+                    v not in prev_on_dev or finish[prev_on_dev[v]] is not None):
+                ready[v] = max([finish[u] for u in P[v]], default=0)
+                start = max(ready[v], finish[prev_on_dev[v]] if v in prev_on_dev else 0)
+                finish[v] = start + int(dur[v])
+                remaining.discard(v)
+                progress = True
+        if not progress:
+            return None
+    return ready, finish
+
+
+def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
+    """All per-device orders whose implied schedule is FIFO by (ready, prio, id).
+
+    Returns a list of finish-time lists, one per consistent order.
+    """
+    prio = list(range(n)) if prio is None else [int(x) for x in prio]
+    P = preds_of(n, succ_ptr, succ_idx)
+    on = [[v for v in range(n) if int(res[v]) == r] for r in range(n_res)]
+    found = []
+    for orders in itertools.product(*[itertools.permutations(o) for o in on]):
+        tr = _times_for_order(n, P, res, dur, orders)
+        if tr is None:
+            continue
+        ready, finish = tr
+        ok = all((ready[a], prio[a], a) < (ready[b], prio[b], b)
+                 for seq in orders for a, b in zip(seq, seq[1:]))
+        if ok:
+            found.append(finish)
+    return found
+
+
+def all_path_lengths(n, succ_ptr, succ_idx, dur):
+    """Longest path by enumerating every source-to-sink path (tiny DAGs)."""
+    S = [[int(succ_idx[e]) for e in range(int(succ_ptr[u]), int(succ_ptr[u + 1]))] for u in range(n)]
+    P = preds_of(n, succ_ptr, succ_idx)
+    best = 0
+    stack = [(v, int(dur[v])) for v in range(n) if not P[v]]
+    while stack:
+        v, L = stack.pop()
+        best = max(best, L)
+        for w in S[v]:
+            stack.append((w, L + int(dur[w])))
+    return best

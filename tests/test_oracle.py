@@ -1,0 +1,414 @@
+"""Pins of the CPU oracle against what the paper's model and mathematics fix.
+
+The oracle (oracle/oracle.c) replays the simulation loop of Sec. 2
+("Dataflow based simulation").  Nothing here re-runs the oracle's own code to
+check it: the pins are hand-derived worked examples, closed forms, bounds,
+structural invariants of a FIFO device, metamorphic relations, a library
+shortest-path routine, and two independent brute-force replays (tests/brute.py).
+"""
+import numpy as np
+import pytest
+import scipy.sparse
+import scipy.sparse.csgraph
+
+import oracle
+import brute
+import goldens
+from paper_2002_06790_amd.workloads import random_dag, random_durations
+
+
+# ------------------------------------------------------------------ helpers
+
+def oracle_run(library, *a, **kw):
+    return oracle.run_batch(*a, library=library, **kw)
+
+
+def oracle_cp(library, *a, **kw):
+    return oracle.critical_path(*a, library=library, **kw)
+
+
+def run(g, dur, library=None, **kw):
+    return oracle.run_batch(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], dur,
+                            prio=g.get("prio"), library=library, **kw)
+
+
+def rand_graph(rng, n, n_res, p, prio=False, dup=False, shuffle=True):
+    ptr, idx, res, pr = random_dag(n, n_res, p, rng, shuffle_ids=shuffle, with_prio=prio,
+                                   dup_edges=dup)
+    return dict(n=n, n_res=n_res, succ_ptr=ptr, succ_idx=idx, op_res=res, prio=pr)
+
+
+def preds(g):
+    return brute.preds_of(g["n"], g["succ_ptr"], g["succ_idx"])
+
+
+def schedule_checks(g, dur_col, fin_col, span):
+    """Structural invariants of one scenario's schedule (FIFO devices)."""
+    n = g["n"]
+    P = preds(g)
+    prio = g["prio"] if g["prio"] is not None else np.arange(n)
+    d = dur_col.astype(np.int64)
+    f = fin_col.astype(np.int64)
+    start = f - d
+    ready = np.array([max([f[u] for u in P[v]], default=0) for v in range(n)])
+    assert (start >= ready).all(), "an op starts before its inputs are ready"
+    assert span == (f.max() if n else 0)
+    for r in range(g["n_res"]):
+        ops = [v for v in range(n) if g["op_res"][v] == r]
+        ops.sort(key=lambda v: start[v])
+        prev_fin = 0
+        for k, v in enumerate(ops):
+            assert start[v] >= prev_fin, "two ops overlap on one device"
+            # non-delay: a device never idles while its queue is non-empty
+            assert start[v] == max(ready[v], prev_fin)
+            prev_fin = f[v]
+            if k:
+                u = ops[k - 1]
+                assert (ready[u], prio[u], u) < (ready[v], prio[v], v), "device not FIFO by key"
+    return start, ready
+
+
+# ------------------------------------------------------------------ goldens
+
+@pytest.mark.parametrize("g", goldens.all_goldens(), ids=lambda g: g["name"])
+def test_worked_examples(g, library):
+    ex = g["expect"]
+    mk, fin, st = run(g, g["dur"], library=library)
+    assert st.tolist() == [0]
+    assert fin[:, 0].tolist() == ex["finish"]
+    assert mk.tolist() == ex["makespan"]
+    if "cp_len" in ex:
+        cp, path = oracle_cp(library, g["succ_ptr"], g["succ_idx"], g["n"], g["dur"], 0)
+        assert cp.tolist() == ex["cp_len"]
+        assert path.tolist() == ex["cp_path"]
+    if "dur2" in ex:
+        d2 = np.array(ex["dur2"], np.int32)[:, None]
+        mk2, fin2, _ = run(g, d2, library=library)
+        assert fin2[:, 0].tolist() == ex["finish2"]
+        assert mk2.tolist() == ex["makespan2"]
+
+
+@pytest.mark.parametrize("g", goldens.all_goldens(), ids=lambda g: g["name"])
+def test_worked_examples_tick_sim(g, library):
+    """The brute-force tick simulator reproduces the hand-derived values."""
+    fin = brute.tick_sim(g["n"], g["n_res"], g["succ_ptr"], g["succ_idx"], g["op_res"],
+                         g["dur"][:, 0], g["prio"])
+    assert fin == g["expect"]["finish"]
+
+
+# -------------------------------------------------------------- closed forms
+
+def test_no_edges_prefix_sums(library):
+    """Without edges each device runs its ops in (priority, id) order back to back."""
+    rng = np.random.default_rng(1)
+    for _ in range(30):
+        n, R = int(rng.integers(1, 40)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, 0.0, prio=bool(rng.integers(2)))
+        dur = random_durations(n, 3, 1, 50, rng)
+        mk, fin, _ = run(g, dur, library=library)
+        prio = g["prio"] if g["prio"] is not None else np.arange(n)
+        for s in range(3):
+            expect = np.zeros(n, np.int64)
+            for r in range(R):
+                ops = sorted((v for v in range(n) if g["op_res"][v] == r), key=lambda v: (prio[v], v))
+                expect[ops] = np.cumsum(dur[ops, s])
+            assert (fin[:, s] == expect).all()
+            assert mk[s] == expect.max()
+
+
+def test_chain_cumulative_sums(library):
+    """A chain runs back to back whatever its devices: finish = prefix sums."""
+    rng = np.random.default_rng(2)
+    for _ in range(30):
+        n, R = int(rng.integers(1, 60)), int(rng.integers(1, 6))
+        order = rng.permutation(n)
+        succ = [[] for _ in range(n)]
+        for a, b in zip(order, order[1:]):
+            succ[a].append(int(b))
+        ptr = np.zeros(n + 1, np.int64)
+        ptr[1:] = np.cumsum([len(s) for s in succ])
+        idx = np.array([w for s in succ for w in s], np.int32)
+        res = rng.integers(0, R, n).astype(np.int32)
+        dur = random_durations(n, 4, 1, 1000, rng)
+        mk, fin, _ = oracle_run(library, ptr, idx, res, R, dur)
+        assert (fin[order] == np.cumsum(dur[order], axis=0)).all()
+        assert (mk == dur.sum(0)).all()
+
+
+def test_single_device_makespan_is_total_work(library):
+    """With one device it never idles: makespan = sum of durations."""
+    rng = np.random.default_rng(3)
+    for _ in range(30):
+        n = int(rng.integers(1, 80))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.3)), prio=True)
+        dur = random_durations(n, 5, 1, 100, rng)
+        mk, _, _ = run(g, dur, library=library)
+        assert (mk == dur.sum(0)).all()
+
+
+def longest_path_scipy(g, dur_col):
+    """Longest path via scipy's Bellman-Ford on negated node weights."""
+    n = g["n"]
+    src, dst, w = [], [], []
+    ptr, idx = g["succ_ptr"], g["succ_idx"]
+    seen = set()
+    for u in range(n):
+        for e in range(ptr[u], ptr[u + 1]):
+            v = int(idx[e])
+            if (u, v) not in seen:
+                seen.add((u, v))
+                src.append(u), dst.append(v), w.append(-float(dur_col[v]))
+    for v in range(n):  # virtual source n
+        src.append(n), dst.append(v), w.append(-float(dur_col[v]))
+    A = scipy.sparse.csr_matrix((w, (src, dst)), shape=(n + 1, n + 1))
+    D = scipy.sparse.csgraph.shortest_path(A, method="BF", directed=True, indices=n)
+    return -D[:n]
+
+
+def test_unlimited_devices_equals_longest_path(library):
+    """One device per op: finish = longest path to the op; makespan = critical path."""
+    rng = np.random.default_rng(4)
+    for _ in range(25):
+        n = int(rng.integers(1, 60))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.25)))
+        g["n_res"] = n
+        g["op_res"] = np.arange(n, dtype=np.int32)
+        dur = random_durations(n, 3, 1, 1000, rng)
+        mk, fin, _ = run(g, dur, library=library)
+        cp, _ = oracle_cp(library, g["succ_ptr"], g["succ_idx"], n, dur)
+        for s in range(3):
+            dist = longest_path_scipy(g, dur[:, s])
+            assert (fin[:, s] == dist).all()
+            assert mk[s] == cp[s] == dist.max()
+
+
+# -------------------------------------------------------------- brute force
+
+def test_matches_tick_simulator(library):
+    rng = np.random.default_rng(5)
+    for _ in range(150):
+        n, R = int(rng.integers(1, 9)), int(rng.integers(1, 4))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.6)), prio=bool(rng.integers(2)),
+                       dup=bool(rng.integers(2)))
+        dur = random_durations(n, 2, 1, 6, rng)
+        mk, fin, _ = run(g, dur, library=library)
+        for s in range(2):
+            ref = brute.tick_sim(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, s], g["prio"])
+            assert fin[:, s].tolist() == ref
+            assert mk[s] == max(ref)
+
+
+def test_unique_fifo_consistent_order(library):
+    """Exactly one per-device order is FIFO by (ready, prio, id); it is the oracle's."""
+    rng = np.random.default_rng(6)
+    for _ in range(60):
+        n, R = int(rng.integers(1, 7)), int(rng.integers(1, 3))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.6)), prio=bool(rng.integers(2)))
+        dur = random_durations(n, 1, 1, 6, rng)
+        _, fin, _ = run(g, dur, library=library)
+        found = brute.enumerate_orders(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0],
+                                       g["prio"])
+        assert len(found) == 1
+        assert found[0] == fin[:, 0].tolist()
+
+
+# --------------------------------------------------------------- invariants
+
+def test_bounds_and_structure_random(library):
+    rng = np.random.default_rng(7)
+    for _ in range(30):
+        n, R = int(rng.integers(1, 300)), int(rng.integers(1, 12))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 8.0 / max(n, 1))), prio=bool(rng.integers(2)))
+        dur = random_durations(n, 3, 1, 10_000, rng)
+        mk, fin, st = run(g, dur, library=library)
+        cp, _ = oracle_cp(library, g["succ_ptr"], g["succ_idx"], n, dur)
+        assert (st == 0).all()
+        for s in range(3):
+            schedule_checks(g, dur[:, s], fin[:, s], mk[s])
+            busy = np.bincount(g["op_res"], weights=dur[:, s], minlength=R).max()
+            assert max(cp[s], busy) <= mk[s] <= dur[:, s].sum()
+
+
+def test_scaling_durations_scales_times(library):
+    rng = np.random.default_rng(8)
+    for _ in range(15):
+        n, R = int(rng.integers(1, 100)), int(rng.integers(1, 6))
+        g = rand_graph(rng, n, R, 0.05, prio=True)
+        dur = random_durations(n, 3, 1, 100, rng)
+        k = int(rng.integers(2, 50))
+        mk, fin, _ = run(g, dur, library=library)
+        mk2, fin2, _ = run(g, dur * k, library=library)
+        assert (mk2 == k * mk).all() and (fin2 == k * fin).all()
+
+
+def test_relabel_resources_and_shuffle_columns(library):
+    rng = np.random.default_rng(9)
+    for _ in range(15):
+        n, R = int(rng.integers(1, 100)), int(rng.integers(1, 8))
+        g = rand_graph(rng, n, R, 0.05)
+        dur = random_durations(n, 16, 1, 100, rng)
+        mk, fin, _ = run(g, dur, library=library)
+        perm = rng.permutation(R).astype(np.int32)
+        g2 = dict(g, op_res=perm[g["op_res"]])
+        cols = rng.permutation(16)
+        mk2, fin2, _ = run(g2, dur[:, cols], library=library)
+        assert (mk2 == mk[cols]).all() and (fin2 == fin[:, cols]).all()
+
+
+def test_relabel_ops_with_equivalent_priorities(library):
+    """Renumbering ops while keeping their (priority, id) order keeps the schedule."""
+    rng = np.random.default_rng(10)
+    for _ in range(15):
+        n, R = int(rng.integers(2, 80)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, 0.08, prio=True)
+        dur = random_durations(n, 4, 1, 8, rng)  # small values: many ties
+        mk, fin, _ = run(g, dur, library=library)
+        pi = rng.permutation(n)  # old id -> new id
+        rank = np.empty(n, np.int32)
+        rank[np.lexsort((np.arange(n), g["prio"]))] = np.arange(n)
+        succ = [[] for _ in range(n)]
+        for u in range(n):
+            for e in range(g["succ_ptr"][u], g["succ_ptr"][u + 1]):
+                succ[pi[u]].append(int(pi[g["succ_idx"][e]]))
+        ptr = np.zeros(n + 1, np.int64)
+        ptr[1:] = np.cumsum([len(s) for s in succ])
+        idx = np.array([w for s in succ for w in s], np.int32)
+        res2 = np.empty(n, np.int32)
+        res2[pi] = g["op_res"]
+        prio2 = np.empty(n, np.int32)
+        prio2[pi] = rank
+        dur2 = np.empty_like(dur)
+        dur2[pi] = dur
+        mk2, fin2, _ = oracle_run(library, ptr, idx, res2, R, dur2, prio=prio2)
+        assert (mk2 == mk).all() and (fin2[pi] == fin).all()
+
+
+def test_static_replay_of_emergent_order(library):
+    """Replaying the oracle's own per-device order reproduces its times."""
+    rng = np.random.default_rng(11)
+    for _ in range(20):
+        n, R = int(rng.integers(1, 40)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, 0.1)
+        dur = random_durations(n, 1, 1, 50, rng)
+        _, fin, _ = run(g, dur, library=library)
+        start = fin[:, 0] - dur[:, 0]
+        orders = [sorted((v for v in range(n) if g["op_res"][v] == r), key=lambda v: start[v])
+                  for r in range(R)]
+        ready, f2 = brute._times_for_order(n, preds(g), g["op_res"], dur[:, 0], orders)
+        assert f2 == fin[:, 0].tolist()
+
+
+def test_duplicate_edges_change_nothing(library):
+    rng = np.random.default_rng(12)
+    for _ in range(20):
+        n, R = int(rng.integers(2, 60)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, 0.1)
+        succ = [list(g["succ_idx"][g["succ_ptr"][u]:g["succ_ptr"][u + 1]]) for u in range(n)]
+        for u in range(n):  # repeat some edges, in shuffled positions
+            if succ[u] and rng.integers(2):
+                succ[u] = list(rng.permutation(succ[u] + list(rng.choice(succ[u], 2))))
+        ptr = np.zeros(n + 1, np.int64)
+        ptr[1:] = np.cumsum([len(x) for x in succ])
+        gd = dict(g, succ_ptr=ptr, succ_idx=np.array([w for x in succ for w in x], np.int32))
+        dur = random_durations(n, 3, 1, 20, rng)
+        a, b = run(g, dur, library=library), run(gd, dur, library=library)
+        assert (a[0] == b[0]).all() and (a[1] == b[1]).all()
+
+
+def test_placement_overrides_op_res(library):
+    """place[v, s] is the resource of v in scenario s (the per-op "device" property)."""
+    rng = np.random.default_rng(13)
+    n, R, S = 50, 6, 12
+    g = rand_graph(rng, n, R, 0.08)
+    dur = random_durations(n, S, 1, 30, rng)
+    place = rng.integers(0, R, size=(n, S)).astype(np.uint16)
+    mk, fin, st = run(g, dur, place=place, library=library)
+    assert (st == 0).all()
+    for s in range(S):
+        gs = dict(g, op_res=place[:, s].astype(np.int32))
+        mk1, fin1, _ = run(gs, dur[:, s:s + 1], library=library)
+        assert mk1[0] == mk[s] and (fin1[:, 0] == fin[:, s]).all()
+
+
+# ------------------------------------------------------------ critical path
+
+def test_critical_path_brute_force_and_path(library):
+    rng = np.random.default_rng(14)
+    for _ in range(60):
+        n = int(rng.integers(1, 10))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.6)), dup=bool(rng.integers(2)))
+        dur = random_durations(n, 3, 1, 5, rng)
+        cp, _ = oracle_cp(library, g["succ_ptr"], g["succ_idx"], n, dur)
+        for s in range(3):
+            assert cp[s] == brute.all_path_lengths(n, g["succ_ptr"], g["succ_idx"], dur[:, s])
+            _, path = oracle_cp(library, g["succ_ptr"], g["succ_idx"], n, dur, s)
+            assert dur[path, s].sum() == cp[s]
+            P = preds(g)
+            assert not P[path[0]]
+            for a, b in zip(path, path[1:]):
+                assert a in P[b]
+            # tie rules: the last op is the lowest id reaching cp; each step back
+            # takes the lowest-id predecessor that lies on a longest path
+            dist = longest_path_scipy(g, dur[:, s])
+            assert path[-1] == int(np.nonzero(dist == cp[s])[0][0])
+            for a, b in zip(path, path[1:]):
+                cands = [p for p in P[b] if dist[p] == dist[b] - dur[b, s]]
+                assert a == min(cands)
+
+
+# ------------------------------------------------------------------- errors
+
+def test_errors_and_status(library):
+    ptr = np.array([0, 1, 1], np.int64)
+    idx = np.array([1], np.int32)
+    res = np.array([0, 0], np.int32)
+    dur = np.array([[1, 0, 5, 1_500_000_000], [1, 1, 5, 1_500_000_000]], np.int32)
+    mk, fin, st = oracle_run(library, ptr, idx, res, 1, dur)
+    assert st.tolist() == [0, oracle.ST_BAD_DUR, 0, oracle.ST_OVERFLOW]
+    assert mk.tolist() == [2, -1, 10, -1]
+    cp, _ = oracle_cp(library, ptr, idx, 2, dur)
+    assert cp.tolist() == [2, -1, 10, -1]
+    place = np.array([[0, 0, 0, 0], [0, 1, 7, 0]], np.uint16)
+    mk, _, st = oracle_run(library, ptr, idx, res, 2, dur, place=place)
+    assert st.tolist() == [0, oracle.ST_BAD_DUR, oracle.ST_BAD_RES, oracle.ST_OVERFLOW]
+    assert mk.tolist() == [2, -1, -1, -1]
+    d1 = dur[:, :1]
+    with pytest.raises(oracle.OracleError) as e:  # cycle 0 -> 1 -> 0
+        oracle_run(library, np.array([0, 1, 2]), np.array([1, 0]), res, 1, d1)
+    assert e.value.code == oracle.E_CYCLE
+    with pytest.raises(oracle.OracleError) as e:  # self loop
+        oracle_run(library, np.array([0, 1, 1]), np.array([0]), res, 1, d1)
+    assert e.value.code == oracle.E_CYCLE
+    with pytest.raises(oracle.OracleError) as e:  # successor out of range
+        oracle_run(library, ptr, np.array([2]), res, 1, d1)
+    assert e.value.code == oracle.E_RANGE
+    with pytest.raises(oracle.OracleError) as e:  # resource out of range
+        oracle_run(library, ptr, idx, np.array([0, 1], np.int32), 1, d1)
+    assert e.value.code == oracle.E_RANGE
+    with pytest.raises(oracle.OracleError) as e:  # decreasing pointers
+        oracle_run(library, np.array([0, 1, 0]), idx, res, 1, d1)
+    assert e.value.code == oracle.E_INVAL
+    with pytest.raises(oracle.OracleError) as e:
+        oracle_cp(library, np.array([0, 1, 2]), np.array([1, 0]), 2, d1)
+    assert e.value.code == oracle.E_CYCLE
+
+
+def test_empty_graph_and_zero_scenarios(library):
+    e = np.zeros(1, np.int64)
+    mk, fin, st = oracle_run(library, e, np.zeros(0, np.int32), np.zeros(0, np.int32), 1,
+                                   np.zeros((0, 5), np.int32))
+    assert mk.tolist() == [0] * 5 and st.tolist() == [0] * 5
+    cp, _ = oracle_cp(library, e, np.zeros(0, np.int32), 0, np.zeros((0, 5), np.int32))
+    assert cp.tolist() == [0] * 5
+    mk, _, _ = oracle_run(library, np.array([0, 0]), np.zeros(0, np.int32), np.array([0], np.int32), 1,
+                                np.zeros((1, 0), np.int32))
+    assert mk.size == 0
+
+
+def test_threads_do_not_change_results(library):
+    rng = np.random.default_rng(15)
+    g = rand_graph(rng, 120, 5, 0.04, prio=True)
+    dur = random_durations(120, 97, 1, 500, rng)
+    a = run(g, dur, n_threads=1, library=library)
+    b = run(g, dur, n_threads=7, library=library)
+    assert all((x == y).all() for x, y in zip(a, b))

@@ -1,0 +1,76 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of oracle/oracle.c (on the CPU, in a
+temporary directory), builds it with gcc, and runs every pin of
+tests/test_oracle.py against that build: at least one pin must fail.
+"""
+import inspect
+import os
+import subprocess
+
+import pytest
+
+import goldens
+import oracle
+import test_oracle
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+# (name, original text, planted mistake)
+MUTANTS = [
+    ("id-before-ready", "if (w->ready[a] != w->ready[b]) return w->ready[a] < w->ready[b];\n"
+                        "  int32_t pa",
+     "int32_t pa"),
+    ("ignore-priority", "if (pa != pb) return pa < pb;", ""),
+    ("ready-tie-by-higher-id", "return a < b;\n}", "return a > b;\n}"),
+    ("ignore-device-busy", "int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];",
+     "int64_t start = w->ready[v];"),
+    ("ignore-inputs", "int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];",
+     "int64_t start = w->rfree[r];"),
+    ("min-instead-of-max", "if (f > w->ready[x]) w->ready[x] = f;", "if (f < w->ready[x] || w->ready[x] == 0) w->ready[x] = f;"),
+    ("ready-on-first-pred", "if (--w->cnt[x] == 0) heap_push(g, w, x);",
+     "if (w->cnt[x]-- == g->indeg[x]) heap_push(g, w, x);"),
+    ("makespan-of-device-0", "for (int32_t r = 0; r < g->nres; ++r)\n        if (w->rfree[r] > span)",
+     "for (int32_t r = 0; r < 1; ++r)\n        if (w->rfree[r] > span)"),
+    ("placement-ignored", "int32_t r = J->place ? (int32_t)J->place[(int64_t)v * J->ld_place + s] : g->res[v];",
+     "int32_t r = g->res[v];"),
+    ("overflow-wraps", "if (f > INT32_MAX) {", "if (0) {"),
+    ("accepts-zero-duration", "if (J->dur[(int64_t)v * J->ld_dur + s] < 1) st |= ORC_ST_BAD_DUR;",
+     "if (J->dur[(int64_t)v * J->ld_dur + s] < 0) st |= ORC_ST_BAD_DUR;"),
+    ("cp-drops-own-duration", "dist[v] = best[v] + d;", "dist[v] = best[v] + (best[v] ? 0 : d);"),
+    ("cp-path-highest-id", "if (dist[p] == want && (nxt < 0 || p < nxt)) nxt = p;",
+     "if (dist[p] == want && (nxt < 0 || p > nxt)) nxt = p;"),
+    ("cp-end-highest-id", "if (dist[x] > dist[v]) v = x;", "if (dist[x] >= dist[v]) v = x;"),
+    ("cycle-undetected", "return tail == g->n;", "return 1;"),
+]
+
+
+def pins():
+    for name, fn in inspect.getmembers(test_oracle, inspect.isfunction):
+        if not name.startswith("test_"):
+            continue
+        if "g" in inspect.signature(fn).parameters:
+            for g in goldens.all_goldens():
+                yield f"{name}[{g['name']}]", (lambda fn=fn, g=g: lambda L: fn(g=g, library=L))()
+        else:
+            yield name, (lambda fn=fn: lambda L: fn(library=L))()
+
+
+@pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmp_path, name, orig, mut):
+    src = open(SRC).read()
+    assert src.count(orig) == 1, f"mutation site of {name} not found"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(orig, mut))
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-pthread",
+                           "-I", os.path.dirname(SRC), str(path), "-o", str(so)])
+    L = oracle.lib(str(so))
+    caught = []
+    for pin_name, pin in pins():
+        try:
+            pin(L)
+        except (Exception, pytest.fail.Exception) as e:  # a failing pin
+            caught.append((pin_name, type(e).__name__))
+            break
+    assert caught, f"no pin catches mutant {name}"
