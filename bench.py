@@ -1,0 +1,184 @@
+#!/usr/bin/env python3
+"""Throughput of the batched dataflow replay on one MI355X.
+
+One step = one pass of the whole hot path over one batch: ``sim_run_batch``
+(event-driven replay of every scenario, finish times written) followed by
+``sim_critical_path``.  Inputs are generated on the host, copied to HBM and
+resident before the timed region starts.  Prints one JSON line.
+
+Default workload: the BERT-large data-parallel graph (16 workers, per-worker
+up/down links; 6624 ops, 48 resources) at 262144 scenarios spanning 12
+strategy knobs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4, help="workload 1..5")
+    ap.add_argument("--scenarios", type=int, default=None)
+    ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep"))
+    ap.add_argument("--cpu-sample", type=int, default=65536,
+                    help="scenarios of the same workload timed on the CPU oracle (0: skip)")
+    ap.add_argument("--no-check", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "scenarios shard across GPUs without communication, but this build measures one GPU only.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2002_06790_amd as mlsim
+    from paper_2002_06790_amd import workloads
+
+    if not os.path.exists(mlsim.LIB_PATH):
+        mlsim.build()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    w = workloads.make_config(args.config, n_scen=args.scenarios)
+    n, S = w.n_ops, w.n_scen
+    log(f"workload {w.name}: n={n} R={w.n_res} S={S}; generating durations")
+    t = time.time()
+    dur_h = w.durations()
+    place_h = w.placement()
+    log(f"generated in {time.time() - t:.1f}s; copying to HBM")
+    t = time.time()
+    dur = torch.from_numpy(dur_h).cuda()
+    place = None
+    if place_h is not None:
+        place = torch.from_numpy(place_h.view(np.int16)).cuda().view(torch.uint16)
+    torch.cuda.synchronize()
+    h2d_s = time.time() - t
+    g = mlsim.Graph.from_workload(w)
+    info = g.info()
+    makespan = torch.empty(S, dtype=torch.int32, device="cuda")
+    status = torch.empty(S, dtype=torch.int32, device="cuda")
+    finish = torch.empty((n, S), dtype=torch.int32, device="cuda")
+    cp_len = torch.empty(S, dtype=torch.int32, device="cuda")
+
+    def step():
+        e0.record()
+        g.run(dur, place=place, algo=args.algo, makespan=makespan, finish=finish, status=status)
+        e1.record()
+        g.critical_path(dur, cp_len=cp_len)
+        e2.record()
+
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    log(f"graph compiled {info}; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev_ms, cp_ms = [], []
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+        e2.synchronize()
+        ev_ms.append(e0.elapsed_time(e1))
+        cp_ms.append(e1.elapsed_time(e2))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"ms/step {ms_per_step:.3f} (run_batch {np.mean(ev_ms):.3f} ms, critical_path {np.mean(cp_ms):.3f} ms)")
+
+    # sampled parity against the oracle (outside the timed region)
+    parity = None
+    if not args.no_check:
+        import oracle
+        rng = np.random.default_rng(0)
+        scen = np.unique(np.r_[0, S - 1, rng.integers(0, S, 30)])
+        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h[:, scen],
+                                          place=None if place_h is None else place_h[:, scen])
+        ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, n, dur_h[:, scen])
+        sel = torch.from_numpy(scen).cuda()
+        ok = (np.array_equal(makespan[sel].cpu().numpy(), omk)
+              and np.array_equal(finish[:, sel].cpu().numpy(), ofin)
+              and np.array_equal(status[sel].cpu().numpy(), ost)
+              and np.array_equal(cp_len[sel].cpu().numpy(), ocp))
+        parity = f"{'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
+        log(parity)
+
+    # CPU oracle baseline on a bounded sample of the same workload
+    cpu = None
+    if args.cpu_sample:
+        import oracle
+        cs = min(args.cpu_sample, S)
+        threads = min(16, len(os.sched_getaffinity(0)))
+        sub = np.ascontiguousarray(dur_h[:, :cs])
+        psub = None if place_h is None else np.ascontiguousarray(place_h[:, :cs])
+        log(f"cpu oracle on {cs} scenarios, {threads} threads")
+        t = time.perf_counter()
+        oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, place=psub,
+                         want_finish=True, n_threads=threads)
+        oracle.critical_path(w.succ_ptr, w.succ_idx, n, sub, n_threads=threads)
+        cpu_s = time.perf_counter() - t
+        cpu = {"value": n * cs / cpu_s, "unit": "op-events/s", "cores": threads, "kind": "oracle",
+               "sample": f"first {cs} of {S} scenarios (run_batch with finish times + critical_path), "
+                         f"{cpu_s:.2f} s"}
+        log(f"cpu oracle {cpu['value']:.3e} op-events/s")
+
+    op_events = n * S
+    ev_s = float(np.mean(ev_ms)) / 1e3
+    alg_bytes = op_events * (4 + 4 + (2 if place is not None else 0)) + S * 8
+    achieved = alg_bytes / ev_s / 1e9
+    out = {
+        "metric": "simulated op-events/sec and scenarios/sec at 1 GPU; % of HBM roofline",
+        "value": op_events / (ms_per_step / 1e3),
+        "unit": "op-events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {n} ops, {info['n_edges']} edges after reduction, "
+                               f"{w.n_res} resources, {S} scenarios", "n_ops": n, "n_scen": S,
+                   "algo": args.algo, "finish_times": True, "parallelism": "single GPU"},
+        "scenarios_per_s": S / (ms_per_step / 1e3),
+        "kernels": {"run_batch_ms": float(np.mean(ev_ms)), "critical_path_ms": float(np.mean(cp_ms)),
+                    "run_batch_op_events_per_s": op_events / ev_s,
+                    "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "kernel": "k_event (sim_run_batch)",
+                     "bytes_per_launch": alg_bytes},
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "h2d_s": h2d_s,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * mlsim.h -- C ABI of the batched dataflow replay library (libmlsim.so).
+ *
+ * The library replays one training iteration, given as a dataflow graph of
+ * profiled ops, for many independent scenarios at once on one AMD Instinct
+ * MI355X (gfx950).  It follows the simulation module of the paper
+ * (Huang et al., "Simulating Performance of ML Systems with Offline
+ * Profiling", Sec. 2, "Dataflow based simulation"):
+ *   - ops are nodes, data/synchronisation dependencies are edges, and every op
+ *     belongs to one device or communication link (a "resource");
+ *   - every resource runs in parallel and keeps a job queue and its finish
+ *     time; an op whose predecessors have all finished is ready and is queued
+ *     on its resource; each resource serves its queue one op at a time,
+ *     first-in-first-out by ready time (Sec. 4, future work, states the FIFO
+ *     assumption);
+ *   - the iteration time is the finish time of the last resource.
+ * Points the paper leaves open are fixed as follows (the same for every
+ * algorithm this library offers, and bit-identical between them):
+ *   - equal ready times are served by lower priority value, then lower op id;
+ *     every op finishing at time t is retired before anything starts at t;
+ *   - sources are ready at t = 0, resources are free at t = 0, edges add no
+ *     latency, an op never shares its resource (no preemption);
+ *   - durations are int32 nanoseconds and must be >= 1; all times are exact
+ *     integers; a time above INT32_MAX is reported, never wrapped.
+ *
+ * Conventions: every function returns an int status (SIM_OK = 0, or a
+ * negative SIM_E_* code) unless stated.  "device" pointers are HIP device
+ * (or managed) memory owned by the caller; "host" pointers are ordinary
+ * memory.  Arrays of shape [n_ops][ld] are op-major: entry (v, s) is at
+ * v * ld + s, so one op's values for consecutive scenarios are contiguous.
+ * Streams are hipStream_t passed as void* (NULL = the null stream).
+ */
+#ifndef MLSIM_H
+#define MLSIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+enum {
+  SIM_OK = 0,
+  SIM_E_INVAL = -1, /* bad argument: NULL where an array is required, ld < n_scen, bad CSR pointers */
+  SIM_E_RANGE = -2, /* an index out of range: successor id, op resource */
+  SIM_E_CYCLE = -3, /* the graph has a cycle (including self loops) */
+  SIM_E_NOMEM = -4, /* host or device allocation failed */
+  SIM_E_HIP = -5,   /* a HIP runtime call failed (e.g. no GPU) */
+  SIM_E_LIMIT = -6  /* the graph exceeds a size limit of this library */
+};
+
+/* per-scenario status bits (status[s]); a scenario with any bit set has
+ * makespan[s] = -1 and unspecified finish values */
+enum {
+  SIM_ST_BAD_DUR = 1,  /* some duration < 1 */
+  SIM_ST_BAD_RES = 2,  /* some placement >= n_res */
+  SIM_ST_OVERFLOW = 4  /* a finish time exceeds INT32_MAX (only reported when
+                          neither bit above is set) */
+};
+
+/* sim_run_batch flags & 3: which exact algorithm computes the replay */
+enum {
+  SIM_ALGO_AUTO = 0,  /* library's choice */
+  SIM_ALGO_EVENT = 1, /* event-driven list scheduling, one scenario per lane */
+  SIM_ALGO_SWEEP = 2  /* level-synchronous conservative sweeps */
+};
+
+/* limits */
+#define SIM_MAX_OPS (1 << 24)
+#define SIM_MAX_RES 1024
+
+typedef struct sim_graph sim_graph; /* opaque; immutable after creation */
+
+/*
+ * Build a graph (Sec. 2: the dataflow graph with each node's "device"
+ * property; the paper's preprocessing module turns framework graphs into
+ * this unified form).
+ *   n_ops   number of ops, 0 <= n_ops <= SIM_MAX_OPS.
+ *   n_res   number of resources, 1 <= n_res <= SIM_MAX_RES.
+ *   succ_ptr host int64 [n_ops+1]: succ_ptr[0] = 0, nondecreasing.
+ *   succ_idx host int32 [succ_ptr[n_ops]]: successor op ids in [0, n_ops);
+ *            repeated edges are allowed and act as one edge.
+ *   op_res  host int32 [n_ops]: resource of each op, in [0, n_res).
+ *   prio    host int32 [n_ops] or NULL (NULL: prio[v] = v).  Lower values
+ *           are served first among ops with equal ready time; ties in
+ *           priority go to the lower op id.
+ *   out     receives the graph.
+ * Every host array is copied; the caller may free them on return.  The graph
+ * owns its device copy and all scratch memory it needs (sized here, for any
+ * number of scenarios).  Needs a HIP device (the current one); argument,
+ * range and cycle errors are detected first, without touching the GPU.
+ */
+int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                     const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                     sim_graph **out);
+
+/* Free a graph.  The caller must first synchronise every stream that used it. */
+void sim_graph_destroy(sim_graph *g);
+
+/*
+ * Replay n_scen scenarios (Sec. 2's simulation loop, once per scenario).
+ *   dur      device int32 [n_ops][ld_dur], ld_dur >= n_scen: duration (ns)
+ *            of op v in scenario s at v * ld_dur + s.
+ *   place    device uint16 [n_ops][ld_place] or NULL: if given, op v runs on
+ *            resource place[v * ld_place + s] in scenario s instead of op_res[v].
+ *   makespan device int32 [n_scen]: iteration time (the finish time of the
+ *            last resource), or -1 if status[s] != 0.
+ *   finish   device int32 [n_ops][ld_fin] or NULL: finish time of every op.
+ *   status   device int32 [n_scen] or NULL: SIM_ST_* bits.
+ *   flags    SIM_ALGO_* in bits 0-1; other bits must be 0.
+ *   stream   hipStream_t (void*), NULL for the null stream.
+ * Asynchronous on `stream`.  Argument errors return synchronously before
+ * anything is enqueued.  No memory is allocated.  Calls on different streams
+ * that share one graph must not overlap in time (they share its scratch
+ * memory); calls on one stream are ordered.
+ */
+int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                  int64_t ld_fin, int32_t *status, uint32_t flags, void *stream);
+
+/*
+ * Critical path per scenario: the longest path through the graph with
+ * resources ignored, dist(v) = d(v) + max over predecessors of dist (0 if
+ * none), cp_len[s] = max over v of dist(v); 0 for an empty graph, -1 if a
+ * duration is < 1 or a path exceeds INT32_MAX.  It is the iteration time
+ * with unlimited resources and the bound the paper's bottleneck analysis
+ * starts from (Sec. 1).
+ *   dur      device int32 [n_ops][ld_dur], ld_dur >= n_scen.
+ *   cp_len   device int32 [n_scen].
+ *   path_scen  -1, or a scenario whose path is returned: then path_ops (host
+ *            int32, capacity path_cap) receives the path from its first op to
+ *            its last and *path_len (host) its length (written even if larger
+ *            than path_cap).  The last op is the lowest-id op of maximum dist;
+ *            each step back goes to the lowest-id predecessor p with
+ *            dist(p) = dist(v) - d(v).  With a path request the call
+ *            synchronises `stream` before returning.
+ * Otherwise asynchronous on `stream`; no memory is allocated.
+ */
+int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      int32_t *cp_len, int64_t path_scen, int32_t *path_ops, int32_t path_cap,
+                      int32_t *path_len, void *stream);
+
+/* Static, human-readable text for a return code. */
+const char *sim_strerror(int code);
+
+/* Graph properties after compilation (host ints, any pointer may be NULL):
+ * ops, resources, edges kept after removing duplicate and transitively
+ * implied edges, ops with two or more predecessors, and the number of
+ * distinct topological levels. */
+int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *n_edges,
+                   int32_t *n_joins, int32_t *n_levels);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

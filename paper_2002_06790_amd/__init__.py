@@ -1,0 +1,190 @@
+"""Batched dataflow replay of ML training iterations on AMD MI355X.
+
+Python binding of ``libmlsim.so`` (C ABI declared in ``include/mlsim.h``).
+This module only marshals arguments: every step of the replay runs in the
+library's HIP kernels.  PyTorch supplies device memory and the stream.
+
+The replay follows the paper's simulation module (Huang et al., "Simulating
+Performance of ML Systems with Offline Profiling", Sec. 2, "Dataflow based
+simulation"): each device or link runs its ready ops one at a time, first in
+first out by ready time, and the iteration time is the finish time of the
+last device.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmlsim.so")
+
+SIM_OK, SIM_E_INVAL, SIM_E_RANGE, SIM_E_CYCLE, SIM_E_NOMEM, SIM_E_HIP, SIM_E_LIMIT = 0, -1, -2, -3, -4, -5, -6
+SIM_ST_BAD_DUR, SIM_ST_BAD_RES, SIM_ST_OVERFLOW = 1, 2, 4
+SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP = 0, 1, 2
+ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP}
+
+EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
+           "sim_strerror", "sim_graph_info")
+
+_lib = None
+
+
+class SimError(RuntimeError):
+    def __init__(self, code: int, what: str = ""):
+        msg = _load().sim_strerror(code).decode() if _lib is not None else str(code)
+        super().__init__(f"{what}: {msg} ({code})" if what else f"{msg} ({code})")
+        self.code = code
+
+
+def build() -> str:
+    """Compile libmlsim.so for gfx950 (always rebuilds)."""
+    from . import buildlib as _b
+    global _lib
+    path = _b.build()
+    _lib = None
+    return path
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: call paper_2002_06790_amd.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, U32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+    L.sim_graph_create.argtypes = [I32, I32, P, P, P, P, ctypes.POINTER(P)]
+    L.sim_graph_create.restype = ctypes.c_int
+    L.sim_graph_destroy.argtypes = [P]
+    L.sim_graph_destroy.restype = None
+    L.sim_run_batch.argtypes = [P, I64, P, I64, P, I64, P, P, I64, P, U32, P]
+    L.sim_run_batch.restype = ctypes.c_int
+    L.sim_critical_path.argtypes = [P, I64, P, I64, P, I64, P, I32, P, P]
+    L.sim_critical_path.restype = ctypes.c_int
+    L.sim_strerror.argtypes = [ctypes.c_int]
+    L.sim_strerror.restype = ctypes.c_char_p
+    L.sim_graph_info.argtypes = [P, P, P, P, P, P]
+    L.sim_graph_info.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def lib():
+    """The loaded ctypes library (raises if it is not built)."""
+    return _load()
+
+
+def _host(a, dt):
+    return None if a is None else np.ascontiguousarray(np.asarray(a), dtype=dt)
+
+
+def _hptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _dev_matrix(t, dtype, n_ops, what):
+    """(pointer, ld) of a [n_ops, S] device tensor with unit column stride."""
+    import torch
+    if t is None:
+        return None, 0
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{what} must be a torch tensor on the GPU")
+    if t.dtype != dtype or t.dim() != 2 or t.shape[0] != n_ops:
+        raise ValueError(f"{what} must be {dtype} of shape (n_ops={n_ops}, n_scen)")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{what} must have unit stride along scenarios")
+    return t.data_ptr(), max(t.stride(0), t.shape[1])
+
+
+def _stream_ptr(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Graph:
+    """A compiled dataflow graph on the current HIP device (sim_graph_create)."""
+
+    def __init__(self, succ_ptr, succ_idx, op_res, n_res: int, prio=None):
+        L = _load()
+        self.succ_ptr = _host(succ_ptr, np.int64)
+        self.succ_idx = _host(succ_idx, np.int32)
+        self.op_res = _host(op_res, np.int32)
+        self.prio = _host(prio, np.int32)
+        self.n_ops = int(self.op_res.size)
+        self.n_res = int(n_res)
+        h = ctypes.c_void_p()
+        rc = L.sim_graph_create(self.n_ops, self.n_res, _hptr(self.succ_ptr), _hptr(self.succ_idx),
+                                _hptr(self.op_res), _hptr(self.prio), ctypes.byref(h))
+        if rc:
+            raise SimError(rc, "sim_graph_create")
+        self._h = h
+
+    @classmethod
+    def from_workload(cls, w) -> "Graph":
+        return cls(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, prio=w.prio)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _load().sim_graph_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self) -> dict:
+        vals = [ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()]
+        rc = _load().sim_graph_info(self._h, *[ctypes.byref(v) for v in vals])
+        if rc:
+            raise SimError(rc, "sim_graph_info")
+        return dict(zip(("n_ops", "n_res", "n_edges", "n_joins", "n_levels"), [v.value for v in vals]))
+
+    def run(self, dur, place=None, want_finish: bool = False, algo: str = "auto",
+            makespan=None, finish=None, status=None, stream=None):
+        """Replay every scenario column of ``dur`` (int32 [n_ops, S] on the GPU).
+
+        Returns ``(makespan [S], finish [n_ops, S] or None, status [S])`` as
+        device tensors (allocated unless passed in).  Asynchronous on the
+        current stream.
+        """
+        import torch
+        dptr, ld = _dev_matrix(dur, torch.int32, self.n_ops, "dur")
+        S = dur.shape[1]
+        pptr, ldp = _dev_matrix(place, torch.uint16, self.n_ops, "place")
+        dev = dur.device
+        if makespan is None:
+            makespan = torch.empty(S, dtype=torch.int32, device=dev)
+        if status is None:
+            status = torch.empty(S, dtype=torch.int32, device=dev)
+        if want_finish and finish is None:
+            finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
+        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        rc = _load().sim_run_batch(self._h, S, dptr, ld, pptr, ldp, makespan.data_ptr(), fptr, ldf,
+                                   status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_run_batch")
+        return makespan, finish, status
+
+    def critical_path(self, dur, path_scen: int = -1, cp_len=None, stream=None):
+        """Longest path per scenario; with ``path_scen`` >= 0 also its op list."""
+        import torch
+        dptr, ld = _dev_matrix(dur, torch.int32, self.n_ops, "dur")
+        S = dur.shape[1]
+        if cp_len is None:
+            cp_len = torch.empty(S, dtype=torch.int32, device=dur.device)
+        cap = max(self.n_ops, 1)
+        path = np.empty(cap, np.int32)
+        plen = np.zeros(1, np.int32)
+        want = path_scen >= 0
+        rc = _load().sim_critical_path(self._h, S, dptr, ld, cp_len.data_ptr(), path_scen,
+                                       path.ctypes.data if want else None, cap if want else 0,
+                                       plen.ctypes.data if want else None, _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_critical_path")
+        return cp_len, (path[: int(plen[0])].copy() if want else None)

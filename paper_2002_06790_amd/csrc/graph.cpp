@@ -1,0 +1,434 @@
+// Graph compilation (host): validation, duplicate-edge removal, cycle check,
+// transitive reduction, renumbering by (priority, id), bounds used to size
+// per-lane state, the critical-path sweep order with its value slots, and the
+// upload of everything to one device allocation.
+//
+// The paper's preprocessing module turns framework graphs into one unified
+// format before simulation (Sec. 2, "Overall System"); successor CSR with an
+// op -> resource map is that format here.
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "sim.hpp"
+
+using namespace mlsim;
+
+namespace {
+
+constexpr int32_t kReduceMaxOps = 32768;  // transitive reduction bitsets: n^2/8 bytes
+
+struct Compiled {
+  std::vector<OpRec> ops;
+  std::vector<int32_t> succ, indeg, src, cp_pred, pred_ptr, pred, topo;
+  std::vector<CpRec> cp;
+  int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0;
+  int64_t m = 0;
+};
+
+// Hopcroft-Karp maximum matching between "u has a successor" and "v has a
+// predecessor" on the edges u -> v.  n - matching = minimum number of
+// vertex-disjoint paths covering the DAG, an upper bound on any antichain
+// (each path meets an antichain at most once), hence on how many ops can be
+// ready at the same time.
+int32_t min_path_cover(int32_t n, const std::vector<std::vector<int32_t>> &adj) {
+  std::vector<int32_t> mu(n, -1), mv(n, -1), dist(n), it(n), q(n);
+  const int32_t INF = INT32_MAX;
+  int32_t matched = 0;
+  for (;;) {
+    int32_t qh = 0, qt = 0;
+    bool found = false;
+    for (int32_t u = 0; u < n; ++u) {
+      if (mu[u] < 0) {
+        dist[u] = 0;
+        q[qt++] = u;
+      } else {
+        dist[u] = INF;
+      }
+    }
+    while (qh < qt) {
+      int32_t u = q[qh++];
+      for (int32_t v : adj[u]) {
+        int32_t w = mv[v];
+        if (w < 0) {
+          found = true;
+        } else if (dist[w] == INF) {
+          dist[w] = dist[u] + 1;
+          q[qt++] = w;
+        }
+      }
+    }
+    if (!found) break;
+    // iterative DFS along layered augmenting paths
+    std::vector<int32_t> stack;
+    for (int32_t u = 0; u < n; ++u) it[u] = 0;
+    for (int32_t root = 0; root < n; ++root) {
+      if (mu[root] >= 0) continue;
+      stack.assign(1, root);
+      while (!stack.empty()) {
+        int32_t u = stack.back();
+        if (it[u] >= (int32_t)adj[u].size()) {
+          dist[u] = INF;
+          stack.pop_back();
+          continue;
+        }
+        int32_t v = adj[u][it[u]];
+        int32_t w = mv[v];
+        if (w < 0) {
+          // augment along the stack
+          for (int32_t k = (int32_t)stack.size() - 1; k >= 0; --k) {
+            int32_t uu = stack[k];
+            int32_t vv = adj[uu][it[uu]];
+            int32_t prev = mu[uu];
+            mu[uu] = vv;
+            mv[vv] = uu;
+            (void)prev;
+          }
+          ++matched;
+          stack.clear();
+        } else if (dist[w] == dist[u] + 1) {
+          stack.push_back(w);
+        } else {
+          ++it[u];
+        }
+      }
+    }
+  }
+  return n - matched;
+}
+
+// Kahn's algorithm; lifo = depth-first flavour.  Returns false on a cycle.
+bool kahn(int32_t n, const std::vector<std::vector<int32_t>> &succ, bool lifo,
+          std::vector<int32_t> &order) {
+  std::vector<int32_t> cnt(n, 0);
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t w : succ[u]) cnt[w]++;
+  std::vector<int32_t> work;
+  order.clear();
+  order.reserve(n);
+  size_t head = 0;
+  for (int32_t v = n - 1; v >= 0; --v)
+    if (cnt[v] == 0) work.push_back(v);
+  if (!lifo) std::reverse(work.begin(), work.end());
+  while (lifo ? !work.empty() : head < work.size()) {
+    int32_t v;
+    if (lifo) {
+      v = work.back();
+      work.pop_back();
+    } else {
+      v = work[head++];
+    }
+    order.push_back(v);
+    const auto &s = succ[v];
+    for (int32_t k = (int32_t)s.size() - 1; k >= 0; --k)
+      if (--cnt[s[k]] == 0) work.push_back(s[k]);
+  }
+  return (int32_t)order.size() == n;
+}
+
+// Slots for the critical-path sweep in `order`: dist(v) lives from v's
+// position to its last successor's position.
+int32_t assign_cp_slots(int32_t n, const std::vector<std::vector<int32_t>> &succ,
+                        const std::vector<std::vector<int32_t>> &pred,
+                        const std::vector<int32_t> &order, std::vector<int32_t> &slot_of) {
+  std::vector<int32_t> pos(n), last(n, -1);
+  for (int32_t k = 0; k < n; ++k) pos[order[k]] = k;
+  for (int32_t v = 0; v < n; ++v)
+    for (int32_t w : succ[v]) last[v] = std::max(last[v], pos[w]);
+  slot_of.assign(n, -1);
+  std::vector<int32_t> freel;
+  int32_t nslots = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    int32_t v = order[k];
+    for (int32_t p : pred[v])
+      if (last[p] == k) freel.push_back(slot_of[p]);
+    if (!succ[v].empty()) {
+      if (freel.empty()) {
+        slot_of[v] = nslots++;
+      } else {
+        slot_of[v] = freel.back();
+        freel.pop_back();
+      }
+    }
+  }
+  return nslots;
+}
+
+int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_idx,
+            const int32_t *op_res, const int32_t *prio, Compiled &C) {
+  // deduplicated successor lists
+  std::vector<std::vector<int32_t>> succ(n);
+  for (int32_t u = 0; u < n; ++u) {
+    succ[u].assign(succ_idx + succ_ptr[u], succ_idx + succ_ptr[u + 1]);
+    std::sort(succ[u].begin(), succ[u].end());
+    succ[u].erase(std::unique(succ[u].begin(), succ[u].end()), succ[u].end());
+  }
+  std::vector<int32_t> topo;
+  if (!kahn(n, succ, false, topo)) return SIM_E_CYCLE;
+  std::vector<int32_t> pos(n);
+  for (int32_t k = 0; k < n; ++k) pos[topo[k]] = k;
+
+  // Transitive reduction: drop u -> w when w is reachable from another
+  // successor of u.  The later of the two predecessors on that path always
+  // finishes after u (durations >= 1), so every ready time is unchanged, and
+  // every op still becomes ready when its last remaining predecessor ends.
+  if (n <= kReduceMaxOps) {
+    const size_t words = ((size_t)n + 63) / 64;
+    std::vector<uint64_t> reach;
+    try {
+      reach.assign(words * (size_t)n, 0);
+    } catch (const std::bad_alloc &) {
+      return SIM_E_NOMEM;
+    }
+    std::vector<uint64_t> acc(words);
+    for (int32_t k = n - 1; k >= 0; --k) {
+      int32_t u = topo[k];
+      auto &s = succ[u];
+      std::sort(s.begin(), s.end(), [&](int32_t a, int32_t b) { return pos[a] < pos[b]; });
+      std::fill(acc.begin(), acc.end(), 0);
+      std::vector<int32_t> keep;
+      for (int32_t w : s) {
+        size_t bit = (size_t)pos[w];
+        if ((acc[bit >> 6] >> (bit & 63)) & 1) continue;
+        keep.push_back(w);
+        const uint64_t *rw = &reach[(size_t)w * words];
+        for (size_t i = 0; i < words; ++i) acc[i] |= rw[i];
+        acc[bit >> 6] |= 1ull << (bit & 63);
+      }
+      std::copy(acc.begin(), acc.end(), reach.begin() + (size_t)u * words);
+      s.swap(keep);
+    }
+  }
+
+  // renumber by (priority, id): compact id order is the tie-break order
+  std::vector<int32_t> orig_of(n), comp(n);
+  std::iota(orig_of.begin(), orig_of.end(), 0);
+  if (prio)
+    std::stable_sort(orig_of.begin(), orig_of.end(),
+                     [&](int32_t a, int32_t b) { return prio[a] < prio[b]; });
+  for (int32_t c = 0; c < n; ++c) comp[orig_of[c]] = c;
+
+  std::vector<std::vector<int32_t>> cs(n), cp(n);  // compact successors / predecessors
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t w : succ[u]) {
+      cs[comp[u]].push_back(comp[w]);
+      cp[comp[w]].push_back(comp[u]);
+    }
+  for (int32_t c = 0; c < n; ++c) {
+    std::sort(cs[c].begin(), cs[c].end());
+    std::sort(cp[c].begin(), cp[c].end());
+  }
+  std::vector<int32_t> ctopo(n);
+  for (int32_t k = 0; k < n; ++k) ctopo[k] = comp[topo[k]];
+
+  // joins numbered in topological order so that concurrently pending joins
+  // have nearby indices
+  C.indeg.assign(n, 0);
+  for (int32_t c = 0; c < n; ++c) C.indeg[c] = (int32_t)cp[c].size();
+  std::vector<int32_t> join(n, -1);
+  C.J = 0;
+  for (int32_t k = 0; k < n; ++k)
+    if (C.indeg[ctopo[k]] >= 2) join[ctopo[k]] = C.J++;
+  C.max_indeg = n ? *std::max_element(C.indeg.begin(), C.indeg.end()) : 0;
+
+  // successor entries are pairs {compact id, join index or -1}
+  C.ops.resize(n + 1);
+  C.succ.clear();
+  int32_t e = 0;
+  for (int32_t c = 0; c < n; ++c) {
+    C.ops[c] = OpRec{orig_of[c], op_res[orig_of[c]], join[c], e};
+    for (int32_t w : cs[c]) {
+      C.succ.push_back(w);
+      C.succ.push_back(join[w]);
+      ++e;
+    }
+  }
+  C.ops[n] = OpRec{-1, -1, -1, e};
+  C.m = e;
+  C.src.clear();
+  for (int32_t c = 0; c < n; ++c)
+    if (C.indeg[c] == 0) C.src.push_back(c);
+
+  C.heap_cap = n ? std::max(1, min_path_cover(n, cs)) : 0;
+
+  // critical-path sweep: the topological order (depth- or breadth-first
+  // flavour) that needs fewer live value slots
+  std::vector<int32_t> o1, o2, s1, s2;
+  kahn(n, cs, true, o1);
+  kahn(n, cs, false, o2);
+  int32_t n1 = assign_cp_slots(n, cs, cp, o1, s1);
+  int32_t n2 = assign_cp_slots(n, cs, cp, o2, s2);
+  const auto &order = n1 <= n2 ? o1 : o2;
+  const auto &slot = n1 <= n2 ? s1 : s2;
+  C.cp_slots = std::min(n1, n2);
+  C.cp.resize(n + 1);
+  C.cp_pred.clear();
+  for (int32_t k = 0; k < n; ++k) {
+    int32_t v = order[k];
+    C.cp[k] = CpRec{orig_of[v], slot[v], (int32_t)C.cp_pred.size(), 0};
+    for (int32_t p : cp[v]) C.cp_pred.push_back(slot[p]);
+  }
+  C.cp[n] = CpRec{-1, -1, (int32_t)C.cp_pred.size(), 0};
+  C.topo = order;
+
+  // compact predecessor CSR (for the sweep variant) and level count
+  C.pred_ptr.assign(n + 1, 0);
+  C.pred.clear();
+  for (int32_t c = 0; c < n; ++c) {
+    C.pred_ptr[c] = (int32_t)C.pred.size();
+    C.pred.insert(C.pred.end(), cp[c].begin(), cp[c].end());
+  }
+  C.pred_ptr[n] = (int32_t)C.pred.size();
+  std::vector<int32_t> lvl(n, 0);
+  C.levels = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    int32_t v = order[k];
+    for (int32_t p : cp[v]) lvl[v] = std::max(lvl[v], lvl[p] + 1);
+    C.levels = std::max(C.levels, lvl[v] + 1);
+  }
+  return SIM_OK;
+}
+
+template <class T>
+size_t bytes_of(const std::vector<T> &v) {
+  return v.size() * sizeof(T);
+}
+
+}  // namespace
+
+extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                                const int32_t *succ_idx, const int32_t *op_res,
+                                const int32_t *prio, sim_graph **out) {
+  if (!out) return SIM_E_INVAL;
+  *out = nullptr;
+  if (n_ops < 0 || n_res < 1) return SIM_E_INVAL;
+  if (n_ops > SIM_MAX_OPS || n_res > SIM_MAX_RES) return SIM_E_LIMIT;
+  if (n_ops > 0 && (!succ_ptr || !op_res)) return SIM_E_INVAL;
+  if (n_ops > 0) {
+    if (succ_ptr[0] != 0) return SIM_E_INVAL;
+    for (int32_t v = 0; v < n_ops; ++v)
+      if (succ_ptr[v + 1] < succ_ptr[v]) return SIM_E_INVAL;
+    if (succ_ptr[n_ops] >= INT32_MAX) return SIM_E_LIMIT;
+    if (succ_ptr[n_ops] > 0 && !succ_idx) return SIM_E_INVAL;
+    for (int64_t e = 0; e < succ_ptr[n_ops]; ++e)
+      if (succ_idx[e] < 0 || succ_idx[e] >= n_ops) return SIM_E_RANGE;
+    for (int32_t v = 0; v < n_ops; ++v)
+      if (op_res[v] < 0 || op_res[v] >= n_res) return SIM_E_RANGE;
+  }
+  Compiled C;
+  int rc;
+  try {
+    rc = compile(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, C);
+  } catch (const std::bad_alloc &) {
+    return SIM_E_NOMEM;
+  }
+  if (rc) return rc;
+  if (C.max_indeg >= 65536) return SIM_E_LIMIT;
+
+  sim_graph *g = new (std::nothrow) sim_graph();
+  if (!g) return SIM_E_NOMEM;
+  g->n_ops = n_ops;
+  g->n_res = n_res;
+  g->n_edges = C.m;
+  g->n_joins = C.J;
+  g->n_levels = C.levels;
+  if (hipGetDevice(&g->device) != hipSuccess) {
+    delete g;
+    return SIM_E_HIP;
+  }
+
+  // one device allocation, 256-byte aligned pieces
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    size_t o = off;
+    off += (b + 255) & ~size_t(255);
+    return o;
+  };
+  size_t o_ops = take(bytes_of(C.ops)), o_succ = take(bytes_of(C.succ)),
+         o_indeg = take(bytes_of(C.indeg)), o_src = take(bytes_of(C.src)),
+         o_cp = take(bytes_of(C.cp)), o_cpp = take(bytes_of(C.cp_pred)),
+         o_pp = take(bytes_of(C.pred_ptr)), o_pr = take(bytes_of(C.pred)),
+         o_topo = take(bytes_of(C.topo));
+  if (hipMalloc(&g->dev_mem, off ? off : 256) != hipSuccess) {
+    delete g;
+    return SIM_E_NOMEM;
+  }
+  char *base = (char *)g->dev_mem;
+  auto put = [&](size_t o, const void *src, size_t b) {
+    return b == 0 || hipMemcpy(base + o, src, b, hipMemcpyHostToDevice) == hipSuccess;
+  };
+  bool ok = put(o_ops, C.ops.data(), bytes_of(C.ops)) && put(o_succ, C.succ.data(), bytes_of(C.succ)) &&
+            put(o_indeg, C.indeg.data(), bytes_of(C.indeg)) && put(o_src, C.src.data(), bytes_of(C.src)) &&
+            put(o_cp, C.cp.data(), bytes_of(C.cp)) && put(o_cpp, C.cp_pred.data(), bytes_of(C.cp_pred)) &&
+            put(o_pp, C.pred_ptr.data(), bytes_of(C.pred_ptr)) && put(o_pr, C.pred.data(), bytes_of(C.pred)) &&
+            put(o_topo, C.topo.data(), bytes_of(C.topo));
+  if (!ok) {
+    (void)hipFree(g->dev_mem);
+    delete g;
+    return SIM_E_HIP;
+  }
+  DevGraph &d = g->dg;
+  d.n = n_ops;
+  d.R = n_res;
+  d.J = C.J;
+  d.nsrc = (int32_t)C.src.size();
+  d.heap_cap = C.heap_cap;
+  d.cp_slots = C.cp_slots;
+  d.max_indeg = C.max_indeg;
+  d.ops = (const OpRec *)(base + o_ops);
+  d.succ = (const int32_t *)(base + o_succ);
+  d.indeg = (const int32_t *)(base + o_indeg);
+  d.src = (const int32_t *)(base + o_src);
+  d.cp = (const CpRec *)(base + o_cp);
+  d.cp_pred = (const int32_t *)(base + o_cpp);
+  d.pred_ptr = (const int32_t *)(base + o_pp);
+  d.pred = (const int32_t *)(base + o_pr);
+  d.topo = (const int32_t *)(base + o_topo);
+
+  g->h_orig_of.resize(n_ops);
+  for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;
+  g->h_pred_ptr = C.pred_ptr;
+  g->h_pred = C.pred;
+
+  g->scratch = nullptr;
+  rc = plan_scratch(g);
+  if (rc) {
+    sim_graph_destroy(g);
+    return rc;
+  }
+  *out = g;
+  return SIM_OK;
+}
+
+extern "C" void sim_graph_destroy(sim_graph *g) {
+  if (!g) return;
+  if (g->scratch) (void)hipFree(g->scratch);
+  if (g->dev_mem) (void)hipFree(g->dev_mem);
+  delete g;
+}
+
+extern "C" int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *n_edges,
+                              int32_t *n_joins, int32_t *n_levels) {
+  if (!g) return SIM_E_INVAL;
+  if (n_ops) *n_ops = g->n_ops;
+  if (n_res) *n_res = g->n_res;
+  if (n_edges) *n_edges = g->n_edges;
+  if (n_joins) *n_joins = g->n_joins;
+  if (n_levels) *n_levels = g->n_levels;
+  return SIM_OK;
+}
+
+extern "C" const char *sim_strerror(int code) {
+  switch (code) {
+    case SIM_OK: return "success";
+    case SIM_E_INVAL: return "invalid argument";
+    case SIM_E_RANGE: return "index out of range";
+    case SIM_E_CYCLE: return "graph has a cycle";
+    case SIM_E_NOMEM: return "out of memory";
+    case SIM_E_HIP: return "HIP runtime error";
+    case SIM_E_LIMIT: return "graph exceeds a library limit";
+    default: return "unknown error";
+  }
+}

@@ -1,0 +1,373 @@
+// gfx950 kernels of the batched dataflow replay.
+//
+// Layout: one wavefront owns a tile of 64 consecutive scenarios, one scenario
+// per lane.  Durations, placements and finish times are op-major x scenario,
+// so a lane reads and writes its own column and lanes that touch the same op
+// touch one contiguous 256-byte row.  Per-lane state is laid out slot-major x
+// lane ([slot][64]) in LDS or in global scratch, so a wave's accesses to one
+// slot index are conflict-free / coalesced.  A persistent grid strides over
+// tiles; every kernel leaves its scratch in the state it found it.
+#include <cstdio>
+#include <cstdlib>
+
+#include "sim.hpp"
+
+namespace mlsim {
+
+namespace {
+
+constexpr uint32_t kI32Max = 0x7fffffffu;
+
+__device__ __forceinline__ uint64_t make_key(uint32_t ready, int32_t c) {
+  return ((uint64_t)ready << 32) | (uint32_t)c;
+}
+
+// Binary min-heap of 64-bit keys (ready << 32 | compact id) for one lane.
+// Compact ids follow (priority, id), so key order is the queue order of a
+// first-in-first-out resource with the tie rules.  Element i lives in LDS for
+// i < hl and in global scratch above; either way at a stride of one wave, so
+// a wave's accesses to one index are conflict-free (LDS) or coalesced.
+struct LaneHeap {
+  uint64_t *l;  // LDS part, this lane's column
+  uint64_t *g;  // global part (index hl upwards), this lane's column
+  int hl;
+  __device__ __forceinline__ uint64_t get(int i) const {
+    return i < hl ? l[i * kWave] : g[(size_t)(i - hl) * kWave];
+  }
+  __device__ __forceinline__ void set(int i, uint64_t x) const {
+    if (i < hl)
+      l[i * kWave] = x;
+    else
+      g[(size_t)(i - hl) * kWave] = x;
+  }
+};
+
+__device__ __forceinline__ void heap_push(const LaneHeap &h, int &hs, uint64_t x) {
+  int i = hs++;
+  while (i > 0) {
+    int p = (i - 1) >> 1;
+    uint64_t a = h.get(p);
+    if (a <= x) break;
+    h.set(i, a);
+    i = p;
+  }
+  h.set(i, x);
+}
+
+// Put x at the root of a heap of hs elements and restore heap order.
+__device__ __forceinline__ void heap_sift_root(const LaneHeap &h, int hs, uint64_t x) {
+  int i = 0;
+  for (;;) {
+    int c = 2 * i + 1;
+    if (c >= hs) break;
+    uint64_t a = h.get(c);
+    if (c + 1 < hs) {
+      uint64_t b = h.get(c + 1);
+      if (b < a) {
+        a = b;
+        ++c;
+      }
+    }
+    if (x <= a) break;
+    h.set(i, a);
+    i = c;
+  }
+  h.set(i, x);
+}
+
+struct EvArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  const uint16_t *place;
+  int64_t ld_place;
+  int32_t *makespan;
+  int32_t *finish;
+  int64_t ld_fin;
+  int32_t *status;
+  uint64_t *heap_g;   // [blocks][heap_cap - heap_lds][64]: heap entries beyond LDS
+  int heap_lds;       // heap entries per lane kept in LDS
+  int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
+  uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
+};
+
+// Event-driven list scheduling, one scenario per lane (the paper's replay
+// loop, Sec. 2).  Each lane keeps its ready list as a heap keyed by (ready
+// time, compact id); it pops the minimum, starts it when both the op is ready
+// and its resource has finished its previous op, and releases successors
+// whose last predecessor this was.  Every lane pops exactly n ops per tile, so
+// the outer loop is wave-uniform.
+template <bool RF_LDS>
+__global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
+  extern __shared__ uint64_t lds[];
+  const int lane = threadIdx.x;
+  const int n = G.n, R = G.R;
+  const LaneHeap heap{lds + lane,
+                      a.heap_g + (size_t)blockIdx.x * (G.heap_cap - a.heap_lds) * kWave + lane,
+                      a.heap_lds};
+  uint32_t *rfree = RF_LDS ? (uint32_t *)(lds + (size_t)a.heap_lds * kWave) + lane
+                           : a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
+  int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
+  const int2 *succ = (const int2 *)G.succ;
+
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    const bool active = s < a.n_scen;
+    const int64_t sc = active ? s : a.n_scen - 1;  // inactive lanes replay a valid column
+    for (int r = 0; r < R; ++r) rfree[r * kWave] = 0;
+    int hs = 0;
+    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, hs, make_key(0, G.src[k]));
+    uint32_t st = 0, span = 0;
+    for (int it = 0; it < n; ++it) {
+      if (hs <= 0) break;  // unreachable for a DAG: some op is always ready
+      const uint64_t key = heap.get(0);
+      const int c = (int)(uint32_t)key;
+      const uint32_t ready = (uint32_t)(key >> 32);
+      const OpRec op = G.ops[c];
+      const int send = G.ops[c + 1].sbeg;
+      int32_t d = a.dur[(int64_t)op.orig * a.ld_dur + sc];
+      int r = op.res;
+      if (a.place) {
+        r = a.place[(int64_t)op.orig * a.ld_place + sc];
+        if (r >= R) {
+          st |= SIM_ST_BAD_RES;
+          r = 0;
+        }
+      }
+      if (d < 1) {
+        st |= SIM_ST_BAD_DUR;
+        d = 1;
+      }
+      const uint32_t rf = rfree[r * kWave];
+      const uint32_t start = ready > rf ? ready : rf;
+      uint32_t fin = start + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
+      if (fin > kI32Max) {
+        st |= SIM_ST_OVERFLOW;
+        fin = kI32Max;
+      }
+      rfree[r * kWave] = fin;
+      span = fin > span ? fin : span;
+      if (a.finish && active) a.finish[(int64_t)op.orig * a.ld_fin + s] = (int32_t)fin;
+      bool hole = true;  // the root slot was popped and is not yet refilled
+      for (int e = op.sbeg; e < send; ++e) {
+        const int2 sw = succ[e];  // {successor, join index or -1}
+        uint64_t nk;
+        if (sw.y < 0) {
+          nk = make_key(fin, sw.x);
+        } else {
+          const int2 js = jst[(size_t)sw.y * kWave];
+          const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
+          if (js.x + 1 < G.indeg[sw.x]) {
+            jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
+            continue;
+          }
+          jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
+          nk = make_key(rdy, sw.x);
+        }
+        if (hole) {
+          heap_sift_root(heap, hs, nk);
+          hole = false;
+        } else {
+          heap_push(heap, hs, nk);
+        }
+      }
+      if (hole) {
+        --hs;
+        if (hs > 0) heap_sift_root(heap, hs, heap.get(hs));
+      }
+    }
+    if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
+    if (active) {
+      a.makespan[s] = st ? -1 : (int32_t)span;
+      if (a.status) a.status[s] = (int32_t)st;
+    }
+  }
+}
+
+struct CpArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *cp_len;
+  int32_t *dist_out;  // dist of every op (by caller id) for scenario dist_scen
+  int64_t dist_scen;
+  uint32_t *slots_g;  // [blocks][cp_slots][64] when slots are not in LDS
+};
+
+constexpr int kCpBatch = 16;  // duration rows loaded ahead of use
+
+// Longest path per scenario: one sweep in a fixed topological order shared by
+// the whole wave (each step reads one coalesced duration row), with dist of
+// ops that still have unvisited successors kept in value slots.
+template <bool LDS>
+__global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
+  extern __shared__ uint32_t lds32[];
+  const int lane = threadIdx.x;
+  const int n = G.n;
+  uint32_t *slots = LDS ? lds32 + lane : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    const bool active = s < a.n_scen;
+    const int64_t sc = active ? s : a.n_scen - 1;
+    const bool want_dist = a.dist_out && s == a.dist_scen;
+    uint32_t mx = 0;
+    bool bad = false;
+    for (int k0 = 0; k0 < n; k0 += kCpBatch) {
+      int32_t dv[kCpBatch];
+#pragma unroll
+      for (int u = 0; u < kCpBatch; ++u) {
+        const int k = k0 + u < n ? k0 + u : n - 1;
+        dv[u] = a.dur[(int64_t)G.cp[k].orig * a.ld_dur + sc];
+      }
+#pragma unroll
+      for (int u = 0; u < kCpBatch; ++u) {
+        const int k = k0 + u;
+        if (k < n) {
+          const CpRec rec = G.cp[k];
+          const int pend = G.cp[k + 1].pbeg;
+          uint32_t best = 0;
+          for (int e = rec.pbeg; e < pend; ++e) {
+            const uint32_t x = slots[(size_t)G.cp_pred[e] * kWave];
+            best = x > best ? x : best;
+          }
+          int32_t d = dv[u];
+          if (d < 1) {
+            bad = true;
+            d = 1;
+          }
+          uint32_t dist = best + (uint32_t)d;
+          if (dist > kI32Max) {
+            bad = true;
+            dist = kI32Max;
+          }
+          if (rec.slot >= 0) slots[(size_t)rec.slot * kWave] = dist;
+          mx = dist > mx ? dist : mx;
+          if (want_dist) a.dist_out[rec.orig] = (int32_t)dist;
+        }
+      }
+    }
+    if (active) a.cp_len[s] = bad ? -1 : (int32_t)mx;
+  }
+}
+
+template <class K>
+int occupancy_blocks(K kernel, size_t lds, int cus) {
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kWave, lds) != hipSuccess)
+    return -1;
+  if (per_cu < 1) per_cu = 1;
+  return per_cu * cus;
+}
+
+constexpr size_t kLdsBudget = 64 * 1024;       // per workgroup
+constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
+constexpr int kHeapLdsMax = 64;                // heap entries per lane kept in LDS
+constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
+
+bool rf_in_lds(const DevGraph &G) { return (size_t)G.R * kWave * 4 <= kRfLdsMax; }
+
+}  // namespace
+
+int plan_scratch(sim_graph *g) {
+  const DevGraph &G = g->dg;
+  ScratchPlan &P = g->plan;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, g->device) != hipSuccess) return SIM_E_HIP;
+  const int cus = prop.multiProcessorCount;
+
+  // event kernel: resource times in LDS when they fit; the top of each lane's
+  // heap in LDS, the rest (up to the exact bound) in global scratch
+  const size_t rf_bytes = (size_t)G.R * kWave * 4;
+  const bool rf_lds = rf_in_lds(G);
+  const size_t heap_room = (kLdsBudget - 16 * 1024 - (rf_lds ? rf_bytes : 0)) / (kWave * 8);
+  P.ev_heap_lds = (int32_t)std::min<size_t>((size_t)G.heap_cap, std::min<size_t>(heap_room, kHeapLdsMax));
+  P.ev_join_lds = 0;
+  P.ev_lds_bytes = std::max<size_t>(8, (size_t)P.ev_heap_lds * kWave * 8 + (rf_lds ? rf_bytes : 0));
+  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true>, P.ev_lds_bytes, cus)
+                            : occupancy_blocks(k_event<false>, P.ev_lds_bytes, cus);
+  if (ev_occ < 0) return SIM_E_HIP;
+  const size_t heap_g_bytes = (size_t)(G.heap_cap - P.ev_heap_lds) * kWave * 8;
+  const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
+  size_t ev_blocks = (size_t)ev_occ;
+  if (ev_per_block) ev_blocks = std::min(ev_blocks, std::max<size_t>(1, kScratchBudget / ev_per_block));
+  P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
+
+  // critical path: slots in LDS when they fit
+  const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
+  P.cp_lds = cp_bytes <= 32 * 1024;
+  P.cp_lds_bytes = P.cp_lds ? std::max<size_t>(cp_bytes, 8) : 8;
+  const int cp_occ = P.cp_lds ? occupancy_blocks(k_cp<true>, P.cp_lds_bytes, cus)
+                              : occupancy_blocks(k_cp<false>, P.cp_lds_bytes, cus);
+  if (cp_occ < 0) return SIM_E_HIP;
+  size_t cp_blocks = (size_t)cp_occ;
+  if (!P.cp_lds && cp_bytes)
+    cp_blocks = std::min(cp_blocks, std::max<size_t>(1, kScratchBudget / cp_bytes));
+  P.cp_blocks = (int32_t)cp_blocks;
+  P.sw_blocks = 0;
+  P.sw_lds_bytes = 0;
+
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    size_t o = off;
+    off += (b + 255) & ~size_t(255);
+    return o;
+  };
+  g->scratch_ev_heap_off = take(heap_g_bytes * P.ev_blocks);
+  g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * P.ev_blocks);
+  g->scratch_sw_off = take(rf_lds ? 0 : rf_bytes * P.ev_blocks);  // event kernel resource times
+  g->scratch_cp_off = take(P.cp_lds ? 0 : cp_bytes * P.cp_blocks);
+  g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
+  g->scratch_bytes = off;
+  if (hipMalloc(&g->scratch, off) != hipSuccess) {
+    g->scratch = nullptr;
+    return SIM_E_NOMEM;
+  }
+  // join state must start cleared; the kernels keep it cleared
+  if (hipMemset(g->scratch, 0, off) != hipSuccess) return SIM_E_HIP;
+  if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
+  if (getenv("MLSIM_VERBOSE"))
+    fprintf(stderr,
+            "[mlsim] n=%d R=%d J=%d heap_cap=%d (lds %d) cp_slots=%d (lds %d) ev_blocks=%d "
+            "cp_blocks=%d ev_lds=%zu scratch=%zu MB\n",
+            G.n, G.R, G.J, G.heap_cap, P.ev_heap_lds, G.cp_slots, P.cp_lds, P.ev_blocks,
+            P.cp_blocks, P.ev_lds_bytes, off >> 20);
+  return SIM_OK;
+}
+
+int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                 int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  const ScratchPlan &P = g->plan;
+  char *base = (char *)g->scratch;
+  EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
+           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_lds,
+           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_sw_off)};
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.ev_blocks);
+  if (rf_in_lds(g->dg))
+    k_event<true><<<dim3(blocks), dim3(kWave), P.ev_lds_bytes, stream>>>(g->dg, a);
+  else
+    k_event<false><<<dim3(blocks), dim3(kWave), P.ev_lds_bytes, stream>>>(g->dg, a);
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream) {
+  const ScratchPlan &P = g->plan;
+  char *base = (char *)g->scratch;
+  CpArgs a{n_scen, dur, ld_dur, cp_len, dist_out, dist_scen, (uint32_t *)(base + g->scratch_cp_off)};
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.cp_blocks);
+  if (P.cp_lds)
+    k_cp<true><<<dim3(blocks), dim3(kWave), P.cp_lds_bytes, stream>>>(g->dg, a);
+  else
+    k_cp<false><<<dim3(blocks), dim3(kWave), P.cp_lds_bytes, stream>>>(g->dg, a);
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+int launch_sweep(const sim_graph *, int64_t, const int32_t *, int64_t, const uint16_t *, int64_t,
+                 int32_t *, int32_t *, int64_t, int32_t *, hipStream_t) {
+  return SIM_E_INVAL;  // not built yet
+}
+
+}  // namespace mlsim

@@ -1,0 +1,89 @@
+// Internal declarations shared by the host runtime and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "mlsim.h"
+
+namespace mlsim {
+
+constexpr int kWave = 64;  // CDNA wavefront width: one scenario per lane
+
+// Per compact op (ops are renumbered by (priority, id), so "lower compact id"
+// is exactly the paper-order tie rule).
+struct OpRec {
+  int32_t orig;  // caller's op id: row of dur / place / finish
+  int32_t res;   // resource (op_res)
+  int32_t join;  // index among ops with >= 2 predecessors, or -1
+  int32_t sbeg;  // first successor in succ[]; the end is ops[c + 1].sbeg
+};
+
+// Per position of the critical-path sweep order.
+struct CpRec {
+  int32_t orig;  // row of dur
+  int32_t slot;  // slot receiving dist(v), or -1 if v has no successors
+  int32_t pbeg;  // predecessor slots in cp_pred[pbeg, next.pbeg)
+  int32_t pad;
+};
+
+// Device view of a compiled graph (plain pointers, passed by value).
+struct DevGraph {
+  int32_t n, R, J, nsrc;
+  int32_t heap_cap;       // bound on simultaneously ready ops (>= DAG width)
+  int32_t cp_slots;       // live values of the critical-path sweep
+  int32_t max_indeg;
+  int32_t pad0;
+  const OpRec *ops;       // [n + 1]
+  const int32_t *succ;    // [2m] pairs {compact successor id, its join index or -1}
+  const int32_t *indeg;   // [n] predecessors after reduction
+  const int32_t *src;     // [nsrc] compact ids of sources
+  const CpRec *cp;        // [n + 1]
+  const int32_t *cp_pred; // predecessor slot lists of the critical-path sweep
+  const int32_t *pred_ptr;// [n + 1] compact predecessor CSR (sweep variant)
+  const int32_t *pred;    // compact predecessor ids
+  const int32_t *topo;    // [n] a topological order (compact ids)
+};
+
+struct ScratchPlan {
+  int32_t ev_blocks;    // persistent grid of the event kernel
+  int32_t ev_heap_lds;  // heap in LDS (1) or global scratch (0)
+  int32_t ev_join_lds;  // join state in LDS (1) or global scratch (0)
+  int32_t cp_blocks;
+  int32_t cp_lds;       // critical-path slots in LDS (1) or global (0)
+  int32_t sw_blocks;
+  size_t ev_lds_bytes, cp_lds_bytes, sw_lds_bytes;
+};
+
+}  // namespace mlsim
+
+struct sim_graph {
+  int32_t n_ops, n_res;
+  int64_t n_edges;  // after dedupe + transitive reduction
+  int32_t n_joins, n_levels;
+  int device;
+  mlsim::DevGraph dg;
+  mlsim::ScratchPlan plan;
+  void *dev_mem;          // one allocation holding every graph array
+  void *scratch;          // event kernel: heaps / join state (global variants)
+  size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_cp_off, scratch_sw_off, scratch_dist_off;
+  // host copies for critical-path recovery
+  std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred;
+  size_t scratch_bytes;
+};
+
+namespace mlsim {
+// launchers (kernels.hip)
+int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                 int64_t ld_fin, int32_t *status, hipStream_t stream);
+int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                 int64_t ld_fin, int32_t *status, hipStream_t stream);
+int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);
+// sizing of persistent grids and LDS, decided once per graph
+int plan_scratch(sim_graph *g);
+}  // namespace mlsim

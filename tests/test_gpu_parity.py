@@ -1,0 +1,229 @@
+"""GPU parity: the HIP replay equals the CPU oracle bit for bit.
+
+Every case calls the library through its C ABI (via the ctypes binding) on
+seeded inputs and compares integer nanosecond outputs element by element with
+oracle/ on the same inputs.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2002_06790_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mlsim():
+    import paper_2002_06790_amd as m
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(m.LIB_PATH):
+        m.build()
+    return m
+
+
+def dev(a, dtype=torch.int32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dtype=dtype, device="cuda")
+
+
+def check_run(mlsim, ptr, idx, res, R, dur, prio=None, place=None, algo="event", ld_pad=0,
+              want_finish=True):
+    g = mlsim.Graph(ptr, idx, res, R, prio=prio)
+    n, S = dur.shape
+    d = dev(np.pad(dur, ((0, 0), (0, ld_pad)))) if ld_pad else dev(dur)
+    d = d[:, :S]
+    p = None
+    if place is not None:
+        p = torch.from_numpy(np.ascontiguousarray(place).view(np.int16)).cuda().view(torch.uint16)
+    mk, fin, st = g.run(d, place=p, want_finish=want_finish, algo=algo)
+    torch.cuda.synchronize()
+    omk, ofin, ost = oracle.run_batch(ptr, idx, res, R, dur, prio=prio, place=place)
+    mk, st = mk.cpu().numpy(), st.cpu().numpy()
+    assert np.array_equal(st, ost), "status differs"
+    assert np.array_equal(mk, omk), f"makespan differs in {np.count_nonzero(mk != omk)} scenarios"
+    if want_finish:
+        fin = fin.cpu().numpy()
+        ok = ost == 0
+        assert np.array_equal(fin[:, ok], ofin[:, ok]), "finish times differ"
+    g.close()
+    return omk
+
+
+def check_cp(mlsim, ptr, idx, res, R, dur, paths=()):
+    g = mlsim.Graph(ptr, idx, res, R)
+    n, S = dur.shape
+    d = dev(dur)
+    cp, _ = g.critical_path(d)
+    torch.cuda.synchronize()
+    ocp, _ = oracle.critical_path(ptr, idx, n, dur)
+    assert np.array_equal(cp.cpu().numpy(), ocp)
+    for s in paths:
+        _, path = g.critical_path(d, path_scen=s)
+        _, opath = oracle.critical_path(ptr, idx, n, dur, path_scen=s)
+        assert np.array_equal(path, opath), f"path of scenario {s}"
+    g.close()
+
+
+# ---------------------------------------------------------------- workloads
+
+@pytest.mark.parametrize("k,S", [(1, 1024), (2, 200), (3, 333), (4, 200), (5, 130)])
+def test_workload_parity(mlsim, k, S):
+    w = W.make_config(k, n_scen=S if k != 1 else None)
+    dur = w.durations()
+    place = w.placement()
+    print(f"workload {w.name} n={w.n_ops} S={dur.shape[1]}", flush=True)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, place=place)
+    check_cp(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, paths=(0, dur.shape[1] - 1))
+
+
+def test_bert_all_knobs(mlsim):
+    """Sampled scenarios of every strategy knob of the BERT workload."""
+    w = W.make_config(4)
+    scen = np.concatenate([np.arange(k * 4096, k * 4096 + 40) for k in range(12)])
+    dur, _ = w.columns(scen)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur)
+
+
+# ----------------------------------------------------------- random graphs
+
+def rand_case(rng, n, R, p, prio, dup, S, lo=1, hi=1000):
+    ptr, idx, res, pr = W.random_dag(n, R, p, rng, with_prio=prio, dup_edges=dup)
+    dur = W.random_durations(n, S, lo, hi, rng)
+    return ptr, idx, res, pr, dur
+
+
+def test_random_graphs(mlsim):
+    rng = np.random.default_rng(2024)
+    for case in range(40):
+        n = int(rng.integers(1, 70))
+        R = int(rng.integers(1, 9))
+        S = int(rng.choice([1, 5, 63, 64, 65, 130]))
+        hi = int(rng.choice([3, 10, 1000]))  # small ranges force ties
+        ptr, idx, res, pr, dur = rand_case(rng, n, R, float(rng.uniform(0, 0.3)),
+                                           bool(rng.integers(2)), bool(rng.integers(2)), S, 1, hi)
+        print(f"random case {case} n={n} R={R} S={S}", flush=True)
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr, ld_pad=int(rng.integers(0, 3)) * 7)
+        check_cp(mlsim, ptr, idx, res, R, dur, paths=(0,))
+
+
+def test_random_with_placement(mlsim):
+    rng = np.random.default_rng(7)
+    for _ in range(10):
+        n, R, S = int(rng.integers(2, 60)), int(rng.integers(1, 12)), 97
+        ptr, idx, res, pr, dur = rand_case(rng, n, R, 0.1, True, False, S, 1, 50)
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16)
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr, place=place)
+
+
+def test_wide_and_deep_shapes(mlsim):
+    rng = np.random.default_rng(8)
+    # no edges, many sources (heap at its bound), one resource and many resources
+    for n, R in ((300, 1), (300, 7), (257, 257)):
+        ptr = np.zeros(n + 1, np.int64)
+        check_run(mlsim, ptr, np.zeros(0, np.int32), rng.integers(0, R, n).astype(np.int32), R,
+                  W.random_durations(n, 70, 1, 20, rng))
+    # a long chain
+    n = 2000
+    ptr = np.arange(n + 1, dtype=np.int64).clip(max=n - 1)
+    idx = np.arange(1, n, dtype=np.int32)
+    ptr = np.concatenate([[0], np.cumsum(np.r_[np.ones(n - 1), 0])]).astype(np.int64)
+    check_run(mlsim, ptr, idx, rng.integers(0, 3, n).astype(np.int32), 3,
+              W.random_durations(n, 65, 1, 1000, rng))
+    check_cp(mlsim, ptr, idx, np.zeros(n, np.int32), 1, W.random_durations(n, 65, 1, 1000, rng), (3,))
+
+
+def test_single_op_and_empty(mlsim):
+    check_run(mlsim, np.array([0, 0]), np.zeros(0, np.int32), np.array([0], np.int32), 1,
+              np.array([[5, 1, 7]], np.int32))
+    g = mlsim.Graph(np.zeros(1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.int32), 1)
+    mk, _, st = g.run(torch.zeros((0, 10), dtype=torch.int32, device="cuda"))
+    cp, _ = g.critical_path(torch.zeros((0, 10), dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    assert mk.cpu().tolist() == [0] * 10 and st.cpu().tolist() == [0] * 10
+    assert cp.cpu().tolist() == [0] * 10
+
+
+def test_status_bits(mlsim):
+    """Bad durations, bad placements and overflow match the oracle's status."""
+    ptr = np.array([0, 1, 2, 2], np.int64)
+    idx = np.array([1, 2], np.int32)
+    res = np.zeros(3, np.int32)
+    dur = np.array([[1, 0, 5, 1_500_000_000, 9, -4],
+                    [1, 1, 5, 1_500_000_000, 9, 1],
+                    [1, 1, 5, 1, 9, 1]], np.int32)
+    place = np.array([[0, 0, 0, 0, 0, 0], [0, 1, 3, 0, 2, 0], [0, 0, 0, 0, 0, 0]], np.uint16)
+    check_run(mlsim, ptr, idx, res, 1, dur)
+    check_run(mlsim, ptr, idx, res, 2, dur, place=place)
+    check_cp(mlsim, ptr, idx, res, 1, dur)
+
+
+def test_goldens(mlsim):
+    import goldens
+    for g in goldens.all_goldens():
+        check_run(mlsim, g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], g["dur"], prio=g["prio"])
+        if "cp_path" in g["expect"]:
+            gg = mlsim.Graph(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], prio=g["prio"])
+            cp, path = gg.critical_path(dev(g["dur"]), path_scen=0)
+            assert cp.cpu().tolist() == g["expect"]["cp_len"]
+            assert path.tolist() == g["expect"]["cp_path"]
+
+
+def test_repeatable(mlsim):
+    w = W.make_config(3, n_scen=500)
+    dur = dev(w.durations())
+    g = mlsim.Graph.from_workload(w)
+    a = [t.clone() for t in g.run(dur, want_finish=True)]
+    for _ in range(3):
+        b = g.run(dur, want_finish=True)
+        torch.cuda.synchronize()
+        assert all(torch.equal(x, y) for x, y in zip(a, b))
+
+
+def test_makespan_only_matches_finish_mode(mlsim):
+    w = W.make_config(2, n_scen=300)
+    dur = dev(w.durations())
+    g = mlsim.Graph.from_workload(w)
+    a, _, sa = g.run(dur, want_finish=True)
+    b, _, sb = g.run(dur, want_finish=False)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(sa, sb)
+
+
+# --------------------------------------------------------------- full sizes
+
+@pytest.mark.parametrize("k", [2, 3, 4, 5])
+def test_full_size_sampled(mlsim, k):
+    """Full scenario count in the benchmark's launch configuration; sampled
+    scenarios against the oracle, every scenario against the bounds."""
+    w = W.make_config(k)
+    print(f"full-size {w.name} n={w.n_ops} S={w.n_scen}", flush=True)
+    dur_h = w.durations()
+    place_h = w.placement()
+    dur = dev(dur_h)
+    place = None
+    if place_h is not None:
+        place = torch.from_numpy(place_h.view(np.int16)).cuda().view(torch.uint16)
+    g = mlsim.Graph.from_workload(w)
+    mk, fin, st = g.run(dur, place=place, want_finish=True)
+    cp, _ = g.critical_path(dur)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(k)
+    scen = np.unique(np.r_[0, w.n_scen - 1, rng.integers(0, w.n_scen, 48)])
+    omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h[:, scen],
+                                      place=None if place_h is None else place_h[:, scen])
+    ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, w.n_ops, dur_h[:, scen])
+    sel = torch.from_numpy(scen).cuda()
+    assert np.array_equal(mk[sel].cpu().numpy(), omk)
+    assert np.array_equal(st[sel].cpu().numpy(), ost)
+    assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
+    assert np.array_equal(cp[sel].cpu().numpy(), ocp)
+    # every scenario: valid status, cp <= makespan <= total work
+    mk_all, cp_all = mk.cpu().numpy().astype(np.int64), cp.cpu().numpy().astype(np.int64)
+    assert (st.cpu().numpy() == 0).all()
+    total = dur.to(torch.int64).sum(0).cpu().numpy()
+    assert (cp_all <= mk_all).all() and (mk_all <= total).all()
+    assert torch.equal(fin.max(0).values, mk)

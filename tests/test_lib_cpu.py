@@ -1,0 +1,68 @@
+"""Host-side checks of the C ABI library that need no GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2002_06790_amd as mlsim
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mlsim.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sim_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(mlsim.LIB_PATH):
+        mlsim.build()
+    return mlsim.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) == set(mlsim.EXPORTS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_strerror(L):
+    for code in range(0, -7, -1):
+        assert L.sim_strerror(code)
+    assert L.sim_strerror(-99) == b"unknown error"
+
+
+def create(L, n, R, ptr, idx, res, prio=None):
+    h = ctypes.c_void_p()
+    a = [np.ascontiguousarray(x, dt) if x is not None else None
+         for x, dt in ((ptr, np.int64), (idx, np.int32), (res, np.int32), (prio, np.int32))]
+    rc = L.sim_graph_create(n, R, *[x.ctypes.data if x is not None else None for x in a], ctypes.byref(h))
+    return rc, h
+
+
+def test_graph_errors_without_gpu(L):
+    """Malformed graphs are rejected on the host before any HIP call."""
+    res = [0, 0]
+    assert create(L, 2, 1, [0, 1, 2], [1, 0], res)[0] == mlsim.SIM_E_CYCLE
+    assert create(L, 2, 1, [0, 1, 1], [0], res)[0] == mlsim.SIM_E_CYCLE  # self loop
+    assert create(L, 2, 1, [0, 1, 1], [2], res)[0] == mlsim.SIM_E_RANGE
+    assert create(L, 2, 1, [0, 1, 1], [1], [0, 1])[0] == mlsim.SIM_E_RANGE
+    assert create(L, 2, 1, [0, 1, 0], [1], res)[0] == mlsim.SIM_E_INVAL
+    assert create(L, 2, 1, [1, 1, 1], [1], res)[0] == mlsim.SIM_E_INVAL
+    assert create(L, 2, 0, [0, 1, 1], [1], res)[0] == mlsim.SIM_E_INVAL
+    assert create(L, -1, 1, [0], [], [])[0] == mlsim.SIM_E_INVAL
+    assert create(L, 2, 5000, [0, 1, 1], [1], res)[0] == mlsim.SIM_E_LIMIT
+    rc = L.sim_graph_create(1, 1, None, None, None, None, ctypes.byref(ctypes.c_void_p()))
+    assert rc == mlsim.SIM_E_INVAL
+    assert L.sim_graph_create(0, 1, None, None, None, None, None) == mlsim.SIM_E_INVAL
+
+
+def test_run_argument_errors_without_gpu(L):
+    assert L.sim_run_batch(None, 1, None, 1, None, 0, None, None, 0, None, 0, None) == mlsim.SIM_E_INVAL
+    assert L.sim_critical_path(None, 1, None, 1, None, -1, None, 0, None, None) == mlsim.SIM_E_INVAL
