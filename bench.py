@@ -38,8 +38,10 @@ def main():
     ap.add_argument("--config", type=int, default=4, help="workload 1..5")
     ap.add_argument("--scenarios", type=int, default=None)
     ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep"))
-    ap.add_argument("--cpu-sample", type=int, default=65536,
+    ap.add_argument("--cpu-sample", type=int, default=262144,
                     help="scenarios of the same workload timed on the CPU oracle (0: skip)")
+    ap.add_argument("--calib-mb", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--no-check", action="store_true")
     args = ap.parse_args()
 
@@ -88,6 +90,14 @@ def main():
         e1.record()
         g.critical_path(dur, cp_len=cp_len)
         e2.record()
+
+    if args.calib_mb:
+        src = torch.ones(args.calib_mb << 18, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"calibration copy of {args.calib_mb} MiB done")
 
     e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
     log(f"graph compiled {info}; warmup {args.warmup}")
