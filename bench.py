@@ -155,6 +155,18 @@ def main():
                          f"{cpu_s:.2f} s"}
         log(f"cpu oracle {cpu['value']:.3e} op-events/s")
 
+    # HBM traffic measured by counters for this exact kernel source, if any
+    traffic = None
+    try:
+        import hashlib
+        prof = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+        src = open(os.path.join(ROOT, "paper_2002_06790_amd", "csrc", "kernels.hip"), "rb").read()
+        if (prof.get("kernels_sha256") == hashlib.sha256(src).hexdigest() and args.config == 4
+                and S == 262144 and args.algo in ("event", "auto")):
+            traffic = prof["k_event"]["read_bytes"] + prof["k_event"]["write_bytes"]
+    except (OSError, ValueError, KeyError):
+        traffic = None
+
     op_events = n * S
     ev_s = float(np.mean(ev_ms)) / 1e3
     alg_bytes = op_events * (4 + 4 + (2 if place is not None else 0)) + S * 8
@@ -180,7 +192,8 @@ def main():
                     "run_batch_op_events_per_s": op_events / ev_s,
                     "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
                      "kernel": "k_event (sim_run_batch)",
                      "bytes_per_launch": alg_bytes},
         "cpu_baseline": cpu,
