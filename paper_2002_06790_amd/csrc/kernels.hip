@@ -250,6 +250,146 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
   }
 }
 
+struct SwArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  const uint16_t *place;
+  int64_t ld_place;
+  int32_t *makespan;
+  int32_t *finish;
+  int64_t ld_fin;
+  int32_t *status;
+  uint32_t *val_g;  // [blocks][n][64] per-op state when not in LDS
+  uint32_t *res_g;  // [blocks][R][64] resource times, then [R][64] x2 uint64 bounds
+};
+
+constexpr uint32_t kDone = 0x80000000u;  // val bit: op committed (low bits: finish)
+
+// Level-synchronous conservative sweeps, one scenario per lane.  A round
+// first walks every uncommitted op in one topological order shared by the
+// wave and computes lower bounds: est = max over predecessors of their finish
+// (committed) or earliest finish (not committed), eft = max(est, resource
+// free time) + d.  An op whose predecessors are all committed is ready at
+// exactly est.  Then each resource commits its ready op of smallest key
+// (est, compact id) if that key is below the bound of every op on the
+// resource that is not ready yet.  Each resource therefore runs its ops in
+// key order, which is the first-in-first-out replay's unique schedule; every
+// round commits at least the globally smallest ready op.
+template <bool VAL_LDS, bool RES_LDS>
+__global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
+  extern __shared__ uint32_t sw_lds[];
+  const int lane = threadIdx.x;
+  const int n = G.n, R = G.R;
+  uint32_t *val = VAL_LDS ? sw_lds + lane : a.val_g + (size_t)blockIdx.x * n * kWave + lane;
+  uint32_t *resb = RES_LDS ? sw_lds + (VAL_LDS ? (size_t)n * kWave : 0)
+                           : a.res_g + (size_t)blockIdx.x * R * kWave * 5;
+  uint32_t *rfree = resb + lane;
+  uint64_t *minf = (uint64_t *)(resb + (size_t)R * kWave) + lane;       // smallest ready key
+  uint64_t *lbnd = (uint64_t *)(resb + (size_t)R * kWave * 3) + lane;   // smallest bound, not ready
+
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    const bool active = s < a.n_scen;
+    const int64_t sc = active ? s : a.n_scen - 1;
+    for (int v = 0; v < n; ++v) val[(size_t)v * kWave] = 0;
+    for (int r = 0; r < R; ++r) rfree[r * kWave] = 0;
+    int done = 0;
+    uint32_t st = 0, span = 0;
+    for (int round = 0; round < n; ++round) {
+      if (__ballot(done < n) == 0) break;
+      for (int r = 0; r < R; ++r) {
+        minf[r * kWave] = ~0ull;
+        lbnd[r * kWave] = ~0ull;
+      }
+      for (int k = 0; k < n; ++k) {
+        const int v = G.topo[k];
+        if (val[(size_t)v * kWave] & kDone) continue;
+        uint32_t est = 0;
+        bool ready = true;
+        for (int e = G.pred_ptr[v]; e < G.pred_ptr[v + 1]; ++e) {
+          const uint32_t y = val[(size_t)G.pred[e] * kWave];
+          const uint32_t t = y & ~kDone;
+          est = t > est ? t : est;
+          ready = ready && (y & kDone);
+        }
+        const OpRec op = G.ops[v];
+        int32_t d = a.dur[(int64_t)op.orig * a.ld_dur + sc];
+        int r = op.res;
+        if (a.place) {
+          r = a.place[(int64_t)op.orig * a.ld_place + sc];
+          if (r >= R) {
+            st |= SIM_ST_BAD_RES;
+            r = 0;
+          }
+        }
+        if (d < 1) {
+          st |= SIM_ST_BAD_DUR;
+          d = 1;
+        }
+        const uint32_t rf = rfree[r * kWave];
+        uint32_t eft = (est > rf ? est : rf) + (uint32_t)d;
+        if (eft > kI32Max) eft = kI32Max;
+        val[(size_t)v * kWave] = eft;
+        const uint64_t key = make_key(est, v);
+        uint64_t *slot = ready ? &minf[r * kWave] : &lbnd[r * kWave];
+        if (key < *slot) *slot = key;
+      }
+      // commit, per resource, the smallest ready op that beats every bound
+      bool progress = false;
+      uint64_t gmin = ~0ull;
+      int gres = 0;
+      for (int r = 0; r < R; ++r) {
+        const uint64_t mf = minf[r * kWave];
+        if (mf < gmin) {
+          gmin = mf;
+          gres = r;
+        }
+        if (mf < lbnd[r * kWave]) {
+          progress = true;
+          const int c = (int)(uint32_t)mf;
+          const uint32_t rdy = (uint32_t)(mf >> 32);
+          const OpRec op = G.ops[c];
+          int32_t d = a.dur[(int64_t)op.orig * a.ld_dur + sc];
+          d = d < 1 ? 1 : d;
+          const uint32_t rf = rfree[r * kWave];
+          uint32_t fin = (rdy > rf ? rdy : rf) + (uint32_t)d;
+          if (fin > kI32Max) {
+            st |= SIM_ST_OVERFLOW;
+            fin = kI32Max;
+          }
+          rfree[r * kWave] = fin;
+          val[(size_t)c * kWave] = fin | kDone;
+          span = fin > span ? fin : span;
+          ++done;
+          if (a.finish && active) a.finish[(int64_t)op.orig * a.ld_fin + s] = (int32_t)fin;
+        }
+      }
+      // Only saturated times (an overflowing scenario) can stall progress;
+      // then commit the smallest ready op anyway so the sweep terminates.
+      if (!progress && done < n && gmin != ~0ull) {
+        const int c = (int)(uint32_t)gmin;
+        const uint32_t rdy = (uint32_t)(gmin >> 32);
+        const OpRec op = G.ops[c];
+        int32_t d = a.dur[(int64_t)op.orig * a.ld_dur + sc];
+        d = d < 1 ? 1 : d;
+        const uint32_t rf = rfree[gres * kWave];
+        uint32_t fin = (rdy > rf ? rdy : rf) + (uint32_t)d;
+        if (fin > kI32Max) fin = kI32Max;
+        st |= SIM_ST_OVERFLOW;
+        rfree[gres * kWave] = fin;
+        val[(size_t)c * kWave] = fin | kDone;
+        ++done;
+      }
+    }
+    if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
+    if (active) {
+      a.makespan[s] = st ? -1 : (int32_t)span;
+      if (a.status) a.status[s] = (int32_t)st;
+    }
+  }
+}
+
 template <class K>
 int occupancy_blocks(K kernel, size_t lds, int cus) {
   int per_cu = 0;
@@ -303,8 +443,24 @@ int plan_scratch(sim_graph *g) {
   if (!P.cp_lds && cp_bytes)
     cp_blocks = std::min(cp_blocks, std::max<size_t>(1, kScratchBudget / cp_bytes));
   P.cp_blocks = (int32_t)cp_blocks;
-  P.sw_blocks = 0;
-  P.sw_lds_bytes = 0;
+  // sweep variant: per-op state and per-resource state in LDS when small
+  const size_t val_bytes = (size_t)G.n * kWave * 4;
+  const size_t res_bytes = (size_t)G.R * kWave * 20;
+  P.sw_val_lds = val_bytes <= 32 * 1024;
+  P.sw_res_lds = res_bytes <= 16 * 1024;
+  P.sw_lds_bytes = std::max<size_t>(8, (P.sw_val_lds ? val_bytes : 0) + (P.sw_res_lds ? res_bytes : 0));
+  int sw_occ;
+  if (P.sw_val_lds)
+    sw_occ = P.sw_res_lds ? occupancy_blocks(k_sweep<true, true>, P.sw_lds_bytes, cus)
+                          : occupancy_blocks(k_sweep<true, false>, P.sw_lds_bytes, cus);
+  else
+    sw_occ = P.sw_res_lds ? occupancy_blocks(k_sweep<false, true>, P.sw_lds_bytes, cus)
+                          : occupancy_blocks(k_sweep<false, false>, P.sw_lds_bytes, cus);
+  if (sw_occ < 0) return SIM_E_HIP;
+  const size_t sw_per_block = (P.sw_val_lds ? 0 : val_bytes) + (P.sw_res_lds ? 0 : res_bytes);
+  size_t sw_blocks = (size_t)sw_occ;
+  if (sw_per_block) sw_blocks = std::min(sw_blocks, std::max<size_t>(1, kScratchBudget / sw_per_block));
+  P.sw_blocks = (int32_t)sw_blocks;
 
   size_t off = 0;
   auto take = [&](size_t b) {
@@ -314,7 +470,9 @@ int plan_scratch(sim_graph *g) {
   };
   g->scratch_ev_heap_off = take(heap_g_bytes * P.ev_blocks);
   g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * P.ev_blocks);
-  g->scratch_sw_off = take(rf_lds ? 0 : rf_bytes * P.ev_blocks);  // event kernel resource times
+  g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * P.ev_blocks);
+  g->scratch_sw_val_off = take(P.sw_val_lds ? 0 : val_bytes * P.sw_blocks);
+  g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_lds ? 0 : cp_bytes * P.cp_blocks);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   g->scratch_bytes = off;
@@ -341,7 +499,7 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_lds,
-           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_sw_off)};
+           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.ev_blocks);
   if (rf_in_lds(g->dg))
@@ -365,9 +523,28 @@ int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
-int launch_sweep(const sim_graph *, int64_t, const int32_t *, int64_t, const uint16_t *, int64_t,
-                 int32_t *, int32_t *, int64_t, int32_t *, hipStream_t) {
-  return SIM_E_INVAL;  // not built yet
+int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                 int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  const ScratchPlan &P = g->plan;
+  char *base = (char *)g->scratch;
+  SwArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
+           (uint32_t *)(base + g->scratch_sw_val_off), (uint32_t *)(base + g->scratch_sw_res_off)};
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.sw_blocks);
+  const size_t lds = P.sw_lds_bytes;
+  if (P.sw_val_lds) {
+    if (P.sw_res_lds)
+      k_sweep<true, true><<<dim3(blocks), dim3(kWave), lds, stream>>>(g->dg, a);
+    else
+      k_sweep<true, false><<<dim3(blocks), dim3(kWave), lds, stream>>>(g->dg, a);
+  } else {
+    if (P.sw_res_lds)
+      k_sweep<false, true><<<dim3(blocks), dim3(kWave), lds, stream>>>(g->dg, a);
+    else
+      k_sweep<false, false><<<dim3(blocks), dim3(kWave), lds, stream>>>(g->dg, a);
+  }
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
 }  // namespace mlsim

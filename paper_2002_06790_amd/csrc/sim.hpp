@@ -54,6 +54,8 @@ struct ScratchPlan {
   int32_t cp_blocks;
   int32_t cp_lds;       // critical-path slots in LDS (1) or global (0)
   int32_t sw_blocks;
+  int32_t sw_val_lds;   // sweep: per-op state in LDS (1) or global (0)
+  int32_t sw_res_lds;   // sweep: per-resource state in LDS (1) or global (0)
   size_t ev_lds_bytes, cp_lds_bytes, sw_lds_bytes;
 };
 
@@ -68,7 +70,8 @@ struct sim_graph {
   mlsim::ScratchPlan plan;
   void *dev_mem;          // one allocation holding every graph array
   void *scratch;          // event kernel: heaps / join state (global variants)
-  size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_cp_off, scratch_sw_off, scratch_dist_off;
+  size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
+  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off;
   // host copies for critical-path recovery
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred;
   size_t scratch_bytes;

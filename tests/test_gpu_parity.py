@@ -227,3 +227,57 @@ def test_full_size_sampled(mlsim, k):
     total = dur.to(torch.int64).sum(0).cpu().numpy()
     assert (cp_all <= mk_all).all() and (mk_all <= total).all()
     assert torch.equal(fin.max(0).values, mk)
+
+
+# ------------------------------------------------------- sweep variant (a8)
+
+@pytest.mark.parametrize("k,S", [(1, 1024), (2, 130), (3, 200), (4, 130), (5, 70)])
+def test_sweep_workload_parity(mlsim, k, S):
+    w = W.make_config(k, n_scen=S if k != 1 else None)
+    dur = w.durations()
+    print(f"sweep workload {w.name} n={w.n_ops} S={dur.shape[1]}", flush=True)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, place=w.placement(), algo="sweep")
+
+
+def test_sweep_random_graphs(mlsim):
+    rng = np.random.default_rng(99)
+    for case in range(30):
+        n = int(rng.integers(1, 60))
+        R = int(rng.integers(1, 9))
+        S = int(rng.choice([1, 63, 65, 130]))
+        hi = int(rng.choice([3, 10, 1000]))
+        ptr, idx, res, pr, dur = rand_case(rng, n, R, float(rng.uniform(0, 0.3)),
+                                           bool(rng.integers(2)), bool(rng.integers(2)), S, 1, hi)
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16) if case % 3 == 0 else None
+        print(f"sweep random case {case} n={n} R={R} S={S}", flush=True)
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr, place=place, algo="sweep",
+                  ld_pad=int(rng.integers(0, 3)) * 5)
+
+
+def test_sweep_status_and_goldens(mlsim):
+    import goldens
+    ptr = np.array([0, 1, 2, 2], np.int64)
+    idx = np.array([1, 2], np.int32)
+    res = np.zeros(3, np.int32)
+    dur = np.array([[1, 0, 5, 1_500_000_000, 9, -4],
+                    [1, 1, 5, 1_500_000_000, 9, 1],
+                    [1, 1, 5, 1, 9, 1]], np.int32)
+    place = np.array([[0, 0, 0, 0, 0, 0], [0, 1, 3, 0, 2, 0], [0, 0, 0, 0, 0, 0]], np.uint16)
+    check_run(mlsim, ptr, idx, res, 1, dur, algo="sweep")
+    check_run(mlsim, ptr, idx, res, 2, dur, place=place, algo="sweep")
+    for g in goldens.all_goldens():
+        check_run(mlsim, g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], g["dur"],
+                  prio=g["prio"], algo="sweep")
+
+
+def test_sweep_equals_event_full_bert_slice(mlsim):
+    """Both algorithms agree bit for bit on a slice of every BERT strategy knob."""
+    w = W.make_config(4)
+    scen = np.concatenate([np.arange(k * 4096, k * 4096 + 64) for k in range(12)])
+    dur_h, _ = w.columns(scen)
+    dur = dev(dur_h)
+    g = mlsim.Graph.from_workload(w)
+    a = g.run(dur, want_finish=True, algo="event")
+    b = g.run(dur, want_finish=True, algo="sweep")
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(a, b))
