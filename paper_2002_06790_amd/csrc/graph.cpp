@@ -8,6 +8,8 @@
 // op -> resource map is that format here.
 #include <algorithm>
 #include <cstring>
+#include <iterator>
+#include <map>
 #include <new>
 #include <numeric>
 #include <vector>
@@ -22,9 +24,9 @@ constexpr int32_t kReduceMaxOps = 32768;  // transitive reduction bitsets: n^2/8
 
 struct Compiled {
   std::vector<OpRec> ops;
-  std::vector<int32_t> succ, indeg, src, cp_pred, pred_ptr, pred, topo;
+  std::vector<int32_t> succ, jneed, src, cp_pred, pred_ptr, pred, topo;
   std::vector<CpRec> cp;
-  int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0;
+  int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0, barriers = 0;
   int64_t m = 0;
 };
 
@@ -223,33 +225,78 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   std::vector<int32_t> ctopo(n);
   for (int32_t k = 0; k < n; ++k) ctopo[k] = comp[topo[k]];
 
-  // joins numbered in topological order so that concurrently pending joins
-  // have nearby indices
-  C.indeg.assign(n, 0);
-  for (int32_t c = 0; c < n; ++c) C.indeg[c] = (int32_t)cp[c].size();
-  std::vector<int32_t> join(n, -1);
-  C.J = 0;
-  for (int32_t k = 0; k < n; ++k)
-    if (C.indeg[ctopo[k]] >= 2) join[ctopo[k]] = C.J++;
-  C.max_indeg = n ? *std::max_element(C.indeg.begin(), C.indeg.end()) : 0;
+  // Successor structure of the event replay.  Ops sharing one predecessor
+  // set of two or more ops wait on one barrier node (id n + b) instead of
+  // each counting the same predecessors: a barrier completes when its last
+  // predecessor finishes and releases its members at that instant, so every
+  // ready time is unchanged.
+  std::vector<std::vector<int32_t>> es(cs);  // successors, barriers included
+  std::vector<int32_t> need(n);
+  for (int32_t c = 0; c < n; ++c) need[c] = (int32_t)cp[c].size();
+  std::map<std::vector<int32_t>, std::vector<int32_t>> groups;
+  for (int32_t c = 0; c < n; ++c)
+    if (cp[c].size() >= 2) groups[cp[c]].push_back(c);
+  std::vector<std::vector<int32_t>> bmem;
+  std::vector<int32_t> bneed;
+  for (auto &kv : groups) {
+    if (kv.second.size() < 2) continue;
+    const int32_t b = n + (int32_t)bmem.size();
+    for (int32_t p : kv.first) {
+      std::vector<int32_t> keep;
+      std::set_difference(es[p].begin(), es[p].end(), kv.second.begin(), kv.second.end(),
+                          std::back_inserter(keep));
+      keep.push_back(b);  // ids above n keep the list sorted
+      es[p].swap(keep);
+    }
+    for (int32_t w : kv.second) need[w] = 1;
+    bmem.push_back(kv.second);
+    bneed.push_back((int32_t)kv.first.size());
+  }
+  const int32_t nb = (int32_t)bmem.size();
+  C.barriers = nb;
 
-  // successor entries are pairs {compact id, join index or -1}
-  C.ops.resize(n + 1);
+  // joins: ops still counting two or more predecessors, in topological order
+  // (concurrently pending joins get nearby indices), then the barriers
+  std::vector<int32_t> join(n + nb, -1);
+  C.J = 0;
+  C.jneed.clear();
+  for (int32_t k = 0; k < n; ++k)
+    if (need[ctopo[k]] >= 2) {
+      join[ctopo[k]] = C.J++;
+      C.jneed.push_back(need[ctopo[k]]);
+    }
+  for (int32_t b = 0; b < nb; ++b) {
+    join[n + b] = C.J++;
+    C.jneed.push_back(bneed[b]);
+  }
+  C.max_indeg = 0;
+  for (int32_t c = 0; c < n; ++c) C.max_indeg = std::max(C.max_indeg, (int32_t)cp[c].size());
+
+  // records and successor entries {id, join index or -1}
+  C.ops.resize(n + nb + 1);
   C.succ.clear();
   int32_t e = 0;
-  for (int32_t c = 0; c < n; ++c) {
-    C.ops[c] = OpRec{orig_of[c], op_res[orig_of[c]], join[c], e};
-    for (int32_t w : cs[c]) {
+  for (int32_t c = 0; c < n + nb; ++c) {
+    const auto &lst = c < n ? es[c] : bmem[c - n];
+    OpRec r{c < n ? orig_of[c] : -1, c < n ? op_res[orig_of[c]] : -1, e, (int32_t)lst.size(),
+            -1, -1, 0, 0};
+    if (!lst.empty()) {
+      r.w0 = lst[0];
+      r.j0 = join[lst[0]];
+    }
+    C.ops[c] = r;
+    for (int32_t w : lst) {
       C.succ.push_back(w);
       C.succ.push_back(join[w]);
       ++e;
     }
   }
-  C.ops[n] = OpRec{-1, -1, -1, e};
-  C.m = e;
+  C.ops[n + nb] = OpRec{-1, -1, e, 0, -1, -1, 0, 0};
+  C.m = 0;
+  for (int32_t c = 0; c < n; ++c) C.m += (int64_t)cs[c].size();
   C.src.clear();
   for (int32_t c = 0; c < n; ++c)
-    if (C.indeg[c] == 0) C.src.push_back(c);
+    if (cp[c].empty()) C.src.push_back(c);
 
   C.heap_cap = n ? std::max(1, min_path_cover(n, cs)) : 0;
 
@@ -267,7 +314,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   C.cp_pred.clear();
   for (int32_t k = 0; k < n; ++k) {
     int32_t v = order[k];
-    C.cp[k] = CpRec{orig_of[v], slot[v], (int32_t)C.cp_pred.size(), 0};
+    C.cp[k] = CpRec{orig_of[v], slot[v], (int32_t)C.cp_pred.size(), (int32_t)cp[v].size()};
     for (int32_t p : cp[v]) C.cp_pred.push_back(slot[p]);
   }
   C.cp[n] = CpRec{-1, -1, (int32_t)C.cp_pred.size(), 0};
@@ -347,7 +394,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
     return o;
   };
   size_t o_ops = take(bytes_of(C.ops)), o_succ = take(bytes_of(C.succ)),
-         o_indeg = take(bytes_of(C.indeg)), o_src = take(bytes_of(C.src)),
+         o_jneed = take(bytes_of(C.jneed)), o_src = take(bytes_of(C.src)),
          o_cp = take(bytes_of(C.cp)), o_cpp = take(bytes_of(C.cp_pred)),
          o_pp = take(bytes_of(C.pred_ptr)), o_pr = take(bytes_of(C.pred)),
          o_topo = take(bytes_of(C.topo));
@@ -360,7 +407,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
     return b == 0 || hipMemcpy(base + o, src, b, hipMemcpyHostToDevice) == hipSuccess;
   };
   bool ok = put(o_ops, C.ops.data(), bytes_of(C.ops)) && put(o_succ, C.succ.data(), bytes_of(C.succ)) &&
-            put(o_indeg, C.indeg.data(), bytes_of(C.indeg)) && put(o_src, C.src.data(), bytes_of(C.src)) &&
+            put(o_jneed, C.jneed.data(), bytes_of(C.jneed)) && put(o_src, C.src.data(), bytes_of(C.src)) &&
             put(o_cp, C.cp.data(), bytes_of(C.cp)) && put(o_cpp, C.cp_pred.data(), bytes_of(C.cp_pred)) &&
             put(o_pp, C.pred_ptr.data(), bytes_of(C.pred_ptr)) && put(o_pr, C.pred.data(), bytes_of(C.pred)) &&
             put(o_topo, C.topo.data(), bytes_of(C.topo));
@@ -379,7 +426,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.max_indeg = C.max_indeg;
   d.ops = (const OpRec *)(base + o_ops);
   d.succ = (const int32_t *)(base + o_succ);
-  d.indeg = (const int32_t *)(base + o_indeg);
+  d.jneed = (const int32_t *)(base + o_jneed);
   d.src = (const int32_t *)(base + o_src);
   d.cp = (const CpRec *)(base + o_cp);
   d.cp_pred = (const int32_t *)(base + o_cpp);
@@ -389,6 +436,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;
+  g->n_barriers = C.barriers;
+  g->row_identity = 1;
+  for (int32_t c = 0; c < n_ops && g->row_identity; ++c) g->row_identity = C.ops[c].orig == c;
   g->h_pred_ptr = C.pred_ptr;
   g->h_pred = C.pred;
 

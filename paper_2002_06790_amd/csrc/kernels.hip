@@ -18,6 +18,23 @@ namespace {
 
 constexpr uint32_t kI32Max = 0x7fffffffu;
 
+// Graph tables are read-only for the whole launch.  Reading them through the
+// constant address space lets wave-uniform reads become scalar loads.
+template <class T>
+using cptr = const __attribute__((address_space(4))) T *;
+template <class T>
+__device__ __forceinline__ cptr<T> as_const(const T *p) {
+  return (cptr<T>)p;
+}
+__device__ __forceinline__ CpRec load_rec(cptr<CpRec> p, int k) {
+  CpRec r;
+  r.orig = p[k].orig;
+  r.slot = p[k].slot;
+  r.pbeg = p[k].pbeg;
+  r.npred = p[k].npred;
+  return r;
+}
+
 __device__ __forceinline__ uint64_t make_key(uint32_t ready, int32_t c) {
   return ((uint64_t)ready << 32) | (uint32_t)c;
 }
@@ -96,8 +113,9 @@ struct EvArgs {
 // time, compact id); it pops the minimum, starts it when both the op is ready
 // and its resource has finished its previous op, and releases successors
 // whose last predecessor this was.  Every lane pops exactly n ops per tile, so
-// the outer loop is wave-uniform.
-template <bool RF_LDS>
+// the outer loop is wave-uniform.  ROW_ID: the caller's op ids equal the
+// compact ids, so the duration row is known as soon as the op is popped.
+template <bool RF_LDS, bool ROW_ID>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -109,6 +127,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
                            : a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
   const int2 *succ = (const int2 *)G.succ;
+  const int4 *rec4 = (const int4 *)G.ops;
 
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
@@ -123,12 +142,16 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       const uint64_t key = heap.get(0);
       const int c = (int)(uint32_t)key;
       const uint32_t ready = (uint32_t)(key >> 32);
-      const OpRec op = G.ops[c];
-      const int send = G.ops[c + 1].sbeg;
-      int32_t d = a.dur[(int64_t)op.orig * a.ld_dur + sc];
-      int r = op.res;
+      // the op's record and (with identity rows) its duration, in parallel
+      int32_t d = 0;
+      if (ROW_ID) d = a.dur[(int64_t)c * a.ld_dur + sc];
+      const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
+      const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, -, -}
+      const int64_t row = ROW_ID ? c : r0.x;
+      if (!ROW_ID) d = a.dur[row * a.ld_dur + sc];
+      int r = r0.y;
       if (a.place) {
-        r = a.place[(int64_t)op.orig * a.ld_place + sc];
+        r = a.place[row * a.ld_place + sc];
         if (r >= R) {
           st |= SIM_ST_BAD_RES;
           r = 0;
@@ -147,28 +170,36 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       }
       rfree[r * kWave] = fin;
       span = fin > span ? fin : span;
-      if (a.finish && active) a.finish[(int64_t)op.orig * a.ld_fin + s] = (int32_t)fin;
+      if (a.finish && active) a.finish[row * a.ld_fin + s] = (int32_t)fin;
       bool hole = true;  // the root slot was popped and is not yet refilled
-      for (int e = op.sbeg; e < send; ++e) {
-        const int2 sw = succ[e];  // {successor, join index or -1}
-        uint64_t nk;
-        if (sw.y < 0) {
-          nk = make_key(fin, sw.x);
-        } else {
-          const int2 js = jst[(size_t)sw.y * kWave];
-          const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
-          if (js.x + 1 < G.indeg[sw.x]) {
-            jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
-            continue;
-          }
-          jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
-          nk = make_key(rdy, sw.x);
-        }
+      auto release = [&](uint32_t t, int w) {
+        const uint64_t nk = make_key(t, w);
         if (hole) {
           heap_sift_root(heap, hs, nk);
           hole = false;
         } else {
           heap_push(heap, hs, nk);
+        }
+      };
+      for (int e = 0; e < r0.w; ++e) {
+        const int2 sw = e == 0 ? make_int2(r1.x, r1.y) : succ[r0.z + e];  // {successor, join or -1}
+        if (sw.y < 0) {
+          release(fin, sw.x);
+          continue;
+        }
+        const int2 js = jst[(size_t)sw.y * kWave];
+        const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
+        if (js.x + 1 < G.jneed[sw.y]) {
+          jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
+          continue;
+        }
+        jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
+        if (sw.x < n) {
+          release(rdy, sw.x);
+        } else {  // a barrier: its members (one predecessor each) are ready now
+          const int4 b0 = rec4[2 * sw.x];
+          const int4 b1 = rec4[2 * sw.x + 1];
+          for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : succ[b0.z + k].x);
         }
       }
       if (hole) {
@@ -204,6 +235,8 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
   const int n = G.n;
+  const cptr<CpRec> cp = as_const(G.cp);
+  const cptr<int32_t> cp_pred = as_const(G.cp_pred);
   uint32_t *slots = LDS ? lds32 + lane : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
@@ -213,21 +246,19 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
     uint32_t mx = 0;
     bool bad = false;
     for (int k0 = 0; k0 < n; k0 += kCpBatch) {
+      // records of the whole batch first (scalar loads), then its duration rows
+      CpRec rec[kCpBatch];
+#pragma unroll
+      for (int u = 0; u < kCpBatch; ++u) rec[u] = load_rec(cp, k0 + u < n ? k0 + u : n - 1);
       int32_t dv[kCpBatch];
 #pragma unroll
-      for (int u = 0; u < kCpBatch; ++u) {
-        const int k = k0 + u < n ? k0 + u : n - 1;
-        dv[u] = a.dur[(int64_t)G.cp[k].orig * a.ld_dur + sc];
-      }
+      for (int u = 0; u < kCpBatch; ++u) dv[u] = a.dur[(int64_t)rec[u].orig * a.ld_dur + sc];
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
-        const int k = k0 + u;
-        if (k < n) {
-          const CpRec rec = G.cp[k];
-          const int pend = G.cp[k + 1].pbeg;
+        if (k0 + u < n) {
           uint32_t best = 0;
-          for (int e = rec.pbeg; e < pend; ++e) {
-            const uint32_t x = slots[(size_t)G.cp_pred[e] * kWave];
+          for (int e = 0; e < rec[u].npred; ++e) {
+            const uint32_t x = slots[(size_t)cp_pred[rec[u].pbeg + e] * kWave];
             best = x > best ? x : best;
           }
           int32_t d = dv[u];
@@ -240,9 +271,9 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
             bad = true;
             dist = kI32Max;
           }
-          if (rec.slot >= 0) slots[(size_t)rec.slot * kWave] = dist;
+          if (rec[u].slot >= 0) slots[(size_t)rec[u].slot * kWave] = dist;
           mx = dist > mx ? dist : mx;
-          if (want_dist) a.dist_out[rec.orig] = (int32_t)dist;
+          if (want_dist) a.dist_out[rec[u].orig] = (int32_t)dist;
         }
       }
     }
@@ -401,7 +432,7 @@ int occupancy_blocks(K kernel, size_t lds, int cus) {
 
 constexpr size_t kLdsBudget = 64 * 1024;       // per workgroup
 constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
-constexpr int kHeapLdsMax = 64;                // heap entries per lane kept in LDS
+constexpr int kHeapLdsMax = 16;                // heap entries per lane kept in LDS
 constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
 
 bool rf_in_lds(const DevGraph &G) { return (size_t)G.R * kWave * 4 <= kRfLdsMax; }
@@ -420,16 +451,21 @@ int plan_scratch(sim_graph *g) {
   const size_t rf_bytes = (size_t)G.R * kWave * 4;
   const bool rf_lds = rf_in_lds(G);
   const size_t heap_room = (kLdsBudget - 16 * 1024 - (rf_lds ? rf_bytes : 0)) / (kWave * 8);
-  P.ev_heap_lds = (int32_t)std::min<size_t>((size_t)G.heap_cap, std::min<size_t>(heap_room, kHeapLdsMax));
+  size_t heap_lds_max = kHeapLdsMax;
+  if (const char *e = getenv("MLSIM_EV_HEAP_LDS"))  // tuning override: heap entries kept in LDS
+    heap_lds_max = (size_t)std::max(0, atoi(e));
+  P.ev_heap_lds = (int32_t)std::min<size_t>((size_t)G.heap_cap, std::min<size_t>(heap_room, heap_lds_max));
   P.ev_join_lds = 0;
   P.ev_lds_bytes = std::max<size_t>(8, (size_t)P.ev_heap_lds * kWave * 8 + (rf_lds ? rf_bytes : 0));
-  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true>, P.ev_lds_bytes, cus)
-                            : occupancy_blocks(k_event<false>, P.ev_lds_bytes, cus);
+  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false>, P.ev_lds_bytes, cus)
+                            : occupancy_blocks(k_event<false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
   const size_t heap_g_bytes = (size_t)(G.heap_cap - P.ev_heap_lds) * kWave * 8;
   const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
   size_t ev_blocks = (size_t)ev_occ;
   if (ev_per_block) ev_blocks = std::min(ev_blocks, std::max<size_t>(1, kScratchBudget / ev_per_block));
+  if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
+    ev_blocks = std::min(ev_blocks, (size_t)std::max(1, atoi(e)));
   P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
 
   // critical path: slots in LDS when they fit
@@ -485,10 +521,10 @@ int plan_scratch(sim_graph *g) {
   if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
   if (getenv("MLSIM_VERBOSE"))
     fprintf(stderr,
-            "[mlsim] n=%d R=%d J=%d heap_cap=%d (lds %d) cp_slots=%d (lds %d) ev_blocks=%d "
-            "cp_blocks=%d ev_lds=%zu scratch=%zu MB\n",
-            G.n, G.R, G.J, G.heap_cap, P.ev_heap_lds, G.cp_slots, P.cp_lds, P.ev_blocks,
-            P.cp_blocks, P.ev_lds_bytes, off >> 20);
+            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (lds %d) cp_slots=%d (lds %d) "
+            "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu scratch=%zu MB\n",
+            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_lds, G.cp_slots, P.cp_lds,
+            P.ev_blocks, P.cp_blocks, P.sw_blocks, P.ev_lds_bytes, off >> 20);
   return SIM_OK;
 }
 
@@ -502,10 +538,19 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.ev_blocks);
-  if (rf_in_lds(g->dg))
-    k_event<true><<<dim3(blocks), dim3(kWave), P.ev_lds_bytes, stream>>>(g->dg, a);
-  else
-    k_event<false><<<dim3(blocks), dim3(kWave), P.ev_lds_bytes, stream>>>(g->dg, a);
+  const dim3 grid(blocks), block(kWave);
+  const size_t lds = P.ev_lds_bytes;
+  if (rf_in_lds(g->dg)) {
+    if (g->row_identity)
+      k_event<true, true><<<grid, block, lds, stream>>>(g->dg, a);
+    else
+      k_event<true, false><<<grid, block, lds, stream>>>(g->dg, a);
+  } else {
+    if (g->row_identity)
+      k_event<false, true><<<grid, block, lds, stream>>>(g->dg, a);
+    else
+      k_event<false, false><<<grid, block, lds, stream>>>(g->dg, a);
+  }
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

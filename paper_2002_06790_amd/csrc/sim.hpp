@@ -13,32 +13,38 @@ namespace mlsim {
 constexpr int kWave = 64;  // CDNA wavefront width: one scenario per lane
 
 // Per compact op (ops are renumbered by (priority, id), so "lower compact id"
-// is exactly the paper-order tie rule).
+// is exactly the paper-order tie rule).  Ids n.. are barrier nodes: a set of
+// ops that share one predecessor set (two or more predecessors) waits on one
+// barrier instead of each counting the predecessors itself; a barrier has no
+// duration or resource and releases its members the moment it completes.
 struct OpRec {
-  int32_t orig;  // caller's op id: row of dur / place / finish
-  int32_t res;   // resource (op_res)
-  int32_t join;  // index among ops with >= 2 predecessors, or -1
-  int32_t sbeg;  // first successor in succ[]; the end is ops[c + 1].sbeg
+  int32_t orig;   // caller's op id: row of dur / place / finish (-1: barrier)
+  int32_t res;    // resource (op_res), -1 for a barrier
+  int32_t sbeg;   // successor entries succ[sbeg, sbeg + nsucc)
+  int32_t nsucc;
+  int32_t w0;     // the first successor entry, repeated here
+  int32_t j0;
+  int32_t pad0, pad1;
 };
 
 // Per position of the critical-path sweep order.
 struct CpRec {
-  int32_t orig;  // row of dur
-  int32_t slot;  // slot receiving dist(v), or -1 if v has no successors
-  int32_t pbeg;  // predecessor slots in cp_pred[pbeg, next.pbeg)
-  int32_t pad;
+  int32_t orig;   // row of dur
+  int32_t slot;   // slot receiving dist(v), or -1 if v has no successors
+  int32_t pbeg;   // predecessor slots in cp_pred[pbeg, pbeg + npred)
+  int32_t npred;
 };
 
 // Device view of a compiled graph (plain pointers, passed by value).
 struct DevGraph {
-  int32_t n, R, J, nsrc;
+  int32_t n, R, J, nsrc;  // n real ops (barriers follow them), J joins
   int32_t heap_cap;       // bound on simultaneously ready ops (>= DAG width)
   int32_t cp_slots;       // live values of the critical-path sweep
   int32_t max_indeg;
   int32_t pad0;
-  const OpRec *ops;       // [n + 1]
-  const int32_t *succ;    // [2m] pairs {compact successor id, its join index or -1}
-  const int32_t *indeg;   // [n] predecessors after reduction
+  const OpRec *ops;       // [n + barriers + 1]
+  const int32_t *succ;    // pairs {successor id, its join index or -1}
+  const int32_t *jneed;   // [J] predecessors a join waits for
   const int32_t *src;     // [nsrc] compact ids of sources
   const CpRec *cp;        // [n + 1]
   const int32_t *cp_pred; // predecessor slot lists of the critical-path sweep
@@ -64,7 +70,8 @@ struct ScratchPlan {
 struct sim_graph {
   int32_t n_ops, n_res;
   int64_t n_edges;  // after dedupe + transitive reduction
-  int32_t n_joins, n_levels;
+  int32_t n_joins, n_levels, n_barriers;
+  int32_t row_identity;  // compact id == caller id for every op (no priorities given)
   int device;
   mlsim::DevGraph dg;
   mlsim::ScratchPlan plan;
