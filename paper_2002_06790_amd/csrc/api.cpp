@@ -35,7 +35,8 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
   const uint32_t algo = flags & 3u;
   if (algo == SIM_ALGO_SWEEP)
     return launch_sweep(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
-  return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
+  return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
+                      st);
 }
 
 extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32_t *dur,

@@ -284,6 +284,10 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
       r.w0 = lst[0];
       r.j0 = join[lst[0]];
     }
+    if (lst.size() > 1) {
+      r.w1 = lst[1];
+      r.j1 = join[lst[1]];
+    }
     C.ops[c] = r;
     for (int32_t w : lst) {
       C.succ.push_back(w);

@@ -44,12 +44,31 @@ __device__ __forceinline__ uint64_t make_key(uint32_t ready, int32_t c) {
 // first-in-first-out resource with the tie rules.  Element i lives in LDS for
 // i < hl and in global scratch above; either way at a stride of one wave, so
 // a wave's accesses to one index are conflict-free (LDS) or coalesced.
+// LDS pointers carry their address space explicitly, so accesses compile to
+// ds_* instructions and never to generic (flat) ones.
+template <class T>
+using lptr = __attribute__((address_space(3))) T *;
+template <class T>
+__device__ __forceinline__ lptr<T> as_lds(T *p) {
+  return (lptr<T>)p;
+}
+
+// Wait for a global load inside the branch that issued it: the empty asm
+// consumes the value, so the compiler's wait lands here and not at a later
+// merge point, where it would also have to cover every load in flight.
+template <class T>
+__device__ __forceinline__ T settle(T v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 struct LaneHeap {
-  uint64_t *l;  // LDS part, this lane's column
-  uint64_t *g;  // global part (index hl upwards), this lane's column
+  lptr<uint64_t> l;  // LDS part, this lane's column
+  uint64_t *g;       // global part (index hl upwards), this lane's column
   int hl;
   __device__ __forceinline__ uint64_t get(int i) const {
-    return i < hl ? l[i * kWave] : g[(size_t)(i - hl) * kWave];
+    if (i < hl) return l[i * kWave];
+    return settle(g[(size_t)(i - hl) * kWave]);
   }
   __device__ __forceinline__ void set(int i, uint64_t x) const {
     if (i < hl)
@@ -59,37 +78,76 @@ struct LaneHeap {
   }
 };
 
+// FAST: every index touched is below hl (the caller checked the whole wave),
+// so the heap is accessed in LDS only.
+template <bool FAST>
+__device__ __forceinline__ uint64_t hget(const LaneHeap &h, int i) {
+  return FAST ? h.l[i * kWave] : h.get(i);
+}
+template <bool FAST>
+__device__ __forceinline__ void hset(const LaneHeap &h, int i, uint64_t x) {
+  if (FAST)
+    h.l[i * kWave] = x;
+  else
+    h.set(i, x);
+}
+
+template <bool FAST>
 __device__ __forceinline__ void heap_push(const LaneHeap &h, int &hs, uint64_t x) {
   int i = hs++;
   while (i > 0) {
     int p = (i - 1) >> 1;
-    uint64_t a = h.get(p);
+    uint64_t a = hget<FAST>(h, p);
     if (a <= x) break;
-    h.set(i, a);
+    hset<FAST>(h, i, a);
     i = p;
   }
-  h.set(i, x);
+  hset<FAST>(h, i, x);
 }
 
 // Put x at the root of a heap of hs elements and restore heap order.
+template <bool FAST>
 __device__ __forceinline__ void heap_sift_root(const LaneHeap &h, int hs, uint64_t x) {
   int i = 0;
   for (;;) {
     int c = 2 * i + 1;
     if (c >= hs) break;
-    uint64_t a = h.get(c);
+    uint64_t a = hget<FAST>(h, c);
     if (c + 1 < hs) {
-      uint64_t b = h.get(c + 1);
+      uint64_t b = hget<FAST>(h, c + 1);
       if (b < a) {
         a = b;
         ++c;
       }
     }
     if (x <= a) break;
-    h.set(i, a);
+    hset<FAST>(h, i, a);
     i = c;
   }
-  h.set(i, x);
+  hset<FAST>(h, i, x);
+}
+
+// Wave-uniform choice between the LDS-only and the general heap code.
+__device__ __forceinline__ void heap_push_any(const LaneHeap &h, int &hs, uint64_t x) {
+  if (__ballot(hs + 1 > h.hl) == 0)
+    heap_push<true>(h, hs, x);
+  else
+    heap_push<false>(h, hs, x);
+}
+__device__ __forceinline__ void heap_sift_root_any(const LaneHeap &h, int hs, uint64_t x) {
+  if (__ballot(hs > h.hl) == 0)
+    heap_sift_root<true>(h, hs, x);
+  else
+    heap_sift_root<false>(h, hs, x);
+}
+
+// The root was popped and nothing replaced it: move the last element up.
+__device__ __forceinline__ void heap_fill_root(const LaneHeap &h, int &hs) {
+  if (--hs <= 0) return;
+  if (__ballot(hs >= h.hl) == 0)
+    heap_sift_root<true>(h, hs, hget<true>(h, hs));
+  else
+    heap_sift_root<false>(h, hs, h.get(hs));
 }
 
 struct EvArgs {
@@ -120,22 +178,29 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
-  const LaneHeap heap{lds + lane,
+  const LaneHeap heap{as_lds(lds) + lane,
                       a.heap_g + (size_t)blockIdx.x * (G.heap_cap - a.heap_lds) * kWave + lane,
                       a.heap_lds};
-  uint32_t *rfree = RF_LDS ? (uint32_t *)(lds + (size_t)a.heap_lds * kWave) + lane
-                           : a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
+  uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
+  lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)a.heap_lds * kWave)) + lane;
   int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
   const int2 *succ = (const int2 *)G.succ;
   const int4 *rec4 = (const int4 *)G.ops;
+  auto rf_get = [&](int r) -> uint32_t { return RF_LDS ? rfree_l[r * kWave] : rfree_g[r * kWave]; };
+  auto rf_set = [&](int r, uint32_t v) {
+    if (RF_LDS)
+      rfree_l[r * kWave] = v;
+    else
+      rfree_g[r * kWave] = v;
+  };
 
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
     const int64_t sc = active ? s : a.n_scen - 1;  // inactive lanes replay a valid column
-    for (int r = 0; r < R; ++r) rfree[r * kWave] = 0;
+    for (int r = 0; r < R; ++r) rf_set(r, 0);
     int hs = 0;
-    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, hs, make_key(0, G.src[k]));
+    for (int k = 0; k < G.nsrc; ++k) heap_push<false>(heap, hs, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
     for (int it = 0; it < n; ++it) {
       if (hs <= 0) break;  // unreachable for a DAG: some op is always ready
@@ -161,28 +226,29 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
         st |= SIM_ST_BAD_DUR;
         d = 1;
       }
-      const uint32_t rf = rfree[r * kWave];
+      const uint32_t rf = rf_get(r);
       const uint32_t start = ready > rf ? ready : rf;
       uint32_t fin = start + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
       if (fin > kI32Max) {
         st |= SIM_ST_OVERFLOW;
         fin = kI32Max;
       }
-      rfree[r * kWave] = fin;
+      rf_set(r, fin);
       span = fin > span ? fin : span;
       if (a.finish && active) a.finish[row * a.ld_fin + s] = (int32_t)fin;
       bool hole = true;  // the root slot was popped and is not yet refilled
       auto release = [&](uint32_t t, int w) {
         const uint64_t nk = make_key(t, w);
         if (hole) {
-          heap_sift_root(heap, hs, nk);
+          heap_sift_root_any(heap, hs, nk);
           hole = false;
         } else {
-          heap_push(heap, hs, nk);
+          heap_push_any(heap, hs, nk);
         }
       };
       for (int e = 0; e < r0.w; ++e) {
-        const int2 sw = e == 0 ? make_int2(r1.x, r1.y) : succ[r0.z + e];  // {successor, join or -1}
+        const int2 sw = e == 0 ? make_int2(r1.x, r1.y)
+                               : e == 1 ? make_int2(r1.z, r1.w) : succ[r0.z + e];  // {successor, join or -1}
         if (sw.y < 0) {
           release(fin, sw.x);
           continue;
@@ -202,10 +268,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
           for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : succ[b0.z + k].x);
         }
       }
-      if (hole) {
-        --hs;
-        if (hs > 0) heap_sift_root(heap, hs, heap.get(hs));
-      }
+      if (hole) heap_fill_root(heap, hs);
     }
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
     if (active) {
@@ -435,7 +498,10 @@ constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up 
 constexpr int kHeapLdsMax = 16;                // heap entries per lane kept in LDS
 constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
 
-bool rf_in_lds(const DevGraph &G) { return (size_t)G.R * kWave * 4 <= kRfLdsMax; }
+bool rf_in_lds(const DevGraph &G) {
+  if (getenv("MLSIM_RF_GLOBAL")) return false;  // tuning override
+  return (size_t)G.R * kWave * 4 <= kRfLdsMax;
+}
 
 }  // namespace
 
@@ -467,6 +533,8 @@ int plan_scratch(sim_graph *g) {
   if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
     ev_blocks = std::min(ev_blocks, (size_t)std::max(1, atoi(e)));
   P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
+
+  const int32_t ev_grid = P.ev_blocks;
 
   // critical path: slots in LDS when they fit
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
@@ -504,9 +572,9 @@ int plan_scratch(sim_graph *g) {
     off += (b + 255) & ~size_t(255);
     return o;
   };
-  g->scratch_ev_heap_off = take(heap_g_bytes * P.ev_blocks);
-  g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * P.ev_blocks);
-  g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * P.ev_blocks);
+  g->scratch_ev_heap_off = take(heap_g_bytes * ev_grid);
+  g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * ev_grid);
+  g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_sw_val_off = take(P.sw_val_lds ? 0 : val_bytes * P.sw_blocks);
   g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_lds ? 0 : cp_bytes * P.cp_blocks);
@@ -522,9 +590,11 @@ int plan_scratch(sim_graph *g) {
   if (getenv("MLSIM_VERBOSE"))
     fprintf(stderr,
             "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (lds %d) cp_slots=%d (lds %d) "
-            "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu scratch=%zu MB\n",
+            "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
+            "scratch=%zu MB\n",
             G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_lds, G.cp_slots, P.cp_lds,
-            P.ev_blocks, P.cp_blocks, P.sw_blocks, P.ev_lds_bytes, off >> 20);
+            P.ev_blocks, P.cp_blocks, P.sw_blocks,
+            P.ev_lds_bytes, off >> 20);
   return SIM_OK;
 }
 
@@ -537,10 +607,11 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_lds,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
-  const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.ev_blocks);
-  const dim3 grid(blocks), block(kWave);
+  const bool rf_lds = rf_in_lds(g->dg);
+  const dim3 block(kWave);
+  const dim3 grid((unsigned)std::min<int64_t>(tiles, P.ev_blocks));
   const size_t lds = P.ev_lds_bytes;
-  if (rf_in_lds(g->dg)) {
+  if (rf_lds) {
     if (g->row_identity)
       k_event<true, true><<<grid, block, lds, stream>>>(g->dg, a);
     else

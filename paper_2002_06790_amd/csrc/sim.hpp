@@ -22,9 +22,10 @@ struct OpRec {
   int32_t res;    // resource (op_res), -1 for a barrier
   int32_t sbeg;   // successor entries succ[sbeg, sbeg + nsucc)
   int32_t nsucc;
-  int32_t w0;     // the first successor entry, repeated here
+  int32_t w0;     // the first two successor entries, repeated here
   int32_t j0;
-  int32_t pad0, pad1;
+  int32_t w1;
+  int32_t j1;
 };
 
 // Per position of the critical-path sweep order.
