@@ -39,11 +39,6 @@ __device__ __forceinline__ uint64_t make_key(uint32_t ready, int32_t c) {
   return ((uint64_t)ready << 32) | (uint32_t)c;
 }
 
-// Binary min-heap of 64-bit keys (ready << 32 | compact id) for one lane.
-// Compact ids follow (priority, id), so key order is the queue order of a
-// first-in-first-out resource with the tie rules.  Element i lives in LDS for
-// i < hl and in global scratch above; either way at a stride of one wave, so
-// a wave's accesses to one index are conflict-free (LDS) or coalesced.
 // LDS pointers carry their address space explicitly, so accesses compile to
 // ds_* instructions and never to generic (flat) ones.
 template <class T>
@@ -61,93 +56,137 @@ __device__ __forceinline__ T settle(T v) {
   asm volatile("" : "+v"(v));
   return v;
 }
+__device__ __forceinline__ int2 settle(int2 v) {
+  asm volatile("" : "+v"(v.x), "+v"(v.y));
+  return v;
+}
+__device__ __forceinline__ int4 settle(int4 v) {
+  asm volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+  return v;
+}
 
-struct LaneHeap {
-  lptr<uint64_t> l;  // LDS part, this lane's column
-  uint64_t *g;       // global part (index hl upwards), this lane's column
-  int hl;
-  __device__ __forceinline__ uint64_t get(int i) const {
-    if (i < hl) return l[i * kWave];
-    return settle(g[(size_t)(i - hl) * kWave]);
+// Per-lane ready list: a 16-ary min-heap of 64-bit keys (ready << 32 |
+// compact id).  Compact ids follow (priority, id), so key order is the queue
+// order of a first-in-first-out resource with the tie rules.
+//
+// Positions run breadth-first from kRoot = 15, which puts the 16 children of
+// position p at 16 (p - 14) ... 16 (p - 14) + 15: every child group is
+// aligned to 16 entries.  The root and its 16 children (positions 15..31) live
+// in LDS, slot-major x lane, conflict-free; positions from 32 on live in
+// global scratch, lane-major, so one child group is one aligned 128-byte line
+// of one lane.  A heap of up to 273 entries thus costs at most one global
+// round trip per pop.  Every position at or beyond the end holds kEmpty,
+// which is larger than any key, so partial groups need no bounds masks; the
+// kernel restores kEmpty wherever the heap shrinks, leaving scratch as found.
+constexpr int kRoot = 15, kLdsEnd = 32;
+constexpr uint64_t kEmpty = ~0ull;
+
+__device__ __forceinline__ int heap_parent(int p) { return (p >> 4) + 14; }
+__device__ __forceinline__ int heap_child0(int p) { return (p - 14) << 4; }
+
+struct WideHeap {
+  lptr<uint64_t> l;  // this lane's LDS column: position p at l[(p - kRoot) * kWave]
+  uint64_t *g;       // this lane's global run: position p at g[p - kLdsEnd]
+  __device__ __forceinline__ uint64_t get(int p) const {
+    if (p < kLdsEnd) return l[(p - kRoot) * kWave];
+    return settle(g[p - kLdsEnd]);
   }
-  __device__ __forceinline__ void set(int i, uint64_t x) const {
-    if (i < hl)
-      l[i * kWave] = x;
+  __device__ __forceinline__ void set(int p, uint64_t x) const {
+    if (p < kLdsEnd)
+      l[(p - kRoot) * kWave] = x;
     else
-      g[(size_t)(i - hl) * kWave] = x;
+      g[p - kLdsEnd] = x;
   }
 };
 
-// FAST: every index touched is below hl (the caller checked the whole wave),
-// so the heap is accessed in LDS only.
-template <bool FAST>
-__device__ __forceinline__ uint64_t hget(const LaneHeap &h, int i) {
-  return FAST ? h.l[i * kWave] : h.get(i);
-}
-template <bool FAST>
-__device__ __forceinline__ void hset(const LaneHeap &h, int i, uint64_t x) {
-  if (FAST)
-    h.l[i * kWave] = x;
-  else
-    h.set(i, x);
-}
-
-template <bool FAST>
-__device__ __forceinline__ void heap_push(const LaneHeap &h, int &hs, uint64_t x) {
-  int i = hs++;
-  while (i > 0) {
-    int p = (i - 1) >> 1;
-    uint64_t a = hget<FAST>(h, p);
-    if (a <= x) break;
-    hset<FAST>(h, i, a);
-    i = p;
-  }
-  hset<FAST>(h, i, x);
-}
-
-// Put x at the root of a heap of hs elements and restore heap order.
-template <bool FAST>
-__device__ __forceinline__ void heap_sift_root(const LaneHeap &h, int hs, uint64_t x) {
-  int i = 0;
-  for (;;) {
-    int c = 2 * i + 1;
-    if (c >= hs) break;
-    uint64_t a = hget<FAST>(h, c);
-    if (c + 1 < hs) {
-      uint64_t b = hget<FAST>(h, c + 1);
-      if (b < a) {
-        a = b;
-        ++c;
+// Minimum of 16 keys and its index, as a balanced tree (short dependency chain).
+__device__ __forceinline__ void min16(uint64_t (&v)[16], uint64_t &m, int &q) {
+  int ix[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) ix[k] = k;
+#pragma unroll
+  for (int st = 1; st < 16; st <<= 1)
+#pragma unroll
+    for (int k = 0; k < 16; k += 2 * st)
+      if (v[k + st] < v[k]) {
+        v[k] = v[k + st];
+        ix[k] = ix[k + st];
       }
+  m = v[0];
+  q = ix[0];
+}
+
+// Smallest child of position p (whose group starts at c = heap_child0(p)).
+__device__ __forceinline__ void child_min(const WideHeap &h, int c, uint64_t &m, int &q) {
+  uint64_t v[16];
+  if (c < kLdsEnd) {  // the root's children
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = h.l[(c + k - kRoot) * kWave];
+  } else {  // one aligned 128-byte line of this lane
+    const uint4 *gp = (const uint4 *)(h.g + (c - kLdsEnd));
+    uint4 w[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = gp[k];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      v[2 * k] = ((uint64_t)w[k].y << 32) | w[k].x;
+      v[2 * k + 1] = ((uint64_t)w[k].w << 32) | w[k].z;
     }
-    if (x <= a) break;
-    hset<FAST>(h, i, a);
-    i = c;
   }
-  hset<FAST>(h, i, x);
+  min16(v, m, q);
+  q += c;
 }
 
-// Wave-uniform choice between the LDS-only and the general heap code.
-__device__ __forceinline__ void heap_push_any(const LaneHeap &h, int &hs, uint64_t x) {
-  if (__ballot(hs + 1 > h.hl) == 0)
-    heap_push<true>(h, hs, x);
-  else
-    heap_push<false>(h, hs, x);
-}
-__device__ __forceinline__ void heap_sift_root_any(const LaneHeap &h, int hs, uint64_t x) {
-  if (__ballot(hs > h.hl) == 0)
-    heap_sift_root<true>(h, hs, x);
-  else
-    heap_sift_root<false>(h, hs, x);
+// Place x at position p of a heap ending at `end` and restore heap order
+// below it.  FAST: no lane's heap reaches beyond LDS (end <= kLdsEnd).
+template <bool FAST>
+__device__ __forceinline__ void sift_down(const WideHeap &h, int end, int p, uint64_t x) {
+  for (;;) {
+    const int c = heap_child0(p);
+    if (c >= end) break;
+    uint64_t m;
+    int q;
+    child_min(h, FAST ? kRoot + 1 : c, m, q);
+    if (x < m) break;  // keys are distinct; kEmpty is above every key
+    h.set(p, m);
+    p = q;
+    if (FAST) break;  // a child of the root has no children in LDS
+  }
+  h.set(p, x);
 }
 
-// The root was popped and nothing replaced it: move the last element up.
-__device__ __forceinline__ void heap_fill_root(const LaneHeap &h, int &hs) {
-  if (--hs <= 0) return;
-  if (__ballot(hs >= h.hl) == 0)
-    heap_sift_root<true>(h, hs, hget<true>(h, hs));
+// Append x and restore heap order above it.
+__device__ __forceinline__ void sift_up(const WideHeap &h, int p, uint64_t x) {
+  while (p > kRoot) {
+    const int par = heap_parent(p);
+    const uint64_t a = h.get(par);
+    if (a < x) break;
+    h.set(p, a);
+    p = par;
+  }
+  h.set(p, x);
+}
+
+// The three heap operations of one replay step, each with a wave-uniform
+// choice of the LDS-only form.
+__device__ __forceinline__ void heap_replace_root(const WideHeap &h, int end, uint64_t x) {
+  if (__ballot(end > kLdsEnd) == 0)
+    sift_down<true>(h, end, kRoot, x);
   else
-    heap_sift_root<false>(h, hs, h.get(hs));
+    sift_down<false>(h, end, kRoot, x);
+}
+__device__ __forceinline__ void heap_push(const WideHeap &h, int &end, uint64_t x) {
+  sift_up(h, end++, x);
+}
+__device__ __forceinline__ void heap_pop_root(const WideHeap &h, int &end) {
+  --end;
+  if (end == kRoot) {
+    h.set(kRoot, kEmpty);
+    return;
+  }
+  const uint64_t x = h.get(end);
+  h.set(end, kEmpty);
+  heap_replace_root(h, end, x);
 }
 
 struct EvArgs {
@@ -160,11 +199,14 @@ struct EvArgs {
   int32_t *finish;
   int64_t ld_fin;
   int32_t *status;
-  uint64_t *heap_g;   // [blocks][heap_cap - heap_lds][64]: heap entries beyond LDS
-  int heap_lds;       // heap entries per lane kept in LDS
+  uint64_t *heap_g;   // [blocks][64][heap_stride]: heap positions from kLdsEnd on, lane-major
+  int heap_stride;    // entries per lane (a multiple of 16)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
 };
+
+constexpr int kHeapLds = kLdsEnd - kRoot;  // heap positions per lane kept in LDS
+constexpr int kFinQ = 8;                   // finish times buffered per lane before a store burst
 
 // Event-driven list scheduling, one scenario per lane (the paper's replay
 // loop, Sec. 2).  Each lane keeps its ready list as a heap keyed by (ready
@@ -173,16 +215,17 @@ struct EvArgs {
 // whose last predecessor this was.  Every lane pops exactly n ops per tile, so
 // the outer loop is wave-uniform.  ROW_ID: the caller's op ids equal the
 // compact ids, so the duration row is known as soon as the op is popped.
+// Finish times are written in bursts of kFinQ stores per lane, so their
+// completion is waited for once per burst instead of once per step.
 template <bool RF_LDS, bool ROW_ID>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
-  const LaneHeap heap{as_lds(lds) + lane,
-                      a.heap_g + (size_t)blockIdx.x * (G.heap_cap - a.heap_lds) * kWave + lane,
-                      a.heap_lds};
+  const WideHeap heap{as_lds(lds) + lane,
+                      a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride};
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
-  lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)a.heap_lds * kWave)) + lane;
+  lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)kHeapLds * kWave)) + lane;
   int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
   const int2 *succ = (const int2 *)G.succ;
   const int4 *rec4 = (const int4 *)G.ops;
@@ -198,25 +241,33 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
     const int64_t sc = active ? s : a.n_scen - 1;  // inactive lanes replay a valid column
+    const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
-    int hs = 0;
-    for (int k = 0; k < G.nsrc; ++k) heap_push<false>(heap, hs, make_key(0, G.src[k]));
+    for (int k = 0; k < kHeapLds; ++k) heap.l[k * kWave] = kEmpty;
+    int end = kRoot;  // one past the last heap position
+    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
+    int32_t fq[kFinQ], rq[kFinQ];  // buffered finish times and their rows
+    auto flush = [&](int cnt) {
+#pragma unroll
+      for (int k = 0; k < kFinQ; ++k)
+        if (k < cnt && store_fin) a.finish[(int64_t)rq[k] * a.ld_fin + s] = fq[k];
+    };
     for (int it = 0; it < n; ++it) {
-      if (hs <= 0) break;  // unreachable for a DAG: some op is always ready
-      const uint64_t key = heap.get(0);
+      if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
+      const uint64_t key = heap.l[0];
       const int c = (int)(uint32_t)key;
       const uint32_t ready = (uint32_t)(key >> 32);
       // the op's record and (with identity rows) its duration, in parallel
       int32_t d = 0;
       if (ROW_ID) d = a.dur[(int64_t)c * a.ld_dur + sc];
       const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
-      const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, -, -}
-      const int64_t row = ROW_ID ? c : r0.x;
-      if (!ROW_ID) d = a.dur[row * a.ld_dur + sc];
+      const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, second, its join}
+      const int32_t row = ROW_ID ? c : r0.x;
+      if (!ROW_ID) d = a.dur[(int64_t)row * a.ld_dur + sc];
       int r = r0.y;
       if (a.place) {
-        r = a.place[row * a.ld_place + sc];
+        r = a.place[(int64_t)row * a.ld_place + sc];
         if (r >= R) {
           st |= SIM_ST_BAD_RES;
           r = 0;
@@ -235,27 +286,35 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       }
       rf_set(r, fin);
       span = fin > span ? fin : span;
-      if (a.finish && active) a.finish[row * a.ld_fin + s] = (int32_t)fin;
-      bool hole = true;  // the root slot was popped and is not yet refilled
+      const int qs = it & (kFinQ - 1);  // wave-uniform
+#pragma unroll
+      for (int k = 0; k < kFinQ; ++k)
+        if (k == qs) {
+          fq[k] = (int32_t)fin;
+          rq[k] = row;
+        }
+      if (qs == kFinQ - 1) flush(kFinQ);
+      bool hole = true;  // the root was popped and is not yet refilled
       auto release = [&](uint32_t t, int w) {
         const uint64_t nk = make_key(t, w);
         if (hole) {
-          heap_sift_root_any(heap, hs, nk);
+          heap_replace_root(heap, end, nk);
           hole = false;
         } else {
-          heap_push_any(heap, hs, nk);
+          heap_push(heap, end, nk);
         }
       };
       for (int e = 0; e < r0.w; ++e) {
         const int2 sw = e == 0 ? make_int2(r1.x, r1.y)
-                               : e == 1 ? make_int2(r1.z, r1.w) : succ[r0.z + e];  // {successor, join or -1}
+                               : e == 1 ? make_int2(r1.z, r1.w) : settle(succ[r0.z + e]);  // {successor, join or -1}
         if (sw.y < 0) {
           release(fin, sw.x);
           continue;
         }
-        const int2 js = jst[(size_t)sw.y * kWave];
+        const int2 js = settle(jst[(size_t)sw.y * kWave]);
+        const int need = settle(G.jneed[sw.y]);
         const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
-        if (js.x + 1 < G.jneed[sw.y]) {
+        if (js.x + 1 < need) {
           jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
           continue;
         }
@@ -263,13 +322,14 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
         if (sw.x < n) {
           release(rdy, sw.x);
         } else {  // a barrier: its members (one predecessor each) are ready now
-          const int4 b0 = rec4[2 * sw.x];
-          const int4 b1 = rec4[2 * sw.x + 1];
-          for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : succ[b0.z + k].x);
+          const int4 b0 = settle(rec4[2 * sw.x]);
+          const int4 b1 = settle(rec4[2 * sw.x + 1]);
+          for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : settle(succ[b0.z + k].x));
         }
       }
-      if (hole) heap_fill_root(heap, hs);
+      if (hole) heap_pop_root(heap, end);
     }
+    flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
     if (active) {
       a.makespan[s] = st ? -1 : (int32_t)span;
@@ -493,10 +553,10 @@ int occupancy_blocks(K kernel, size_t lds, int cus) {
   return per_cu * cus;
 }
 
-constexpr size_t kLdsBudget = 64 * 1024;       // per workgroup
 constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
-constexpr int kHeapLdsMax = 16;                // heap entries per lane kept in LDS
 constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
+
+char *base_heap(sim_graph *g) { return (char *)g->scratch + g->scratch_ev_heap_off; }
 
 bool rf_in_lds(const DevGraph &G) {
   if (getenv("MLSIM_RF_GLOBAL")) return false;  // tuning override
@@ -512,21 +572,17 @@ int plan_scratch(sim_graph *g) {
   if (hipGetDeviceProperties(&prop, g->device) != hipSuccess) return SIM_E_HIP;
   const int cus = prop.multiProcessorCount;
 
-  // event kernel: resource times in LDS when they fit; the top of each lane's
-  // heap in LDS, the rest (up to the exact bound) in global scratch
+  // event kernel: resource times in LDS when they fit; the root of each
+  // lane's heap and its children in LDS, deeper positions (up to the exact
+  // bound on ready ops) in global scratch
   const size_t rf_bytes = (size_t)G.R * kWave * 4;
   const bool rf_lds = rf_in_lds(G);
-  const size_t heap_room = (kLdsBudget - 16 * 1024 - (rf_lds ? rf_bytes : 0)) / (kWave * 8);
-  size_t heap_lds_max = kHeapLdsMax;
-  if (const char *e = getenv("MLSIM_EV_HEAP_LDS"))  // tuning override: heap entries kept in LDS
-    heap_lds_max = (size_t)std::max(0, atoi(e));
-  P.ev_heap_lds = (int32_t)std::min<size_t>((size_t)G.heap_cap, std::min<size_t>(heap_room, heap_lds_max));
-  P.ev_join_lds = 0;
-  P.ev_lds_bytes = std::max<size_t>(8, (size_t)P.ev_heap_lds * kWave * 8 + (rf_lds ? rf_bytes : 0));
+  P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 16 + 15) & ~size_t(15));
+  P.ev_lds_bytes = (size_t)kHeapLds * kWave * 8 + (rf_lds ? rf_bytes : 0);
   const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false>, P.ev_lds_bytes, cus)
                             : occupancy_blocks(k_event<false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
-  const size_t heap_g_bytes = (size_t)(G.heap_cap - P.ev_heap_lds) * kWave * 8;
+  const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
   size_t ev_blocks = (size_t)ev_occ;
   if (ev_per_block) ev_blocks = std::min(ev_blocks, std::max<size_t>(1, kScratchBudget / ev_per_block));
@@ -584,15 +640,17 @@ int plan_scratch(sim_graph *g) {
     g->scratch = nullptr;
     return SIM_E_NOMEM;
   }
-  // join state must start cleared; the kernels keep it cleared
+  // join state must start cleared and heap positions empty (all ones); the
+  // kernels leave both that way
   if (hipMemset(g->scratch, 0, off) != hipSuccess) return SIM_E_HIP;
+  if (hipMemset(base_heap(g), 0xff, heap_g_bytes * ev_grid) != hipSuccess) return SIM_E_HIP;
   if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
   if (getenv("MLSIM_VERBOSE"))
     fprintf(stderr,
-            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (lds %d) cp_slots=%d (lds %d) "
+            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d) cp_slots=%d (lds %d) "
             "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
             "scratch=%zu MB\n",
-            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_lds, G.cp_slots, P.cp_lds,
+            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, G.cp_slots, P.cp_lds,
             P.ev_blocks, P.cp_blocks, P.sw_blocks,
             P.ev_lds_bytes, off >> 20);
   return SIM_OK;
@@ -604,7 +662,7 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
-           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_lds,
+           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
