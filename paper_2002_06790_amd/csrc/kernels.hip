@@ -71,31 +71,47 @@ __device__ __forceinline__ int4 settle(int4 v) {
 //
 // Positions run breadth-first from kRoot = 15, which puts the 16 children of
 // position p at 16 (p - 14) ... 16 (p - 14) + 15: every child group is
-// aligned to 16 entries.  The root and its 16 children (positions 15..31) live
-// in LDS, slot-major x lane, conflict-free; positions from 32 on live in
-// global scratch, lane-major, so one child group is one aligned 128-byte line
-// of one lane.  A heap of up to 273 entries thus costs at most one global
-// round trip per pop.  Every position at or beyond the end holds kEmpty,
-// which is larger than any key, so partial groups need no bounds masks; the
-// kernel restores kEmpty wherever the heap shrinks, leaving scratch as found.
-constexpr int kRoot = 15, kLdsEnd = 32;
+// aligned to 16 entries.  The root is kept in a register, its 16 children
+// (positions 16..31) in LDS, slot-major x lane, conflict-free; positions from
+// 32 on live in global scratch, lane-major, so one child group is one aligned
+// 128-byte line of one lane.  Every position at or beyond the end holds
+// kEmpty, which is larger than any key, so partial groups need no bounds
+// masks; the kernel restores kEmpty wherever the heap shrinks, leaving
+// scratch as it found it.
+constexpr int kRoot = 15, kL1 = 16, kLdsEnd = 32;
 constexpr uint64_t kEmpty = ~0ull;
 
 __device__ __forceinline__ int heap_parent(int p) { return (p >> 4) + 14; }
 __device__ __forceinline__ int heap_child0(int p) { return (p - 14) << 4; }
 
 struct WideHeap {
-  lptr<uint64_t> l;  // this lane's LDS column: position p at l[(p - kRoot) * kWave]
-  uint64_t *g;       // this lane's global run: position p at g[p - kLdsEnd]
+  lptr<uint64_t> l;  // this lane's LDS column: position p (16..31) at l[(p - kL1) * kWave]
+  uint64_t *g;       // this lane's global run: position p (>= 32) at g[p - kLdsEnd]
   __device__ __forceinline__ uint64_t get(int p) const {
-    if (p < kLdsEnd) return l[(p - kRoot) * kWave];
+    if (p < kLdsEnd) return l[(p - kL1) * kWave];
     return settle(g[p - kLdsEnd]);
   }
   __device__ __forceinline__ void set(int p, uint64_t x) const {
     if (p < kLdsEnd)
-      l[(p - kRoot) * kWave] = x;
+      l[(p - kL1) * kWave] = x;
     else
       g[p - kLdsEnd] = x;
+  }
+  __device__ __forceinline__ void lds_group(uint64_t (&v)[16]) const {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = l[k * kWave];
+  }
+  // the group starting at c >= kLdsEnd: one aligned 128-byte line
+  __device__ __forceinline__ void global_group(int c, uint64_t (&v)[16]) const {
+    const uint4 *gp = (const uint4 *)(g + (c - kLdsEnd));
+    uint4 w[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = gp[k];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      v[2 * k] = ((uint64_t)w[k].y << 32) | w[k].x;
+      v[2 * k + 1] = ((uint64_t)w[k].w << 32) | w[k].z;
+    }
   }
 };
 
@@ -116,77 +132,141 @@ __device__ __forceinline__ void min16(uint64_t (&v)[16], uint64_t &m, int &q) {
   q = ix[0];
 }
 
-// Smallest child of position p (whose group starts at c = heap_child0(p)).
-__device__ __forceinline__ void child_min(const WideHeap &h, int c, uint64_t &m, int &q) {
-  uint64_t v[16];
-  if (c < kLdsEnd) {  // the root's children
-#pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = h.l[(c + k - kRoot) * kWave];
-  } else {  // one aligned 128-byte line of this lane
-    const uint4 *gp = (const uint4 *)(h.g + (c - kLdsEnd));
-    uint4 w[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) w[k] = gp[k];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      v[2 * k] = ((uint64_t)w[k].y << 32) | w[k].x;
-      v[2 * k + 1] = ((uint64_t)w[k].w << 32) | w[k].z;
-    }
-  }
-  min16(v, m, q);
-  q += c;
-}
-
-// Place x at position p of a heap ending at `end` and restore heap order
-// below it.  FAST: no lane's heap reaches beyond LDS (end <= kLdsEnd).
-template <bool FAST>
-__device__ __forceinline__ void sift_down(const WideHeap &h, int end, int p, uint64_t x) {
+// Place x at position p (>= 32) of a heap ending at `end` and restore heap
+// order below it (one global round trip per level).
+__device__ __forceinline__ void sift_down_deep(const WideHeap &h, int end, int p, uint64_t x) {
   for (;;) {
     const int c = heap_child0(p);
     if (c >= end) break;
-    uint64_t m;
+    uint64_t v[16], m;
     int q;
-    child_min(h, FAST ? kRoot + 1 : c, m, q);
+    h.global_group(c, v);
+    min16(v, m, q);
     if (x < m) break;  // keys are distinct; kEmpty is above every key
     h.set(p, m);
-    p = q;
-    if (FAST) break;  // a child of the root has no children in LDS
+    p = c + q;
   }
   h.set(p, x);
 }
 
 // Append x and restore heap order above it.
-__device__ __forceinline__ void sift_up(const WideHeap &h, int p, uint64_t x) {
+__device__ __forceinline__ void heap_push(const WideHeap &h, uint64_t &root, int &end, uint64_t x) {
+  int p = end++;
   while (p > kRoot) {
     const int par = heap_parent(p);
-    const uint64_t a = h.get(par);
+    const uint64_t a = par == kRoot ? root : h.get(par);
     if (a < x) break;
     h.set(p, a);
     p = par;
   }
-  h.set(p, x);
+  if (p == kRoot)
+    root = x;
+  else
+    h.set(p, x);
 }
 
-// The three heap operations of one replay step, each with a wave-uniform
-// choice of the LDS-only form.
-__device__ __forceinline__ void heap_replace_root(const WideHeap &h, int end, uint64_t x) {
-  if (__ballot(end > kLdsEnd) == 0)
-    sift_down<true>(h, end, kRoot, x);
-  else
-    sift_down<false>(h, end, kRoot, x);
+// What one replay step reads of its heap before it knows the new key: the
+// smallest child of the root (LDS) and, for heaps beyond LDS, that child's
+// own child group and the last element (global).  These loads go out with
+// the step's duration and record loads, so a sift-down costs no round trip
+// of its own unless it goes deeper than position 272.
+struct HeapAhead {
+  uint64_t m1;      // smallest child of the root (kEmpty if none)
+  int q1;           // its position
+  int c2;           // first child of q1 (>= end: none)
+  uint64_t v2[16];  // that group (valid if c2 < end)
+  uint64_t m2;      // its minimum
+  int q2;           // the minimum's index in the group
+  uint64_t last;    // the last element when it sits in global memory
+};
+
+template <bool DEEP>
+__device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, HeapAhead &A) {
+  A.m1 = kEmpty;
+  A.q1 = kL1;
+  if (end > kL1) {
+    uint64_t v[16];
+    h.lds_group(v);
+    min16(v, A.m1, A.q1);
+    A.q1 += kL1;
+  }
+  A.c2 = heap_child0(A.q1);
+  if (DEEP) {
+    // loads stay inside this lane's run: groups and positions past the end
+    // are replaced by position 32, which every run holds
+    h.global_group(A.c2 < end ? A.c2 : kLdsEnd, A.v2);
+    A.last = h.g[(end - 1 >= kLdsEnd ? end - 1 : kLdsEnd) - kLdsEnd];
+  }
 }
-__device__ __forceinline__ void heap_push(const WideHeap &h, int &end, uint64_t x) {
-  sift_up(h, end++, x);
+
+// Use the look-ahead loads on every path (their minimum is needed on most),
+// so no load is still in flight when the step ends: a wait at the top of the
+// next step would also wait for this step's stores.
+template <bool DEEP>
+__device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
+  if (DEEP) {
+    uint64_t v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = A.v2[k];
+    min16(v, A.m2, A.q2);
+    A.last = settle(A.last);
+  }
 }
-__device__ __forceinline__ void heap_pop_root(const WideHeap &h, int &end) {
-  --end;
-  if (end == kRoot) {
-    h.set(kRoot, kEmpty);
+
+// Replace the root by x (the first op a step releases), using the look-ahead.
+template <bool DEEP>
+__device__ __forceinline__ void heap_replace_root(const WideHeap &h, uint64_t &root, int end,
+                                                  HeapAhead &A, uint64_t x) {
+  if (x < A.m1) {  // also when the root has no children (m1 = kEmpty)
+    root = x;
     return;
   }
-  const uint64_t x = h.get(end);
-  h.set(end, kEmpty);
-  heap_replace_root(h, end, x);
+  root = A.m1;
+  const int p = A.q1;
+  if (!DEEP || A.c2 >= end) {
+    h.l[(p - kL1) * kWave] = x;
+    return;
+  }
+  if (x < A.m2) {
+    h.l[(p - kL1) * kWave] = x;
+    return;
+  }
+  h.l[(p - kL1) * kWave] = A.m2;
+  sift_down_deep(h, end, A.c2 + A.q2, x);
+}
+
+// Remove the root when the step released nothing, using the look-ahead.
+template <bool DEEP>
+__device__ __forceinline__ void heap_pop_root(const WideHeap &h, uint64_t &root, int &end, HeapAhead &A) {
+  const int lp = --end;  // position of the last element
+  if (lp == kRoot) {
+    root = kEmpty;
+    return;
+  }
+  if (lp < kLdsEnd) {  // the heap fits in LDS: take the last child, rescan
+    const uint64_t x = h.l[(lp - kL1) * kWave];
+    h.l[(lp - kL1) * kWave] = kEmpty;
+    uint64_t v[16], m1;
+    int q1;
+    h.lds_group(v);
+    min16(v, m1, q1);
+    if (x < m1) {
+      root = x;
+    } else {
+      root = m1;
+      h.l[q1 * kWave] = x;
+    }
+    return;
+  }
+  const uint64_t x = A.last;
+  h.g[lp - kLdsEnd] = kEmpty;
+  if (DEEP && lp == A.c2 + A.q2) {  // the group's minimum left it: find the next one
+#pragma unroll
+    for (int k = 0; k < 16; ++k)  // unrolled: no indexed register access
+      if (k == A.q2) A.v2[k] = kEmpty;
+    min16(A.v2, A.m2, A.q2);
+  }
+  heap_replace_root<DEEP>(h, root, end, A, x);
 }
 
 struct EvArgs {
@@ -205,8 +285,103 @@ struct EvArgs {
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
 };
 
-constexpr int kHeapLds = kLdsEnd - kRoot;  // heap positions per lane kept in LDS
-constexpr int kFinQ = 8;                   // finish times buffered per lane before a store burst
+constexpr int kHeapLds = kLdsEnd - kL1;  // heap positions per lane kept in LDS
+constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
+
+// One replay step of k_event (see there).  DEEP: some lane's heap reaches
+// global memory, so the step reads its heap ahead.
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, class RfGet, class RfSet, class Flush>
+__device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, const WideHeap &heap,
+                                           uint64_t &root, int &end, int2 *jst, int it, int64_t s,
+                                           int64_t sc, uint32_t &st, uint32_t &span,
+                                           int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
+                                           RfGet rf_get, RfSet rf_set, Flush flush) {
+  const int n = G.n, R = G.R;
+  const int2 *succ = (const int2 *)G.succ;
+  const int4 *rec4 = (const int4 *)G.ops;
+  const uint64_t key = root;
+  const int c = (int)(uint32_t)key;
+  const uint32_t ready = (uint32_t)(key >> 32);
+  // every global load of the step is issued before the first is used
+  const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
+  const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, second, its join}
+  int32_t d = 0;
+  int rp = 0;
+  if (ROW_ID) {
+    d = a.dur[(int64_t)c * a.ld_dur + sc];
+    if (PLACE) rp = a.place[(int64_t)c * a.ld_place + sc];
+  }
+  HeapAhead A;
+  heap_look_ahead<DEEP>(heap, end, A);
+  // keep the scheduler from sinking these loads below the first use of d
+  __builtin_amdgcn_sched_barrier(0);
+  const int32_t row = ROW_ID ? c : r0.x;
+  if (!ROW_ID) {
+    d = a.dur[(int64_t)row * a.ld_dur + sc];
+    if (PLACE) rp = a.place[(int64_t)row * a.ld_place + sc];
+  }
+  int r = PLACE ? rp : r0.y;
+  if (PLACE && r >= R) {
+    st |= SIM_ST_BAD_RES;
+    r = 0;
+  }
+  if (d < 1) {
+    st |= SIM_ST_BAD_DUR;
+    d = 1;
+  }
+  const uint32_t rf = rf_get(r);
+  const uint32_t start = ready > rf ? ready : rf;
+  uint32_t fin = start + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
+  if (fin > kI32Max) {
+    st |= SIM_ST_OVERFLOW;
+    fin = kI32Max;
+  }
+  rf_set(r, fin);
+  span = fin > span ? fin : span;
+  heap_settle_ahead<DEEP>(A);
+  const int qs = it & (kFinQ - 1);  // wave-uniform
+#pragma unroll
+  for (int k = 0; k < kFinQ; ++k)
+    if (k == qs) {
+      fq[k] = (int32_t)fin;
+      rq[k] = row;
+    }
+  if (qs == kFinQ - 1) flush(kFinQ);
+  bool hole = true;  // the root was popped and is not yet replaced
+  auto release = [&](uint32_t t, int w) {
+    const uint64_t nk = make_key(t, w);
+    if (hole) {
+      heap_replace_root<DEEP>(heap, root, end, A, nk);
+      hole = false;
+    } else {
+      heap_push(heap, root, end, nk);
+    }
+  };
+  for (int e = 0; e < r0.w; ++e) {
+    const int2 sw = e == 0 ? make_int2(r1.x, r1.y)
+                           : e == 1 ? make_int2(r1.z, r1.w) : settle(succ[r0.z + e]);  // {successor, join or -1}
+    if (sw.y < 0) {
+      release(fin, sw.x);
+      continue;
+    }
+    const int2 js = settle(jst[(size_t)sw.y * kWave]);
+    const int need = settle(G.jneed[sw.y]);
+    const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
+    if (js.x + 1 < need) {
+      jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
+      continue;
+    }
+    jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
+    if (sw.x < n) {
+      release(rdy, sw.x);
+    } else {  // a barrier: its members (one predecessor each) are ready now
+      const int4 b0 = settle(rec4[2 * sw.x]);
+      const int4 b1 = settle(rec4[2 * sw.x + 1]);
+      for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : settle(succ[b0.z + k].x));
+    }
+  }
+  if (hole) heap_pop_root<DEEP>(heap, root, end, A);
+}
 
 // Event-driven list scheduling, one scenario per lane (the paper's replay
 // loop, Sec. 2).  Each lane keeps its ready list as a heap keyed by (ready
@@ -215,9 +390,10 @@ constexpr int kFinQ = 8;                   // finish times buffered per lane bef
 // whose last predecessor this was.  Every lane pops exactly n ops per tile, so
 // the outer loop is wave-uniform.  ROW_ID: the caller's op ids equal the
 // compact ids, so the duration row is known as soon as the op is popped.
-// Finish times are written in bursts of kFinQ stores per lane, so their
-// completion is waited for once per burst instead of once per step.
-template <bool RF_LDS, bool ROW_ID>
+// PLACE: resources come from the per-scenario placement matrix.  Finish times
+// are written in bursts of kFinQ stores per lane, so their completion is
+// waited for once per burst instead of once per step.
+template <bool RF_LDS, bool ROW_ID, bool PLACE>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -227,8 +403,6 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)kHeapLds * kWave)) + lane;
   int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
-  const int2 *succ = (const int2 *)G.succ;
-  const int4 *rec4 = (const int4 *)G.ops;
   auto rf_get = [&](int r) -> uint32_t { return RF_LDS ? rfree_l[r * kWave] : rfree_g[r * kWave]; };
   auto rf_set = [&](int r, uint32_t v) {
     if (RF_LDS)
@@ -244,8 +418,9 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     for (int k = 0; k < kHeapLds; ++k) heap.l[k * kWave] = kEmpty;
+    uint64_t root = kEmpty;
     int end = kRoot;  // one past the last heap position
-    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
+    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, root, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
     int32_t fq[kFinQ], rq[kFinQ];  // buffered finish times and their rows
     auto flush = [&](int cnt) {
@@ -255,79 +430,12 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     };
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
-      const uint64_t key = heap.l[0];
-      const int c = (int)(uint32_t)key;
-      const uint32_t ready = (uint32_t)(key >> 32);
-      // the op's record and (with identity rows) its duration, in parallel
-      int32_t d = 0;
-      if (ROW_ID) d = a.dur[(int64_t)c * a.ld_dur + sc];
-      const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
-      const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, second, its join}
-      const int32_t row = ROW_ID ? c : r0.x;
-      if (!ROW_ID) d = a.dur[(int64_t)row * a.ld_dur + sc];
-      int r = r0.y;
-      if (a.place) {
-        r = a.place[(int64_t)row * a.ld_place + sc];
-        if (r >= R) {
-          st |= SIM_ST_BAD_RES;
-          r = 0;
-        }
-      }
-      if (d < 1) {
-        st |= SIM_ST_BAD_DUR;
-        d = 1;
-      }
-      const uint32_t rf = rf_get(r);
-      const uint32_t start = ready > rf ? ready : rf;
-      uint32_t fin = start + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
-      if (fin > kI32Max) {
-        st |= SIM_ST_OVERFLOW;
-        fin = kI32Max;
-      }
-      rf_set(r, fin);
-      span = fin > span ? fin : span;
-      const int qs = it & (kFinQ - 1);  // wave-uniform
-#pragma unroll
-      for (int k = 0; k < kFinQ; ++k)
-        if (k == qs) {
-          fq[k] = (int32_t)fin;
-          rq[k] = row;
-        }
-      if (qs == kFinQ - 1) flush(kFinQ);
-      bool hole = true;  // the root was popped and is not yet refilled
-      auto release = [&](uint32_t t, int w) {
-        const uint64_t nk = make_key(t, w);
-        if (hole) {
-          heap_replace_root(heap, end, nk);
-          hole = false;
-        } else {
-          heap_push(heap, end, nk);
-        }
-      };
-      for (int e = 0; e < r0.w; ++e) {
-        const int2 sw = e == 0 ? make_int2(r1.x, r1.y)
-                               : e == 1 ? make_int2(r1.z, r1.w) : settle(succ[r0.z + e]);  // {successor, join or -1}
-        if (sw.y < 0) {
-          release(fin, sw.x);
-          continue;
-        }
-        const int2 js = settle(jst[(size_t)sw.y * kWave]);
-        const int need = settle(G.jneed[sw.y]);
-        const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
-        if (js.x + 1 < need) {
-          jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
-          continue;
-        }
-        jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
-        if (sw.x < n) {
-          release(rdy, sw.x);
-        } else {  // a barrier: its members (one predecessor each) are ready now
-          const int4 b0 = settle(rec4[2 * sw.x]);
-          const int4 b1 = settle(rec4[2 * sw.x + 1]);
-          for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : settle(succ[b0.z + k].x));
-        }
-      }
-      if (hole) heap_pop_root(heap, end);
+      if (__ballot(end > kLdsEnd))
+        event_step<true, RF_LDS, ROW_ID, PLACE>(G, a, heap, root, end, jst, it, s, sc, st, span, fq, rq,
+                                         rf_get, rf_set, flush);
+      else
+        event_step<false, RF_LDS, ROW_ID, PLACE>(G, a, heap, root, end, jst, it, s, sc, st, span, fq, rq,
+                                          rf_get, rf_set, flush);
     }
     flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
@@ -579,8 +687,8 @@ int plan_scratch(sim_graph *g) {
   const bool rf_lds = rf_in_lds(G);
   P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 16 + 15) & ~size_t(15));
   P.ev_lds_bytes = (size_t)kHeapLds * kWave * 8 + (rf_lds ? rf_bytes : 0);
-  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false>, P.ev_lds_bytes, cus)
-                            : occupancy_blocks(k_event<false, false>, P.ev_lds_bytes, cus);
+  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false>, P.ev_lds_bytes, cus)
+                            : occupancy_blocks(k_event<false, false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
@@ -669,16 +777,16 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
   const dim3 block(kWave);
   const dim3 grid((unsigned)std::min<int64_t>(tiles, P.ev_blocks));
   const size_t lds = P.ev_lds_bytes;
-  if (rf_lds) {
-    if (g->row_identity)
-      k_event<true, true><<<grid, block, lds, stream>>>(g->dg, a);
-    else
-      k_event<true, false><<<grid, block, lds, stream>>>(g->dg, a);
-  } else {
-    if (g->row_identity)
-      k_event<false, true><<<grid, block, lds, stream>>>(g->dg, a);
-    else
-      k_event<false, false><<<grid, block, lds, stream>>>(g->dg, a);
+  const int variant = (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+  switch (variant) {
+    case 0: k_event<false, false, false><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 1: k_event<false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 2: k_event<false, true, false><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 3: k_event<false, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 4: k_event<true, false, false><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 5: k_event<true, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 6: k_event<true, true, false><<<grid, block, lds, stream>>>(g->dg, a); break;
+    default: k_event<true, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   }
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
