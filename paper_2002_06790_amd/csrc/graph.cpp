@@ -254,10 +254,20 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   }
   const int32_t nb = (int32_t)bmem.size();
   C.barriers = nb;
+  // A barrier's members share one ready time, so they leave the ready list in
+  // compact-id order one after another.  The barrier releases only its first
+  // member; popping member i releases member i + 1 at the same ready time
+  // (a "sibling" entry, first in its list).  The ready list then holds one
+  // entry per completed barrier instead of all its members, and the pop
+  // order is unchanged: the held-back members are never the minimum.
+  for (int32_t b = 0; b < nb; ++b) {
+    const auto &mem = bmem[b];
+    for (size_t i = 0; i + 1 < mem.size(); ++i) es[mem[i]].insert(es[mem[i]].begin(), mem[i + 1]);
+  }
 
   // joins: ops still counting two or more predecessors, in topological order
   // (concurrently pending joins get nearby indices), then the barriers
-  std::vector<int32_t> join(n + nb, -1);
+  std::vector<int32_t> join(n + nb, -1);  // kJoinNone for plain successors
   C.J = 0;
   C.jneed.clear();
   for (int32_t k = 0; k < n; ++k)
@@ -276,22 +286,29 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   C.ops.resize(n + nb + 1);
   C.succ.clear();
   int32_t e = 0;
+  // sibling entries: the first entry of a barrier member that has a next one
+  std::vector<uint8_t> has_sib(n, 0);
+  for (int32_t b = 0; b < nb; ++b)
+    for (size_t i = 0; i + 1 < bmem[b].size(); ++i) has_sib[bmem[b][i]] = 1;
   for (int32_t c = 0; c < n + nb; ++c) {
-    const auto &lst = c < n ? es[c] : bmem[c - n];
+    std::vector<int32_t> lst = c < n ? es[c] : std::vector<int32_t>{bmem[c - n][0]};
+    std::vector<int32_t> jl(lst.size());
+    for (size_t k = 0; k < lst.size(); ++k) jl[k] = join[lst[k]];
+    if (c < n && has_sib[c]) jl[0] = kJoinSibling;
     OpRec r{c < n ? orig_of[c] : -1, c < n ? op_res[orig_of[c]] : -1, e, (int32_t)lst.size(),
             -1, -1, 0, 0};
     if (!lst.empty()) {
       r.w0 = lst[0];
-      r.j0 = join[lst[0]];
+      r.j0 = jl[0];
     }
     if (lst.size() > 1) {
       r.w1 = lst[1];
-      r.j1 = join[lst[1]];
+      r.j1 = jl[1];
     }
     C.ops[c] = r;
-    for (int32_t w : lst) {
-      C.succ.push_back(w);
-      C.succ.push_back(join[w]);
+    for (size_t k = 0; k < lst.size(); ++k) {
+      C.succ.push_back(lst[k]);
+      C.succ.push_back(jl[k]);
       ++e;
     }
   }

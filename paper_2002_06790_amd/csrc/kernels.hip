@@ -205,9 +205,11 @@ __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, Heap
 template <bool DEEP>
 __device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
   if (DEEP) {
+    // the empty asm pins the wait here: a plain use could be sunk into the
+    // branch that needs the minimum, leaving the loads pending on the others
     uint64_t v[16];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = A.v2[k];
+    for (int k = 0; k < 16; ++k) v[k] = A.v2[k] = settle(A.v2[k]);
     min16(v, A.m2, A.q2);
     A.last = settle(A.last);
   }
@@ -339,6 +341,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
   rf_set(r, fin);
   span = fin > span ? fin : span;
   heap_settle_ahead<DEEP>(A);
+  // the record too: a step that releases nothing leaves its second half
+  // unused, and a load still in flight at the end of a step makes the next
+  // step wait for every store of this one before it can issue its loads
+  const int4 r0s = settle(r0), r1s = settle(r1);
   const int qs = it & (kFinQ - 1);  // wave-uniform
 #pragma unroll
   for (int k = 0; k < kFinQ; ++k)
@@ -357,11 +363,11 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
       heap_push(heap, root, end, nk);
     }
   };
-  for (int e = 0; e < r0.w; ++e) {
-    const int2 sw = e == 0 ? make_int2(r1.x, r1.y)
-                           : e == 1 ? make_int2(r1.z, r1.w) : settle(succ[r0.z + e]);  // {successor, join or -1}
-    if (sw.y < 0) {
-      release(fin, sw.x);
+  for (int e = 0; e < r0s.w; ++e) {
+    const int2 sw = e == 0 ? make_int2(r1s.x, r1s.y)
+                           : e == 1 ? make_int2(r1s.z, r1s.w) : settle(succ[r0s.z + e]);  // {successor, join}
+    if (sw.y < 0) {  // a plain successor, or the next member of a barrier
+      release(sw.y == kJoinSibling ? ready : fin, sw.x);
       continue;
     }
     const int2 js = settle(jst[(size_t)sw.y * kWave]);
@@ -374,10 +380,8 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
     jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
     if (sw.x < n) {
       release(rdy, sw.x);
-    } else {  // a barrier: its members (one predecessor each) are ready now
-      const int4 b0 = settle(rec4[2 * sw.x]);
-      const int4 b1 = settle(rec4[2 * sw.x + 1]);
-      for (int k = 0; k < b0.w; ++k) release(rdy, k == 0 ? b1.x : settle(succ[b0.z + k].x));
+    } else {  // a barrier: its first member is ready now (the others follow it)
+      release(rdy, settle(rec4[2 * sw.x + 1]).x);
     }
   }
   if (hole) heap_pop_root<DEEP>(heap, root, end, A);
@@ -428,6 +432,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       for (int k = 0; k < kFinQ; ++k)
         if (k < cnt && store_fin) a.finish[(int64_t)rq[k] * a.ld_fin + s] = fq[k];
     };
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the steps start with nothing in flight
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
       if (__ballot(end > kLdsEnd))

@@ -16,7 +16,13 @@ constexpr int kWave = 64;  // CDNA wavefront width: one scenario per lane
 // is exactly the paper-order tie rule).  Ids n.. are barrier nodes: a set of
 // ops that share one predecessor set (two or more predecessors) waits on one
 // barrier instead of each counting the predecessors itself; a barrier has no
-// duration or resource and releases its members the moment it completes.
+// duration or resource.  When it completes it releases its first member
+// (lowest compact id); each member then releases the next one, at the same
+// ready time, through a sibling entry (join index kJoinSibling).
+
+// join index of a successor entry: a join counter, or one of these
+constexpr int32_t kJoinNone = -1;     // released at the op's finish time
+constexpr int32_t kJoinSibling = -2;  // next barrier member, released at the op's ready time
 struct OpRec {
   int32_t orig;   // caller's op id: row of dur / place / finish (-1: barrier)
   int32_t res;    // resource (op_res), -1 for a barrier
@@ -44,7 +50,7 @@ struct DevGraph {
   int32_t max_indeg;
   int32_t pad0;
   const OpRec *ops;       // [n + barriers + 1]
-  const int32_t *succ;    // pairs {successor id, its join index or -1}
+  const int32_t *succ;    // pairs {successor id, its join index, kJoinNone or kJoinSibling}
   const int32_t *jneed;   // [J] predecessors a join waits for
   const int32_t *src;     // [nsrc] compact ids of sources
   const CpRec *cp;        // [n + 1]

@@ -136,6 +136,49 @@ def test_wide_and_deep_shapes(mlsim):
     check_cp(mlsim, ptr, idx, np.zeros(n, np.int32), 1, W.random_durations(n, 65, 1, 1000, rng), (3,))
 
 
+def barrier_case(rng, n_src, groups, n_free, R, S, hi):
+    """Sources, then groups of ops that share one predecessor set of two or
+    more sources (each group waits on one barrier), then free ops with a
+    single predecessor; random priorities interleave the groups' members with
+    each other and with free ops, and small durations force equal times."""
+    preds = [[] for _ in range(n_src)]
+    for _ in range(groups):
+        ps = sorted(rng.choice(n_src, size=int(rng.integers(2, n_src + 1)), replace=False).tolist())
+        for _ in range(int(rng.integers(2, 7))):
+            preds.append(ps)
+    for _ in range(n_free):
+        preds.append([int(rng.integers(0, n_src))])
+    n = len(preds)
+    perm = rng.permutation(n)  # shuffle ids (sources stay sources)
+    inv = np.argsort(perm)
+    succ = [[] for _ in range(n)]
+    for v, ps in enumerate(preds):
+        for p in ps:
+            succ[perm[p]].append(int(perm[v]))
+    ptr = np.zeros(n + 1, np.int64)
+    ptr[1:] = np.cumsum([len(x) for x in succ])
+    idx = np.array([w for x in succ for w in x], np.int32)
+    res = rng.integers(0, R, n).astype(np.int32)
+    prio = rng.integers(0, 4, n).astype(np.int32)
+    dur = W.random_durations(n, S, 1, hi, rng)
+    return ptr, idx, res, prio, dur
+
+
+def test_barrier_members_interleaved(mlsim):
+    """Ops sharing a predecessor set leave the ready list in the same order as
+    in the oracle, also when their ready times tie with other ops."""
+    rng = np.random.default_rng(404)
+    for case in range(30):
+        ptr, idx, res, prio, dur = barrier_case(rng, int(rng.integers(2, 6)), int(rng.integers(1, 6)),
+                                                int(rng.integers(0, 12)), int(rng.integers(1, 4)),
+                                                int(rng.choice([64, 130])), int(rng.choice([1, 3, 50])))
+        print(f"barrier case {case} n={res.size}", flush=True)
+        g = mlsim.Graph(ptr, idx, res, int(res.max()) + 1, prio=prio)
+        assert g.info()["n_joins"] >= 1
+        g.close()
+        check_run(mlsim, ptr, idx, res, int(res.max()) + 1, dur, prio=prio)
+
+
 def test_single_op_and_empty(mlsim):
     check_run(mlsim, np.array([0, 0]), np.zeros(0, np.int32), np.array([0], np.int32), 1,
               np.array([[5, 1, 7]], np.int32))
