@@ -71,39 +71,42 @@ __device__ __forceinline__ int4 settle(int4 v) {
 //
 // Positions run breadth-first from kRoot = 15, which puts the 16 children of
 // position p at 16 (p - 14) ... 16 (p - 14) + 15: every child group is
-// aligned to 16 entries.  The root is kept in a register, its 16 children
-// (positions 16..31) in LDS, slot-major x lane, conflict-free; positions from
-// 32 on live in global scratch, lane-major, so one child group is one aligned
-// 128-byte line of one lane.  Every position at or beyond the end holds
-// kEmpty, which is larger than any key, so partial groups need no bounds
-// masks; the kernel restores kEmpty wherever the heap shrinks, leaving
-// scratch as it found it.
-constexpr int kRoot = 15, kL1 = 16, kLdsEnd = 32;
+// aligned to 16 entries.  The root is kept in a register.  Positions 16 ..
+// le - 1 (the root's 16 children and the first (le - 32) / 16 groups below
+// them, which breadth-first order fills first) live in LDS, slot-major x
+// lane, conflict-free; positions from le on live in global scratch,
+// lane-major, so one child group there is one aligned 128-byte line of one
+// lane.  Every position at or beyond the end holds kEmpty, which is larger
+// than any key, so partial groups need no bounds masks; the kernel restores
+// kEmpty wherever the heap shrinks, leaving scratch as it found it.
+constexpr int kRoot = 15, kL1 = 16, kL2 = 32;
 constexpr uint64_t kEmpty = ~0ull;
 
 __device__ __forceinline__ int heap_parent(int p) { return (p >> 4) + 14; }
 __device__ __forceinline__ int heap_child0(int p) { return (p - 14) << 4; }
 
 struct WideHeap {
-  lptr<uint64_t> l;  // this lane's LDS column: position p (16..31) at l[(p - kL1) * kWave]
-  uint64_t *g;       // this lane's global run: position p (>= 32) at g[p - kLdsEnd]
+  lptr<uint64_t> l;  // this lane's LDS column: position p (16 .. le-1) at l[(p - kL1) * kWave]
+  uint64_t *g;       // this lane's global run: position p (>= le) at g[p - le]
+  int le;            // first position in global memory (32 + 16 k)
   __device__ __forceinline__ uint64_t get(int p) const {
-    if (p < kLdsEnd) return l[(p - kL1) * kWave];
-    return settle(g[p - kLdsEnd]);
+    if (p < le) return l[(p - kL1) * kWave];
+    return settle(g[p - le]);
   }
   __device__ __forceinline__ void set(int p, uint64_t x) const {
-    if (p < kLdsEnd)
+    if (p < le)
       l[(p - kL1) * kWave] = x;
     else
-      g[p - kLdsEnd] = x;
+      g[p - le] = x;
   }
-  __device__ __forceinline__ void lds_group(uint64_t (&v)[16]) const {
+  // the group starting at c (a multiple of 16) when it lies in LDS
+  __device__ __forceinline__ void lds_group(int c, uint64_t (&v)[16]) const {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = l[k * kWave];
+    for (int k = 0; k < 16; ++k) v[k] = l[(c + k - kL1) * kWave];
   }
-  // the group starting at c >= kLdsEnd: one aligned 128-byte line
+  // the group starting at c >= le: one aligned 128-byte line
   __device__ __forceinline__ void global_group(int c, uint64_t (&v)[16]) const {
-    const uint4 *gp = (const uint4 *)(g + (c - kLdsEnd));
+    const uint4 *gp = (const uint4 *)(g + (c - le));
     uint4 w[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) w[k] = gp[k];
@@ -132,8 +135,9 @@ __device__ __forceinline__ void min16(uint64_t (&v)[16], uint64_t &m, int &q) {
   q = ix[0];
 }
 
-// Place x at position p (>= 32) of a heap ending at `end` and restore heap
-// order below it (one global round trip per level).
+// Place x at position p (a grandchild of the root or deeper) of a heap
+// ending at `end` and restore heap order below it; every group below a
+// grandchild of the root lies in global memory (one round trip per level).
 __device__ __forceinline__ void sift_down_deep(const WideHeap &h, int end, int p, uint64_t x) {
   for (;;) {
     const int c = heap_child0(p);
@@ -166,10 +170,10 @@ __device__ __forceinline__ void heap_push(const WideHeap &h, uint64_t &root, int
 }
 
 // What one replay step reads of its heap before it knows the new key: the
-// smallest child of the root (LDS) and, for heaps beyond LDS, that child's
-// own child group and the last element (global).  These loads go out with
-// the step's duration and record loads, so a sift-down costs no round trip
-// of its own unless it goes deeper than position 272.
+// smallest child of the root, that child's own child group and, when it sits
+// in global memory, the last element.  The global loads go out with the
+// step's duration and record loads, so a sift-down costs no round trip of
+// its own unless it goes deeper than the root's grandchildren.
 struct HeapAhead {
   uint64_t m1;      // smallest child of the root (kEmpty if none)
   int q1;           // its position
@@ -186,17 +190,19 @@ __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, Heap
   A.q1 = kL1;
   if (end > kL1) {
     uint64_t v[16];
-    h.lds_group(v);
+    h.lds_group(kL1, v);
     min16(v, A.m1, A.q1);
     A.q1 += kL1;
   }
   A.c2 = heap_child0(A.q1);
+#pragma unroll
+  for (int k = 0; k < 16; ++k) A.v2[k] = kEmpty;
+  A.last = kEmpty;
   if (DEEP) {
-    // loads stay inside this lane's run: groups and positions past the end
-    // are replaced by position 32, which every run holds
-    h.global_group(A.c2 < end ? A.c2 : kLdsEnd, A.v2);
-    A.last = h.g[(end - 1 >= kLdsEnd ? end - 1 : kLdsEnd) - kLdsEnd];
+    if (A.c2 < end && A.c2 >= h.le) h.global_group(A.c2, A.v2);
+    if (end - 1 >= h.le) A.last = h.g[end - 1 - h.le];
   }
+  if (A.c2 < end && A.c2 < h.le) h.lds_group(A.c2, A.v2);
 }
 
 // Use the look-ahead loads on every path (their minimum is needed on most),
@@ -204,32 +210,25 @@ __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, Heap
 // next step would also wait for this step's stores.
 template <bool DEEP>
 __device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
-  if (DEEP) {
-    // the empty asm pins the wait here: a plain use could be sunk into the
-    // branch that needs the minimum, leaving the loads pending on the others
-    uint64_t v[16];
+  // the empty asm pins the wait here: a plain use could be sunk into the
+  // branch that needs the minimum, leaving the loads pending on the others
+  uint64_t v[16];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = A.v2[k] = settle(A.v2[k]);
-    min16(v, A.m2, A.q2);
-    A.last = settle(A.last);
-  }
+  for (int k = 0; k < 16; ++k) v[k] = A.v2[k] = DEEP ? settle(A.v2[k]) : A.v2[k];
+  min16(v, A.m2, A.q2);
+  if (DEEP) A.last = settle(A.last);
 }
 
 // Replace the root by x (the first op a step releases), using the look-ahead.
-template <bool DEEP>
 __device__ __forceinline__ void heap_replace_root(const WideHeap &h, uint64_t &root, int end,
-                                                  HeapAhead &A, uint64_t x) {
+                                                  const HeapAhead &A, uint64_t x) {
   if (x < A.m1) {  // also when the root has no children (m1 = kEmpty)
     root = x;
     return;
   }
   root = A.m1;
   const int p = A.q1;
-  if (!DEEP || A.c2 >= end) {
-    h.l[(p - kL1) * kWave] = x;
-    return;
-  }
-  if (x < A.m2) {
+  if (A.c2 >= end || x < A.m2) {
     h.l[(p - kL1) * kWave] = x;
     return;
   }
@@ -238,37 +237,33 @@ __device__ __forceinline__ void heap_replace_root(const WideHeap &h, uint64_t &r
 }
 
 // Remove the root when the step released nothing, using the look-ahead.
-template <bool DEEP>
 __device__ __forceinline__ void heap_pop_root(const WideHeap &h, uint64_t &root, int &end, HeapAhead &A) {
   const int lp = --end;  // position of the last element
   if (lp == kRoot) {
     root = kEmpty;
     return;
   }
-  if (lp < kLdsEnd) {  // the heap fits in LDS: take the last child, rescan
-    const uint64_t x = h.l[(lp - kL1) * kWave];
+  uint64_t x;
+  if (lp < h.le) {
+    x = h.l[(lp - kL1) * kWave];
     h.l[(lp - kL1) * kWave] = kEmpty;
-    uint64_t v[16], m1;
-    int q1;
-    h.lds_group(v);
-    min16(v, m1, q1);
-    if (x < m1) {
-      root = x;
-    } else {
-      root = m1;
-      h.l[q1 * kWave] = x;
-    }
-    return;
+  } else {
+    x = A.last;
+    h.g[lp - h.le] = kEmpty;
   }
-  const uint64_t x = A.last;
-  h.g[lp - kLdsEnd] = kEmpty;
-  if (DEEP && lp == A.c2 + A.q2) {  // the group's minimum left it: find the next one
+  if (lp < kL2) {  // a child of the root left: rescan them (no grandchildren remain)
+    uint64_t v[16];
+    h.lds_group(kL1, v);
+    min16(v, A.m1, A.q1);
+    A.q1 += kL1;
+    A.c2 = heap_child0(A.q1);
+  } else if (lp == A.c2 + A.q2) {  // the look-ahead group's minimum left it: find the next one
 #pragma unroll
     for (int k = 0; k < 16; ++k)  // unrolled: no indexed register access
       if (k == A.q2) A.v2[k] = kEmpty;
     min16(A.v2, A.m2, A.q2);
   }
-  heap_replace_root<DEEP>(h, root, end, A, x);
+  heap_replace_root(h, root, end, A, x);
 }
 
 struct EvArgs {
@@ -281,13 +276,13 @@ struct EvArgs {
   int32_t *finish;
   int64_t ld_fin;
   int32_t *status;
-  uint64_t *heap_g;   // [blocks][64][heap_stride]: heap positions from kLdsEnd on, lane-major
+  uint64_t *heap_g;   // [blocks][64][heap_stride]: heap positions from heap_le on, lane-major
   int heap_stride;    // entries per lane (a multiple of 16)
+  int heap_le;        // first heap position in global memory (32 + 16 k)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
 };
 
-constexpr int kHeapLds = kLdsEnd - kL1;  // heap positions per lane kept in LDS
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
 
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
@@ -357,7 +352,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
   auto release = [&](uint32_t t, int w) {
     const uint64_t nk = make_key(t, w);
     if (hole) {
-      heap_replace_root<DEEP>(heap, root, end, A, nk);
+      heap_replace_root(heap, root, end, A, nk);
       hole = false;
     } else {
       heap_push(heap, root, end, nk);
@@ -384,7 +379,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
       release(rdy, settle(rec4[2 * sw.x + 1]).x);
     }
   }
-  if (hole) heap_pop_root<DEEP>(heap, root, end, A);
+  if (hole) heap_pop_root(heap, root, end, A);
 }
 
 // Event-driven list scheduling, one scenario per lane (the paper's replay
@@ -403,9 +398,10 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
   const WideHeap heap{as_lds(lds) + lane,
-                      a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride};
+                      a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride, a.heap_le};
+  const int heap_lds = a.heap_le - kL1;  // heap positions per lane kept in LDS
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
-  lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)kHeapLds * kWave)) + lane;
+  lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)heap_lds * kWave)) + lane;
   int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
   auto rf_get = [&](int r) -> uint32_t { return RF_LDS ? rfree_l[r * kWave] : rfree_g[r * kWave]; };
   auto rf_set = [&](int r, uint32_t v) {
@@ -421,7 +417,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     const int64_t sc = active ? s : a.n_scen - 1;  // inactive lanes replay a valid column
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
-    for (int k = 0; k < kHeapLds; ++k) heap.l[k * kWave] = kEmpty;
+    for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
     uint64_t root = kEmpty;
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, root, end, make_key(0, G.src[k]));
@@ -435,7 +431,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the steps start with nothing in flight
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
-      if (__ballot(end > kLdsEnd))
+      if (__ballot(end > heap.le))
         event_step<true, RF_LDS, ROW_ID, PLACE>(G, a, heap, root, end, jst, it, s, sc, st, span, fq, rq,
                                          rf_get, rf_set, flush);
       else
@@ -691,7 +687,14 @@ int plan_scratch(sim_graph *g) {
   const size_t rf_bytes = (size_t)G.R * kWave * 4;
   const bool rf_lds = rf_in_lds(G);
   P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 16 + 15) & ~size_t(15));
-  P.ev_lds_bytes = (size_t)kHeapLds * kWave * 8 + (rf_lds ? rf_bytes : 0);
+  // groups of the root's grandchildren kept in LDS: two (heaps of up to 49
+  // entries never touch global memory) unless the resource times leave no
+  // room for four waves per CU
+  int lds_groups = rf_lds && rf_bytes > 16 * 1024 ? 0 : 2;
+  if (const char *e = getenv("MLSIM_EV_LDS_GROUPS"))  // tuning override
+    lds_groups = std::min(16, std::max(0, atoi(e)));
+  P.ev_heap_le = kL2 + 16 * lds_groups;
+  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + (rf_lds ? rf_bytes : 0);
   const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false>, P.ev_lds_bytes, cus)
                             : occupancy_blocks(k_event<false, false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
@@ -760,10 +763,10 @@ int plan_scratch(sim_graph *g) {
   if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
   if (getenv("MLSIM_VERBOSE"))
     fprintf(stderr,
-            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d) cp_slots=%d (lds %d) "
+            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (lds %d) "
             "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
             "scratch=%zu MB\n",
-            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, G.cp_slots, P.cp_lds,
+            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, P.ev_heap_le, G.cp_slots, P.cp_lds,
             P.ev_blocks, P.cp_blocks, P.sw_blocks,
             P.ev_lds_bytes, off >> 20);
   return SIM_OK;
@@ -775,7 +778,7 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
-           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride,
+           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);

@@ -63,6 +63,7 @@ struct DevGraph {
 struct ScratchPlan {
   int32_t ev_blocks;    // persistent grid of the event kernel
   int32_t ev_heap_stride;  // global heap entries per lane (lane-major, multiple of 16)
+  int32_t ev_heap_le;      // first heap position kept in global memory
   int32_t cp_blocks;
   int32_t cp_lds;       // critical-path slots in LDS (1) or global (0)
   int32_t sw_blocks;

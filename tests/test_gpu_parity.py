@@ -179,6 +179,22 @@ def test_barrier_members_interleaved(mlsim):
         check_run(mlsim, ptr, idx, res, int(res.max()) + 1, dur, prio=prio)
 
 
+@pytest.mark.parametrize("groups", ["0", "1", "4"])
+def test_heap_groups_in_lds(mlsim, groups, monkeypatch):
+    """The ready heap with some of its grandchild groups in LDS (a launch
+    parameter) gives the same results as the oracle."""
+    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    for k, S in ((4, 130), (5, 70), (2, 100)):
+        w = W.make_config(k, n_scen=S)
+        check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), place=w.placement())
+    rng = np.random.default_rng(77)
+    for case in range(10):  # wide graphs: heaps well beyond LDS
+        n, R = int(rng.integers(100, 600)), int(rng.integers(1, 5))
+        ptr, idx, res, pr, dur = rand_case(rng, n, R, 0.01, bool(rng.integers(2)), False, 65, 1,
+                                           int(rng.choice([3, 1000])))
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
+
+
 def test_single_op_and_empty(mlsim):
     check_run(mlsim, np.array([0, 0]), np.zeros(0, np.int32), np.array([0], np.int32), 1,
               np.array([[5, 1, 7]], np.int32))
