@@ -65,30 +65,31 @@ __device__ __forceinline__ int4 settle(int4 v) {
   return v;
 }
 
-// Per-lane ready list: a 16-ary min-heap of 64-bit keys (ready << 32 |
+// Per-lane ready list: an 8-ary min-heap of 64-bit keys (ready << 32 |
 // compact id).  Compact ids follow (priority, id), so key order is the queue
 // order of a first-in-first-out resource with the tie rules.
 //
-// Positions run breadth-first from kRoot = 15, which puts the 16 children of
-// position p at 16 (p - 14) ... 16 (p - 14) + 15: every child group is
-// aligned to 16 entries.  The root is kept in a register.  Positions 16 ..
-// le - 1 (the root's 16 children and the first (le - 32) / 16 groups below
-// them, which breadth-first order fills first) live in LDS, slot-major x
-// lane, conflict-free; positions from le on live in global scratch,
-// lane-major, so one child group there is one aligned 128-byte line of one
-// lane.  Every position at or beyond the end holds kEmpty, which is larger
-// than any key, so partial groups need no bounds masks; the kernel restores
-// kEmpty wherever the heap shrinks, leaving scratch as it found it.
-constexpr int kRoot = 15, kL1 = 16, kL2 = 32;
+// Positions run breadth-first from kRoot = 7, which puts the 8 children of
+// position p at 8 (p - 6) ... 8 (p - 6) + 7: every child group is aligned to
+// 8 entries.  The root is kept in a register; positions 8 .. le - 1 (the
+// root's 8 children and the first (le - 16) / 8 groups below them, which
+// breadth-first order fills first) live in LDS, slot-major x lane,
+// conflict-free; positions from le on live in global scratch, lane-major, so
+// one child group there is one aligned 64-byte segment of one lane.  Every
+// position at or beyond the end holds kEmpty, which is larger than any key,
+// so partial groups need no bounds masks; the kernel restores kEmpty
+// wherever the heap shrinks, leaving scratch as it found it.
+constexpr int kD = 8, kRoot = kD - 1, kL1 = kD, kL2 = 2 * kD;
 constexpr uint64_t kEmpty = ~0ull;
 
-__device__ __forceinline__ int heap_parent(int p) { return (p >> 4) + 14; }
-__device__ __forceinline__ int heap_child0(int p) { return (p - 14) << 4; }
+__device__ __forceinline__ int heap_parent(int p) { return p / kD + (kRoot - 1); }
+__device__ __forceinline__ int heap_child0(int p) { return kD * (p - (kRoot - 1)); }
 
 struct WideHeap {
-  lptr<uint64_t> l;  // this lane's LDS column: position p (16 .. le-1) at l[(p - kL1) * kWave]
+  uint64_t root;     // position kRoot
+  lptr<uint64_t> l;  // this lane's LDS column: position p (kL1 .. le-1) at l[(p - kL1) * kWave]
   uint64_t *g;       // this lane's global run: position p (>= le) at g[p - le]
-  int le;            // first position in global memory (32 + 16 k)
+  int le;            // first position in global memory (kL2 + kD k)
   __device__ __forceinline__ uint64_t get(int p) const {
     if (p < le) return l[(p - kL1) * kWave];
     return settle(g[p - le]);
@@ -99,34 +100,34 @@ struct WideHeap {
     else
       g[p - le] = x;
   }
-  // the group starting at c (a multiple of 16) when it lies in LDS
-  __device__ __forceinline__ void lds_group(int c, uint64_t (&v)[16]) const {
+  // the group starting at c (< le, a multiple of kD) in LDS
+  __device__ __forceinline__ void lds_group(int c, uint64_t (&v)[kD]) const {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = l[(c + k - kL1) * kWave];
+    for (int k = 0; k < kD; ++k) v[k] = l[(c + k - kL1) * kWave];
   }
-  // the group starting at c >= le: one aligned 128-byte line
-  __device__ __forceinline__ void global_group(int c, uint64_t (&v)[16]) const {
+  // the group starting at c >= le: one aligned 64-byte segment
+  __device__ __forceinline__ void global_group(int c, uint64_t (&v)[kD]) const {
     const uint4 *gp = (const uint4 *)(g + (c - le));
-    uint4 w[8];
+    uint4 w[kD / 2];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) w[k] = gp[k];
+    for (int k = 0; k < kD / 2; ++k) w[k] = gp[k];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kD / 2; ++k) {
       v[2 * k] = ((uint64_t)w[k].y << 32) | w[k].x;
       v[2 * k + 1] = ((uint64_t)w[k].w << 32) | w[k].z;
     }
   }
 };
 
-// Minimum of 16 keys and its index, as a balanced tree (short dependency chain).
-__device__ __forceinline__ void min16(uint64_t (&v)[16], uint64_t &m, int &q) {
-  int ix[16];
+// Minimum of kD keys and its index, as a balanced tree (short dependency chain).
+__device__ __forceinline__ void min_group(uint64_t (&v)[kD], uint64_t &m, int &q) {
+  int ix[kD];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) ix[k] = k;
+  for (int k = 0; k < kD; ++k) ix[k] = k;
 #pragma unroll
-  for (int st = 1; st < 16; st <<= 1)
+  for (int st = 1; st < kD; st <<= 1)
 #pragma unroll
-    for (int k = 0; k < 16; k += 2 * st)
+    for (int k = 0; k < kD; k += 2 * st)
       if (v[k + st] < v[k]) {
         v[k] = v[k + st];
         ix[k] = ix[k + st];
@@ -142,10 +143,10 @@ __device__ __forceinline__ void sift_down_deep(const WideHeap &h, int end, int p
   for (;;) {
     const int c = heap_child0(p);
     if (c >= end) break;
-    uint64_t v[16], m;
+    uint64_t v[kD], m;
     int q;
     h.global_group(c, v);
-    min16(v, m, q);
+    min_group(v, m, q);
     if (x < m) break;  // keys are distinct; kEmpty is above every key
     h.set(p, m);
     p = c + q;
@@ -154,17 +155,17 @@ __device__ __forceinline__ void sift_down_deep(const WideHeap &h, int end, int p
 }
 
 // Append x and restore heap order above it.
-__device__ __forceinline__ void heap_push(const WideHeap &h, uint64_t &root, int &end, uint64_t x) {
+__device__ __forceinline__ void heap_push(WideHeap &h, int &end, uint64_t x) {
   int p = end++;
   while (p > kRoot) {
     const int par = heap_parent(p);
-    const uint64_t a = par == kRoot ? root : h.get(par);
+    const uint64_t a = par == kRoot ? h.root : h.get(par);
     if (a < x) break;
     h.set(p, a);
     p = par;
   }
   if (p == kRoot)
-    root = x;
+    h.root = x;
   else
     h.set(p, x);
 }
@@ -178,7 +179,7 @@ struct HeapAhead {
   uint64_t m1;      // smallest child of the root (kEmpty if none)
   int q1;           // its position
   int c2;           // first child of q1 (>= end: none)
-  uint64_t v2[16];  // that group (valid if c2 < end)
+  uint64_t v2[kD];  // that group (valid if c2 < end)
   uint64_t m2;      // its minimum
   int q2;           // the minimum's index in the group
   uint64_t last;    // the last element when it sits in global memory
@@ -186,17 +187,11 @@ struct HeapAhead {
 
 template <bool DEEP>
 __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, HeapAhead &A) {
-  A.m1 = kEmpty;
-  A.q1 = kL1;
-  if (end > kL1) {
-    uint64_t v[16];
-    h.lds_group(kL1, v);
-    min16(v, A.m1, A.q1);
-    A.q1 += kL1;
-  }
+  uint64_t v[kD];
+  h.lds_group(kL1, v);  // all kEmpty when the root has no children
+  min_group(v, A.m1, A.q1);
+  A.q1 += kL1;
   A.c2 = heap_child0(A.q1);
-#pragma unroll
-  for (int k = 0; k < 16; ++k) A.v2[k] = kEmpty;
   A.last = kEmpty;
   if (DEEP) {
     if (A.c2 < end && A.c2 >= h.le) h.global_group(A.c2, A.v2);
@@ -207,26 +202,26 @@ __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, Heap
 
 // Use the look-ahead loads on every path (their minimum is needed on most),
 // so no load is still in flight when the step ends: a wait at the top of the
-// next step would also wait for this step's stores.
+// next step would also wait for this step's stores.  Lanes whose root child
+// has no children compute a minimum of stale values that nothing reads.
 template <bool DEEP>
 __device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
   // the empty asm pins the wait here: a plain use could be sunk into the
   // branch that needs the minimum, leaving the loads pending on the others
-  uint64_t v[16];
+  uint64_t v[kD];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = A.v2[k] = DEEP ? settle(A.v2[k]) : A.v2[k];
-  min16(v, A.m2, A.q2);
+  for (int k = 0; k < kD; ++k) v[k] = A.v2[k] = DEEP ? settle(A.v2[k]) : A.v2[k];
+  min_group(v, A.m2, A.q2);
   if (DEEP) A.last = settle(A.last);
 }
 
 // Replace the root by x (the first op a step releases), using the look-ahead.
-__device__ __forceinline__ void heap_replace_root(const WideHeap &h, uint64_t &root, int end,
-                                                  const HeapAhead &A, uint64_t x) {
+__device__ __forceinline__ void heap_replace_root(WideHeap &h, int end, const HeapAhead &A, uint64_t x) {
   if (x < A.m1) {  // also when the root has no children (m1 = kEmpty)
-    root = x;
+    h.root = x;
     return;
   }
-  root = A.m1;
+  h.root = A.m1;
   const int p = A.q1;
   if (A.c2 >= end || x < A.m2) {
     h.l[(p - kL1) * kWave] = x;
@@ -237,10 +232,10 @@ __device__ __forceinline__ void heap_replace_root(const WideHeap &h, uint64_t &r
 }
 
 // Remove the root when the step released nothing, using the look-ahead.
-__device__ __forceinline__ void heap_pop_root(const WideHeap &h, uint64_t &root, int &end, HeapAhead &A) {
+__device__ __forceinline__ void heap_pop_root(WideHeap &h, int &end, HeapAhead &A) {
   const int lp = --end;  // position of the last element
   if (lp == kRoot) {
-    root = kEmpty;
+    h.root = kEmpty;
     return;
   }
   uint64_t x;
@@ -252,18 +247,18 @@ __device__ __forceinline__ void heap_pop_root(const WideHeap &h, uint64_t &root,
     h.g[lp - h.le] = kEmpty;
   }
   if (lp < kL2) {  // a child of the root left: rescan them (no grandchildren remain)
-    uint64_t v[16];
+    uint64_t v[kD];
     h.lds_group(kL1, v);
-    min16(v, A.m1, A.q1);
+    min_group(v, A.m1, A.q1);
     A.q1 += kL1;
     A.c2 = heap_child0(A.q1);
   } else if (lp == A.c2 + A.q2) {  // the look-ahead group's minimum left it: find the next one
 #pragma unroll
-    for (int k = 0; k < 16; ++k)  // unrolled: no indexed register access
+    for (int k = 0; k < kD; ++k)  // unrolled: no indexed register access
       if (k == A.q2) A.v2[k] = kEmpty;
-    min16(A.v2, A.m2, A.q2);
+    min_group(A.v2, A.m2, A.q2);
   }
-  heap_replace_root(h, root, end, A, x);
+  heap_replace_root(h, end, A, x);
 }
 
 struct EvArgs {
@@ -288,15 +283,15 @@ constexpr int kFinQ = 8;                 // finish times buffered per lane befor
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
 template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, class RfGet, class RfSet, class Flush>
-__device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, const WideHeap &heap,
-                                           uint64_t &root, int &end, int2 *jst, int it, int64_t s,
+__device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
+                                           int &end, int2 *jst, int it, int64_t s,
                                            int64_t sc, uint32_t &st, uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
                                            RfGet rf_get, RfSet rf_set, Flush flush) {
   const int n = G.n, R = G.R;
   const int2 *succ = (const int2 *)G.succ;
   const int4 *rec4 = (const int4 *)G.ops;
-  const uint64_t key = root;
+  const uint64_t key = heap.root;
   const int c = (int)(uint32_t)key;
   const uint32_t ready = (uint32_t)(key >> 32);
   // every global load of the step is issued before the first is used
@@ -352,10 +347,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
   auto release = [&](uint32_t t, int w) {
     const uint64_t nk = make_key(t, w);
     if (hole) {
-      heap_replace_root(heap, root, end, A, nk);
+      heap_replace_root(heap, end, A, nk);
       hole = false;
     } else {
-      heap_push(heap, root, end, nk);
+      heap_push(heap, end, nk);
     }
   };
   for (int e = 0; e < r0s.w; ++e) {
@@ -379,7 +374,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, c
       release(rdy, settle(rec4[2 * sw.x + 1]).x);
     }
   }
-  if (hole) heap_pop_root(heap, root, end, A);
+  if (hole) heap_pop_root(heap, end, A);
 }
 
 // Event-driven list scheduling, one scenario per lane (the paper's replay
@@ -397,8 +392,10 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
-  const WideHeap heap{as_lds(lds) + lane,
-                      a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride, a.heap_le};
+  WideHeap heap;
+  heap.l = as_lds(lds) + lane;
+  heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
+  heap.le = a.heap_le;
   const int heap_lds = a.heap_le - kL1;  // heap positions per lane kept in LDS
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)heap_lds * kWave)) + lane;
@@ -418,9 +415,9 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
-    uint64_t root = kEmpty;
+    heap.root = kEmpty;
     int end = kRoot;  // one past the last heap position
-    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, root, end, make_key(0, G.src[k]));
+    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
     int32_t fq[kFinQ], rq[kFinQ];  // buffered finish times and their rows
     auto flush = [&](int cnt) {
@@ -432,10 +429,10 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
       if (__ballot(end > heap.le))
-        event_step<true, RF_LDS, ROW_ID, PLACE>(G, a, heap, root, end, jst, it, s, sc, st, span, fq, rq,
+        event_step<true, RF_LDS, ROW_ID, PLACE>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
                                          rf_get, rf_set, flush);
       else
-        event_step<false, RF_LDS, ROW_ID, PLACE>(G, a, heap, root, end, jst, it, s, sc, st, span, fq, rq,
+        event_step<false, RF_LDS, ROW_ID, PLACE>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
                                           rf_get, rf_set, flush);
     }
     flush(n & (kFinQ - 1));
@@ -686,15 +683,16 @@ int plan_scratch(sim_graph *g) {
   // bound on ready ops) in global scratch
   const size_t rf_bytes = (size_t)G.R * kWave * 4;
   const bool rf_lds = rf_in_lds(G);
-  P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 16 + 15) & ~size_t(15));
-  // groups of the root's grandchildren kept in LDS: two (heaps of up to 49
-  // entries never touch global memory) unless the resource times leave no
-  // room for four waves per CU
-  int lds_groups = rf_lds && rf_bytes > 16 * 1024 ? 0 : 2;
+  P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 2 * kD) & ~size_t(kD - 1));
+  // groups of the root's grandchildren kept in LDS (4 KB per wave each):
+  // four beside a small resource-time table, two beside a large one (heaps
+  // of up to 41 or 25 entries then never touch global memory)
+  const size_t rf_lds_bytes = rf_lds ? rf_bytes : 0;
+  int lds_groups = rf_lds_bytes <= 8 * 1024 ? 4 : 2;
   if (const char *e = getenv("MLSIM_EV_LDS_GROUPS"))  // tuning override
-    lds_groups = std::min(16, std::max(0, atoi(e)));
-  P.ev_heap_le = kL2 + 16 * lds_groups;
-  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + (rf_lds ? rf_bytes : 0);
+    lds_groups = std::min(kD, std::max(0, atoi(e)));
+  P.ev_heap_le = kL2 + kD * lds_groups;
+  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes;
   const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false>, P.ev_lds_bytes, cus)
                             : occupancy_blocks(k_event<false, false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
@@ -783,7 +781,12 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
-  const dim3 grid((unsigned)std::min<int64_t>(tiles, P.ev_blocks));
+  // when the last round of tiles would fill less than half the grid, use
+  // fewer blocks that each take the same number of tiles (within one)
+  const int64_t rounds = (tiles + P.ev_blocks - 1) / P.ev_blocks;
+  const int64_t tail = tiles - (rounds - 1) * P.ev_blocks;
+  const dim3 grid((unsigned)(2 * tail >= P.ev_blocks ? std::min<int64_t>(tiles, P.ev_blocks)
+                                                     : (tiles + rounds - 1) / rounds));
   const size_t lds = P.ev_lds_bytes;
   const int variant = (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
   switch (variant) {
