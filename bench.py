@@ -37,7 +37,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5")
     ap.add_argument("--scenarios", type=int, default=None)
-    ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep"))
+    ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep", "walk"))
     ap.add_argument("--cpu-sample", type=int, default=262144,
                     help="scenarios of the same workload timed on the CPU oracle (0: skip)")
     ap.add_argument("--calib-mb", type=int, default=0,

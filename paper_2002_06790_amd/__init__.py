@@ -23,11 +23,11 @@ LIB_PATH = os.path.join(HERE, "libmlsim.so")
 
 SIM_OK, SIM_E_INVAL, SIM_E_RANGE, SIM_E_CYCLE, SIM_E_NOMEM, SIM_E_HIP, SIM_E_LIMIT = 0, -1, -2, -3, -4, -5, -6
 SIM_ST_BAD_DUR, SIM_ST_BAD_RES, SIM_ST_OVERFLOW = 1, 2, 4
-SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP = 0, 1, 2
-ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP}
+SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP, SIM_ALGO_WALK = 0, 1, 2, 3
+ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP, "walk": SIM_ALGO_WALK}
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
-           "sim_strerror", "sim_graph_info")
+           "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible")
 
 _lib = None
 
@@ -68,6 +68,8 @@ def _load():
     L.sim_strerror.restype = ctypes.c_char_p
     L.sim_graph_info.argtypes = [P, P, P, P, P, P]
     L.sim_graph_info.restype = ctypes.c_int
+    L.sim_graph_walk_eligible.argtypes = [P]
+    L.sim_graph_walk_eligible.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -144,6 +146,14 @@ class Graph:
         if rc:
             raise SimError(rc, "sim_graph_info")
         return dict(zip(("n_ops", "n_res", "n_edges", "n_joins", "n_levels"), [v.value for v in vals]))
+
+    def walk_eligible(self) -> bool:
+        """Whether the lockstep walk (algo "walk", and "auto" without
+        placement) runs this graph; otherwise those run the event kernel."""
+        rc = _load().sim_graph_walk_eligible(self._h)
+        if rc < 0:
+            raise SimError(rc, "sim_graph_walk_eligible")
+        return rc == 1
 
     def run(self, dur, place=None, want_finish: bool = False, algo: str = "auto",
             makespan=None, finish=None, status=None, stream=None):

@@ -19,7 +19,7 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
                              const uint16_t *place, int64_t ld_place, int32_t *makespan,
                              int32_t *finish, int64_t ld_fin, int32_t *status, uint32_t flags,
                              void *stream) {
-  if (!g || n_scen < 0 || (flags & ~3u) || (flags & 3u) == 3u) return SIM_E_INVAL;
+  if (!g || n_scen < 0 || (flags & ~3u)) return SIM_E_INVAL;
   if (n_scen == 0) return SIM_OK;
   if (!makespan) return SIM_E_INVAL;
   if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
@@ -35,6 +35,9 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
   const uint32_t algo = flags & 3u;
   if (algo == SIM_ALGO_SWEEP)
     return launch_sweep(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
+  // the lockstep walk needs one resource map for every scenario
+  if ((algo == SIM_ALGO_WALK || algo == SIM_ALGO_AUTO) && !place && walk_eligible(g))
+    return launch_walk(g, n_scen, dur, ld_dur, makespan, finish, ld_fin, status, st);
   return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
                       st);
 }

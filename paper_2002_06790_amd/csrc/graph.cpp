@@ -25,6 +25,7 @@ constexpr int32_t kReduceMaxOps = 32768;  // transitive reduction bitsets: n^2/8
 struct Compiled {
   std::vector<OpRec> ops;
   std::vector<int32_t> succ, jneed, src, cp_pred, pred_ptr, pred, topo;
+  std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
   int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0, barriers = 0;
   int64_t m = 0;
@@ -265,6 +266,41 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     for (size_t i = 0; i + 1 < mem.size(); ++i) es[mem[i]].insert(es[mem[i]].begin(), mem[i + 1]);
   }
 
+  // Walk graph (pull model): node ids are the compact ops 0..n-1 and the
+  // barriers n..n+nb-1.  A barrier's predecessors are its shared set; each
+  // member has the barrier as its only predecessor; every other op keeps its
+  // reduced predecessors.  Successor lists are the reverse.
+  {
+    const int32_t N = n + nb;
+    std::vector<int32_t> bar_of(n, -1);
+    for (int32_t b = 0; b < nb; ++b)
+      for (int32_t w : bmem[b]) bar_of[w] = n + b;
+    std::vector<std::vector<int32_t>> wpl(N);
+    for (int32_t c = 0; c < n; ++c) {
+      if (bar_of[c] >= 0)
+        wpl[c].push_back(bar_of[c]);
+      else
+        wpl[c] = cp[c];
+    }
+    for (auto &kv : groups)
+      if (kv.second.size() >= 2) wpl[bar_of[kv.second[0]]] = kv.first;
+    std::vector<std::vector<int32_t>> wsl(N);
+    for (int32_t x = 0; x < N; ++x)
+      for (int32_t p : wpl[x]) wsl[p].push_back(x);
+    C.wp_ptr.assign(N + 1, 0);
+    C.ws_ptr.assign(N + 1, 0);
+    C.wp.clear();
+    C.ws.clear();
+    for (int32_t x = 0; x < N; ++x) {
+      C.wp_ptr[x] = (int32_t)C.wp.size();
+      C.wp.insert(C.wp.end(), wpl[x].begin(), wpl[x].end());
+      C.ws_ptr[x] = (int32_t)C.ws.size();
+      C.ws.insert(C.ws.end(), wsl[x].begin(), wsl[x].end());
+    }
+    C.wp_ptr[N] = (int32_t)C.wp.size();
+    C.ws_ptr[N] = (int32_t)C.ws.size();
+  }
+
   // joins: ops still counting two or more predecessors, in topological order
   // (concurrently pending joins get nearby indices), then the barriers
   std::vector<int32_t> join(n + nb, -1);  // kJoinNone for plain successors
@@ -418,7 +454,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
          o_jneed = take(bytes_of(C.jneed)), o_src = take(bytes_of(C.src)),
          o_cp = take(bytes_of(C.cp)), o_cpp = take(bytes_of(C.cp_pred)),
          o_pp = take(bytes_of(C.pred_ptr)), o_pr = take(bytes_of(C.pred)),
-         o_topo = take(bytes_of(C.topo));
+         o_topo = take(bytes_of(C.topo)), o_wpp = take(bytes_of(C.wp_ptr)),
+         o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws));
   if (hipMalloc(&g->dev_mem, off ? off : 256) != hipSuccess) {
     delete g;
     return SIM_E_NOMEM;
@@ -431,7 +468,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
             put(o_jneed, C.jneed.data(), bytes_of(C.jneed)) && put(o_src, C.src.data(), bytes_of(C.src)) &&
             put(o_cp, C.cp.data(), bytes_of(C.cp)) && put(o_cpp, C.cp_pred.data(), bytes_of(C.cp_pred)) &&
             put(o_pp, C.pred_ptr.data(), bytes_of(C.pred_ptr)) && put(o_pr, C.pred.data(), bytes_of(C.pred)) &&
-            put(o_topo, C.topo.data(), bytes_of(C.topo));
+            put(o_topo, C.topo.data(), bytes_of(C.topo)) &&
+            put(o_wpp, C.wp_ptr.data(), bytes_of(C.wp_ptr)) && put(o_wp, C.wp.data(), bytes_of(C.wp)) &&
+            put(o_wsp, C.ws_ptr.data(), bytes_of(C.ws_ptr)) && put(o_ws, C.ws.data(), bytes_of(C.ws));
   if (!ok) {
     (void)hipFree(g->dev_mem);
     delete g;
@@ -454,6 +493,11 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.pred_ptr = (const int32_t *)(base + o_pp);
   d.pred = (const int32_t *)(base + o_pr);
   d.topo = (const int32_t *)(base + o_topo);
+  d.nb = C.barriers;
+  d.wp_ptr = (const int32_t *)(base + o_wpp);
+  d.wp = (const int32_t *)(base + o_wp);
+  d.ws_ptr = (const int32_t *)(base + o_wsp);
+  d.ws = (const int32_t *)(base + o_ws);
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;
@@ -489,6 +533,11 @@ extern "C" int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res
   if (n_joins) *n_joins = g->n_joins;
   if (n_levels) *n_levels = g->n_levels;
   return SIM_OK;
+}
+
+extern "C" int sim_graph_walk_eligible(const sim_graph *g) {
+  if (!g) return SIM_E_INVAL;
+  return walk_eligible(g) ? 1 : 0;
 }
 
 extern "C" const char *sim_strerror(int code) {

@@ -276,6 +276,7 @@ struct EvArgs {
   int heap_le;        // first heap position in global memory (32 + 16 k)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
+  int retry;          // replay only scenarios whose makespan holds kWalkRetry
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
@@ -410,8 +411,10 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
 
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
-    const bool active = s < a.n_scen;
-    const int64_t sc = active ? s : a.n_scen - 1;  // inactive lanes replay a valid column
+    const bool in_range = s < a.n_scen;
+    const bool active = in_range && (!a.retry || a.makespan[s] == kWalkRetry);
+    if (a.retry && !__ballot(active)) continue;  // nothing to replay in this tile
+    const int64_t sc = in_range ? s : a.n_scen - 1;  // inactive lanes replay a valid column
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
@@ -749,6 +752,11 @@ int plan_scratch(sim_graph *g) {
   g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_lds ? 0 : cp_bytes * P.cp_blocks);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
+  {
+    const int rc = plan_walk(g, cus);
+    if (rc) return rc;
+  }
+  g->scratch_wk_off = take(P.wk_ok ? ((size_t)P.wk_groups_max * (size_t)P.wk_group_words + kWave) * 4 : 0);
   g->scratch_bytes = off;
   if (hipMalloc(&g->scratch, off) != hipSuccess) {
     g->scratch = nullptr;
@@ -763,21 +771,24 @@ int plan_scratch(sim_graph *g) {
     fprintf(stderr,
             "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (lds %d) "
             "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
+            "walk=%d (groups %d, words %lld, rs_cap %d, slots %d, pilot_lds %zu, walk_lds %zu, blocks %d) "
             "scratch=%zu MB\n",
             G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, P.ev_heap_le, G.cp_slots, P.cp_lds,
             P.ev_blocks, P.cp_blocks, P.sw_blocks,
-            P.ev_lds_bytes, off >> 20);
+            P.ev_lds_bytes, P.wk_ok, P.wk_groups_max, (long long)P.wk_group_words, P.wk_rs_cap,
+            P.wk_slot_max, P.wk_pilot_lds, P.wk_walk_lds, P.wk_blocks, off >> 20);
   return SIM_OK;
 }
 
-int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
-                 int64_t ld_fin, int32_t *status, hipStream_t stream) {
+namespace {
+int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                      int64_t ld_fin, int32_t *status, int retry, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
-           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off)};
+           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
@@ -800,6 +811,21 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
     default: k_event<true, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   }
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+}  // namespace
+
+int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                 int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
+                           status, 0, stream);
+}
+
+int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                       int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                       hipStream_t stream) {
+  return launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
+                           1, stream);
 }
 
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

@@ -58,6 +58,55 @@ struct DevGraph {
   const int32_t *pred_ptr;// [n + 1] compact predecessor CSR (sweep variant)
   const int32_t *pred;    // compact predecessor ids
   const int32_t *topo;    // [n] a topological order (compact ids)
+  // walk graph over nodes 0..n+nb-1 (ops, then barriers): a barrier's
+  // predecessors are its shared set, a member's only predecessor is its
+  // barrier; successor lists are the reverse
+  int32_t nb, pad1;
+  const int32_t *wp_ptr;  // [n+nb+1]
+  const int32_t *wp;
+  const int32_t *ws_ptr;  // [n+nb+1]
+  const int32_t *ws;
+};
+
+// Lockstep walk (walk.hip).  Per group of tiles, k_pilot writes a header of
+// kHdrWords words, then kProgWords words per position and the slot lists.
+// A position record holds: the op's row; its resource and output slot; its
+// compact id and sink flag; its packed predecessor slots (or the offset of
+// its slot lists); the row kAhead positions ahead; and up to kInlineCand
+// pull-forward candidates with their offsets, compact ids, rows and packed
+// predecessor slots.
+constexpr int kHdrWords = 8, kProgWords = 16;
+constexpr int kInlineCand = 3;
+constexpr int kCand = 7;      // pull-forward candidates per position: next ops on the resource
+constexpr int kRing = 64;     // duration rows held in LDS (positions k .. k + kAhead)
+constexpr int kAhead = 60;    // rows requested this many positions ahead of the walk
+constexpr int kLat = 16;      // steps a row request has to arrive
+constexpr int kDefer = 16;    // per-lane deferred sinks
+constexpr int kSlotMax = 128; // value slots a walk program may use (packed as 8-bit indices)
+constexpr int kWalkMaxRes = 64;  // resource state lives in registers
+constexpr int32_t kWalkRetry = -2;  // makespan marker: replay this scenario with k_event
+struct WalkHdr {
+  int32_t valid;  // 1: program usable; 0: every tile of the group is replayed by k_event
+  int32_t slots;  // value slots used
+  int32_t pad[6];
+};
+struct WalkArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *makespan;
+  int32_t *finish;
+  int64_t ld_fin;
+  int32_t *status;
+  int32_t *groups;       // [n_groups][group_words]
+  int64_t group_words;
+  int32_t n_groups;
+  int32_t tiles_per_group;
+  int32_t rs_cap;        // pilot ready-list capacity (LDS)
+  int32_t slot_max;      // walk value slots (LDS)
+  int32_t pslot_cap;     // predecessor-slot words per group
+  int32_t pad;
+  int32_t *dummy;        // [64] target of finish stores that lanes skip
 };
 
 struct ScratchPlan {
@@ -70,6 +119,13 @@ struct ScratchPlan {
   int32_t sw_val_lds;   // sweep: per-op state in LDS (1) or global (0)
   int32_t sw_res_lds;   // sweep: per-resource state in LDS (1) or global (0)
   size_t ev_lds_bytes, cp_lds_bytes, sw_lds_bytes;
+  // lockstep walk: 0 when the graph does not fit its limits
+  int32_t wk_ok;
+  int32_t wk_groups_max;  // groups the scratch holds
+  int32_t wk_blocks;      // persistent grid of k_walk
+  int32_t wk_rs_cap, wk_slot_max, wk_pslot_cap;
+  int64_t wk_group_words;
+  size_t wk_pilot_lds, wk_walk_lds;
 };
 
 }  // namespace mlsim
@@ -85,7 +141,7 @@ struct sim_graph {
   void *dev_mem;          // one allocation holding every graph array
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
-  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off;
+  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off;
   // host copies for critical-path recovery
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred;
   size_t scratch_bytes;
@@ -99,8 +155,18 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
 int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream);
+int launch_walk(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                hipStream_t stream);
+// k_event over the scenarios a walk flagged (makespan == kWalkRetry)
+int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                       int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                       hipStream_t stream);
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);
 // sizing of persistent grids and LDS, decided once per graph
 int plan_scratch(sim_graph *g);
+// walk limits and sizes (walk.hip); fills the wk_* fields of g->plan except the offset
+int plan_walk(sim_graph *g, int cus);
+bool walk_eligible(const sim_graph *g);
 }  // namespace mlsim
