@@ -61,7 +61,7 @@ enum {
 
 /* sim_run_batch flags & 3: which exact algorithm computes the replay */
 enum {
-  SIM_ALGO_AUTO = 0,  /* library's choice: WALK when it applies, else EVENT */
+  SIM_ALGO_AUTO = 0,  /* library's choice (currently EVENT) */
   SIM_ALGO_EVENT = 1, /* event-driven list scheduling, one scenario per lane */
   SIM_ALGO_SWEEP = 2, /* level-synchronous conservative sweeps */
   SIM_ALGO_WALK = 3   /* lockstep walk along a pilot scenario's event order, each
@@ -157,7 +157,7 @@ int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *
 
 /* Whether SIM_ALGO_WALK runs this graph (for scenarios without placement):
  * 1 if it does, 0 if the graph exceeds the walk's limits (too many ops or
- * resources for its on-chip state), in which case WALK and AUTO run EVENT;
+ * resources for its on-chip state), in which case WALK runs EVENT;
  * SIM_E_INVAL for a NULL graph. */
 int sim_graph_walk_eligible(const sim_graph *g);
 

@@ -36,7 +36,7 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
   if (algo == SIM_ALGO_SWEEP)
     return launch_sweep(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
   // the lockstep walk needs one resource map for every scenario
-  if ((algo == SIM_ALGO_WALK || algo == SIM_ALGO_AUTO) && !place && walk_eligible(g))
+  if (algo == SIM_ALGO_WALK && !place && walk_eligible(g))
     return launch_walk(g, n_scen, dur, ld_dur, makespan, finish, ld_fin, status, st);
   return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
                       st);
