@@ -276,7 +276,11 @@ struct EvArgs {
   int heap_le;        // first heap position in global memory (32 + 16 k)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
-  int retry;          // replay only scenarios whose makespan holds kWalkRetry
+  int retry;          // 0: every scenario; 1: those whose makespan holds kWalkRetry, when
+                      // the retry list overflowed; 2: the scenarios on the retry list
+  const int32_t *list;        // retry list (scenario indices) and its length
+  const int32_t *list_count;
+  int32_t list_cap;
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
@@ -409,12 +413,20 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       rfree_g[r * kWave] = v;
   };
 
-  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
-    const int64_t s = tile * kWave + lane;
-    const bool in_range = s < a.n_scen;
-    const bool active = in_range && (!a.retry || a.makespan[s] == kWalkRetry);
-    if (a.retry && !__ballot(active)) continue;  // nothing to replay in this tile
-    const int64_t sc = in_range ? s : a.n_scen - 1;  // inactive lanes replay a valid column
+  int64_t items = a.n_scen;
+  if (a.retry) {
+    const int32_t cnt = *(const volatile int32_t *)a.list_count;
+    if (a.retry == 2) items = cnt < a.list_cap ? cnt : a.list_cap;
+    if (a.retry == 1 && cnt <= a.list_cap) return;  // every flagged scenario was on the list
+  }
+  for (int64_t tile = blockIdx.x; tile * kWave < items; tile += gridDim.x) {
+    const int64_t idx = tile * kWave + lane;
+    const bool in_range = idx < items;
+    // the scenario of this lane (inactive lanes replay a valid column)
+    const int64_t s = a.retry == 2 ? (int64_t)a.list[in_range ? idx : items - 1] : idx;
+    const bool active = in_range && (a.retry != 1 || a.makespan[s] == kWalkRetry);
+    if (a.retry == 1 && !__ballot(active)) continue;  // nothing to replay in this tile
+    const int64_t sc = in_range || a.retry == 2 ? s : a.n_scen - 1;
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
@@ -757,6 +769,7 @@ int plan_scratch(sim_graph *g) {
     if (rc) return rc;
   }
   g->scratch_wk_off = take(P.wk_ok ? ((size_t)P.wk_groups_max * (size_t)P.wk_group_words + kWave) * 4 : 0);
+  g->scratch_retry_off = take(P.wk_ok ? ((size_t)kRetryCap + 64) * 4 : 0);
   g->scratch_bytes = off;
   if (hipMalloc(&g->scratch, off) != hipSuccess) {
     g->scratch = nullptr;
@@ -783,12 +796,14 @@ int plan_scratch(sim_graph *g) {
 namespace {
 int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
-                      int64_t ld_fin, int32_t *status, int retry, hipStream_t stream) {
+                      int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
+                      const int32_t *list_count, int32_t list_cap, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
-           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry};
+           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
+           list, list_count, list_cap};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
@@ -818,14 +833,19 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream) {
   return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
-                           status, 0, stream);
+                           status, 0, nullptr, nullptr, 0, stream);
 }
 
 int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                        int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                       const int32_t *list, const int32_t *list_count, int32_t list_cap,
                        hipStream_t stream) {
+  // the listed scenarios, then (only if the list overflowed) every flagged one
+  int rc = launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
+                             2, list, list_count, list_cap, stream);
+  if (rc) return rc;
   return launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
-                           1, stream);
+                           1, list, list_count, list_cap, stream);
 }
 
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

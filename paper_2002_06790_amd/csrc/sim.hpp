@@ -83,8 +83,9 @@ constexpr int kAhead = 60;    // rows requested this many positions ahead of the
 constexpr int kLat = 16;      // steps a row request has to arrive
 constexpr int kDefer = 16;    // per-lane deferred sinks
 constexpr int kSlotMax = 128; // value slots a walk program may use (packed as 8-bit indices)
-constexpr int kWalkMaxRes = 64;  // resource state lives in registers
+constexpr int kWalkMaxRes = 48;  // resource state lives in registers (more would spill)
 constexpr int32_t kWalkRetry = -2;  // makespan marker: replay this scenario with k_event
+constexpr int32_t kRetryCap = 1 << 20;  // scenarios the retry list holds (then: marker scan)
 struct WalkHdr {
   int32_t valid;  // 1: program usable; 0: every tile of the group is replayed by k_event
   int32_t slots;  // value slots used
@@ -107,6 +108,8 @@ struct WalkArgs {
   int32_t pslot_cap;     // predecessor-slot words per group
   int32_t pad;
   int32_t *dummy;        // [64] target of finish stores that lanes skip
+  int32_t *retry_list;   // [kRetryCap] flagged scenarios
+  int32_t *retry_count;  // entries appended (may exceed kRetryCap)
 };
 
 struct ScratchPlan {
@@ -141,7 +144,7 @@ struct sim_graph {
   void *dev_mem;          // one allocation holding every graph array
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
-  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off;
+  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
   // host copies for critical-path recovery
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred;
   size_t scratch_bytes;
@@ -158,9 +161,11 @@ int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
 int launch_walk(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
                 hipStream_t stream);
-// k_event over the scenarios a walk flagged (makespan == kWalkRetry)
+// k_event over the scenarios a walk flagged: those on the retry list, then,
+// if the list overflowed, every scenario whose makespan holds kWalkRetry
 int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                        int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                       const int32_t *list, const int32_t *list_count, int32_t list_cap,
                        hipStream_t stream);
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);

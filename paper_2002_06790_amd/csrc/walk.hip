@@ -107,6 +107,7 @@ __global__ __launch_bounds__(kWave) void k_pilot(DevGraph G, WalkArgs a) {
   uint64_t *rs = (uint64_t *)(jst + J);        // [cap] ready list; phase B: slot expiry
   int32_t *bord = (int32_t *)(rs + a.rs_cap);  // [nb] barriers by evaluation position
 
+  if (blockIdx.x == 0 && lane == 0) *a.retry_count = 0;  // k_walk appends after this kernel
   for (int g = blockIdx.x; g < a.n_groups; g += gridDim.x) {
     int32_t *gb = a.groups + (size_t)g * a.group_words;
     WalkHdr *hdr = (WalkHdr *)gb;
@@ -448,6 +449,17 @@ __device__ __forceinline__ int32_t comp(int4 x) {
 
 constexpr int kNsBuf = 4;  // pulled-forward ops with successors awaiting their position
 
+// Append the flagged lanes' scenarios to the retry list (one atomic per wave).
+__device__ __forceinline__ void append_retry(const WalkArgs &a, bool flag, int64_t s) {
+  const uint64_t bm = __ballot(flag);
+  if (!bm) return;
+  int base = 0;
+  if (threadIdx.x == __builtin_ctzll(bm)) base = atomicAdd(a.retry_list + kRetryCap, __popcll(bm));
+  base = __builtin_amdgcn_readlane(base, __builtin_ctzll(bm));
+  const int off = __builtin_amdgcn_mbcnt_hi((uint32_t)(bm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bm, 0));
+  if (flag && base + off < kRetryCap) a.retry_list[base + off] = (int32_t)s;
+}
+
 // FIN: finish times are written; NR: registers for the per-resource state;
 // ROW_ID: every op's row equals its compact id.
 template <bool FIN, int NR, bool ROW_ID>
@@ -467,6 +479,7 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
     const int32_t *gb = a.groups + (size_t)g * a.group_words;
     if (!uni(*(const volatile int32_t *)gb)) {
       if (active) a.makespan[s] = kWalkRetry;
+      append_retry(a, active, s);
       continue;
     }
     const int4 *prog4 = (const int4 *)(gb + kHdrWords);
@@ -494,6 +507,9 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
                                        (__attribute__((address_space(3))) void *)(ring0 + (p & (kRing - 1)) * kWave),
                                        4, 0, 0);
     };
+    // ring loads of the previous tile (requested past its end, or cut short
+    // by an abort) land before this tile's requests reuse their slots
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     for (int p = 0; p < kAhead; ++p) ring_load(p, __builtin_amdgcn_readlane(a0.x, min(p, n - 1)));
 
     RegArr<NR> rf, lr;  // resource time; ready time of the last commit (-1: none)
@@ -671,7 +687,13 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
     };
 
     constexpr int kVm = FIN ? 2 * kLat : kLat;  // VMEM operations newer than the row needed now
+    bool aborted = false;
     for (int k = 0; k < n; ++k) {
+      if ((k & 255) == 255 &&
+          2 * __popcll(__ballot(active && fail)) > __popcll(__ballot(active))) {
+        aborted = true;  // most scenarios of this tile need the event replay anyway
+        break;
+      }
       if (k - B == 64) {
         B = k;
         a0 = b0;
@@ -741,7 +763,15 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
       bool busy = !done_v, deferred = false;
       const uint64_t kv = make_key(ready, (int)c);
       const int nc = (int)(cw & 0xFFu);
-      bool need = busy && ((dres >> r) & 1);
+      bool need = false;
+      if (__ballot(busy && ((dres >> r) & 1))) {
+        // a deferred sink on r goes first only if it became ready no later than v
+        uint32_t dm = ~0u;
+#pragma unroll
+        for (int e = 0; e < kDefer; ++e)
+          if ((int)(df_cr[e] >> 16) == r && df_ready[e] < dm) dm = df_ready[e];
+        need = busy && dm <= ready;
+      }
       uint32_t cready[KC], cc[KC];
       bool cvalid[KC], csink[KC];
       int cpos[KC], crow[KC];
@@ -806,8 +836,10 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
         }
       }
     }
+    if (aborted) fail = true;
     // deferred sinks left at the end: each resource in key order
     uint64_t rem = 0;
+    if (!aborted)
     for (int i = 0; i < NR; ++i) rem |= __ballot(((dres >> i) & 1) != 0) ? (1ull << i) : 0;
     {
       bool cvalid[KC];
@@ -835,6 +867,7 @@ __global__ __launch_bounds__(kWave) void k_walk(DevGraph G, WalkArgs a) {
       a.makespan[s] = fail ? kWalkRetry : (int32_t)span;
       if (!fail && a.status) a.status[s] = 0;
     }
+    append_retry(a, active && fail, s);
   }
 }
 
@@ -880,7 +913,7 @@ int plan_walk(sim_graph *g, int cus) {
   words = (words + 63) & ~int64_t(63);
   P.wk_group_words = words;
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_walk<true, 64, false>, kWave, P.wk_walk_lds) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_walk<true, 48, false>, kWave, P.wk_walk_lds) != hipSuccess)
     return SIM_E_HIP;
   if (per_cu < 1) return SIM_OK;
   P.wk_blocks = per_cu * cus;
@@ -908,11 +941,13 @@ int launch_walk(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t 
   WalkArgs a{n_scen, dur, ld_dur, makespan, finish, ld_fin, status,
              (int32_t *)((char *)g->scratch + g->scratch_wk_off), P.wk_group_words, (int32_t)n_groups,
              (int32_t)tpg, P.wk_rs_cap, P.wk_slot_max, P.wk_pslot_cap, 0,
-             (int32_t *)((char *)g->scratch + g->scratch_wk_off) + (size_t)P.wk_groups_max * P.wk_group_words};
+             (int32_t *)((char *)g->scratch + g->scratch_wk_off) + (size_t)P.wk_groups_max * P.wk_group_words,
+             (int32_t *)((char *)g->scratch + g->scratch_retry_off),
+             (int32_t *)((char *)g->scratch + g->scratch_retry_off) + kRetryCap};
   k_pilot<<<dim3((unsigned)n_groups), dim3(kWave), P.wk_pilot_lds, stream>>>(g->dg, a);
   if (hipGetLastError() != hipSuccess) return SIM_E_HIP;
   const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.wk_blocks);
-  const int nr = g->dg.R <= 32 ? 32 : g->dg.R <= 48 ? 48 : 64;
+  const int nr = g->dg.R <= 32 ? 32 : 48;
   const int variant = (finish ? 1 : 0) | (g->row_identity ? 2 : 0);
   const dim3 grid(blocks), blk(kWave);
   const size_t lds = P.wk_walk_lds;
@@ -925,16 +960,15 @@ int launch_walk(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t 
   }
   if (nr == 32) {
     WALK_CASE(32)
-  } else if (nr == 48) {
-    WALK_CASE(48)
   } else {
-    WALK_CASE(64)
+    WALK_CASE(48)
   }
 #undef WALK_CASE
   if (hipGetLastError() != hipSuccess) return SIM_E_HIP;
   // diagnostics: leave flagged scenarios at kWalkRetry to count them
   if (getenv("MLSIM_WALK_NO_RETRY")) return SIM_OK;
-  return launch_event_retry(g, n_scen, dur, ld_dur, makespan, finish, ld_fin, status, stream);
+  return launch_event_retry(g, n_scen, dur, ld_dur, makespan, finish, ld_fin, status, a.retry_list,
+                            a.retry_count, kRetryCap, stream);
 }
 
 }  // namespace mlsim
