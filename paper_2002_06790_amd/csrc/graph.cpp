@@ -366,15 +366,24 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   int32_t n2 = assign_cp_slots(n, cs, cp, o2, s2);
   const auto &order = n1 <= n2 ? o1 : o2;
   const auto &slot = n1 <= n2 ? s1 : s2;
-  C.cp_slots = std::min(n1, n2);
-  C.cp.resize(n + 1);
+  // two more slots: one that always holds 0 (unused inline predecessors
+  // read it) and one that ops without successors write (never read)
+  C.cp_slots = std::min(n1, n2) + 2;
+  const int32_t zslot = C.cp_slots - 2, sink = C.cp_slots - 1;
+  const int32_t cp_pad = (n + kCpBatch - 1) / kCpBatch * kCpBatch + kCpBatch * kCpAhead;
+  C.cp.assign(cp_pad, CpRec{n ? orig_of[0] : 0, sink, 0, 0, {zslot, zslot, zslot, zslot}});
   C.cp_pred.clear();
   for (int32_t k = 0; k < n; ++k) {
     int32_t v = order[k];
-    C.cp[k] = CpRec{orig_of[v], slot[v], (int32_t)C.cp_pred.size(), (int32_t)cp[v].size()};
-    for (int32_t p : cp[v]) C.cp_pred.push_back(slot[p]);
+    CpRec r{orig_of[v], slot[v] >= 0 ? slot[v] : sink, (int32_t)cp[v].size(), (int32_t)C.cp_pred.size(),
+            {zslot, zslot, zslot, zslot}};
+    if (cp[v].size() <= 4)
+      for (size_t e = 0; e < cp[v].size(); ++e) r.p[e] = slot[cp[v][e]];
+    else
+      for (int32_t p : cp[v]) C.cp_pred.push_back(slot[p]);
+    C.cp[k] = r;
   }
-  C.cp[n] = CpRec{-1, -1, (int32_t)C.cp_pred.size(), 0};
+  if (C.cp_pred.empty()) C.cp_pred.push_back(0);
   C.topo = order;
 
   // compact predecessor CSR (for the sweep variant) and level count

@@ -26,15 +26,6 @@ template <class T>
 __device__ __forceinline__ cptr<T> as_const(const T *p) {
   return (cptr<T>)p;
 }
-__device__ __forceinline__ CpRec load_rec(cptr<CpRec> p, int k) {
-  CpRec r;
-  r.orig = p[k].orig;
-  r.slot = p[k].slot;
-  r.pbeg = p[k].pbeg;
-  r.npred = p[k].npred;
-  return r;
-}
-
 __device__ __forceinline__ uint64_t make_key(uint32_t ready, int32_t c) {
   return ((uint64_t)ready << 32) | (uint32_t)c;
 }
@@ -469,19 +460,29 @@ struct CpArgs {
   uint32_t *slots_g;  // [blocks][cp_slots][64] when slots are not in LDS
 };
 
-constexpr int kCpBatch = 16;  // duration rows loaded ahead of use
-
 // Longest path per scenario: one sweep in a fixed topological order shared by
-// the whole wave (each step reads one coalesced duration row), with dist of
-// ops that still have unvisited successors kept in value slots.
+// the whole wave, in batches of kCpBatch ops.  Each op reads one coalesced
+// duration row; dist of ops that still have unvisited successors lives in
+// value slots.  Software pipeline: while batch t is swept, the duration rows
+// of batch t + 1 and the records of batch t + 2 are in flight.  A batch's
+// records arrive in registers (lane i holds words i and 64 + i), give the
+// row numbers of the batch by readlane and are copied to a two-batch LDS
+// ring, from which the sweep takes them back into registers.
 template <bool LDS>
 __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
   const int n = G.n;
-  const cptr<CpRec> cp = as_const(G.cp);
+  constexpr int kRecWords = (int)(sizeof(CpRec) / 4);  // 8
+  constexpr int kBatchWords = kCpBatch * kRecWords;    // 128: two words per lane
+  static_assert(kBatchWords == 2 * kWave, "a batch of records is two words per lane");
+  const int32_t *recw = (const int32_t *)G.cp;
   const cptr<int32_t> cp_pred = as_const(G.cp_pred);
-  uint32_t *slots = LDS ? lds32 + lane : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+  int32_t *ring = (int32_t *)lds32;  // [2][kBatchWords]
+  uint32_t *slots = LDS ? lds32 + 2 * kBatchWords + lane
+                        : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+  const int nbat = (n + kCpBatch - 1) / kCpBatch;
+  slots[(size_t)(G.cp_slots - 2) * kWave] = 0;  // the slot that holds 0
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
@@ -489,37 +490,81 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
     const bool want_dist = a.dist_out && s == a.dist_scen;
     uint32_t mx = 0;
     bool bad = false;
-    for (int k0 = 0; k0 < n; k0 += kCpBatch) {
-      // records of the whole batch first (scalar loads), then its duration rows
-      CpRec rec[kCpBatch];
-#pragma unroll
-      for (int u = 0; u < kCpBatch; ++u) rec[u] = load_rec(cp, k0 + u < n ? k0 + u : n - 1);
-      int32_t dv[kCpBatch];
-#pragma unroll
-      for (int u = 0; u < kCpBatch; ++u) dv[u] = a.dur[(int64_t)rec[u].orig * a.ld_dur + sc];
+    int32_t rx0, rx1;  // records of one batch in flight
+    auto load_recs = [&](int t) {
+      rx0 = recw[(size_t)t * kBatchWords + lane];
+      rx1 = recw[(size_t)t * kBatchWords + kWave + lane];
+    };
+    auto stage_recs = [&](int t) {
+      ring[(t & 1) * kBatchWords + lane] = rx0;
+      ring[(t & 1) * kBatchWords + kWave + lane] = rx1;
+    };
+    auto load_rows = [&](int32_t (&dv)[kCpBatch]) {
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
-        if (k0 + u < n) {
-          uint32_t best = 0;
-          for (int e = 0; e < rec[u].npred; ++e) {
-            const uint32_t x = slots[(size_t)cp_pred[rec[u].pbeg + e] * kWave];
+        const int w = u * kRecWords;  // word of the batch holding the row
+        const int row = __builtin_amdgcn_readlane(w < kWave ? rx0 : rx1, w & (kWave - 1));
+        dv[u] = a.dur[(int64_t)row * a.ld_dur + sc];
+      }
+    };
+    auto sweep = [&](int t, const int32_t (&dv)[kCpBatch]) {
+      // the batch's records back in registers (lane i: words i and 64 + i), fields by readlane
+      const int32_t y0 = ring[(t & 1) * kBatchWords + lane];
+      const int32_t y1 = ring[(t & 1) * kBatchWords + kWave + lane];
+#define CP_FIELD(u, f) __builtin_amdgcn_readlane(((u) * kRecWords + (f)) < kWave ? y0 : y1, ((u) * kRecWords + (f)) & (kWave - 1))
+#pragma unroll
+      for (int u = 0; u < kCpBatch; ++u) {
+        if (t * kCpBatch + u >= n) break;
+        const int np = CP_FIELD(u, 2);
+        uint32_t best;
+        if (np <= 4) {  // unused entries name the slot that holds 0
+          const uint32_t x0 = slots[(size_t)CP_FIELD(u, 4) * kWave];
+          const uint32_t x1 = slots[(size_t)CP_FIELD(u, 5) * kWave];
+          const uint32_t x2 = slots[(size_t)CP_FIELD(u, 6) * kWave];
+          const uint32_t x3 = slots[(size_t)CP_FIELD(u, 7) * kWave];
+          const uint32_t m01 = x0 > x1 ? x0 : x1, m23 = x2 > x3 ? x2 : x3;
+          best = m01 > m23 ? m01 : m23;
+        } else {
+          best = 0;
+          const int pb = CP_FIELD(u, 3);
+          for (int e = 0; e < np; ++e) {
+            const uint32_t x = slots[(size_t)cp_pred[pb + e] * kWave];
             best = x > best ? x : best;
           }
-          int32_t d = dv[u];
-          if (d < 1) {
-            bad = true;
-            d = 1;
-          }
-          uint32_t dist = best + (uint32_t)d;
-          if (dist > kI32Max) {
-            bad = true;
-            dist = kI32Max;
-          }
-          if (rec[u].slot >= 0) slots[(size_t)rec[u].slot * kWave] = dist;
-          mx = dist > mx ? dist : mx;
-          if (want_dist) a.dist_out[rec[u].orig] = (int32_t)dist;
         }
+        int32_t d = dv[u];
+        if (d < 1) {
+          bad = true;
+          d = 1;
+        }
+        uint32_t dist = best + (uint32_t)d;
+        if (dist > kI32Max) {
+          bad = true;
+          dist = kI32Max;
+        }
+        slots[(size_t)CP_FIELD(u, 1) * kWave] = dist;
+        mx = dist > mx ? dist : mx;
+        if (want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
       }
+#undef CP_FIELD
+    };
+    // one pipeline step: batch t + 1's records go to the ring and its rows
+    // out, batch t + 2's records out, then batch t is swept
+    auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&nxt)[kCpBatch]) {
+      stage_recs(t + 1);
+      load_rows(nxt);
+      load_recs(t + 2);
+      sweep(t, cur);
+    };
+    int32_t da[kCpBatch], db[kCpBatch];
+    load_recs(0);
+    stage_recs(0);
+    load_rows(da);
+    load_recs(1);
+    for (int t = 0; t < nbat; t += 2) {
+      step(t, da, db);
+      if (t + 1 >= nbat) break;
+      step(t + 1, db, da);
     }
     if (active) a.cp_len[s] = bad ? -1 : (int32_t)mx;
   }
@@ -723,8 +768,9 @@ int plan_scratch(sim_graph *g) {
 
   // critical path: slots in LDS when they fit
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
+  const size_t cp_ring = 2 * sizeof(CpRec) * kCpBatch;  // record ring
   P.cp_lds = cp_bytes <= 32 * 1024;
-  P.cp_lds_bytes = P.cp_lds ? std::max<size_t>(cp_bytes, 8) : 8;
+  P.cp_lds_bytes = cp_ring + (P.cp_lds ? cp_bytes : 0);
   const int cp_occ = P.cp_lds ? occupancy_blocks(k_cp<true>, P.cp_lds_bytes, cus)
                               : occupancy_blocks(k_cp<false>, P.cp_lds_bytes, cus);
   if (cp_occ < 0) return SIM_E_HIP;

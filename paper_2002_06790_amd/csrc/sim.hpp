@@ -34,26 +34,33 @@ struct OpRec {
   int32_t j1;
 };
 
-// Per position of the critical-path sweep order.
+// Per position of the critical-path sweep order (32 bytes).  The table is
+// padded with empty records (row 0, no slot, no predecessors) to whole
+// batches of kCpBatch plus kCpBatch * kCpAhead more, so a sweep can read
+// records and rows ahead without bounds checks.
+constexpr int kCpBatch = 16;  // ops per batch of the sweep
+constexpr int kCpAhead = 2;   // batches of records read ahead
 struct CpRec {
   int32_t orig;   // row of dur
-  int32_t slot;   // slot receiving dist(v), or -1 if v has no successors
-  int32_t pbeg;   // predecessor slots in cp_pred[pbeg, pbeg + npred)
+  int32_t slot;   // slot receiving dist(v) (ops without successors: slot cp_slots - 1)
   int32_t npred;
+  int32_t pbeg;   // predecessor slots in cp_pred[pbeg, pbeg + npred) when npred > 4
+  int32_t p[4];   // the predecessor slots themselves when npred <= 4, then slot
+                  // cp_slots - 2, which always holds 0
 };
 
 // Device view of a compiled graph (plain pointers, passed by value).
 struct DevGraph {
   int32_t n, R, J, nsrc;  // n real ops (barriers follow them), J joins
   int32_t heap_cap;       // bound on simultaneously ready ops (>= DAG width)
-  int32_t cp_slots;       // live values of the critical-path sweep
+  int32_t cp_slots;       // value slots of the critical-path sweep (live values + 2)
   int32_t max_indeg;
   int32_t pad0;
   const OpRec *ops;       // [n + barriers + 1]
   const int32_t *succ;    // pairs {successor id, its join index, kJoinNone or kJoinSibling}
   const int32_t *jneed;   // [J] predecessors a join waits for
   const int32_t *src;     // [nsrc] compact ids of sources
-  const CpRec *cp;        // [n + 1]
+  const CpRec *cp;        // [round_up(n, kCpBatch) + kCpBatch * kCpAhead]
   const int32_t *cp_pred; // predecessor slot lists of the critical-path sweep
   const int32_t *pred_ptr;// [n + 1] compact predecessor CSR (sweep variant)
   const int32_t *pred;    // compact predecessor ids
