@@ -9,7 +9,9 @@
 // tiles; every kernel leaves its scratch in the state it found it.
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 
+#include "regarr.hpp"
 #include "sim.hpp"
 
 namespace mlsim {
@@ -467,8 +469,9 @@ struct CpArgs {
 // of batch t + 1 and the records of batch t + 2 are in flight.  A batch's
 // records arrive in registers (lane i holds words i and 64 + i), give the
 // row numbers of the batch by readlane and are copied to a two-batch LDS
-// ring, from which the sweep takes them back into registers.
-template <bool LDS>
+// ring, from which the sweep takes them back into registers.  MODE: where
+// the value slots live (kCpSlotsLds or kCpSlotsGlobal).
+template <int MODE>
 __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
@@ -479,10 +482,12 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
   const int32_t *recw = (const int32_t *)G.cp;
   const cptr<int32_t> cp_pred = as_const(G.cp_pred);
   int32_t *ring = (int32_t *)lds32;  // [2][kBatchWords]
-  uint32_t *slots = LDS ? lds32 + 2 * kBatchWords + lane
-                        : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+  uint32_t *slots = MODE == kCpSlotsLds ? lds32 + 2 * kBatchWords + lane
+                                        : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+  auto sget = [&](int i) -> uint32_t { return slots[(size_t)i * kWave]; };
+  auto sset = [&](int i, uint32_t x) { slots[(size_t)i * kWave] = x; };
   const int nbat = (n + kCpBatch - 1) / kCpBatch;
-  slots[(size_t)(G.cp_slots - 2) * kWave] = 0;  // the slot that holds 0
+  sset(G.cp_slots - 2, 0u);  // the slot that holds 0 (every other slot is written before it is read)
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
@@ -518,17 +523,17 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
         const int np = CP_FIELD(u, 2);
         uint32_t best;
         if (np <= 4) {  // unused entries name the slot that holds 0
-          const uint32_t x0 = slots[(size_t)CP_FIELD(u, 4) * kWave];
-          const uint32_t x1 = slots[(size_t)CP_FIELD(u, 5) * kWave];
-          const uint32_t x2 = slots[(size_t)CP_FIELD(u, 6) * kWave];
-          const uint32_t x3 = slots[(size_t)CP_FIELD(u, 7) * kWave];
+          const uint32_t x0 = sget(CP_FIELD(u, 4));
+          const uint32_t x1 = sget(CP_FIELD(u, 5));
+          const uint32_t x2 = sget(CP_FIELD(u, 6));
+          const uint32_t x3 = sget(CP_FIELD(u, 7));
           const uint32_t m01 = x0 > x1 ? x0 : x1, m23 = x2 > x3 ? x2 : x3;
           best = m01 > m23 ? m01 : m23;
         } else {
           best = 0;
           const int pb = CP_FIELD(u, 3);
           for (int e = 0; e < np; ++e) {
-            const uint32_t x = slots[(size_t)cp_pred[pb + e] * kWave];
+            const uint32_t x = sget(cp_pred[pb + e]);
             best = x > best ? x : best;
           }
         }
@@ -542,7 +547,7 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
           bad = true;
           dist = kI32Max;
         }
-        slots[(size_t)CP_FIELD(u, 1) * kWave] = dist;
+        sset(CP_FIELD(u, 1), dist);
         mx = dist > mx ? dist : mx;
         if (want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
       }
@@ -766,16 +771,18 @@ int plan_scratch(sim_graph *g) {
 
   const int32_t ev_grid = P.ev_blocks;
 
-  // critical path: slots in LDS when they fit
+  // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
   const size_t cp_ring = 2 * sizeof(CpRec) * kCpBatch;  // record ring
-  P.cp_lds = cp_bytes <= 32 * 1024;
-  P.cp_lds_bytes = cp_ring + (P.cp_lds ? cp_bytes : 0);
-  const int cp_occ = P.cp_lds ? occupancy_blocks(k_cp<true>, P.cp_lds_bytes, cus)
-                              : occupancy_blocks(k_cp<false>, P.cp_lds_bytes, cus);
+  P.cp_mode = cp_bytes <= 32 * 1024 ? kCpSlotsLds : kCpSlotsGlobal;
+  if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
+    if (!strcmp(e, "global")) P.cp_mode = kCpSlotsGlobal;
+  P.cp_lds_bytes = cp_ring + (P.cp_mode == kCpSlotsLds ? cp_bytes : 0);
+  const int cp_occ = P.cp_mode == kCpSlotsLds ? occupancy_blocks(k_cp<kCpSlotsLds>, P.cp_lds_bytes, cus)
+                                              : occupancy_blocks(k_cp<kCpSlotsGlobal>, P.cp_lds_bytes, cus);
   if (cp_occ < 0) return SIM_E_HIP;
   size_t cp_blocks = (size_t)cp_occ;
-  if (!P.cp_lds && cp_bytes)
+  if (P.cp_mode == kCpSlotsGlobal && cp_bytes)
     cp_blocks = std::min(cp_blocks, std::max<size_t>(1, kScratchBudget / cp_bytes));
   P.cp_blocks = (int32_t)cp_blocks;
   // sweep variant: per-op state and per-resource state in LDS when small
@@ -808,7 +815,7 @@ int plan_scratch(sim_graph *g) {
   g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_sw_val_off = take(P.sw_val_lds ? 0 : val_bytes * P.sw_blocks);
   g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
-  g->scratch_cp_off = take(P.cp_lds ? 0 : cp_bytes * P.cp_blocks);
+  g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   {
     const int rc = plan_walk(g, cus);
@@ -828,11 +835,11 @@ int plan_scratch(sim_graph *g) {
   if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
   if (getenv("MLSIM_VERBOSE"))
     fprintf(stderr,
-            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (lds %d) "
+            "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (mode %d) "
             "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
             "walk=%d (groups %d, words %lld, rs_cap %d, slots %d, pilot_lds %zu, walk_lds %zu, blocks %d) "
             "scratch=%zu MB\n",
-            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, P.ev_heap_le, G.cp_slots, P.cp_lds,
+            G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, P.ev_heap_le, G.cp_slots, P.cp_mode,
             P.ev_blocks, P.cp_blocks, P.sw_blocks,
             P.ev_lds_bytes, P.wk_ok, P.wk_groups_max, (long long)P.wk_group_words, P.wk_rs_cap,
             P.wk_slot_max, P.wk_pilot_lds, P.wk_walk_lds, P.wk_blocks, off >> 20);
@@ -901,10 +908,11 @@ int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld
   CpArgs a{n_scen, dur, ld_dur, cp_len, dist_out, dist_scen, (uint32_t *)(base + g->scratch_cp_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.cp_blocks);
-  if (P.cp_lds)
-    k_cp<true><<<dim3(blocks), dim3(kWave), P.cp_lds_bytes, stream>>>(g->dg, a);
+  const dim3 grid(blocks), blk(kWave);
+  if (P.cp_mode == kCpSlotsLds)
+    k_cp<kCpSlotsLds><<<grid, blk, P.cp_lds_bytes, stream>>>(g->dg, a);
   else
-    k_cp<false><<<dim3(blocks), dim3(kWave), P.cp_lds_bytes, stream>>>(g->dg, a);
+    k_cp<kCpSlotsGlobal><<<grid, blk, P.cp_lds_bytes, stream>>>(g->dg, a);
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

@@ -40,6 +40,7 @@ struct OpRec {
 // records and rows ahead without bounds checks.
 constexpr int kCpBatch = 16;  // ops per batch of the sweep
 constexpr int kCpAhead = 2;   // batches of records read ahead
+constexpr int kCpSlotsGlobal = 0, kCpSlotsLds = 1;  // where the sweep's value slots live
 struct CpRec {
   int32_t orig;   // row of dur
   int32_t slot;   // slot receiving dist(v) (ops without successors: slot cp_slots - 1)
@@ -124,7 +125,7 @@ struct ScratchPlan {
   int32_t ev_heap_stride;  // global heap entries per lane (lane-major, multiple of 16)
   int32_t ev_heap_le;      // first heap position kept in global memory
   int32_t cp_blocks;
-  int32_t cp_lds;       // critical-path slots in LDS (1) or global (0)
+  int32_t cp_mode;      // critical-path slots: kCpSlotsLds or kCpSlotsGlobal
   int32_t sw_blocks;
   int32_t sw_val_lds;   // sweep: per-op state in LDS (1) or global (0)
   int32_t sw_res_lds;   // sweep: per-resource state in LDS (1) or global (0)

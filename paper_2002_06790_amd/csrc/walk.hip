@@ -24,6 +24,7 @@
 #include <cstdio>
 #include <cstdlib>
 
+#include "regarr.hpp"
 #include "sim.hpp"
 
 extern "C" __device__ uint32_t __ockl_wfred_min_u32(uint32_t);
@@ -397,51 +398,6 @@ __global__ __launch_bounds__(kWave) void k_pilot(DevGraph G, WalkArgs a) {
 // global-to-LDS loads; the program is read through register windows of 64
 // positions (one position per lane, read back with readlane).
 // ---------------------------------------------------------------------------
-typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
-typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
-
-// NR per-lane words indexed by a wave-uniform value (register indexing)
-template <int NR>
-struct RegArr;
-template <>
-struct RegArr<32> {
-  u32x32 lo;
-  __device__ __forceinline__ void fill(uint32_t x) { lo = x; }
-  __device__ __forceinline__ uint32_t get(int i) const { return lo[i]; }
-  __device__ __forceinline__ void set(int i, uint32_t x) { lo[i] = x; }
-};
-template <>
-struct RegArr<48> {
-  u32x32 lo;
-  u32x16 hi;
-  __device__ __forceinline__ void fill(uint32_t x) {
-    lo = x;
-    hi = x;
-  }
-  __device__ __forceinline__ uint32_t get(int i) const { return i < 32 ? lo[i] : hi[i - 32]; }
-  __device__ __forceinline__ void set(int i, uint32_t x) {
-    if (i < 32)
-      lo[i] = x;
-    else
-      hi[i - 32] = x;
-  }
-};
-template <>
-struct RegArr<64> {
-  u32x32 lo, hi;
-  __device__ __forceinline__ void fill(uint32_t x) {
-    lo = x;
-    hi = x;
-  }
-  __device__ __forceinline__ uint32_t get(int i) const { return i < 32 ? lo[i] : hi[i - 32]; }
-  __device__ __forceinline__ void set(int i, uint32_t x) {
-    if (i < 32)
-      lo[i] = x;
-    else
-      hi[i - 32] = x;
-  }
-};
-
 template <int C>
 __device__ __forceinline__ int32_t comp(int4 x) {
   return C == 0 ? x.x : C == 1 ? x.y : C == 2 ? x.z : x.w;

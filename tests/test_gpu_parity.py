@@ -195,6 +195,26 @@ def test_heap_groups_in_lds(mlsim, groups, monkeypatch):
         check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
 
 
+@pytest.mark.parametrize("slots", ["lds", "global"])
+def test_critical_path_slots(mlsim, slots, monkeypatch):
+    """The critical-path sweep with its value slots in LDS or in global
+    scratch, on workloads and on random graphs with sources, long predecessor
+    lists (more than four, read from the list) and ops without successors;
+    batch counts that leave partial batches."""
+    if slots == "global":
+        monkeypatch.setenv("MLSIM_CP_SLOTS", "global")
+    for k, S in ((4, 130), (2, 70), (3, 200)):
+        w = W.make_config(k, n_scen=S)
+        check_cp(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), paths=(0, S - 1))
+    rng = np.random.default_rng(4242)
+    for case in range(12):
+        n = int(rng.choice([1, 15, 16, 17, 33, 250]))
+        ptr, idx, res, _ = W.random_dag(n, 3, float(rng.uniform(0.05, 0.5)), rng, with_prio=False,
+                                        dup_edges=bool(rng.integers(2)))
+        dur = W.random_durations(n, int(rng.choice([1, 64, 100])), 1, 1000, rng)
+        check_cp(mlsim, ptr, idx, res, 3, dur, paths=(0,))
+
+
 def test_single_op_and_empty(mlsim):
     check_run(mlsim, np.array([0, 0]), np.zeros(0, np.int32), np.array([0], np.int32), 1,
               np.array([[5, 1, 7]], np.int32))
