@@ -47,6 +47,9 @@ def lib(path: Optional[str] = None):
         L.oracle_critical_path.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, P, ctypes.c_int64,
                                            P, ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
         L.oracle_critical_path.restype = ctypes.c_int
+        L.oracle_static_run.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, ctypes.c_int64,
+                                        P, ctypes.c_int64, P, P, ctypes.c_int64, P, ctypes.c_int32]
+        L.oracle_static_run.restype = ctypes.c_int
         if path is not None:
             return L
         _lib = L
@@ -108,3 +111,23 @@ def critical_path(succ_ptr, succ_idx, n_ops: int, dur, path_scen: int = -1,
     if rc:
         raise OracleError(rc)
     return cp, (path[: int(plen[0])].copy() if path_scen >= 0 else None)
+
+
+def static_run(succ_ptr, succ_idx, op_res, n_res: int, order, dur, want_finish: bool = True,
+               n_threads: Optional[int] = None, library=None):
+    """Static-order replay of every scenario column of ``dur``: each device
+    runs its ops in the order they appear in ``order``.  Returns
+    ``(makespan [S], finish [n_ops, S] or None, status [S])``."""
+    succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
+    op_res, order, dur = _c(op_res, np.int32), _c(order, np.int32), _c(dur, np.int32)
+    n = op_res.size
+    S = dur.shape[1] if dur.ndim == 2 else 0
+    makespan = np.empty(S, np.int32)
+    status = np.empty(S, np.int32)
+    finish = np.empty((n, S), np.int32) if want_finish else None
+    rc = (library or lib()).oracle_static_run(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res),
+                                              _ptr(order), S, _ptr(dur), S, _ptr(makespan), _ptr(finish),
+                                              S, _ptr(status), _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return makespan, finish, status

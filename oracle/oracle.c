@@ -416,3 +416,144 @@ int oracle_critical_path(int32_t n_ops, const int64_t *succ_ptr, const int32_t *
   free(g.indeg);
   return rc;
 }
+
+/* ------------------------------------------------- static-order replay */
+
+/*
+ * Each device runs its ops in one fixed order: the order in which they appear
+ * in a given permutation of all ops (Sec. 2 describes each device's queue;
+ * here the queue order is fixed in advance instead of by arrival).  An op
+ * starts when every predecessor and the op before it on its device have
+ * finished, so finish(v) = d(v) + max(finish of predecessors, finish of the
+ * previous op on the device).  The ops are visited in a topological order of
+ * the DAG together with the device-order edges.
+ */
+typedef struct {
+  const graph_t *g;
+  const int32_t *topo, *next_on_dev;
+  int64_t s0, s1;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *makespan, *finish, *status;
+  int64_t ld_fin;
+  int rc;
+} st_job;
+
+static void static_one(const st_job *J, int64_t *ready, int64_t *fin, int64_t s) {
+  const graph_t *g = J->g;
+  int32_t st = 0;
+  for (int32_t v = 0; v < g->n; ++v)
+    if (J->dur[(int64_t)v * J->ld_dur + s] < 1) st = ORC_ST_BAD_DUR;
+  int64_t span = 0;
+  if (!st) {
+    for (int32_t v = 0; v < g->n; ++v) ready[v] = 0;
+    for (int32_t k = 0; k < g->n; ++k) {
+      int32_t v = J->topo[k];
+      fin[v] = ready[v] + J->dur[(int64_t)v * J->ld_dur + s];
+      if (fin[v] > INT32_MAX) {
+        st = ORC_ST_OVERFLOW;
+        break;
+      }
+      if (fin[v] > span) span = fin[v];
+      for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e)
+        if (fin[v] > ready[g->si[e]]) ready[g->si[e]] = fin[v];
+      int32_t nx = J->next_on_dev[v];
+      if (nx >= 0 && fin[v] > ready[nx]) ready[nx] = fin[v];
+    }
+  }
+  if (J->status) J->status[s] = st;
+  J->makespan[s] = st ? -1 : (int32_t)span;
+  if (J->finish && !st)
+    for (int32_t v = 0; v < g->n; ++v) J->finish[(int64_t)v * J->ld_fin + s] = (int32_t)fin[v];
+}
+
+static void *static_range(void *arg) {
+  st_job *J = (st_job *)arg;
+  size_t n = (size_t)(J->g->n ? J->g->n : 1);
+  int64_t *ready = (int64_t *)malloc(n * sizeof(int64_t));
+  int64_t *fin = (int64_t *)malloc(n * sizeof(int64_t));
+  if (!ready || !fin)
+    J->rc = ORC_E_NOMEM;
+  else
+    for (int64_t s = J->s0; s < J->s1; ++s) static_one(J, ready, fin, s);
+  free(ready);
+  free(fin);
+  return NULL;
+}
+
+static void set_static_range(void *p, int64_t a, int64_t b) {
+  ((st_job *)p)->s0 = a;
+  ((st_job *)p)->s1 = b;
+}
+
+int oracle_static_run(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                      const int32_t *succ_idx, const int32_t *op_res, const int32_t *order,
+                      int64_t n_scen, const int32_t *dur, int64_t ld_dur, int32_t *makespan,
+                      int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
+  graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, NULL, NULL};
+  int rc = check_graph(&g, 1);
+  if (rc) return rc;
+  if (n_ops > 0 && !order) return ORC_E_INVAL;
+  if (n_scen < 0 || (n_scen > 0 && !makespan)) return ORC_E_INVAL;
+  if (n_scen > 0 && n_ops > 0 && (!dur || ld_dur < n_scen || (finish && ld_fin < n_scen)))
+    return ORC_E_INVAL;
+  size_t n = (size_t)(n_ops ? n_ops : 1);
+  int32_t *seen = (int32_t *)calloc(n, sizeof(int32_t));
+  int32_t *next_on_dev = (int32_t *)malloc(n * sizeof(int32_t));
+  int32_t *last_on_dev = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_res > 0 ? n_res : 1));
+  int32_t *cnt = (int32_t *)calloc(n, sizeof(int32_t));
+  int32_t *topo = (int32_t *)malloc(n * sizeof(int32_t));
+  if (!seen || !next_on_dev || !last_on_dev || !cnt || !topo) rc = ORC_E_NOMEM;
+  /* the order must name every op exactly once */
+  for (int32_t k = 0; k < n_ops && !rc; ++k) {
+    int32_t v = order[k];
+    if (v < 0 || v >= n_ops || seen[v]) rc = ORC_E_INVAL;
+    else seen[v] = 1;
+  }
+  if (!rc) {
+    /* device-order edges: each op to the next op on its device */
+    for (int32_t r = 0; r < n_res; ++r) last_on_dev[r] = -1;
+    for (int32_t v = 0; v < n_ops; ++v) next_on_dev[v] = -1;
+    for (int32_t k = 0; k < n_ops; ++k) {
+      int32_t v = order[k], r = op_res[v];
+      if (last_on_dev[r] >= 0) next_on_dev[last_on_dev[r]] = v;
+      last_on_dev[r] = v;
+    }
+    /* Kahn over DAG edges (with repeats) plus device-order edges */
+    for (int32_t u = 0; u < n_ops; ++u) {
+      for (int64_t e = succ_ptr[u]; e < succ_ptr[u + 1]; ++e) cnt[succ_idx[e]]++;
+      if (next_on_dev[u] >= 0) cnt[next_on_dev[u]]++;
+    }
+    int32_t head = 0, tail = 0;
+    for (int32_t v = 0; v < n_ops; ++v)
+      if (cnt[v] == 0) topo[tail++] = v;
+    while (head < tail) {
+      int32_t v = topo[head++];
+      for (int64_t e = succ_ptr[v]; e < succ_ptr[v + 1]; ++e)
+        if (--cnt[succ_idx[e]] == 0) topo[tail++] = succ_idx[e];
+      if (next_on_dev[v] >= 0 && --cnt[next_on_dev[v]] == 0) topo[tail++] = next_on_dev[v];
+    }
+    if (tail != n_ops) rc = ORC_E_CYCLE; /* the device orders contradict the dependencies */
+  }
+  if (!rc && n_scen > 0) {
+    if (n_threads < 1) n_threads = 1;
+    st_job *jobs = (st_job *)calloc((size_t)n_threads, sizeof(st_job));
+    if (!jobs) {
+      rc = ORC_E_NOMEM;
+    } else {
+      for (int32_t t = 0; t < n_threads; ++t) {
+        st_job J = {&g, topo, next_on_dev, 0, 0, dur, ld_dur, makespan, finish, status, ld_fin, 0};
+        jobs[t] = J;
+      }
+      rc = run_threads(static_range, jobs, sizeof(st_job), n_scen, n_threads, set_static_range);
+      for (int32_t t = 0; t < n_threads && !rc; ++t) rc = jobs[t].rc;
+      free(jobs);
+    }
+  }
+  free(seen);
+  free(next_on_dev);
+  free(last_on_dev);
+  free(cnt);
+  free(topo);
+  return rc;
+}

@@ -82,6 +82,22 @@ int oracle_critical_path(int32_t n_ops,
                          int32_t *path_ops, int32_t path_cap, int32_t *path_len,
                          int32_t n_threads);
 
+/*
+ * Static-order replay: every device runs its ops in the order they appear in
+ * order[] (a permutation of 0..n_ops-1); an op starts when all its
+ * predecessors and the previous op on its device (in that order) have
+ * finished: finish(v) = d(v) + max(those finish times, 0).  Outputs and
+ * status bits as oracle_run_batch (no placement: devices come from op_res).
+ * Returns ORC_E_INVAL if order is not a permutation and ORC_E_CYCLE if the
+ * device orders contradict the dependencies.
+ */
+int oracle_static_run(int32_t n_ops, int32_t n_res,
+                      const int64_t *succ_ptr, const int32_t *succ_idx,
+                      const int32_t *op_res, const int32_t *order,
+                      int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                      int32_t *status, int32_t n_threads);
+
 #ifdef __cplusplus
 }
 #endif

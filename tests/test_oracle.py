@@ -412,3 +412,136 @@ def test_threads_do_not_change_results(library):
     a = run(g, dur, n_threads=1, library=library)
     b = run(g, dur, n_threads=7, library=library)
     assert all((x == y).all() for x, y in zip(a, b))
+
+
+# ------------------------------------------------------ static-order replay
+
+def oracle_static(library, g, order, dur, **kw):
+    return oracle.static_run(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], order, dur,
+                             library=library, **kw)
+
+
+def des_order(g, dur_col, fin_col):
+    """All ops sorted by their start time in a replay (ties by op id): on each
+    device the starts are strictly increasing, so each device's part of this
+    order is the device's own run order."""
+    start = fin_col.astype(np.int64) - dur_col
+    return np.array(sorted(range(g["n"]), key=lambda v: (start[v], v)), np.int32)
+
+
+def test_static_single_device_prefix_sums(library):
+    """One device, no edges: the ops run back to back in the given order, so
+    the finish times are the prefix sums of the durations in that order."""
+    rng = np.random.default_rng(21)
+    for _ in range(20):
+        n = int(rng.integers(1, 50))
+        g = dict(n=n, n_res=1, succ_ptr=np.zeros(n + 1, np.int64), succ_idx=np.zeros(0, np.int32),
+                 op_res=np.zeros(n, np.int32))
+        order = rng.permutation(n).astype(np.int32)
+        dur = random_durations(n, 4, 1, 1000, rng)
+        mk, fin, st = oracle_static(library, g, order, dur)
+        assert (st == 0).all()
+        for s in range(4):
+            expect = np.cumsum(dur[order, s].astype(np.int64))
+            assert (fin[order, s] == expect).all()
+            assert mk[s] == expect[-1]
+
+
+def test_static_own_devices_is_longest_path(library):
+    """Every op on its own device: no device order constrains anything and
+    the finish times are the longest paths (scipy Bellman-Ford)."""
+    rng = np.random.default_rng(22)
+    for _ in range(20):
+        n = int(rng.integers(1, 60))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.25)), dup=bool(rng.integers(2)))
+        g["n_res"], g["op_res"] = n, np.arange(n, dtype=np.int32)
+        order = rng.permutation(n).astype(np.int32)
+        dur = random_durations(n, 3, 1, 1000, rng)
+        mk, fin, _ = oracle_static(library, g, order, dur)
+        for s in range(3):
+            dist = longest_path_scipy(g, dur[:, s])
+            assert (fin[:, s] == dist).all()
+            assert mk[s] == dist.max()
+
+
+def test_static_replays_the_event_order(library):
+    """Given the run order that the event replay produced on every device
+    (its start order), the static-order replay reproduces that scenario's
+    finish times exactly; with several scenarios sharing one order, the
+    scenario the order came from is reproduced."""
+    rng = np.random.default_rng(23)
+    for _ in range(40):
+        n, R = int(rng.integers(1, 60)), int(rng.integers(1, 6))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.3)), prio=bool(rng.integers(2)),
+                       dup=bool(rng.integers(2)))
+        dur = random_durations(n, 3, 1, int(rng.choice([3, 50, 10000])), rng)
+        _, fin, _ = run(g, dur, library=library)
+        for s in range(3):
+            order = des_order(g, dur[:, s], fin[:, s])
+            mk2, fin2, st2 = oracle_static(library, g, order, dur)
+            assert st2[s] == 0
+            assert (fin2[:, s] == fin[:, s]).all()
+            assert mk2[s] == fin[:, s].max()
+
+
+def test_static_order_is_respected(library):
+    """Structure of every static replay: inputs are ready at the start, each
+    device runs its ops in the given order without overlap, and an op starts
+    exactly when the later of its inputs and its device's previous op allow."""
+    rng = np.random.default_rng(24)
+    for _ in range(30):
+        n, R = int(rng.integers(1, 40)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.3)))
+        # a topological order of the DAG keeps every device order consistent
+        P0 = preds(g)
+        topo, done = [], set()
+        while len(topo) < n:  # smallest id whose predecessors are all placed
+            v = min(v for v in range(n) if v not in done and all(u in done for u in P0[v]))
+            topo.append(v)
+            done.add(v)
+        topo = np.array(topo, np.int32)
+        dur = random_durations(n, 2, 1, 100, rng)
+        mk, fin, st = oracle_static(library, g, topo, dur)
+        assert (st == 0).all()
+        P = preds(g)
+        for s in range(2):
+            f = fin[:, s].astype(np.int64)
+            start = f - dur[:, s]
+            prev = {}
+            for v in topo:
+                r = g["op_res"][v]
+                ready = max([f[u] for u in P[v]], default=0)
+                assert start[v] == max(ready, f[prev[r]] if r in prev else 0)
+                prev[r] = v
+            assert mk[s] == f.max()
+
+
+def test_static_errors_and_status(library):
+    # order must be a permutation
+    g = dict(n=3, n_res=1, succ_ptr=np.array([0, 1, 1, 1], np.int64), succ_idx=np.array([1], np.int32),
+             op_res=np.zeros(3, np.int32))
+    dur = np.ones((3, 2), np.int32)
+    for bad in ([0, 0, 1], [0, 1, 3], [0, 1, -1]):
+        with pytest.raises(oracle.OracleError) as e:
+            oracle_static(library, g, np.array(bad, np.int32), dur)
+        assert e.value.code == oracle.E_INVAL
+    # the device order contradicts an edge on the same device
+    with pytest.raises(oracle.OracleError) as e:
+        oracle_static(library, g, np.array([1, 0, 2], np.int32), dur)
+    assert e.value.code == oracle.E_CYCLE
+    # a cycle through two devices: a->d and b->c are edges; device 0 runs c
+    # before a, device 1 runs d before b
+    g2 = dict(n=4, n_res=2, succ_ptr=np.array([0, 1, 2, 2, 2], np.int64), succ_idx=np.array([3, 2], np.int32),
+              op_res=np.array([0, 1, 0, 1], np.int32))
+    with pytest.raises(oracle.OracleError) as e:
+        oracle_static(library, g2, np.array([2, 0, 3, 1], np.int32), np.ones((4, 1), np.int32))
+    assert e.value.code == oracle.E_CYCLE
+    mk, _, _ = oracle_static(library, g2, np.array([0, 2, 1, 3], np.int32), np.ones((4, 1), np.int32))
+    assert mk[0] == 2
+    # bad durations and overflow
+    dur = np.array([[1, 0, 5, 1_500_000_000],
+                    [1, 1, 5, 1_500_000_000],
+                    [1, 1, -3, 1]], np.int32)
+    mk, _, st = oracle_static(library, g, np.array([0, 1, 2], np.int32), dur)
+    assert st.tolist() == [0, oracle.ST_BAD_DUR, oracle.ST_BAD_DUR, oracle.ST_OVERFLOW]
+    assert mk.tolist() == [3, -1, -1, -1]

@@ -42,6 +42,14 @@ MUTANTS = [
      "if (dist[p] == want && (nxt < 0 || p > nxt)) nxt = p;"),
     ("cp-end-highest-id", "if (dist[x] > dist[v]) v = x;", "if (dist[x] >= dist[v]) v = x;"),
     ("cycle-undetected", "return tail == g->n;", "return 1;"),
+    ("static-ignores-device-order", "if (nx >= 0 && fin[v] > ready[nx]) ready[nx] = fin[v];", ""),
+    ("static-ignores-inputs", "if (fin[v] > ready[g->si[e]]) ready[g->si[e]] = fin[v];", "(void)0;"),
+    ("static-device-edges-reversed", "if (last_on_dev[r] >= 0) next_on_dev[last_on_dev[r]] = v;",
+     "if (last_on_dev[r] >= 0) next_on_dev[v] = last_on_dev[r];"),
+    ("static-accepts-repeats", "if (v < 0 || v >= n_ops || seen[v]) rc = ORC_E_INVAL;",
+     "if (v < 0 || v >= n_ops) rc = ORC_E_INVAL;"),
+    ("static-cycle-undetected", "if (tail != n_ops) rc = ORC_E_CYCLE;", "if (tail != n_ops) n_scen = 0;"),
+    ("static-overflow-wraps", "if (fin[v] > INT32_MAX) {", "if (0) {"),
 ]
 
 
