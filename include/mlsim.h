@@ -161,6 +161,43 @@ int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *
  * SIM_E_INVAL for a NULL graph. */
 int sim_graph_walk_eligible(const sim_graph *g);
 
+/*
+ * Static-order replay.  Sec. 2's devices each keep a queue of jobs; here
+ * every device runs its ops in one order fixed in advance: the order in
+ * which they appear in `order`.  An op starts when all its predecessors and
+ * the op before it on its device have finished:
+ *   finish(v) = d(v) + max(finish of v's predecessors,
+ *                          finish of the previous op on res(v) in order, 0).
+ * Given the order in which the event replay ran each device in a scenario,
+ * it reproduces that scenario's finish times exactly.
+ *
+ * sim_static_create compiles the order against a graph (resources from the
+ * graph's op_res):
+ *   order  host int32 [n_ops]: a permutation of 0..n_ops-1 (copied).
+ * Returns SIM_E_INVAL if order is NULL (n_ops > 0) or not a permutation,
+ * SIM_E_CYCLE if the device orders contradict the dependencies (the DAG
+ * plus each device's order has a cycle).  The result does not refer to g
+ * after creation.  Allocates device memory on the current device.
+ */
+typedef struct sim_static sim_static; /* opaque; immutable after creation */
+int sim_static_create(const sim_graph *g, const int32_t *order, sim_static **out);
+
+/* Free a static-order replay.  The caller must first synchronise every
+ * stream that used it. */
+void sim_static_destroy(sim_static *st);
+
+/*
+ * Run the static-order replay for n_scen scenarios.  Arguments, outputs and
+ * status bits as sim_run_batch without placement: makespan = max finish, or
+ * -1 with SIM_ST_BAD_DUR (a duration < 1) or SIM_ST_OVERFLOW (a finish time
+ * above INT32_MAX) in status; finish values of such scenarios are
+ * unspecified.  Asynchronous on `stream`; no memory is allocated.  Calls on
+ * different streams that share one object must not overlap in time.
+ */
+int sim_static_run(const sim_static *st, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                   int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                   void *stream);
+
 #ifdef __cplusplus
 }
 #endif

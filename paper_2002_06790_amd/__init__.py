@@ -27,7 +27,8 @@ SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP, SIM_ALGO_WALK = 0, 1, 2, 3
 ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP, "walk": SIM_ALGO_WALK}
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
-           "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible")
+           "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
+           "sim_static_destroy", "sim_static_run")
 
 _lib = None
 
@@ -70,6 +71,12 @@ def _load():
     L.sim_graph_info.restype = ctypes.c_int
     L.sim_graph_walk_eligible.argtypes = [P]
     L.sim_graph_walk_eligible.restype = ctypes.c_int
+    L.sim_static_create.argtypes = [P, P, ctypes.POINTER(P)]
+    L.sim_static_create.restype = ctypes.c_int
+    L.sim_static_destroy.argtypes = [P]
+    L.sim_static_destroy.restype = None
+    L.sim_static_run.argtypes = [P, I64, P, I64, P, P, I64, P, P]
+    L.sim_static_run.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -181,6 +188,11 @@ class Graph:
             raise SimError(rc, "sim_run_batch")
         return makespan, finish, status
 
+    def static_order(self, order) -> "StaticReplay":
+        """A static-order replay of this graph: every resource runs its ops
+        in the order they appear in ``order`` (a permutation of the op ids)."""
+        return StaticReplay(self, order)
+
     def critical_path(self, dur, path_scen: int = -1, cp_len=None, stream=None):
         """Longest path per scenario; with ``path_scen`` >= 0 also its op list."""
         import torch
@@ -198,3 +210,49 @@ class Graph:
         if rc:
             raise SimError(rc, "sim_critical_path")
         return cp_len, (path[: int(plen[0])].copy() if want else None)
+
+
+class StaticReplay:
+    """Static-order replay compiled against a graph (sim_static_create)."""
+
+    def __init__(self, graph: Graph, order):
+        L = _load()
+        self.n_ops = graph.n_ops
+        self.order = _host(order, np.int32)
+        h = ctypes.c_void_p()
+        rc = L.sim_static_create(graph._h, _hptr(self.order), ctypes.byref(h))
+        if rc:
+            raise SimError(rc, "sim_static_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _load().sim_static_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def run(self, dur, want_finish: bool = False, makespan=None, finish=None, status=None, stream=None):
+        """Replay every scenario column of ``dur`` (int32 [n_ops, S] on the
+        GPU); returns ``(makespan [S], finish [n_ops, S] or None, status [S])``
+        as device tensors.  Asynchronous on the current stream."""
+        import torch
+        dptr, ld = _dev_matrix(dur, torch.int32, self.n_ops, "dur")
+        S = dur.shape[1]
+        dev = dur.device
+        if makespan is None:
+            makespan = torch.empty(S, dtype=torch.int32, device=dev)
+        if status is None:
+            status = torch.empty(S, dtype=torch.int32, device=dev)
+        if want_finish and finish is None:
+            finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
+        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        rc = _load().sim_static_run(self._h, S, dptr, ld, makespan.data_ptr(), fptr, ldf,
+                                    status.data_ptr(), _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_static_run")
+        return makespan, finish, status

@@ -357,33 +357,9 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
 
   C.heap_cap = n ? std::max(1, min_path_cover(n, cs)) : 0;
 
-  // critical-path sweep: the topological order (depth- or breadth-first
-  // flavour) that needs fewer live value slots
-  std::vector<int32_t> o1, o2, s1, s2;
-  kahn(n, cs, true, o1);
-  kahn(n, cs, false, o2);
-  int32_t n1 = assign_cp_slots(n, cs, cp, o1, s1);
-  int32_t n2 = assign_cp_slots(n, cs, cp, o2, s2);
-  const auto &order = n1 <= n2 ? o1 : o2;
-  const auto &slot = n1 <= n2 ? s1 : s2;
-  // two more slots: one that always holds 0 (unused inline predecessors
-  // read it) and one that ops without successors write (never read)
-  C.cp_slots = std::min(n1, n2) + 2;
-  const int32_t zslot = C.cp_slots - 2, sink = C.cp_slots - 1;
-  const int32_t cp_pad = (n + kCpBatch - 1) / kCpBatch * kCpBatch + kCpBatch * kCpAhead;
-  C.cp.assign(cp_pad, CpRec{n ? orig_of[0] : 0, sink, 0, 0, {zslot, zslot, zslot, zslot}});
-  C.cp_pred.clear();
-  for (int32_t k = 0; k < n; ++k) {
-    int32_t v = order[k];
-    CpRec r{orig_of[v], slot[v] >= 0 ? slot[v] : sink, (int32_t)cp[v].size(), (int32_t)C.cp_pred.size(),
-            {zslot, zslot, zslot, zslot}};
-    if (cp[v].size() <= 4)
-      for (size_t e = 0; e < cp[v].size(); ++e) r.p[e] = slot[cp[v][e]];
-    else
-      for (int32_t p : cp[v]) C.cp_pred.push_back(slot[p]);
-    C.cp[k] = r;
-  }
-  if (C.cp_pred.empty()) C.cp_pred.push_back(0);
+  // critical-path sweep
+  std::vector<int32_t> order;
+  build_maxplus(n, cs, cp, orig_of, C.cp, C.cp_pred, C.cp_slots, order);
   C.topo = order;
 
   // compact predecessor CSR (for the sweep variant) and level count
@@ -410,6 +386,44 @@ size_t bytes_of(const std::vector<T> &v) {
 }
 
 }  // namespace
+
+namespace mlsim {
+
+bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
+                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
+                   std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
+                   std::vector<int32_t> &order) {
+  // the topological order (depth- or breadth-first flavour) that needs fewer
+  // live value slots
+  std::vector<int32_t> o1, o2, s1, s2;
+  if (!kahn(n, succ, true, o1) || !kahn(n, succ, false, o2)) return false;
+  const int32_t n1 = assign_cp_slots(n, succ, pred, o1, s1);
+  const int32_t n2 = assign_cp_slots(n, succ, pred, o2, s2);
+  order = n1 <= n2 ? o1 : o2;
+  const auto &slot = n1 <= n2 ? s1 : s2;
+  // two more slots: one that always holds 0 (unused inline predecessors
+  // read it) and one that ops without successors write (never read)
+  slots = std::min(n1, n2) + 2;
+  const int32_t zslot = slots - 2, sink = slots - 1;
+  const int32_t pad = (n + kCpBatch - 1) / kCpBatch * kCpBatch + kCpBatch * kCpAhead;
+  rec.assign(pad, CpRec{n ? row_of[0] : 0, sink, 0, 0, {zslot, zslot, zslot, zslot}});
+  plist.clear();
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t v = order[k];
+    CpRec r{row_of[v], slot[v] >= 0 ? slot[v] : sink, (int32_t)pred[v].size(), (int32_t)plist.size(),
+            {zslot, zslot, zslot, zslot}};
+    if (pred[v].size() <= 4)
+      for (size_t e = 0; e < pred[v].size(); ++e) r.p[e] = slot[pred[v][e]];
+    else
+      for (int32_t p : pred[v]) plist.push_back(slot[p]);
+    rec[k] = r;
+  }
+  if (plist.empty()) plist.push_back(0);
+  return true;
+}
+
+}  // namespace mlsim
+
 
 extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
                                 const int32_t *succ_idx, const int32_t *op_res,
@@ -515,6 +529,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   for (int32_t c = 0; c < n_ops && g->row_identity; ++c) g->row_identity = C.ops[c].orig == c;
   g->h_pred_ptr = C.pred_ptr;
   g->h_pred = C.pred;
+  g->h_res.assign(op_res, op_res + n_ops);
 
   g->scratch = nullptr;
   rc = plan_scratch(g);

@@ -452,49 +452,56 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   }
 }
 
-struct CpArgs {
+struct MpArgs {
   int64_t n_scen;
   const int32_t *dur;
   int64_t ld_dur;
-  int32_t *cp_len;
-  int32_t *dist_out;  // dist of every op (by caller id) for scenario dist_scen
+  int32_t *out;       // [n_scen] longest path / makespan, -1 for a flagged scenario
+  int32_t *status;    // [n_scen] status bits, or null
+  int32_t *finish;    // [n_ops][ld_fin] dist of every op (FIN only)
+  int64_t ld_fin;
+  int32_t *dist_out;  // dist of every op (by caller id) for scenario dist_scen, or null
   int64_t dist_scen;
-  uint32_t *slots_g;  // [blocks][cp_slots][64] when slots are not in LDS
+  uint32_t *slots_g;  // [blocks][slots][64] when slots are not in LDS
 };
 
-// Longest path per scenario: one sweep in a fixed topological order shared by
-// the whole wave, in batches of kCpBatch ops.  Each op reads one coalesced
-// duration row; dist of ops that still have unvisited successors lives in
-// value slots.  Software pipeline: while batch t is swept, the duration rows
-// of batch t + 1 and the records of batch t + 2 are in flight.  A batch's
-// records arrive in registers (lane i holds words i and 64 + i), give the
-// row numbers of the batch by readlane and are copied to a two-batch LDS
-// ring, from which the sweep takes them back into registers.  MODE: where
-// the value slots live (kCpSlotsLds or kCpSlotsGlobal).
-template <int MODE>
-__global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
+// Max-plus sweep, one scenario per lane: dist(v) = d(v) + max over v's
+// predecessors in the table of their dist, in one topological order shared by
+// the whole wave, in batches of kCpBatch ops.  With the DAG's predecessors
+// this is the longest path (critical path); with each op's previous op on its
+// device added it is the static-order replay, whose dist is the finish time.
+// Each op reads one coalesced duration row (and with FIN writes one finish
+// row); dist of ops that still have unvisited successors lives in value
+// slots.  Software pipeline: while batch t is swept, the duration rows of
+// batch t + 1 and the records of batch t + 2 are in flight.  A batch's
+// records arrive in registers (lane i holds words i and 64 + i), give the row
+// numbers of the batch by readlane and are copied to a two-batch LDS ring,
+// from which the sweep takes them back into registers.  MODE: where the value
+// slots live (kCpSlotsLds or kCpSlotsGlobal).
+template <int MODE, bool FIN>
+__global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
-  const int n = G.n;
+  const int n = T.n;
   constexpr int kRecWords = (int)(sizeof(CpRec) / 4);  // 8
   constexpr int kBatchWords = kCpBatch * kRecWords;    // 128: two words per lane
   static_assert(kBatchWords == 2 * kWave, "a batch of records is two words per lane");
-  const int32_t *recw = (const int32_t *)G.cp;
-  const cptr<int32_t> cp_pred = as_const(G.cp_pred);
+  const int32_t *recw = (const int32_t *)T.rec;
+  const cptr<int32_t> cp_pred = as_const(T.pred);
   int32_t *ring = (int32_t *)lds32;  // [2][kBatchWords]
   uint32_t *slots = MODE == kCpSlotsLds ? lds32 + 2 * kBatchWords + lane
-                                        : a.slots_g + (size_t)blockIdx.x * G.cp_slots * kWave + lane;
+                                        : a.slots_g + (size_t)blockIdx.x * T.slots * kWave + lane;
   auto sget = [&](int i) -> uint32_t { return slots[(size_t)i * kWave]; };
   auto sset = [&](int i, uint32_t x) { slots[(size_t)i * kWave] = x; };
   const int nbat = (n + kCpBatch - 1) / kCpBatch;
-  sset(G.cp_slots - 2, 0u);  // the slot that holds 0 (every other slot is written before it is read)
+  sset(T.slots - 2, 0u);  // the slot that holds 0 (every other slot is written before it is read)
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
     const int64_t sc = active ? s : a.n_scen - 1;
     const bool want_dist = a.dist_out && s == a.dist_scen;
     uint32_t mx = 0;
-    bool bad = false;
+    bool bad_dur = false, ovf = false;
     int32_t rx0, rx1;  // records of one batch in flight
     auto load_recs = [&](int t) {
       rx0 = recw[(size_t)t * kBatchWords + lane];
@@ -539,16 +546,17 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
         }
         int32_t d = dv[u];
         if (d < 1) {
-          bad = true;
+          bad_dur = true;
           d = 1;
         }
-        uint32_t dist = best + (uint32_t)d;
+        uint32_t dist = best + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
         if (dist > kI32Max) {
-          bad = true;
+          ovf = true;
           dist = kI32Max;
         }
         sset(CP_FIELD(u, 1), dist);
         mx = dist > mx ? dist : mx;
+        if (FIN && active) a.finish[(int64_t)CP_FIELD(u, 0) * a.ld_fin + s] = (int32_t)dist;
         if (want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
       }
 #undef CP_FIELD
@@ -571,7 +579,11 @@ __global__ __launch_bounds__(kWave) void k_cp(DevGraph G, CpArgs a) {
       if (t + 1 >= nbat) break;
       step(t + 1, db, da);
     }
-    if (active) a.cp_len[s] = bad ? -1 : (int32_t)mx;
+    const int32_t st = bad_dur ? SIM_ST_BAD_DUR : ovf ? SIM_ST_OVERFLOW : 0;
+    if (active) {
+      a.out[s] = st ? -1 : (int32_t)mx;
+      if (a.status) a.status[s] = st;
+    }
   }
 }
 
@@ -778,8 +790,7 @@ int plan_scratch(sim_graph *g) {
   if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
     if (!strcmp(e, "global")) P.cp_mode = kCpSlotsGlobal;
   P.cp_lds_bytes = cp_ring + (P.cp_mode == kCpSlotsLds ? cp_bytes : 0);
-  const int cp_occ = P.cp_mode == kCpSlotsLds ? occupancy_blocks(k_cp<kCpSlotsLds>, P.cp_lds_bytes, cus)
-                                              : occupancy_blocks(k_cp<kCpSlotsGlobal>, P.cp_lds_bytes, cus);
+  const int cp_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus);
   if (cp_occ < 0) return SIM_E_HIP;
   size_t cp_blocks = (size_t)cp_occ;
   if (P.cp_mode == kCpSlotsGlobal && cp_bytes)
@@ -901,19 +912,42 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                            1, list, list_count, list_cap, stream);
 }
 
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus) {
+  if (mode == kCpSlotsLds)
+    return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, true>, lds, cus)
+               : occupancy_blocks(k_maxplus<kCpSlotsLds, false>, lds, cus);
+  return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, true>, lds, cus)
+             : occupancy_blocks(k_maxplus<kCpSlotsGlobal, false>, lds, cus);
+}
+
+int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
+                   const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
+                   int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
+                   uint32_t *slots_g, hipStream_t stream) {
+  MpArgs a{n_scen, dur, ld_dur, out, status, finish, ld_fin, dist_out, dist_scen, slots_g};
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const dim3 grid((unsigned)std::min<int64_t>(tiles, max_blocks)), blk(kWave);
+  if (mode == kCpSlotsLds) {
+    if (finish)
+      k_maxplus<kCpSlotsLds, true><<<grid, blk, lds, stream>>>(T, a);
+    else
+      k_maxplus<kCpSlotsLds, false><<<grid, blk, lds, stream>>>(T, a);
+  } else {
+    if (finish)
+      k_maxplus<kCpSlotsGlobal, true><<<grid, blk, lds, stream>>>(T, a);
+    else
+      k_maxplus<kCpSlotsGlobal, false><<<grid, blk, lds, stream>>>(T, a);
+  }
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
-  char *base = (char *)g->scratch;
-  CpArgs a{n_scen, dur, ld_dur, cp_len, dist_out, dist_scen, (uint32_t *)(base + g->scratch_cp_off)};
-  const int64_t tiles = (n_scen + kWave - 1) / kWave;
-  const unsigned blocks = (unsigned)std::min<int64_t>(tiles, P.cp_blocks);
-  const dim3 grid(blocks), blk(kWave);
-  if (P.cp_mode == kCpSlotsLds)
-    k_cp<kCpSlotsLds><<<grid, blk, P.cp_lds_bytes, stream>>>(g->dg, a);
-  else
-    k_cp<kCpSlotsGlobal><<<grid, blk, P.cp_lds_bytes, stream>>>(g->dg, a);
-  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+  const MpTable T{g->dg.n, g->dg.cp_slots, g->dg.cp, g->dg.cp_pred};
+  return launch_maxplus(T, P.cp_mode, P.cp_blocks, P.cp_lds_bytes, n_scen, dur, ld_dur, cp_len, nullptr,
+                        nullptr, 0, dist_out, dist_scen,
+                        (uint32_t *)((char *)g->scratch + g->scratch_cp_off), stream);
 }
 
 int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

@@ -50,6 +50,15 @@ struct CpRec {
                   // cp_slots - 2, which always holds 0
 };
 
+// Device view of a max-plus sweep table (critical path or static-order
+// replay): records in sweep order and the long predecessor lists.
+struct MpTable {
+  int32_t n;      // ops
+  int32_t slots;  // value slots (live values + the zero slot + the sink slot)
+  const CpRec *rec;
+  const int32_t *pred;
+};
+
 // Device view of a compiled graph (plain pointers, passed by value).
 struct DevGraph {
   int32_t n, R, J, nsrc;  // n real ops (barriers follow them), J joins
@@ -153,8 +162,10 @@ struct sim_graph {
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
-  // host copies for critical-path recovery
-  std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred;
+  // host copies: critical-path recovery (compact predecessor CSR and the
+  // caller id of each compact id) and static-order compilation (resource of
+  // each op by caller id)
+  std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred, h_res;
   size_t scratch_bytes;
 };
 
@@ -177,6 +188,20 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                        hipStream_t stream);
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);
+// the max-plus sweep on any table: blocks resident per launch for a slot mode
+// and LDS size, and the launch itself (finish != null writes finish rows)
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus);
+int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
+                   const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
+                   int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
+                   uint32_t *slots_g, hipStream_t stream);
+// Records of a max-plus sweep over ops 0..n-1 (duration row of op v:
+// row_of[v]) with the given successor and predecessor lists: a topological
+// order, its value slots and the padded records.  False on a cycle.
+bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
+                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
+                   std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
+                   std::vector<int32_t> &order);
 // sizing of persistent grids and LDS, decided once per graph
 int plan_scratch(sim_graph *g);
 // walk limits and sizes (walk.hip); fills the wk_* fields of g->plan except the offset

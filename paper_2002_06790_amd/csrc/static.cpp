@@ -1,0 +1,145 @@
+// Static-order replay: compile a fixed per-device run order against a graph
+// into a max-plus sweep table (the DAG's predecessors plus each op's previous
+// op on its device), and run it with the critical path's sweep kernel.
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "sim.hpp"
+
+using namespace mlsim;
+
+struct sim_static {
+  int32_t n_ops;
+  int device;
+  MpTable tab;      // device view of the records and long predecessor lists
+  int mode;         // where the sweep's value slots live
+  int blocks;       // persistent grid
+  size_t lds;       // LDS bytes per block
+  void *dev_mem;    // records and predecessor lists
+  uint32_t *slots;  // global value slots when they do not fit LDS
+};
+
+namespace {
+
+constexpr size_t kSlotsLdsMax = 32 * 1024;
+constexpr size_t kSlotsScratchBudget = 1ull << 30;
+
+}  // namespace
+
+extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_static **out) {
+  if (!out) return SIM_E_INVAL;
+  *out = nullptr;
+  if (!g) return SIM_E_INVAL;
+  const int32_t n = g->n_ops;
+  if (n > 0 && !order) return SIM_E_INVAL;
+  // the order names every op once
+  std::vector<char> seen(n, 0);
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t v = order[k];
+    if (v < 0 || v >= n || seen[v]) return SIM_E_INVAL;
+    seen[v] = 1;
+  }
+  // predecessors by caller id: the compiled DAG's (duplicates and implied
+  // edges removed: an implied predecessor finishes before the one implying
+  // it) and the previous op on the device in the given order
+  std::vector<std::vector<int32_t>> pred(n), succ(n);
+  for (int32_t c = 0; c < n; ++c) {
+    const int32_t v = g->h_orig_of[c];
+    for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k) pred[v].push_back(g->h_orig_of[g->h_pred[k]]);
+  }
+  std::vector<int32_t> last(g->n_res, -1);
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t v = order[k], r = g->h_res[v];
+    if (last[r] >= 0 && std::find(pred[v].begin(), pred[v].end(), last[r]) == pred[v].end())
+      pred[v].push_back(last[r]);
+    last[r] = v;
+  }
+  for (int32_t v = 0; v < n; ++v) {
+    std::sort(pred[v].begin(), pred[v].end());
+    for (int32_t p : pred[v]) succ[p].push_back(v);
+  }
+  std::vector<int32_t> rows(n), sweep_order;
+  for (int32_t v = 0; v < n; ++v) rows[v] = v;
+  std::vector<CpRec> rec;
+  std::vector<int32_t> plist;
+  int32_t slots = 0;
+  if (!build_maxplus(n, succ, pred, rows, rec, plist, slots, sweep_order)) return SIM_E_CYCLE;
+
+  sim_static *st = new (std::nothrow) sim_static();
+  if (!st) return SIM_E_NOMEM;
+  st->n_ops = n;
+  st->dev_mem = nullptr;
+  st->slots = nullptr;
+  if (hipGetDevice(&st->device) != hipSuccess) {
+    delete st;
+    return SIM_E_HIP;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, st->device) != hipSuccess) {
+    delete st;
+    return SIM_E_HIP;
+  }
+  const size_t rec_bytes = rec.size() * sizeof(CpRec), pl_bytes = plist.size() * 4;
+  const size_t pl_off = (rec_bytes + 255) & ~size_t(255);
+  if (hipMalloc(&st->dev_mem, pl_off + pl_bytes) != hipSuccess) {
+    delete st;
+    return SIM_E_NOMEM;
+  }
+  char *base = (char *)st->dev_mem;
+  if (hipMemcpy(base, rec.data(), rec_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(base + pl_off, plist.data(), pl_bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    sim_static_destroy(st);
+    return SIM_E_HIP;
+  }
+  st->tab = MpTable{n, slots, (const CpRec *)base, (const int32_t *)(base + pl_off)};
+  // value slots in LDS when they fit, else in global scratch for the grid
+  const size_t slot_bytes = (size_t)slots * kWave * 4;
+  const size_t ring = 2 * sizeof(CpRec) * kCpBatch;
+  st->mode = slot_bytes <= kSlotsLdsMax ? kCpSlotsLds : kCpSlotsGlobal;
+  if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
+    if (!strcmp(e, "global")) st->mode = kCpSlotsGlobal;
+  st->lds = ring + (st->mode == kCpSlotsLds ? slot_bytes : 0);
+  int blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount);
+  if (blocks < 0) {
+    sim_static_destroy(st);
+    return SIM_E_HIP;
+  }
+  if (st->mode == kCpSlotsGlobal) {
+    blocks = (int)std::min<size_t>((size_t)blocks, std::max<size_t>(1, kSlotsScratchBudget / slot_bytes));
+    if (hipMalloc((void **)&st->slots, slot_bytes * (size_t)blocks) != hipSuccess) {
+      sim_static_destroy(st);
+      return SIM_E_NOMEM;
+    }
+  }
+  st->blocks = std::max(1, blocks);
+  *out = st;
+  return SIM_OK;
+}
+
+extern "C" void sim_static_destroy(sim_static *st) {
+  if (!st) return;
+  if (st->dev_mem) (void)hipFree(st->dev_mem);
+  if (st->slots) (void)hipFree(st->slots);
+  delete st;
+}
+
+extern "C" int sim_static_run(const sim_static *st, int64_t n_scen, const int32_t *dur,
+                              int64_t ld_dur, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                              int32_t *status, void *stream) {
+  if (!st || n_scen < 0) return SIM_E_INVAL;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (st->n_ops > 0 && (!dur || ld_dur < n_scen)) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (st->n_ops == 0) {
+    // no ops: every iteration takes 0 ns
+    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    return SIM_OK;
+  }
+  return launch_maxplus(st->tab, st->mode, st->blocks, st->lds, n_scen, dur, ld_dur, makespan, status,
+                        finish, ld_fin, nullptr, 0, st->slots, s);
+}
