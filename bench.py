@@ -4,7 +4,10 @@
 One step = one pass of the whole hot path over one batch: ``sim_run_batch``
 (event-driven replay of every scenario, finish times written) followed by
 ``sim_critical_path``.  Inputs are generated on the host, copied to HBM and
-resident before the timed region starts.  Prints one JSON line.
+resident before the timed region starts.  Prints one JSON line.  Outside the
+step it also times the static-order replay (every resource running its ops
+in the order the event replay ran them in scenario 0) and, on a bounded
+sample, the CPU oracle, whose outputs check sampled GPU results.
 
 Default workload: the BERT-large data-parallel graph (16 workers, per-worker
 up/down links; 6624 ops, 48 resources) at 262144 scenarios spanning 12
@@ -119,25 +122,30 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     log(f"ms/step {ms_per_step:.3f} (run_batch {np.mean(ev_ms):.3f} ms, critical_path {np.mean(cp_ms):.3f} ms)")
 
-    # sampled parity against the oracle (outside the timed region)
-    parity = None
-    if not args.no_check:
-        import oracle
-        rng = np.random.default_rng(0)
-        scen = np.unique(np.r_[0, S - 1, rng.integers(0, S, 30)])
-        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h[:, scen],
-                                          place=None if place_h is None else place_h[:, scen])
-        ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, n, dur_h[:, scen])
-        sel = torch.from_numpy(scen).cuda()
-        ok = (np.array_equal(makespan[sel].cpu().numpy(), omk)
-              and np.array_equal(finish[:, sel].cpu().numpy(), ofin)
-              and np.array_equal(status[sel].cpu().numpy(), ost)
-              and np.array_equal(cp_len[sel].cpu().numpy(), ocp))
-        parity = f"{'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
-        log(parity)
+    # static-order replay (outside the step): every resource runs its ops in
+    # the order the event replay ran them in scenario 0
+    fin0 = finish[:, 0].cpu().numpy().astype(np.int64)
+    order = np.lexsort((np.arange(n), fin0 - dur_h[:, 0])).astype(np.int32)
+    sr = g.static_order(order)
+    sr.run(dur, want_finish=True, makespan=makespan, finish=finish, status=status)
+    torch.cuda.synchronize()
+    sr_ms = []
+    for _ in range(args.steps):
+        e0.record()
+        sr.run(dur, want_finish=True, makespan=makespan, finish=finish, status=status)
+        e1.record()
+        e1.synchronize()
+        sr_ms.append(e0.elapsed_time(e1))
+    log(f"static-order replay {np.mean(sr_ms):.3f} ms")
+    sr.close()
+    # the step's outputs again (the static replay reused the buffers)
+    step()
+    torch.cuda.synchronize()
 
-    # CPU oracle baseline on a bounded sample of the same workload
+    # CPU oracle baseline on a bounded sample of the same workload; its
+    # outputs also check sampled GPU results
     cpu = None
+    parity = None
     if args.cpu_sample:
         import oracle
         cs = min(args.cpu_sample, S)
@@ -146,14 +154,25 @@ def main():
         psub = None if place_h is None else np.ascontiguousarray(place_h[:, :cs])
         log(f"cpu oracle on {cs} scenarios, {threads} threads")
         t = time.perf_counter()
-        oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, place=psub,
-                         want_finish=True, n_threads=threads)
-        oracle.critical_path(w.succ_ptr, w.succ_idx, n, sub, n_threads=threads)
+        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, place=psub,
+                                          want_finish=True, n_threads=threads)
+        ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, n, sub, n_threads=threads)
         cpu_s = time.perf_counter() - t
         cpu = {"value": n * cs / cpu_s, "unit": "op-events/s", "cores": threads, "kind": "oracle",
                "sample": f"first {cs} of {S} scenarios (run_batch with finish times + critical_path), "
                          f"{cpu_s:.2f} s"}
         log(f"cpu oracle {cpu['value']:.3e} op-events/s")
+        if not args.no_check:
+            rng = np.random.default_rng(0)
+            scen = np.unique(np.r_[0, cs - 1, rng.integers(0, cs, 30)])
+            sel = torch.from_numpy(scen).cuda()
+            ok = (np.array_equal(makespan[sel].cpu().numpy(), omk[scen])
+                  and np.array_equal(finish[:, sel].cpu().numpy(), ofin[:, scen])
+                  and np.array_equal(status[sel].cpu().numpy(), ost[scen])
+                  and np.array_equal(cp_len[sel].cpu().numpy(), ocp[scen]))
+            parity = f"{'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
+            log(parity)
+        del ofin
 
     # HBM traffic measured by counters for this exact kernel source, if any
     traffic = None
@@ -190,7 +209,9 @@ def main():
         "scenarios_per_s": S / (ms_per_step / 1e3),
         "kernels": {"run_batch_ms": float(np.mean(ev_ms)), "critical_path_ms": float(np.mean(cp_ms)),
                     "run_batch_op_events_per_s": op_events / ev_s,
-                    "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3)},
+                    "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3),
+                    "static_replay_ms": float(np.mean(sr_ms)),
+                    "static_replay_op_events_per_s": op_events / (float(np.mean(sr_ms)) / 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
