@@ -50,6 +50,10 @@ def lib(path: Optional[str] = None):
         L.oracle_static_run.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, ctypes.c_int64,
                                         P, ctypes.c_int64, P, P, ctypes.c_int64, P, ctypes.c_int32]
         L.oracle_static_run.restype = ctypes.c_int
+        L.oracle_attribute.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, ctypes.c_int64, P,
+                                       ctypes.c_int64, P, ctypes.c_int64, P, P, P, P, ctypes.c_int64, P,
+                                       ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
+        L.oracle_attribute.restype = ctypes.c_int
         if path is not None:
             return L
         _lib = L
@@ -131,3 +135,34 @@ def static_run(succ_ptr, succ_idx, op_res, n_res: int, order, dur, want_finish: 
     if rc:
         raise OracleError(rc)
     return makespan, finish, status
+
+
+def attribute(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None, path_scen: int = -1,
+              n_threads: Optional[int] = None, library=None):
+    """Bottleneck attribution of the replay of every scenario column of ``dur``.
+
+    Returns ``(makespan [S], status [S], busy [n_res, S], chain [n_res, S],
+    chain_ops [S], path or None)``: per resource its busy time and the time
+    the binding chain spends on it, the chain's op count, and (for
+    ``path_scen``) the chain from its first op to its last.
+    """
+    succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
+    op_res, prio = _c(op_res, np.int32), _c(prio, np.int32)
+    dur, place = _c(dur, np.int32), _c(place, np.uint16)
+    n = op_res.size
+    S = dur.shape[1] if dur.ndim == 2 else 0
+    makespan = np.empty(S, np.int32)
+    status = np.empty(S, np.int32)
+    busy = np.empty((n_res, S), np.int32)
+    chain = np.empty((n_res, S), np.int32)
+    chain_ops = np.empty(S, np.int32)
+    cap = max(n, 1)
+    path = np.empty(cap, np.int32)
+    plen = np.zeros(1, np.int32)
+    rc = (library or lib()).oracle_attribute(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res),
+                                             _ptr(prio), S, _ptr(dur), S, _ptr(place), S, _ptr(makespan),
+                                             _ptr(status), _ptr(busy), _ptr(chain), S, _ptr(chain_ops),
+                                             path_scen, _ptr(path), cap, _ptr(plen), _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return makespan, status, busy, chain, chain_ops, (path[: int(plen[0])].copy() if path_scen >= 0 else None)

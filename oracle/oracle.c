@@ -84,6 +84,8 @@ typedef struct {
   int64_t *rfree; /* [nres] time each device finishes its last op */
   int32_t *heap;  /* [n] the ready list */
   int32_t hsize;
+  int32_t *prev;  /* [n] or NULL: the op that ran before each op on its device (-1: none) */
+  int32_t *last;  /* [nres] with prev: the last op each device ran */
 } sim_ws;
 
 /* key order of the ready list: ready time, then priority, then op id */
@@ -151,6 +153,8 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
       w->cnt[v] = g->indeg[v];
     }
     for (int32_t r = 0; r < g->nres; ++r) w->rfree[r] = 0;
+    if (w->prev)
+      for (int32_t r = 0; r < g->nres; ++r) w->last[r] = -1;
     w->hsize = 0;
     /* (1) every op with no predecessors is ready at t = 0 */
     for (int32_t v = 0; v < g->n; ++v)
@@ -166,6 +170,10 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
       }
       w->fin[v] = f;
       w->rfree[r] = f;
+      if (w->prev) {
+        w->prev[v] = w->last[r];
+        w->last[r] = v;
+      }
       /* (2) the finished op updates its successors' dependency counters */
       for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e) {
         int32_t x = g->si[e];
@@ -193,6 +201,7 @@ static void *run_range(void *arg) {
   w.fin = (int64_t *)malloc(n * sizeof(int64_t));
   w.rfree = (int64_t *)malloc((R ? R : 1) * sizeof(int64_t));
   w.heap = (int32_t *)malloc(n * sizeof(int32_t));
+  w.prev = w.last = NULL;
   if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap) {
     J->rc = ORC_E_NOMEM;
   } else {
@@ -555,5 +564,170 @@ int oracle_static_run(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
   free(last_on_dev);
   free(cnt);
   free(topo);
+  return rc;
+}
+
+
+/* ------------------------------------------------ bottleneck attribution */
+
+/*
+ * Where the iteration time goes (Sec. 1: finding the performance
+ * bottleneck).  After the replay of a scenario, the binding chain starts at
+ * the op that finishes last (lowest id among equals) and walks back: an op
+ * that starts at t > 0 started then either because a predecessor finished at
+ * t (the chain steps to the lowest-id such predecessor) or because its device
+ * finished the op before it at t (the chain steps to that op); it ends at an
+ * op that starts at 0.  The chain has no gaps, so its durations sum to the
+ * makespan; chain[r] is the part spent on device r.  busy[r] is the total
+ * duration of the ops device r ran.
+ */
+typedef struct {
+  run_job run;
+  const int32_t *pred_ptr, *pred_idx;
+  int32_t *busy, *chain, *chain_ops;
+  int64_t ld_res, path_scen;
+  int32_t *path_ops, path_cap, *path_len;
+} at_job;
+
+static int32_t device_of(const run_job *J, int32_t v, int64_t s) {
+  return J->place ? (int32_t)J->place[(int64_t)v * J->ld_place + s] : J->g->res[v];
+}
+
+static void attribute_one(const at_job *A, sim_ws *w, int32_t *rev, int64_t s) {
+  const run_job *J = &A->run;
+  const graph_t *g = J->g;
+  replay_one(J, w, s);
+  int32_t st = J->status[s];
+  for (int32_t r = 0; r < g->nres; ++r) {
+    A->busy[(int64_t)r * A->ld_res + s] = 0;
+    A->chain[(int64_t)r * A->ld_res + s] = 0;
+  }
+  A->chain_ops[s] = -1;
+  if (s == A->path_scen) *A->path_len = 0;
+  if (st || g->n == 0) {
+    if (!st) A->chain_ops[s] = 0;
+    return;
+  }
+  int64_t busy_r, chain_r;
+  int32_t last = 0;
+  for (int32_t v = 0; v < g->n; ++v) {
+    int32_t r = device_of(J, v, s);
+    busy_r = A->busy[(int64_t)r * A->ld_res + s] + J->dur[(int64_t)v * J->ld_dur + s];
+    A->busy[(int64_t)r * A->ld_res + s] = (int32_t)busy_r;
+    if (w->fin[v] > w->fin[last]) last = v;
+  }
+  int32_t len = 0, v = last;
+  for (;;) {
+    int32_t r = device_of(J, v, s);
+    int64_t d = J->dur[(int64_t)v * J->ld_dur + s];
+    chain_r = A->chain[(int64_t)r * A->ld_res + s] + d;
+    A->chain[(int64_t)r * A->ld_res + s] = (int32_t)chain_r;
+    rev[len++] = v;
+    int64_t start = w->fin[v] - d;
+    if (start == 0) break;
+    int32_t nxt = -1;
+    for (int32_t k = A->pred_ptr[v]; k < A->pred_ptr[v + 1]; ++k) {
+      int32_t p = A->pred_idx[k];
+      if (w->fin[p] == start && (nxt < 0 || p < nxt)) nxt = p;
+    }
+    v = nxt >= 0 ? nxt : w->prev[v];
+    if (v < 0) break; /* cannot happen after a correct replay: the device finished an op at start */
+  }
+  A->chain_ops[s] = len;
+  if (s == A->path_scen) {
+    *A->path_len = len;
+    for (int32_t k = 0; k < len && k < A->path_cap; ++k) A->path_ops[k] = rev[len - 1 - k];
+  }
+}
+
+static void *attribute_range(void *arg) {
+  at_job *A = (at_job *)arg;
+  const graph_t *g = A->run.g;
+  size_t n = (size_t)(g->n ? g->n : 1), R = (size_t)g->nres;
+  sim_ws w;
+  w.ready = (int64_t *)malloc(n * sizeof(int64_t));
+  w.cnt = (int32_t *)malloc(n * sizeof(int32_t));
+  w.fin = (int64_t *)malloc(n * sizeof(int64_t));
+  w.rfree = (int64_t *)malloc((R ? R : 1) * sizeof(int64_t));
+  w.heap = (int32_t *)malloc(n * sizeof(int32_t));
+  w.prev = (int32_t *)malloc(n * sizeof(int32_t));
+  w.last = (int32_t *)malloc((R ? R : 1) * sizeof(int32_t));
+  int32_t *rev = (int32_t *)malloc(n * sizeof(int32_t));
+  if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap || !w.prev || !w.last || !rev)
+    A->run.rc = ORC_E_NOMEM;
+  else
+    for (int64_t s = A->run.s0; s < A->run.s1; ++s) attribute_one(A, &w, rev, s);
+  free(w.ready);
+  free(w.cnt);
+  free(w.fin);
+  free(w.rfree);
+  free(w.heap);
+  free(w.prev);
+  free(w.last);
+  free(rev);
+  return NULL;
+}
+
+static void set_attribute_range(void *p, int64_t a, int64_t b) {
+  ((at_job *)p)->run.s0 = a;
+  ((at_job *)p)->run.s1 = b;
+}
+
+int oracle_attribute(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                     const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                     int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, int32_t *makespan,
+                     int32_t *status, int32_t *busy, int32_t *chain, int64_t ld_res,
+                     int32_t *chain_ops, int64_t path_scen, int32_t *path_ops,
+                     int32_t path_cap, int32_t *path_len, int32_t n_threads) {
+  graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL};
+  int rc = check_graph(&g, 1);
+  if (rc) return rc;
+  if (n_scen < 0 || (n_scen > 0 && (!makespan || !status || !busy || !chain || !chain_ops)))
+    return ORC_E_INVAL;
+  if (n_scen > 0 && (ld_res < n_scen || (n_ops > 0 && (!dur || ld_dur < n_scen))))
+    return ORC_E_INVAL;
+  if (n_scen > 0 && n_ops > 0 && place && ld_place < n_scen) return ORC_E_INVAL;
+  if (path_scen >= n_scen || (path_scen >= 0 && (!path_len || (path_cap > 0 && !path_ops))))
+    return ORC_E_INVAL;
+  if ((rc = build_indeg(&g))) return rc;
+  size_t n = (size_t)(n_ops ? n_ops : 1);
+  int32_t *order = (int32_t *)malloc(n * sizeof(int32_t));
+  int32_t *pred_ptr = (int32_t *)calloc(n + 1, sizeof(int32_t));
+  int32_t *pred_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_ops ? succ_ptr[n_ops] + 1 : 1));
+  int32_t *fill = (int32_t *)malloc(n * sizeof(int32_t));
+  if (!order || !pred_ptr || !pred_idx || !fill) rc = ORC_E_NOMEM;
+  if (!rc) {
+    int acyclic = topo_order(&g, order);
+    if (acyclic != 1) rc = acyclic < 0 ? ORC_E_NOMEM : ORC_E_CYCLE;
+  }
+  if (!rc) { /* predecessor lists */
+    for (int32_t v = 0; v < n_ops; ++v) pred_ptr[v + 1] = pred_ptr[v] + g.indeg[v];
+    for (int32_t v = 0; v < n_ops; ++v) fill[v] = pred_ptr[v];
+    for (int32_t u = 0; u < n_ops; ++u)
+      for (int64_t e = succ_ptr[u]; e < succ_ptr[u + 1]; ++e) pred_idx[fill[succ_idx[e]]++] = u;
+  }
+  if (!rc && n_scen > 0) {
+    if (n_threads < 1) n_threads = 1;
+    at_job *jobs = (at_job *)calloc((size_t)n_threads, sizeof(at_job));
+    if (!jobs) {
+      rc = ORC_E_NOMEM;
+    } else {
+      for (int32_t t = 0; t < n_threads; ++t) {
+        at_job A = {{&g, 0, 0, dur, ld_dur, place, ld_place, makespan, NULL, status, 0, 0},
+                    pred_ptr, pred_idx, busy, chain, chain_ops, ld_res, path_scen, path_ops,
+                    path_cap, path_len};
+        jobs[t] = A;
+      }
+      rc = run_threads(attribute_range, jobs, sizeof(at_job), n_scen, n_threads, set_attribute_range);
+      for (int32_t t = 0; t < n_threads && !rc; ++t) rc = jobs[t].run.rc;
+      free(jobs);
+    }
+  }
+  free(order);
+  free(pred_ptr);
+  free(pred_idx);
+  free(fill);
+  free(g.indeg);
   return rc;
 }

@@ -98,6 +98,31 @@ int oracle_static_run(int32_t n_ops, int32_t n_res,
                       int32_t *makespan, int32_t *finish, int64_t ld_fin,
                       int32_t *status, int32_t n_threads);
 
+/*
+ * Bottleneck attribution of the replay (same inputs as oracle_run_batch;
+ * makespan and status as there).  Per scenario without status bits:
+ *   busy[r*ld_res+s]   total duration of the ops device r ran;
+ *   chain[r*ld_res+s]  time the binding chain spends on device r (the
+ *                      entries of a scenario sum to its makespan);
+ *   chain_ops[s]       ops on the binding chain (0 for an empty graph).
+ * The binding chain starts at the lowest-id op of largest finish time; from
+ * an op v starting at t > 0 it steps to the lowest-id predecessor finishing
+ * at t if there is one, else to the op that ran before v on its device (it
+ * finished at t); it ends at an op starting at 0.  Scenarios with status
+ * bits get busy = chain = 0 and chain_ops = -1.  If path_scen >= 0 the chain
+ * of that scenario is written to path_ops from its first op to its last and
+ * its length to *path_len (0 for a flagged scenario).
+ */
+int oracle_attribute(int32_t n_ops, int32_t n_res,
+                     const int64_t *succ_ptr, const int32_t *succ_idx,
+                     const int32_t *op_res, const int32_t *prio,
+                     int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place,
+                     int32_t *makespan, int32_t *status,
+                     int32_t *busy, int32_t *chain, int64_t ld_res,
+                     int32_t *chain_ops, int64_t path_scen, int32_t *path_ops,
+                     int32_t path_cap, int32_t *path_len, int32_t n_threads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -545,3 +545,131 @@ def test_static_errors_and_status(library):
     mk, _, st = oracle_static(library, g, np.array([0, 1, 2], np.int32), dur)
     assert st.tolist() == [0, oracle.ST_BAD_DUR, oracle.ST_BAD_DUR, oracle.ST_OVERFLOW]
     assert mk.tolist() == [3, -1, -1, -1]
+
+
+# -------------------------------------------------- bottleneck attribution
+
+def oracle_attr(library, g, dur, place=None, path_scen=-1):
+    return oracle.attribute(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], dur,
+                            prio=g.get("prio"), place=place, path_scen=path_scen, library=library)
+
+
+def test_attribution_hand_examples(library):
+    """Two schedules worked by hand.  (1) a (device 0, 3 ns) and b (device 0,
+    2 ns) are sources, c (device 1, 4 ns) needs b: a 0-3, b 3-5, c 5-9.  The
+    chain from c steps to b (its input, finished at 5), then to a (device 0
+    finished a at 3, when b started), which starts at 0: device 0 holds 5 ns
+    of the 9, device 1 4 ns.  (2) a (device 0, 3 ns), c (device 1, 1 ns) and
+    d (device 1, 2 ns, needs a): d runs 3-5 after device 1 idled from 1 to 3;
+    the chain is a, d (3 + 2 ns) and device 1 is busy 3 ns of which the chain
+    holds 2."""
+    g = dict(n=3, n_res=2, succ_ptr=np.array([0, 0, 1, 1], np.int64), succ_idx=np.array([2], np.int32),
+             op_res=np.array([0, 0, 1], np.int32), prio=None)
+    mk, st, busy, chain, cops, path = oracle_attr(library, g, np.array([[3], [2], [4]], np.int32), path_scen=0)
+    assert mk[0] == 9 and st[0] == 0
+    assert chain[:, 0].tolist() == [5, 4] and busy[:, 0].tolist() == [5, 4]
+    assert cops[0] == 3 and path.tolist() == [0, 1, 2]
+    g = dict(n=3, n_res=2, succ_ptr=np.array([0, 1, 1, 1], np.int64), succ_idx=np.array([2], np.int32),
+             op_res=np.array([0, 1, 1], np.int32), prio=None)
+    mk, st, busy, chain, cops, path = oracle_attr(library, g, np.array([[3], [1], [2]], np.int32), path_scen=0)
+    assert mk[0] == 5
+    assert chain[:, 0].tolist() == [3, 2] and busy[:, 0].tolist() == [3, 3]
+    assert cops[0] == 2 and path.tolist() == [0, 2]
+
+
+def test_attribution_chain_covers_makespan(library):
+    """The chain has no gaps: per scenario its per-device times sum to the
+    makespan; busy time is each device's total duration (a plain sum); the
+    chain's share of a device never exceeds its busy time, which never
+    exceeds the makespan; the makespan equals the replay's."""
+    rng = np.random.default_rng(31)
+    for _ in range(40):
+        n, R = int(rng.integers(1, 60)), int(rng.integers(1, 6))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.3)), prio=bool(rng.integers(2)),
+                       dup=bool(rng.integers(2)))
+        S = 4
+        dur = random_durations(n, S, 1, int(rng.choice([3, 100, 10000])), rng)
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16) if rng.integers(2) else None
+        mk, st, busy, chain, cops, _ = oracle_attr(library, g, dur, place=place)
+        rmk, _, _ = run(g, dur, library=library, place=place)
+        assert (mk == rmk).all() and (st == 0).all()
+        res = place.astype(np.int64) if place is not None else np.repeat(g["op_res"][:, None], S, 1)
+        for s in range(S):
+            expect = np.bincount(res[:, s], weights=dur[:, s], minlength=R).astype(np.int64)
+            assert (busy[:, s] == expect).all()
+        assert (chain.sum(0) == mk).all()
+        assert (chain <= busy).all() and (busy <= mk[None, :]).all()
+        assert ((1 <= cops) & (cops <= n)).all()
+
+
+def test_attribution_own_devices_is_critical_path(library):
+    """One device per op: nothing waits for a device, so the chain is the
+    critical path (same end and tie rules) and each op on it contributes its
+    duration on its own device."""
+    rng = np.random.default_rng(32)
+    for _ in range(25):
+        n = int(rng.integers(1, 50))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.3)), dup=bool(rng.integers(2)))
+        g["n_res"], g["op_res"] = n, np.arange(n, dtype=np.int32)
+        dur = random_durations(n, 3, 1, int(rng.choice([3, 1000])), rng)
+        for s in range(3):
+            mk, _, _, chain, cops, path = oracle_attr(library, g, dur, path_scen=s)
+            cp, cpath = oracle_cp(library, g["succ_ptr"], g["succ_idx"], n, dur, path_scen=s)
+            assert mk[s] == cp[s]
+            assert path.tolist() == cpath.tolist() and cops[s] == len(cpath)
+            expect = np.zeros(n, np.int64)
+            expect[cpath] = dur[cpath, s]
+            assert (chain[:, s] == expect).all()
+
+
+def test_attribution_single_device_chain_is_everything(library):
+    """One device never idles while ops remain, so the chain holds every op."""
+    rng = np.random.default_rng(33)
+    for _ in range(20):
+        n = int(rng.integers(1, 50))
+        g = rand_graph(rng, n, 1, float(rng.uniform(0, 0.3)), prio=True)
+        dur = random_durations(n, 3, 1, 50, rng)
+        mk, _, busy, chain, cops, _ = oracle_attr(library, g, dur)
+        assert (cops == n).all() and (chain[0] == mk).all() and (busy[0] == mk).all()
+
+
+def test_attribution_chain_binds(library):
+    """Each step of the chain, checked against the replay's finish times: the
+    chain ends at the lowest-id op of largest finish and starts at 0; each op
+    finishes exactly when the next one starts; a step goes to the lowest-id
+    predecessor finishing then if one does, otherwise to the op that ran
+    right before on the same device."""
+    rng = np.random.default_rng(34)
+    for _ in range(60):
+        n, R = int(rng.integers(1, 40)), int(rng.integers(1, 5))
+        g = rand_graph(rng, n, R, float(rng.uniform(0, 0.4)), prio=bool(rng.integers(2)))
+        dur = random_durations(n, 2, 1, int(rng.choice([2, 4, 100])), rng)
+        _, fin, _ = run(g, dur, library=library)
+        P = preds(g)
+        for s in range(2):
+            _, _, _, _, cops, path = oracle_attr(library, g, dur, path_scen=s)
+            f = fin[:, s].astype(np.int64)
+            start = f - dur[:, s]
+            assert path[-1] == int(np.flatnonzero(f == f.max())[0])
+            assert start[path[0]] == 0 and cops[s] == len(path)
+            for u, v in zip(path[:-1], path[1:]):
+                assert f[u] == start[v]
+                data = [p for p in P[v] if f[p] == start[v]]
+                if data:
+                    assert u == min(data)
+                else:
+                    r = g["op_res"][v]
+                    assert g["op_res"][u] == r
+                    between = [x for x in range(n) if g["op_res"][x] == r and start[u] < start[x] < start[v]]
+                    assert not between
+
+
+def test_attribution_status(library):
+    g = dict(n=3, n_res=1, succ_ptr=np.array([0, 1, 2, 2], np.int64), succ_idx=np.array([1, 2], np.int32),
+             op_res=np.zeros(3, np.int32), prio=None)
+    dur = np.array([[1, 0, 1_500_000_000], [1, 1, 1_500_000_000], [1, 1, 1]], np.int32)
+    mk, st, busy, chain, cops, path = oracle_attr(library, g, dur, path_scen=1)
+    assert st.tolist() == [0, oracle.ST_BAD_DUR, oracle.ST_OVERFLOW]
+    assert mk.tolist() == [3, -1, -1] and cops.tolist() == [3, -1, -1]
+    assert busy[:, 1:].tolist() == [[0, 0]] and chain[:, 1:].tolist() == [[0, 0]]
+    assert path.tolist() == []

@@ -50,6 +50,14 @@ MUTANTS = [
      "if (v < 0 || v >= n_ops) rc = ORC_E_INVAL;"),
     ("static-cycle-undetected", "if (tail != n_ops) rc = ORC_E_CYCLE;", "if (tail != n_ops) n_scen = 0;"),
     ("static-overflow-wraps", "if (fin[v] > INT32_MAX) {", "if (0) {"),
+    ("attr-highest-id-pred", "if (w->fin[p] == start && (nxt < 0 || p < nxt)) nxt = p;",
+     "if (w->fin[p] == start && (nxt < 0 || p > nxt)) nxt = p;"),
+    ("attr-device-first", "v = nxt >= 0 ? nxt : w->prev[v];", "v = w->prev[v] >= 0 ? w->prev[v] : nxt;"),
+    ("attr-end-highest-id", "if (w->fin[v] > w->fin[last]) last = v;", "if (w->fin[v] >= w->fin[last]) last = v;"),
+    ("attr-busy-overwrites", "busy_r = A->busy[(int64_t)r * A->ld_res + s] + J->dur[(int64_t)v * J->ld_dur + s];",
+     "busy_r = J->dur[(int64_t)v * J->ld_dur + s];"),
+    ("attr-chain-stops-early", "if (start == 0) break;", "if (start <= d) break;"),
+    ("attr-prev-not-recorded", "w->prev[v] = w->last[r];", "w->prev[v] = -1;"),
 ]
 
 
