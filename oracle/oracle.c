@@ -411,6 +411,7 @@ int oracle_critical_path(int32_t n_ops, const int64_t *succ_ptr, const int32_t *
           if (dist[p] == want && (nxt < 0 || p < nxt)) nxt = p;
         }
         v = nxt;
+        if (v < 0) break; /* cannot happen: some predecessor lies on a longest path */
       }
       *path_len = len;
       for (int32_t k = 0; k < len && k < path_cap; ++k) path_ops[k] = rev[len - 1 - k];
