@@ -162,6 +162,36 @@ int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *
 int sim_graph_walk_eligible(const sim_graph *g);
 
 /*
+ * Bottleneck attribution (Sec. 1: the simulator is used to find the
+ * performance bottleneck).  Replays every scenario as sim_run_batch does
+ * (same dur/place/makespan/status/finish arguments; finish and status are
+ * required here) and additionally returns, per scenario s without status
+ * bits:
+ *   prev      device int32 [n_ops][ld_op] (required): the op that ran right
+ *             before op v on its resource, -1 if none (same ld as finish);
+ *   busy      device int32 [n_res][ld_res]: total duration of the ops
+ *             resource r ran;
+ *   chain     device int32 [n_res][ld_res]: time the binding chain spends on
+ *             resource r; a scenario's entries sum to its makespan;
+ *   chain_ops device int32 [n_scen]: ops on the binding chain.
+ * The binding chain starts at the lowest-id op with the largest finish time
+ * and walks back: from an op that starts at t > 0 to the lowest-id
+ * predecessor that finished at t if one did (its input arrived last), else to
+ * the op that ran before it on its resource (which finished at t: the op
+ * waited for its resource); it ends at an op that starts at 0.  Scenarios
+ * with status bits get busy = chain = 0 and chain_ops = -1.  path_scen,
+ * path_ops, path_cap and path_len as in sim_critical_path, for the binding
+ * chain (from its first op to its last; length 0 for a flagged scenario);
+ * with a path request the call synchronises `stream`.  Otherwise
+ * asynchronous; no memory is allocated.
+ */
+int sim_attribute(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *status,
+                  int32_t *finish, int32_t *prev, int64_t ld_op, int32_t *busy, int32_t *chain,
+                  int64_t ld_res, int32_t *chain_ops, int64_t path_scen, int32_t *path_ops,
+                  int32_t path_cap, int32_t *path_len, void *stream);
+
+/*
  * Static-order replay.  Sec. 2's devices each keep a queue of jobs; here
  * every device runs its ops in one order fixed in advance: the order in
  * which they appear in `order`.  An op starts when all its predecessors and

@@ -28,7 +28,7 @@ ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
            "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
-           "sim_static_destroy", "sim_static_run")
+           "sim_static_destroy", "sim_static_run", "sim_attribute")
 
 _lib = None
 
@@ -77,6 +77,8 @@ def _load():
     L.sim_static_destroy.restype = None
     L.sim_static_run.argtypes = [P, I64, P, I64, P, P, I64, P, P]
     L.sim_static_run.restype = ctypes.c_int
+    L.sim_attribute.argtypes = [P, I64, P, I64, P, I64, P, P, P, P, I64, P, P, I64, P, I64, P, I32, P, P]
+    L.sim_attribute.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -192,6 +194,37 @@ class Graph:
         """A static-order replay of this graph: every resource runs its ops
         in the order they appear in ``order`` (a permutation of the op ids)."""
         return StaticReplay(self, order)
+
+    def attribute(self, dur, place=None, path_scen: int = -1, stream=None) -> dict:
+        """Replay every scenario column of ``dur`` and attribute its
+        iteration time (sim_attribute).  Returns a dict of device tensors
+        ``makespan``, ``status``, ``finish``, ``prev`` (op that ran before each
+        op on its resource), ``busy`` and ``chain`` ([n_res, S]: busy time and
+        binding-chain time per resource), ``chain_ops`` ([S]), and ``path``
+        (host array, the binding chain of ``path_scen``, or None)."""
+        import torch
+        dptr, ld = _dev_matrix(dur, torch.int32, self.n_ops, "dur")
+        S = dur.shape[1]
+        pptr, ldp = _dev_matrix(place, torch.uint16, self.n_ops, "place")
+        dev = dur.device
+        out = {k: torch.empty(S, dtype=torch.int32, device=dev) for k in ("makespan", "status", "chain_ops")}
+        out["finish"] = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
+        out["prev"] = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
+        out["busy"] = torch.empty((self.n_res, S), dtype=torch.int32, device=dev)
+        out["chain"] = torch.empty((self.n_res, S), dtype=torch.int32, device=dev)
+        cap = max(self.n_ops, 1)
+        path = np.empty(cap, np.int32)
+        plen = np.zeros(1, np.int32)
+        want = path_scen >= 0
+        rc = _load().sim_attribute(self._h, S, dptr, ld, pptr, ldp, out["makespan"].data_ptr(),
+                                   out["status"].data_ptr(), out["finish"].data_ptr(), out["prev"].data_ptr(),
+                                   max(S, 1), out["busy"].data_ptr(), out["chain"].data_ptr(), max(S, 1),
+                                   out["chain_ops"].data_ptr(), path_scen, path.ctypes.data if want else None,
+                                   cap if want else 0, plen.ctypes.data if want else None, _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_attribute")
+        out["path"] = path[: int(plen[0])].copy() if want else None
+        return out
 
     def critical_path(self, dur, path_scen: int = -1, cp_len=None, stream=None):
         """Longest path per scenario; with ``path_scen`` >= 0 also its op list."""

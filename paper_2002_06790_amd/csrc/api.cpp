@@ -100,3 +100,75 @@ extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32
   for (int32_t k = 0; k < (int32_t)rev.size() && k < path_cap; ++k) path_ops[k] = rev[rev.size() - 1 - k];
   return SIM_OK;
 }
+
+extern "C" int sim_attribute(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                             const uint16_t *place, int64_t ld_place, int32_t *makespan,
+                             int32_t *status, int32_t *finish, int32_t *prev, int64_t ld_op,
+                             int32_t *busy, int32_t *chain, int64_t ld_res, int32_t *chain_ops,
+                             int64_t path_scen, int32_t *path_ops, int32_t path_cap,
+                             int32_t *path_len, void *stream) {
+  if (!g || n_scen < 0) return SIM_E_INVAL;
+  if (path_scen >= n_scen || path_scen < -1) return SIM_E_INVAL;
+  if (path_scen >= 0 && (!path_len || (path_cap > 0 && !path_ops) || path_cap < 0)) return SIM_E_INVAL;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan || !status || !chain_ops || !busy || !chain || ld_res < n_scen) return SIM_E_INVAL;
+  const int32_t n = g->n_ops, R = g->n_res;
+  if (n > 0 && (!finish || !prev || ld_op < n_scen)) return SIM_E_INVAL;
+  if (bad_matrix(dur, ld_dur, n_scen, n)) return SIM_E_INVAL;
+  if (place && ld_place < n_scen) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (n == 0) {
+    // no ops: every iteration takes 0 ns on an empty chain
+    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess ||
+        hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess ||
+        hipMemsetAsync(chain_ops, 0, (size_t)n_scen * 4, st) != hipSuccess ||
+        hipMemset2DAsync(busy, (size_t)ld_res * 4, 0, (size_t)n_scen * 4, R, st) != hipSuccess ||
+        hipMemset2DAsync(chain, (size_t)ld_res * 4, 0, (size_t)n_scen * 4, R, st) != hipSuccess)
+      return SIM_E_HIP;
+    if (path_scen >= 0) *path_len = 0;
+    return SIM_OK;
+  }
+  int rc = launch_event_prev(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, prev, ld_op,
+                             status, st);
+  if (rc) return rc;
+  rc = launch_attr(g, n_scen, dur, ld_dur, place, ld_place, finish, prev, ld_op, status, busy, chain,
+                   ld_res, chain_ops, st);
+  if (rc || path_scen < 0) return rc;
+
+  // the chain of one scenario, walked on the host by the kernel's rule
+  std::vector<int32_t> f(n), d(n), pv(n), res(n);
+  std::vector<uint16_t> pl(place ? n : 0);
+  int32_t st_s = 0;
+  const int64_t ps = path_scen;
+  if (hipMemcpy2DAsync(f.data(), 4, finish + ps, (size_t)ld_op * 4, 4, n, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpy2DAsync(d.data(), 4, dur + ps, (size_t)ld_dur * 4, 4, n, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpy2DAsync(pv.data(), 4, prev + ps, (size_t)ld_op * 4, 4, n, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      (place && hipMemcpy2DAsync(pl.data(), 2, place + ps, (size_t)ld_place * 2, 2, n, hipMemcpyDeviceToHost,
+                                 st) != hipSuccess) ||
+      hipMemcpyAsync(&st_s, status + ps, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return SIM_E_HIP;
+  *path_len = 0;
+  if (st_s) return SIM_OK;
+  // predecessors by caller id
+  std::vector<std::vector<int32_t>> pred(n);
+  for (int32_t c = 0; c < n; ++c)
+    for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k)
+      pred[g->h_orig_of[c]].push_back(g->h_orig_of[g->h_pred[k]]);
+  int32_t v = 0;
+  for (int32_t x = 1; x < n; ++x)
+    if (f[x] > f[v]) v = x;
+  std::vector<int32_t> rev;
+  while (v >= 0 && v < n && (int32_t)rev.size() < n) {
+    rev.push_back(v);
+    const int32_t start = f[v] - d[v];
+    if (start <= 0) break;
+    int32_t nxt = -1;
+    for (int32_t p : pred[v])
+      if (f[p] == start && (nxt < 0 || p < nxt)) nxt = p;
+    v = nxt >= 0 ? nxt : pv[v];
+  }
+  *path_len = (int32_t)rev.size();
+  for (int32_t k = 0; k < (int32_t)rev.size() && k < path_cap; ++k) path_ops[k] = rev[rev.size() - 1 - k];
+  return SIM_OK;
+}

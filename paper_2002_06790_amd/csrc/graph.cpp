@@ -479,6 +479,20 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
          o_pp = take(bytes_of(C.pred_ptr)), o_pr = take(bytes_of(C.pred)),
          o_topo = take(bytes_of(C.topo)), o_wpp = take(bytes_of(C.wp_ptr)),
          o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws));
+  // attribution: predecessors by caller id (ascending; implied ones removed:
+  // they finish strictly before the op that implies them) and resources
+  std::vector<int32_t> ap_ptr(n_ops + 1, 0), ap, row_res(op_res, op_res + n_ops);
+  {
+    std::vector<std::vector<int32_t>> pl(n_ops);
+    for (int32_t c = 0; c < n_ops; ++c)
+      for (int32_t k = C.pred_ptr[c]; k < C.pred_ptr[c + 1]; ++k) pl[C.ops[c].orig].push_back(C.ops[C.pred[k]].orig);
+    for (int32_t v = 0; v < n_ops; ++v) {
+      std::sort(pl[v].begin(), pl[v].end());
+      ap.insert(ap.end(), pl[v].begin(), pl[v].end());
+      ap_ptr[v + 1] = (int32_t)ap.size();
+    }
+  }
+  const size_t o_app = take(bytes_of(ap_ptr)), o_ap = take(bytes_of(ap)), o_rres = take(bytes_of(row_res));
   if (hipMalloc(&g->dev_mem, off ? off : 256) != hipSuccess) {
     delete g;
     return SIM_E_NOMEM;
@@ -493,7 +507,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
             put(o_pp, C.pred_ptr.data(), bytes_of(C.pred_ptr)) && put(o_pr, C.pred.data(), bytes_of(C.pred)) &&
             put(o_topo, C.topo.data(), bytes_of(C.topo)) &&
             put(o_wpp, C.wp_ptr.data(), bytes_of(C.wp_ptr)) && put(o_wp, C.wp.data(), bytes_of(C.wp)) &&
-            put(o_wsp, C.ws_ptr.data(), bytes_of(C.ws_ptr)) && put(o_ws, C.ws.data(), bytes_of(C.ws));
+            put(o_wsp, C.ws_ptr.data(), bytes_of(C.ws_ptr)) && put(o_ws, C.ws.data(), bytes_of(C.ws)) &&
+            put(o_app, ap_ptr.data(), bytes_of(ap_ptr)) && put(o_ap, ap.data(), bytes_of(ap)) &&
+            put(o_rres, row_res.data(), bytes_of(row_res));
   if (!ok) {
     (void)hipFree(g->dev_mem);
     delete g;
@@ -521,6 +537,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.wp = (const int32_t *)(base + o_wp);
   d.ws_ptr = (const int32_t *)(base + o_wsp);
   d.ws = (const int32_t *)(base + o_ws);
+  d.ap_ptr = (const int32_t *)(base + o_app);
+  d.ap = (const int32_t *)(base + o_ap);
+  d.row_res = (const int32_t *)(base + o_rres);
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;

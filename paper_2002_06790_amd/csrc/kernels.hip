@@ -274,18 +274,22 @@ struct EvArgs {
   const int32_t *list;        // retry list (scenario indices) and its length
   const int32_t *list_count;
   int32_t list_cap;
+  int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
+  int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
 
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
-template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, class RfGet, class RfSet, class Flush>
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, class RfGet, class RfSet,
+          class LastXchg, class Flush>
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
                                            int &end, int2 *jst, int it, int64_t s,
                                            int64_t sc, uint32_t &st, uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
-                                           RfGet rf_get, RfSet rf_set, Flush flush) {
+                                           int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
+                                           LastXchg last_xchg, Flush flush) {
   const int n = G.n, R = G.R;
   const int2 *succ = (const int2 *)G.succ;
   const int4 *rec4 = (const int4 *)G.ops;
@@ -328,6 +332,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
   }
   rf_set(r, fin);
   span = fin > span ? fin : span;
+  const int32_t before = PREV ? last_xchg(r, row) : 0;  // the op this resource ran last
   heap_settle_ahead<DEEP>(A);
   // the record too: a step that releases nothing leaves its second half
   // unused, and a load still in flight at the end of a step makes the next
@@ -339,6 +344,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
     if (k == qs) {
       fq[k] = (int32_t)fin;
       rq[k] = row;
+      if (PREV) pq[k] = before;
     }
   if (qs == kFinQ - 1) flush(kFinQ);
   bool hole = true;  // the root was popped and is not yet replaced
@@ -385,7 +391,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
 // PLACE: resources come from the per-scenario placement matrix.  Finish times
 // are written in bursts of kFinQ stores per lane, so their completion is
 // waited for once per burst instead of once per step.
-template <bool RF_LDS, bool ROW_ID, bool PLACE>
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -405,6 +411,20 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     else
       rfree_g[r * kWave] = v;
   };
+  // PREV: the last op (row) each resource ran, next to the resource times
+  lptr<int32_t> last_l = as_lds((int32_t *)(lds + (size_t)heap_lds * kWave) + (size_t)R * kWave) + lane;
+  int32_t *last_g = PREV && !RF_LDS ? a.last_g + (size_t)blockIdx.x * R * kWave + lane : nullptr;
+  auto last_xchg = [&](int r, int32_t row) -> int32_t {
+    int32_t x;
+    if (RF_LDS) {
+      x = last_l[r * kWave];
+      last_l[r * kWave] = row;
+    } else {
+      x = last_g[r * kWave];
+      last_g[r * kWave] = row;
+    }
+    return x;
+  };
 
   int64_t items = a.n_scen;
   if (a.retry) {
@@ -422,26 +442,36 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     const int64_t sc = in_range || a.retry == 2 ? s : a.n_scen - 1;
     const bool store_fin = a.finish && active;
     for (int r = 0; r < R; ++r) rf_set(r, 0);
+    if (PREV)
+      for (int r = 0; r < R; ++r) {
+        if (RF_LDS)
+          last_l[r * kWave] = -1;
+        else
+          last_g[r * kWave] = -1;
+      }
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
     heap.root = kEmpty;
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
-    int32_t fq[kFinQ], rq[kFinQ];  // buffered finish times and their rows
+    int32_t fq[kFinQ], rq[kFinQ], pq[kFinQ];  // buffered finish times, their rows, previous ops
     auto flush = [&](int cnt) {
 #pragma unroll
       for (int k = 0; k < kFinQ; ++k)
-        if (k < cnt && store_fin) a.finish[(int64_t)rq[k] * a.ld_fin + s] = fq[k];
+        if (k < cnt && store_fin) {
+          a.finish[(int64_t)rq[k] * a.ld_fin + s] = fq[k];
+          if (PREV) a.prev[(int64_t)rq[k] * a.ld_fin + s] = pq[k];
+        }
     };
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the steps start with nothing in flight
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
       if (__ballot(end > heap.le))
-        event_step<true, RF_LDS, ROW_ID, PLACE>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
-                                         rf_get, rf_set, flush);
+        event_step<true, RF_LDS, ROW_ID, PLACE, PREV>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
+                                                      pq, rf_get, rf_set, last_xchg, flush);
       else
-        event_step<false, RF_LDS, ROW_ID, PLACE>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
-                                          rf_get, rf_set, flush);
+        event_step<false, RF_LDS, ROW_ID, PLACE, PREV>(G, a, heap, end, jst, it, s, sc, st, span, fq,
+                                                       rq, pq, rf_get, rf_set, last_xchg, flush);
     }
     flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
@@ -583,6 +613,121 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
     if (active) {
       a.out[s] = st ? -1 : (int32_t)mx;
       if (a.status) a.status[s] = st;
+    }
+  }
+}
+
+struct AtArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  const uint16_t *place;
+  int64_t ld_place;
+  const int32_t *finish;  // [n_ops][ld_op] from the event replay
+  const int32_t *prev;    // [n_ops][ld_op] each op's predecessor on its resource (-1: none)
+  int64_t ld_op;
+  const int32_t *status;  // [n_scen]
+  int32_t *busy;          // [R][ld_res]
+  int32_t *chain;         // [R][ld_res]
+  int64_t ld_res;
+  int32_t *chain_ops;     // [n_scen]
+  uint32_t *acc_g;        // [blocks][2 R][64] when the accumulators are not in LDS
+};
+
+constexpr int kAtBatch = 8;  // rows loaded together in the busy-time sweep
+constexpr int kAtPreds = 4;  // predecessor finish times loaded together in a chain step
+
+// Bottleneck attribution, one scenario per lane (the paper's use of the
+// simulator to find the bottleneck, Sec. 1).  First a sweep over all ops in
+// id order (coalesced rows of durations and finish times) sums each
+// resource's busy time and finds the op that finishes last (the lowest id
+// among equals).  Then each lane walks its binding chain back from that op:
+// from an op that starts at t > 0, to the lowest-id predecessor finishing at
+// t if there is one, else to the op that ran before it on its resource; the
+// walk ends at an op starting at 0 and adds each op's duration to its
+// resource.  Scenarios with status bits get zeros and a chain length of -1.
+template <bool PLACE, bool LDS>
+__global__ __launch_bounds__(kWave) void k_attr(DevGraph G, AtArgs a) {
+  extern __shared__ uint32_t lds32[];
+  const int lane = threadIdx.x;
+  const int n = G.n, R = G.R;
+  uint32_t *busy_acc = LDS ? lds32 + lane : a.acc_g + (size_t)blockIdx.x * 2 * R * kWave + lane;
+  uint32_t *chain_acc = busy_acc + (size_t)R * kWave;
+  auto res_of = [&](int v, int64_t sc) -> int {
+    return PLACE ? (int)a.place[(int64_t)v * a.ld_place + sc] : G.row_res[v];
+  };
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    const bool active = s < a.n_scen;
+    const int64_t sc = active ? s : a.n_scen - 1;
+    const bool ok = active && a.status[s] == 0;
+    for (int r = 0; r < R; ++r) {
+      busy_acc[(size_t)r * kWave] = 0;
+      chain_acc[(size_t)r * kWave] = 0;
+    }
+    uint32_t best = 0;
+    int last = 0;
+    for (int v0 = 0; v0 < n; v0 += kAtBatch) {
+      int32_t dv[kAtBatch], fv[kAtBatch];
+      int rv[kAtBatch];
+#pragma unroll
+      for (int u = 0; u < kAtBatch; ++u) {
+        const int v = v0 + u < n ? v0 + u : n - 1;
+        dv[u] = a.dur[(int64_t)v * a.ld_dur + sc];
+        fv[u] = a.finish[(int64_t)v * a.ld_op + sc];
+        rv[u] = res_of(v, sc);
+      }
+#pragma unroll
+      for (int u = 0; u < kAtBatch; ++u) {
+        if (v0 + u >= n) break;
+        if ((unsigned)rv[u] < (unsigned)R) busy_acc[(size_t)rv[u] * kWave] += (uint32_t)dv[u];
+        if ((uint32_t)fv[u] > best) {
+          best = (uint32_t)fv[u];
+          last = v0 + u;
+        }
+      }
+    }
+    // the binding chain (each op at most once: at most n steps)
+    bool walking = ok;
+    int v = last, ops = 0;
+    for (int step = 0; step < n && __ballot(walking); ++step) {
+      if (!walking) continue;
+      const int32_t d = a.dur[(int64_t)v * a.ld_dur + s];
+      const int32_t f = a.finish[(int64_t)v * a.ld_op + s];
+      const int r = res_of(v, s);
+      if ((unsigned)r < (unsigned)R) chain_acc[(size_t)r * kWave] += (uint32_t)d;
+      ++ops;
+      const int32_t start = f - d;
+      if (start <= 0) {
+        walking = false;
+        continue;
+      }
+      int nxt = -1;
+      for (int e0 = G.ap_ptr[v]; e0 < G.ap_ptr[v + 1] && nxt < 0; e0 += kAtPreds) {
+        const int e1 = G.ap_ptr[v + 1];
+        int pv[kAtPreds];
+        int32_t fp[kAtPreds];
+#pragma unroll
+        for (int u = 0; u < kAtPreds; ++u) {
+          pv[u] = G.ap[e0 + u < e1 ? e0 + u : e1 - 1];
+          fp[u] = a.finish[(int64_t)pv[u] * a.ld_op + s];
+        }
+#pragma unroll
+        for (int u = 0; u < kAtPreds; ++u)  // ascending ids: the first match is the lowest
+          if (nxt < 0 && e0 + u < e1 && fp[u] == start) nxt = pv[u];
+      }
+      if (nxt < 0) nxt = a.prev[(int64_t)v * a.ld_op + s];
+      if ((unsigned)nxt >= (unsigned)n)
+        walking = false;  // cannot happen for a replay's own outputs
+      else
+        v = nxt;
+    }
+    if (active) {
+      for (int r = 0; r < R; ++r) {
+        a.busy[(int64_t)r * a.ld_res + s] = ok ? (int32_t)busy_acc[(size_t)r * kWave] : 0;
+        a.chain[(int64_t)r * a.ld_res + s] = ok ? (int32_t)chain_acc[(size_t)r * kWave] : 0;
+      }
+      a.chain_ops[s] = ok ? ops : -1;
     }
   }
 }
@@ -770,8 +915,8 @@ int plan_scratch(sim_graph *g) {
     lds_groups = std::min(kD, std::max(0, atoi(e)));
   P.ev_heap_le = kL2 + kD * lds_groups;
   P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes;
-  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false>, P.ev_lds_bytes, cus)
-                            : occupancy_blocks(k_event<false, false, false>, P.ev_lds_bytes, cus);
+  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus)
+                            : occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
@@ -780,6 +925,21 @@ int plan_scratch(sim_graph *g) {
   if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
     ev_blocks = std::min(ev_blocks, (size_t)std::max(1, atoi(e)));
   P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
+  // the event kernel for attribution: a last-op table beside the resource times
+  P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
+  const int ev_prev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
+                                 : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
+  if (ev_prev_occ < 0) return SIM_E_HIP;
+  P.ev_prev_blocks = std::max(1, std::min(ev_prev_occ, P.ev_blocks));
+  // attribution chains: busy and chain accumulators in LDS when they fit
+  const size_t at_bytes = (size_t)2 * G.R * kWave * 4;
+  P.at_lds = at_bytes <= 64 * 1024;
+  P.at_lds_bytes = P.at_lds ? at_bytes : 8;
+  const int at_occ = P.at_lds ? occupancy_blocks(k_attr<false, true>, P.at_lds_bytes, cus)
+                              : occupancy_blocks(k_attr<false, false>, P.at_lds_bytes, cus);
+  if (at_occ < 0) return SIM_E_HIP;
+  P.at_blocks = (int32_t)(P.at_lds ? at_occ
+                                   : std::min<size_t>(at_occ, std::max<size_t>(1, kScratchBudget / at_bytes)));
 
   const int32_t ev_grid = P.ev_blocks;
 
@@ -824,6 +984,8 @@ int plan_scratch(sim_graph *g) {
   g->scratch_ev_heap_off = take(heap_g_bytes * ev_grid);
   g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * ev_grid);
   g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
+  g->scratch_ev_last_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
+  g->scratch_at_off = take(P.at_lds ? 0 : (size_t)2 * G.R * kWave * 4 * P.at_blocks);
   g->scratch_sw_val_off = take(P.sw_val_lds ? 0 : val_bytes * P.sw_blocks);
   g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
@@ -861,34 +1023,46 @@ namespace {
 int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
-                      const int32_t *list_count, int32_t list_cap, hipStream_t stream) {
+                      const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
-           list, list_count, list_cap};
+           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
   // when the last round of tiles would fill less than half the grid, use
   // fewer blocks that each take the same number of tiles (within one)
-  const int64_t rounds = (tiles + P.ev_blocks - 1) / P.ev_blocks;
-  const int64_t tail = tiles - (rounds - 1) * P.ev_blocks;
-  const dim3 grid((unsigned)(2 * tail >= P.ev_blocks ? std::min<int64_t>(tiles, P.ev_blocks)
-                                                     : (tiles + rounds - 1) / rounds));
-  const size_t lds = P.ev_lds_bytes;
-  const int variant = (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+  const int64_t blocks = prev ? P.ev_prev_blocks : P.ev_blocks;
+  const int64_t rounds = (tiles + blocks - 1) / blocks;
+  const int64_t tail = tiles - (rounds - 1) * blocks;
+  const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
+                                                : (tiles + rounds - 1) / rounds));
+  const size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
+  const int variant = (prev ? 8 : 0) | (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+#define EV_CASE(V, A, B, C, D) \
+  case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
-    case 0: k_event<false, false, false><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 1: k_event<false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 2: k_event<false, true, false><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 3: k_event<false, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 4: k_event<true, false, false><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 5: k_event<true, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
-    case 6: k_event<true, true, false><<<grid, block, lds, stream>>>(g->dg, a); break;
-    default: k_event<true, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+    EV_CASE(0, false, false, false, false)
+    EV_CASE(1, false, false, true, false)
+    EV_CASE(2, false, true, false, false)
+    EV_CASE(3, false, true, true, false)
+    EV_CASE(4, true, false, false, false)
+    EV_CASE(5, true, false, true, false)
+    EV_CASE(6, true, true, false, false)
+    EV_CASE(7, true, true, true, false)
+    EV_CASE(8, false, false, false, true)
+    EV_CASE(9, false, false, true, true)
+    EV_CASE(10, false, true, false, true)
+    EV_CASE(11, false, true, true, true)
+    EV_CASE(12, true, false, false, true)
+    EV_CASE(13, true, false, true, true)
+    EV_CASE(14, true, true, false, true)
+    default: k_event<true, true, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   }
+#undef EV_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 }  // namespace
@@ -897,7 +1071,14 @@ int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream) {
   return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
-                           status, 0, nullptr, nullptr, 0, stream);
+                           status, 0, nullptr, nullptr, 0, nullptr, stream);
+}
+
+int launch_event_prev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                      int32_t *prev, int64_t ld_op, int32_t *status, hipStream_t stream) {
+  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_op,
+                           status, 0, nullptr, nullptr, 0, prev, stream);
 }
 
 int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
@@ -906,10 +1087,10 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                        hipStream_t stream) {
   // the listed scenarios, then (only if the list overflowed) every flagged one
   int rc = launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
-                             2, list, list_count, list_cap, stream);
+                             2, list, list_count, list_cap, nullptr, stream);
   if (rc) return rc;
   return launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
-                           1, list, list_count, list_cap, stream);
+                           1, list, list_count, list_cap, nullptr, stream);
 }
 
 int maxplus_occupancy(int mode, bool fin, size_t lds, int cus) {
@@ -948,6 +1129,30 @@ int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld
   return launch_maxplus(T, P.cp_mode, P.cp_blocks, P.cp_lds_bytes, n_scen, dur, ld_dur, cp_len, nullptr,
                         nullptr, 0, dist_out, dist_scen,
                         (uint32_t *)((char *)g->scratch + g->scratch_cp_off), stream);
+}
+
+int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                const uint16_t *place, int64_t ld_place, const int32_t *finish, const int32_t *prev,
+                int64_t ld_op, const int32_t *status, int32_t *busy, int32_t *chain, int64_t ld_res,
+                int32_t *chain_ops, hipStream_t stream) {
+  const ScratchPlan &P = g->plan;
+  AtArgs a{n_scen, dur, ld_dur, place, ld_place, finish, prev, ld_op, status, busy, chain, ld_res,
+           chain_ops, (uint32_t *)((char *)g->scratch + g->scratch_at_off)};
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const dim3 grid((unsigned)std::min<int64_t>(tiles, P.at_blocks)), blk(kWave);
+  const size_t lds = P.at_lds_bytes;
+  if (P.at_lds) {
+    if (place)
+      k_attr<true, true><<<grid, blk, lds, stream>>>(g->dg, a);
+    else
+      k_attr<false, true><<<grid, blk, lds, stream>>>(g->dg, a);
+  } else {
+    if (place)
+      k_attr<true, false><<<grid, blk, lds, stream>>>(g->dg, a);
+    else
+      k_attr<false, false><<<grid, blk, lds, stream>>>(g->dg, a);
+  }
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
 int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

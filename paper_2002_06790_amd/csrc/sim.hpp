@@ -83,6 +83,11 @@ struct DevGraph {
   const int32_t *wp;
   const int32_t *ws_ptr;  // [n+nb+1]
   const int32_t *ws;
+  // attribution: predecessors by caller id, ascending ([n+1] CSR), and the
+  // resource of each op by caller id
+  const int32_t *ap_ptr;
+  const int32_t *ap;
+  const int32_t *row_res;
 };
 
 // Lockstep walk (walk.hip).  Per group of tiles, k_pilot writes a header of
@@ -139,6 +144,10 @@ struct ScratchPlan {
   int32_t sw_val_lds;   // sweep: per-op state in LDS (1) or global (0)
   int32_t sw_res_lds;   // sweep: per-resource state in LDS (1) or global (0)
   size_t ev_lds_bytes, cp_lds_bytes, sw_lds_bytes;
+  // attribution: the event kernel with each op's predecessor on its resource
+  // (its last-op table beside the resource times), then the chain kernel
+  int32_t ev_prev_blocks, at_blocks, at_lds;
+  size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
   int32_t wk_ok;
   int32_t wk_groups_max;  // groups the scratch holds
@@ -162,6 +171,7 @@ struct sim_graph {
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
+  size_t scratch_ev_last_off, scratch_at_off;
   // host copies: critical-path recovery (compact predecessor CSR and the
   // caller id of each compact id) and static-order compilation (resource of
   // each op by caller id)
@@ -188,6 +198,15 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                        hipStream_t stream);
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);
+// attribution: the event replay that also records each op's predecessor on
+// its resource, and the busy-time / binding-chain kernel over its outputs
+int launch_event_prev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                      int32_t *prev, int64_t ld_op, int32_t *status, hipStream_t stream);
+int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                const uint16_t *place, int64_t ld_place, const int32_t *finish, const int32_t *prev,
+                int64_t ld_op, const int32_t *status, int32_t *busy, int32_t *chain, int64_t ld_res,
+                int32_t *chain_ops, hipStream_t stream);
 // the max-plus sweep on any table: blocks resident per launch for a slot mode
 // and LDS size, and the launch itself (finish != null writes finish rows)
 int maxplus_occupancy(int mode, bool fin, size_t lds, int cus);
