@@ -6,8 +6,9 @@ One step = one pass of the whole hot path over one batch: ``sim_run_batch``
 ``sim_critical_path``.  Inputs are generated on the host, copied to HBM and
 resident before the timed region starts.  Prints one JSON line.  Outside the
 step it also times the static-order replay (every resource running its ops
-in the order the event replay ran them in scenario 0) and, on a bounded
-sample, the CPU oracle, whose outputs check sampled GPU results.
+in the order the event replay ran them in scenario 0), the bottleneck
+attribution and, on a bounded sample, the CPU oracle, whose outputs check
+sampled GPU results.
 
 Default workload: the BERT-large data-parallel graph (16 workers, per-worker
 up/down links; 6624 ops, 48 resources) at 262144 scenarios spanning 12
@@ -138,6 +139,21 @@ def main():
         sr_ms.append(e0.elapsed_time(e1))
     log(f"static-order replay {np.mean(sr_ms):.3f} ms")
     sr.close()
+    # bottleneck attribution (outside the step): the replay with each op's
+    # predecessor on its resource, busy time and binding chain per resource
+    del sr
+    at = g.attribute(dur, place=place)
+    torch.cuda.synchronize()
+    at_ms = []
+    for _ in range(args.steps):
+        del at
+        e0.record()
+        at = g.attribute(dur, place=place)
+        e1.record()
+        e1.synchronize()
+        at_ms.append(e0.elapsed_time(e1))
+    del at
+    log(f"attribution {np.mean(at_ms):.3f} ms")
     # the step's outputs again (the static replay reused the buffers)
     step()
     torch.cuda.synchronize()
@@ -211,7 +227,8 @@ def main():
                     "run_batch_op_events_per_s": op_events / ev_s,
                     "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3),
                     "static_replay_ms": float(np.mean(sr_ms)),
-                    "static_replay_op_events_per_s": op_events / (float(np.mean(sr_ms)) / 1e3)},
+                    "static_replay_op_events_per_s": op_events / (float(np.mean(sr_ms)) / 1e3),
+                    "attribution_ms": float(np.mean(at_ms))},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
