@@ -503,12 +503,14 @@ struct MpArgs {
 // Each op reads one coalesced duration row (and with FIN writes one finish
 // row); dist of ops that still have unvisited successors lives in value
 // slots.  Software pipeline: while batch t is swept, the duration rows of
-// batch t + 1 and the records of batch t + 2 are in flight.  A batch's
-// records arrive in registers (lane i holds words i and 64 + i), give the row
-// numbers of the batch by readlane and are copied to a two-batch LDS ring,
-// from which the sweep takes them back into registers.  MODE: where the value
-// slots live (kCpSlotsLds or kCpSlotsGlobal).
-template <int MODE, bool FIN>
+// batches t + 1 and t + 2 and the records of batch t + 3 are in flight.  A
+// batch's records arrive in registers (lane i holds words i and 64 + i) and
+// are parked in a four-batch LDS ring; reading a batch back gives its row
+// numbers (for its loads) and its fields (for its sweep) by readlane.  MODE:
+// where the value slots live (kCpSlotsLds or kCpSlotsGlobal); OUT: what
+// besides the per-scenario result is written (kMpOutFinish: every op's dist
+// as finish rows; kMpOutDist: every op's dist for one scenario).
+template <int MODE, int OUT>
 __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
@@ -518,8 +520,8 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   static_assert(kBatchWords == 2 * kWave, "a batch of records is two words per lane");
   const int32_t *recw = (const int32_t *)T.rec;
   const cptr<int32_t> cp_pred = as_const(T.pred);
-  int32_t *ring = (int32_t *)lds32;  // [2][kBatchWords]
-  uint32_t *slots = MODE == kCpSlotsLds ? lds32 + 2 * kBatchWords + lane
+  int32_t *ring = (int32_t *)lds32;  // [4][kBatchWords]
+  uint32_t *slots = MODE == kCpSlotsLds ? lds32 + 4 * kBatchWords + lane
                                         : a.slots_g + (size_t)blockIdx.x * T.slots * kWave + lane;
   auto sget = [&](int i) -> uint32_t { return slots[(size_t)i * kWave]; };
   auto sset = [&](int i, uint32_t x) { slots[(size_t)i * kWave] = x; };
@@ -529,7 +531,7 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
     const int64_t s = tile * kWave + lane;
     const bool active = s < a.n_scen;
     const int64_t sc = active ? s : a.n_scen - 1;
-    const bool want_dist = a.dist_out && s == a.dist_scen;
+    const bool want_dist = OUT == kMpOutDist && s == a.dist_scen;
     uint32_t mx = 0;
     bool bad_dur = false, ovf = false;
     int32_t rx0, rx1;  // records of one batch in flight
@@ -538,28 +540,31 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
       rx1 = recw[(size_t)t * kBatchWords + kWave + lane];
     };
     auto stage_recs = [&](int t) {
-      ring[(t & 1) * kBatchWords + lane] = rx0;
-      ring[(t & 1) * kBatchWords + kWave + lane] = rx1;
+      ring[(t & 3) * kBatchWords + lane] = rx0;
+      ring[(t & 3) * kBatchWords + kWave + lane] = rx1;
     };
-    auto load_rows = [&](int32_t (&dv)[kCpBatch]) {
+    // rows of batch t, whose records are in the ring
+    auto load_rows = [&](int t, int32_t (&dv)[kCpBatch]) {
+      const int32_t y0 = ring[(t & 3) * kBatchWords + lane];
+      const int32_t y1 = ring[(t & 3) * kBatchWords + kWave + lane];
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
         const int w = u * kRecWords;  // word of the batch holding the row
-        const int row = __builtin_amdgcn_readlane(w < kWave ? rx0 : rx1, w & (kWave - 1));
-        dv[u] = a.dur[(int64_t)row * a.ld_dur + sc];
+        const uint32_t row = (uint32_t)__builtin_amdgcn_readlane(w < kWave ? y0 : y1, w & (kWave - 1));
+        dv[u] = a.dur[(uint64_t)row * (uint64_t)a.ld_dur + sc];  // rows are never negative
       }
     };
     auto sweep = [&](int t, const int32_t (&dv)[kCpBatch]) {
       // the batch's records back in registers (lane i: words i and 64 + i), fields by readlane
-      const int32_t y0 = ring[(t & 1) * kBatchWords + lane];
-      const int32_t y1 = ring[(t & 1) * kBatchWords + kWave + lane];
+      const int32_t y0 = ring[(t & 3) * kBatchWords + lane];
+      const int32_t y1 = ring[(t & 3) * kBatchWords + kWave + lane];
 #define CP_FIELD(u, f) __builtin_amdgcn_readlane(((u) * kRecWords + (f)) < kWave ? y0 : y1, ((u) * kRecWords + (f)) & (kWave - 1))
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
         if (t * kCpBatch + u >= n) break;
         const int np = CP_FIELD(u, 2);
         uint32_t best;
-        if (np <= 4) {  // unused entries name the slot that holds 0
+        if (__builtin_expect(np <= 4, 1)) {  // unused entries name the slot that holds 0
           const uint32_t x0 = sget(CP_FIELD(u, 4));
           const uint32_t x1 = sget(CP_FIELD(u, 5));
           const uint32_t x2 = sget(CP_FIELD(u, 6));
@@ -586,28 +591,36 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
         }
         sset(CP_FIELD(u, 1), dist);
         mx = dist > mx ? dist : mx;
-        if (FIN && active) a.finish[(int64_t)CP_FIELD(u, 0) * a.ld_fin + s] = (int32_t)dist;
-        if (want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
+        if (OUT == kMpOutFinish && active) a.finish[(int64_t)CP_FIELD(u, 0) * a.ld_fin + s] = (int32_t)dist;
+        if (OUT == kMpOutDist && want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
       }
 #undef CP_FIELD
     };
-    // one pipeline step: batch t + 1's records go to the ring and its rows
-    // out, batch t + 2's records out, then batch t is swept
-    auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&nxt)[kCpBatch]) {
-      stage_recs(t + 1);
-      load_rows(nxt);
-      load_recs(t + 2);
+    // One pipeline step: batch t + 2's records (loaded during step t - 1,
+    // before batch t + 1's rows) go to the ring, batch t + 3's records and
+    // batch t + 2's rows go out, then batch t is swept.  Loads complete in
+    // issue order, so waiting for the records leaves batch t + 1's rows in
+    // flight, and waiting for batch t's rows leaves t + 1's and t + 2's.
+    auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&ahead2)[kCpBatch]) {
+      stage_recs(t + 2);
+      load_recs(t + 3);
+      load_rows(t + 2, ahead2);
       sweep(t, cur);
     };
-    int32_t da[kCpBatch], db[kCpBatch];
+    int32_t da[kCpBatch], db[kCpBatch], dc[kCpBatch];
     load_recs(0);
     stage_recs(0);
-    load_rows(da);
     load_recs(1);
-    for (int t = 0; t < nbat; t += 2) {
-      step(t, da, db);
+    stage_recs(1);
+    load_rows(0, da);
+    load_recs(2);
+    load_rows(1, db);
+    for (int t = 0; t < nbat; t += 3) {
+      step(t, da, dc);
       if (t + 1 >= nbat) break;
       step(t + 1, db, da);
+      if (t + 2 >= nbat) break;
+      step(t + 2, dc, db);
     }
     const int32_t st = bad_dur ? SIM_ST_BAD_DUR : ovf ? SIM_ST_OVERFLOW : 0;
     if (active) {
@@ -945,7 +958,7 @@ int plan_scratch(sim_graph *g) {
 
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
-  const size_t cp_ring = 2 * sizeof(CpRec) * kCpBatch;  // record ring
+  const size_t cp_ring = 4 * sizeof(CpRec) * kCpBatch;  // record ring
   P.cp_mode = cp_bytes <= 32 * 1024 ? kCpSlotsLds : kCpSlotsGlobal;
   if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
     if (!strcmp(e, "global")) P.cp_mode = kCpSlotsGlobal;
@@ -1095,10 +1108,10 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
 
 int maxplus_occupancy(int mode, bool fin, size_t lds, int cus) {
   if (mode == kCpSlotsLds)
-    return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, true>, lds, cus)
-               : occupancy_blocks(k_maxplus<kCpSlotsLds, false>, lds, cus);
-  return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, true>, lds, cus)
-             : occupancy_blocks(k_maxplus<kCpSlotsGlobal, false>, lds, cus);
+    return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutFinish>, lds, cus)
+               : occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutNone>, lds, cus);
+  return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutFinish>, lds, cus)
+             : occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutNone>, lds, cus);
 }
 
 int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
@@ -1108,17 +1121,16 @@ int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64
   MpArgs a{n_scen, dur, ld_dur, out, status, finish, ld_fin, dist_out, dist_scen, slots_g};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const dim3 grid((unsigned)std::min<int64_t>(tiles, max_blocks)), blk(kWave);
-  if (mode == kCpSlotsLds) {
-    if (finish)
-      k_maxplus<kCpSlotsLds, true><<<grid, blk, lds, stream>>>(T, a);
-    else
-      k_maxplus<kCpSlotsLds, false><<<grid, blk, lds, stream>>>(T, a);
-  } else {
-    if (finish)
-      k_maxplus<kCpSlotsGlobal, true><<<grid, blk, lds, stream>>>(T, a);
-    else
-      k_maxplus<kCpSlotsGlobal, false><<<grid, blk, lds, stream>>>(T, a);
-  }
+  const int out_kind = finish ? kMpOutFinish : dist_out ? kMpOutDist : kMpOutNone;
+#define MP_CASE(M, O) \
+  if (mode == M && out_kind == O) k_maxplus<M, O><<<grid, blk, lds, stream>>>(T, a);
+  MP_CASE(kCpSlotsLds, kMpOutNone)
+  MP_CASE(kCpSlotsLds, kMpOutFinish)
+  MP_CASE(kCpSlotsLds, kMpOutDist)
+  MP_CASE(kCpSlotsGlobal, kMpOutNone)
+  MP_CASE(kCpSlotsGlobal, kMpOutFinish)
+  MP_CASE(kCpSlotsGlobal, kMpOutDist)
+#undef MP_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

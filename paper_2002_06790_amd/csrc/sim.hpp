@@ -39,8 +39,9 @@ struct OpRec {
 // batches of kCpBatch plus kCpBatch * kCpAhead more, so a sweep can read
 // records and rows ahead without bounds checks.
 constexpr int kCpBatch = 16;  // ops per batch of the sweep
-constexpr int kCpAhead = 2;   // batches of records read ahead
+constexpr int kCpAhead = 3;   // batches of records read ahead
 constexpr int kCpSlotsGlobal = 0, kCpSlotsLds = 1;  // where the sweep's value slots live
+constexpr int kMpOutNone = 0, kMpOutFinish = 1, kMpOutDist = 2;  // what else the sweep writes
 struct CpRec {
   int32_t orig;   // row of dur
   int32_t slot;   // slot receiving dist(v) (ops without successors: slot cp_slots - 1)

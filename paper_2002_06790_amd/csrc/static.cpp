@@ -96,7 +96,7 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   st->tab = MpTable{n, slots, (const CpRec *)base, (const int32_t *)(base + pl_off)};
   // value slots in LDS when they fit, else in global scratch for the grid
   const size_t slot_bytes = (size_t)slots * kWave * 4;
-  const size_t ring = 2 * sizeof(CpRec) * kCpBatch;
+  const size_t ring = 4 * sizeof(CpRec) * kCpBatch;
   st->mode = slot_bytes <= kSlotsLdsMax ? kCpSlotsLds : kCpSlotsGlobal;
   if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
     if (!strcmp(e, "global")) st->mode = kCpSlotsGlobal;
