@@ -54,6 +54,14 @@ def lib(path: Optional[str] = None):
                                        ctypes.c_int64, P, ctypes.c_int64, P, P, P, P, ctypes.c_int64, P,
                                        ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
         L.oracle_attribute.restype = ctypes.c_int
+        L.oracle_philox4x32_10.argtypes = [P, P, P]
+        L.oracle_philox4x32_10.restype = None
+        L.oracle_philox4x64_10.argtypes = [P, P, P]
+        L.oracle_philox4x64_10.restype = None
+        L.oracle_generate.argtypes = [ctypes.c_int32, ctypes.c_int64, P, ctypes.c_int32, ctypes.c_int64,
+                                      ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int64, P, ctypes.c_int64,
+                                      ctypes.c_int32]
+        L.oracle_generate.restype = ctypes.c_int
         if path is not None:
             return L
         _lib = L
@@ -166,3 +174,34 @@ def attribute(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None
     if rc:
         raise OracleError(rc)
     return makespan, status, busy, chain, chain_ops, (path[: int(plen[0])].copy() if path_scen >= 0 else None)
+
+
+def philox4x32_10(ctr, key, library=None) -> np.ndarray:
+    """Philox4x32-10 of one counter block (4 uint32) under one key (2 uint32)."""
+    c, k = np.asarray(ctr, np.uint32).copy(), np.asarray(key, np.uint32).copy()
+    out = np.empty(4, np.uint32)
+    (library or lib()).oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def philox4x64_10(ctr, key, library=None) -> np.ndarray:
+    """Philox4x64-10 of one counter block (4 uint64) under one key (2 uint64)."""
+    c, k = np.asarray(ctr, np.uint64).copy(), np.asarray(key, np.uint64).copy()
+    out = np.empty(4, np.uint64)
+    (library or lib()).oracle_philox4x64_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def generate(base, n_scen: int, knob_block: int, noise: int, seed: int, scen0: int = 0,
+             n_threads: Optional[int] = None, library=None) -> np.ndarray:
+    """Generated durations int32 [n_ops, n_scen] from ``base`` ([n_knobs, n_ops]
+    int32): knob grid times counter-based noise (``oracle.h`` states the formula)."""
+    base = _c(np.atleast_2d(base), np.int32)
+    n_knobs, n = base.shape
+    dur = np.empty((n, n_scen), np.int32)
+    rc = (library or lib()).oracle_generate(n, n_scen, _ptr(base), n_knobs, knob_block, noise,
+                                            seed & (2**64 - 1), scen0, _ptr(dur), n_scen,
+                                            _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return dur

@@ -732,3 +732,120 @@ int oracle_attribute(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
   free(g.indeg);
   return rc;
 }
+
+/* ------------------------------------------------- scenario generation */
+/*
+ * Philox4x32-10 and Philox4x64-10, the counter-based generators of Salmon,
+ * Moraes, Dror and Shaw ("Parallel random numbers: as easy as 1, 2, 3",
+ * SC'11), written from that definition: ten rounds; a round multiplies
+ * words 0 and 2 by the two round multipliers, and the new words are
+ * (hi(M1*x2) ^ x1 ^ k0, lo(M1*x2), hi(M0*x0) ^ x3 ^ k1, lo(M0*x0)); the key
+ * words grow by the Weyl constants (golden ratio, sqrt(3) - 1) after every
+ * round.
+ */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; ++r) {
+    uint64_t p0 = (uint64_t)0xD2511F53u * x0;
+    uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;
+    uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    uint32_t y1 = (uint32_t)p1;
+    uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    uint32_t y3 = (uint32_t)p0;
+    x0 = y0, x1 = y1, x2 = y2, x3 = y3;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = x0, out[1] = x1, out[2] = x2, out[3] = x3;
+}
+
+void oracle_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]) {
+  uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint64_t k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; ++r) {
+    unsigned __int128 p0 = (unsigned __int128)0xD2E7470EE14C6C93ull * x0;
+    unsigned __int128 p1 = (unsigned __int128)0xCA5A826395121157ull * x2;
+    uint64_t y0 = (uint64_t)(p1 >> 64) ^ x1 ^ k0;
+    uint64_t y1 = (uint64_t)p1;
+    uint64_t y2 = (uint64_t)(p0 >> 64) ^ x3 ^ k1;
+    uint64_t y3 = (uint64_t)p0;
+    x0 = y0, x1 = y1, x2 = y2, x3 = y3;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+  out[0] = x0, out[1] = x1, out[2] = x2, out[3] = x3;
+}
+
+/*
+ * One generated duration (the scenario generator's definition):
+ *   S = scen0 + s (global scenario index), k = (S / knob_block) mod n_knobs,
+ *   b = base[k][v];
+ *   (x0..x3) = Philox4x32-10(counter (lo32(S), hi32(S), v, 0),
+ *                            key (lo32(seed), hi32(seed)));
+ *   U = sum of the eight 16-bit halves of x0..x3 (an Irwin-Hall sum of 8
+ *       uniforms on 0..65535), t = 2U - 524280 (zero mean, |t| <= 524280);
+ *   d = b + floor((b * t * noise + 2^39) / 2^40), exact in int64.
+ * A base outside [1, 2^24] gives d = 0 (an invalid duration).
+ */
+static int32_t gen_one(const int32_t *base, int32_t n_ops, int32_t n_knobs, int64_t knob_block,
+                       uint32_t noise, uint64_t seed, int64_t S, int32_t v) {
+  int64_t k = (S / knob_block) % n_knobs;
+  int64_t b = base[k * (int64_t)n_ops + v];
+  if (b < 1 || b > ((int64_t)1 << 24)) return 0;
+  uint32_t ctr[4] = {(uint32_t)S, (uint32_t)((uint64_t)S >> 32), (uint32_t)v, 0};
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t x[4];
+  oracle_philox4x32_10(ctr, key, x);
+  int64_t U = 0;
+  for (int i = 0; i < 4; ++i) U += (int64_t)(x[i] & 0xFFFFu) + (int64_t)(x[i] >> 16);
+  int64_t t = 2 * U - 524280;
+  int64_t q = b * t * (int64_t)noise; /* |q| < 2^24 * 2^19 * 2^20 = 2^63 */
+  int64_t adj = (q + ((int64_t)1 << 39)) >> 40; /* arithmetic shift: floor */
+  return (int32_t)(b + adj);
+}
+
+typedef struct {
+  int32_t n;
+  const int32_t *base;
+  int32_t n_knobs;
+  int64_t knob_block;
+  uint32_t noise;
+  uint64_t seed;
+  int64_t scen0;
+  int32_t *dur;
+  int64_t ld;
+  int64_t s0, s1;
+} gen_job;
+
+static void *gen_range(void *arg) {
+  gen_job *J = (gen_job *)arg;
+  for (int32_t v = 0; v < J->n; ++v)
+    for (int64_t s = J->s0; s < J->s1; ++s)
+      J->dur[v * J->ld + s] =
+          gen_one(J->base, J->n, J->n_knobs, J->knob_block, J->noise, J->seed, J->scen0 + s, v);
+  return NULL;
+}
+
+static void set_gen_range(void *p, int64_t a, int64_t b) {
+  ((gen_job *)p)->s0 = a;
+  ((gen_job *)p)->s1 = b;
+}
+
+int oracle_generate(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                    int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
+                    int32_t *dur, int64_t ld_dur, int32_t n_threads) {
+  if (n_ops < 0 || n_scen < 0 || n_knobs < 1 || knob_block < 1 || scen0 < 0 ||
+      noise >= (1u << 20) || ld_dur < n_scen || n_scen > INT64_MAX - scen0)
+    return ORC_E_INVAL;
+  if (n_ops == 0 || n_scen == 0) return ORC_OK;
+  if (!base || !dur) return ORC_E_INVAL;
+  if (n_threads < 1) n_threads = 1;
+  gen_job *jobs = (gen_job *)calloc((size_t)n_threads, sizeof(gen_job));
+  if (!jobs) return ORC_E_NOMEM;
+  for (int32_t t = 0; t < n_threads; ++t)
+    jobs[t] = (gen_job){n_ops, base, n_knobs, knob_block, noise, seed, scen0, dur, ld_dur, 0, 0};
+  int rc = run_threads(gen_range, jobs, sizeof(gen_job), n_scen, n_threads, set_gen_range);
+  free(jobs);
+  return rc;
+}

@@ -123,6 +123,34 @@ int oracle_attribute(int32_t n_ops, int32_t n_res,
                      int32_t *chain_ops, int64_t path_scen, int32_t *path_ops,
                      int32_t path_cap, int32_t *path_len, int32_t n_threads);
 
+/*
+ * Counter-based generators (Salmon et al., SC'11): Philox4x32-10 and
+ * Philox4x64-10 applied to one counter block under one key.
+ */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+void oracle_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+
+/*
+ * Scenario generation: durations of a strategy-knob grid with per-op
+ * counter-based noise (the paper's motivation: many strategies and
+ * configurations evaluated by simulation, Sec. 1; op times vary by under
+ * 1 % of their mean, Sec. 3).  For op v and scenario s (global index
+ * S = scen0 + s):
+ *   knob k = (S / knob_block) mod n_knobs, b = base[k * n_ops + v];
+ *   (x0..x3) = Philox4x32-10(counter (lo32 S, hi32 S, v, 0),
+ *                            key (lo32 seed, hi32 seed));
+ *   U = sum of the eight 16-bit halves of x0..x3, t = 2U - 524280;
+ *   dur[v * ld_dur + s] = b + floor((b * t * noise + 2^39) / 2^40)
+ * in exact 64-bit integer arithmetic; a base outside [1, 2^24] yields 0 (an
+ * invalid duration).  noise must be below 2^20; the relative noise has
+ * standard deviation noise * 2 sqrt(2 (65536^2 - 1) / 3) / 2^40, about
+ * noise * 9.73e-8.  Returns ORC_E_INVAL for n_knobs < 1, knob_block < 1,
+ * scen0 < 0, noise >= 2^20 or ld_dur < n_scen.
+ */
+int oracle_generate(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                    int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
+                    int32_t *dur, int64_t ld_dur, int32_t n_threads);
+
 #ifdef __cplusplus
 }
 #endif

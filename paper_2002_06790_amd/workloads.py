@@ -71,6 +71,10 @@ class Workload:
     # block -> uint16 [n_ops, BLOCK] per-scenario resource of each op, or None
     _place_block: Optional[Callable[[int], np.ndarray]] = dataclasses.field(default=None, repr=False)
     info: dict = dataclasses.field(default_factory=dict)
+    # float64 [n_knobs, n_ops] un-rounded base ns per strategy knob, and the
+    # number of consecutive scenarios that share a knob (on-device generation)
+    _gen_base: Optional[np.ndarray] = dataclasses.field(default=None, repr=False)
+    knob_block: int = 1
 
     @property
     def n_edges(self) -> int:
@@ -140,6 +144,17 @@ class Workload:
             if place is not None:
                 place[:, sel] = self.place_block(int(b))[:, cols]
         return dur, place
+
+    def gen_base(self) -> np.ndarray:
+        """int32 [n_knobs, n_ops] base durations for on-device generation.
+
+        Scenario s (global index) uses knob ``(s // knob_block) % n_knobs``;
+        the generator multiplies the base by a per-(op, scenario) noise
+        factor drawn inside the kernel instead of reading ``durations()``.
+        """
+        if self._gen_base is None:
+            raise ValueError(f"{self.name} has no base table")
+        return _to_ns(np.array(self._gen_base, np.float64, ndmin=2))
 
     def manifest(self) -> dict:
         indeg = np.bincount(self.succ_idx, minlength=self.n_ops) if self.n_ops else np.zeros(0)
@@ -409,7 +424,7 @@ def tiny_dp_mlp(n_scen: int = 1024, seed: int = _SEED_BASE + 1) -> Workload:
     base = _rng(seed, 0).integers(10_000, 1_000_000, size=res.size, endpoint=True).astype(np.float64)
     return Workload("tiny-dp-mlp", res.size, 3, ptr, idx, res, n_scen, seed,
                     _dur_block=lambda b: _noisy(base, _rng(seed, 1, b)),
-                    info=dict(workers=2, layers=3))
+                    info=dict(workers=2, layers=3), _gen_base=base[None, :])
 
 
 def resnet50_ps(n_scen: int = 65536, seed: int = _SEED_BASE + 2, workers: int = 8) -> Workload:
@@ -466,7 +481,7 @@ def resnet50_ps(n_scen: int = 65536, seed: int = _SEED_BASE + 2, workers: int = 
     return Workload("resnet50-ps", res.size, 2 * W + 1, ptr, idx, res, n_scen, seed,
                     _dur_block=lambda b: _noisy(base, _rng(seed, 1, b)),
                     info=dict(workers=W, fwd_ops=len(fwd), bwd_ops=len(bwd),
-                              param_layers=len(layers)))
+                              param_layers=len(layers)), _gen_base=base[None, :])
 
 
 def inception_v3_ring(n_scen: int = 65536, seed: int = _SEED_BASE + 3, devices: int = 4,
@@ -532,7 +547,7 @@ def inception_v3_ring(n_scen: int = 65536, seed: int = _SEED_BASE + 3, devices: 
                     _dur_block=lambda b: _noisy(base, _rng(seed, 1, b)),
                     info=dict(devices=D, buckets=buckets, fwd_ops=len(fwd), bwd_ops=len(bwd),
                               bucket_mb=[float(pbytes[bucket_of == b].sum() / 1e6)
-                                         for b in range(buckets)]))
+                                         for b in range(buckets)]), _gen_base=base[None, :])
 
 
 #: strategy knobs of the BERT workload: (compute batch factor, link GB/s)
@@ -608,17 +623,19 @@ def bert_large_ps(n_scen: int = 262144, seed: int = _SEED_BASE + 4, workers: int
     ptr, idx, res = B.csr()
     comp, comm, cls = np.array(comp), np.array(comm), np.array(cls)
 
+    def knob_base(bf, bw):
+        return np.where(cls == 1, comm / bw, np.where(cls == 0, comp * bf, comp))
+
     def dur_block(b):
-        bf, bw = BERT_KNOBS[(b * BLOCK // 4096) % len(BERT_KNOBS)]
-        base = np.where(cls == 1, comm / bw, np.where(cls == 0, comp * bf, comp))
-        return _noisy(base, _rng(seed, 1, b))
+        return _noisy(knob_base(*BERT_KNOBS[(b * BLOCK // 4096) % len(BERT_KNOBS)]), _rng(seed, 1, b))
 
     assert BLOCK % 4096 == 0 or 4096 % BLOCK == 0
     return Workload("bert-large-ps", res.size, 3 * W, ptr, idx, res, n_scen, seed,
                     _dur_block=dur_block,
                     info=dict(workers=W, buckets=nb, fwd_ops=len(fwd), bwd_ops=len(bwd),
                               knob_block=4096, knobs=BERT_KNOBS,
-                              bucket_mb=[float(x / 1e6) for x in nbytes]))
+                              bucket_mb=[float(x / 1e6) for x in nbytes]),
+                    _gen_base=np.stack([knob_base(bf, bw) for bf, bw in BERT_KNOBS]), knob_block=4096)
 
 
 def random_layered(n_scen: int = 16384, seed: int = _SEED_BASE + 5, levels: int = 200,
@@ -653,7 +670,8 @@ def random_layered(n_scen: int = 16384, seed: int = _SEED_BASE + 5, levels: int 
 
     return Workload("random-layered", n, n_res, ptr, idx, res, n_scen, seed,
                     _dur_block=dur_block, _place_block=place_block,
-                    info=dict(levels=levels, width=width))
+                    info=dict(levels=levels, width=width),
+                    _gen_base=_log_uniform(_rng(seed, 3), 1e3, 1e7, (1, n)))
 
 
 CONFIGS = {

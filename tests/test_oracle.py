@@ -6,6 +6,8 @@ check it: the pins are hand-derived worked examples, closed forms, bounds,
 structural invariants of a FIFO device, metamorphic relations, a library
 shortest-path routine, and two independent brute-force replays (tests/brute.py).
 """
+import os
+
 import numpy as np
 import pytest
 import scipy.sparse
@@ -673,3 +675,134 @@ def test_attribution_status(library):
     assert mk.tolist() == [3, -1, -1] and cops.tolist() == [3, -1, -1]
     assert busy[:, 1:].tolist() == [[0, 0]] and chain[:, 1:].tolist() == [[0, 0]]
     assert path.tolist() == []
+
+
+# ------------------------------------------------- scenario generation pins
+#
+# The generator (oracle.h, oracle_generate) is knob grid x counter-based
+# noise.  Its building block, Philox4x32-10, is pinned by the published
+# known-answer vectors; the round structure it shares with Philox4x64-10 is
+# pinned against numpy's Philox (a 4x64-10 implementation); the integer
+# composition is checked against arbitrary-precision arithmetic, and the
+# noise's distribution against the moments of an 8-term Irwin-Hall sum.
+
+SIGMA_UNIT = 2.0 * np.sqrt(2.0 * (65536.0**2 - 1.0) / 3.0) / 2.0**40  # relative std per unit of noise
+
+
+def _kat():
+    rows = []
+    for line in open(os.path.join(goldens.GOLDEN_DIR, "philox4x32_10.kat")):
+        line = line.split("#", 1)[0].split()
+        if line:
+            rows.append([int(x, 16) for x in line])
+    return rows
+
+
+def test_philox4x32_known_answers(library=None):
+    for row in _kat():
+        out = oracle.philox4x32_10(row[0:4], row[4:6], library=library)
+        assert [int(x) for x in out] == row[6:10]
+
+
+def test_philox4x64_matches_numpy(library=None):
+    rng = np.random.default_rng(11)
+    for _ in range(20):
+        ctr = rng.integers(1, 2**63, size=4, dtype=np.uint64)
+        key = rng.integers(0, 2**63, size=2, dtype=np.uint64)
+        before = ctr.copy()
+        before[0] -= np.uint64(1)  # numpy advances the counter before each block
+        ref = np.random.Philox(counter=before, key=key).random_raw(4)
+        assert np.array_equal(oracle.philox4x64_10(ctr, key, library=library), ref)
+
+
+def _gen_exact(base_row_of, S, v, noise, seed, library=None):
+    """One generated duration with Python integers, from the pinned Philox block."""
+    b = base_row_of(S)[v]
+    if b < 1 or b > 2**24:
+        return 0
+    x = oracle.philox4x32_10([S & 0xFFFFFFFF, S >> 32, v, 0], [seed & 0xFFFFFFFF, seed >> 32],
+                             library=library)
+    U = sum(int(w) & 0xFFFF for w in x) + sum(int(w) >> 16 for w in x)
+    t = 2 * U - 524280
+    return b + ((b * t * noise + 2**39) >> 40)
+
+
+def test_generate_exact_integer_composition(library=None):
+    rng = np.random.default_rng(5)
+    n, K, kb = 7, 3, 5
+    base = rng.integers(1, 2**24, size=(K, n), endpoint=True).astype(np.int32)
+    base[0, 0], base[1, 1], base[2, 2] = 1, 2**24, 2**24  # extremes of the valid range
+    base[0, 3] = 0  # invalid bases give 0
+    base[1, 4] = 2**24 + 1
+    for noise in (0, 1, 102739, 2**20 - 1):
+        for seed in (0, 2**64 - 1, 0x123456789ABCDEF):
+            scen0 = 2**32 - 6  # the counter's high word changes inside the batch
+            S_n = 12
+            got = oracle.generate(base, S_n, kb, noise, seed, scen0=scen0, library=library)
+            for s in range(S_n):
+                S = scen0 + s
+                for v in range(n):
+                    want = _gen_exact(lambda S: base[(S // kb) % K].tolist(), S, v, noise, seed, library)
+                    assert got[v, s] == want, (noise, seed, s, v)
+
+
+def test_generate_knob_grid_without_noise(library=None):
+    n, K, kb = 5, 4, 3
+    base = np.array([[1000 * (k + 1) + v for v in range(n)] for k in range(K)], np.int32)
+    dur = oracle.generate(base, 40, kb, 0, 99, scen0=7, library=library)
+    for s in range(40):
+        k = ((7 + s) // kb) % K
+        assert np.array_equal(dur[:, s], base[k])
+
+
+def test_generate_global_scenario_index(library=None):
+    base = np.arange(1, 9, dtype=np.int32)[None, :] * 10_000
+    full = oracle.generate(base, 300, 16, 102739, 42, library=library)
+    part = oracle.generate(base, 100, 16, 102739, 42, scen0=150, library=library)
+    assert np.array_equal(part, full[:, 150:250])
+    other = oracle.generate(base, 300, 16, 102739, 43, library=library)
+    assert not np.array_equal(other, full)
+
+
+def test_generate_noise_moments(library=None):
+    b, noise = 1_000_000, 102739  # relative sigma 0.01
+    base = np.full((1, 50), b, np.int32)
+    dur = oracle.generate(base, 4000, 1, noise, 2024, library=library).astype(np.float64)
+    r = dur / b - 1.0
+    sigma = noise * SIGMA_UNIT
+    assert abs(sigma - 0.01) < 1e-6
+    N = r.size
+    assert abs(r.mean()) < 4 * sigma / np.sqrt(N)
+    assert abs(r.std() / sigma - 1.0) < 0.01
+    z = (r - r.mean()) / r.std()
+    assert abs((z**3).mean()) < 0.03
+    # excess kurtosis of a sum of 8 uniforms is -6/(5*8) = -0.15
+    assert abs((z**4).mean() - 3.0 + 0.15) < 0.04
+    lim = b * 524280 * noise / 2**40 + 1
+    assert np.abs(dur - b).max() <= lim
+    # neighbouring counters are uncorrelated
+    assert abs(np.corrcoef(r[:, :-1].ravel(), r[:, 1:].ravel())[0, 1]) < 0.02
+    assert abs(np.corrcoef(r[:-1].ravel(), r[1:].ravel())[0, 1]) < 0.02
+
+
+def test_generate_invalid_base_flags_scenario(library=None):
+    g = dict(n=3, n_res=1, succ_ptr=np.array([0, 1, 2, 2], np.int64),
+             succ_idx=np.array([1, 2], np.int32), op_res=np.zeros(3, np.int32), prio=None)
+    base = np.array([[10, 0, 10], [10, 20, 10]], np.int32)
+    dur = oracle.generate(base, 4, 1, 0, 0, library=library)
+    mk, _, st = run(g, dur, library=library)
+    assert list(st) == [ORC_BAD, 0, ORC_BAD, 0]
+    assert list(mk) == [-1, 40, -1, 40]
+
+
+ORC_BAD = oracle.ST_BAD_DUR
+
+
+def test_generate_argument_errors(library=None):
+    base = np.ones((1, 3), np.int32)
+    for kw in (dict(knob_block=0), dict(noise=2**20), dict(scen0=-1)):
+        args = dict(knob_block=1, noise=0, seed=0, scen0=0)
+        args.update(kw)
+        with pytest.raises(oracle.OracleError):
+            oracle.generate(base, 4, args["knob_block"], args["noise"], args["seed"],
+                            scen0=args["scen0"], library=library)

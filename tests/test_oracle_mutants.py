@@ -58,6 +58,18 @@ MUTANTS = [
      "busy_r = J->dur[(int64_t)v * J->ld_dur + s];"),
     ("attr-chain-stops-early", "if (start == 0) break;", "if (start <= d) break;"),
     ("attr-prev-not-recorded", "w->prev[v] = w->last[r];", "w->prev[v] = -1;"),
+    ("philox-multipliers-swapped", "uint64_t p0 = (uint64_t)0xD2511F53u * x0;\n    uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;",
+     "uint64_t p0 = (uint64_t)0xCD9E8D57u * x0;\n    uint64_t p1 = (uint64_t)0xD2511F53u * x2;"),
+    ("philox-key-not-bumped", "    k1 += 0xBB67AE85u;\n", ""),
+    ("philox64-words-crossed", "uint64_t y0 = (uint64_t)(p1 >> 64) ^ x1 ^ k0;", "uint64_t y0 = (uint64_t)(p0 >> 64) ^ x1 ^ k0;"),
+    ("gen-drops-high-halves", "U += (int64_t)(x[i] & 0xFFFFu) + (int64_t)(x[i] >> 16);", "U += 2 * (int64_t)(x[i] & 0xFFFFu);"),
+    ("gen-truncates-not-rounds", "int64_t adj = (q + ((int64_t)1 << 39)) >> 40;", "int64_t adj = q >> 40;"),
+    ("gen-counter-words-swapped", "uint32_t ctr[4] = {(uint32_t)S, (uint32_t)((uint64_t)S >> 32), (uint32_t)v, 0};",
+     "uint32_t ctr[4] = {(uint32_t)S, (uint32_t)v, (uint32_t)((uint64_t)S >> 32), 0};"),
+    ("gen-knob-off-by-one", "int64_t k = (S / knob_block) % n_knobs;", "int64_t k = ((S + 1) / knob_block) % n_knobs;"),
+    ("gen-local-scenario-index", "gen_one(J->base, J->n, J->n_knobs, J->knob_block, J->noise, J->seed, J->scen0 + s, v);",
+     "gen_one(J->base, J->n, J->n_knobs, J->knob_block, J->noise, J->seed, s, v);"),
+    ("gen-accepts-large-base", "if (b < 1 || b > ((int64_t)1 << 24)) return 0;", "if (b < 1) return 0;"),
 ]
 
 
