@@ -228,6 +228,60 @@ int sim_static_run(const sim_static *st, int64_t n_scen, const int32_t *dur, int
                    int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
                    void *stream);
 
+/*
+ * On-device scenario generation.  The paper's simulator exists to evaluate
+ * many parallelisation strategies and configurations quickly (Sec. 1), and
+ * its profiled op times vary by under 1 % of their mean (Sec. 3).  These
+ * calls take a table of base durations per strategy knob instead of a
+ * duration matrix and compute every duration inside the kernels:
+ *   global scenario S = scen0 + s, knob k = (S / knob_block) mod n_knobs,
+ *   b = base[k * n_ops + v];
+ *   (x0, x1, x2, x3) = Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) of
+ *       the counter (lo32 S, hi32 S, v, 0) under the key (lo32 seed, hi32 seed);
+ *   U = the sum of the eight 16-bit halves of x0..x3, t = 2U - 524280;
+ *   d(v, s) = b + floor((b * t * noise + 2^39) / 2^40)
+ * in exact integer arithmetic, so every call, kernel and host reproduces the
+ * same durations.  The relative noise has mean 0 and standard deviation
+ * noise * 2 sqrt(2 (65536^2 - 1) / 3) / 2^40 (about noise * 9.7334e-8;
+ * noise = 102739 gives 1 %); its shape is an 8-term Irwin-Hall sum (bounded,
+ * nearly normal).  Durations then follow the sim_run_batch rules; a base
+ * outside [1, SIM_GEN_BASE_MAX] yields d = 0, reported as SIM_ST_BAD_DUR.
+ * Common arguments:
+ *   base       device int32 [n_knobs][n_ops] (caller-owned, read only).
+ *   n_knobs    >= 1; knob_block >= 1 (scenarios sharing a knob).
+ *   noise      < SIM_GEN_NOISE_MAX (so that d >= b / 2 >= 1); 0: no noise.
+ *   seed       the Philox key.
+ *   scen0      >= 0: global index of scenario 0, so a sweep split over calls
+ *              (or devices) generates the same scenarios as one call.
+ * Any other value returns SIM_E_INVAL before anything is enqueued, as does
+ * scen0 + n_scen > INT64_MAX.  Asynchronous on `stream`; no memory is
+ * allocated.
+ */
+#define SIM_GEN_BASE_MAX (1 << 24)
+#define SIM_GEN_NOISE_MAX (1u << 20)
+
+/* Write the generated durations: dur device int32 [n_ops][ld_dur], ld_dur >= n_scen. */
+int sim_generate(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                 int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0, int32_t *dur,
+                 int64_t ld_dur, void *stream);
+
+/* sim_run_batch on generated durations, without placement; makespan, finish,
+ * ld_fin, status and stream as there.  flags: SIM_ALGO_AUTO or SIM_ALGO_EVENT
+ * (the event kernel; other values return SIM_E_INVAL).  Calls on different
+ * streams sharing one graph must not overlap in time. */
+int sim_run_generated(const sim_graph *g, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                      int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
+                      int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                      uint32_t flags, void *stream);
+
+/* sim_critical_path on generated durations; cp_len, path_scen, path_ops,
+ * path_cap, path_len and stream as there (a path request synchronises
+ * `stream`). */
+int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, const int32_t *base,
+                                int32_t n_knobs, int64_t knob_block, uint32_t noise, uint64_t seed,
+                                int64_t scen0, int32_t *cp_len, int64_t path_scen, int32_t *path_ops,
+                                int32_t path_cap, int32_t *path_len, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

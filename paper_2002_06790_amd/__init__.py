@@ -28,7 +28,13 @@ ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
            "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
-           "sim_static_destroy", "sim_static_run", "sim_attribute")
+           "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
+           "sim_critical_path_generated")
+
+#: generator limits (include/mlsim.h): largest base duration, noise bound
+SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
+#: relative standard deviation of the generated noise per unit of ``noise``
+GEN_SIGMA_UNIT = 2.0 * (2.0 * (65536.0**2 - 1.0) / 3.0) ** 0.5 / 2.0**40
 
 _lib = None
 
@@ -79,6 +85,13 @@ def _load():
     L.sim_static_run.restype = ctypes.c_int
     L.sim_attribute.argtypes = [P, I64, P, I64, P, I64, P, P, P, P, I64, P, P, I64, P, I64, P, I32, P, P]
     L.sim_attribute.restype = ctypes.c_int
+    U64 = ctypes.c_uint64
+    L.sim_generate.argtypes = [I32, I64, P, I32, I64, U32, U64, I64, P, I64, P]
+    L.sim_generate.restype = ctypes.c_int
+    L.sim_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, U32, P]
+    L.sim_run_generated.restype = ctypes.c_int
+    L.sim_critical_path_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, I64, P, I32, P, P]
+    L.sim_critical_path_generated.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -108,6 +121,51 @@ def _dev_matrix(t, dtype, n_ops, what):
     if t.shape[1] > 1 and t.stride(1) != 1:
         raise ValueError(f"{what} must have unit stride along scenarios")
     return t.data_ptr(), max(t.stride(0), t.shape[1])
+
+
+def noise_for_sigma(sigma: float) -> int:
+    """The generator's ``noise`` argument for a relative standard deviation."""
+    noise = int(round(sigma / GEN_SIGMA_UNIT))
+    if not 0 <= noise < SIM_GEN_NOISE_MAX:
+        raise ValueError(f"sigma {sigma} outside the generator's range")
+    return noise
+
+
+class Gen:
+    """Parameters of on-device scenario generation (include/mlsim.h).
+
+    ``base``: int32 [n_knobs, n_ops] device tensor of base durations per
+    strategy knob; global scenario S uses knob ``(S // knob_block) % n_knobs``
+    and multiplies each base by counter-based noise of relative standard
+    deviation ``noise * GEN_SIGMA_UNIT`` keyed by ``seed``; ``scen0`` is the
+    global index of the call's first scenario.
+    """
+
+    def __init__(self, base, knob_block: int = 1, noise: int = 0, seed: int = 0, scen0: int = 0):
+        import torch
+        if not isinstance(base, torch.Tensor) or not base.is_cuda or base.dtype != torch.int32:
+            raise TypeError("base must be an int32 torch tensor on the GPU")
+        if base.dim() == 1:
+            base = base[None, :]
+        self.base = base.contiguous()
+        self.n_knobs, self.n_ops = int(self.base.shape[0]), int(self.base.shape[1])
+        self.knob_block, self.noise, self.seed, self.scen0 = int(knob_block), int(noise), int(seed), int(scen0)
+
+    def args(self):
+        return (self.base.data_ptr(), self.n_knobs, self.knob_block, self.noise,
+                self.seed & (2**64 - 1), self.scen0)
+
+
+def generate(gen: Gen, n_scen: int, out=None, stream=None):
+    """The generated durations, int32 [n_ops, n_scen] on the GPU (sim_generate)."""
+    import torch
+    if out is None:
+        out = torch.empty((gen.n_ops, n_scen), dtype=torch.int32, device=gen.base.device)
+    optr, ld = _dev_matrix(out, torch.int32, gen.n_ops, "out")
+    rc = _load().sim_generate(gen.n_ops, n_scen, *gen.args(), optr, ld, _stream_ptr(stream))
+    if rc:
+        raise SimError(rc, "sim_generate")
+    return out
 
 
 def _stream_ptr(stream):
@@ -189,6 +247,47 @@ class Graph:
         if rc:
             raise SimError(rc, "sim_run_batch")
         return makespan, finish, status
+
+    def run_generated(self, gen: Gen, n_scen: int, want_finish: bool = False, algo: str = "auto",
+                      makespan=None, finish=None, status=None, stream=None):
+        """Replay ``n_scen`` scenarios whose durations the kernel generates
+        from ``gen`` (sim_run_generated); returns ``(makespan, finish or
+        None, status)`` as device tensors."""
+        import torch
+        if gen.n_ops != self.n_ops:
+            raise ValueError("base table does not match the graph's op count")
+        dev = gen.base.device
+        if makespan is None:
+            makespan = torch.empty(n_scen, dtype=torch.int32, device=dev)
+        if status is None:
+            status = torch.empty(n_scen, dtype=torch.int32, device=dev)
+        if want_finish and finish is None:
+            finish = torch.empty((self.n_ops, n_scen), dtype=torch.int32, device=dev)
+        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        rc = _load().sim_run_generated(self._h, n_scen, *gen.args(), makespan.data_ptr(), fptr, ldf,
+                                       status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_run_generated")
+        return makespan, finish, status
+
+    def critical_path_generated(self, gen: Gen, n_scen: int, path_scen: int = -1, cp_len=None,
+                                stream=None):
+        """Longest path per generated scenario (sim_critical_path_generated)."""
+        import torch
+        if gen.n_ops != self.n_ops:
+            raise ValueError("base table does not match the graph's op count")
+        if cp_len is None:
+            cp_len = torch.empty(n_scen, dtype=torch.int32, device=gen.base.device)
+        cap = max(self.n_ops, 1)
+        path = np.empty(cap, np.int32)
+        plen = np.zeros(1, np.int32)
+        want = path_scen >= 0
+        rc = _load().sim_critical_path_generated(self._h, n_scen, *gen.args(), cp_len.data_ptr(), path_scen,
+                                                 path.ctypes.data if want else None, cap if want else 0,
+                                                 plen.ctypes.data if want else None, _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_critical_path_generated")
+        return cp_len, (path[: int(plen[0])].copy() if want else None)
 
     def static_order(self, order) -> "StaticReplay":
         """A static-order replay of this graph: every resource runs its ops

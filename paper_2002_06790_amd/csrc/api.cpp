@@ -13,6 +13,53 @@ bool bad_matrix(const void *p, int64_t ld, int64_t n_scen, int32_t n_ops) {
   return n_ops > 0 && n_scen > 0 && (!p || ld < n_scen);
 }
 
+// Generation parameters, checked: SIM_OK or SIM_E_INVAL.
+int make_gen(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs, int64_t knob_block,
+             uint32_t noise, uint64_t seed, int64_t scen0, DurGen &gen) {
+  if (n_knobs < 1 || knob_block < 1 || scen0 < 0 || noise >= kGenNoiseMax) return SIM_E_INVAL;
+  if (n_scen > INT64_MAX - scen0) return SIM_E_INVAL;
+  if (n_ops > 0 && !base) return SIM_E_INVAL;
+  if ((int64_t)n_knobs * n_ops > INT64_MAX / 4) return SIM_E_INVAL;
+  gen = DurGen{base, n_ops, n_knobs, knob_block, scen0, noise, (uint32_t)seed, (uint32_t)(seed >> 32)};
+  return SIM_OK;
+}
+
+// Walk back from the lowest-id op of maximum dist, each time to the
+// lowest-id predecessor p with dist(p) = dist(v) - d(v); the path from its
+// first op to its last goes to path_ops (up to path_cap), its length to
+// *path_len.
+void walk_critical_path(const sim_graph *g, const std::vector<int32_t> &dist, const std::vector<int32_t> &d,
+                        int32_t cp_s, int32_t *path_ops, int32_t path_cap, int32_t *path_len) {
+  const int32_t n = g->n_ops;
+  if (cp_s < 0) {
+    *path_len = 0;
+    return;
+  }
+  std::vector<int32_t> comp(n);
+  for (int32_t c = 0; c < n; ++c) comp[g->h_orig_of[c]] = c;
+  int32_t v = -1;
+  for (int32_t o = 0; o < n; ++o)
+    if (dist[o] == cp_s) {
+      v = o;
+      break;
+    }
+  std::vector<int32_t> rev;
+  while (v >= 0) {
+    rev.push_back(v);
+    const int32_t want = dist[v] - d[v];
+    if (want == 0) break;
+    int32_t nxt = -1;
+    const int32_t c = comp[v];
+    for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k) {
+      const int32_t p = g->h_orig_of[g->h_pred[k]];
+      if (dist[p] == want && (nxt < 0 || p < nxt)) nxt = p;
+    }
+    v = nxt;
+  }
+  *path_len = (int32_t)rev.size();
+  for (int32_t k = 0; k < (int32_t)rev.size() && k < path_cap; ++k) path_ops[k] = rev[rev.size() - 1 - k];
+}
+
 }  // namespace
 
 extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
@@ -71,33 +118,75 @@ extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32
       hipMemcpyAsync(&cp_s, cp_len + path_scen, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipStreamSynchronize(st) != hipSuccess)
     return SIM_E_HIP;
-  if (cp_s < 0) {
-    *path_len = 0;
+  walk_critical_path(g, dist, d, cp_s, path_ops, path_cap, path_len);
+  return SIM_OK;
+}
+
+extern "C" int sim_generate(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                            int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
+                            int32_t *dur, int64_t ld_dur, void *stream) {
+  if (n_ops < 0 || n_scen < 0) return SIM_E_INVAL;
+  DurGen gen;
+  if (int rc = make_gen(n_ops, n_scen, base, n_knobs, knob_block, noise, seed, scen0, gen)) return rc;
+  if (n_ops == 0 || n_scen == 0) return SIM_OK;
+  if (bad_matrix(dur, ld_dur, n_scen, n_ops)) return SIM_E_INVAL;
+  return launch_generate(gen, n_scen, dur, ld_dur, (hipStream_t)stream);
+}
+
+extern "C" int sim_run_generated(const sim_graph *g, int64_t n_scen, const int32_t *base, int32_t n_knobs,
+                                 int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
+                                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                                 uint32_t flags, void *stream) {
+  if (!g || n_scen < 0 || (flags != SIM_ALGO_AUTO && flags != SIM_ALGO_EVENT)) return SIM_E_INVAL;
+  DurGen gen;
+  if (int rc = make_gen(g->n_ops, n_scen, base, n_knobs, knob_block, noise, seed, scen0, gen)) return rc;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (g->n_ops == 0) {
+    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
     return SIM_OK;
   }
-  std::vector<int32_t> comp(n);
-  for (int32_t c = 0; c < n; ++c) comp[g->h_orig_of[c]] = c;
-  int32_t v = -1;
-  for (int32_t o = 0; o < n; ++o)
-    if (dist[o] == cp_s) {
-      v = o;
-      break;
-    }
-  std::vector<int32_t> rev;
-  while (v >= 0) {
-    rev.push_back(v);
-    const int32_t want = dist[v] - d[v];
-    if (want == 0) break;
-    int32_t nxt = -1;
-    const int32_t c = comp[v];
-    for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k) {
-      const int32_t p = g->h_orig_of[g->h_pred[k]];
-      if (dist[p] == want && (nxt < 0 || p < nxt)) nxt = p;
-    }
-    v = nxt;
+  return launch_event_gen(g, n_scen, gen, makespan, finish, ld_fin, status, st);
+}
+
+extern "C" int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, const int32_t *base,
+                                           int32_t n_knobs, int64_t knob_block, uint32_t noise,
+                                           uint64_t seed, int64_t scen0, int32_t *cp_len,
+                                           int64_t path_scen, int32_t *path_ops, int32_t path_cap,
+                                           int32_t *path_len, void *stream) {
+  if (!g || n_scen < 0) return SIM_E_INVAL;
+  if (path_scen >= n_scen || path_scen < -1) return SIM_E_INVAL;
+  if (path_scen >= 0 && (!path_len || (path_cap > 0 && !path_ops) || path_cap < 0)) return SIM_E_INVAL;
+  DurGen gen;
+  if (int rc = make_gen(g->n_ops, n_scen, base, n_knobs, knob_block, noise, seed, scen0, gen)) return rc;
+  if (n_scen == 0) return SIM_OK;
+  if (!cp_len) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  const int32_t n = g->n_ops;
+  if (n == 0) {
+    if (hipMemsetAsync(cp_len, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (path_scen >= 0) *path_len = 0;
+    return SIM_OK;
   }
-  *path_len = (int32_t)rev.size();
-  for (int32_t k = 0; k < (int32_t)rev.size() && k < path_cap; ++k) path_ops[k] = rev[rev.size() - 1 - k];
+  int32_t *dist_dev = path_scen >= 0 ? (int32_t *)((char *)g->scratch + g->scratch_dist_off) : nullptr;
+  int rc = launch_cp(g, n_scen, nullptr, 0, cp_len, dist_dev, path_scen, st, &gen);
+  if (rc || path_scen < 0) return rc;
+  // the path scenario's durations, generated once more into scratch
+  int32_t *dcol = (int32_t *)((char *)g->scratch + g->scratch_gen_off);
+  DurGen one = gen;
+  one.scen0 = gen.scen0 + path_scen;
+  if ((rc = launch_generate(one, 1, dcol, 1, st))) return rc;
+  std::vector<int32_t> dist(n), d(n);
+  int32_t cp_s = 0;
+  if (hipMemcpyAsync(dist.data(), dist_dev, (size_t)n * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(d.data(), dcol, (size_t)n * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(&cp_s, cp_len + path_scen, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return SIM_E_HIP;
+  walk_critical_path(g, dist, d, cp_s, path_ops, path_cap, path_len);
   return SIM_OK;
 }
 

@@ -11,6 +11,7 @@
 #include <cstdlib>
 #include <cstring>
 
+#include "philox.hpp"
 #include "regarr.hpp"
 #include "sim.hpp"
 
@@ -276,17 +277,19 @@ struct EvArgs {
   int32_t list_cap;
   int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
   int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
+  DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
 
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
-template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, class RfGet, class RfSet,
-          class LastXchg, class Flush>
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class RfGet,
+          class RfSet, class LastXchg, class Flush>
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
                                            int &end, int2 *jst, int it, int64_t s,
-                                           int64_t sc, uint32_t &st, uint32_t &span,
+                                           int64_t sc, const int32_t *brow, uint32_t s_lo,
+                                           uint32_t s_hi, uint32_t &st, uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
                                            int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
                                            LastXchg last_xchg, Flush flush) {
@@ -302,7 +305,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
   int32_t d = 0;
   int rp = 0;
   if (ROW_ID) {
-    d = a.dur[(int64_t)c * a.ld_dur + sc];
+    d = GEN ? brow[c] : a.dur[(int64_t)c * a.ld_dur + sc];
     if (PLACE) rp = a.place[(int64_t)c * a.ld_place + sc];
   }
   HeapAhead A;
@@ -311,9 +314,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
   __builtin_amdgcn_sched_barrier(0);
   const int32_t row = ROW_ID ? c : r0.x;
   if (!ROW_ID) {
-    d = a.dur[(int64_t)row * a.ld_dur + sc];
+    d = GEN ? brow[row] : a.dur[(int64_t)row * a.ld_dur + sc];
     if (PLACE) rp = a.place[(int64_t)row * a.ld_place + sc];
   }
+  if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)row, a.gen.key0, a.gen.key1, a.gen.noise);
   int r = PLACE ? rp : r0.y;
   if (PLACE && r >= R) {
     st |= SIM_ST_BAD_RES;
@@ -390,8 +394,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
 // compact ids, so the duration row is known as soon as the op is popped.
 // PLACE: resources come from the per-scenario placement matrix.  Finish times
 // are written in bursts of kFinQ stores per lane, so their completion is
-// waited for once per burst instead of once per step.
-template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV>
+// waited for once per burst instead of once per step.  GEN: durations are
+// generated from the knob grid and counter-based noise of a.gen instead of
+// read from a.dur.
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -441,6 +447,9 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     if (a.retry == 1 && !__ballot(active)) continue;  // nothing to replay in this tile
     const int64_t sc = in_range || a.retry == 2 ? s : a.n_scen - 1;
     const bool store_fin = a.finish && active;
+    const int64_t S = GEN ? a.gen.scen0 + sc : 0;  // global scenario index of the generator
+    const int32_t *brow = GEN ? gen_knob_row(a.gen, S) : nullptr;
+    const uint32_t s_lo = (uint32_t)S, s_hi = (uint32_t)((uint64_t)S >> 32);
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     if (PREV)
       for (int r = 0; r < R; ++r) {
@@ -467,11 +476,13 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
       if (__ballot(end > heap.le))
-        event_step<true, RF_LDS, ROW_ID, PLACE, PREV>(G, a, heap, end, jst, it, s, sc, st, span, fq, rq,
-                                                      pq, rf_get, rf_set, last_xchg, flush);
+        event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jst, it, s, sc, brow, s_lo, s_hi,
+                                                           st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
+                                                           flush);
       else
-        event_step<false, RF_LDS, ROW_ID, PLACE, PREV>(G, a, heap, end, jst, it, s, sc, st, span, fq,
-                                                       rq, pq, rf_get, rf_set, last_xchg, flush);
+        event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jst, it, s, sc, brow, s_lo,
+                                                            s_hi, st, span, fq, rq, pq, rf_get, rf_set,
+                                                            last_xchg, flush);
     }
     flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
@@ -493,6 +504,7 @@ struct MpArgs {
   int32_t *dist_out;  // dist of every op (by caller id) for scenario dist_scen, or null
   int64_t dist_scen;
   uint32_t *slots_g;  // [blocks][slots][64] when slots are not in LDS
+  DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
 };
 
 // Max-plus sweep, one scenario per lane: dist(v) = d(v) + max over v's
@@ -509,8 +521,10 @@ struct MpArgs {
 // numbers (for its loads) and its fields (for its sweep) by readlane.  MODE:
 // where the value slots live (kCpSlotsLds or kCpSlotsGlobal); OUT: what
 // besides the per-scenario result is written (kMpOutFinish: every op's dist
-// as finish rows; kMpOutDist: every op's dist for one scenario).
-template <int MODE, int OUT>
+// as finish rows; kMpOutDist: every op's dist for one scenario).  GEN: a
+// batch's "rows" are base durations of the lane's knob, and the sweep turns
+// them into durations with the counter-based noise of a.gen.
+template <int MODE, int OUT, bool GEN = false>
 __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
@@ -532,6 +546,9 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
     const bool active = s < a.n_scen;
     const int64_t sc = active ? s : a.n_scen - 1;
     const bool want_dist = OUT == kMpOutDist && s == a.dist_scen;
+    const int64_t S = GEN ? a.gen.scen0 + sc : 0;  // global scenario index of the generator
+    const int32_t *brow = GEN ? gen_knob_row(a.gen, S) : nullptr;
+    const uint32_t s_lo = (uint32_t)S, s_hi = (uint32_t)((uint64_t)S >> 32);
     uint32_t mx = 0;
     bool bad_dur = false, ovf = false;
     int32_t rx0, rx1;  // records of one batch in flight
@@ -551,7 +568,7 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
       for (int u = 0; u < kCpBatch; ++u) {
         const int w = u * kRecWords;  // word of the batch holding the row
         const uint32_t row = (uint32_t)__builtin_amdgcn_readlane(w < kWave ? y0 : y1, w & (kWave - 1));
-        dv[u] = a.dur[(uint64_t)row * (uint64_t)a.ld_dur + sc];  // rows are never negative
+        dv[u] = GEN ? brow[row] : a.dur[(uint64_t)row * (uint64_t)a.ld_dur + sc];  // rows are never negative
       }
     };
     auto sweep = [&](int t, const int32_t (&dv)[kCpBatch]) {
@@ -580,6 +597,7 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
           }
         }
         int32_t d = dv[u];
+        if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)CP_FIELD(u, 0), a.gen.key0, a.gen.key1, a.gen.noise);
         if (d < 1) {
           bad_dur = true;
           d = 1;
@@ -944,6 +962,11 @@ int plan_scratch(sim_graph *g) {
                                  : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
   P.ev_prev_blocks = std::max(1, std::min(ev_prev_occ, P.ev_blocks));
+  // the event kernel with generated durations: same LDS and scratch per block
+  const int ev_gen_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus)
+                                : occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
+  if (ev_gen_occ < 0) return SIM_E_HIP;
+  P.ev_gen_blocks = std::max(1, std::min(ev_gen_occ, P.ev_blocks));
   // attribution chains: busy and chain accumulators in LDS when they fit
   const size_t at_bytes = (size_t)2 * G.R * kWave * 4;
   P.at_lds = at_bytes <= 64 * 1024;
@@ -964,11 +987,13 @@ int plan_scratch(sim_graph *g) {
     if (!strcmp(e, "global")) P.cp_mode = kCpSlotsGlobal;
   P.cp_lds_bytes = cp_ring + (P.cp_mode == kCpSlotsLds ? cp_bytes : 0);
   const int cp_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus);
-  if (cp_occ < 0) return SIM_E_HIP;
+  const int cp_gen_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus, true);
+  if (cp_occ < 0 || cp_gen_occ < 0) return SIM_E_HIP;
   size_t cp_blocks = (size_t)cp_occ;
   if (P.cp_mode == kCpSlotsGlobal && cp_bytes)
     cp_blocks = std::min(cp_blocks, std::max<size_t>(1, kScratchBudget / cp_bytes));
   P.cp_blocks = (int32_t)cp_blocks;
+  P.cp_gen_blocks = (int32_t)std::min<size_t>(cp_blocks, (size_t)cp_gen_occ);
   // sweep variant: per-op state and per-resource state in LDS when small
   const size_t val_bytes = (size_t)G.n * kWave * 4;
   const size_t res_bytes = (size_t)G.R * kWave * 20;
@@ -1003,6 +1028,7 @@ int plan_scratch(sim_graph *g) {
   g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
+  g->scratch_gen_off = take((size_t)std::max(G.n, 1) * 4);  // one generated duration column
   {
     const int rc = plan_walk(g, cus);
     if (rc) return rc;
@@ -1036,28 +1062,37 @@ namespace {
 int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
-                      const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream) {
+                      const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream,
+                      const DurGen *gen = nullptr) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
-           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off)};
+           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}};
+  if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
   // when the last round of tiles would fill less than half the grid, use
   // fewer blocks that each take the same number of tiles (within one)
-  const int64_t blocks = prev ? P.ev_prev_blocks : P.ev_blocks;
+  const int64_t blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : P.ev_blocks;
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
   const size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
-  const int variant = (prev ? 8 : 0) | (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+  const int variant = (gen ? 16 : 0) | (prev ? 8 : 0) | (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) |
+                      (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
+#define EV_GEN_CASE(V, A, B) \
+  case V: k_event<A, B, false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
+    EV_GEN_CASE(16, false, false)
+    EV_GEN_CASE(18, false, true)
+    EV_GEN_CASE(20, true, false)
+    EV_GEN_CASE(22, true, true)
     EV_CASE(0, false, false, false, false)
     EV_CASE(1, false, false, true, false)
     EV_CASE(2, false, true, false, false)
@@ -1076,9 +1111,37 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
     default: k_event<true, true, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   }
 #undef EV_CASE
+#undef EV_GEN_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
+
+// Generated durations written out: dur[v * ld + s] for every op and scenario
+// (one thread per scenario column, blocks striding over ops; each store row
+// of a block is 1 KB contiguous).
+__global__ __launch_bounds__(256) void k_generate(DurGen gen, int64_t n_scen, int32_t *dur, int64_t ld) {
+  const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (s >= n_scen) return;
+  const int64_t S = gen.scen0 + s;
+  const int32_t *brow = gen_knob_row(gen, S);
+  const uint32_t s_lo = (uint32_t)S, s_hi = (uint32_t)((uint64_t)S >> 32);
+  for (int32_t v = blockIdx.y; v < gen.n_ops; v += gridDim.y)
+    dur[(int64_t)v * ld + s] = gen_duration(brow[v], s_lo, s_hi, (uint32_t)v, gen.key0, gen.key1, gen.noise);
+}
 }  // namespace
+
+int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream) {
+  const int64_t xb = (n_scen + 255) / 256;
+  // enough blocks to fill the chip several times over, each op row once
+  const int64_t yb = std::min<int64_t>(gen.n_ops, std::max<int64_t>(1, 8192 / xb));
+  k_generate<<<dim3((unsigned)xb, (unsigned)yb), dim3(256), 0, stream>>>(gen, n_scen, dur, ld);
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
+                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  return launch_event_impl(g, n_scen, nullptr, 0, nullptr, 0, makespan, finish, ld_fin, status, 0, nullptr,
+                           nullptr, 0, nullptr, stream, &gen);
+}
 
 int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
@@ -1106,7 +1169,14 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                            1, list, list_count, list_cap, nullptr, stream);
 }
 
-int maxplus_occupancy(int mode, bool fin, size_t lds, int cus) {
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen) {
+  if (gen) {
+    if (mode == kCpSlotsLds)
+      return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutFinish, true>, lds, cus)
+                 : occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutNone, true>, lds, cus);
+    return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutFinish, true>, lds, cus)
+               : occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutNone, true>, lds, cus);
+  }
   if (mode == kCpSlotsLds)
     return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutFinish>, lds, cus)
                : occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutNone>, lds, cus);
@@ -1117,13 +1187,19 @@ int maxplus_occupancy(int mode, bool fin, size_t lds, int cus) {
 int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
                    const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
                    int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
-                   uint32_t *slots_g, hipStream_t stream) {
-  MpArgs a{n_scen, dur, ld_dur, out, status, finish, ld_fin, dist_out, dist_scen, slots_g};
+                   uint32_t *slots_g, hipStream_t stream, const DurGen *gen) {
+  MpArgs a{n_scen, dur, ld_dur, out, status, finish, ld_fin, dist_out, dist_scen, slots_g, DurGen{}};
+  if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const dim3 grid((unsigned)std::min<int64_t>(tiles, max_blocks)), blk(kWave);
   const int out_kind = finish ? kMpOutFinish : dist_out ? kMpOutDist : kMpOutNone;
 #define MP_CASE(M, O) \
-  if (mode == M && out_kind == O) k_maxplus<M, O><<<grid, blk, lds, stream>>>(T, a);
+  if (mode == M && out_kind == O) {                                  \
+    if (gen)                                                         \
+      k_maxplus<M, O, true><<<grid, blk, lds, stream>>>(T, a);       \
+    else                                                             \
+      k_maxplus<M, O><<<grid, blk, lds, stream>>>(T, a);             \
+  }
   MP_CASE(kCpSlotsLds, kMpOutNone)
   MP_CASE(kCpSlotsLds, kMpOutFinish)
   MP_CASE(kCpSlotsLds, kMpOutDist)
@@ -1135,12 +1211,13 @@ int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64
 }
 
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream) {
+              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
+              const DurGen *gen) {
   const ScratchPlan &P = g->plan;
   const MpTable T{g->dg.n, g->dg.cp_slots, g->dg.cp, g->dg.cp_pred};
-  return launch_maxplus(T, P.cp_mode, P.cp_blocks, P.cp_lds_bytes, n_scen, dur, ld_dur, cp_len, nullptr,
-                        nullptr, 0, dist_out, dist_scen,
-                        (uint32_t *)((char *)g->scratch + g->scratch_cp_off), stream);
+  return launch_maxplus(T, P.cp_mode, gen ? P.cp_gen_blocks : P.cp_blocks, P.cp_lds_bytes, n_scen, dur,
+                        ld_dur, cp_len, nullptr, nullptr, 0, dist_out, dist_scen,
+                        (uint32_t *)((char *)g->scratch + g->scratch_cp_off), stream, gen);
 }
 
 int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

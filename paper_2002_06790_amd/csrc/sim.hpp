@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "mlsim.h"
+#include "philox.hpp"
 
 namespace mlsim {
 
@@ -148,6 +149,8 @@ struct ScratchPlan {
   // attribution: the event kernel with each op's predecessor on its resource
   // (its last-op table beside the resource times), then the chain kernel
   int32_t ev_prev_blocks, at_blocks, at_lds;
+  // generated durations: persistent grids of the event and critical-path kernels
+  int32_t ev_gen_blocks, cp_gen_blocks;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
   int32_t wk_ok;
@@ -172,7 +175,7 @@ struct sim_graph {
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
-  size_t scratch_ev_last_off, scratch_at_off;
+  size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off;
   // host copies: critical-path recovery (compact predecessor CSR and the
   // caller id of each compact id) and static-order compilation (resource of
   // each op by caller id)
@@ -198,7 +201,12 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
                        const int32_t *list, const int32_t *list_count, int32_t list_cap,
                        hipStream_t stream);
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream);
+              int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
+              const DurGen *gen = nullptr);
+// generated durations: written out, or consumed by the event replay
+int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream);
+int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
+                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 // attribution: the event replay that also records each op's predecessor on
 // its resource, and the busy-time / binding-chain kernel over its outputs
 int launch_event_prev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
@@ -210,11 +218,11 @@ int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t 
                 int32_t *chain_ops, hipStream_t stream);
 // the max-plus sweep on any table: blocks resident per launch for a slot mode
 // and LDS size, and the launch itself (finish != null writes finish rows)
-int maxplus_occupancy(int mode, bool fin, size_t lds, int cus);
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen = false);
 int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
                    const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
                    int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
-                   uint32_t *slots_g, hipStream_t stream);
+                   uint32_t *slots_g, hipStream_t stream, const DurGen *gen = nullptr);
 // Records of a max-plus sweep over ops 0..n-1 (duration row of op v:
 // row_of[v]) with the given successor and predecessor lists: a topological
 // order, its value slots and the padded records.  False on a cycle.

@@ -66,3 +66,36 @@ def test_graph_errors_without_gpu(L):
 def test_run_argument_errors_without_gpu(L):
     assert L.sim_run_batch(None, 1, None, 1, None, 0, None, None, 0, None, 0, None) == mlsim.SIM_E_INVAL
     assert L.sim_critical_path(None, 1, None, 1, None, -1, None, 0, None, None) == mlsim.SIM_E_INVAL
+
+
+def test_generate_argument_errors_without_gpu(L):
+    """Generator parameters are checked on the host before any HIP call."""
+    base = ctypes.c_void_p(16)  # never dereferenced: every call below fails its checks first
+    out = ctypes.c_void_p(16)
+    ok = dict(n_knobs=1, knob_block=1, noise=0, seed=0, scen0=0)
+
+    def gen(n_ops=4, n_scen=8, ld=8, **kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.sim_generate(n_ops, n_scen, base, a["n_knobs"], a["knob_block"], a["noise"], a["seed"],
+                              a["scen0"], out, ld, None)
+
+    assert gen(n_knobs=0) == mlsim.SIM_E_INVAL
+    assert gen(knob_block=0) == mlsim.SIM_E_INVAL
+    assert gen(noise=mlsim.SIM_GEN_NOISE_MAX) == mlsim.SIM_E_INVAL
+    assert gen(scen0=-1) == mlsim.SIM_E_INVAL
+    assert gen(scen0=2**63 - 4) == mlsim.SIM_E_INVAL  # scen0 + n_scen beyond int64
+    assert gen(ld=7) == mlsim.SIM_E_INVAL
+    assert gen(n_ops=-1) == mlsim.SIM_E_INVAL
+    assert gen(n_scen=0) == mlsim.SIM_OK  # nothing to do
+    assert gen(n_ops=0) == mlsim.SIM_OK
+    assert L.sim_run_generated(None, 1, base, 1, 1, 0, 0, 0, out, None, 0, None, 0, None) == mlsim.SIM_E_INVAL
+    assert L.sim_critical_path_generated(None, 1, base, 1, 1, 0, 0, 0, out, -1, None, 0, None,
+                                         None) == mlsim.SIM_E_INVAL
+
+
+def test_noise_for_sigma():
+    assert mlsim.noise_for_sigma(0.0) == 0
+    assert mlsim.noise_for_sigma(0.01) == 102739
+    with pytest.raises(ValueError):
+        mlsim.noise_for_sigma(0.2)
