@@ -7,8 +7,9 @@ One step = one pass of the whole hot path over one batch: ``sim_run_batch``
 resident before the timed region starts.  Prints one JSON line.  Outside the
 step it also times the static-order replay (every resource running its ops
 in the order the event replay ran them in scenario 0), the bottleneck
-attribution and, on a bounded sample, the CPU oracle, whose outputs check
-sampled GPU results.
+attribution, the replay and critical path on durations generated inside the
+kernels (knob table x counter-based noise) and, on a bounded sample, the CPU
+oracle, whose outputs check sampled GPU results.
 
 Default workload: the BERT-large data-parallel graph (16 workers, per-worker
 up/down links; 6624 ops, 48 resources) at 262144 scenarios spanning 12
@@ -154,6 +155,28 @@ def main():
         at_ms.append(e0.elapsed_time(e1))
     del at
     log(f"attribution {np.mean(at_ms):.3f} ms")
+    # on-device scenario generation (outside the step): the same hot path with
+    # every duration computed in the kernels from the workload's knob table
+    # and 1 % counter-based noise instead of read from HBM
+    gen = mlsim.Gen(torch.from_numpy(w.gen_base()).cuda(), knob_block=w.knob_block,
+                    noise=mlsim.noise_for_sigma(0.01), seed=w.seed)
+    gmk = torch.empty(S, dtype=torch.int32, device="cuda")
+    gst = torch.empty(S, dtype=torch.int32, device="cuda")
+    gcp = torch.empty(S, dtype=torch.int32, device="cuda")
+    g.run_generated(gen, S, makespan=gmk, finish=finish, status=gst)
+    g.critical_path_generated(gen, S, cp_len=gcp)
+    torch.cuda.synchronize()
+    gev_ms, gcp_ms = [], []
+    for _ in range(args.steps):
+        e0.record()
+        g.run_generated(gen, S, makespan=gmk, finish=finish, status=gst)
+        e1.record()
+        g.critical_path_generated(gen, S, cp_len=gcp)
+        e2.record()
+        e2.synchronize()
+        gev_ms.append(e0.elapsed_time(e1))
+        gcp_ms.append(e1.elapsed_time(e2))
+    log(f"generated: run {np.mean(gev_ms):.3f} ms, critical path {np.mean(gcp_ms):.3f} ms")
     # the step's outputs again (the static replay reused the buffers)
     step()
     torch.cuda.synchronize()
@@ -189,6 +212,21 @@ def main():
             parity = f"{'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
             log(parity)
         del ofin
+        if not args.no_check:
+            # generated scenarios: the oracle generates and replays a few columns
+            base_h = w.gen_base()
+            scen = np.unique(np.r_[0, S - 1, np.random.default_rng(1).integers(0, S, 6)])
+            ok = True
+            gmk_h, gst_h, gcp_h = gmk.cpu().numpy(), gst.cpu().numpy(), gcp.cpu().numpy()
+            for sc in scen:
+                dcol = oracle.generate(base_h, 1, w.knob_block, gen.noise, gen.seed, scen0=int(sc))
+                omk1, _, ost1 = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dcol,
+                                                 want_finish=False)
+                ocp1, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, n, dcol)
+                ok &= gmk_h[sc] == omk1[0] and gst_h[sc] == ost1[0] and gcp_h[sc] == ocp1[0]
+            gp = f"generated {'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
+            parity = f"{parity}; {gp}" if parity else gp
+            log(gp)
 
     # HBM traffic measured by counters for this exact kernel source, if any
     traffic = None
@@ -228,7 +266,11 @@ def main():
                     "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3),
                     "static_replay_ms": float(np.mean(sr_ms)),
                     "static_replay_op_events_per_s": op_events / (float(np.mean(sr_ms)) / 1e3),
-                    "attribution_ms": float(np.mean(at_ms))},
+                    "attribution_ms": float(np.mean(at_ms)),
+                    "generated_run_ms": float(np.mean(gev_ms)),
+                    "generated_critical_path_ms": float(np.mean(gcp_ms)),
+                    "generated_run_op_events_per_s": op_events / (float(np.mean(gev_ms)) / 1e3),
+                    "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",

@@ -65,10 +65,12 @@ __device__ __forceinline__ int4 settle(int4 v) {
 //
 // Positions run breadth-first from kRoot = 7, which puts the 8 children of
 // position p at 8 (p - 6) ... 8 (p - 6) + 7: every child group is aligned to
-// 8 entries.  The root is kept in a register; positions 8 .. le - 1 (the
-// root's 8 children and the first (le - 16) / 8 groups below them, which
-// breadth-first order fills first) live in LDS, slot-major x lane,
-// conflict-free; positions from le on live in global scratch, lane-major, so
+// 8 entries.  The root and its 8 children are kept in registers (the
+// children's array is only indexed through unrolled selects, so it stays in
+// registers); positions 16 .. le - 1 (the first (le - 16) / 8 groups of the
+// root's grandchildren, which breadth-first order fills first) live in LDS,
+// slot-major x lane, conflict-free; positions from le on live in global
+// scratch, lane-major, so
 // one child group there is one aligned 64-byte segment of one lane.  Every
 // position at or beyond the end holds kEmpty, which is larger than any key,
 // so partial groups need no bounds masks; the kernel restores kEmpty
@@ -81,23 +83,41 @@ __device__ __forceinline__ int heap_child0(int p) { return kD * (p - (kRoot - 1)
 
 struct WideHeap {
   uint64_t root;     // position kRoot
-  lptr<uint64_t> l;  // this lane's LDS column: position p (kL1 .. le-1) at l[(p - kL1) * kWave]
+  uint64_t ch[kD];   // positions kL1 .. kL2 - 1: the root's children
+  lptr<uint64_t> l;  // this lane's LDS column: position p (kL2 .. le-1) at l[(p - kL2) * kWave]
   uint64_t *g;       // this lane's global run: position p (>= le) at g[p - le]
   int le;            // first position in global memory (kL2 + kD k)
+  // child k of the root (k lane-dependent): a tree of selects on the bits of
+  // k (a chain of equality selects would be turned back into an indexed load,
+  // which would move the array to scratch memory)
+  __device__ __forceinline__ uint64_t child(int k) const {
+    const bool b0 = k & 1, b1 = k & 2, b2 = k & 4;
+    const uint64_t a01 = b0 ? ch[1] : ch[0], a23 = b0 ? ch[3] : ch[2];
+    const uint64_t a45 = b0 ? ch[5] : ch[4], a67 = b0 ? ch[7] : ch[6];
+    const uint64_t a03 = b1 ? a23 : a01, a47 = b1 ? a67 : a45;
+    return b2 ? a47 : a03;
+  }
+  __device__ __forceinline__ void set_child(int k, uint64_t x) {
+#pragma unroll
+    for (int j = 0; j < kD; ++j) ch[j] = k == j ? x : ch[j];
+  }
   __device__ __forceinline__ uint64_t get(int p) const {
-    if (p < le) return l[(p - kL1) * kWave];
+    if (p < kL2) return child(p - kL1);
+    if (p < le) return l[(p - kL2) * kWave];
     return settle(g[p - le]);
   }
-  __device__ __forceinline__ void set(int p, uint64_t x) const {
-    if (p < le)
-      l[(p - kL1) * kWave] = x;
+  __device__ __forceinline__ void set(int p, uint64_t x) {
+    if (p < kL2)
+      set_child(p - kL1, x);
+    else if (p < le)
+      l[(p - kL2) * kWave] = x;
     else
       g[p - le] = x;
   }
-  // the group starting at c (< le, a multiple of kD) in LDS
+  // the group starting at c (kL2 <= c < le, a multiple of kD) in LDS
   __device__ __forceinline__ void lds_group(int c, uint64_t (&v)[kD]) const {
 #pragma unroll
-    for (int k = 0; k < kD; ++k) v[k] = l[(c + k - kL1) * kWave];
+    for (int k = 0; k < kD; ++k) v[k] = l[(c + k - kL2) * kWave];
   }
   // the group starting at c >= le: one aligned 64-byte segment
   __device__ __forceinline__ void global_group(int c, uint64_t (&v)[kD]) const {
@@ -133,7 +153,7 @@ __device__ __forceinline__ void min_group(uint64_t (&v)[kD], uint64_t &m, int &q
 // Place x at position p (a grandchild of the root or deeper) of a heap
 // ending at `end` and restore heap order below it; every group below a
 // grandchild of the root lies in global memory (one round trip per level).
-__device__ __forceinline__ void sift_down_deep(const WideHeap &h, int end, int p, uint64_t x) {
+__device__ __forceinline__ void sift_down_deep(WideHeap &h, int end, int p, uint64_t x) {
   for (;;) {
     const int c = heap_child0(p);
     if (c >= end) break;
@@ -182,7 +202,8 @@ struct HeapAhead {
 template <bool DEEP>
 __device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, HeapAhead &A) {
   uint64_t v[kD];
-  h.lds_group(kL1, v);  // all kEmpty when the root has no children
+#pragma unroll
+  for (int k = 0; k < kD; ++k) v[k] = h.ch[k];  // all kEmpty when the root has no children
   min_group(v, A.m1, A.q1);
   A.q1 += kL1;
   A.c2 = heap_child0(A.q1);
@@ -218,10 +239,10 @@ __device__ __forceinline__ void heap_replace_root(WideHeap &h, int end, const He
   h.root = A.m1;
   const int p = A.q1;
   if (A.c2 >= end || x < A.m2) {
-    h.l[(p - kL1) * kWave] = x;
+    h.set_child(p - kL1, x);
     return;
   }
-  h.l[(p - kL1) * kWave] = A.m2;
+  h.set_child(p - kL1, A.m2);
   sift_down_deep(h, end, A.c2 + A.q2, x);
 }
 
@@ -233,16 +254,20 @@ __device__ __forceinline__ void heap_pop_root(WideHeap &h, int &end, HeapAhead &
     return;
   }
   uint64_t x;
-  if (lp < h.le) {
-    x = h.l[(lp - kL1) * kWave];
-    h.l[(lp - kL1) * kWave] = kEmpty;
+  if (lp < kL2) {
+    x = h.child(lp - kL1);
+    h.set_child(lp - kL1, kEmpty);
+  } else if (lp < h.le) {
+    x = h.l[(lp - kL2) * kWave];
+    h.l[(lp - kL2) * kWave] = kEmpty;
   } else {
     x = A.last;
     h.g[lp - h.le] = kEmpty;
   }
   if (lp < kL2) {  // a child of the root left: rescan them (no grandchildren remain)
     uint64_t v[kD];
-    h.lds_group(kL1, v);
+#pragma unroll
+    for (int k = 0; k < kD; ++k) v[k] = h.ch[k];
     min_group(v, A.m1, A.q1);
     A.q1 += kL1;
     A.c2 = heap_child0(A.q1);
@@ -267,7 +292,7 @@ struct EvArgs {
   int32_t *status;
   uint64_t *heap_g;   // [blocks][64][heap_stride]: heap positions from heap_le on, lane-major
   int heap_stride;    // entries per lane (a multiple of 16)
-  int heap_le;        // first heap position in global memory (32 + 16 k)
+  int heap_le;        // first heap position in global memory (16 + 8 k)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
   int retry;          // 0: every scenario; 1: those whose makespan holds kWalkRetry, when
@@ -282,12 +307,30 @@ struct EvArgs {
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
 
+// A lane's join state {predecessors finished, max finish} per join index, in
+// global scratch ([J][64] int2) or in LDS ([J][64] packed into 64 bits).
+struct JoinGlobal {
+  int2 *p;
+  __device__ __forceinline__ int2 get(int j) const { return p[(size_t)j * kWave]; }
+  __device__ __forceinline__ void set(int j, int2 v) const { p[(size_t)j * kWave] = v; }
+};
+struct JoinLds {
+  lptr<uint64_t> p;
+  __device__ __forceinline__ int2 get(int j) const {
+    const uint64_t x = p[(size_t)j * kWave];
+    return make_int2((int)(uint32_t)x, (int)(uint32_t)(x >> 32));
+  }
+  __device__ __forceinline__ void set(int j, int2 v) const {
+    p[(size_t)j * kWave] = (uint64_t)(uint32_t)v.x | ((uint64_t)(uint32_t)v.y << 32);
+  }
+};
+
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
-template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class RfGet,
-          class RfSet, class LastXchg, class Flush>
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class JPtr,
+          class RfGet, class RfSet, class LastXchg, class Flush>
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
-                                           int &end, int2 *jst, int it, int64_t s,
+                                           int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
                                            uint32_t s_hi, uint32_t &st, uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
@@ -368,14 +411,14 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
       release(sw.y == kJoinSibling ? ready : fin, sw.x);
       continue;
     }
-    const int2 js = settle(jst[(size_t)sw.y * kWave]);
+    const int2 js = settle(jst.get(sw.y));
     const int need = settle(G.jneed[sw.y]);
     const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
     if (js.x + 1 < need) {
-      jst[(size_t)sw.y * kWave] = make_int2(js.x + 1, (int)rdy);
+      jst.set(sw.y, make_int2(js.x + 1, (int)rdy));
       continue;
     }
-    jst[(size_t)sw.y * kWave] = make_int2(0, 0);  // leave scratch clean
+    jst.set(sw.y, make_int2(0, 0));  // leave the join state clean
     if (sw.x < n) {
       release(rdy, sw.x);
     } else {  // a barrier: its first member is ready now (the others follow it)
@@ -396,8 +439,9 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
 // are written in bursts of kFinQ stores per lane, so their completion is
 // waited for once per burst instead of once per step.  GEN: durations are
 // generated from the knob grid and counter-based noise of a.gen instead of
-// read from a.dur.
-template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false>
+// read from a.dur.  JOIN_LDS: the join state lives in LDS after the resource
+// times (and last-op table) instead of in global scratch.
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool JOIN_LDS = false>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -406,10 +450,15 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   heap.l = as_lds(lds) + lane;
   heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
   heap.le = a.heap_le;
-  const int heap_lds = a.heap_le - kL1;  // heap positions per lane kept in LDS
+  const int heap_lds = a.heap_le - kL2;  // heap positions per lane kept in LDS
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)heap_lds * kWave)) + lane;
-  int2 *jst = a.join_g + (size_t)blockIdx.x * G.J * kWave + lane;
+  const JoinGlobal jst_g{a.join_g + (size_t)blockIdx.x * G.J * kWave + lane};
+  // LDS after the heap, the resource times and (PREV) the last-op table
+  const JoinLds jst_l{as_lds((uint64_t *)((uint32_t *)(lds + (size_t)heap_lds * kWave) +
+                                          (size_t)(PREV ? 2 : 1) * R * kWave)) + lane};
+  if (JOIN_LDS)  // cleared once: every join is reset to zero when it fires
+    for (int j = 0; j < G.J; ++j) jst_l.set(j, make_int2(0, 0));
   auto rf_get = [&](int r) -> uint32_t { return RF_LDS ? rfree_l[r * kWave] : rfree_g[r * kWave]; };
   auto rf_set = [&](int r, uint32_t v) {
     if (RF_LDS)
@@ -460,6 +509,8 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       }
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
     heap.root = kEmpty;
+#pragma unroll
+    for (int k = 0; k < kD; ++k) heap.ch[k] = kEmpty;
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
@@ -475,14 +526,20 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the steps start with nothing in flight
     for (int it = 0; it < n; ++it) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
-      if (__ballot(end > heap.le))
-        event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jst, it, s, sc, brow, s_lo, s_hi,
-                                                           st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
-                                                           flush);
+      auto run_step = [&](auto jp) {
+        if (__ballot(end > heap.le))
+          event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
+                                                             st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
+                                                             flush);
+        else
+          event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
+                                                              st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
+                                                              flush);
+      };
+      if constexpr (JOIN_LDS)
+        run_step(jst_l);
       else
-        event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jst, it, s, sc, brow, s_lo,
-                                                            s_hi, st, span, fq, rq, pq, rf_get, rf_set,
-                                                            last_xchg, flush);
+        run_step(jst_g);
     }
     flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
@@ -913,6 +970,9 @@ int occupancy_blocks(K kernel, size_t lds, int cus) {
 }
 
 constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
+// join state kept in LDS up to this size: 0, since on the BERT workload the
+// occupancy it costs outweighs the global round trip it saves (45.4 vs 41.2 ms)
+constexpr size_t kJoinLdsMax = 0;
 constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
 
 char *base_heap(sim_graph *g) { return (char *)g->scratch + g->scratch_ev_heap_off; }
@@ -945,12 +1005,20 @@ int plan_scratch(sim_graph *g) {
   if (const char *e = getenv("MLSIM_EV_LDS_GROUPS"))  // tuning override
     lds_groups = std::min(kD, std::max(0, atoi(e)));
   P.ev_heap_le = kL2 + kD * lds_groups;
-  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes;
-  const int ev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus)
-                            : occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
+  // join state in LDS beside resource times in LDS when it is small
+  const size_t join_bytes = (size_t)G.J * kWave * 8;
+  P.ev_join_lds = rf_lds && G.J > 0 && join_bytes <= kJoinLdsMax;  // off: see kJoinLdsMax
+  if (const char *e = getenv("MLSIM_JOIN_LDS"))  // tuning override
+    P.ev_join_lds = rf_lds && G.J > 0 && atoi(e) != 0;
+  const size_t join_lds_bytes = P.ev_join_lds ? join_bytes : 0;
+  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes + join_lds_bytes;
+  const int ev_occ = P.ev_join_lds
+                         ? occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes, cus)
+                     : rf_lds ? occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus)
+                              : occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
   if (ev_occ < 0) return SIM_E_HIP;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
-  const size_t ev_per_block = (size_t)G.J * kWave * 8 + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
+  const size_t ev_per_block = (P.ev_join_lds ? 0 : join_bytes) + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
   size_t ev_blocks = (size_t)ev_occ;
   if (ev_per_block) ev_blocks = std::min(ev_blocks, std::max<size_t>(1, kScratchBudget / ev_per_block));
   if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
@@ -958,13 +1026,17 @@ int plan_scratch(sim_graph *g) {
   P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
   // the event kernel for attribution: a last-op table beside the resource times
   P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
-  const int ev_prev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
-                                 : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
+  const int ev_prev_occ =
+      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, true, false, true>, P.ev_prev_lds_bytes, cus)
+      : rf_lds      ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
+                    : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
   P.ev_prev_blocks = std::max(1, std::min(ev_prev_occ, P.ev_blocks));
   // the event kernel with generated durations: same LDS and scratch per block
-  const int ev_gen_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus)
-                                : occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
+  const int ev_gen_occ =
+      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_lds_bytes, cus)
+      : rf_lds      ? occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus)
+                    : occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
   if (ev_gen_occ < 0) return SIM_E_HIP;
   P.ev_gen_blocks = std::max(1, std::min(ev_gen_occ, P.ev_blocks));
   // attribution chains: busy and chain accumulators in LDS when they fit
@@ -1020,7 +1092,7 @@ int plan_scratch(sim_graph *g) {
     return o;
   };
   g->scratch_ev_heap_off = take(heap_g_bytes * ev_grid);
-  g->scratch_ev_join_off = take((size_t)G.J * kWave * 8 * ev_grid);
+  g->scratch_ev_join_off = take(P.ev_join_lds ? 0 : join_bytes * ev_grid);
   g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_ev_last_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_at_off = take(P.at_lds ? 0 : (size_t)2 * G.R * kWave * 4 * P.at_blocks);
@@ -1082,13 +1154,26 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
   const size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
-  const int variant = (gen ? 16 : 0) | (prev ? 8 : 0) | (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) |
-                      (place ? 1 : 0);
+  const int variant = (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) | (rf_lds ? 4 : 0) |
+                      (g->row_identity ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_GEN_CASE(V, A, B) \
   case V: k_event<A, B, false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+#define EV_JOIN_CASE(V, B, C, D, E) \
+  case V: k_event<true, B, C, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
+    // join state in LDS (always with resource times in LDS)
+    EV_JOIN_CASE(36, false, false, false, false)
+    EV_JOIN_CASE(37, false, true, false, false)
+    EV_JOIN_CASE(38, true, false, false, false)
+    EV_JOIN_CASE(39, true, true, false, false)
+    EV_JOIN_CASE(44, false, false, true, false)
+    EV_JOIN_CASE(45, false, true, true, false)
+    EV_JOIN_CASE(46, true, false, true, false)
+    EV_JOIN_CASE(47, true, true, true, false)
+    EV_JOIN_CASE(52, false, false, false, true)
+    EV_JOIN_CASE(54, true, false, false, true)
     EV_GEN_CASE(16, false, false)
     EV_GEN_CASE(18, false, true)
     EV_GEN_CASE(20, true, false)
@@ -1112,6 +1197,7 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   }
 #undef EV_CASE
 #undef EV_GEN_CASE
+#undef EV_JOIN_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

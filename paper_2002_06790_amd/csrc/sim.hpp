@@ -151,6 +151,7 @@ struct ScratchPlan {
   int32_t ev_prev_blocks, at_blocks, at_lds;
   // generated durations: persistent grids of the event and critical-path kernels
   int32_t ev_gen_blocks, cp_gen_blocks;
+  int32_t ev_join_lds;  // event kernel: join state in LDS (after the resource times)
   size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
   int32_t wk_ok;
