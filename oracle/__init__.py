@@ -44,6 +44,10 @@ def lib(path: Optional[str] = None):
                                        P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
                                        P, ctypes.c_int32]
         L.oracle_run_batch.restype = ctypes.c_int
+        L.oracle_run_batch_gap.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, ctypes.c_int64,
+                                           P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
+                                           P, ctypes.c_int32]
+        L.oracle_run_batch_gap.restype = ctypes.c_int
         L.oracle_critical_path.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, P, ctypes.c_int64,
                                            P, ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
         L.oracle_critical_path.restype = ctypes.c_int
@@ -87,22 +91,30 @@ def _threads(n_threads: Optional[int]) -> int:
 
 
 def run_batch(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None,
-              want_finish: bool = True, n_threads: Optional[int] = None, library=None):
-    """Replay every scenario column of ``dur`` ([n_ops, n_scen] int32).
+              want_finish: bool = True, n_threads: Optional[int] = None, library=None, gap=None):
+    """Replay every scenario column of ``dur`` ([n_ops, n_scen] int32);
+    ``gap`` ([n_res] int32 or None) is each device's idle time between
+    consecutive ops.
 
     Returns ``(makespan [S], finish [n_ops, S] or None, status [S])``.
     """
     succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
-    op_res, prio = _c(op_res, np.int32), _c(prio, np.int32)
+    op_res, prio, gap = _c(op_res, np.int32), _c(prio, np.int32), _c(gap, np.int32)
     dur, place = _c(dur, np.int32), _c(place, np.uint16)
     n = op_res.size
     S = dur.shape[1] if dur.ndim == 2 else 0
     makespan = np.empty(S, np.int32)
     status = np.empty(S, np.int32)
     finish = np.empty((n, S), np.int32) if want_finish else None
-    rc = (library or lib()).oracle_run_batch(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
+    L = library or lib()
+    if gap is None:
+        rc = L.oracle_run_batch(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
                                 S, _ptr(dur), S, _ptr(place), S, _ptr(makespan), _ptr(finish), S,
                                 _ptr(status), _threads(n_threads))
+    else:
+        rc = L.oracle_run_batch_gap(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
+                                    _ptr(gap), S, _ptr(dur), S, _ptr(place), S, _ptr(makespan), _ptr(finish),
+                                    S, _ptr(status), _threads(n_threads))
     if rc:
         raise OracleError(rc)
     return makespan, finish, status

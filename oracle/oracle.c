@@ -86,6 +86,7 @@ typedef struct {
   int32_t hsize;
   int32_t *prev;  /* [n] or NULL: the op that ran before each op on its device (-1: none) */
   int32_t *last;  /* [nres] with prev: the last op each device ran */
+  int32_t *nrun;  /* [nres] with gaps: ops each device has run */
 } sim_ws;
 
 /* key order of the ready list: ready time, then priority, then op id */
@@ -136,6 +137,7 @@ typedef struct {
   int32_t *makespan, *finish, *status;
   int64_t ld_fin;
   int rc;
+  const int32_t *gap; /* [nres] or NULL: a device's idle time between consecutive ops */
 } run_job;
 
 static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
@@ -155,6 +157,8 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
     for (int32_t r = 0; r < g->nres; ++r) w->rfree[r] = 0;
     if (w->prev)
       for (int32_t r = 0; r < g->nres; ++r) w->last[r] = -1;
+    if (J->gap)
+      for (int32_t r = 0; r < g->nres; ++r) w->nrun[r] = 0;
     w->hsize = 0;
     /* (1) every op with no predecessors is ready at t = 0 */
     for (int32_t v = 0; v < g->n; ++v)
@@ -162,7 +166,11 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
     while (w->hsize > 0) {
       int32_t v = heap_pop(g, w);
       int32_t r = J->place ? (int32_t)J->place[(int64_t)v * J->ld_place + s] : g->res[v];
-      int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];
+      /* the device can start again when its last op has finished and, with
+       * gaps, its gap after that op has passed */
+      int64_t avail = w->rfree[r];
+      if (J->gap && w->nrun[r] > 0) avail += J->gap[r];
+      int64_t start = w->ready[v] > avail ? w->ready[v] : avail;
       int64_t f = start + J->dur[(int64_t)v * J->ld_dur + s];
       if (f > INT32_MAX) {
         st |= ORC_ST_OVERFLOW;
@@ -170,6 +178,7 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
       }
       w->fin[v] = f;
       w->rfree[r] = f;
+      if (J->gap) w->nrun[r]++;
       if (w->prev) {
         w->prev[v] = w->last[r];
         w->last[r] = v;
@@ -202,7 +211,8 @@ static void *run_range(void *arg) {
   w.rfree = (int64_t *)malloc((R ? R : 1) * sizeof(int64_t));
   w.heap = (int32_t *)malloc(n * sizeof(int32_t));
   w.prev = w.last = NULL;
-  if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap) {
+  w.nrun = (int32_t *)malloc((R ? R : 1) * sizeof(int32_t));
+  if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap || !w.nrun) {
     J->rc = ORC_E_NOMEM;
   } else {
     for (int64_t s = J->s0; s < J->s1; ++s) replay_one(J, &w, s);
@@ -212,6 +222,7 @@ static void *run_range(void *arg) {
   free(w.fin);
   free(w.rfree);
   free(w.heap);
+  free(w.nrun);
   return NULL;
 }
 
@@ -248,9 +259,21 @@ int oracle_run_batch(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
                      int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                      const uint16_t *place, int64_t ld_place, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
+  return oracle_run_batch_gap(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL, n_scen, dur,
+                              ld_dur, place, ld_place, makespan, finish, ld_fin, status, n_threads);
+}
+
+int oracle_run_batch_gap(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                         const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                         const int32_t *gap, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         const uint16_t *place, int64_t ld_place, int32_t *makespan,
+                         int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
   graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL};
   int rc = check_graph(&g, 1);
   if (rc) return rc;
+  if (gap)
+    for (int32_t r = 0; r < n_res; ++r)
+      if (gap[r] < 0) return ORC_E_INVAL;
   if (n_scen < 0 || (n_scen > 0 && !makespan)) return ORC_E_INVAL;
   if (n_scen > 0 && n_ops > 0) {
     if (!dur || ld_dur < n_scen) return ORC_E_INVAL;
@@ -276,7 +299,7 @@ int oracle_run_batch(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
     return ORC_E_NOMEM;
   }
   for (int32_t t = 0; t < n_threads; ++t) {
-    run_job J = {&g, 0, 0, dur, ld_dur, place, ld_place, makespan, finish, status, ld_fin, 0};
+    run_job J = {&g, 0, 0, dur, ld_dur, place, ld_place, makespan, finish, status, ld_fin, 0, gap};
     jobs[t] = J;
   }
   rc = run_threads(run_range, jobs, sizeof(run_job), n_scen, n_threads, set_run_range);
@@ -653,6 +676,7 @@ static void *attribute_range(void *arg) {
   w.heap = (int32_t *)malloc(n * sizeof(int32_t));
   w.prev = (int32_t *)malloc(n * sizeof(int32_t));
   w.last = (int32_t *)malloc((R ? R : 1) * sizeof(int32_t));
+  w.nrun = NULL;
   int32_t *rev = (int32_t *)malloc(n * sizeof(int32_t));
   if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap || !w.prev || !w.last || !rev)
     A->run.rc = ORC_E_NOMEM;
@@ -715,7 +739,7 @@ int oracle_attribute(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
       rc = ORC_E_NOMEM;
     } else {
       for (int32_t t = 0; t < n_threads; ++t) {
-        at_job A = {{&g, 0, 0, dur, ld_dur, place, ld_place, makespan, NULL, status, 0, 0},
+        at_job A = {{&g, 0, 0, dur, ld_dur, place, ld_place, makespan, NULL, status, 0, 0, NULL},
                     pred_ptr, pred_idx, busy, chain, chain_ops, ld_res, path_scen, path_ops,
                     path_cap, path_len};
         jobs[t] = A;

@@ -66,6 +66,26 @@ int oracle_run_batch(int32_t n_ops, int32_t n_res,
                      int32_t *status, int32_t n_threads);
 
 /*
+ * The replay with a gap per device (the paper names the idle time between
+ * consecutive ops on a device as a source of the simulator's residual error,
+ * Sec. 3): after a device finishes an op it cannot start its next op for
+ * gap[r] ns, so an op popped from the ready list starts at
+ *   max(ready time, finish of the device's previous op + gap[r]),
+ * or at its ready time if it is the device's first op.  Queues stay
+ * first-in-first-out by ready time; the makespan is still the largest finish
+ * time (a trailing gap does not count).  gap: [n_res] with every entry >= 0
+ * (else ORC_E_INVAL), or NULL for no gaps (oracle_run_batch).  Everything
+ * else as oracle_run_batch.
+ */
+int oracle_run_batch_gap(int32_t n_ops, int32_t n_res,
+                         const int64_t *succ_ptr, const int32_t *succ_idx,
+                         const int32_t *op_res, const int32_t *prio, const int32_t *gap,
+                         int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         const uint16_t *place, int64_t ld_place,
+                         int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                         int32_t *status, int32_t n_threads);
+
+/*
  * Longest path through the DAG, resources ignored: dist(v) = d(v) + max over
  * predecessors p of dist(p) (0 without predecessors); cp_len[s] = max_v
  * dist(v), 0 for an empty graph, -1 if a duration is < 1 or a path exceeds

@@ -31,8 +31,12 @@ def preds_of(n, succ_ptr, succ_idx):
     return P
 
 
-def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
-    """One scenario: returns finish times (list) by 1-ns time stepping."""
+def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
+    """One scenario: returns finish times (list) by 1-ns time stepping.
+
+    With ``gap``, a device that finishes an op at t stays idle until
+    t + gap[device] before it starts its next one.
+    """
     prio = list(range(n)) if prio is None else [int(x) for x in prio]
     P = preds_of(n, succ_ptr, succ_idx)
     S = [set() for _ in range(n)]
@@ -42,13 +46,14 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
     cnt = [len(P[v]) for v in range(n)]
     queue = [deque() for _ in range(n_res)]
     running = [None] * n_res  # (op, finish)
+    avail = [0] * n_res  # first tick at which each device may start an op
     finish = [None] * n
     done = 0
     arrivals = sorted((v for v in range(n) if cnt[v] == 0), key=lambda v: (prio[v], v))
     for v in arrivals:
         queue[int(res[v])].append(v)
     t = 0
-    limit = int(np.sum(dur)) + 1
+    limit = int(np.sum(dur)) + 1 + (n * int(max(gap)) if gap is not None and len(gap) else 0)
     while done < n:
         # retire everything finishing now
         newly = []
@@ -56,6 +61,7 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
             if running[r] is not None and running[r][1] == t:
                 v = running[r][0]
                 running[r] = None
+                avail[r] = t + (int(gap[r]) if gap is not None else 0)
                 done += 1
                 for w in S[v]:
                     cnt[w] -= 1
@@ -65,7 +71,7 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
             queue[int(res[w])].append(w)
         # idle devices start their queue heads
         for r in range(n_res):
-            if running[r] is None and queue[r]:
+            if running[r] is None and queue[r] and t >= avail[r]:
                 v = queue[r].popleft()
                 finish[v] = t + int(dur[v])
                 running[r] = (v, finish[v])
@@ -75,7 +81,7 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
     return finish
 
 
-def _times_for_order(n, P, res, dur, orders):
+def _times_for_order(n, P, res, dur, orders, gap=None):
     """Start/finish/ready times implied by per-device orders, or None if the
     orders contradict the DAG (a cycle through device and data edges)."""
     prev_on_dev = {}
@@ -91,7 +97,9 @@ def _times_for_order(n, P, res, dur, orders):
             if all(finish[u] is not None for u in P[v]) and (
                     v not in prev_on_dev or finish[prev_on_dev[v]] is not None):
                 ready[v] = max([finish[u] for u in P[v]], default=0)
-                start = max(ready[v], finish[prev_on_dev[v]] if v in prev_on_dev else 0)
+                avail = (finish[prev_on_dev[v]] + (int(gap[int(res[v])]) if gap is not None else 0)
+                         if v in prev_on_dev else 0)
+                start = max(ready[v], avail)
                 finish[v] = start + int(dur[v])
                 remaining.discard(v)
                 progress = True
@@ -100,7 +108,7 @@ def _times_for_order(n, P, res, dur, orders):
     return ready, finish
 
 
-def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
+def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
     """All per-device orders whose implied schedule is FIFO by (ready, prio, id).
 
     Returns a list of finish-time lists, one per consistent order.
@@ -110,7 +118,7 @@ def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None):
     on = [[v for v in range(n) if int(res[v]) == r] for r in range(n_res)]
     found = []
     for orders in itertools.product(*[itertools.permutations(o) for o in on]):
-        tr = _times_for_order(n, P, res, dur, orders)
+        tr = _times_for_order(n, P, res, dur, orders, gap)
         if tr is None:
             continue
         ready, finish = tr

@@ -806,3 +806,129 @@ def test_generate_argument_errors(library=None):
         with pytest.raises(oracle.OracleError):
             oracle.generate(base, 4, args["knob_block"], args["noise"], args["seed"],
                             scen0=args["scen0"], library=library)
+
+
+# ------------------------------------------------------ device gap pins
+#
+# oracle_run_batch_gap: after a device finishes an op it idles gap[r] ns
+# before its next op (the paper names this gap as unmodelled, Sec. 3).
+
+def run_gap(g, dur, gap, library=None, **kw):
+    return oracle.run_batch(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], dur,
+                            prio=g.get("prio"), library=library, gap=np.asarray(gap, np.int32), **kw)
+
+
+def test_gap_hand_example(library=None):
+    # R0 has a 3 ns gap, R1 none.  op0 (R0, 5), op1 (R1, 2), op2 (R0, 4, after
+    # op1), op3 (R0, 1).  t=0: R0 runs op0 [0,5), R1 runs op1 [0,2); t=2: op2
+    # ready; R0 is free again at 5+3=8 and serves op3 (ready 0) [8,9), then is
+    # free at 12 and serves op2 (ready 2) [12,16).  Without the gap: [5,2,10,6].
+    g = dict(n=4, n_res=2, succ_ptr=np.array([0, 0, 1, 1, 1], np.int64), succ_idx=np.array([2], np.int32),
+             op_res=np.array([0, 1, 0, 0], np.int32), prio=None)
+    dur = np.array([[5], [2], [4], [1]], np.int32)
+    mk, fin, st = run_gap(g, dur, [3, 0], library)
+    assert list(fin[:, 0]) == [5, 2, 16, 9] and mk[0] == 16 and st[0] == 0
+    mk0, fin0, _ = run_gap(g, dur, [0, 0], library)
+    assert list(fin0[:, 0]) == [5, 2, 10, 6] and mk0[0] == 10
+
+
+def test_gap_one_device_closed_form(library=None):
+    rng = np.random.default_rng(21)
+    n = 9
+    g = dict(n=n, n_res=1, succ_ptr=np.zeros(n + 1, np.int64), succ_idx=np.zeros(0, np.int32),
+             op_res=np.zeros(n, np.int32), prio=rng.permutation(n).astype(np.int32))
+    dur = rng.integers(1, 50, size=(n, 6)).astype(np.int32)
+    gap = 7
+    mk, fin, _ = run_gap(g, dur, [gap], library)
+    order = np.argsort(g["prio"], kind="stable")
+    for s in range(dur.shape[1]):
+        f = np.cumsum(dur[order, s]) + gap * np.arange(n)
+        assert np.array_equal(fin[order, s], f)
+        assert mk[s] == dur[:, s].sum() + gap * (n - 1)
+
+
+def test_gap_chain_closed_forms(library=None):
+    rng = np.random.default_rng(22)
+    n = 10
+    ptr = np.r_[np.arange(n, dtype=np.int64), n - 1]
+    idx = np.arange(1, n, dtype=np.int32)
+    dur = rng.integers(1, 30, size=(n, 5)).astype(np.int32)
+    # one device: every op waits its predecessor's finish plus the gap
+    g1 = dict(n=n, n_res=1, succ_ptr=ptr, succ_idx=idx, op_res=np.zeros(n, np.int32), prio=None)
+    _, fin, _ = run_gap(g1, dur, [4], library)
+    assert np.array_equal(fin, np.cumsum(dur, axis=0) + 4 * np.arange(n)[:, None])
+    # two alternating devices: op k's device last ran op k-2, so op k starts
+    # at max(f(k-1), f(k-2) + gap)
+    g2 = dict(n=n, n_res=2, succ_ptr=ptr, succ_idx=idx, op_res=(np.arange(n) % 2).astype(np.int32), prio=None)
+    gap = 12
+    _, fin, _ = run_gap(g2, dur, [gap, gap], library)
+    for s in range(dur.shape[1]):
+        f = [int(dur[0, s]), int(dur[0, s] + dur[1, s])]
+        for k in range(2, n):
+            f.append(max(f[-1], f[-2] + gap) + int(dur[k, s]))
+        assert list(fin[:, s]) == f
+
+
+def test_gap_one_device_per_op_is_longest_path(library=None):
+    rng = np.random.default_rng(23)
+    for _ in range(5):
+        n = 14
+        g = rand_graph(rng, n, n, 0.25)
+        g["op_res"] = np.arange(n, dtype=np.int32)
+        dur = rng.integers(1, 100, size=(n, 4)).astype(np.int32)
+        mk, fin, _ = run_gap(g, dur, rng.integers(0, 1000, size=n), library)
+        mk0, fin0, _ = run(g, dur, library=library)
+        assert np.array_equal(fin, fin0) and np.array_equal(mk, mk0)
+
+
+def test_gap_matches_brute_force(library=None):
+    rng = np.random.default_rng(24)
+    for trial in range(40):
+        n = int(rng.integers(2, 7))
+        R = int(rng.integers(1, 3))
+        g = rand_graph(rng, n, R, 0.35, prio=trial % 2 == 0)
+        dur = rng.integers(1, 6, size=(n, 1)).astype(np.int32)
+        gap = rng.integers(0, 5, size=R).astype(np.int32)
+        mk, fin, st = run_gap(g, dur, gap, library)
+        assert st[0] == 0
+        tick = brute.tick_sim(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], g["prio"], gap=gap)
+        assert list(fin[:, 0]) == tick
+        found = brute.enumerate_orders(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], g["prio"],
+                                       gap=gap)
+        assert found == [tick]
+
+
+def test_gap_bounds(library=None):
+    rng = np.random.default_rng(25)
+    for _ in range(6):
+        n, R = 40, 4
+        g = rand_graph(rng, n, R, 0.08)
+        dur = rng.integers(1, 200, size=(n, 8)).astype(np.int32)
+        gap = rng.integers(0, 150, size=R).astype(np.int32)
+        mk, fin, _ = run_gap(g, dur, gap, library)
+        cp, _ = oracle.critical_path(g["succ_ptr"], g["succ_idx"], n, dur, library=library)
+        cnt = np.bincount(g["op_res"], minlength=R)
+        for s in range(dur.shape[1]):
+            busy = np.bincount(g["op_res"], weights=dur[:, s], minlength=R)
+            lower = max(cp[s], int((busy + gap * np.maximum(cnt - 1, 0)).max()))
+            upper = int(dur[:, s].sum() + (gap * np.maximum(cnt - 1, 0)).sum())
+            assert lower <= mk[s] <= upper
+            # consecutive ops on a device are at least the gap apart
+            start = fin[:, s] - dur[:, s]
+            for r in range(R):
+                ops = np.nonzero(g["op_res"] == r)[0]
+                o = ops[np.argsort(start[ops])]
+                assert (start[o[1:]] >= fin[o[:-1], s] + gap[r]).all()
+
+
+def test_gap_errors_and_overflow(library=None):
+    g = dict(n=2, n_res=1, succ_ptr=np.array([0, 0, 0], np.int64), succ_idx=np.zeros(0, np.int32),
+             op_res=np.zeros(2, np.int32), prio=None)
+    with pytest.raises(oracle.OracleError):
+        run_gap(g, np.ones((2, 1), np.int32), [-1], library)
+    # two ops of 2^30 ns with a 2^30 - 1 ns gap between them pass INT32_MAX;
+    # 2^29 and 1 ns with that gap end at 2^29 + 2^30
+    dur = np.array([[2**30, 2**29], [2**30, 1]], np.int32)
+    mk, _, st = run_gap(g, dur, [2**30 - 1], library)
+    assert st[0] == oracle.ST_OVERFLOW and mk[0] == -1
+    assert st[1] == 0 and mk[1] == 2**29 + 2**30

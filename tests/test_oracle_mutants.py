@@ -69,6 +69,12 @@ MUTANTS = [
     ("gen-knob-off-by-one", "int64_t k = (S / knob_block) % n_knobs;", "int64_t k = ((S + 1) / knob_block) % n_knobs;"),
     ("gen-local-scenario-index", "gen_one(J->base, J->n, J->n_knobs, J->knob_block, J->noise, J->seed, J->scen0 + s, v);",
      "gen_one(J->base, J->n, J->n_knobs, J->knob_block, J->noise, J->seed, s, v);"),
+    ("gap-before-first-op", "if (J->gap && w->nrun[r] > 0) avail += J->gap[r];", "if (J->gap) avail += J->gap[r];"),
+    ("gap-ignored", "if (J->gap && w->nrun[r] > 0) avail += J->gap[r];", "(void)0;"),
+    ("gap-of-device-0", "if (J->gap && w->nrun[r] > 0) avail += J->gap[r];",
+     "if (J->gap && w->nrun[r] > 0) avail += J->gap[0];"),
+    ("gap-counted-in-makespan", "      w->rfree[r] = f;\n      if (J->gap) w->nrun[r]++;",
+     "      w->rfree[r] = f + (J->gap && w->nrun[r] > 0 ? 0 : 0) + (J->gap ? J->gap[r] : 0);\n      if (J->gap) w->nrun[r]++;"),
     ("gen-accepts-large-base", "if (b < 1 || b > ((int64_t)1 << 24)) return 0;", "if (b < 1) return 0;"),
 ]
 
