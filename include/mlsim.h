@@ -124,6 +124,29 @@ int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_
                   int64_t ld_fin, int32_t *status, uint32_t flags, void *stream);
 
 /*
+ * The replay with a gap per resource.  The paper attributes part of its
+ * simulator's remaining error to the idle time between consecutive ops on a
+ * device, which its loop does not model (Sec. 3).  Here a resource that
+ * finishes an op at time f cannot start its next op before f + gap[r]; its
+ * first op is not delayed.  An op popped from the ready list therefore
+ * starts at max(ready time, previous finish on its resource + gap[r]); the
+ * queues stay first-in-first-out by ready time, with the same tie rules, and
+ * the makespan is the largest finish time (a trailing gap does not count).
+ *   gap  host int32 [n_res], every entry >= 0 (else SIM_E_INVAL); read
+ *        before the call returns (copied into the graph's scratch memory in
+ *        stream order).
+ * Other arguments and outputs as sim_run_batch (placement allowed; a finish
+ * time above INT32_MAX sets SIM_ST_OVERFLOW); flags: SIM_ALGO_AUTO or
+ * SIM_ALGO_EVENT (others return SIM_E_INVAL).  With every gap 0 the result
+ * equals sim_run_batch.  Asynchronous on `stream`; no memory is allocated;
+ * calls on different streams sharing one graph must not overlap in time.
+ */
+int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      const uint16_t *place, int64_t ld_place, const int32_t *gap,
+                      int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                      uint32_t flags, void *stream);
+
+/*
  * Critical path per scenario: the longest path through the graph with
  * resources ignored, dist(v) = d(v) + max over predecessors of dist (0 if
  * none), cp_len[s] = max over v of dist(v); 0 for an empty graph, -1 if a

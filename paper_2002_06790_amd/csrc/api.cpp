@@ -89,6 +89,33 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
                       st);
 }
 
+extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                                 const uint16_t *place, int64_t ld_place, const int32_t *gap,
+                                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                                 uint32_t flags, void *stream) {
+  if (!g || n_scen < 0 || (flags != SIM_ALGO_AUTO && flags != SIM_ALGO_EVENT)) return SIM_E_INVAL;
+  if (!gap) return SIM_E_INVAL;
+  for (int32_t r = 0; r < g->n_res; ++r)
+    if (gap[r] < 0) return SIM_E_INVAL;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
+  if (place && ld_place < n_scen) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (g->n_ops == 0) {
+    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    return SIM_OK;
+  }
+  // the gaps go to the graph's scratch, in stream order before the replay
+  int32_t *gap_dev = (int32_t *)((char *)g->scratch + g->scratch_gap_off);
+  if (hipMemcpyAsync(gap_dev, gap, (size_t)g->n_res * 4, hipMemcpyHostToDevice, st) != hipSuccess)
+    return SIM_E_HIP;
+  return launch_event_gap(g, n_scen, dur, ld_dur, place, ld_place, gap_dev, makespan, finish, ld_fin,
+                          status, st);
+}
+
 extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32_t *dur,
                                  int64_t ld_dur, int32_t *cp_len, int64_t path_scen,
                                  int32_t *path_ops, int32_t path_cap, int32_t *path_len,

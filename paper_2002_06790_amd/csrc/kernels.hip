@@ -303,6 +303,8 @@ struct EvArgs {
   int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
   int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
   DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
+  const int32_t *gap; // [R] or null: each resource's idle time between consecutive ops
+  int gap_lds;        // byte offset of the resource gap table in LDS (when gap is set)
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
@@ -332,7 +334,8 @@ template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, 
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
-                                           uint32_t s_hi, uint32_t &st, uint32_t &span,
+                                           uint32_t s_hi, lptr<const int32_t> gap_l, uint32_t &st,
+                                           uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
                                            int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
                                            LastXchg last_xchg, Flush flush) {
@@ -377,7 +380,14 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
     st |= SIM_ST_OVERFLOW;
     fin = kI32Max;
   }
-  rf_set(r, fin);
+  // the resource can start its next op at fin, or with gaps fin + gap[r]
+  // (saturated at 2^31, which still makes any later finish overflow)
+  uint32_t avail = fin;
+  if (a.gap) {
+    const uint32_t x = fin + (uint32_t)gap_l[r];
+    avail = x < kI32Max + 1u ? x : kI32Max + 1u;
+  }
+  rf_set(r, avail);
   span = fin > span ? fin : span;
   const int32_t before = PREV ? last_xchg(r, row) : 0;  // the op this resource ran last
   heap_settle_ahead<DEEP>(A);
@@ -446,6 +456,13 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
+  // resource gaps (one table per wave, after every per-lane region)
+  const lptr<int32_t> gap_w = as_lds((int32_t *)((char *)lds + a.gap_lds));
+  if (a.gap) {
+    for (int r = lane; r < R; r += kWave) gap_w[r] = a.gap[r];
+    __syncthreads();
+  }
+  const lptr<const int32_t> gap_l = (lptr<const int32_t>)gap_w;
   WideHeap heap;
   heap.l = as_lds(lds) + lane;
   heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
@@ -529,12 +546,12 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       auto run_step = [&](auto jp) {
         if (__ballot(end > heap.le))
           event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
-                                                             st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
-                                                             flush);
+                                                             gap_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                             last_xchg, flush);
         else
-          event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
-                                                              st, span, fq, rq, pq, rf_get, rf_set, last_xchg,
-                                                              flush);
+          event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo,
+                                                              s_hi, gap_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                              last_xchg, flush);
       };
       if constexpr (JOIN_LDS)
         run_step(jst_l);
@@ -1039,6 +1056,14 @@ int plan_scratch(sim_graph *g) {
                     : occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
   if (ev_gen_occ < 0) return SIM_E_HIP;
   P.ev_gen_blocks = std::max(1, std::min(ev_gen_occ, P.ev_blocks));
+  // the event kernel with resource gaps: their table after the per-lane regions
+  const size_t gap_lds_bytes = P.ev_lds_bytes + (((size_t)G.R * 4 + 15) & ~size_t(15));
+  const int ev_gap_occ =
+      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, false, false, true>, gap_lds_bytes, cus)
+      : rf_lds      ? occupancy_blocks(k_event<true, false, false, false>, gap_lds_bytes, cus)
+                    : occupancy_blocks(k_event<false, false, false, false>, gap_lds_bytes, cus);
+  if (ev_gap_occ < 0) return SIM_E_HIP;
+  P.ev_gap_blocks = std::max(1, std::min(ev_gap_occ, P.ev_blocks));
   // attribution chains: busy and chain accumulators in LDS when they fit
   const size_t at_bytes = (size_t)2 * G.R * kWave * 4;
   P.at_lds = at_bytes <= 64 * 1024;
@@ -1101,6 +1126,7 @@ int plan_scratch(sim_graph *g) {
   g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   g->scratch_gen_off = take((size_t)std::max(G.n, 1) * 4);  // one generated duration column
+  g->scratch_gap_off = take((size_t)G.R * 4);                 // the resource gaps of a call
   {
     const int rc = plan_walk(g, cus);
     if (rc) return rc;
@@ -1135,25 +1161,29 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
                       const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream,
-                      const DurGen *gen = nullptr) {
+                      const DurGen *gen = nullptr, const int32_t *gap = nullptr) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
-           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}};
+           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, gap, 0};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
   const dim3 block(kWave);
   // when the last round of tiles would fill less than half the grid, use
   // fewer blocks that each take the same number of tiles (within one)
-  const int64_t blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : P.ev_blocks;
+  const int64_t blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : gap ? P.ev_gap_blocks : P.ev_blocks;
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
-  const size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
+  size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
+  if (gap) {  // the resource gap table after the per-lane regions
+    a.gap_lds = (int)lds;
+    lds += ((size_t)g->dg.R * 4 + 15) & ~size_t(15);
+  }
   const int variant = (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) | (rf_lds ? 4 : 0) |
                       (g->row_identity ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
@@ -1221,6 +1251,13 @@ int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld,
   const int64_t yb = std::min<int64_t>(gen.n_ops, std::max<int64_t>(1, 8192 / xb));
   k_generate<<<dim3((unsigned)xb, (unsigned)yb), dim3(256), 0, stream>>>(gen, n_scen, dur, ld);
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+int launch_event_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, const int32_t *gap, int32_t *makespan,
+                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, 0,
+                           nullptr, nullptr, 0, nullptr, stream, nullptr, gap);
 }
 
 int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,

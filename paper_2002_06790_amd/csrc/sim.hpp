@@ -152,6 +152,7 @@ struct ScratchPlan {
   // generated durations: persistent grids of the event and critical-path kernels
   int32_t ev_gen_blocks, cp_gen_blocks;
   int32_t ev_join_lds;  // event kernel: join state in LDS (after the resource times)
+  int32_t ev_gap_blocks;  // event kernel with resource gaps (their table in LDS)
   size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
   int32_t wk_ok;
@@ -176,7 +177,7 @@ struct sim_graph {
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
-  size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off;
+  size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off, scratch_gap_off;
   // host copies: critical-path recovery (compact predecessor CSR and the
   // caller id of each compact id) and static-order compilation (resource of
   // each op by caller id)
@@ -206,6 +207,9 @@ int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld
               const DurGen *gen = nullptr);
 // generated durations: written out, or consumed by the event replay
 int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream);
+int launch_event_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, const int32_t *gap, int32_t *makespan,
+                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 // attribution: the event replay that also records each op's predecessor on

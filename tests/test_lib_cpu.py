@@ -99,3 +99,9 @@ def test_noise_for_sigma():
     assert mlsim.noise_for_sigma(0.01) == 102739
     with pytest.raises(ValueError):
         mlsim.noise_for_sigma(0.2)
+
+
+def test_gap_argument_errors_without_gpu(L):
+    gap = np.zeros(4, np.int32)
+    assert L.sim_run_batch_gap(None, 1, None, 1, None, 0, gap.ctypes.data, None, None, 0, None, 0,
+                               None) == mlsim.SIM_E_INVAL
