@@ -23,10 +23,10 @@ MUTANTS = [
      "int32_t pa"),
     ("ignore-priority", "if (pa != pb) return pa < pb;", ""),
     ("ready-tie-by-higher-id", "return a < b;\n}", "return a > b;\n}"),
-    ("ignore-device-busy", "int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];",
+    ("ignore-device-busy", "int64_t start = w->ready[v] > avail ? w->ready[v] : avail;",
      "int64_t start = w->ready[v];"),
-    ("ignore-inputs", "int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];",
-     "int64_t start = w->rfree[r];"),
+    ("ignore-inputs", "int64_t start = w->ready[v] > avail ? w->ready[v] : avail;",
+     "int64_t start = avail;"),
     ("min-instead-of-max", "if (f > w->ready[x]) w->ready[x] = f;", "if (f < w->ready[x] || w->ready[x] == 0) w->ready[x] = f;"),
     ("ready-on-first-pred", "if (--w->cnt[x] == 0) heap_push(g, w, x);",
      "if (w->cnt[x]-- == g->indeg[x]) heap_push(g, w, x);"),
