@@ -8,7 +8,8 @@ resident before the timed region starts.  Prints one JSON line.  Outside the
 step it also times the static-order replay (every resource running its ops
 in the order the event replay ran them in scenario 0), the bottleneck
 attribution, the replay and critical path on durations generated inside the
-kernels (knob table x counter-based noise) and, on a bounded sample, the CPU
+kernels (knob table x counter-based noise), the replay with a gap per
+resource and, on a bounded sample, the CPU
 oracle, whose outputs check sampled GPU results.
 
 Default workload: the BERT-large data-parallel graph (16 workers, per-worker
@@ -177,6 +178,20 @@ def main():
         gev_ms.append(e0.elapsed_time(e1))
         gcp_ms.append(e1.elapsed_time(e2))
     log(f"generated: run {np.mean(gev_ms):.3f} ms, critical path {np.mean(gcp_ms):.3f} ms")
+    # resource gaps (outside the step): 5 us between consecutive ops on the
+    # first quarter of the resources, 2 us on the rest
+    gaps = np.full(w.n_res, 2_000, np.int32)
+    gaps[: max(1, w.n_res // 4)] = 5_000
+    g.run(dur, place=place, makespan=gmk, finish=finish, status=gst, gap=gaps)
+    torch.cuda.synchronize()
+    gap_ms = []
+    for _ in range(args.steps):
+        e0.record()
+        g.run(dur, place=place, makespan=gmk, finish=finish, status=gst, gap=gaps)
+        e1.record()
+        e1.synchronize()
+        gap_ms.append(e0.elapsed_time(e1))
+    log(f"replay with resource gaps {np.mean(gap_ms):.3f} ms")
     # the step's outputs again (the static replay reused the buffers)
     step()
     torch.cuda.synchronize()
@@ -270,7 +285,9 @@ def main():
                     "generated_run_ms": float(np.mean(gev_ms)),
                     "generated_critical_path_ms": float(np.mean(gcp_ms)),
                     "generated_run_op_events_per_s": op_events / (float(np.mean(gev_ms)) / 1e3),
-                    "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3)},
+                    "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3),
+                    "gap_run_ms": float(np.mean(gap_ms)),
+                    "gap_run_op_events_per_s": op_events / (float(np.mean(gap_ms)) / 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
