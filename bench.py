@@ -182,12 +182,14 @@ def main():
     # first quarter of the resources, 2 us on the rest
     gaps = np.full(w.n_res, 2_000, np.int32)
     gaps[: max(1, w.n_res // 4)] = 5_000
-    g.run(dur, place=place, makespan=gmk, finish=finish, status=gst, gap=gaps)
+    pmk = torch.empty(S, dtype=torch.int32, device="cuda")
+    pst = torch.empty(S, dtype=torch.int32, device="cuda")
+    g.run(dur, place=place, makespan=pmk, finish=finish, status=pst, gap=gaps)
     torch.cuda.synchronize()
     gap_ms = []
     for _ in range(args.steps):
         e0.record()
-        g.run(dur, place=place, makespan=gmk, finish=finish, status=gst, gap=gaps)
+        g.run(dur, place=place, makespan=pmk, finish=finish, status=pst, gap=gaps)
         e1.record()
         e1.synchronize()
         gap_ms.append(e0.elapsed_time(e1))
