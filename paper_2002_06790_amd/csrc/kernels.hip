@@ -65,12 +65,13 @@ __device__ __forceinline__ int4 settle(int4 v) {
 //
 // Positions run breadth-first from kRoot = 7, which puts the 8 children of
 // position p at 8 (p - 6) ... 8 (p - 6) + 7: every child group is aligned to
-// 8 entries.  The root and its 8 children are kept in registers (the
-// children's array is only indexed through unrolled selects, so it stays in
-// registers); positions 16 .. le - 1 (the first (le - 16) / 8 groups of the
-// root's grandchildren, which breadth-first order fills first) live in LDS,
-// slot-major x lane, conflict-free; positions from le on live in global
-// scratch, lane-major, so
+// 8 entries.  The root is kept in a register, and with REG so are its 8
+// children (an array read through selects only, so it stays in registers):
+// that frees 4 KB of LDS per wavefront for more resident wavefronts at the
+// price of some VALU work per step.  The next positions up to le - 1 (the
+// children unless REG, then the first groups of the root's grandchildren,
+// which breadth-first order fills first) live in LDS, slot-major x lane,
+// conflict-free; positions from le on live in global scratch, lane-major, so
 // one child group there is one aligned 64-byte segment of one lane.  Every
 // position at or beyond the end holds kEmpty, which is larger than any key,
 // so partial groups need no bounds masks; the kernel restores kEmpty
@@ -81,16 +82,19 @@ constexpr uint64_t kEmpty = ~0ull;
 __device__ __forceinline__ int heap_parent(int p) { return p / kD + (kRoot - 1); }
 __device__ __forceinline__ int heap_child0(int p) { return kD * (p - (kRoot - 1)); }
 
+template <bool REG>
 struct WideHeap {
+  static constexpr int kLB = REG ? kL2 : kL1;  // first heap position in LDS
   uint64_t root;     // position kRoot
-  uint64_t ch[kD];   // positions kL1 .. kL2 - 1: the root's children
-  lptr<uint64_t> l;  // this lane's LDS column: position p (kL2 .. le-1) at l[(p - kL2) * kWave]
+  uint64_t ch[kD];   // REG: positions kL1 .. kL2 - 1, the root's children
+  lptr<uint64_t> l;  // this lane's LDS column: position p (kLB .. le-1) at l[(p - kLB) * kWave]
   uint64_t *g;       // this lane's global run: position p (>= le) at g[p - le]
   int le;            // first position in global memory (kL2 + kD k)
-  // child k of the root (k lane-dependent): a tree of selects on the bits of
-  // k (a chain of equality selects would be turned back into an indexed load,
-  // which would move the array to scratch memory)
+  // child k of the root (k lane-dependent).  REG: a tree of selects on the
+  // bits of k (a chain of equality selects would be turned back into an
+  // indexed load, which would move the array to scratch memory)
   __device__ __forceinline__ uint64_t child(int k) const {
+    if (!REG) return l[k * kWave];
     const bool b0 = k & 1, b1 = k & 2, b2 = k & 4;
     const uint64_t a01 = b0 ? ch[1] : ch[0], a23 = b0 ? ch[3] : ch[2];
     const uint64_t a45 = b0 ? ch[5] : ch[4], a67 = b0 ? ch[7] : ch[6];
@@ -98,26 +102,35 @@ struct WideHeap {
     return b2 ? a47 : a03;
   }
   __device__ __forceinline__ void set_child(int k, uint64_t x) {
+    if (!REG) {
+      l[k * kWave] = x;
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < kD; ++j) ch[j] = k == j ? x : ch[j];
   }
+  // all 8 children of the root
+  __device__ __forceinline__ void children(uint64_t (&v)[kD]) const {
+#pragma unroll
+    for (int k = 0; k < kD; ++k) v[k] = REG ? ch[k] : l[k * kWave];
+  }
   __device__ __forceinline__ uint64_t get(int p) const {
-    if (p < kL2) return child(p - kL1);
-    if (p < le) return l[(p - kL2) * kWave];
+    if (REG && p < kL2) return child(p - kL1);
+    if (p < le) return l[(p - kLB) * kWave];
     return settle(g[p - le]);
   }
   __device__ __forceinline__ void set(int p, uint64_t x) {
-    if (p < kL2)
+    if (REG && p < kL2)
       set_child(p - kL1, x);
     else if (p < le)
-      l[(p - kL2) * kWave] = x;
+      l[(p - kLB) * kWave] = x;
     else
       g[p - le] = x;
   }
-  // the group starting at c (kL2 <= c < le, a multiple of kD) in LDS
+  // the group starting at c (kLB <= c < le, a multiple of kD) in LDS
   __device__ __forceinline__ void lds_group(int c, uint64_t (&v)[kD]) const {
 #pragma unroll
-    for (int k = 0; k < kD; ++k) v[k] = l[(c + k - kL2) * kWave];
+    for (int k = 0; k < kD; ++k) v[k] = l[(c + k - kLB) * kWave];
   }
   // the group starting at c >= le: one aligned 64-byte segment
   __device__ __forceinline__ void global_group(int c, uint64_t (&v)[kD]) const {
@@ -153,7 +166,8 @@ __device__ __forceinline__ void min_group(uint64_t (&v)[kD], uint64_t &m, int &q
 // Place x at position p (a grandchild of the root or deeper) of a heap
 // ending at `end` and restore heap order below it; every group below a
 // grandchild of the root lies in global memory (one round trip per level).
-__device__ __forceinline__ void sift_down_deep(WideHeap &h, int end, int p, uint64_t x) {
+template <class H>
+__device__ __forceinline__ void sift_down_deep(H &h, int end, int p, uint64_t x) {
   for (;;) {
     const int c = heap_child0(p);
     if (c >= end) break;
@@ -169,7 +183,8 @@ __device__ __forceinline__ void sift_down_deep(WideHeap &h, int end, int p, uint
 }
 
 // Append x and restore heap order above it.
-__device__ __forceinline__ void heap_push(WideHeap &h, int &end, uint64_t x) {
+template <class H>
+__device__ __forceinline__ void heap_push(H &h, int &end, uint64_t x) {
   int p = end++;
   while (p > kRoot) {
     const int par = heap_parent(p);
@@ -199,11 +214,10 @@ struct HeapAhead {
   uint64_t last;    // the last element when it sits in global memory
 };
 
-template <bool DEEP>
-__device__ __forceinline__ void heap_look_ahead(const WideHeap &h, int end, HeapAhead &A) {
+template <bool DEEP, class H>
+__device__ __forceinline__ void heap_look_ahead(const H &h, int end, HeapAhead &A) {
   uint64_t v[kD];
-#pragma unroll
-  for (int k = 0; k < kD; ++k) v[k] = h.ch[k];  // all kEmpty when the root has no children
+  h.children(v);  // all kEmpty when the root has no children
   min_group(v, A.m1, A.q1);
   A.q1 += kL1;
   A.c2 = heap_child0(A.q1);
@@ -231,7 +245,8 @@ __device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
 }
 
 // Replace the root by x (the first op a step releases), using the look-ahead.
-__device__ __forceinline__ void heap_replace_root(WideHeap &h, int end, const HeapAhead &A, uint64_t x) {
+template <class H>
+__device__ __forceinline__ void heap_replace_root(H &h, int end, const HeapAhead &A, uint64_t x) {
   if (x < A.m1) {  // also when the root has no children (m1 = kEmpty)
     h.root = x;
     return;
@@ -247,7 +262,8 @@ __device__ __forceinline__ void heap_replace_root(WideHeap &h, int end, const He
 }
 
 // Remove the root when the step released nothing, using the look-ahead.
-__device__ __forceinline__ void heap_pop_root(WideHeap &h, int &end, HeapAhead &A) {
+template <class H>
+__device__ __forceinline__ void heap_pop_root(H &h, int &end, HeapAhead &A) {
   const int lp = --end;  // position of the last element
   if (lp == kRoot) {
     h.root = kEmpty;
@@ -258,16 +274,15 @@ __device__ __forceinline__ void heap_pop_root(WideHeap &h, int &end, HeapAhead &
     x = h.child(lp - kL1);
     h.set_child(lp - kL1, kEmpty);
   } else if (lp < h.le) {
-    x = h.l[(lp - kL2) * kWave];
-    h.l[(lp - kL2) * kWave] = kEmpty;
+    x = h.l[(lp - H::kLB) * kWave];
+    h.l[(lp - H::kLB) * kWave] = kEmpty;
   } else {
     x = A.last;
     h.g[lp - h.le] = kEmpty;
   }
   if (lp < kL2) {  // a child of the root left: rescan them (no grandchildren remain)
     uint64_t v[kD];
-#pragma unroll
-    for (int k = 0; k < kD; ++k) v[k] = h.ch[k];
+    h.children(v);
     min_group(v, A.m1, A.q1);
     A.q1 += kL1;
     A.c2 = heap_child0(A.q1);
@@ -329,9 +344,9 @@ struct JoinLds {
 
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
-template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class JPtr,
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class Heap, class JPtr,
           class RfGet, class RfSet, class LastXchg, class Flush>
-__device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, WideHeap &heap,
+__device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, Heap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
                                            uint32_t s_hi, lptr<const int32_t> gap_l, uint32_t &st,
@@ -450,8 +465,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, W
 // waited for once per burst instead of once per step.  GEN: durations are
 // generated from the knob grid and counter-based noise of a.gen instead of
 // read from a.dur.  JOIN_LDS: the join state lives in LDS after the resource
-// times (and last-op table) instead of in global scratch.
-template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool JOIN_LDS = false>
+// times (and last-op table) instead of in global scratch.  REG: the heap
+// root's children live in registers (see WideHeap).
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool JOIN_LDS = false,
+          bool REG = false>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -463,11 +480,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     __syncthreads();
   }
   const lptr<const int32_t> gap_l = (lptr<const int32_t>)gap_w;
-  WideHeap heap;
+  WideHeap<REG> heap;
   heap.l = as_lds(lds) + lane;
   heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
   heap.le = a.heap_le;
-  const int heap_lds = a.heap_le - kL2;  // heap positions per lane kept in LDS
+  const int heap_lds = a.heap_le - WideHeap<REG>::kLB;  // heap positions per lane kept in LDS
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)heap_lds * kWave)) + lane;
   const JoinGlobal jst_g{a.join_g + (size_t)blockIdx.x * G.J * kWave + lane};
@@ -526,8 +543,9 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       }
     for (int k = 0; k < heap_lds; ++k) heap.l[k * kWave] = kEmpty;
     heap.root = kEmpty;
+    if (REG)
 #pragma unroll
-    for (int k = 0; k < kD; ++k) heap.ch[k] = kEmpty;
+      for (int k = 0; k < kD; ++k) heap.ch[k] = kEmpty;
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
     uint32_t st = 0, span = 0;
@@ -1028,19 +1046,51 @@ int plan_scratch(sim_graph *g) {
   if (const char *e = getenv("MLSIM_JOIN_LDS"))  // tuning override
     P.ev_join_lds = rf_lds && G.J > 0 && atoi(e) != 0;
   const size_t join_lds_bytes = P.ev_join_lds ? join_bytes : 0;
-  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes + join_lds_bytes;
-  const int ev_occ = P.ev_join_lds
-                         ? occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes, cus)
-                     : rf_lds ? occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus)
-                              : occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
-  if (ev_occ < 0) return SIM_E_HIP;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = (P.ev_join_lds ? 0 : join_bytes) + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
-  size_t ev_blocks = (size_t)ev_occ;
-  if (ev_per_block) ev_blocks = std::min(ev_blocks, std::max<size_t>(1, kScratchBudget / ev_per_block));
-  if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
-    ev_blocks = std::min(ev_blocks, (size_t)std::max(1, atoi(e)));
-  P.ev_blocks = (int32_t)std::max<size_t>(1, ev_blocks);
+  const size_t gap_table = ((size_t)G.R * 4 + 15) & ~size_t(15);  // resource gaps, after the per-lane regions
+  auto grid_of = [&](int occ) -> int32_t {  // resident blocks within the scratch budget
+    size_t b = (size_t)std::max(occ, 1);
+    if (ev_per_block) b = std::min(b, std::max<size_t>(1, kScratchBudget / ev_per_block));
+    if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
+      b = std::min(b, (size_t)std::max(1, atoi(e)));
+    return (int32_t)b;
+  };
+  // the root's children in LDS (every variant)
+  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes + join_lds_bytes;
+  int occ[3];  // plain, generated durations, resource gaps
+  if (P.ev_join_lds) {
+    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes, cus);
+    occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_lds_bytes, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes + gap_table, cus);
+  } else if (rf_lds) {
+    occ[0] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus);
+    occ[1] = occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes + gap_table, cus);
+  } else {
+    occ[0] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
+    occ[1] = occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
+    occ[2] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes + gap_table, cus);
+  }
+  if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
+  P.ev_blocks = grid_of(occ[0]);
+  P.ev_gen_blocks = grid_of(occ[1]);
+  P.ev_gap_blocks = grid_of(occ[2]);
+  // the root's children in registers (resource times in LDS, join state in
+  // global memory, no placement, no predecessor recording): 4 KB less LDS
+  P.ev_reg = rf_lds && !P.ev_join_lds;
+  P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
+  P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_gap_blocks = 1;
+  if (P.ev_reg) {
+    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
+    occ[1] = occupancy_blocks(k_event<true, false, false, false, true, false, true>, P.ev_reg_lds_bytes, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, false, true>,
+                              P.ev_reg_lds_bytes + gap_table, cus);
+    if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
+    P.ev_reg_blocks = grid_of(occ[0]);
+    P.ev_reg_gen_blocks = grid_of(occ[1]);
+    P.ev_reg_gap_blocks = grid_of(occ[2]);
+  }
   // the event kernel for attribution: a last-op table beside the resource times
   P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
   const int ev_prev_occ =
@@ -1048,22 +1098,7 @@ int plan_scratch(sim_graph *g) {
       : rf_lds      ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
                     : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
-  P.ev_prev_blocks = std::max(1, std::min(ev_prev_occ, P.ev_blocks));
-  // the event kernel with generated durations: same LDS and scratch per block
-  const int ev_gen_occ =
-      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_lds_bytes, cus)
-      : rf_lds      ? occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus)
-                    : occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
-  if (ev_gen_occ < 0) return SIM_E_HIP;
-  P.ev_gen_blocks = std::max(1, std::min(ev_gen_occ, P.ev_blocks));
-  // the event kernel with resource gaps: their table after the per-lane regions
-  const size_t gap_lds_bytes = P.ev_lds_bytes + (((size_t)G.R * 4 + 15) & ~size_t(15));
-  const int ev_gap_occ =
-      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, false, false, true>, gap_lds_bytes, cus)
-      : rf_lds      ? occupancy_blocks(k_event<true, false, false, false>, gap_lds_bytes, cus)
-                    : occupancy_blocks(k_event<false, false, false, false>, gap_lds_bytes, cus);
-  if (ev_gap_occ < 0) return SIM_E_HIP;
-  P.ev_gap_blocks = std::max(1, std::min(ev_gap_occ, P.ev_blocks));
+  P.ev_prev_blocks = grid_of(ev_prev_occ);
   // attribution chains: busy and chain accumulators in LDS when they fit
   const size_t at_bytes = (size_t)2 * G.R * kWave * 4;
   P.at_lds = at_bytes <= 64 * 1024;
@@ -1074,7 +1109,9 @@ int plan_scratch(sim_graph *g) {
   P.at_blocks = (int32_t)(P.at_lds ? at_occ
                                    : std::min<size_t>(at_occ, std::max<size_t>(1, kScratchBudget / at_bytes)));
 
-  const int32_t ev_grid = P.ev_blocks;
+  // scratch for the largest persistent grid of any event variant
+  const int32_t ev_grid = std::max({P.ev_blocks, P.ev_gen_blocks, P.ev_gap_blocks, P.ev_prev_blocks,
+                                    P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_gap_blocks});
 
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
@@ -1174,25 +1211,38 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   const dim3 block(kWave);
   // when the last round of tiles would fill less than half the grid, use
   // fewer blocks that each take the same number of tiles (within one)
-  const int64_t blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : gap ? P.ev_gap_blocks : P.ev_blocks;
+  // registers for the heap root's children when the chip is full: the
+  // variant with the children in LDS would need two or more rounds of tiles
+  const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : gap ? P.ev_gap_blocks : P.ev_blocks;
+  bool reg = P.ev_reg && !place && !prev && tiles >= 2 * lds_blocks;
+  if (const char *e = getenv("MLSIM_EV_REG"))  // tuning override
+    reg = P.ev_reg && !place && !prev && atoi(e) != 0;
+  const int64_t blocks = !reg ? lds_blocks : gen ? P.ev_reg_gen_blocks : gap ? P.ev_reg_gap_blocks : P.ev_reg_blocks;
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
-  size_t lds = prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes;
+  size_t lds = prev ? P.ev_prev_lds_bytes : reg ? P.ev_reg_lds_bytes : P.ev_lds_bytes;
   if (gap) {  // the resource gap table after the per-lane regions
     a.gap_lds = (int)lds;
     lds += ((size_t)g->dg.R * 4 + 15) & ~size_t(15);
   }
-  const int variant = (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) | (rf_lds ? 4 : 0) |
-                      (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+  const int variant = (reg ? 64 : 0) | (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
+                      (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_GEN_CASE(V, A, B) \
   case V: k_event<A, B, false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_JOIN_CASE(V, B, C, D, E) \
   case V: k_event<true, B, C, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+#define EV_REG_CASE(V, B, E) \
+  case V: k_event<true, B, false, false, E, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
+    // the heap root's children in registers
+    EV_REG_CASE(68, false, false)
+    EV_REG_CASE(70, true, false)
+    EV_REG_CASE(84, false, true)
+    EV_REG_CASE(86, true, true)
     // join state in LDS (always with resource times in LDS)
     EV_JOIN_CASE(36, false, false, false, false)
     EV_JOIN_CASE(37, false, true, false, false)
@@ -1228,6 +1278,7 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
 #undef EV_CASE
 #undef EV_GEN_CASE
 #undef EV_JOIN_CASE
+#undef EV_REG_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

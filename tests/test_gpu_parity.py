@@ -195,6 +195,44 @@ def test_heap_groups_in_lds(mlsim, groups, monkeypatch):
         check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
 
 
+@pytest.mark.parametrize("groups", ["0", "1", "2", "4"])
+def test_heap_children_in_registers(mlsim, groups, monkeypatch):
+    """The event kernel with the heap root's children in registers (chosen
+    by the launcher when the chip is full; forced here on small and ragged
+    batches), with 0-4 grandchild groups in LDS, equals the oracle: plain,
+    with resource gaps and with generated durations."""
+    monkeypatch.setenv("MLSIM_EV_REG", "1")
+    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    for k, S in ((4, 130), (2, 100), (1, 1024), (3, 70)):
+        w = W.make_config(k, n_scen=S if k != 1 else None)
+        dur = w.durations()
+        check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur)
+        gap = np.arange(w.n_res, dtype=np.int32) * 397
+        g = mlsim.Graph.from_workload(w)
+        mk, fin, st = g.run(dev(dur), want_finish=True, gap=gap)
+        torch.cuda.synchronize()
+        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, gap=gap)
+        assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(fin.cpu().numpy(), ofin)
+        base = w.gen_base()
+        gen = mlsim.Gen(dev(base), knob_block=29, noise=102739, seed=k)
+        S2 = dur.shape[1]
+        mk, fin, st = g.run_generated(gen, S2, want_finish=True)
+        torch.cuda.synchronize()
+        gdur = oracle.generate(base, S2, 29, 102739, k)
+        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, gdur)
+        assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(fin.cpu().numpy(), ofin)
+        g.close()
+    rng = np.random.default_rng(78)
+    for case in range(12):  # random graphs with priorities, then wide ones with heaps beyond LDS
+        if case < 6:
+            n, R, p = int(rng.integers(1, 70)), int(rng.integers(1, 9)), float(rng.uniform(0, 0.3))
+        else:
+            n, R, p = int(rng.integers(100, 600)), int(rng.integers(1, 5)), 0.01
+        ptr, idx, res, pr, dur = rand_case(rng, n, R, p, bool(rng.integers(2)), bool(rng.integers(2)),
+                                           int(rng.choice([1, 63, 65, 130])), 1, int(rng.choice([3, 1000])))
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
+
+
 @pytest.mark.parametrize("slots", ["lds", "global"])
 def test_critical_path_slots(mlsim, slots, monkeypatch):
     """The critical-path sweep with its value slots in LDS or in global
