@@ -305,6 +305,14 @@ int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, const int32_
                                 int64_t scen0, int32_t *cp_len, int64_t path_scen, int32_t *path_ops,
                                 int32_t path_cap, int32_t *path_len, void *stream);
 
+/* sim_static_run on generated durations (the generation arguments above);
+ * makespan, finish, ld_fin, status and stream as sim_static_run.  Calls on
+ * different streams sharing one object must not overlap in time. */
+int sim_static_run_generated(const sim_static *st, int64_t n_scen, const int32_t *base,
+                             int32_t n_knobs, int64_t knob_block, uint32_t noise, uint64_t seed,
+                             int64_t scen0, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                             int32_t *status, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,7 +29,7 @@ ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
            "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
-           "sim_critical_path_generated", "sim_run_batch_gap")
+           "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -94,6 +94,8 @@ def _load():
     L.sim_critical_path_generated.restype = ctypes.c_int
     L.sim_run_batch_gap.argtypes = [P, I64, P, I64, P, I64, P, P, P, I64, P, U32, P]
     L.sim_run_batch_gap.restype = ctypes.c_int
+    L.sim_static_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, P]
+    L.sim_static_run_generated.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -401,4 +403,25 @@ class StaticReplay:
                                     status.data_ptr(), _stream_ptr(stream))
         if rc:
             raise SimError(rc, "sim_static_run")
+        return makespan, finish, status
+
+    def run_generated(self, gen: Gen, n_scen: int, want_finish: bool = False, makespan=None, finish=None,
+                      status=None, stream=None):
+        """The static-order replay of ``n_scen`` scenarios whose durations the
+        kernel generates from ``gen`` (sim_static_run_generated)."""
+        import torch
+        if gen.n_ops != self.n_ops:
+            raise ValueError("base table does not match the graph's op count")
+        dev = gen.base.device
+        if makespan is None:
+            makespan = torch.empty(n_scen, dtype=torch.int32, device=dev)
+        if status is None:
+            status = torch.empty(n_scen, dtype=torch.int32, device=dev)
+        if want_finish and finish is None:
+            finish = torch.empty((self.n_ops, n_scen), dtype=torch.int32, device=dev)
+        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        rc = _load().sim_static_run_generated(self._h, n_scen, *gen.args(), makespan.data_ptr(), fptr, ldf,
+                                              status.data_ptr(), _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_static_run_generated")
         return makespan, finish, status

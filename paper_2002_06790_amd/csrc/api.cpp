@@ -13,17 +13,6 @@ bool bad_matrix(const void *p, int64_t ld, int64_t n_scen, int32_t n_ops) {
   return n_ops > 0 && n_scen > 0 && (!p || ld < n_scen);
 }
 
-// Generation parameters, checked: SIM_OK or SIM_E_INVAL.
-int make_gen(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs, int64_t knob_block,
-             uint32_t noise, uint64_t seed, int64_t scen0, DurGen &gen) {
-  if (n_knobs < 1 || knob_block < 1 || scen0 < 0 || noise >= kGenNoiseMax) return SIM_E_INVAL;
-  if (n_scen > INT64_MAX - scen0) return SIM_E_INVAL;
-  if (n_ops > 0 && !base) return SIM_E_INVAL;
-  if ((int64_t)n_knobs * n_ops > INT64_MAX / 4) return SIM_E_INVAL;
-  gen = DurGen{base, n_ops, n_knobs, knob_block, scen0, noise, (uint32_t)seed, (uint32_t)(seed >> 32)};
-  return SIM_OK;
-}
-
 // Walk back from the lowest-id op of maximum dist, each time to the
 // lowest-id predecessor p with dist(p) = dist(v) - d(v); the path from its
 // first op to its last goes to path_ops (up to path_cap), its length to
@@ -61,6 +50,18 @@ void walk_critical_path(const sim_graph *g, const std::vector<int32_t> &dist, co
 }
 
 }  // namespace
+
+namespace mlsim {
+int make_gen(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs, int64_t knob_block,
+             uint32_t noise, uint64_t seed, int64_t scen0, DurGen &gen) {
+  if (n_knobs < 1 || knob_block < 1 || scen0 < 0 || noise >= kGenNoiseMax) return SIM_E_INVAL;
+  if (n_scen > INT64_MAX - scen0) return SIM_E_INVAL;
+  if (n_ops > 0 && !base) return SIM_E_INVAL;
+  if ((int64_t)n_knobs * n_ops > INT64_MAX / 4) return SIM_E_INVAL;
+  gen = DurGen{base, n_ops, n_knobs, knob_block, scen0, noise, (uint32_t)seed, (uint32_t)(seed >> 32)};
+  return SIM_OK;
+}
+}  // namespace mlsim
 
 extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                              const uint16_t *place, int64_t ld_place, int32_t *makespan,

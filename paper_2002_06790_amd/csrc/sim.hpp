@@ -209,6 +209,9 @@ int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, i
 int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
               const DurGen *gen = nullptr);
+// generation parameters of a call, checked (SIM_OK or SIM_E_INVAL)
+int make_gen(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs, int64_t knob_block,
+             uint32_t noise, uint64_t seed, int64_t scen0, DurGen &gen);
 // generated durations: written out, or consumed by the event replay
 int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream);
 int launch_event_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,

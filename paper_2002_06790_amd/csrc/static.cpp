@@ -16,6 +16,7 @@ struct sim_static {
   MpTable tab;      // device view of the records and long predecessor lists
   int mode;         // where the sweep's value slots live
   int blocks;       // persistent grid
+  int gen_blocks;   // persistent grid with generated durations
   size_t lds;       // LDS bytes per block
   void *dev_mem;    // records and predecessor lists
   uint32_t *slots;  // global value slots when they do not fit LDS
@@ -114,6 +115,12 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
     }
   }
   st->blocks = std::max(1, blocks);
+  const int gen_blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount, true);
+  if (gen_blocks < 0) {
+    sim_static_destroy(st);
+    return SIM_E_HIP;
+  }
+  st->gen_blocks = std::max(1, std::min(gen_blocks, st->blocks));  // within the slot scratch
   *out = st;
   return SIM_OK;
 }
@@ -142,4 +149,24 @@ extern "C" int sim_static_run(const sim_static *st, int64_t n_scen, const int32_
   }
   return launch_maxplus(st->tab, st->mode, st->blocks, st->lds, n_scen, dur, ld_dur, makespan, status,
                         finish, ld_fin, nullptr, 0, st->slots, s);
+}
+
+extern "C" int sim_static_run_generated(const sim_static *st, int64_t n_scen, const int32_t *base,
+                                        int32_t n_knobs, int64_t knob_block, uint32_t noise, uint64_t seed,
+                                        int64_t scen0, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                                        int32_t *status, void *stream) {
+  if (!st || n_scen < 0) return SIM_E_INVAL;
+  DurGen gen;
+  if (int rc = make_gen(st->n_ops, n_scen, base, n_knobs, knob_block, noise, seed, scen0, gen)) return rc;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (st->n_ops == 0) {
+    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    return SIM_OK;
+  }
+  return launch_maxplus(st->tab, st->mode, st->gen_blocks, st->lds, n_scen, nullptr, 0, makespan, status,
+                        finish, ld_fin, nullptr, 0, st->slots, s, &gen);
 }

@@ -179,3 +179,26 @@ def test_empty_and_tiny(mlsim):
     with pytest.raises(mlsim.SimError):
         G.run_generated(g, 4, algo="sweep")
     G.close()
+
+
+@pytest.mark.parametrize("k", [1, 2, 4])
+def test_static_replay_generated(mlsim, k):
+    """The static-order replay on generated durations equals the oracle's
+    static-order replay of the oracle's generated durations."""
+    w = W.make_config(k, n_scen=64)
+    base = w.gen_base()
+    S = 150
+    G = mlsim.Graph.from_workload(w)
+    order = np.arange(w.n_ops, dtype=np.int32)  # op ids are emitted in topological order
+    sr = G.static_order(order)
+    g = gen_of(mlsim, base, 7, SIGMA1, 11, 3)
+    mk, fin, st = sr.run_generated(g, S, want_finish=True)
+    mk0, _, st0 = sr.run_generated(g, S)
+    torch.cuda.synchronize()
+    dur = oracle.generate(base, S, 7, SIGMA1, 11, scen0=3)
+    omk, ofin, ost = oracle.static_run(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, order, dur)
+    assert np.array_equal(st.cpu().numpy(), ost) and (ost == 0).all()
+    assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(mk0.cpu().numpy(), omk)
+    assert np.array_equal(fin.cpu().numpy(), ofin)
+    sr.close()
+    G.close()
