@@ -1080,7 +1080,8 @@ int plan_scratch(sim_graph *g) {
   // global memory, no placement, no predecessor recording): 4 KB less LDS
   P.ev_reg = rf_lds && !P.ev_join_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
-  P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_gap_blocks = 1;
+  P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_gap_blocks = P.ev_reg_prev_blocks = 1;
+  P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + rf_lds_bytes;  // with the last-op table
   if (P.ev_reg) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, false, true>, P.ev_reg_lds_bytes, cus);
@@ -1090,6 +1091,10 @@ int plan_scratch(sim_graph *g) {
     P.ev_reg_blocks = grid_of(occ[0]);
     P.ev_reg_gen_blocks = grid_of(occ[1]);
     P.ev_reg_gap_blocks = grid_of(occ[2]);
+    const int prev_occ =
+        occupancy_blocks(k_event<true, false, false, true, false, false, true>, P.ev_reg_prev_lds_bytes, cus);
+    if (prev_occ < 0) return SIM_E_HIP;
+    P.ev_reg_prev_blocks = grid_of(prev_occ);
   }
   // the event kernel for attribution: a last-op table beside the resource times
   P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
@@ -1111,7 +1116,8 @@ int plan_scratch(sim_graph *g) {
 
   // scratch for the largest persistent grid of any event variant
   const int32_t ev_grid = std::max({P.ev_blocks, P.ev_gen_blocks, P.ev_gap_blocks, P.ev_prev_blocks,
-                                    P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_gap_blocks});
+                                    P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_gap_blocks,
+                                    P.ev_reg_prev_blocks});
 
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
@@ -1214,15 +1220,20 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   // registers for the heap root's children when the chip is full: the
   // variant with the children in LDS would need two or more rounds of tiles
   const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : gap ? P.ev_gap_blocks : P.ev_blocks;
-  bool reg = P.ev_reg && !place && !prev && tiles >= 2 * lds_blocks;
+  bool reg = P.ev_reg && !place && tiles >= 2 * lds_blocks;
   if (const char *e = getenv("MLSIM_EV_REG"))  // tuning override
-    reg = P.ev_reg && !place && !prev && atoi(e) != 0;
-  const int64_t blocks = !reg ? lds_blocks : gen ? P.ev_reg_gen_blocks : gap ? P.ev_reg_gap_blocks : P.ev_reg_blocks;
+    reg = P.ev_reg && !place && atoi(e) != 0;
+  const int64_t blocks = !reg ? lds_blocks
+                         : prev ? P.ev_reg_prev_blocks
+                         : gen  ? P.ev_reg_gen_blocks
+                         : gap  ? P.ev_reg_gap_blocks
+                                : P.ev_reg_blocks;
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
-  size_t lds = prev ? P.ev_prev_lds_bytes : reg ? P.ev_reg_lds_bytes : P.ev_lds_bytes;
+  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
+                   : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
   if (gap) {  // the resource gap table after the per-lane regions
     a.gap_lds = (int)lds;
     lds += ((size_t)g->dg.R * 4 + 15) & ~size_t(15);
@@ -1235,14 +1246,16 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   case V: k_event<A, B, false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_JOIN_CASE(V, B, C, D, E) \
   case V: k_event<true, B, C, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
-#define EV_REG_CASE(V, B, E) \
-  case V: k_event<true, B, false, false, E, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+#define EV_REG_CASE(V, B, D, E) \
+  case V: k_event<true, B, false, D, E, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
     // the heap root's children in registers
-    EV_REG_CASE(68, false, false)
-    EV_REG_CASE(70, true, false)
-    EV_REG_CASE(84, false, true)
-    EV_REG_CASE(86, true, true)
+    EV_REG_CASE(68, false, false, false)
+    EV_REG_CASE(70, true, false, false)
+    EV_REG_CASE(76, false, true, false)
+    EV_REG_CASE(78, true, true, false)
+    EV_REG_CASE(84, false, false, true)
+    EV_REG_CASE(86, true, false, true)
     // join state in LDS (always with resource times in LDS)
     EV_JOIN_CASE(36, false, false, false, false)
     EV_JOIN_CASE(37, false, true, false, false)

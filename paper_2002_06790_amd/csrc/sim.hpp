@@ -155,8 +155,8 @@ struct ScratchPlan {
   int32_t ev_gap_blocks;  // event kernel with resource gaps (their table in LDS)
   // event kernel with the heap root's children in registers: available,
   // persistent grids (plain, generated durations, gaps) and LDS per block
-  int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_gap_blocks;
-  size_t ev_reg_lds_bytes;
+  int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_gap_blocks, ev_reg_prev_blocks;
+  size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
   int32_t wk_ok;

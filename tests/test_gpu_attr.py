@@ -102,6 +102,24 @@ def test_attr_random_graphs(mlsim):
         check_attr(mlsim, ptr, idx, res, R, dur, prio=pr, place=place, path_scen=int(rng.integers(S)))
 
 
+@pytest.mark.parametrize("groups", ["1", "2"])
+def test_attr_heap_children_in_registers(mlsim, groups, monkeypatch):
+    """The recording replay with the heap root's children in registers
+    (chosen by the launcher when the chip is full; forced here)."""
+    monkeypatch.setenv("MLSIM_EV_REG", "1")
+    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    for k, S in ((4, 130), (2, 70), (1, 1024)):
+        w = W.make_config(k, n_scen=S)
+        check_attr(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), prio=w.prio,
+                   path_scen=S - 1)
+    rng = np.random.default_rng(2719)
+    for case in range(10):
+        n, R, S = int(rng.integers(1, 80)), int(rng.integers(1, 9)), int(rng.choice([1, 65, 130]))
+        ptr, idx, res, pr = W.random_dag(n, R, float(rng.uniform(0, 0.3)), rng, with_prio=True)
+        dur = W.random_durations(n, S, 1, int(rng.choice([3, 1000])), rng)
+        check_attr(mlsim, ptr, idx, res, R, dur, prio=pr, path_scen=int(rng.integers(S)))
+
+
 def test_attr_status_and_empty(mlsim):
     ptr = np.array([0, 1, 2, 2], np.int64)
     idx = np.array([1, 2], np.int32)
