@@ -25,6 +25,12 @@ constexpr int32_t kReduceMaxOps = 32768;  // transitive reduction bitsets: n^2/8
 struct Compiled {
   std::vector<OpRec> ops;
   std::vector<int32_t> succ, jneed, src, cp_pred, pred_ptr, pred, topo;
+  std::vector<int32_t> jtarget;  // [J] the op a join releases: its own op, or a barrier's first member
+  // event kernel: records and successor entries holding heap-key words,
+  // {predecessors needed, word released} per join, source words
+  std::vector<OpRec> ev_ops;
+  std::vector<int32_t> ev_succ, jinfo, ev_src;
+  int32_t pk_sh = 0, pk_join = 0, pk_jn = 0;
   std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
   int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0, barriers = 0;
@@ -306,14 +312,17 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   std::vector<int32_t> join(n + nb, -1);  // kJoinNone for plain successors
   C.J = 0;
   C.jneed.clear();
+  C.jtarget.clear();
   for (int32_t k = 0; k < n; ++k)
     if (need[ctopo[k]] >= 2) {
       join[ctopo[k]] = C.J++;
       C.jneed.push_back(need[ctopo[k]]);
+      C.jtarget.push_back(ctopo[k]);
     }
   for (int32_t b = 0; b < nb; ++b) {
     join[n + b] = C.J++;
     C.jneed.push_back(bneed[b]);
+    C.jtarget.push_back(bmem[b][0]);
   }
   C.max_indeg = 0;
   for (int32_t c = 0; c < n; ++c) C.max_indeg = std::max(C.max_indeg, (int32_t)cp[c].size());
@@ -354,6 +363,56 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   C.src.clear();
   for (int32_t c = 0; c < n; ++c)
     if (cp[c].empty()) C.src.push_back(c);
+
+  // Heap-key words of the event kernel.  The low 32 bits of a ready-list key
+  // hold the compact id; when the bits allow, they also hold the join index
+  // of the op's first successor entry (all ones: not a join) below it, so a
+  // popped op's first join state can be read together with its record
+  // instead of after it.  The id in the top bits keeps the key order (ids
+  // are distinct).  (A second field for the second entry measured slower on
+  // the BERT workload: 39.5 vs 37.1 ms.)
+  {
+    int32_t jb = 0;
+    while ((1ll << jb) < (int64_t)C.J + 1) ++jb;
+    const bool pack = jb > 0 && jb < 32 && (int64_t)n <= (1ll << (32 - jb));
+    C.pk_sh = pack ? jb : 0;
+    C.pk_join = pack;
+    const uint32_t jnone = pack ? (1u << jb) - 1u : 0u;
+    auto word = [&](int32_t c) -> int32_t {  // c: a compact op id (never a barrier)
+      if (!pack || c < 0 || c >= n) return c;
+      const OpRec &r = C.ops[c];
+      const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)r.j0 : jnone;
+      return (int32_t)(((uint32_t)c << jb) | jf);
+    };
+    // A join entry can carry everything its firing needs: the word of the op
+    // it releases and, beside the join index, the number of predecessors it
+    // waits for (when they fit 16 and 15 bits), so no per-join table is read.
+    bool jn = C.J <= 65536;
+    for (int32_t j = 0; j < C.J && jn; ++j) jn = C.jneed[j] < 32768;
+    C.pk_jn = jn;
+    auto entry = [&](int32_t &x, int32_t &y) {
+      if (y < 0) {
+        x = word(x);  // released directly (or a sibling)
+      } else if (jn) {
+        x = word(C.jtarget[y]);
+        y = (int32_t)((uint32_t)y | ((uint32_t)C.jneed[y] << 16));
+      }
+    };
+    C.ev_ops = C.ops;
+    for (OpRec &r : C.ev_ops) {
+      if (r.nsucc > 0) entry(r.w0, r.j0);
+      if (r.nsucc > 1) entry(r.w1, r.j1);
+    }
+    C.ev_succ = C.succ;
+    for (size_t k = 0; k + 1 < C.ev_succ.size(); k += 2) entry(C.ev_succ[k], C.ev_succ[k + 1]);
+    C.jinfo.resize(2 * (size_t)C.J);
+    for (int32_t j = 0; j < C.J; ++j) {
+      C.jinfo[2 * j] = C.jneed[j];
+      C.jinfo[2 * j + 1] = word(C.jtarget[j]);
+    }
+    C.ev_src.clear();
+    for (int32_t c : C.src) C.ev_src.push_back(word(c));
+  }
 
   C.heap_cap = n ? std::max(1, min_path_cover(n, cs)) : 0;
 
@@ -478,7 +537,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
          o_cp = take(bytes_of(C.cp)), o_cpp = take(bytes_of(C.cp_pred)),
          o_pp = take(bytes_of(C.pred_ptr)), o_pr = take(bytes_of(C.pred)),
          o_topo = take(bytes_of(C.topo)), o_wpp = take(bytes_of(C.wp_ptr)),
-         o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws));
+         o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws)),
+         o_evops = take(bytes_of(C.ev_ops)), o_evsucc = take(bytes_of(C.ev_succ)),
+         o_jinfo = take(bytes_of(C.jinfo)), o_evsrc = take(bytes_of(C.ev_src));
   // attribution: predecessors by caller id (ascending; implied ones removed:
   // they finish strictly before the op that implies them) and resources
   std::vector<int32_t> ap_ptr(n_ops + 1, 0), ap, row_res(op_res, op_res + n_ops);
@@ -509,7 +570,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
             put(o_wpp, C.wp_ptr.data(), bytes_of(C.wp_ptr)) && put(o_wp, C.wp.data(), bytes_of(C.wp)) &&
             put(o_wsp, C.ws_ptr.data(), bytes_of(C.ws_ptr)) && put(o_ws, C.ws.data(), bytes_of(C.ws)) &&
             put(o_app, ap_ptr.data(), bytes_of(ap_ptr)) && put(o_ap, ap.data(), bytes_of(ap)) &&
-            put(o_rres, row_res.data(), bytes_of(row_res));
+            put(o_rres, row_res.data(), bytes_of(row_res)) &&
+            put(o_evops, C.ev_ops.data(), bytes_of(C.ev_ops)) && put(o_evsucc, C.ev_succ.data(), bytes_of(C.ev_succ)) &&
+            put(o_jinfo, C.jinfo.data(), bytes_of(C.jinfo)) && put(o_evsrc, C.ev_src.data(), bytes_of(C.ev_src));
   if (!ok) {
     (void)hipFree(g->dev_mem);
     delete g;
@@ -540,6 +603,13 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.ap_ptr = (const int32_t *)(base + o_app);
   d.ap = (const int32_t *)(base + o_ap);
   d.row_res = (const int32_t *)(base + o_rres);
+  d.ev_ops = (const OpRec *)(base + o_evops);
+  d.ev_succ = (const int32_t *)(base + o_evsucc);
+  d.jinfo = (const int2 *)(base + o_jinfo);
+  d.ev_src = (const int32_t *)(base + o_evsrc);
+  d.pk_sh = C.pk_sh;
+  d.pk_join = C.pk_join;
+  d.pk_jn = C.pk_jn;
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;

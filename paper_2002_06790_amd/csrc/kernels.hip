@@ -354,11 +354,12 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
                                            int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
                                            LastXchg last_xchg, Flush flush) {
-  const int n = G.n, R = G.R;
-  const int2 *succ = (const int2 *)G.succ;
-  const int4 *rec4 = (const int4 *)G.ops;
+  const int R = G.R;
+  const int2 *succ = (const int2 *)G.ev_succ;
+  const int4 *rec4 = (const int4 *)G.ev_ops;
   const uint64_t key = heap.root;
-  const int c = (int)(uint32_t)key;
+  const uint32_t low = (uint32_t)key;  // key word: compact id, and maybe the first join
+  const int c = (int)(low >> G.pk_sh);
   const uint32_t ready = (uint32_t)(key >> 32);
   // every global load of the step is issued before the first is used
   const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
@@ -368,6 +369,15 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   if (ROW_ID) {
     d = GEN ? brow[c] : a.dur[(int64_t)c * a.ld_dur + sc];
     if (PLACE) rp = a.place[(int64_t)c * a.ld_place + sc];
+  }
+  // the first successor's join state, when the key word names the join:
+  // read together with the record instead of after it
+  const uint32_t jmask = (1u << G.pk_sh) - 1u;
+  const int jf = (int)(low & jmask);
+  int2 js0 = make_int2(0, 0), ji0 = make_int2(0, 0);
+  if (G.pk_join && (uint32_t)jf != jmask) {
+    js0 = jst.get(jf);
+    if (!G.pk_jn) ji0 = G.jinfo[jf];
   }
   HeapAhead A;
   heap_look_ahead<DEEP>(heap, end, A);
@@ -410,6 +420,8 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   // unused, and a load still in flight at the end of a step makes the next
   // step wait for every store of this one before it can issue its loads
   const int4 r0s = settle(r0), r1s = settle(r1);
+  js0 = settle(js0);
+  ji0 = settle(ji0);
   const int qs = it & (kFinQ - 1);  // wave-uniform
 #pragma unroll
   for (int k = 0; k < kFinQ; ++k)
@@ -436,19 +448,27 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
       release(sw.y == kJoinSibling ? ready : fin, sw.x);
       continue;
     }
-    const int2 js = settle(jst.get(sw.y));
-    const int need = settle(G.jneed[sw.y]);
+    // the join's state {predecessors finished, max finish} (already read for
+    // the first entry when the key named it) and {predecessors needed, word
+    // of the op released} (in the entry itself, or in the join table)
+    const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
+    int2 js, ji;
+    if (e == 0 && G.pk_join) {
+      js = js0;
+      ji = ji0;
+    } else {
+      js = settle(jst.get(j));
+      if (!G.pk_jn) ji = settle(G.jinfo[j]);
+    }
+    if (G.pk_jn) ji = make_int2((int)((uint32_t)sw.y >> 16), sw.x);
     const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
-    if (js.x + 1 < need) {
-      jst.set(sw.y, make_int2(js.x + 1, (int)rdy));
+    if (js.x + 1 < ji.x) {
+      jst.set(j, make_int2(js.x + 1, (int)rdy));
       continue;
     }
-    jst.set(sw.y, make_int2(0, 0));  // leave the join state clean
-    if (sw.x < n) {
-      release(rdy, sw.x);
-    } else {  // a barrier: its first member is ready now (the others follow it)
-      release(rdy, settle(rec4[2 * sw.x + 1]).x);
-    }
+    jst.set(j, make_int2(0, 0));  // leave the join state clean
+    // the join's op, or for a barrier its first member (the others follow it)
+    release(rdy, ji.y);
   }
   if (hole) heap_pop_root(heap, end, A);
 }
@@ -547,7 +567,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
 #pragma unroll
       for (int k = 0; k < kD; ++k) heap.ch[k] = kEmpty;
     int end = kRoot;  // one past the last heap position
-    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.src[k]));
+    for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.ev_src[k]));
     uint32_t st = 0, span = 0;
     int32_t fq[kFinQ], rq[kFinQ], pq[kFinQ];  // buffered finish times, their rows, previous ops
     auto flush = [&](int cnt) {

@@ -90,6 +90,18 @@ struct DevGraph {
   const int32_t *ap_ptr;
   const int32_t *ap;
   const int32_t *row_res;
+  // event kernel: ready-list key words (low 32 bits of a key) are
+  // (compact id << pk_sh) | join index of the op's first successor entry
+  // (pk_sh bits, all ones: not a join) when pk_join, else the compact id;
+  // records, successor entries and sources hold such words for the ops they
+  // release directly, and jinfo[j] = {predecessors needed, word released}
+  // per join.  With pk_jn a join entry {x, y} itself holds x = the word
+  // released and y = join index | predecessors needed << 16.
+  const OpRec *ev_ops;     // [n + barriers + 1]
+  const int32_t *ev_succ;  // pairs {word or barrier id, join index / kJoinNone / kJoinSibling}
+  const int2 *jinfo;       // [J]
+  const int32_t *ev_src;   // [nsrc]
+  int32_t pk_sh, pk_join, pk_jn;
 };
 
 // Lockstep walk (walk.hip).  Per group of tiles, k_pilot writes a header of
