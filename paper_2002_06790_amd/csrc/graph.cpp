@@ -30,7 +30,8 @@ struct Compiled {
   // {predecessors needed, word released} per join, source words
   std::vector<OpRec> ev_ops;
   std::vector<int32_t> ev_succ, jinfo, ev_src;
-  int32_t pk_sh = 0, pk_join = 0, pk_jn = 0;
+  int32_t pk_sh = 0, pk_join = 0, pk_jn = 0, pk_jb = 0, pk_rb = 0, ev_compact = 0;
+  std::vector<int32_t> ev_rec16;  // [n][4] compact event records (ev_compact)
   std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
   int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0, barriers = 0;
@@ -365,31 +366,44 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     if (cp[c].empty()) C.src.push_back(c);
 
   // Heap-key words of the event kernel.  The low 32 bits of a ready-list key
-  // hold the compact id; when the bits allow, they also hold the join index
-  // of the op's first successor entry (all ones: not a join) below it, so a
-  // popped op's first join state can be read together with its record
-  // instead of after it.  The id in the top bits keeps the key order (ids
-  // are distinct).  (A second field for the second entry measured slower on
-  // the BERT workload: 39.5 vs 37.1 ms.)
+  // hold the compact id; when the bits allow, they also hold (below it) the
+  // op's resource and the join index of its first successor entry (all
+  // ones: not a join), so a popped op's first join state can be read
+  // together with its record instead of after it, and its resource without
+  // its record.  The id in the top bits keeps the key order (ids are
+  // distinct).  (A second join field for the second entry measured slower
+  // on the BERT workload: 39.5 vs 37.1 ms.)
   {
-    int32_t jb = 0;
-    while ((1ll << jb) < (int64_t)C.J + 1) ++jb;
-    const bool pack = jb > 0 && jb < 32 && (int64_t)n <= (1ll << (32 - jb));
-    C.pk_sh = pack ? jb : 0;
-    C.pk_join = pack;
-    const uint32_t jnone = pack ? (1u << jb) - 1u : 0u;
-    auto word = [&](int32_t c) -> int32_t {  // c: a compact op id (never a barrier)
-      if (!pack || c < 0 || c >= n) return c;
-      const OpRec &r = C.ops[c];
-      const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)r.j0 : jnone;
-      return (int32_t)(((uint32_t)c << jb) | jf);
-    };
     // A join entry can carry everything its firing needs: the word of the op
     // it releases and, beside the join index, the number of predecessors it
     // waits for (when they fit 16 and 15 bits), so no per-join table is read.
     bool jn = C.J <= 65536;
     for (int32_t j = 0; j < C.J && jn; ++j) jn = C.jneed[j] < 32768;
     C.pk_jn = jn;
+    int32_t jb = 0, rb = 0;
+    while ((1ll << jb) < (int64_t)C.J + 1) ++jb;
+    while ((1ll << rb) < (int64_t)R) ++rb;
+    bool ident = true;  // caller ids equal compact ids: the duration row is the id
+    for (int32_t c = 0; c < n && ident; ++c) ident = orig_of[c] == c;
+    // compact records: identity rows, self-contained join entries, and id,
+    // resource and join field in one word
+    const bool compact = ident && jn && rb + jb < 32 && (int64_t)n <= (1ll << (32 - rb - jb));
+    const bool pack = compact || (jb > 0 && jb < 32 && (int64_t)n <= (1ll << (32 - jb)));
+    if (!compact) rb = 0;
+    if (!pack) jb = 0;
+    C.ev_compact = compact;
+    C.pk_jb = jb;
+    C.pk_rb = rb;
+    C.pk_sh = rb + jb;
+    C.pk_join = jb > 0;
+    const uint32_t jnone = (1u << jb) - 1u;
+    auto word = [&](int32_t c) -> int32_t {  // c: a compact op id (never a barrier)
+      if (!pack || c < 0 || c >= n) return c;
+      const OpRec &r = C.ops[c];
+      const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)r.j0 : jnone;
+      const uint32_t res = compact ? (uint32_t)r.res << jb : 0u;
+      return (int32_t)(((uint32_t)c << (rb + jb)) | res | jf);
+    };
     auto entry = [&](int32_t &x, int32_t &y) {
       if (y < 0) {
         x = word(x);  // released directly (or a sibling)
@@ -412,6 +426,19 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     }
     C.ev_src.clear();
     for (int32_t c : C.src) C.ev_src.push_back(word(c));
+    // compact records {entry 0, entry 1} per op: an entry {x, y} as in the
+    // successor list, {0, kRecNoSucc} when absent; an op with three or more
+    // successors keeps entry 0 and {index of its entry 1 in the successor
+    // list, kRecMore - (successors - 1)}
+    C.ev_rec16.assign(compact ? 4 * (size_t)n : 0, 0);
+    for (int32_t c = 0; compact && c < n; ++c) {
+      const OpRec &r = C.ev_ops[c];
+      int32_t *q = &C.ev_rec16[4 * (size_t)c];
+      q[1] = q[3] = kRecNoSucc;
+      if (r.nsucc > 0) q[0] = r.w0, q[1] = r.j0;
+      if (r.nsucc == 2) q[2] = r.w1, q[3] = r.j1;
+      if (r.nsucc > 2) q[2] = r.sbeg + 1, q[3] = kRecMore - (r.nsucc - 1);
+    }
   }
 
   C.heap_cap = n ? std::max(1, min_path_cover(n, cs)) : 0;
@@ -539,7 +566,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
          o_topo = take(bytes_of(C.topo)), o_wpp = take(bytes_of(C.wp_ptr)),
          o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws)),
          o_evops = take(bytes_of(C.ev_ops)), o_evsucc = take(bytes_of(C.ev_succ)),
-         o_jinfo = take(bytes_of(C.jinfo)), o_evsrc = take(bytes_of(C.ev_src));
+         o_jinfo = take(bytes_of(C.jinfo)), o_evsrc = take(bytes_of(C.ev_src)),
+         o_rec16 = take(bytes_of(C.ev_rec16));
   // attribution: predecessors by caller id (ascending; implied ones removed:
   // they finish strictly before the op that implies them) and resources
   std::vector<int32_t> ap_ptr(n_ops + 1, 0), ap, row_res(op_res, op_res + n_ops);
@@ -572,7 +600,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
             put(o_app, ap_ptr.data(), bytes_of(ap_ptr)) && put(o_ap, ap.data(), bytes_of(ap)) &&
             put(o_rres, row_res.data(), bytes_of(row_res)) &&
             put(o_evops, C.ev_ops.data(), bytes_of(C.ev_ops)) && put(o_evsucc, C.ev_succ.data(), bytes_of(C.ev_succ)) &&
-            put(o_jinfo, C.jinfo.data(), bytes_of(C.jinfo)) && put(o_evsrc, C.ev_src.data(), bytes_of(C.ev_src));
+            put(o_jinfo, C.jinfo.data(), bytes_of(C.jinfo)) && put(o_evsrc, C.ev_src.data(), bytes_of(C.ev_src)) &&
+            put(o_rec16, C.ev_rec16.data(), bytes_of(C.ev_rec16));
   if (!ok) {
     (void)hipFree(g->dev_mem);
     delete g;
@@ -610,6 +639,10 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.pk_sh = C.pk_sh;
   d.pk_join = C.pk_join;
   d.pk_jn = C.pk_jn;
+  d.pk_jb = C.pk_jb;
+  d.pk_rmask = (int32_t)((1u << C.pk_rb) - 1u);
+  d.ev_compact = C.ev_compact;
+  d.ev_rec16 = (const int4 *)(base + o_rec16);
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;

@@ -358,12 +358,19 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   const int2 *succ = (const int2 *)G.ev_succ;
   const int4 *rec4 = (const int4 *)G.ev_ops;
   const uint64_t key = heap.root;
-  const uint32_t low = (uint32_t)key;  // key word: compact id, and maybe the first join
+  const uint32_t low = (uint32_t)key;  // key word: compact id, maybe resource and first join
   const int c = (int)(low >> G.pk_sh);
   const uint32_t ready = (uint32_t)(key >> 32);
-  // every global load of the step is issued before the first is used
-  const int4 r0 = rec4[2 * c];      // {orig, res, sbeg, nsucc}
-  const int4 r1 = rec4[2 * c + 1];  // {first successor, its join, second, its join}
+  // every global load of the step is issued before the first is used.
+  // ROW_ID: the compact record {entry 0, entry 1}; otherwise the record
+  // {orig, res, sbeg, nsucc} and {entry 0, entry 1}
+  int4 r0, r1 = make_int4(0, 0, 0, 0);
+  if (ROW_ID) {
+    r0 = G.ev_rec16[c];
+  } else {
+    r0 = rec4[2 * c];
+    r1 = rec4[2 * c + 1];
+  }
   int32_t d = 0;
   int rp = 0;
   if (ROW_ID) {
@@ -372,7 +379,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   }
   // the first successor's join state, when the key word names the join:
   // read together with the record instead of after it
-  const uint32_t jmask = (1u << G.pk_sh) - 1u;
+  const uint32_t jmask = (1u << G.pk_jb) - 1u;
   const int jf = (int)(low & jmask);
   int2 js0 = make_int2(0, 0), ji0 = make_int2(0, 0);
   if (G.pk_join && (uint32_t)jf != jmask) {
@@ -389,7 +396,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     if (PLACE) rp = a.place[(int64_t)row * a.ld_place + sc];
   }
   if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)row, a.gen.key0, a.gen.key1, a.gen.noise);
-  int r = PLACE ? rp : r0.y;
+  int r = PLACE ? rp : ROW_ID ? (int)((low >> G.pk_jb) & (uint32_t)G.pk_rmask) : r0.y;
   if (PLACE && r >= R) {
     st |= SIM_ST_BAD_RES;
     r = 0;
@@ -419,7 +426,24 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   // the record too: a step that releases nothing leaves its second half
   // unused, and a load still in flight at the end of a step makes the next
   // step wait for every store of this one before it can issue its loads
-  const int4 r0s = settle(r0), r1s = settle(r1);
+  const int4 r0s = settle(r0), r1s = ROW_ID ? r1 : settle(r1);
+  // successor entries: the first two inline, the others (from index sbeg +
+  // 2, or with ROW_ID from sbeg + 1) in the successor list
+  int nsucc, sbeg;
+  int2 e0, e1;
+  bool more = false;
+  if (ROW_ID) {
+    e0 = make_int2(r0s.x, r0s.y);
+    e1 = make_int2(r0s.z, r0s.w);
+    more = e1.y < kRecNoSucc;
+    nsucc = e0.y == kRecNoSucc ? 0 : e1.y == kRecNoSucc ? 1 : more ? 1 + (kRecMore - e1.y) : 2;
+    sbeg = e1.x - 1;
+  } else {
+    e0 = make_int2(r1s.x, r1s.y);
+    e1 = make_int2(r1s.z, r1s.w);
+    nsucc = r0s.w;
+    sbeg = r0s.z;
+  }
   js0 = settle(js0);
   ji0 = settle(ji0);
   const int qs = it & (kFinQ - 1);  // wave-uniform
@@ -441,9 +465,8 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
       heap_push(heap, end, nk);
     }
   };
-  for (int e = 0; e < r0s.w; ++e) {
-    const int2 sw = e == 0 ? make_int2(r1s.x, r1s.y)
-                           : e == 1 ? make_int2(r1s.z, r1s.w) : settle(succ[r0s.z + e]);  // {successor, join}
+  for (int e = 0; e < nsucc; ++e) {
+    const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);  // {successor, join}
     if (sw.y < 0) {  // a plain successor, or the next member of a barrier
       release(sw.y == kJoinSibling ? ready : fin, sw.x);
       continue;
@@ -479,7 +502,9 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
 // and its resource has finished its previous op, and releases successors
 // whose last predecessor this was.  Every lane pops exactly n ops per tile, so
 // the outer loop is wave-uniform.  ROW_ID: the caller's op ids equal the
-// compact ids, so the duration row is known as soon as the op is popped.
+// compact ids, so the duration row is known as soon as the op is popped, and
+// the graph has compact records (one 16-byte load per step; the resource
+// comes from the key word).
 // PLACE: resources come from the per-scenario placement matrix.  Finish times
 // are written in bursts of kFinQ stores per lane, so their completion is
 // waited for once per burst instead of once per step.  GEN: durations are
@@ -1259,7 +1284,7 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
     lds += ((size_t)g->dg.R * 4 + 15) & ~size_t(15);
   }
   const int variant = (reg ? 64 : 0) | (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
-                      (rf_lds ? 4 : 0) | (g->row_identity ? 2 : 0) | (place ? 1 : 0);
+                      (rf_lds ? 4 : 0) | (g->dg.ev_compact ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_GEN_CASE(V, A, B) \

@@ -24,6 +24,10 @@ constexpr int kWave = 64;  // CDNA wavefront width: one scenario per lane
 // join index of a successor entry: a join counter, or one of these
 constexpr int32_t kJoinNone = -1;     // released at the op's finish time
 constexpr int32_t kJoinSibling = -2;  // next barrier member, released at the op's ready time
+// compact event records only: no entry, and (minus the count of further
+// entries) "entries 1.. are in the successor list"
+constexpr int32_t kRecNoSucc = -3;
+constexpr int32_t kRecMore = -4;
 struct OpRec {
   int32_t orig;   // caller's op id: row of dur / place / finish (-1: barrier)
   int32_t res;    // resource (op_res), -1 for a barrier
@@ -91,8 +95,9 @@ struct DevGraph {
   const int32_t *ap;
   const int32_t *row_res;
   // event kernel: ready-list key words (low 32 bits of a key) are
-  // (compact id << pk_sh) | join index of the op's first successor entry
-  // (pk_sh bits, all ones: not a join) when pk_join, else the compact id;
+  // (compact id << pk_sh) | (resource << pk_jb) | join index of the op's
+  // first successor entry (pk_jb bits, all ones: not a join), with
+  // pk_sh = resource bits + pk_jb (resource bits only with ev_compact);
   // records, successor entries and sources hold such words for the ops they
   // release directly, and jinfo[j] = {predecessors needed, word released}
   // per join.  With pk_jn a join entry {x, y} itself holds x = the word
@@ -101,7 +106,11 @@ struct DevGraph {
   const int32_t *ev_succ;  // pairs {word or barrier id, join index / kJoinNone / kJoinSibling}
   const int2 *jinfo;       // [J]
   const int32_t *ev_src;   // [nsrc]
-  int32_t pk_sh, pk_join, pk_jn;
+  int32_t pk_sh, pk_join, pk_jn, pk_jb, pk_rmask;
+  // compact event records (identity rows): 16 bytes per op, entries 0 and 1
+  // (see kRecNoSucc, kRecMore); the op's resource comes from its key word
+  int32_t ev_compact, pad2;
+  const int4 *ev_rec16;
 };
 
 // Lockstep walk (walk.hip).  Per group of tiles, k_pilot writes a header of
