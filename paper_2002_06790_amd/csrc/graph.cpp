@@ -371,8 +371,8 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   // ones: not a join), so a popped op's first join state can be read
   // together with its record instead of after it, and its resource without
   // its record.  The id in the top bits keeps the key order (ids are
-  // distinct).  (A second join field for the second entry measured slower
-  // on the BERT workload: 39.5 vs 37.1 ms.)
+  // distinct).  (A second join field for the second entry did not measure
+  // faster on the BERT workload.)
   {
     // A join entry can carry everything its firing needs: the word of the op
     // it releases and, beside the join index, the number of predecessors it
