@@ -9,7 +9,8 @@ step it also times the static-order replay (every resource running its ops
 in the order the event replay ran them in scenario 0), the bottleneck
 attribution, the replay and critical path on durations generated inside the
 kernels (knob table x counter-based noise), the replay with a gap per
-resource and, on a bounded sample, the CPU
+resource, the sweep variant on a slice of the scenarios and, on a bounded
+sample, the CPU
 oracle, whose outputs check sampled GPU results.
 
 Default workload: the BERT-large data-parallel graph (16 workers, per-worker
@@ -194,6 +195,21 @@ def main():
         e1.synchronize()
         gap_ms.append(e0.elapsed_time(e1))
     log(f"replay with resource gaps {np.mean(gap_ms):.3f} ms")
+    # the level-synchronous sweep variant (outside the step) on a bounded
+    # slice of the scenarios: it re-sweeps the graph every round, so it is
+    # the slow exact variant; its makespans must equal the event replay's
+    sw_n = min(S, 16384)
+    sw_dur = dur[:, :sw_n]
+    sw_place = None if place is None else place[:, :sw_n]
+    e0.record()
+    swmk, _, swst = g.run(sw_dur, place=sw_place, algo="sweep")
+    e1.record()
+    e1.synchronize()
+    sweep_ms = e0.elapsed_time(e1)
+    evmk, _, _ = g.run(sw_dur, place=sw_place, algo="event")
+    torch.cuda.synchronize()
+    sweep_equal = bool(torch.equal(swmk, evmk))
+    log(f"sweep variant {sweep_ms:.1f} ms on {sw_n} scenarios, equal to the event replay: {sweep_equal}")
     # the step's outputs again (the static replay reused the buffers)
     step()
     torch.cuda.synchronize()
@@ -289,7 +305,10 @@ def main():
                     "generated_run_op_events_per_s": op_events / (float(np.mean(gev_ms)) / 1e3),
                     "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3),
                     "gap_run_ms": float(np.mean(gap_ms)),
-                    "gap_run_op_events_per_s": op_events / (float(np.mean(gap_ms)) / 1e3)},
+                    "gap_run_op_events_per_s": op_events / (float(np.mean(gap_ms)) / 1e3),
+                    "sweep_ms": sweep_ms, "sweep_scenarios": sw_n,
+                    "sweep_op_events_per_s": n * sw_n / (sweep_ms / 1e3),
+                    "sweep_equals_event": sweep_equal},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
