@@ -398,3 +398,21 @@ def test_sweep_equals_event_full_bert_slice(mlsim):
     b = g.run(dur, want_finish=True, algo="sweep")
     torch.cuda.synchronize()
     assert all(torch.equal(x, y) for x, y in zip(a, b))
+
+
+def test_join_beyond_entry_limits(mlsim):
+    """A join waiting for more predecessors than a successor entry can
+    count (32768) uses the per-join table; results equal the oracle's."""
+    n_src = 33000
+    n = n_src + 2
+    sink, tail = n_src, n_src + 1
+    ptr = np.zeros(n + 1, np.int64)
+    ptr[1:n_src + 1] = np.arange(1, n_src + 1)
+    ptr[n_src + 1] = n_src + 1  # sink -> tail
+    ptr[n_src + 2] = n_src + 1
+    idx = np.r_[np.full(n_src, sink, np.int32), np.int32(tail)].astype(np.int32)
+    res = (np.arange(n) % 4).astype(np.int32)
+    rng = np.random.default_rng(12)
+    dur = W.random_durations(n, 65, 1, 50, rng)
+    print(f"join with {n_src} predecessors", flush=True)
+    check_run(mlsim, ptr, idx, res, 4, dur)
