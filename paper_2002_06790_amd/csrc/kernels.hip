@@ -925,7 +925,8 @@ constexpr uint32_t kDone = 0x80000000u;  // val bit: op committed (low bits: fin
 // (est, compact id) if that key is below the bound of every op on the
 // resource that is not ready yet.  Each resource therefore runs its ops in
 // key order, which is the first-in-first-out replay's unique schedule; every
-// round commits at least the globally smallest ready op.
+// round commits at least the globally smallest ready op.  A round starts at
+// the first position of the order that some lane has not committed.
 template <bool VAL_LDS, bool RES_LDS>
 __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
   extern __shared__ uint32_t sw_lds[];
@@ -946,13 +947,15 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
     for (int r = 0; r < R; ++r) rfree[r * kWave] = 0;
     int done = 0;
     uint32_t st = 0, span = 0;
+    int lo = 0;  // topological positions before lo are committed in every lane
     for (int round = 0; round < n; ++round) {
       if (__ballot(done < n) == 0) break;
       for (int r = 0; r < R; ++r) {
         minf[r * kWave] = ~0ull;
         lbnd[r * kWave] = ~0ull;
       }
-      for (int k = 0; k < n; ++k) {
+      while (lo < n && __ballot(!(val[(size_t)G.topo[lo] * kWave] & kDone)) == 0) ++lo;
+      for (int k = lo; k < n; ++k) {
         const int v = G.topo[k];
         if (val[(size_t)v * kWave] & kDone) continue;
         uint32_t est = 0;
