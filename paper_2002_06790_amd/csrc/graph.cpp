@@ -25,6 +25,7 @@ constexpr int32_t kReduceMaxOps = 32768;  // transitive reduction bitsets: n^2/8
 struct Compiled {
   std::vector<OpRec> ops;
   std::vector<int32_t> succ, jneed, src, cp_pred, pred_ptr, pred, topo;
+  std::vector<int32_t> lvl_of, levend;  // sweep variant: level of each op, last position of each level
   std::vector<int32_t> jtarget;  // [J] the op a join releases: its own op, or a barrier's first member
   // event kernel: records and successor entries holding heap-key words,
   // {predecessors needed, word released} per join, source words
@@ -446,7 +447,6 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   // critical-path sweep
   std::vector<int32_t> order;
   build_maxplus(n, cs, cp, orig_of, C.cp, C.cp_pred, C.cp_slots, order);
-  C.topo = order;
 
   // compact predecessor CSR (for the sweep variant) and level count
   C.pred_ptr.assign(n + 1, 0);
@@ -463,6 +463,14 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     for (int32_t p : cp[v]) lvl[v] = std::max(lvl[v], lvl[p] + 1);
     C.levels = std::max(C.levels, lvl[v] + 1);
   }
+  // sweep-variant order: by level (longest path from a source), then id, so
+  // every level is a contiguous range of positions
+  C.topo.resize(n);
+  for (int32_t c = 0; c < n; ++c) C.topo[c] = c;
+  std::stable_sort(C.topo.begin(), C.topo.end(), [&](int32_t a, int32_t b) { return lvl[a] < lvl[b]; });
+  C.lvl_of = lvl;
+  C.levend.assign(std::max(C.levels, 1), -1);
+  for (int32_t k = 0; k < n; ++k) C.levend[lvl[C.topo[k]]] = k;
   return SIM_OK;
 }
 
@@ -567,7 +575,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
          o_wp = take(bytes_of(C.wp)), o_wsp = take(bytes_of(C.ws_ptr)), o_ws = take(bytes_of(C.ws)),
          o_evops = take(bytes_of(C.ev_ops)), o_evsucc = take(bytes_of(C.ev_succ)),
          o_jinfo = take(bytes_of(C.jinfo)), o_evsrc = take(bytes_of(C.ev_src)),
-         o_rec16 = take(bytes_of(C.ev_rec16));
+         o_rec16 = take(bytes_of(C.ev_rec16)), o_lvl = take(bytes_of(C.lvl_of)),
+         o_levend = take(bytes_of(C.levend));
   // attribution: predecessors by caller id (ascending; implied ones removed:
   // they finish strictly before the op that implies them) and resources
   std::vector<int32_t> ap_ptr(n_ops + 1, 0), ap, row_res(op_res, op_res + n_ops);
@@ -601,7 +610,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
             put(o_rres, row_res.data(), bytes_of(row_res)) &&
             put(o_evops, C.ev_ops.data(), bytes_of(C.ev_ops)) && put(o_evsucc, C.ev_succ.data(), bytes_of(C.ev_succ)) &&
             put(o_jinfo, C.jinfo.data(), bytes_of(C.jinfo)) && put(o_evsrc, C.ev_src.data(), bytes_of(C.ev_src)) &&
-            put(o_rec16, C.ev_rec16.data(), bytes_of(C.ev_rec16));
+            put(o_rec16, C.ev_rec16.data(), bytes_of(C.ev_rec16)) &&
+            put(o_lvl, C.lvl_of.data(), bytes_of(C.lvl_of)) && put(o_levend, C.levend.data(), bytes_of(C.levend));
   if (!ok) {
     (void)hipFree(g->dev_mem);
     delete g;
@@ -643,6 +653,9 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.pk_rmask = (int32_t)((1u << C.pk_rb) - 1u);
   d.ev_compact = C.ev_compact;
   d.ev_rec16 = (const int4 *)(base + o_rec16);
+  d.lvl_of = (const int32_t *)(base + o_lvl);
+  d.levend = (const int32_t *)(base + o_levend);
+  d.n_levels = C.levels;
 
   g->h_orig_of.resize(n_ops);
   for (int32_t c = 0; c < n_ops; ++c) g->h_orig_of[c] = C.ops[c].orig;

@@ -925,8 +925,10 @@ constexpr uint32_t kDone = 0x80000000u;  // val bit: op committed (low bits: fin
 // (est, compact id) if that key is below the bound of every op on the
 // resource that is not ready yet.  Each resource therefore runs its ops in
 // key order, which is the first-in-first-out replay's unique schedule; every
-// round commits at least the globally smallest ready op.  A round starts at
-// the first position of the order that some lane has not committed.
+// round commits at least the globally smallest ready op.  The order is by
+// level; a round sweeps from the first position some lane has not committed
+// to the end of the level after the highest one committed, and bounds every
+// op beyond it by one value (see below).
 template <bool VAL_LDS, bool RES_LDS>
 __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
   extern __shared__ uint32_t sw_lds[];
@@ -947,7 +949,8 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
     for (int r = 0; r < R; ++r) rfree[r * kWave] = 0;
     int done = 0;
     uint32_t st = 0, span = 0;
-    int lo = 0;  // topological positions before lo are committed in every lane
+    int lo = 0;       // positions before lo are committed in every lane
+    int maxlc = -1;   // highest level this lane has committed
     for (int round = 0; round < n; ++round) {
       if (__ballot(done < n) == 0) break;
       for (int r = 0; r < R; ++r) {
@@ -955,7 +958,21 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
         lbnd[r * kWave] = ~0ull;
       }
       while (lo < n && __ballot(!(val[(size_t)G.topo[lo] * kWave] & kDone)) == 0) ++lo;
-      for (int k = lo; k < n; ++k) {
+      // An op can be ready only if its level is at most one above the
+      // highest level committed, so positions past the end of that level
+      // (highest over the wave) hold no ready op.  Every op there waits on a
+      // chain of uncommitted ops that reaches the window, so its ready time
+      // is at least bfar, the smallest earliest finish of an uncommitted op
+      // in the window: one bound stands for all of them.
+      int wl = maxlc;
+#pragma unroll
+      for (int off = kWave / 2; off > 0; off >>= 1) {
+        const int o = __shfl_xor(wl, off);
+        wl = o > wl ? o : wl;
+      }
+      const int hi = G.levend[wl + 1 < G.n_levels ? wl + 1 : G.n_levels - 1] + 1;
+      uint32_t bfar = ~0u;
+      for (int k = lo; k < hi; ++k) {
         const int v = G.topo[k];
         if (val[(size_t)v * kWave] & kDone) continue;
         uint32_t est = 0;
@@ -984,6 +1001,7 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
         uint32_t eft = (est > rf ? est : rf) + (uint32_t)d;
         if (eft > kI32Max) eft = kI32Max;
         val[(size_t)v * kWave] = eft;
+        bfar = eft < bfar ? eft : bfar;
         const uint64_t key = make_key(est, v);
         uint64_t *slot = ready ? &minf[r * kWave] : &lbnd[r * kWave];
         if (key < *slot) *slot = key;
@@ -998,7 +1016,7 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
           gmin = mf;
           gres = r;
         }
-        if (mf < lbnd[r * kWave]) {
+        if (mf < lbnd[r * kWave] && (uint32_t)(mf >> 32) < bfar) {
           progress = true;
           const int c = (int)(uint32_t)mf;
           const uint32_t rdy = (uint32_t)(mf >> 32);
@@ -1015,6 +1033,7 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
           val[(size_t)c * kWave] = fin | kDone;
           span = fin > span ? fin : span;
           ++done;
+          maxlc = G.lvl_of[c] > maxlc ? G.lvl_of[c] : maxlc;
           if (a.finish && active) a.finish[(int64_t)op.orig * a.ld_fin + s] = (int32_t)fin;
         }
       }
@@ -1033,6 +1052,7 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
         rfree[gres * kWave] = fin;
         val[(size_t)c * kWave] = fin | kDone;
         ++done;
+        maxlc = G.lvl_of[c] > maxlc ? G.lvl_of[c] : maxlc;
       }
     }
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;

@@ -80,7 +80,10 @@ struct DevGraph {
   const int32_t *cp_pred; // predecessor slot lists of the critical-path sweep
   const int32_t *pred_ptr;// [n + 1] compact predecessor CSR (sweep variant)
   const int32_t *pred;    // compact predecessor ids
-  const int32_t *topo;    // [n] a topological order (compact ids)
+  const int32_t *topo;    // [n] compact ids by (level, id): each level a contiguous range
+  const int32_t *lvl_of;  // [n] level of each compact op (longest path from a source)
+  const int32_t *levend;  // [levels] last position of each level in topo
+  int32_t n_levels, pad3;
   // walk graph over nodes 0..n+nb-1 (ops, then barriers): a barrier's
   // predecessors are its shared set, a member's only predecessor is its
   // barrier; successor lists are the reverse
