@@ -133,8 +133,8 @@ int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_
  * queues stay first-in-first-out by ready time, with the same tie rules, and
  * the makespan is the largest finish time (a trailing gap does not count).
  *   gap  host int32 [n_res], every entry >= 0 (else SIM_E_INVAL); read
- *        before the call returns (copied into the graph's scratch memory in
- *        stream order).
+ *        before the call returns (its values travel to the graph's scratch
+ *        memory in stream order as kernel arguments).
  * Other arguments and outputs as sim_run_batch (placement allowed; a finish
  * time above INT32_MAX sets SIM_ST_OVERFLOW); flags: SIM_ALGO_AUTO or
  * SIM_ALGO_EVENT (others return SIM_E_INVAL).  With every gap 0 the result

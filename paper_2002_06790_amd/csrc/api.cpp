@@ -109,10 +109,10 @@ extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32
     if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
     return SIM_OK;
   }
-  // the gaps go to the graph's scratch, in stream order before the replay
+  // the gaps go to the graph's scratch in stream order before the replay,
+  // passed by value, so the caller's array is no longer read on return
   int32_t *gap_dev = (int32_t *)((char *)g->scratch + g->scratch_gap_off);
-  if (hipMemcpyAsync(gap_dev, gap, (size_t)g->n_res * 4, hipMemcpyHostToDevice, st) != hipSuccess)
-    return SIM_E_HIP;
+  if (int rc = launch_put_words(gap_dev, gap, g->n_res, st)) return rc;
   return launch_event_gap(g, n_scen, dur, ld_dur, place, ld_place, gap_dev, makespan, finish, ld_fin,
                           status, st);
 }

@@ -1377,6 +1377,29 @@ __global__ __launch_bounds__(256) void k_generate(DurGen gen, int64_t n_scen, in
 }
 }  // namespace
 
+// Up to kPutWords values passed by value (kernel arguments are captured at
+// launch, so the caller's host array may change as soon as the launch
+// returns) written to device memory in stream order.
+constexpr int kPutWords = 256;
+struct PutWords {
+  int32_t v[kPutWords];
+};
+__global__ __launch_bounds__(kPutWords) void k_put_words(int32_t *dst, PutWords w, int count) {
+  const int i = threadIdx.x;
+  if (i < count) dst[i] = w.v[i];
+}
+
+int launch_put_words(int32_t *dst, const int32_t *src, int32_t count, hipStream_t stream) {
+  for (int32_t k = 0; k < count; k += kPutWords) {
+    PutWords w;
+    const int32_t m = std::min(kPutWords, count - k);
+    memcpy(w.v, src + k, (size_t)m * 4);
+    k_put_words<<<1, kPutWords, 0, stream>>>(dst + k, w, m);
+    if (hipGetLastError() != hipSuccess) return SIM_E_HIP;
+  }
+  return SIM_OK;
+}
+
 int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream) {
   const int64_t xb = (n_scen + 255) / 256;
   // enough blocks to fill the chip several times over, each op row once

@@ -125,3 +125,21 @@ def test_bert_full_size_sampled(mlsim):
     assert np.array_equal(st[sel].cpu().numpy(), ost)
     assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
     g.close()
+
+
+def test_gap_array_read_before_return(mlsim):
+    """The call has read the host gap array when it returns: overwriting it
+    before the stream runs does not change the result."""
+    w = W.make_config(2, n_scen=128)
+    dur = w.durations()
+    gap = np.full(w.n_res, 3000, np.int32)
+    keep = gap.copy()
+    g = mlsim.Graph.from_workload(w)
+    d = dev(dur)
+    torch.cuda._sleep(50_000_000)  # keep the stream busy so the replay runs after the overwrite
+    mk, fin, st = g.run(d, want_finish=True, gap=gap)
+    gap[:] = 10**9
+    torch.cuda.synchronize()
+    omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, gap=keep)
+    assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(fin.cpu().numpy(), ofin)
+    g.close()
