@@ -76,8 +76,8 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
   hipStream_t st = (hipStream_t)stream;
   if (g->n_ops == 0) {
     // no ops: every iteration takes 0 ns
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
-    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
   const uint32_t algo = flags & 3u;
@@ -105,8 +105,8 @@ extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32
   if (finish && ld_fin < n_scen) return SIM_E_INVAL;
   hipStream_t st = (hipStream_t)stream;
   if (g->n_ops == 0) {
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
-    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
   // the gaps go to the graph's scratch in stream order before the replay,
@@ -129,7 +129,7 @@ extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32
   hipStream_t st = (hipStream_t)stream;
   const int32_t n = g->n_ops;
   if (n == 0) {
-    if (hipMemsetAsync(cp_len, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(cp_len, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;
   }
@@ -173,8 +173,8 @@ extern "C" int sim_run_generated(const sim_graph *g, int64_t n_scen, const int32
   if (finish && ld_fin < n_scen) return SIM_E_INVAL;
   hipStream_t st = (hipStream_t)stream;
   if (g->n_ops == 0) {
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
-    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
   return launch_event_gen(g, n_scen, gen, makespan, finish, ld_fin, status, st);
@@ -195,7 +195,7 @@ extern "C" int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, c
   hipStream_t st = (hipStream_t)stream;
   const int32_t n = g->n_ops;
   if (n == 0) {
-    if (hipMemsetAsync(cp_len, 0, (size_t)n_scen * 4, st) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(cp_len, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;
   }
@@ -236,11 +236,10 @@ extern "C" int sim_attribute(const sim_graph *g, int64_t n_scen, const int32_t *
   hipStream_t st = (hipStream_t)stream;
   if (n == 0) {
     // no ops: every iteration takes 0 ns on an empty chain
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, st) != hipSuccess ||
-        hipMemsetAsync(status, 0, (size_t)n_scen * 4, st) != hipSuccess ||
-        hipMemsetAsync(chain_ops, 0, (size_t)n_scen * 4, st) != hipSuccess ||
-        hipMemset2DAsync(busy, (size_t)ld_res * 4, 0, (size_t)n_scen * 4, R, st) != hipSuccess ||
-        hipMemset2DAsync(chain, (size_t)ld_res * 4, 0, (size_t)n_scen * 4, R, st) != hipSuccess)
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK ||
+        launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK ||
+        launch_zero(chain_ops, n_scen, n_scen, 1, st) != SIM_OK ||
+        launch_zero(busy, n_scen, ld_res, R, st) != SIM_OK || launch_zero(chain, n_scen, ld_res, R, st) != SIM_OK)
       return SIM_E_HIP;
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;

@@ -1389,6 +1389,24 @@ __global__ __launch_bounds__(kPutWords) void k_put_words(int32_t *dst, PutWords 
   if (i < count) dst[i] = w.v[i];
 }
 
+// dst[r * ld + i] = 0 for r < rows, i < count (a kernel rather than a memset,
+// so a caller may capture the call in a graph)
+__global__ __launch_bounds__(256) void k_zero2d(int32_t *dst, int64_t count, int64_t ld) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < count) dst[(int64_t)blockIdx.y * ld + i] = 0;
+}
+
+int launch_zero(int32_t *dst, int64_t count, int64_t ld, int32_t rows, hipStream_t stream) {
+  if (!dst || count <= 0 || rows <= 0) return SIM_OK;
+  const int64_t xb = (count + 255) / 256;
+  for (int32_t r0 = 0; r0 < rows; r0 += 65535) {  // grid y limit
+    const int32_t ry = std::min(65535, rows - r0);
+    k_zero2d<<<dim3((unsigned)xb, (unsigned)ry), dim3(256), 0, stream>>>(dst + (int64_t)r0 * ld, count, ld);
+    if (hipGetLastError() != hipSuccess) return SIM_E_HIP;
+  }
+  return SIM_OK;
+}
+
 int launch_put_words(int32_t *dst, const int32_t *src, int32_t count, hipStream_t stream) {
   for (int32_t k = 0; k < count; k += kPutWords) {
     PutWords w;

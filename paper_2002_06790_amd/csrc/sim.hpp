@@ -236,6 +236,8 @@ int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld
 // generation parameters of a call, checked (SIM_OK or SIM_E_INVAL)
 int make_gen(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_knobs, int64_t knob_block,
              uint32_t noise, uint64_t seed, int64_t scen0, DurGen &gen);
+// zero rows x count int32 entries (row stride ld) in stream order
+int launch_zero(int32_t *dst, int64_t count, int64_t ld, int32_t rows, hipStream_t stream);
 // host values copied to device memory in stream order through kernel arguments
 int launch_put_words(int32_t *dst, const int32_t *src, int32_t count, hipStream_t stream);
 // generated durations: written out, or consumed by the event replay

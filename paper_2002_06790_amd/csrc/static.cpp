@@ -143,8 +143,8 @@ extern "C" int sim_static_run(const sim_static *st, int64_t n_scen, const int32_
   hipStream_t s = (hipStream_t)stream;
   if (st->n_ops == 0) {
     // no ops: every iteration takes 0 ns
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
-    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(makespan, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
   return launch_maxplus(st->tab, st->mode, st->blocks, st->lds, n_scen, dur, ld_dur, makespan, status,
@@ -163,8 +163,8 @@ extern "C" int sim_static_run_generated(const sim_static *st, int64_t n_scen, co
   if (finish && ld_fin < n_scen) return SIM_E_INVAL;
   hipStream_t s = (hipStream_t)stream;
   if (st->n_ops == 0) {
-    if (hipMemsetAsync(makespan, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
-    if (status && hipMemsetAsync(status, 0, (size_t)n_scen * 4, s) != hipSuccess) return SIM_E_HIP;
+    if (launch_zero(makespan, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
   return launch_maxplus(st->tab, st->mode, st->gen_blocks, st->lds, n_scen, nullptr, 0, makespan, status,
