@@ -416,3 +416,43 @@ def test_join_beyond_entry_limits(mlsim):
     dur = W.random_durations(n, 65, 1, 50, rng)
     print(f"join with {n_src} predecessors", flush=True)
     check_run(mlsim, ptr, idx, res, 4, dur)
+
+
+def test_hip_graph_capture_replays(mlsim):
+    """sim_run_batch and sim_critical_path captured in a HIP graph (through
+    torch's graph capture on the current stream): each replay, with new
+    durations written between replays, equals the eager calls and the
+    oracle."""
+    w = W.make_config(4, n_scen=192)
+    G = mlsim.Graph.from_workload(w)
+    rng = np.random.default_rng(5)
+    durs = [w.durations()] + [np.maximum(1, w.durations() + rng.integers(-500, 500, size=(w.n_ops, 192)))
+                              .astype(np.int32) for _ in range(2)]
+    d = dev(durs[0])
+    mk = torch.empty(192, dtype=torch.int32, device="cuda")
+    st = torch.empty(192, dtype=torch.int32, device="cuda")
+    fin = torch.empty((w.n_ops, 192), dtype=torch.int32, device="cuda")
+    cp = torch.empty(192, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):  # warm up outside the capture
+        G.run(d, want_finish=True, algo="event", makespan=mk, finish=fin, status=st)
+        G.critical_path(d, cp_len=cp)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        G.run(d, want_finish=True, algo="event", makespan=mk, finish=fin, status=st)
+        G.critical_path(d, cp_len=cp)
+    for rep in range(3):
+        dh = durs[rep % len(durs)]
+        d.copy_(torch.from_numpy(dh))  # eager work between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        emk, efin, est = G.run(d, want_finish=True, algo="event")
+        ecp, _ = G.critical_path(d)
+        torch.cuda.synchronize()
+        assert torch.equal(mk, emk) and torch.equal(fin, efin) and torch.equal(st, est) and torch.equal(cp, ecp)
+        omk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh, want_finish=False)
+        assert np.array_equal(mk.cpu().numpy(), omk), f"replay {rep}"
+    G.close()
