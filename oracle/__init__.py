@@ -48,6 +48,10 @@ def lib(path: Optional[str] = None):
                                            P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
                                            P, ctypes.c_int32]
         L.oracle_run_batch_gap.restype = ctypes.c_int
+        L.oracle_run_batch_dev.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int64,
+                                           P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
+                                           P, ctypes.c_int32]
+        L.oracle_run_batch_dev.restype = ctypes.c_int
         L.oracle_critical_path.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, P, ctypes.c_int64,
                                            P, ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
         L.oracle_critical_path.restype = ctypes.c_int
@@ -91,15 +95,18 @@ def _threads(n_threads: Optional[int]) -> int:
 
 
 def run_batch(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None,
-              want_finish: bool = True, n_threads: Optional[int] = None, library=None, gap=None):
+              want_finish: bool = True, n_threads: Optional[int] = None, library=None, gap=None,
+              delay=None):
     """Replay every scenario column of ``dur`` ([n_ops, n_scen] int32);
     ``gap`` ([n_res] int32 or None) is each device's idle time between
-    consecutive ops.
+    consecutive ops, ``delay`` ([n_res] int32 or None) the time after an op
+    finishes until its outputs reach its successors.
 
     Returns ``(makespan [S], finish [n_ops, S] or None, status [S])``.
     """
     succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
     op_res, prio, gap = _c(op_res, np.int32), _c(prio, np.int32), _c(gap, np.int32)
+    delay = _c(delay, np.int32)
     dur, place = _c(dur, np.int32), _c(place, np.uint16)
     n = op_res.size
     S = dur.shape[1] if dur.ndim == 2 else 0
@@ -107,7 +114,11 @@ def run_batch(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None
     status = np.empty(S, np.int32)
     finish = np.empty((n, S), np.int32) if want_finish else None
     L = library or lib()
-    if gap is None:
+    if delay is not None:
+        rc = L.oracle_run_batch_dev(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
+                                    _ptr(gap), _ptr(delay), S, _ptr(dur), S, _ptr(place), S, _ptr(makespan),
+                                    _ptr(finish), S, _ptr(status), _threads(n_threads))
+    elif gap is None:
         rc = L.oracle_run_batch(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
                                 S, _ptr(dur), S, _ptr(place), S, _ptr(makespan), _ptr(finish), S,
                                 _ptr(status), _threads(n_threads))

@@ -138,6 +138,7 @@ typedef struct {
   int64_t ld_fin;
   int rc;
   const int32_t *gap; /* [nres] or NULL: a device's idle time between consecutive ops */
+  const int32_t *delay; /* [nres] or NULL: time after an op finishes until its outputs reach its successors */
 } run_job;
 
 static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
@@ -183,10 +184,12 @@ static void replay_one(const run_job *J, sim_ws *w, int64_t s) {
         w->prev[v] = w->last[r];
         w->last[r] = v;
       }
-      /* (2) the finished op updates its successors' dependency counters */
+      /* (2) the finished op updates its successors' dependency counters; its
+       * outputs reach them at f, or with delays f + delay[r] */
+      const int64_t out = J->delay ? f + J->delay[r] : f;
       for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e) {
         int32_t x = g->si[e];
-        if (f > w->ready[x]) w->ready[x] = f;
+        if (out > w->ready[x]) w->ready[x] = out;
         if (--w->cnt[x] == 0) heap_push(g, w, x);
       }
     }
@@ -259,7 +262,7 @@ int oracle_run_batch(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
                      int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                      const uint16_t *place, int64_t ld_place, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
-  return oracle_run_batch_gap(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL, n_scen, dur,
+  return oracle_run_batch_dev(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL, NULL, n_scen, dur,
                               ld_dur, place, ld_place, makespan, finish, ld_fin, status, n_threads);
 }
 
@@ -268,12 +271,20 @@ int oracle_run_batch_gap(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
                          const int32_t *gap, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                          const uint16_t *place, int64_t ld_place, int32_t *makespan,
                          int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
+  return oracle_run_batch_dev(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, gap, NULL, n_scen, dur,
+                              ld_dur, place, ld_place, makespan, finish, ld_fin, status, n_threads);
+}
+
+int oracle_run_batch_dev(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                         const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                         const int32_t *gap, const int32_t *delay, int64_t n_scen, const int32_t *dur,
+                         int64_t ld_dur, const uint16_t *place, int64_t ld_place, int32_t *makespan,
+                         int32_t *finish, int64_t ld_fin, int32_t *status, int32_t n_threads) {
   graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL};
   int rc = check_graph(&g, 1);
   if (rc) return rc;
-  if (gap)
-    for (int32_t r = 0; r < n_res; ++r)
-      if (gap[r] < 0) return ORC_E_INVAL;
+  for (int32_t r = 0; r < n_res; ++r)
+    if ((gap && gap[r] < 0) || (delay && delay[r] < 0)) return ORC_E_INVAL;
   if (n_scen < 0 || (n_scen > 0 && !makespan)) return ORC_E_INVAL;
   if (n_scen > 0 && n_ops > 0) {
     if (!dur || ld_dur < n_scen) return ORC_E_INVAL;
@@ -299,7 +310,7 @@ int oracle_run_batch_gap(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
     return ORC_E_NOMEM;
   }
   for (int32_t t = 0; t < n_threads; ++t) {
-    run_job J = {&g, 0, 0, dur, ld_dur, place, ld_place, makespan, finish, status, ld_fin, 0, gap};
+    run_job J = {&g, 0, 0, dur, ld_dur, place, ld_place, makespan, finish, status, ld_fin, 0, gap, delay};
     jobs[t] = J;
   }
   rc = run_threads(run_range, jobs, sizeof(run_job), n_scen, n_threads, set_run_range);
@@ -739,7 +750,7 @@ int oracle_attribute(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
       rc = ORC_E_NOMEM;
     } else {
       for (int32_t t = 0; t < n_threads; ++t) {
-        at_job A = {{&g, 0, 0, dur, ld_dur, place, ld_place, makespan, NULL, status, 0, 0, NULL},
+        at_job A = {{&g, 0, 0, dur, ld_dur, place, ld_place, makespan, NULL, status, 0, 0, NULL, NULL},
                     pred_ptr, pred_idx, busy, chain, chain_ops, ld_res, path_scen, path_ops,
                     path_cap, path_len};
         jobs[t] = A;

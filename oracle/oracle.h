@@ -86,6 +86,25 @@ int oracle_run_batch_gap(int32_t n_ops, int32_t n_res,
                          int32_t *status, int32_t n_threads);
 
 /*
+ * The replay with gaps and output delays per device.  The paper lists the
+ * memcpy time around ops among its simulator's unmodelled overheads
+ * (Sec. 3); here an op on device r hands its outputs to its successors
+ * delay[r] ns after it finishes (the device itself is free at its finish,
+ * plus its gap), so a successor's ready time is the largest
+ * finish + delay[device] over its predecessors.  gap and delay: [n_res]
+ * with entries >= 0 (else ORC_E_INVAL), each may be NULL (zeros).  The
+ * makespan is the largest finish time.  Everything else as
+ * oracle_run_batch.
+ */
+int oracle_run_batch_dev(int32_t n_ops, int32_t n_res,
+                         const int64_t *succ_ptr, const int32_t *succ_idx,
+                         const int32_t *op_res, const int32_t *prio, const int32_t *gap,
+                         const int32_t *delay, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         const uint16_t *place, int64_t ld_place,
+                         int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                         int32_t *status, int32_t n_threads);
+
+/*
  * Longest path through the DAG, resources ignored: dist(v) = d(v) + max over
  * predecessors p of dist(p) (0 without predecessors); cp_len[s] = max_v
  * dist(v), 0 for an empty graph, -1 if a duration is < 1 or a path exceeds

@@ -31,11 +31,13 @@ def preds_of(n, succ_ptr, succ_idx):
     return P
 
 
-def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
+def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None, delay=None):
     """One scenario: returns finish times (list) by 1-ns time stepping.
 
     With ``gap``, a device that finishes an op at t stays idle until
-    t + gap[device] before it starts its next one.
+    t + gap[device] before it starts its next one.  With ``delay``, an op
+    finishing at t on a device counts as done for its successors at
+    t + delay[device].
     """
     prio = list(range(n)) if prio is None else [int(x) for x in prio]
     P = preds_of(n, succ_ptr, succ_idx)
@@ -47,6 +49,7 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
     queue = [deque() for _ in range(n_res)]
     running = [None] * n_res  # (op, finish)
     avail = [0] * n_res  # first tick at which each device may start an op
+    arrive = {}  # tick -> ops whose outputs reach their successors then
     finish = [None] * n
     done = 0
     arrivals = sorted((v for v in range(n) if cnt[v] == 0), key=lambda v: (prio[v], v))
@@ -54,19 +57,23 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
         queue[int(res[v])].append(v)
     t = 0
     limit = int(np.sum(dur)) + 1 + (n * int(max(gap)) if gap is not None and len(gap) else 0)
-    while done < n:
+    limit += n * int(max(delay)) if delay is not None and len(delay) else 0
+    while done < n or arrive:
         # retire everything finishing now
-        newly = []
         for r in range(n_res):
             if running[r] is not None and running[r][1] == t:
                 v = running[r][0]
                 running[r] = None
                 avail[r] = t + (int(gap[r]) if gap is not None else 0)
                 done += 1
-                for w in S[v]:
-                    cnt[w] -= 1
-                    if cnt[w] == 0:
-                        newly.append(w)
+                arrive.setdefault(t + (int(delay[r]) if delay is not None else 0), []).append(v)
+        # outputs arriving now count down their successors
+        newly = []
+        for v in arrive.pop(t, []):
+            for w in S[v]:
+                cnt[w] -= 1
+                if cnt[w] == 0:
+                    newly.append(w)
         for w in sorted(newly, key=lambda v: (prio[v], v)):
             queue[int(res[w])].append(w)
         # idle devices start their queue heads
@@ -81,7 +88,7 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
     return finish
 
 
-def _times_for_order(n, P, res, dur, orders, gap=None):
+def _times_for_order(n, P, res, dur, orders, gap=None, delay=None):
     """Start/finish/ready times implied by per-device orders, or None if the
     orders contradict the DAG (a cycle through device and data edges)."""
     prev_on_dev = {}
@@ -96,7 +103,8 @@ def _times_for_order(n, P, res, dur, orders, gap=None):
         for v in sorted(remaining):
             if all(finish[u] is not None for u in P[v]) and (
                     v not in prev_on_dev or finish[prev_on_dev[v]] is not None):
-                ready[v] = max([finish[u] for u in P[v]], default=0)
+                ready[v] = max([finish[u] + (int(delay[int(res[u])]) if delay is not None else 0)
+                                for u in P[v]], default=0)
                 avail = (finish[prev_on_dev[v]] + (int(gap[int(res[v])]) if gap is not None else 0)
                          if v in prev_on_dev else 0)
                 start = max(ready[v], avail)
@@ -108,7 +116,7 @@ def _times_for_order(n, P, res, dur, orders, gap=None):
     return ready, finish
 
 
-def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None):
+def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None, delay=None):
     """All per-device orders whose implied schedule is FIFO by (ready, prio, id).
 
     Returns a list of finish-time lists, one per consistent order.
@@ -118,7 +126,7 @@ def enumerate_orders(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None
     on = [[v for v in range(n) if int(res[v]) == r] for r in range(n_res)]
     found = []
     for orders in itertools.product(*[itertools.permutations(o) for o in on]):
-        tr = _times_for_order(n, P, res, dur, orders, gap)
+        tr = _times_for_order(n, P, res, dur, orders, gap, delay)
         if tr is None:
             continue
         ready, finish = tr

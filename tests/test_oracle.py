@@ -932,3 +932,101 @@ def test_gap_errors_and_overflow(library=None):
     mk, _, st = run_gap(g, dur, [2**30 - 1], library)
     assert st[0] == oracle.ST_OVERFLOW and mk[0] == -1
     assert st[1] == 0 and mk[1] == 2**29 + 2**30
+
+
+# ----------------------------------------------------- output delay pins
+#
+# oracle_run_batch_dev: an op on device r hands its outputs to its
+# successors delay[r] ns after it finishes (the memcpy time the paper lists
+# as unmodelled, Sec. 3); the device itself is free at the finish (plus gap).
+
+def run_dev(g, dur, gap=None, delay=None, library=None, **kw):
+    return oracle.run_batch(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], dur, prio=g.get("prio"),
+                            library=library, gap=None if gap is None else np.asarray(gap, np.int32),
+                            delay=np.asarray(delay, np.int32), **kw)
+
+
+def test_delay_hand_example(library=None):
+    # op0 (R0, 5) -> op1 (R1, 3); op2 (R0, 2).  R0's outputs take 4 ns to
+    # arrive: op1 is ready at 9 and ends at 12, while R0 is free at 5 and
+    # runs op2 over [5, 7).  Without the delay op1 ends at 8.
+    g = dict(n=3, n_res=2, succ_ptr=np.array([0, 1, 1, 1], np.int64), succ_idx=np.array([1], np.int32),
+             op_res=np.array([0, 1, 0], np.int32), prio=None)
+    dur = np.array([[5], [3], [2]], np.int32)
+    mk, fin, st = run_dev(g, dur, delay=[4, 0], library=library)
+    assert list(fin[:, 0]) == [5, 12, 7] and mk[0] == 12 and st[0] == 0
+    mk, fin, _ = run_dev(g, dur, delay=[0, 100], library=library)  # R1's delay: no successors
+    assert list(fin[:, 0]) == [5, 8, 7] and mk[0] == 8
+
+
+def test_delay_one_device_per_op_is_weighted_longest_path(library=None):
+    rng = np.random.default_rng(31)
+    for _ in range(5):
+        n = 15
+        g = rand_graph(rng, n, n, 0.25)
+        g["op_res"] = np.arange(n, dtype=np.int32)
+        dur = rng.integers(1, 100, size=(n, 3)).astype(np.int32)
+        delay = rng.integers(0, 50, size=n).astype(np.int32)
+        mk, fin, _ = run_dev(g, dur, delay=delay, library=library)
+        for s in range(3):
+            # longest path from a super-source: node n -> v weighs d(v),
+            # u -> v weighs delay(u) + d(v); scipy finds it on negated weights
+            rows, cols, wts = [], [], []
+            for v in range(n):
+                rows.append(n), cols.append(v), wts.append(-float(dur[v, s]))
+            for u in range(n):
+                for e in range(g["succ_ptr"][u], g["succ_ptr"][u + 1]):
+                    v = int(g["succ_idx"][e])
+                    rows.append(u), cols.append(v), wts.append(-float(delay[u] + dur[v, s]))
+            A = scipy.sparse.csr_matrix((wts, (rows, cols)), shape=(n + 1, n + 1))
+            dist = scipy.sparse.csgraph.bellman_ford(A, indices=n)
+            assert np.array_equal(fin[:, s], (-dist[:n]).astype(np.int64))
+
+
+def test_delay_chain_closed_form(library=None):
+    rng = np.random.default_rng(32)
+    n = 10
+    ptr = np.r_[np.arange(n, dtype=np.int64), n - 1]
+    idx = np.arange(1, n, dtype=np.int32)
+    g = dict(n=n, n_res=2, succ_ptr=ptr, succ_idx=idx, op_res=(np.arange(n) % 2).astype(np.int32), prio=None)
+    dur = rng.integers(1, 30, size=(n, 4)).astype(np.int32)
+    gap, delay = [6, 9], [11, 3]
+    _, fin, _ = run_dev(g, dur, gap=gap, delay=delay, library=library)
+    for s in range(4):
+        f = [int(dur[0, s])]
+        for k in range(1, n):  # ready when the previous op's outputs arrive; the device after its gap
+            start = f[-1] + delay[(k - 1) % 2]
+            if k >= 2:
+                start = max(start, f[-2] + gap[k % 2])
+            f.append(start + int(dur[k, s]))
+        assert list(fin[:, s]) == f
+
+
+def test_delay_matches_brute_force(library=None):
+    rng = np.random.default_rng(33)
+    for trial in range(40):
+        n = int(rng.integers(2, 7))
+        R = int(rng.integers(1, 3))
+        g = rand_graph(rng, n, R, 0.4, prio=trial % 2 == 0)
+        dur = rng.integers(1, 6, size=(n, 1)).astype(np.int32)
+        gap = rng.integers(0, 4, size=R).astype(np.int32)
+        delay = rng.integers(0, 5, size=R).astype(np.int32)
+        mk, fin, st = run_dev(g, dur, gap=gap, delay=delay, library=library)
+        assert st[0] == 0
+        tick = brute.tick_sim(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], g["prio"], gap=gap,
+                              delay=delay)
+        assert list(fin[:, 0]) == tick
+        found = brute.enumerate_orders(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], g["prio"],
+                                       gap=gap, delay=delay)
+        assert found == [tick]
+
+
+def test_delay_zero_and_errors(library=None):
+    rng = np.random.default_rng(34)
+    g = rand_graph(rng, 30, 3, 0.1)
+    dur = rng.integers(1, 100, size=(30, 6)).astype(np.int32)
+    mk0, fin0, _ = run(g, dur, library=library)
+    mk, fin, _ = run_dev(g, dur, delay=[0, 0, 0], library=library)
+    assert np.array_equal(mk, mk0) and np.array_equal(fin, fin0)
+    with pytest.raises(oracle.OracleError):
+        run_dev(g, dur, delay=[0, -1, 0], library=library)

@@ -27,7 +27,8 @@ MUTANTS = [
      "int64_t start = w->ready[v];"),
     ("ignore-inputs", "int64_t start = w->ready[v] > avail ? w->ready[v] : avail;",
      "int64_t start = avail;"),
-    ("min-instead-of-max", "if (f > w->ready[x]) w->ready[x] = f;", "if (f < w->ready[x] || w->ready[x] == 0) w->ready[x] = f;"),
+    ("min-instead-of-max", "if (out > w->ready[x]) w->ready[x] = out;",
+     "if (out < w->ready[x] || w->ready[x] == 0) w->ready[x] = out;"),
     ("ready-on-first-pred", "if (--w->cnt[x] == 0) heap_push(g, w, x);",
      "if (w->cnt[x]-- == g->indeg[x]) heap_push(g, w, x);"),
     ("makespan-of-device-0", "for (int32_t r = 0; r < g->nres; ++r)\n        if (w->rfree[r] > span)",
@@ -75,6 +76,11 @@ MUTANTS = [
      "if (J->gap && w->nrun[r] > 0) avail += J->gap[0];"),
     ("gap-counted-in-makespan", "      w->rfree[r] = f;\n      if (J->gap) w->nrun[r]++;",
      "      w->rfree[r] = f + (J->gap && w->nrun[r] > 0 ? 0 : 0) + (J->gap ? J->gap[r] : 0);\n      if (J->gap) w->nrun[r]++;"),
+    ("delay-of-device-0", "const int64_t out = J->delay ? f + J->delay[r] : f;",
+     "const int64_t out = J->delay ? f + J->delay[0] : f;"),
+    ("delay-ignored", "const int64_t out = J->delay ? f + J->delay[r] : f;", "const int64_t out = f;"),
+    ("delay-holds-device", "      w->rfree[r] = f;\n      if (J->gap) w->nrun[r]++;",
+     "      w->rfree[r] = J->delay ? f + J->delay[r] : f;\n      if (J->gap) w->nrun[r]++;"),
     ("gen-accepts-large-base", "if (b < 1 || b > ((int64_t)1 << 24)) return 0;", "if (b < 1) return 0;"),
 ]
 
