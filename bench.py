@@ -9,7 +9,7 @@ step it also times the static-order replay (every resource running its ops
 in the order the event replay ran them in scenario 0), the bottleneck
 attribution, the replay and critical path on durations generated inside the
 kernels (knob table x counter-based noise), the replay with a gap per
-resource, the sweep variant on a slice of the scenarios and, on a bounded
+resource, the replay with gaps and output delays, the sweep variant on a slice of the scenarios and, on a bounded
 sample, the CPU
 oracle, whose outputs check sampled GPU results.
 
@@ -195,6 +195,21 @@ def main():
         e1.synchronize()
         gap_ms.append(e0.elapsed_time(e1))
     log(f"replay with resource gaps {np.mean(gap_ms):.3f} ms")
+    # the device model (outside the step): the same gaps, and the outputs of
+    # ops on the last three quarters of the resources arrive 10 us after
+    # they finish
+    delays = np.full(w.n_res, 10_000, np.int32)
+    delays[: max(1, w.n_res // 4)] = 0
+    g.run(dur, place=place, makespan=pmk, finish=finish, status=pst, gap=gaps, delay=delays)
+    torch.cuda.synchronize()
+    dev_ms = []
+    for _ in range(args.steps):
+        e0.record()
+        g.run(dur, place=place, makespan=pmk, finish=finish, status=pst, gap=gaps, delay=delays)
+        e1.record()
+        e1.synchronize()
+        dev_ms.append(e0.elapsed_time(e1))
+    log(f"replay with gaps and output delays {np.mean(dev_ms):.3f} ms")
     # the level-synchronous sweep variant (outside the step) on a bounded
     # slice of the scenarios: it re-sweeps the graph every round, so it is
     # the slow exact variant; its makespans must equal the event replay's
@@ -306,6 +321,8 @@ def main():
                     "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3),
                     "gap_run_ms": float(np.mean(gap_ms)),
                     "gap_run_op_events_per_s": op_events / (float(np.mean(gap_ms)) / 1e3),
+                    "device_model_run_ms": float(np.mean(dev_ms)),
+                    "device_model_run_op_events_per_s": op_events / (float(np.mean(dev_ms)) / 1e3),
                     "sweep_ms": sweep_ms, "sweep_scenarios": sw_n,
                     "sweep_op_events_per_s": n * sw_n / (sweep_ms / 1e3),
                     "sweep_equals_event": sweep_equal},

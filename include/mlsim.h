@@ -147,6 +147,31 @@ int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
                       uint32_t flags, void *stream);
 
 /*
+ * The replay with a device model: a gap per resource (as sim_run_batch_gap)
+ * and an output delay per resource.  The paper names memory copies, with
+ * the gaps between ops, among the costs its loop leaves out (Sec. 3).  Here
+ * the outputs of an op that finishes at f on resource r reach its
+ * successors at f + delay[r] (a copy that does not occupy the resource: r
+ * can start its next op at f, or f + gap[r]).  An op is ready when the
+ * outputs of all its predecessors have arrived, and its queue order uses
+ * that ready time.  The makespan stays the largest finish time (the delay
+ * after the last op does not count).
+ *   gap    host int32 [n_res] or NULL (no gaps), every entry >= 0.
+ *   delay  host int32 [n_res] or NULL (no delays), every entry >= 0.
+ *          A negative entry returns SIM_E_INVAL.  Both arrays are read
+ *          before the call returns (their values travel to the graph's
+ *          scratch memory in stream order as kernel arguments).
+ * Other arguments, outputs and flags as sim_run_batch_gap; with both arrays
+ * NULL, or all entries 0, the result equals sim_run_batch.  Asynchronous on
+ * `stream`; no memory is allocated; calls on different streams sharing one
+ * graph must not overlap in time.
+ */
+int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                      const uint16_t *place, int64_t ld_place, const int32_t *gap,
+                      const int32_t *delay, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                      int32_t *status, uint32_t flags, void *stream);
+
+/*
  * Critical path per scenario: the longest path through the graph with
  * resources ignored, dist(v) = d(v) + max over predecessors of dist (0 if
  * none), cp_len[s] = max over v of dist(v); 0 for an empty graph, -1 if a

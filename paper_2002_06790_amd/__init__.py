@@ -29,7 +29,8 @@ ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
            "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
-           "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated")
+           "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
+           "sim_run_batch_dev")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -94,6 +95,8 @@ def _load():
     L.sim_critical_path_generated.restype = ctypes.c_int
     L.sim_run_batch_gap.argtypes = [P, I64, P, I64, P, I64, P, P, P, I64, P, U32, P]
     L.sim_run_batch_gap.restype = ctypes.c_int
+    L.sim_run_batch_dev.argtypes = [P, I64, P, I64, P, I64, P, P, P, P, I64, P, U32, P]
+    L.sim_run_batch_dev.restype = ctypes.c_int
     L.sim_static_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, P]
     L.sim_static_run_generated.restype = ctypes.c_int
     _lib = L
@@ -227,11 +230,14 @@ class Graph:
         return rc == 1
 
     def run(self, dur, place=None, want_finish: bool = False, algo: str = "auto",
-            makespan=None, finish=None, status=None, stream=None, gap=None):
+            makespan=None, finish=None, status=None, stream=None, gap=None, delay=None):
         """Replay every scenario column of ``dur`` (int32 [n_ops, S] on the GPU).
 
         ``gap`` (host int32 [n_res], or None): each resource's idle time
         between consecutive ops (sim_run_batch_gap; event algorithm only).
+        ``delay`` (host int32 [n_res], or None): the time from an op's finish
+        on each resource until its outputs reach its successors
+        (sim_run_batch_dev, with ``gap`` if given; event algorithm only).
 
         Returns ``(makespan [S], finish [n_ops, S] or None, status [S])`` as
         device tensors (allocated unless passed in).  Asynchronous on the
@@ -249,15 +255,26 @@ class Graph:
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
         fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
-        if gap is None:
+        def _res_vec(x, name):
+            x = _host(x, np.int32)
+            if x.shape != (self.n_res,):
+                raise ValueError(f"{name} must have shape (n_res={self.n_res},)")
+            return x
+
+        if delay is not None:
+            g = None if gap is None else _res_vec(gap, "gap")
+            d = _res_vec(delay, "delay")
+            rc = _load().sim_run_batch_dev(self._h, S, dptr, ld, pptr, ldp, _hptr(g), _hptr(d), makespan.data_ptr(),
+                                           fptr, ldf, status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
+            if rc:
+                raise SimError(rc, "sim_run_batch_dev")
+        elif gap is None:
             rc = _load().sim_run_batch(self._h, S, dptr, ld, pptr, ldp, makespan.data_ptr(), fptr, ldf,
                                        status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
             if rc:
                 raise SimError(rc, "sim_run_batch")
         else:
-            g = _host(gap, np.int32)
-            if g.shape != (self.n_res,):
-                raise ValueError(f"gap must have shape (n_res={self.n_res},)")
+            g = _res_vec(gap, "gap")
             rc = _load().sim_run_batch_gap(self._h, S, dptr, ld, pptr, ldp, _hptr(g), makespan.data_ptr(), fptr,
                                            ldf, status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
             if rc:

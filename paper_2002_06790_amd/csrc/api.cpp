@@ -90,14 +90,13 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
                       st);
 }
 
-extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                                  const uint16_t *place, int64_t ld_place, const int32_t *gap,
-                                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
-                                 uint32_t flags, void *stream) {
+                                 const int32_t *delay, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                                 int32_t *status, uint32_t flags, void *stream) {
   if (!g || n_scen < 0 || (flags != SIM_ALGO_AUTO && flags != SIM_ALGO_EVENT)) return SIM_E_INVAL;
-  if (!gap) return SIM_E_INVAL;
   for (int32_t r = 0; r < g->n_res; ++r)
-    if (gap[r] < 0) return SIM_E_INVAL;
+    if ((gap && gap[r] < 0) || (delay && delay[r] < 0)) return SIM_E_INVAL;
   if (n_scen == 0) return SIM_OK;
   if (!makespan) return SIM_E_INVAL;
   if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
@@ -109,12 +108,30 @@ extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32
     if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
-  // the gaps go to the graph's scratch in stream order before the replay,
-  // passed by value, so the caller's array is no longer read on return
-  int32_t *gap_dev = (int32_t *)((char *)g->scratch + g->scratch_gap_off);
-  if (int rc = launch_put_words(gap_dev, gap, g->n_res, st)) return rc;
-  return launch_event_gap(g, n_scen, dur, ld_dur, place, ld_place, gap_dev, makespan, finish, ld_fin,
-                          status, st);
+  if (!gap && !delay)
+    return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
+  // gaps then delays go to the graph's scratch in stream order before the
+  // replay, passed by value, so the caller's arrays are no longer read on
+  // return
+  const int32_t R = g->n_res;
+  std::vector<int32_t> words((size_t)2 * R, 0);
+  for (int32_t r = 0; r < R; ++r) {
+    if (gap) words[r] = gap[r];
+    if (delay) words[R + r] = delay[r];
+  }
+  int32_t *dev = (int32_t *)((char *)g->scratch + g->scratch_dev_off);
+  if (int rc = launch_put_words(dev, words.data(), 2 * R, st)) return rc;
+  return launch_event_dev(g, n_scen, dur, ld_dur, place, ld_place, dev, gap != nullptr, delay != nullptr,
+                          makespan, finish, ld_fin, status, st);
+}
+
+extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                                 const uint16_t *place, int64_t ld_place, const int32_t *gap,
+                                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                                 uint32_t flags, void *stream) {
+  if (!gap) return SIM_E_INVAL;
+  return sim_run_batch_dev(g, n_scen, dur, ld_dur, place, ld_place, gap, nullptr, makespan, finish, ld_fin,
+                           status, flags, stream);
 }
 
 extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32_t *dur,

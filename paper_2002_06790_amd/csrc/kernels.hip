@@ -318,8 +318,12 @@ struct EvArgs {
   int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
   int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
   DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
-  const int32_t *gap; // [R] or null: each resource's idle time between consecutive ops
-  int gap_lds;        // byte offset of the resource gap table in LDS (when gap is set)
+  // device model, or null: [2R] words, each resource's idle time between
+  // consecutive ops (gap) and then the time from an op's finish until its
+  // outputs reach its successors (output delay)
+  const int32_t *dev;
+  int dev_gap, dev_delay;  // which of the two halves apply (uniform)
+  int dev_lds;             // byte offset of the device-model table in LDS (when dev is set)
 };
 
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
@@ -349,7 +353,7 @@ template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, 
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, Heap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
-                                           uint32_t s_hi, lptr<const int32_t> gap_l, uint32_t &st,
+                                           uint32_t s_hi, lptr<const int32_t> dev_l, uint32_t &st,
                                            uint32_t &span,
                                            int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
                                            int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
@@ -412,12 +416,17 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     st |= SIM_ST_OVERFLOW;
     fin = kI32Max;
   }
-  // the resource can start its next op at fin, or with gaps fin + gap[r]
-  // (saturated at 2^31, which still makes any later finish overflow)
-  uint32_t avail = fin;
-  if (a.gap) {
-    const uint32_t x = fin + (uint32_t)gap_l[r];
+  // the resource can start its next op at fin, or with gaps fin + gap[r];
+  // successors see the outputs at fin, or with delays fin + delay[r] (both
+  // saturated at 2^31, which still makes any later finish overflow)
+  uint32_t avail = fin, out = fin;
+  if (a.dev_gap) {
+    const uint32_t x = fin + (uint32_t)dev_l[r];
     avail = x < kI32Max + 1u ? x : kI32Max + 1u;
+  }
+  if (a.dev_delay) {
+    const uint32_t x = fin + (uint32_t)dev_l[R + r];
+    out = x < kI32Max + 1u ? x : kI32Max + 1u;
   }
   rf_set(r, avail);
   span = fin > span ? fin : span;
@@ -468,7 +477,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   for (int e = 0; e < nsucc; ++e) {
     const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);  // {successor, join}
     if (sw.y < 0) {  // a plain successor, or the next member of a barrier
-      release(sw.y == kJoinSibling ? ready : fin, sw.x);
+      release(sw.y == kJoinSibling ? ready : out, sw.x);
       continue;
     }
     // the join's state {predecessors finished, max finish} (already read for
@@ -484,7 +493,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
       if (!G.pk_jn) ji = settle(G.jinfo[j]);
     }
     if (G.pk_jn) ji = make_int2((int)((uint32_t)sw.y >> 16), sw.x);
-    const uint32_t rdy = (uint32_t)js.y > fin ? (uint32_t)js.y : fin;
+    const uint32_t rdy = (uint32_t)js.y > out ? (uint32_t)js.y : out;
     if (js.x + 1 < ji.x) {
       jst.set(j, make_int2(js.x + 1, (int)rdy));
       continue;
@@ -518,13 +527,13 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
-  // resource gaps (one table per wave, after every per-lane region)
-  const lptr<int32_t> gap_w = as_lds((int32_t *)((char *)lds + a.gap_lds));
-  if (a.gap) {
-    for (int r = lane; r < R; r += kWave) gap_w[r] = a.gap[r];
+  // device model (one table per wave, after every per-lane region)
+  const lptr<int32_t> dev_w = as_lds((int32_t *)((char *)lds + a.dev_lds));
+  if (a.dev) {
+    for (int r = lane; r < 2 * R; r += kWave) dev_w[r] = a.dev[r];
     __syncthreads();
   }
-  const lptr<const int32_t> gap_l = (lptr<const int32_t>)gap_w;
+  const lptr<const int32_t> dev_l = (lptr<const int32_t>)dev_w;
   WideHeap<REG> heap;
   heap.l = as_lds(lds) + lane;
   heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
@@ -609,11 +618,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       auto run_step = [&](auto jp) {
         if (__ballot(end > heap.le))
           event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
-                                                             gap_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                             dev_l, st, span, fq, rq, pq, rf_get, rf_set,
                                                              last_xchg, flush);
         else
           event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo,
-                                                              s_hi, gap_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                              s_hi, dev_l, st, span, fq, rq, pq, rf_get, rf_set,
                                                               last_xchg, flush);
       };
       if constexpr (JOIN_LDS)
@@ -1116,7 +1125,8 @@ int plan_scratch(sim_graph *g) {
   const size_t join_lds_bytes = P.ev_join_lds ? join_bytes : 0;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = (P.ev_join_lds ? 0 : join_bytes) + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
-  const size_t gap_table = ((size_t)G.R * 4 + 15) & ~size_t(15);  // resource gaps, after the per-lane regions
+  // device model (gaps, output delays), after the per-lane regions
+  const size_t dev_table = ((size_t)G.R * 8 + 15) & ~size_t(15);
   auto grid_of = [&](int occ) -> int32_t {  // resident blocks within the scratch budget
     size_t b = (size_t)std::max(occ, 1);
     if (ev_per_block) b = std::min(b, std::max<size_t>(1, kScratchBudget / ev_per_block));
@@ -1126,39 +1136,39 @@ int plan_scratch(sim_graph *g) {
   };
   // the root's children in LDS (every variant)
   P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes + join_lds_bytes;
-  int occ[3];  // plain, generated durations, resource gaps
+  int occ[3];  // plain, generated durations, device model
   if (P.ev_join_lds) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes + gap_table, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes + dev_table, cus);
   } else if (rf_lds) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes + gap_table, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes + dev_table, cus);
   } else {
     occ[0] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes + gap_table, cus);
+    occ[2] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes + dev_table, cus);
   }
   if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
   P.ev_blocks = grid_of(occ[0]);
   P.ev_gen_blocks = grid_of(occ[1]);
-  P.ev_gap_blocks = grid_of(occ[2]);
+  P.ev_dev_blocks = grid_of(occ[2]);
   // the root's children in registers (resource times in LDS, join state in
   // global memory, no placement, no predecessor recording): 4 KB less LDS
   P.ev_reg = rf_lds && !P.ev_join_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
-  P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_gap_blocks = P.ev_reg_prev_blocks = 1;
+  P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_dev_blocks = P.ev_reg_prev_blocks = 1;
   P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + rf_lds_bytes;  // with the last-op table
   if (P.ev_reg) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, false, true>, P.ev_reg_lds_bytes, cus);
     occ[2] = occupancy_blocks(k_event<true, false, false, false, false, false, true>,
-                              P.ev_reg_lds_bytes + gap_table, cus);
+                              P.ev_reg_lds_bytes + dev_table, cus);
     if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
     P.ev_reg_blocks = grid_of(occ[0]);
     P.ev_reg_gen_blocks = grid_of(occ[1]);
-    P.ev_reg_gap_blocks = grid_of(occ[2]);
+    P.ev_reg_dev_blocks = grid_of(occ[2]);
     const int prev_occ =
         occupancy_blocks(k_event<true, false, false, true, false, false, true>, P.ev_reg_prev_lds_bytes, cus);
     if (prev_occ < 0) return SIM_E_HIP;
@@ -1183,8 +1193,8 @@ int plan_scratch(sim_graph *g) {
                                    : std::min<size_t>(at_occ, std::max<size_t>(1, kScratchBudget / at_bytes)));
 
   // scratch for the largest persistent grid of any event variant
-  const int32_t ev_grid = std::max({P.ev_blocks, P.ev_gen_blocks, P.ev_gap_blocks, P.ev_prev_blocks,
-                                    P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_gap_blocks,
+  const int32_t ev_grid = std::max({P.ev_blocks, P.ev_gen_blocks, P.ev_dev_blocks, P.ev_prev_blocks,
+                                    P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_dev_blocks,
                                     P.ev_reg_prev_blocks});
 
   // critical path: slots in LDS when they fit, else in global scratch
@@ -1237,7 +1247,7 @@ int plan_scratch(sim_graph *g) {
   g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   g->scratch_gen_off = take((size_t)std::max(G.n, 1) * 4);  // one generated duration column
-  g->scratch_gap_off = take((size_t)G.R * 4);                 // the resource gaps of a call
+  g->scratch_dev_off = take((size_t)G.R * 8);                 // the device model of a call
   {
     const int rc = plan_walk(g, cus);
     if (rc) return rc;
@@ -1272,13 +1282,15 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
                       const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream,
-                      const DurGen *gen = nullptr, const int32_t *gap = nullptr) {
+                      const DurGen *gen = nullptr, const int32_t *dev = nullptr, bool has_gap = false,
+                      bool has_delay = false) {
   const ScratchPlan &P = g->plan;
   char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
-           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, gap, 0};
+           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{},
+           dev, has_gap, has_delay, 0};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = rf_in_lds(g->dg);
@@ -1287,14 +1299,14 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   // fewer blocks that each take the same number of tiles (within one)
   // registers for the heap root's children when the chip is full: the
   // variant with the children in LDS would need two or more rounds of tiles
-  const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : gap ? P.ev_gap_blocks : P.ev_blocks;
+  const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : dev ? P.ev_dev_blocks : P.ev_blocks;
   bool reg = P.ev_reg && !place && tiles >= 2 * lds_blocks;
   if (const char *e = getenv("MLSIM_EV_REG"))  // tuning override
     reg = P.ev_reg && !place && atoi(e) != 0;
   const int64_t blocks = !reg ? lds_blocks
                          : prev ? P.ev_reg_prev_blocks
                          : gen  ? P.ev_reg_gen_blocks
-                         : gap  ? P.ev_reg_gap_blocks
+                         : dev  ? P.ev_reg_dev_blocks
                                 : P.ev_reg_blocks;
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
@@ -1302,9 +1314,9 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
                                                 : (tiles + rounds - 1) / rounds));
   size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
                    : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
-  if (gap) {  // the resource gap table after the per-lane regions
-    a.gap_lds = (int)lds;
-    lds += ((size_t)g->dg.R * 4 + 15) & ~size_t(15);
+  if (dev) {  // the device-model table after the per-lane regions
+    a.dev_lds = (int)lds;
+    lds += ((size_t)g->dg.R * 8 + 15) & ~size_t(15);
   }
   const int variant = (reg ? 64 : 0) | (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
                       (rf_lds ? 4 : 0) | (g->dg.ev_compact ? 2 : 0) | (place ? 1 : 0);
@@ -1426,11 +1438,12 @@ int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld,
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
-int launch_event_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                     const uint16_t *place, int64_t ld_place, const int32_t *gap, int32_t *makespan,
-                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
+int launch_event_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, const int32_t *dev, bool has_gap,
+                     bool has_delay, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                     hipStream_t stream) {
   return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, 0,
-                           nullptr, nullptr, 0, nullptr, stream, nullptr, gap);
+                           nullptr, nullptr, 0, nullptr, stream, nullptr, dev, has_gap, has_delay);
 }
 
 int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,

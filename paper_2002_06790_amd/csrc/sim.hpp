@@ -176,10 +176,10 @@ struct ScratchPlan {
   // generated durations: persistent grids of the event and critical-path kernels
   int32_t ev_gen_blocks, cp_gen_blocks;
   int32_t ev_join_lds;  // event kernel: join state in LDS (after the resource times)
-  int32_t ev_gap_blocks;  // event kernel with resource gaps (their table in LDS)
+  int32_t ev_dev_blocks;  // event kernel with a device model (gaps, delays: their table in LDS)
   // event kernel with the heap root's children in registers: available,
-  // persistent grids (plain, generated durations, gaps) and LDS per block
-  int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_gap_blocks, ev_reg_prev_blocks;
+  // persistent grids (plain, generated durations, device model) and LDS per block
+  int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_dev_blocks, ev_reg_prev_blocks;
   size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   // lockstep walk: 0 when the graph does not fit its limits
@@ -205,7 +205,7 @@ struct sim_graph {
   void *scratch;          // event kernel: heaps / join state (global variants)
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
-  size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off, scratch_gap_off;
+  size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off, scratch_dev_off;
   // host copies: critical-path recovery (compact predecessor CSR and the
   // caller id of each compact id) and static-order compilation (resource of
   // each op by caller id)
@@ -242,9 +242,12 @@ int launch_zero(int32_t *dst, int64_t count, int64_t ld, int32_t rows, hipStream
 int launch_put_words(int32_t *dst, const int32_t *src, int32_t count, hipStream_t stream);
 // generated durations: written out, or consumed by the event replay
 int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream);
-int launch_event_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                     const uint16_t *place, int64_t ld_place, const int32_t *gap, int32_t *makespan,
-                     int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
+// the event replay with a device model: dev is device memory of 2 n_res
+// words (gaps, then output delays); has_gap / has_delay say which apply
+int launch_event_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                     const uint16_t *place, int64_t ld_place, const int32_t *dev, bool has_gap,
+                     bool has_delay, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                     hipStream_t stream);
 int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 // attribution: the event replay that also records each op's predecessor on

@@ -105,3 +105,12 @@ def test_gap_argument_errors_without_gpu(L):
     gap = np.zeros(4, np.int32)
     assert L.sim_run_batch_gap(None, 1, None, 1, None, 0, gap.ctypes.data, None, None, 0, None, 0,
                                None) == mlsim.SIM_E_INVAL
+
+
+def test_device_model_argument_errors_without_gpu(L):
+    gap = np.zeros(4, np.int32)
+    delay = np.zeros(4, np.int32)
+    assert L.sim_run_batch_dev(None, 1, None, 1, None, 0, gap.ctypes.data, delay.ctypes.data, None, None, 0, None,
+                               0, None) == mlsim.SIM_E_INVAL
+    assert L.sim_run_batch_dev(None, 1, None, 1, None, 0, None, None, None, None, 0, None, 0,
+                               None) == mlsim.SIM_E_INVAL
