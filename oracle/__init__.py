@@ -17,7 +17,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "liboracle.so")
 
 OK, E_INVAL, E_RANGE, E_CYCLE, E_NOMEM = 0, -1, -2, -3, -4
-ST_BAD_DUR, ST_BAD_RES, ST_OVERFLOW = 1, 2, 4
+ST_BAD_DUR, ST_BAD_RES, ST_OVERFLOW, ST_SHARE_LIMIT = 1, 2, 4, 8
+#: bandwidth sharing: most ops at once on a shared device; service units per ns
+SHARE_MAX, SHARE_UNIT = 16, 720720
 
 
 def build() -> str:
@@ -52,6 +54,9 @@ def lib(path: Optional[str] = None):
                                            P, ctypes.c_int64, P, ctypes.c_int64, P, P, ctypes.c_int64,
                                            P, ctypes.c_int32]
         L.oracle_run_batch_dev.restype = ctypes.c_int
+        L.oracle_run_batch_share.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, ctypes.c_int64,
+                                             P, ctypes.c_int64, P, P, ctypes.c_int64, P, ctypes.c_int32]
+        L.oracle_run_batch_share.restype = ctypes.c_int
         L.oracle_critical_path.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, P, ctypes.c_int64,
                                            P, ctypes.c_int64, P, ctypes.c_int32, P, ctypes.c_int32]
         L.oracle_critical_path.restype = ctypes.c_int
@@ -126,6 +131,30 @@ def run_batch(succ_ptr, succ_idx, op_res, n_res: int, dur, prio=None, place=None
         rc = L.oracle_run_batch_gap(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio),
                                     _ptr(gap), S, _ptr(dur), S, _ptr(place), S, _ptr(makespan), _ptr(finish),
                                     S, _ptr(status), _threads(n_threads))
+    if rc:
+        raise OracleError(rc)
+    return makespan, finish, status
+
+
+def run_batch_share(succ_ptr, succ_idx, op_res, n_res: int, dur, share=None, prio=None,
+                    want_finish: bool = True, n_threads: Optional[int] = None, library=None):
+    """Replay every scenario column of ``dur`` with bandwidth sharing on the
+    devices where ``share`` ([n_res], nonzero: shared) is set.
+
+    Returns ``(makespan [S], finish [n_ops, S] or None, status [S])``.
+    """
+    succ_ptr, succ_idx = _c(succ_ptr, np.int64), _c(succ_idx, np.int32)
+    op_res, prio, dur = _c(op_res, np.int32), _c(prio, np.int32), _c(dur, np.int32)
+    share = None if share is None else np.ascontiguousarray(np.asarray(share) != 0, dtype=np.uint8)
+    n = op_res.size
+    S = dur.shape[1] if dur.ndim == 2 else 0
+    makespan = np.empty(S, np.int32)
+    status = np.empty(S, np.int32)
+    finish = np.empty((n, S), np.int32) if want_finish else None
+    L = library or lib()
+    rc = L.oracle_run_batch_share(n, n_res, _ptr(succ_ptr), _ptr(succ_idx), _ptr(op_res), _ptr(prio), _ptr(share),
+                                  S, _ptr(dur), S, _ptr(makespan), _ptr(finish), S, _ptr(status),
+                                  _threads(n_threads))
     if rc:
         raise OracleError(rc)
     return makespan, finish, status

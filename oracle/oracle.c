@@ -320,6 +320,222 @@ int oracle_run_batch_dev(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
   return rc;
 }
 
+/* ------------------------------------------------- bandwidth sharing */
+
+typedef struct {
+  const graph_t *g;
+  int64_t s0, s1;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *makespan, *finish, *status;
+  int64_t ld_fin;
+  int rc;
+  const uint8_t *share;
+} share_job;
+
+/* one shared device: the service units each active op has received since
+ * time 0 (vt, as of time tl), and its active ops with the units at which
+ * each is done */
+typedef struct {
+  int64_t vt, tl;
+  int32_t k;
+  int32_t op[ORC_SHARE_MAX];
+  int64_t need[ORC_SHARE_MAX];
+} link_t;
+
+/* bring the device's service count to time t (k constant since tl) */
+static void link_advance(link_t *L, int64_t t) {
+  if (L->k > 0) L->vt += (t - L->tl) * (ORC_SHARE_UNIT / L->k);
+  L->tl = t;
+}
+
+/* the first integer ns at which the device's next op is done (k > 0) */
+static int64_t link_next(const link_t *L) {
+  int64_t m = L->need[0];
+  for (int32_t i = 1; i < L->k; ++i)
+    if (L->need[i] < m) m = L->need[i];
+  const int64_t per_ns = ORC_SHARE_UNIT / L->k;
+  return L->tl + (m - L->vt + per_ns - 1) / per_ns;
+}
+
+static void release_succ(const graph_t *g, sim_ws *w, int32_t v, int64_t t) {
+  for (int64_t e = g->sp[v]; e < g->sp[v + 1]; ++e) {
+    int32_t x = g->si[e];
+    if (t > w->ready[x]) w->ready[x] = t;
+    w->cnt[x] -= 1;
+    if (w->cnt[x] == 0) heap_push(g, w, x);
+  }
+}
+
+static void share_one(share_job *J, sim_ws *w, link_t *links, int64_t s) {
+  const graph_t *g = J->g;
+  int32_t st = 0;
+  for (int32_t v = 0; v < g->n; ++v) {
+    const int32_t dv = J->dur[(int64_t)v * J->ld_dur + s];
+    if (dv < 1) st |= ORC_ST_BAD_DUR;
+  }
+  int64_t span = 0;
+  if (!st) {
+    for (int32_t v = 0; v < g->n; ++v) {
+      w->ready[v] = 0;
+      w->cnt[v] = g->indeg[v];
+    }
+    for (int32_t r = 0; r < g->nres; ++r) {
+      w->rfree[r] = 0;
+      links[r].vt = links[r].tl = 0;
+      links[r].k = 0;
+    }
+    w->hsize = 0;
+    for (int32_t v = 0; v < g->n; ++v)
+      if (w->cnt[v] == 0) heap_push(g, w, v);
+    for (;;) {
+      /* the earliest finish on a shared device (lowest device on ties) */
+      int32_t lr = -1;
+      int64_t lt = 0;
+      for (int32_t r = 0; r < g->nres; ++r)
+        if (J->share[r] && links[r].k > 0) {
+          int64_t t = link_next(&links[r]);
+          if (lr < 0 || t < lt) {
+            lr = r;
+            lt = t;
+          }
+        }
+      if (lr >= 0 && (w->hsize == 0 || lt <= w->ready[w->heap[0]])) {
+        if (lt > INT32_MAX) {
+          st |= ORC_ST_OVERFLOW;
+          break;
+        }
+        link_t *L = &links[lr];
+        link_advance(L, lt);
+        /* every active op that has its units leaves at lt */
+        for (int32_t i = 0; i < L->k;) {
+          if (L->need[i] <= L->vt) {
+            int32_t v = L->op[i];
+            w->fin[v] = lt;
+            if (lt > span) span = lt;
+            L->op[i] = L->op[L->k - 1];
+            L->need[i] = L->need[L->k - 1];
+            L->k--;
+            release_succ(g, w, v, lt);
+          } else {
+            ++i;
+          }
+        }
+        continue;
+      }
+      if (w->hsize == 0) break;
+      int32_t v = heap_pop(g, w);
+      int32_t r = g->res[v];
+      int64_t d = J->dur[(int64_t)v * J->ld_dur + s];
+      if (J->share[r]) {
+        /* joins the device's active ops at its ready time */
+        link_t *L = &links[r];
+        if (L->k == ORC_SHARE_MAX) {
+          st |= ORC_ST_SHARE_LIMIT;
+          break;
+        }
+        link_advance(L, w->ready[v]);
+        L->op[L->k] = v;
+        L->need[L->k] = L->vt + d * ORC_SHARE_UNIT;
+        L->k++;
+        continue;
+      }
+      int64_t start = w->ready[v] > w->rfree[r] ? w->ready[v] : w->rfree[r];
+      int64_t f = start + d;
+      if (f > (int64_t)INT32_MAX) {
+        st |= ORC_ST_OVERFLOW;
+        break;
+      }
+      w->fin[v] = f;
+      w->rfree[r] = f;
+      if (f > span) span = f;
+      release_succ(g, w, v, f);
+    }
+  }
+  if (J->status) J->status[s] = st;
+  J->makespan[s] = st ? -1 : (int32_t)span;
+  if (J->finish && !st)
+    for (int32_t v = 0; v < g->n; ++v) J->finish[(int64_t)v * J->ld_fin + s] = (int32_t)w->fin[v];
+}
+
+static void *share_range(void *arg) {
+  share_job *J = (share_job *)arg;
+  const graph_t *g = J->g;
+  size_t n = (size_t)(g->n ? g->n : 1), R = (size_t)(g->nres ? g->nres : 1);
+  sim_ws w;
+  memset(&w, 0, sizeof(w));
+  w.ready = (int64_t *)malloc(n * sizeof(int64_t));
+  w.cnt = (int32_t *)malloc(n * sizeof(int32_t));
+  w.fin = (int64_t *)malloc(n * sizeof(int64_t));
+  w.rfree = (int64_t *)malloc(R * sizeof(int64_t));
+  w.heap = (int32_t *)malloc(n * sizeof(int32_t));
+  link_t *links = (link_t *)malloc(R * sizeof(link_t));
+  if (!w.ready || !w.cnt || !w.fin || !w.rfree || !w.heap || !links) {
+    J->rc = ORC_E_NOMEM;
+  } else {
+    for (int64_t s = J->s0; s < J->s1; ++s) share_one(J, &w, links, s);
+  }
+  free(w.ready);
+  free(w.cnt);
+  free(w.fin);
+  free(w.rfree);
+  free(w.heap);
+  free(links);
+  return NULL;
+}
+
+static void set_share_range(void *p, int64_t a, int64_t b) {
+  ((share_job *)p)->s0 = a;
+  ((share_job *)p)->s1 = b;
+}
+
+int oracle_run_batch_share(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                           const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                           const uint8_t *share, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                           int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                           int32_t n_threads) {
+  graph_t g = {n_ops, n_res, succ_ptr, succ_idx, op_res, prio, NULL};
+  int rc = check_graph(&g, 1);
+  if (rc) return rc;
+  if (n_scen < 0 || (n_scen > 0 && !makespan)) return ORC_E_INVAL;
+  if (n_scen > 0 && n_ops > 0) {
+    if (!dur || ld_dur < n_scen) return ORC_E_INVAL;
+    if (finish && ld_fin < n_scen) return ORC_E_INVAL;
+  }
+  uint8_t *sh = (uint8_t *)calloc((size_t)(n_res > 0 ? n_res : 1), 1);
+  if (!sh) return ORC_E_NOMEM;
+  for (int32_t r = 0; r < n_res; ++r) sh[r] = share ? share[r] != 0 : 0;
+  if ((rc = build_indeg(&g))) {
+    free(sh);
+    return rc;
+  }
+  int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_ops ? n_ops : 1));
+  int acyclic = order ? topo_order(&g, order) : -1;
+  free(order);
+  if (acyclic != 1) {
+    free(g.indeg);
+    free(sh);
+    return acyclic < 0 ? ORC_E_NOMEM : ORC_E_CYCLE;
+  }
+  if (n_threads < 1) n_threads = 1;
+  share_job *jobs = (share_job *)calloc((size_t)n_threads, sizeof(share_job));
+  if (!jobs) {
+    free(g.indeg);
+    free(sh);
+    return ORC_E_NOMEM;
+  }
+  for (int32_t t = 0; t < n_threads; ++t) {
+    share_job J = {&g, 0, 0, dur, ld_dur, makespan, finish, status, ld_fin, 0, sh};
+    jobs[t] = J;
+  }
+  rc = run_threads(share_range, jobs, sizeof(share_job), n_scen, n_threads, set_share_range);
+  for (int32_t t = 0; t < n_threads && !rc; ++t) rc = jobs[t].rc;
+  free(jobs);
+  free(g.indeg);
+  free(sh);
+  return rc;
+}
+
 /* --------------------------------------------------------- critical path */
 
 typedef struct {

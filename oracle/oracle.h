@@ -43,6 +43,13 @@ extern "C" {
 #define ORC_ST_BAD_DUR 1
 #define ORC_ST_BAD_RES 2
 #define ORC_ST_OVERFLOW 4
+#define ORC_ST_SHARE_LIMIT 8 /* more than ORC_SHARE_MAX ops at once on a shared device */
+
+/* bandwidth sharing: concurrent ops per shared device, and the service unit
+ * (lcm(1..16): the service one op receives per ns is an integer number of
+ * units for every count of active ops up to ORC_SHARE_MAX) */
+#define ORC_SHARE_MAX 16
+#define ORC_SHARE_UNIT 720720
 
 /*
  * Replay every scenario s in [0, n_scen).
@@ -103,6 +110,30 @@ int oracle_run_batch_dev(int32_t n_ops, int32_t n_res,
                          const uint16_t *place, int64_t ld_place,
                          int32_t *makespan, int32_t *finish, int64_t ld_fin,
                          int32_t *status, int32_t n_threads);
+
+/*
+ * The replay with bandwidth sharing on some devices.  The paper leaves
+ * concurrent transfers dividing one link's bandwidth to future work
+ * (Sec. 4).  A device with share[r] != 0 has no queue: every op that becomes
+ * ready on it starts at once, and the ops active on it divide its rate
+ * equally (processor sharing), an op's duration being its time when alone.
+ * Time is kept in integer ns: between two consecutive event times every
+ * active op receives (t2 - t1) * ORC_SHARE_UNIT / k service units, k being
+ * the number of active ops; an op needs dur * ORC_SHARE_UNIT units and
+ * finishes at the first integer ns at which it has them.  Events at one time
+ * are taken in this order: ops finishing on shared devices (lower device
+ * first), then ready ops in (ready time, priority, id) order.  More than
+ * ORC_SHARE_MAX ops at once on one shared device set ORC_ST_SHARE_LIMIT;
+ * the replay of that scenario stops at the first such event or overflow.
+ * Devices with share[r] == 0 behave as in oracle_run_batch.  share: [n_res]
+ * or NULL (no shared devices).  No placement.
+ */
+int oracle_run_batch_share(int32_t n_ops, int32_t n_res,
+                           const int64_t *succ_ptr, const int32_t *succ_idx,
+                           const int32_t *op_res, const int32_t *prio, const uint8_t *share,
+                           int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                           int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                           int32_t *status, int32_t n_threads);
 
 /*
  * Longest path through the DAG, resources ignored: dist(v) = d(v) + max over

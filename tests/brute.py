@@ -88,6 +88,73 @@ def tick_sim(n, n_res, succ_ptr, succ_idx, res, dur, prio=None, gap=None, delay=
     return finish
 
 
+def tick_sim_share(n, n_res, succ_ptr, succ_idx, res, dur, share, prio=None):
+    """One scenario with bandwidth sharing, by 1-ns time stepping: finish
+    times (list).
+
+    A device with share[r] set runs every op ready on it at once; over each
+    nanosecond its k active ops each receive 1/k ns of service (exact
+    fractions), and an op leaves at the first tick at which its service
+    reaches its duration.  Other devices run their queues first in first out
+    as in tick_sim.
+    """
+    from fractions import Fraction
+    prio = list(range(n)) if prio is None else [int(x) for x in prio]
+    P = preds_of(n, succ_ptr, succ_idx)
+    S = [set() for _ in range(n)]
+    for v in range(n):
+        for u in P[v]:
+            S[u].add(v)
+    cnt = [len(P[v]) for v in range(n)]
+    queue = [deque() for _ in range(n_res)]
+    running = [None] * n_res
+    active = [dict() for _ in range(n_res)]  # shared devices: op -> service received
+    finish = [None] * n
+
+    def enter(ops):
+        for v in sorted(ops, key=lambda v: (prio[v], v)):
+            r = int(res[v])
+            if share[r]:
+                active[r][v] = Fraction(0)
+            else:
+                queue[r].append(v)
+
+    enter([v for v in range(n) if cnt[v] == 0])
+    done, t = 0, 0
+    limit = int(np.sum(dur)) + n + 1
+    while done < n:
+        ended = []
+        for r in range(n_res):
+            if running[r] is not None and running[r][1] == t:
+                ended.append(running[r][0])
+                running[r] = None
+            for v in [v for v, got in active[r].items() if got >= int(dur[v])]:
+                del active[r][v]
+                finish[v] = t
+                ended.append(v)
+        newly = []
+        for v in ended:
+            done += 1
+            for w in S[v]:
+                cnt[w] -= 1
+                if cnt[w] == 0:
+                    newly.append(w)
+        enter(newly)
+        for r in range(n_res):
+            if running[r] is None and queue[r]:
+                v = queue[r].popleft()
+                finish[v] = t + int(dur[v])
+                running[r] = (v, finish[v])
+        for r in range(n_res):
+            k = len(active[r])
+            for v in active[r]:
+                active[r][v] += Fraction(1, k)
+        t += 1
+        if t > limit:
+            raise RuntimeError("tick simulation did not terminate")
+    return finish
+
+
 def _times_for_order(n, P, res, dur, orders, gap=None, delay=None):
     """Start/finish/ready times implied by per-device orders, or None if the
     orders contradict the DAG (a cycle through device and data edges)."""

@@ -1030,3 +1030,136 @@ def test_delay_zero_and_errors(library=None):
     assert np.array_equal(mk, mk0) and np.array_equal(fin, fin0)
     with pytest.raises(oracle.OracleError):
         run_dev(g, dur, delay=[0, -1, 0], library=library)
+
+
+# ---------------------------------------------------------------- bandwidth sharing
+
+
+def run_share(g, dur, share, library=None, **kw):
+    return oracle.run_batch_share(g["succ_ptr"], g["succ_idx"], g["op_res"], g["n_res"], dur, share=share,
+                                  prio=g.get("prio"), library=library, **kw)
+
+
+def no_edges(res):
+    n = len(res)
+    return dict(n=n, n_res=int(max(res)) + 1, succ_ptr=np.zeros(n + 1, np.int64), succ_idx=np.zeros(0, np.int32),
+                op_res=np.asarray(res, np.int32), prio=None)
+
+
+def test_share_hand_example(library=None):
+    # op0 (d 10) on shared link 0 from t = 0; op1 (device 1, 4) -> op2 (link
+    # 0, d 2).  Alone over [0, 4) op0 receives 4 ns; from 4 the two share:
+    # op2 needs 2 ns of service, which takes 4 ns, so it leaves at 8; op0
+    # then holds 6 and finishes its last 4 ns alone at 12.
+    g = dict(n=3, n_res=2, succ_ptr=np.array([0, 0, 1, 1], np.int64), succ_idx=np.array([2], np.int32),
+             op_res=np.array([0, 1, 0], np.int32), prio=None)
+    dur = np.array([[10], [4], [2]], np.int32)
+    mk, fin, st = run_share(g, dur, [1, 0], library=library)
+    assert list(fin[:, 0]) == [12, 4, 8] and mk[0] == 12 and st[0] == 0
+    mk, fin, _ = run_share(g, dur, [0, 0], library=library)  # exclusive: op2 waits for op0
+    assert list(fin[:, 0]) == [10, 4, 12] and mk[0] == 12
+    # equal sharing from one start: 4 and 10 -> 8 and 14; three of 3 -> 9
+    mk, fin, _ = run_share(no_edges([0, 0]), np.array([[4], [10]], np.int32), [1], library=library)
+    assert list(fin[:, 0]) == [8, 14]
+    mk, fin, _ = run_share(no_edges([0, 0, 0]), np.full((3, 1), 3, np.int32), [1], library=library)
+    assert list(fin[:, 0]) == [9, 9, 9]
+    # ties: ops 0 and 1 share link 0 and both leave at 4, when op 2 also ends
+    # on device 1.  Op 3 (after op 0) and op 4 (after op 2) become ready on
+    # device 2 at 4; the lower id runs first, although op 4 was known to be
+    # ready at 4 before the link's finishes at 4 were taken.
+    g = dict(n=5, n_res=3, succ_ptr=np.array([0, 1, 1, 2, 2, 2], np.int64), succ_idx=np.array([3, 4], np.int32),
+             op_res=np.array([0, 0, 1, 2, 2], np.int32), prio=None)
+    dur = np.array([[2], [2], [4], [5], [5]], np.int32)
+    _, fin, _ = run_share(g, dur, [1, 0, 0], library=library)
+    assert list(fin[:, 0]) == [4, 4, 4, 9, 14]
+
+
+def test_share_simultaneous_start_closed_form(library=None):
+    # k ops entering one shared link together leave in order of duration;
+    # the i-th (ascending d) at sum_{j<i} d_j + (k - i) d_i (0-based i)
+    rng = np.random.default_rng(41)
+    for k in (1, 2, 5, 16):
+        g = no_edges([0] * k)
+        dur = rng.integers(1, 1000, size=(k, 8)).astype(np.int32)
+        _, fin, st = run_share(g, dur, [1], library=library)
+        assert (st == 0).all()
+        for s in range(8):
+            d = np.sort(dur[:, s].astype(np.int64))
+            want = np.cumsum(np.r_[0, d[:-1]]) + (k - np.arange(k)) * d
+            order = np.argsort(dur[:, s], kind="stable")
+            assert np.array_equal(np.sort(fin[:, s]), want)
+            assert np.all(np.diff(fin[order, s]) >= 0)  # shorter never leaves later
+            assert fin[:, s].max() == d.sum()  # the link never idles: work conserved
+
+
+def test_share_matches_tick_simulation(library=None):
+    rng = np.random.default_rng(42)
+    for trial in range(60):
+        n = int(rng.integers(2, 12))
+        R = int(rng.integers(1, 4))
+        g = rand_graph(rng, n, R, 0.3, prio=trial % 2 == 0)
+        share = (rng.random(R) < 0.6).astype(np.uint8)
+        dur = rng.integers(1, 9, size=(n, 1)).astype(np.int32)
+        mk, fin, st = run_share(g, dur, share, library=library)
+        assert st[0] == 0
+        tick = brute.tick_sim_share(n, R, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], share, g["prio"])
+        assert list(fin[:, 0]) == tick, (trial, share)
+        assert mk[0] == max(tick)
+
+
+def test_share_off_or_without_overlap_is_the_plain_replay(library=None):
+    rng = np.random.default_rng(43)
+    g = rand_graph(rng, 40, 4, 0.1, prio=True)
+    dur = rng.integers(1, 100, size=(40, 5)).astype(np.int32)
+    mk0, fin0, _ = run(g, dur, library=library)
+    mk, fin, _ = run_share(g, dur, [0, 0, 0, 0], library=library)
+    assert np.array_equal(mk, mk0) and np.array_equal(fin, fin0)
+    mk, fin, _ = run_share(g, dur, None, library=library)
+    assert np.array_equal(fin, fin0)
+    # a chain never has two ops at once, so sharing changes nothing
+    n = 12
+    chain = dict(n=n, n_res=2, succ_ptr=np.r_[np.arange(n, dtype=np.int64), n - 1],
+                 succ_idx=np.arange(1, n, dtype=np.int32), op_res=(np.arange(n) % 2).astype(np.int32), prio=None)
+    cd = rng.integers(1, 50, size=(n, 3)).astype(np.int32)
+    _, f0, _ = run(chain, cd, library=library)
+    _, f1, _ = run_share(chain, cd, [1, 1], library=library)
+    assert np.array_equal(f0, f1)
+    # one op per shared device: never shared, the critical path
+    one = rand_graph(rng, 20, 20, 0.2)
+    one["op_res"] = np.arange(20, dtype=np.int32)
+    od = rng.integers(1, 50, size=(20, 3)).astype(np.int32)
+    mk, _, _ = run_share(one, od, np.ones(20, np.uint8), library=library)
+    cp, _ = oracle.critical_path(one["succ_ptr"], one["succ_idx"], 20, od, library=library)
+    assert np.array_equal(mk, cp)
+
+
+def test_share_bounds(library=None):
+    # with every device shared: critical path <= makespan, and each device
+    # is work conserving, so makespan <= sum of durations + one ns per op
+    rng = np.random.default_rng(44)
+    for _ in range(10):
+        g = rand_graph(rng, 30, 3, 0.08)
+        dur = rng.integers(1, 200, size=(30, 4)).astype(np.int32)
+        mk, fin, st = run_share(g, dur, [1, 1, 1], library=library)
+        cp, _ = oracle.critical_path(g["succ_ptr"], g["succ_idx"], 30, dur, library=library)
+        assert (st == 0).all() and (mk >= cp).all() and (mk <= dur.sum(0) + 30).all()
+        for v in range(30):  # an op takes at least its duration
+            for e in range(g["succ_ptr"][v], g["succ_ptr"][v + 1]):
+                assert (fin[g["succ_idx"][e]] >= fin[v] + dur[g["succ_idx"][e]]).all()
+
+
+def test_share_limit_overflow_and_errors(library=None):
+    dur = np.full((17, 2), 5, np.int32)
+    dur[3, 1] = 0
+    mk, _, st = run_share(no_edges([0] * 17), dur, [1], library=library)
+    assert st[0] == oracle.ST_SHARE_LIMIT and mk[0] == -1 and st[1] == oracle.ST_BAD_DUR
+    mk, fin, st = run_share(no_edges([0] * 16), dur[:16, :1], [1], library=library)
+    assert st[0] == 0 and (fin[:, 0] == 80).all()
+    big = np.full((2, 1), 2**30 + 1, np.int32)  # two shared ops of 2^30 + 1: both end at 2^31 + 2
+    mk, _, st = run_share(no_edges([0, 0]), big, [1], library=library)
+    assert st[0] == oracle.ST_OVERFLOW and mk[0] == -1
+    mk, _, st = run_share(no_edges([0, 0]), big, [0], library=library)  # exclusive: also overflows
+    assert st[0] == oracle.ST_OVERFLOW
+    with pytest.raises(oracle.OracleError):
+        oracle.run_batch_share(np.array([0, 1, 1], np.int64), np.array([0], np.int32), np.zeros(2, np.int32), 1,
+                               np.ones((2, 1), np.int32), share=[1], library=library)

@@ -82,6 +82,20 @@ MUTANTS = [
     ("delay-holds-device", "      w->rfree[r] = f;\n      if (J->gap) w->nrun[r]++;",
      "      w->rfree[r] = J->delay ? f + J->delay[r] : f;\n      if (J->gap) w->nrun[r]++;"),
     ("gen-accepts-large-base", "if (b < 1 || b > ((int64_t)1 << 24)) return 0;", "if (b < 1) return 0;"),
+    # bandwidth sharing
+    ("share-ignores-count", "if (L->k > 0) L->vt += (t - L->tl) * (ORC_SHARE_UNIT / L->k);",
+     "if (L->k > 0) L->vt += (t - L->tl) * ORC_SHARE_UNIT;"),
+    ("share-finish-one-ns-late", "return L->tl + (m - L->vt + per_ns - 1) / per_ns;",
+     "return L->tl + (m - L->vt + per_ns) / per_ns;"),
+    ("share-no-advance-on-arrival", "link_advance(L, w->ready[v]);\n        L->op[L->k] = v;",
+     "L->op[L->k] = v;"),
+    ("share-ops-before-finishes-on-ties", "lt <= w->ready[w->heap[0]]", "lt < w->ready[w->heap[0]]"),
+    ("share-limit-off-by-one", "if (L->k == ORC_SHARE_MAX) {", "if (L->k == ORC_SHARE_MAX - 1) {"),
+    ("share-accepts-zero-duration", "if (dv < 1) st |= ORC_ST_BAD_DUR;", "if (dv < 0) st |= ORC_ST_BAD_DUR;"),
+    ("share-ready-on-first-pred", "w->cnt[x] -= 1;\n    if (w->cnt[x] == 0) heap_push(g, w, x);",
+     "if (w->cnt[x]-- == g->indeg[x]) heap_push(g, w, x);"),
+    ("share-overflow-wraps", "if (f > (int64_t)INT32_MAX) {", "if (0) {"),
+    ("share-link-overflow-wraps", "if (lt > INT32_MAX) {", "if (0) {"),
 ]
 
 
