@@ -55,9 +55,20 @@ enum {
 enum {
   SIM_ST_BAD_DUR = 1,  /* some duration < 1 */
   SIM_ST_BAD_RES = 2,  /* some placement >= n_res */
-  SIM_ST_OVERFLOW = 4  /* a finish time exceeds INT32_MAX (only reported when
+  SIM_ST_OVERFLOW = 4, /* a finish time exceeds INT32_MAX (only reported when
                           neither bit above is set) */
+  SIM_ST_SHARE_LIMIT = 8, /* sim_run_batch_share: more than SIM_SHARE_MAX ops at
+                             once on one shared resource */
+  SIM_ST_INTERNAL = 16    /* sim_run_batch_share: a consistency check of the
+                             library failed (a defect; please report) */
 };
+
+/* bandwidth sharing (sim_run_batch_share): most ops active at once on one
+ * shared resource, and the service units a resource delivers per ns
+ * (2^12 lcm(1..16), below 2^32: k active ops get exactly equal shares when k
+ * divides it, every k <= 16 among them) */
+#define SIM_SHARE_MAX 64
+#define SIM_SHARE_UNIT 2952069120u
 
 /* sim_run_batch flags & 3: which exact algorithm computes the replay */
 enum {
@@ -170,6 +181,36 @@ int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
                       const uint16_t *place, int64_t ld_place, const int32_t *gap,
                       const int32_t *delay, int32_t *makespan, int32_t *finish, int64_t ld_fin,
                       int32_t *status, uint32_t flags, void *stream);
+
+/*
+ * The replay with bandwidth sharing on chosen resources.  The paper leaves
+ * concurrent transfers dividing one link's bandwidth to future work
+ * (Sec. 4).  A resource with share[r] != 0 has no queue: every op that
+ * becomes ready on it starts at once, and its active ops divide its rate
+ * equally (processor sharing); an op's duration is its time when alone.
+ * Time stays in integer ns: between two consecutive event times t1 < t2
+ * each of the k active ops receives (t2 - t1) * floor(SIM_SHARE_UNIT / k)
+ * service units (an exact equal share when k divides SIM_SHARE_UNIT); an
+ * op needs dur * SIM_SHARE_UNIT units and finishes at the first integer ns
+ * at which it has them.  At one time, finishes on shared
+ * resources (lower resource first) come before ready ops, which keep the
+ * (ready time, priority, id) order of sim_run_batch; other resources run
+ * first in first out as there.  The makespan is the largest finish time.
+ *   share  host uint8 [n_res] (nonzero: shared) or NULL (none shared, the
+ *          result of sim_run_batch); read before the call returns.
+ *   status SIM_ST_BAD_DUR, SIM_ST_OVERFLOW (a finish time above INT32_MAX),
+ *          SIM_ST_SHARE_LIMIT (more than SIM_SHARE_MAX ops at once on one
+ *          shared resource); a scenario's replay stops at the first
+ *          overflow or limit event in time order.
+ * dur, makespan, finish, ld_fin as sim_run_batch; no placement.  The first
+ * call on a graph allocates the scratch memory of this replay (up to about
+ * 8 GiB, held until sim_graph_destroy); later calls allocate nothing.
+ * Asynchronous on `stream`; calls on different streams sharing one graph
+ * must not overlap in time.
+ */
+int sim_run_batch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                        const uint8_t *share, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                        int32_t *status, void *stream);
 
 /*
  * Critical path per scenario: the longest path through the graph with

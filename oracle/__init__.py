@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 OK, E_INVAL, E_RANGE, E_CYCLE, E_NOMEM = 0, -1, -2, -3, -4
 ST_BAD_DUR, ST_BAD_RES, ST_OVERFLOW, ST_SHARE_LIMIT = 1, 2, 4, 8
 #: bandwidth sharing: most ops at once on a shared device; service units per ns
-SHARE_MAX, SHARE_UNIT = 16, 720720
+SHARE_MAX, SHARE_UNIT = 64, 2952069120
 
 
 def build() -> str:

@@ -337,25 +337,26 @@ typedef struct {
  * time 0 (vt, as of time tl), and its active ops with the units at which
  * each is done */
 typedef struct {
-  int64_t vt, tl;
+  uint64_t vt;
+  int64_t tl;
   int32_t k;
   int32_t op[ORC_SHARE_MAX];
-  int64_t need[ORC_SHARE_MAX];
+  uint64_t need[ORC_SHARE_MAX];
 } link_t;
 
 /* bring the device's service count to time t (k constant since tl) */
 static void link_advance(link_t *L, int64_t t) {
-  if (L->k > 0) L->vt += (t - L->tl) * (ORC_SHARE_UNIT / L->k);
+  if (L->k > 0) L->vt += (uint64_t)(t - L->tl) * (ORC_SHARE_UNIT / (uint64_t)L->k);
   L->tl = t;
 }
 
 /* the first integer ns at which the device's next op is done (k > 0) */
 static int64_t link_next(const link_t *L) {
-  int64_t m = L->need[0];
+  uint64_t m = L->need[0];
   for (int32_t i = 1; i < L->k; ++i)
     if (L->need[i] < m) m = L->need[i];
-  const int64_t per_ns = ORC_SHARE_UNIT / L->k;
-  return L->tl + (m - L->vt + per_ns - 1) / per_ns;
+  const uint64_t per_ns = ORC_SHARE_UNIT / (uint64_t)L->k;
+  return L->tl + (int64_t)((m - L->vt + per_ns - 1) / per_ns);
 }
 
 static void release_succ(const graph_t *g, sim_ws *w, int32_t v, int64_t t) {
@@ -436,7 +437,7 @@ static void share_one(share_job *J, sim_ws *w, link_t *links, int64_t s) {
         }
         link_advance(L, w->ready[v]);
         L->op[L->k] = v;
-        L->need[L->k] = L->vt + d * ORC_SHARE_UNIT;
+        L->need[L->k] = L->vt + (uint64_t)d * ORC_SHARE_UNIT;
         L->k++;
         continue;
       }

@@ -45,11 +45,11 @@ extern "C" {
 #define ORC_ST_OVERFLOW 4
 #define ORC_ST_SHARE_LIMIT 8 /* more than ORC_SHARE_MAX ops at once on a shared device */
 
-/* bandwidth sharing: concurrent ops per shared device, and the service unit
- * (lcm(1..16): the service one op receives per ns is an integer number of
- * units for every count of active ops up to ORC_SHARE_MAX) */
-#define ORC_SHARE_MAX 16
-#define ORC_SHARE_UNIT 720720
+/* bandwidth sharing: concurrent ops per shared device, and the service units
+ * a device delivers per ns (2^12 lcm(1..16), below 2^32: k active ops get
+ * exactly equal shares whenever k divides it, every k <= 16 among them) */
+#define ORC_SHARE_MAX 64
+#define ORC_SHARE_UNIT 2952069120u
 
 /*
  * Replay every scenario s in [0, n_scen).
@@ -117,10 +117,12 @@ int oracle_run_batch_dev(int32_t n_ops, int32_t n_res,
  * (Sec. 4).  A device with share[r] != 0 has no queue: every op that becomes
  * ready on it starts at once, and the ops active on it divide its rate
  * equally (processor sharing), an op's duration being its time when alone.
- * Time is kept in integer ns: between two consecutive event times every
- * active op receives (t2 - t1) * ORC_SHARE_UNIT / k service units, k being
- * the number of active ops; an op needs dur * ORC_SHARE_UNIT units and
- * finishes at the first integer ns at which it has them.  Events at one time
+ * Time is kept in integer ns: between two consecutive event times t1 < t2
+ * every active op receives (t2 - t1) * floor(ORC_SHARE_UNIT / k) service
+ * units, k being the number of active ops (an exact equal share when k
+ * divides ORC_SHARE_UNIT; otherwise less than k of ORC_SHARE_UNIT units per
+ * ns go unused); an op needs dur * ORC_SHARE_UNIT units and finishes at the
+ * first integer ns at which it has them.  Events at one time
  * are taken in this order: ops finishing on shared devices (lower device
  * first), then ready ops in (ready time, priority, id) order.  More than
  * ORC_SHARE_MAX ops at once on one shared device set ORC_ST_SHARE_LIMIT;

@@ -22,7 +22,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmlsim.so")
 
 SIM_OK, SIM_E_INVAL, SIM_E_RANGE, SIM_E_CYCLE, SIM_E_NOMEM, SIM_E_HIP, SIM_E_LIMIT = 0, -1, -2, -3, -4, -5, -6
-SIM_ST_BAD_DUR, SIM_ST_BAD_RES, SIM_ST_OVERFLOW = 1, 2, 4
+SIM_ST_BAD_DUR, SIM_ST_BAD_RES, SIM_ST_OVERFLOW, SIM_ST_SHARE_LIMIT, SIM_ST_INTERNAL = 1, 2, 4, 8, 16
+#: bandwidth sharing (include/mlsim.h): most active ops per shared resource, service units per ns
+SIM_SHARE_MAX, SIM_SHARE_UNIT = 64, 2952069120
 SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP, SIM_ALGO_WALK = 0, 1, 2, 3
 ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP, "walk": SIM_ALGO_WALK}
 
@@ -30,7 +32,7 @@ EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critic
            "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
            "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
-           "sim_run_batch_dev")
+           "sim_run_batch_dev", "sim_run_batch_share")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -97,6 +99,8 @@ def _load():
     L.sim_run_batch_gap.restype = ctypes.c_int
     L.sim_run_batch_dev.argtypes = [P, I64, P, I64, P, I64, P, P, P, P, I64, P, U32, P]
     L.sim_run_batch_dev.restype = ctypes.c_int
+    L.sim_run_batch_share.argtypes = [P, I64, P, I64, P, P, P, I64, P, P]
+    L.sim_run_batch_share.restype = ctypes.c_int
     L.sim_static_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, P]
     L.sim_static_run_generated.restype = ctypes.c_int
     _lib = L
@@ -279,6 +283,32 @@ class Graph:
                                            ldf, status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
             if rc:
                 raise SimError(rc, "sim_run_batch_gap")
+        return makespan, finish, status
+
+    def run_share(self, dur, share, want_finish: bool = False, makespan=None, finish=None, status=None,
+                  stream=None):
+        """Replay every scenario column of ``dur`` with bandwidth sharing on
+        the resources where ``share`` (host [n_res], nonzero: shared) is set
+        (sim_run_batch_share).  Returns ``(makespan, finish or None, status)``.
+        """
+        import torch
+        dptr, ld = _dev_matrix(dur, torch.int32, self.n_ops, "dur")
+        S = dur.shape[1]
+        dev = dur.device
+        sh = np.ascontiguousarray(np.asarray(share) != 0, dtype=np.uint8)
+        if sh.shape != (self.n_res,):
+            raise ValueError(f"share must have shape (n_res={self.n_res},)")
+        if makespan is None:
+            makespan = torch.empty(S, dtype=torch.int32, device=dev)
+        if status is None:
+            status = torch.empty(S, dtype=torch.int32, device=dev)
+        if want_finish and finish is None:
+            finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
+        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        rc = _load().sim_run_batch_share(self._h, S, dptr, ld, _hptr(sh), makespan.data_ptr(), fptr, ldf,
+                                         status.data_ptr(), _stream_ptr(stream))
+        if rc:
+            raise SimError(rc, "sim_run_batch_share")
         return makespan, finish, status
 
     def run_generated(self, gen: Gen, n_scen: int, want_finish: bool = False, algo: str = "auto",

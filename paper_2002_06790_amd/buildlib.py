@@ -8,7 +8,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmlsim.so")
-SOURCES = ["csrc/graph.cpp", "csrc/api.cpp", "csrc/static.cpp", "csrc/kernels.hip", "csrc/walk.hip"]
+SOURCES = ["csrc/graph.cpp", "csrc/api.cpp", "csrc/static.cpp", "csrc/kernels.hip", "csrc/walk.hip",
+           "csrc/share.hip"]
 ARCH = os.environ.get("MLSIM_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

@@ -125,6 +125,31 @@ extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32
                           makespan, finish, ld_fin, status, st);
 }
 
+extern "C" int sim_run_batch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                                   const uint8_t *share, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                                   int32_t *status, void *stream) {
+  if (!g || n_scen < 0) return SIM_E_INVAL;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (g->n_ops == 0) {
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    return SIM_OK;
+  }
+  bool any = false;
+  std::vector<int32_t> words((size_t)g->n_res, 0);
+  for (int32_t r = 0; r < g->n_res; ++r) {
+    words[r] = share && share[r] ? 1 : 0;
+    any = any || words[r];
+  }
+  if (!any)  // nothing shared: the plain replay
+    return launch_event(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status, st);
+  return launch_share(g, n_scen, dur, ld_dur, words.data(), makespan, finish, ld_fin, status, st);
+}
+
 extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                                  const uint16_t *place, int64_t ld_place, const int32_t *gap,
                                  int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,

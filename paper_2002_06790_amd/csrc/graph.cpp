@@ -679,6 +679,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
 extern "C" void sim_graph_destroy(sim_graph *g) {
   if (!g) return;
   if (g->scratch) (void)hipFree(g->scratch);
+  if (g->share_scratch) (void)hipFree(g->share_scratch);
   if (g->dev_mem) (void)hipFree(g->dev_mem);
   delete g;
 }

@@ -1,0 +1,311 @@
+// gfx950 kernel of the replay with bandwidth sharing: on a shared resource
+// (a link) every op that becomes ready starts at once and the active ops
+// divide its rate equally (processor sharing; the paper leaves concurrent
+// transfers sharing one link's bandwidth to future work, Sec. 4).
+//
+// Model, in integer ns.  Between two consecutive event times t1 < t2 every
+// active op of a shared resource with k active ops receives
+// (t2 - t1) * floor(kShareUnit / k) service units (kShareUnit =
+// 2^12 lcm(1..16): an exact equal share whenever k divides it).  The resource
+// keeps the units one op has received since time 0 (vt, as of time tl); an
+// op that arrives at time a with duration d needs vt(a) + d * kShareUnit and
+// leaves at the first integer ns t with vt(t) >= that.  Finishes on shared
+// resources at time t come before ready ops keyed t (lower resource first);
+// ready ops keep the (ready time, priority, id) order of the plain replay,
+// and other resources run their queues first in first out as there.
+//
+// Layout.  One scenario per lane.  A lane's event list is a binary heap in
+// global scratch of 64-bit keys (time << 32 | word), word = resource for a
+// pending finish on a shared resource and n_res + compact id for a ready
+// op, so one key order gives all the tie rules above.  The next finish of a
+// shared resource changes when an op arrives; every change pushes a new key
+// and a popped key is used only if it still equals the resource's current
+// next finish (older keys are skipped).  All per-lane state is lane-major
+// ([index][64]), so the lanes of a wave touch consecutive words for equal
+// indexes.
+#include <algorithm>
+
+#include "sim.hpp"
+
+namespace mlsim {
+
+namespace {
+
+constexpr uint32_t kI32Max = 0x7fffffffu;
+constexpr uint32_t kNoTime = 0xffffffffu;
+
+struct ShArgs {
+  int64_t n_scen;
+  const int32_t *dur;
+  int64_t ld_dur;
+  int32_t *makespan;
+  int32_t *finish;  // [n_ops][ld_fin] or null
+  int64_t ld_fin;
+  int32_t *status;
+  const int32_t *share;  // [R] 0 / 1
+  char *scratch;         // per block: the regions below, lane-major
+  int64_t block_bytes;
+  int64_t heap_cap;      // heap entries per lane
+  int64_t o_rd, o_cnt, o_rf, o_vt, o_tl, o_k, o_nd, o_need, o_op;  // byte offsets in a block's region
+};
+
+template <class T>
+struct Lane {  // element i of a lane-major array
+  T *p;
+  __device__ __forceinline__ T &operator[](int64_t i) const { return p[i * kWave]; }
+};
+
+__global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
+  const int lane = threadIdx.x;
+  const int n = G.n, R = G.R, N = G.n + G.nb;
+  char *blk = a.scratch + (int64_t)blockIdx.x * a.block_bytes;
+  const Lane<uint64_t> heap{(uint64_t *)blk + lane};
+  const Lane<uint32_t> rd{(uint32_t *)(blk + a.o_rd) + lane};
+  const Lane<int32_t> cnt{(int32_t *)(blk + a.o_cnt) + lane};
+  const Lane<uint32_t> rf{(uint32_t *)(blk + a.o_rf) + lane};
+  const Lane<uint64_t> vt{(uint64_t *)(blk + a.o_vt) + lane};
+  const Lane<uint32_t> tl{(uint32_t *)(blk + a.o_tl) + lane};
+  const Lane<int32_t> kk{(int32_t *)(blk + a.o_k) + lane};
+  const Lane<uint32_t> nd{(uint32_t *)(blk + a.o_nd) + lane};
+  const Lane<uint64_t> need{(uint64_t *)(blk + a.o_need) + lane};  // [R][kShareMax]
+  const Lane<int32_t> eop{(int32_t *)(blk + a.o_op) + lane};     // [R][kShareMax]
+
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    if (s >= a.n_scen) continue;
+    uint32_t st = 0;
+    for (int c = 0; c < n; ++c)
+      if (a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s] < 1) st |= SIM_ST_BAD_DUR;
+    uint32_t span = 0;
+    if (!st) {
+      for (int x = 0; x < N; ++x) {
+        rd[x] = 0;
+        cnt[x] = G.wp_ptr[x + 1] - G.wp_ptr[x];
+      }
+      for (int r = 0; r < R; ++r) {
+        rf[r] = 0;
+        vt[r] = 0;
+        tl[r] = 0;
+        kk[r] = 0;
+        nd[r] = kNoTime;
+      }
+      int64_t hs = 0;
+      auto push = [&](uint64_t key) -> bool {
+        if (hs >= a.heap_cap) return false;
+        int64_t i = hs++;
+        while (i > 0) {
+          const int64_t p = (i - 1) >> 1;
+          const uint64_t kp = heap[p];
+          if (kp <= key) break;
+          heap[i] = kp;
+          i = p;
+        }
+        heap[i] = key;
+        return true;
+      };
+      auto pop = [&]() -> uint64_t {
+        const uint64_t top = heap[0];
+        const uint64_t last = heap[--hs];
+        int64_t i = 0;
+        for (;;) {
+          const int64_t l = 2 * i + 1;
+          if (l >= hs) break;
+          int64_t m = l;
+          uint64_t km = heap[l];
+          if (l + 1 < hs) {
+            const uint64_t kr = heap[l + 1];
+            if (kr < km) {
+              m = l + 1;
+              km = kr;
+            }
+          }
+          if (km >= last) break;
+          heap[i] = km;
+          i = m;
+        }
+        if (hs > 0) heap[i] = last;
+        return top;
+      };
+      auto key_of = [](uint32_t t, uint32_t w) -> uint64_t { return ((uint64_t)t << 32) | w; };
+      // a node's predecessor finished (outputs at time t): an op whose count
+      // reaches zero is ready; a barrier passes its ready time to its members
+      bool ok = true;
+      auto release = [&](int x, uint32_t t) {
+        const uint32_t v = rd[x] > t ? rd[x] : t;
+        rd[x] = v;
+        const int left = cnt[x] - 1;
+        cnt[x] = left;
+        if (left != 0) return;
+        if (x < n) {
+          ok = ok && push(key_of(v, (uint32_t)(R + x)));
+          return;
+        }
+        for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {
+          const int y = G.ws[e];
+          rd[y] = rd[y] > v ? rd[y] : v;
+          cnt[y] = cnt[y] - 1;
+          if (cnt[y] == 0) ok = ok && push(key_of(rd[y], (uint32_t)(R + y)));
+        }
+      };
+      auto advance = [&](int r, uint32_t t) {
+        const int k = kk[r];
+        if (k > 0) vt[r] = vt[r] + (uint64_t)(t - tl[r]) * (kShareUnit / (uint64_t)k);
+        tl[r] = t;
+      };
+      // the first integer ns at which the resource's next op is done (k > 0),
+      // saturated at 2^31 (a finish there overflows)
+      auto next_finish = [&](int r) -> uint32_t {
+        const int k = kk[r];
+        uint64_t m = need[(int64_t)r * kShareMax];
+        for (int i = 1; i < k; ++i) {
+          const uint64_t x = need[(int64_t)r * kShareMax + i];
+          m = x < m ? x : m;
+        }
+        const uint64_t per_ns = kShareUnit / (uint64_t)k;
+        const uint64_t dt = (m - vt[r] + per_ns - 1) / per_ns;
+        const uint64_t t = (uint64_t)tl[r] + dt;
+        return t > kI32Max ? kI32Max + 1u : (uint32_t)t;
+      };
+      for (int k = 0; k < G.nsrc; ++k) ok = ok && push(key_of(0, (uint32_t)(R + G.src[k])));
+      // every iteration pops one key and the keys pushed are bounded by the
+      // heap capacity, so the loop ends; the guard only bounds it explicitly
+      for (int64_t it = 0; hs > 0 && ok && it <= a.heap_cap; ++it) {
+        const uint64_t key = pop();
+        const uint32_t t = (uint32_t)(key >> 32), w = (uint32_t)key;
+        if (w < (uint32_t)R) {  // a pending finish on shared resource w
+          const int r = (int)w;
+          if (kk[r] == 0 || nd[r] != t) continue;  // superseded
+          if (t > kI32Max) {
+            st |= SIM_ST_OVERFLOW;
+            break;
+          }
+          advance(r, t);
+          int k = kk[r], gone = 0;
+          const uint64_t v_now = vt[r];
+          for (int i = 0; i < k;) {
+            const int64_t base = (int64_t)r * kShareMax;
+            if (need[base + i] <= v_now) {
+              const int c = eop[base + i];
+              need[base + i] = need[base + k - 1];
+              eop[base + i] = eop[base + k - 1];
+              --k;
+              ++gone;
+              if (a.finish) a.finish[(int64_t)G.ops[c].orig * a.ld_fin + s] = (int32_t)t;
+              span = t > span ? t : span;
+              for (int e = G.ws_ptr[c]; e < G.ws_ptr[c + 1]; ++e) release(G.ws[e], t);
+            } else {
+              ++i;
+            }
+          }
+          kk[r] = k;
+          if (gone == 0) {  // cannot happen: the finish time was computed to complete an op
+            ok = false;
+            break;
+          }
+          if (k > 0) {
+            const uint32_t f = next_finish(r);
+            nd[r] = f;
+            ok = ok && push(key_of(f, (uint32_t)r));
+          } else {
+            nd[r] = kNoTime;
+          }
+          continue;
+        }
+        const int c = (int)(w - (uint32_t)R);
+        const int r = G.ops[c].res;
+        const int32_t d = a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s];
+        if (a.share[r]) {  // joins the resource's active ops at its ready time
+          const int k = kk[r];
+          if (k == kShareMax) {
+            st |= SIM_ST_SHARE_LIMIT;
+            break;
+          }
+          advance(r, t);
+          need[(int64_t)r * kShareMax + k] = vt[r] + (uint64_t)d * kShareUnit;
+          eop[(int64_t)r * kShareMax + k] = c;
+          kk[r] = k + 1;
+          const uint32_t f = next_finish(r);
+          nd[r] = f;
+          ok = ok && push(key_of(f, (uint32_t)r));
+          continue;
+        }
+        const uint32_t start = t > rf[r] ? t : rf[r];
+        const uint32_t f = start + (uint32_t)d;  // both terms <= INT32_MAX
+        if (f > kI32Max) {
+          st |= SIM_ST_OVERFLOW;
+          break;
+        }
+        rf[r] = f;
+        span = f > span ? f : span;
+        if (a.finish) a.finish[(int64_t)G.ops[c].orig * a.ld_fin + s] = (int32_t)f;
+        for (int e = G.ws_ptr[c]; e < G.ws_ptr[c + 1]; ++e) release(G.ws[e], f);
+      }
+      if (!ok) st |= SIM_ST_INTERNAL;
+    }
+    a.makespan[s] = st ? -1 : (int32_t)span;
+    if (a.status) a.status[s] = (int32_t)st;
+  }
+}
+
+}  // namespace
+
+int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur, const int32_t *share_words,
+                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  const DevGraph &G = g->dg;
+  const int64_t N = (int64_t)G.n + G.nb, R = G.R;
+  const int64_t cap = 3 * (int64_t)G.n + 1;  // ready ops (n) + two keys per op on a shared resource
+  auto al = [](int64_t b) { return (b + 255) & ~(int64_t)255; };
+  ShArgs a{};
+  int64_t off = 0;
+  off += al(cap * 8 * kWave);
+  a.o_rd = off;
+  off += al(N * 4 * kWave);
+  a.o_cnt = off;
+  off += al(N * 4 * kWave);
+  a.o_rf = off;
+  off += al(R * 4 * kWave);
+  a.o_vt = off;
+  off += al(R * 8 * kWave);
+  a.o_tl = off;
+  off += al(R * 4 * kWave);
+  a.o_k = off;
+  off += al(R * 4 * kWave);
+  a.o_nd = off;
+  off += al(R * 4 * kWave);
+  a.o_need = off;
+  off += al(R * kShareMax * 8 * kWave);
+  a.o_op = off;
+  off += al(R * kShareMax * 4 * kWave);
+  a.block_bytes = off;
+  a.heap_cap = cap;
+  // a persistent grid within the scratch budget, allocated on first use:
+  // the resource flags, then one region per block
+  const int64_t flags_bytes = al(R * 4);
+  if (!g->share_scratch) {
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(kShareBlocksMax, kShareScratchBudget / off));
+    if (hipMalloc(&g->share_scratch, (size_t)(flags_bytes + blocks * off)) != hipSuccess) {
+      g->share_scratch = nullptr;
+      return SIM_E_NOMEM;
+    }
+    g->share_blocks = (int32_t)blocks;
+  }
+  // the flags travel in stream order as kernel arguments, so the caller's
+  // array is no longer read on return
+  int32_t *flags = (int32_t *)g->share_scratch;
+  if (int rc = launch_put_words(flags, share_words, (int32_t)R, stream)) return rc;
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const int64_t blocks = std::min<int64_t>(tiles, g->share_blocks);
+  a.n_scen = n_scen;
+  a.dur = dur;
+  a.ld_dur = ld_dur;
+  a.makespan = makespan;
+  a.finish = finish;
+  a.ld_fin = ld_fin;
+  a.status = status;
+  a.share = flags;
+  a.scratch = (char *)g->share_scratch + flags_bytes;
+  k_share<<<dim3((unsigned)blocks), dim3(kWave), 0, stream>>>(G, a);
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+}  // namespace mlsim

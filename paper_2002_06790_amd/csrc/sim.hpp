@@ -211,9 +211,21 @@ struct sim_graph {
   // each op by caller id)
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred, h_res;
   size_t scratch_bytes;
+  // bandwidth-sharing replay: its scratch (allocated on first use), the
+  // resource flags of the current call at its start, and its persistent grid
+  void *share_scratch = nullptr;
+  int32_t share_blocks = 0;
 };
 
 namespace mlsim {
+// bandwidth sharing (share.hip): service units per ns, most active ops per
+// resource, persistent grid limits
+constexpr uint64_t kShareUnit = SIM_SHARE_UNIT;
+constexpr int kShareMax = SIM_SHARE_MAX;
+constexpr int64_t kShareBlocksMax = 2048;
+constexpr int64_t kShareScratchBudget = (int64_t)8 << 30;
+int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur, const int32_t *share_words,
+                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 // launchers (kernels.hip)
 int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,

@@ -1,0 +1,140 @@
+"""GPU parity of the replay with bandwidth sharing (sim_run_batch_share).
+
+On a shared resource every ready op starts at once and the active ops divide
+its rate equally, in integer ns (see include/mlsim.h).  Every case calls the
+library through its C ABI and compares the integer outputs element by
+element with the oracle's sharing replay.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2002_06790_amd import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+# link resources of the workload configs (tiny: the shared link; ResNet:
+# the workers' links; Inception: the copy streams; BERT: up- and downlinks)
+LINKS = {1: [2], 2: list(range(8, 16)), 3: list(range(4, 8)), 4: list(range(16, 48))}
+
+
+@pytest.fixture(scope="module")
+def mlsim():
+    import paper_2002_06790_amd as m
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(m.LIB_PATH):
+        m.build()
+    return m
+
+
+def dev(a, dtype=torch.int32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dtype=dtype, device="cuda")
+
+
+def check(mlsim, ptr, idx, res, R, dur, share, prio=None):
+    g = mlsim.Graph(ptr, idx, res, R, prio=prio)
+    mk, fin, st = g.run_share(dev(dur), share, want_finish=True)
+    torch.cuda.synchronize()
+    omk, ofin, ost = oracle.run_batch_share(ptr, idx, res, R, dur, share=share, prio=prio)
+    st = st.cpu().numpy()
+    assert np.array_equal(st, ost), "status differs"
+    assert np.array_equal(mk.cpu().numpy(), omk), "makespan differs"
+    ok = ost == 0
+    assert np.array_equal(fin.cpu().numpy()[:, ok], ofin[:, ok]), "finish times differ"
+    g.close()
+    return omk, ost
+
+
+def test_hand_examples(mlsim):
+    g = mlsim.Graph(np.array([0, 0, 1, 1], np.int64), np.array([2], np.int32), np.array([0, 1, 0], np.int32), 2)
+    mk, fin, _ = g.run_share(dev(np.array([[10], [4], [2]])), [1, 0], want_finish=True)
+    torch.cuda.synchronize()
+    assert fin.cpu().numpy()[:, 0].tolist() == [12, 4, 8] and int(mk[0]) == 12
+    g.close()
+    # finishes on a shared resource come before ready ops at the same time
+    g = mlsim.Graph(np.array([0, 1, 1, 2, 2, 2], np.int64), np.array([3, 4], np.int32),
+                    np.array([0, 0, 1, 2, 2], np.int32), 3)
+    mk, fin, _ = g.run_share(dev(np.array([[2], [2], [4], [5], [5]])), [1, 0, 0], want_finish=True)
+    torch.cuda.synchronize()
+    assert fin.cpu().numpy()[:, 0].tolist() == [4, 4, 4, 9, 14]
+    g.close()
+
+
+def test_simultaneous_start_many_ops(mlsim):
+    """Up to the limit of active ops, ragged tiles, counts that do not divide the unit."""
+    rng = np.random.default_rng(61)
+    for k in (2, 16, 17, 25, 64, 65):
+        dur = rng.integers(1, 100_000, size=(k, 130)).astype(np.int32)
+        check(mlsim, np.zeros(k + 1, np.int64), np.zeros(0, np.int32), np.zeros(k, np.int32), 1, dur,
+              np.array([1], np.uint8))
+
+
+def test_random_graphs(mlsim):
+    """Shared and exclusive resources, priorities, duplicate edges, barriers."""
+    rng = np.random.default_rng(62)
+    for n, R, p in ((12, 2, 0.3), (60, 3, 0.1), (200, 6, 0.05), (150, 40, 0.05), (300, 4, 0.3)):
+        ptr, idx, res, prio = W.random_dag(n, R, p, rng, with_prio=True, dup_edges=True)
+        dur = W.random_durations(n, 97, 1, 5000, rng)
+        share = (rng.random(R) < 0.5).astype(np.uint8)
+        share[0] = 1
+        print(f"random n={n} R={R} shared={int(share.sum())}", flush=True)
+        check(mlsim, ptr, idx, res, R, dur, share, prio=prio)
+
+
+@pytest.mark.parametrize("k,S", [(1, 1024), (2, 200), (3, 333), (4, 200)])
+def test_workload_parity(mlsim, k, S):
+    w = W.make_config(k, n_scen=S if k != 1 else None)
+    dur = w.durations()
+    share = np.zeros(w.n_res, np.uint8)
+    share[LINKS[k]] = 1
+    print(f"share workload {w.name} S={dur.shape[1]}", flush=True)
+    omk, ost = check(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, share, prio=w.prio)
+    assert (ost == 0).all()
+
+
+def test_nothing_shared_is_the_plain_replay(mlsim):
+    w = W.make_config(4, n_scen=256)
+    dur = dev(w.durations())
+    g = mlsim.Graph.from_workload(w)
+    mk, fin, st = g.run(dur, want_finish=True, algo="event")
+    smk, sfin, sst = g.run_share(dur, np.zeros(w.n_res, np.uint8), want_finish=True)
+    torch.cuda.synchronize()
+    assert torch.equal(mk, smk) and torch.equal(fin, sfin) and torch.equal(st, sst)
+    g.close()
+
+
+def test_overflow_limit_and_bad_durations(mlsim):
+    k = 3
+    dur = np.full((k, 4), 2**30 + 1, np.int32)  # three shared ops: all end past INT32_MAX
+    dur[:, 1] = 7
+    dur[1, 2] = 0
+    omk, ost = check(mlsim, np.zeros(k + 1, np.int64), np.zeros(0, np.int32), np.zeros(k, np.int32), 1, dur,
+                     np.array([1], np.uint8))
+    assert ost.tolist() == [oracle.ST_OVERFLOW, 0, oracle.ST_BAD_DUR, oracle.ST_OVERFLOW]
+
+
+def test_bert_sampled_scenarios(mlsim):
+    """BERT with both link directions shared (up to 25 pushes at once on an
+    uplink) on 2048 scenarios; the oracle checks a sample."""
+    w = W.make_config(4, n_scen=2048)
+    dur = w.durations()
+    share = np.zeros(w.n_res, np.uint8)
+    share[LINKS[4]] = 1
+    g = mlsim.Graph.from_workload(w)
+    mk, fin, st = g.run_share(dev(dur), share, want_finish=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(6)
+    scen = np.unique(np.r_[0, w.n_scen - 1, rng.integers(0, w.n_scen, 14)])
+    sub = np.ascontiguousarray(dur[:, scen])
+    omk, ofin, ost = oracle.run_batch_share(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, share=share, prio=w.prio)
+    sel = torch.from_numpy(scen).cuda()
+    assert (ost == 0).all()
+    assert np.array_equal(mk[sel].cpu().numpy(), omk)
+    assert np.array_equal(st[sel].cpu().numpy(), ost)
+    assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
+    assert (st.cpu().numpy() == 0).all()
+    g.close()

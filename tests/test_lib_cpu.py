@@ -1,5 +1,6 @@
 """Host-side checks of the C ABI library that need no GPU."""
 import ctypes
+import math
 import os
 import re
 
@@ -114,3 +115,12 @@ def test_device_model_argument_errors_without_gpu(L):
                                0, None) == mlsim.SIM_E_INVAL
     assert L.sim_run_batch_dev(None, 1, None, 1, None, 0, None, None, None, None, 0, None, 0,
                                None) == mlsim.SIM_E_INVAL
+
+
+def test_share_argument_errors_without_gpu(L):
+    share = np.ones(4, np.uint8)
+    assert L.sim_run_batch_share(None, 1, None, 1, share.ctypes.data, None, None, 0, None, None) == mlsim.SIM_E_INVAL
+    hdr = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "mlsim.h")).read()
+    assert int(re.search(r"#define SIM_SHARE_MAX (\d+)", hdr).group(1)) == mlsim.SIM_SHARE_MAX
+    assert int(re.search(r"#define SIM_SHARE_UNIT (\d+)", hdr).group(1)) == mlsim.SIM_SHARE_UNIT
+    assert 4096 * math.lcm(*range(1, 17)) == mlsim.SIM_SHARE_UNIT < 2**32

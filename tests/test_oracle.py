@@ -8,6 +8,8 @@ shortest-path routine, and two independent brute-force replays (tests/brute.py).
 """
 import os
 
+import math
+
 import numpy as np
 import pytest
 import scipy.sparse
@@ -1077,8 +1079,9 @@ def test_share_hand_example(library=None):
 def test_share_simultaneous_start_closed_form(library=None):
     # k ops entering one shared link together leave in order of duration;
     # the i-th (ascending d) at sum_{j<i} d_j + (k - i) d_i (0-based i)
+    assert oracle.SHARE_UNIT == 4096 * math.lcm(*range(1, 17)) < 2**32
     rng = np.random.default_rng(41)
-    for k in (1, 2, 5, 16):
+    for k in (1, 2, 5, 16):  # every count 1..k divides the service unit: exact shares
         g = no_edges([0] * k)
         dur = rng.integers(1, 1000, size=(k, 8)).astype(np.int32)
         _, fin, st = run_share(g, dur, [1], library=library)
@@ -1090,6 +1093,20 @@ def test_share_simultaneous_start_closed_form(library=None):
             assert np.array_equal(np.sort(fin[:, s]), want)
             assert np.all(np.diff(fin[order, s]) >= 0)  # shorter never leaves later
             assert fin[:, s].max() == d.sum()  # the link never idles: work conserved
+    # above 16 some counts do not divide the unit: an op gets its share
+    # rounded down, and a finish is seen at the next whole ns while the
+    # others still share with it, so each op leaves no earlier than under
+    # exact sharing and a few ns later at most
+    for k in (17, 25, 64):
+        g = no_edges([0] * k)
+        dur = rng.integers(1, 1000, size=(k, 8)).astype(np.int32)
+        _, fin, st = run_share(g, dur, [1], library=library)
+        assert (st == 0).all()
+        for s in range(8):
+            d = np.sort(dur[:, s].astype(np.int64))
+            want = np.cumsum(np.r_[0, d[:-1]]) + (k - np.arange(k)) * d
+            got = np.sort(fin[:, s])
+            assert np.all(got >= want) and np.all(got <= want + k)
 
 
 def test_share_matches_tick_simulation(library=None):
@@ -1149,12 +1166,13 @@ def test_share_bounds(library=None):
 
 
 def test_share_limit_overflow_and_errors(library=None):
-    dur = np.full((17, 2), 5, np.int32)
+    m = oracle.SHARE_MAX
+    dur = np.full((m + 1, 2), 5, np.int32)
     dur[3, 1] = 0
-    mk, _, st = run_share(no_edges([0] * 17), dur, [1], library=library)
+    mk, _, st = run_share(no_edges([0] * (m + 1)), dur, [1], library=library)
     assert st[0] == oracle.ST_SHARE_LIMIT and mk[0] == -1 and st[1] == oracle.ST_BAD_DUR
-    mk, fin, st = run_share(no_edges([0] * 16), dur[:16, :1], [1], library=library)
-    assert st[0] == 0 and (fin[:, 0] == 80).all()
+    mk, fin, st = run_share(no_edges([0] * m), dur[:m, :1], [1], library=library)
+    assert st[0] == 0 and (fin[:, 0] == 5 * m).all()  # 64 divides the unit: exact shares
     big = np.full((2, 1), 2**30 + 1, np.int32)  # two shared ops of 2^30 + 1: both end at 2^31 + 2
     mk, _, st = run_share(no_edges([0, 0]), big, [1], library=library)
     assert st[0] == oracle.ST_OVERFLOW and mk[0] == -1

@@ -83,10 +83,10 @@ MUTANTS = [
      "      w->rfree[r] = J->delay ? f + J->delay[r] : f;\n      if (J->gap) w->nrun[r]++;"),
     ("gen-accepts-large-base", "if (b < 1 || b > ((int64_t)1 << 24)) return 0;", "if (b < 1) return 0;"),
     # bandwidth sharing
-    ("share-ignores-count", "if (L->k > 0) L->vt += (t - L->tl) * (ORC_SHARE_UNIT / L->k);",
-     "if (L->k > 0) L->vt += (t - L->tl) * ORC_SHARE_UNIT;"),
-    ("share-finish-one-ns-late", "return L->tl + (m - L->vt + per_ns - 1) / per_ns;",
-     "return L->tl + (m - L->vt + per_ns) / per_ns;"),
+    ("share-ignores-count", "L->vt += (uint64_t)(t - L->tl) * (ORC_SHARE_UNIT / (uint64_t)L->k);",
+     "L->vt += (uint64_t)(t - L->tl) * ORC_SHARE_UNIT;"),
+    ("share-finish-one-ns-late", "return L->tl + (int64_t)((m - L->vt + per_ns - 1) / per_ns);",
+     "return L->tl + (int64_t)((m - L->vt + per_ns) / per_ns);"),
     ("share-no-advance-on-arrival", "link_advance(L, w->ready[v]);\n        L->op[L->k] = v;",
      "L->op[L->k] = v;"),
     ("share-ops-before-finishes-on-ties", "lt <= w->ready[w->heap[0]]", "lt < w->ready[w->heap[0]]"),
