@@ -9,7 +9,8 @@ step it also times the static-order replay (every resource running its ops
 in the order the event replay ran them in scenario 0), the bottleneck
 attribution, the replay and critical path on durations generated inside the
 kernels (knob table x counter-based noise), the replay with a gap per
-resource, the replay with gaps and output delays, the sweep variant on a slice of the scenarios and, on a bounded
+resource, the replay with gaps and output delays, the sweep variant and the
+replay with bandwidth sharing on the links on a slice of the scenarios and, on a bounded
 sample, the CPU
 oracle, whose outputs check sampled GPU results.
 
@@ -225,6 +226,27 @@ def main():
     torch.cuda.synchronize()
     sweep_equal = bool(torch.equal(swmk, evmk))
     log(f"sweep variant {sweep_ms:.1f} ms on {sw_n} scenarios, equal to the event replay: {sweep_equal}")
+    # bandwidth sharing on the workload's links (outside the step), on the
+    # same slice: every transfer ready on a link starts at once and the
+    # active ones divide its rate
+    share_ms, share_ok = None, None
+    links = workloads.link_resources(w)
+    if place is None and links.size:
+        share = np.zeros(w.n_res, np.uint8)
+        share[links] = 1
+        g.run_share(sw_dur, share)
+        torch.cuda.synchronize()
+        sh_ms = []
+        for _ in range(max(1, min(args.steps, 3))):
+            e0.record()
+            shmk, _, shst = g.run_share(sw_dur, share)
+            e1.record()
+            e1.synchronize()
+            sh_ms.append(e0.elapsed_time(e1))
+        share_ms = float(np.mean(sh_ms))
+        share_ok = int((shst == 0).sum())
+        log(f"bandwidth sharing on {links.size} links: {share_ms:.1f} ms on {sw_n} scenarios "
+            f"({share_ok} without a status bit)")
     # the step's outputs again (the static replay reused the buffers)
     step()
     torch.cuda.synchronize()
@@ -325,7 +347,9 @@ def main():
                     "device_model_run_op_events_per_s": op_events / (float(np.mean(dev_ms)) / 1e3),
                     "sweep_ms": sweep_ms, "sweep_scenarios": sw_n,
                     "sweep_op_events_per_s": n * sw_n / (sweep_ms / 1e3),
-                    "sweep_equals_event": sweep_equal},
+                    "sweep_equals_event": sweep_equal,
+                    "share_ms": share_ms, "share_scenarios": sw_n if share_ms else None,
+                    "share_op_events_per_s": n * sw_n / (share_ms / 1e3) if share_ms else None},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",

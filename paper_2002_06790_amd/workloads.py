@@ -683,6 +683,23 @@ CONFIGS = {
 }
 
 
+def link_resources(w: Workload) -> np.ndarray:
+    """Resources of ``w`` that carry transfers (candidates for bandwidth
+    sharing): the tiny model's shared link, the workers' links of the
+    parameter-server graphs, the copy streams of the ring graph; none for
+    the random layered graph."""
+    name, info = w.name, w.info
+    if name.startswith("tiny-dp-mlp"):
+        return np.array([2])
+    if name.startswith("resnet50-ps"):
+        return np.arange(info["workers"], 2 * info["workers"])
+    if name.startswith("inception-v3-ring"):
+        return np.arange(info["devices"], 2 * info["devices"])
+    if name.startswith("bert-large-ps"):
+        return np.arange(info["workers"], 3 * info["workers"])
+    return np.zeros(0, np.int64)
+
+
 def make_config(k: int, n_scen: Optional[int] = None) -> Workload:
     """Workload k (1..5) at its full scenario count, or at ``n_scen``."""
     fn = CONFIGS[k]

@@ -16,10 +16,6 @@ from paper_2002_06790_amd import workloads as W
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-# link resources of the workload configs (tiny: the shared link; ResNet:
-# the workers' links; Inception: the copy streams; BERT: up- and downlinks)
-LINKS = {1: [2], 2: list(range(8, 16)), 3: list(range(4, 8)), 4: list(range(16, 48))}
-
 
 @pytest.fixture(scope="module")
 def mlsim():
@@ -90,7 +86,7 @@ def test_workload_parity(mlsim, k, S):
     w = W.make_config(k, n_scen=S if k != 1 else None)
     dur = w.durations()
     share = np.zeros(w.n_res, np.uint8)
-    share[LINKS[k]] = 1
+    share[W.link_resources(w)] = 1
     print(f"share workload {w.name} S={dur.shape[1]}", flush=True)
     omk, ost = check(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, share, prio=w.prio)
     assert (ost == 0).all()
@@ -123,7 +119,7 @@ def test_bert_sampled_scenarios(mlsim):
     w = W.make_config(4, n_scen=2048)
     dur = w.durations()
     share = np.zeros(w.n_res, np.uint8)
-    share[LINKS[4]] = 1
+    share[W.link_resources(w)] = 1
     g = mlsim.Graph.from_workload(w)
     mk, fin, st = g.run_share(dev(dur), share, want_finish=True)
     torch.cuda.synchronize()

@@ -71,3 +71,15 @@ def test_bert_knob_headroom():
     mk, _, st = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, want_finish=False)
     assert (st == 0).all()
     assert mk.max() < 2**31 // 3
+
+
+def test_link_resources_carry_transfers_only():
+    """The resources offered for bandwidth sharing exist, are distinct and
+    run ops; every workload keeps some compute resource outside them."""
+    for k in (1, 2, 3, 4, 5):
+        w = W.make_config(k, n_scen=64)
+        links = W.link_resources(w)
+        assert np.all((links >= 0) & (links < w.n_res)) and np.unique(links).size == links.size
+        used = np.bincount(w.op_res, minlength=w.n_res)
+        assert np.all(used[links] > 0)
+        assert links.size < w.n_res  # some resource computes
