@@ -20,9 +20,10 @@
 // op, so one key order gives all the tie rules above.  The next finish of a
 // shared resource changes when an op arrives; every change pushes a new key
 // and a popped key is used only if it still equals the resource's current
-// next finish (older keys are skipped).  All per-lane state is lane-major
-// ([index][64]), so the lanes of a wave touch consecutive words for equal
-// indexes.
+// next finish (older keys are skipped).  The heap's top positions live in
+// LDS, the rest and all other per-lane state in global scratch,
+// lane-major ([index][64]), so the lanes of a wave touch consecutive words
+// for equal indexes.
 #include <algorithm>
 
 #include "sim.hpp"
@@ -33,6 +34,8 @@ namespace {
 
 constexpr uint32_t kI32Max = 0x7fffffffu;
 constexpr uint32_t kNoTime = 0xffffffffu;
+constexpr int64_t kShareHeapLds = 119;   // heap positions per lane in LDS: 59.5 KB per wavefront
+constexpr int64_t kShareFlagsLds = 1024; // resource flags in LDS (4 KB) up to this many resources
 
 struct ShArgs {
   int64_t n_scen;
@@ -46,7 +49,10 @@ struct ShArgs {
   char *scratch;         // per block: the regions below, lane-major
   int64_t block_bytes;
   int64_t heap_cap;      // heap entries per lane
-  int64_t o_rd, o_cnt, o_rf, o_vt, o_tl, o_k, o_nd, o_need, o_op;  // byte offsets in a block's region
+  int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
+  int flags_lds;         // the resource flags are copied to LDS after the heap
+  int rows_identity;     // compact ids equal the caller's op ids (duration rows)
+  int64_t o_rc, o_rf, o_vt, o_tl, o_k, o_nd, o_need, o_op;  // byte offsets in a block's region
 };
 
 template <class T>
@@ -56,12 +62,28 @@ struct Lane {  // element i of a lane-major array
 };
 
 __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
+  extern __shared__ uint64_t lds_heap[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R, N = G.n + G.nb;
   char *blk = a.scratch + (int64_t)blockIdx.x * a.block_bytes;
-  const Lane<uint64_t> heap{(uint64_t *)blk + lane};
-  const Lane<uint32_t> rd{(uint32_t *)(blk + a.o_rd) + lane};
-  const Lane<int32_t> cnt{(int32_t *)(blk + a.o_cnt) + lane};
+  const Lane<uint64_t> heap_g{(uint64_t *)blk + lane};
+  // heap position i: in LDS below heap_lds, else in global scratch
+  const int64_t HL = a.heap_lds;
+  auto hget = [&](int64_t i) -> uint64_t { return i < HL ? lds_heap[i * kWave + lane] : heap_g[i]; };
+  auto hset = [&](int64_t i, uint64_t v) {
+    if (i < HL)
+      lds_heap[i * kWave + lane] = v;
+    else
+      heap_g[i] = v;
+  };
+  int32_t *flags_l = (int32_t *)(lds_heap + HL * kWave);
+  if (a.flags_lds) {
+    for (int r = lane; r < R; r += kWave) flags_l[r] = a.share[r];
+    __syncthreads();
+  }
+  const int32_t *flags = a.flags_lds ? flags_l : a.share;
+  // per node: ready time (high word) and predecessors not yet finished
+  const Lane<uint64_t> rc{(uint64_t *)(blk + a.o_rc) + lane};
   const Lane<uint32_t> rf{(uint32_t *)(blk + a.o_rf) + lane};
   const Lane<uint64_t> vt{(uint64_t *)(blk + a.o_vt) + lane};
   const Lane<uint32_t> tl{(uint32_t *)(blk + a.o_tl) + lane};
@@ -78,10 +100,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       if (a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s] < 1) st |= SIM_ST_BAD_DUR;
     uint32_t span = 0;
     if (!st) {
-      for (int x = 0; x < N; ++x) {
-        rd[x] = 0;
-        cnt[x] = G.wp_ptr[x + 1] - G.wp_ptr[x];
-      }
+      for (int x = 0; x < N; ++x) rc[x] = (uint64_t)(uint32_t)(G.wp_ptr[x + 1] - G.wp_ptr[x]);
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
         vt[r] = 0;
@@ -95,56 +114,60 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         int64_t i = hs++;
         while (i > 0) {
           const int64_t p = (i - 1) >> 1;
-          const uint64_t kp = heap[p];
+          const uint64_t kp = hget(p);
           if (kp <= key) break;
-          heap[i] = kp;
+          hset(i, kp);
           i = p;
         }
-        heap[i] = key;
+        hset(i, key);
         return true;
       };
       auto pop = [&]() -> uint64_t {
-        const uint64_t top = heap[0];
-        const uint64_t last = heap[--hs];
+        const uint64_t top = hget(0);
+        const uint64_t last = hget(--hs);
         int64_t i = 0;
         for (;;) {
           const int64_t l = 2 * i + 1;
           if (l >= hs) break;
           int64_t m = l;
-          uint64_t km = heap[l];
+          uint64_t km = hget(l);
           if (l + 1 < hs) {
-            const uint64_t kr = heap[l + 1];
+            const uint64_t kr = hget(l + 1);
             if (kr < km) {
               m = l + 1;
               km = kr;
             }
           }
           if (km >= last) break;
-          heap[i] = km;
+          hset(i, km);
           i = m;
         }
-        if (hs > 0) heap[i] = last;
+        if (hs > 0) hset(i, last);
         return top;
       };
       auto key_of = [](uint32_t t, uint32_t w) -> uint64_t { return ((uint64_t)t << 32) | w; };
       // a node's predecessor finished (outputs at time t): an op whose count
       // reaches zero is ready; a barrier passes its ready time to its members
       bool ok = true;
+      auto arrive = [&](int x, uint32_t t) -> uint64_t {  // new {ready, count} of node x
+        const uint64_t o = rc[x];
+        const uint32_t r0 = (uint32_t)(o >> 32);
+        const uint64_t nw = ((uint64_t)(r0 > t ? r0 : t) << 32) | (uint32_t)((uint32_t)o - 1u);
+        rc[x] = nw;
+        return nw;
+      };
       auto release = [&](int x, uint32_t t) {
-        const uint32_t v = rd[x] > t ? rd[x] : t;
-        rd[x] = v;
-        const int left = cnt[x] - 1;
-        cnt[x] = left;
-        if (left != 0) return;
+        const uint64_t nw = arrive(x, t);
+        if ((uint32_t)nw != 0) return;
+        const uint32_t v = (uint32_t)(nw >> 32);
         if (x < n) {
           ok = ok && push(key_of(v, (uint32_t)(R + x)));
           return;
         }
-        for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {
+        for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {  // a barrier's members
           const int y = G.ws[e];
-          rd[y] = rd[y] > v ? rd[y] : v;
-          cnt[y] = cnt[y] - 1;
-          if (cnt[y] == 0) ok = ok && push(key_of(rd[y], (uint32_t)(R + y)));
+          const uint64_t ny = arrive(y, v);
+          if ((uint32_t)ny == 0) ok = ok && push(key_of((uint32_t)(ny >> 32), (uint32_t)(R + y)));
         }
       };
       auto advance = [&](int r, uint32_t t) {
@@ -212,9 +235,14 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           continue;
         }
         const int c = (int)(w - (uint32_t)R);
-        const int r = G.ops[c].res;
-        const int32_t d = a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s];
-        if (a.share[r]) {  // joins the resource's active ops at its ready time
+        // the op's row and resource, its successor range and (identity
+        // rows) its duration, all requested before the first is used
+        const int2 orr = *(const int2 *)&G.ops[c];
+        const int e0 = G.ws_ptr[c], e1 = G.ws_ptr[c + 1];
+        int32_t d = a.rows_identity ? a.dur[(int64_t)c * a.ld_dur + s] : 0;
+        const int row = orr.x, r = orr.y;
+        if (!a.rows_identity) d = a.dur[(int64_t)row * a.ld_dur + s];
+        if (flags[r]) {  // joins the resource's active ops at its ready time
           const int k = kk[r];
           if (k == kShareMax) {
             st |= SIM_ST_SHARE_LIMIT;
@@ -237,8 +265,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         }
         rf[r] = f;
         span = f > span ? f : span;
-        if (a.finish) a.finish[(int64_t)G.ops[c].orig * a.ld_fin + s] = (int32_t)f;
-        for (int e = G.ws_ptr[c]; e < G.ws_ptr[c + 1]; ++e) release(G.ws[e], f);
+        if (a.finish) a.finish[(int64_t)row * a.ld_fin + s] = (int32_t)f;
+        for (int e = e0; e < e1; ++e) release(G.ws[e], f);
       }
       if (!ok) st |= SIM_ST_INTERNAL;
     }
@@ -258,10 +286,8 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   ShArgs a{};
   int64_t off = 0;
   off += al(cap * 8 * kWave);
-  a.o_rd = off;
-  off += al(N * 4 * kWave);
-  a.o_cnt = off;
-  off += al(N * 4 * kWave);
+  a.o_rc = off;
+  off += al(N * 8 * kWave);
   a.o_rf = off;
   off += al(R * 4 * kWave);
   a.o_vt = off;
@@ -278,6 +304,11 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   off += al(R * kShareMax * 4 * kWave);
   a.block_bytes = off;
   a.heap_cap = cap;
+  // LDS: the heap's top levels, then the resource flags when they are few
+  a.flags_lds = R <= kShareFlagsLds;
+  a.heap_lds = (int)std::min<int64_t>(cap, kShareHeapLds);
+  a.rows_identity = g->row_identity;
+  const size_t lds = (size_t)a.heap_lds * 8 * kWave + (a.flags_lds ? (size_t)R * 4 : 0);
   // a persistent grid within the scratch budget, allocated on first use:
   // the resource flags, then one region per block
   const int64_t flags_bytes = al(R * 4);
@@ -304,7 +335,7 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   a.status = status;
   a.share = flags;
   a.scratch = (char *)g->share_scratch + flags_bytes;
-  k_share<<<dim3((unsigned)blocks), dim3(kWave), 0, stream>>>(G, a);
+  k_share<<<dim3((unsigned)blocks), dim3(kWave), lds, stream>>>(G, a);
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 

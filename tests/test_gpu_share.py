@@ -134,3 +134,25 @@ def test_bert_sampled_scenarios(mlsim):
     assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
     assert (st.cpu().numpy() == 0).all()
     g.close()
+
+
+def test_deep_event_heap(mlsim):
+    """A thousand ops ready at once: the event heap reaches far below its
+    levels kept in LDS."""
+    rng = np.random.default_rng(63)
+    n, R = 1000, 40
+    res = (np.arange(n) % R).astype(np.int32)
+    ptr = np.zeros(n + 1, np.int64)
+    dur = rng.integers(1, 10_000, size=(n, 70)).astype(np.int32)
+    share = np.zeros(R, np.uint8)
+    share[::2] = 1
+    omk, ost = check(mlsim, ptr, np.zeros(0, np.int32), res, R, dur, share)
+    assert (ost == 0).all()
+    # and with dependencies: 10 layers of 100, each op after two of the layer before
+    succ = [[] for _ in range(n)]
+    for v in range(100, n):
+        for u in rng.choice(np.arange(v - v % 100 - 100, v - v % 100), 2, replace=False):
+            succ[u].append(v)
+    ptr = np.r_[0, np.cumsum([len(x) for x in succ])].astype(np.int64)
+    idx = np.array([v for x in succ for v in x], np.int32)
+    check(mlsim, ptr, idx, res, R, dur, share, prio=rng.integers(-3, 4, size=n).astype(np.int32))
