@@ -52,7 +52,7 @@ struct ShArgs {
   int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
   int flags_lds;         // the resource flags are copied to LDS after the heap
   int rows_identity;     // compact ids equal the caller's op ids (duration rows)
-  int64_t o_rc, o_rf, o_vt, o_tl, o_k, o_nd, o_need, o_op;  // byte offsets in a block's region
+  int64_t o_rc, o_rf, o_vt, o_tl, o_k, o_nd, o_mn, o_need, o_op;  // byte offsets in a block's region
 };
 
 template <class T>
@@ -89,6 +89,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   const Lane<uint32_t> tl{(uint32_t *)(blk + a.o_tl) + lane};
   const Lane<int32_t> kk{(int32_t *)(blk + a.o_k) + lane};
   const Lane<uint32_t> nd{(uint32_t *)(blk + a.o_nd) + lane};
+  const Lane<uint64_t> mn{(uint64_t *)(blk + a.o_mn) + lane};  // least need of the active ops
   const Lane<uint64_t> need{(uint64_t *)(blk + a.o_need) + lane};  // [R][kShareMax]
   const Lane<int32_t> eop{(int32_t *)(blk + a.o_op) + lane};     // [R][kShareMax]
 
@@ -175,15 +176,10 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         if (k > 0) vt[r] = vt[r] + (uint64_t)(t - tl[r]) * (kShareUnit / (uint64_t)k);
         tl[r] = t;
       };
-      // the first integer ns at which the resource's next op is done (k > 0),
-      // saturated at 2^31 (a finish there overflows)
-      auto next_finish = [&](int r) -> uint32_t {
-        const int k = kk[r];
-        uint64_t m = need[(int64_t)r * kShareMax];
-        for (int i = 1; i < k; ++i) {
-          const uint64_t x = need[(int64_t)r * kShareMax + i];
-          m = x < m ? x : m;
-        }
+      // the first integer ns at which the resource's next op (the one that
+      // needs m units) is done, k > 0 ops active; saturated at 2^31 (a finish
+      // there overflows)
+      auto finish_at = [&](int r, int k, uint64_t m) -> uint32_t {
         const uint64_t per_ns = kShareUnit / (uint64_t)k;
         const uint64_t dt = (m - vt[r] + per_ns - 1) / per_ns;
         const uint64_t t = (uint64_t)tl[r] + dt;
@@ -203,30 +199,51 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
             break;
           }
           advance(r, t);
-          int k = kk[r], gone = 0;
+          int k = kk[r];
           const uint64_t v_now = vt[r];
-          for (int i = 0; i < k;) {
-            const int64_t base = (int64_t)r * kShareMax;
-            if (need[base + i] <= v_now) {
-              const int c = eop[base + i];
-              need[base + i] = need[base + k - 1];
-              eop[base + i] = eop[base + k - 1];
-              --k;
-              ++gone;
-              if (a.finish) a.finish[(int64_t)G.ops[c].orig * a.ld_fin + s] = (int32_t)t;
-              span = t > span ? t : span;
-              for (int e = G.ws_ptr[c]; e < G.ws_ptr[c + 1]; ++e) release(G.ws[e], t);
-            } else {
-              ++i;
-            }
+          const int64_t base = (int64_t)r * kShareMax;
+          // which active ops have their units (bit i: entry i), and the
+          // least need of the others; eight entries requested at a time
+          // (entries from k on are in bounds and ignored)
+          uint64_t gone = 0, m_rest = ~0ull;
+          for (int i0 = 0; i0 < k; i0 += 8) {
+            uint64_t x[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = need[base + i0 + j];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              if (i0 + j < k) {
+                if (x[j] <= v_now)
+                  gone |= 1ull << (i0 + j);
+                else
+                  m_rest = x[j] < m_rest ? x[j] : m_rest;
+              }
           }
-          kk[r] = k;
           if (gone == 0) {  // cannot happen: the finish time was computed to complete an op
             ok = false;
             break;
           }
+          // remove them from the highest entry down, moving the last entry
+          // into each hole (entries above the hole are staying ones)
+          while (gone) {
+            const int i = 63 - __builtin_clzll(gone);
+            gone &= ~(1ull << i);
+            const int c = eop[base + i];
+            if (i != k - 1) {
+              need[base + i] = need[base + k - 1];
+              eop[base + i] = eop[base + k - 1];
+            }
+            --k;
+            const int2 orr = *(const int2 *)&G.ops[c];
+            if (a.finish) a.finish[(int64_t)orr.x * a.ld_fin + s] = (int32_t)t;
+            span = t > span ? t : span;
+            const int e1 = G.ws_ptr[c + 1];
+            for (int e = G.ws_ptr[c]; e < e1; ++e) release(G.ws[e], t);
+          }
+          kk[r] = k;
           if (k > 0) {
-            const uint32_t f = next_finish(r);
+            mn[r] = m_rest;
+            const uint32_t f = finish_at(r, k, m_rest);
             nd[r] = f;
             ok = ok && push(key_of(f, (uint32_t)r));
           } else {
@@ -249,10 +266,13 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
             break;
           }
           advance(r, t);
-          need[(int64_t)r * kShareMax + k] = vt[r] + (uint64_t)d * kShareUnit;
+          const uint64_t nv = vt[r] + (uint64_t)d * kShareUnit;
+          need[(int64_t)r * kShareMax + k] = nv;
           eop[(int64_t)r * kShareMax + k] = c;
           kk[r] = k + 1;
-          const uint32_t f = next_finish(r);
+          const uint64_t m = k == 0 || nv < mn[r] ? nv : mn[r];
+          mn[r] = m;
+          const uint32_t f = finish_at(r, k + 1, m);
           nd[r] = f;
           ok = ok && push(key_of(f, (uint32_t)r));
           continue;
@@ -298,6 +318,8 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   off += al(R * 4 * kWave);
   a.o_nd = off;
   off += al(R * 4 * kWave);
+  a.o_mn = off;
+  off += al(R * 8 * kWave);
   a.o_need = off;
   off += al(R * kShareMax * 8 * kWave);
   a.o_op = off;
