@@ -157,18 +157,37 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         rc[x] = nw;
         return nw;
       };
-      auto release = [&](int x, uint32_t t) {
-        const uint64_t nw = arrive(x, t);
-        if ((uint32_t)nw != 0) return;
-        const uint32_t v = (uint32_t)(nw >> 32);
-        if (x < n) {
-          ok = ok && push(key_of(v, (uint32_t)(R + x)));
-          return;
-        }
-        for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {  // a barrier's members
-          const int y = G.ws[e];
-          const uint64_t ny = arrive(y, v);
-          if ((uint32_t)ny == 0) ok = ok && push(key_of((uint32_t)(ny >> 32), (uint32_t)(R + y)));
+      // every successor of an op finished at t, four nodes at a time: their
+      // ids, then their {ready, count} words are requested together (the
+      // nodes of one list are distinct, and a barrier's members are never
+      // in another node's list, so the words are independent)
+      auto release_all = [&](int e0, int e1, uint32_t t) {
+        for (int eb = e0; eb < e1; eb += 4) {
+          int xs[4];
+          uint64_t os[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) xs[j] = eb + j < e1 ? G.ws[eb + j] : -1;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) os[j] = xs[j] >= 0 ? rc[xs[j]] : 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (xs[j] < 0) continue;
+            const int x = xs[j];
+            const uint32_t r0 = (uint32_t)(os[j] >> 32);
+            const uint32_t v = r0 > t ? r0 : t;
+            const uint32_t left = (uint32_t)os[j] - 1u;
+            rc[x] = ((uint64_t)v << 32) | left;
+            if (left != 0) continue;
+            if (x < n) {
+              ok = ok && push(key_of(v, (uint32_t)(R + x)));
+              continue;
+            }
+            for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {  // a barrier's members
+              const int y = G.ws[e];
+              const uint64_t ny = arrive(y, v);
+              if ((uint32_t)ny == 0) ok = ok && push(key_of((uint32_t)(ny >> 32), (uint32_t)(R + y)));
+            }
+          }
         }
       };
       auto advance = [&](int r, uint32_t t) {
@@ -237,8 +256,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
             const int2 orr = *(const int2 *)&G.ops[c];
             if (a.finish) a.finish[(int64_t)orr.x * a.ld_fin + s] = (int32_t)t;
             span = t > span ? t : span;
-            const int e1 = G.ws_ptr[c + 1];
-            for (int e = G.ws_ptr[c]; e < e1; ++e) release(G.ws[e], t);
+            release_all(G.ws_ptr[c], G.ws_ptr[c + 1], t);
           }
           kk[r] = k;
           if (k > 0) {
@@ -286,7 +304,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         rf[r] = f;
         span = f > span ? f : span;
         if (a.finish) a.finish[(int64_t)row * a.ld_fin + s] = (int32_t)f;
-        for (int e = e0; e < e1; ++e) release(G.ws[e], f);
+        release_all(e0, e1, f);
       }
       if (!ok) st |= SIM_ST_INTERNAL;
     }
