@@ -156,3 +156,30 @@ def test_deep_event_heap(mlsim):
     ptr = np.r_[0, np.cumsum([len(x) for x in succ])].astype(np.int64)
     idx = np.array([v for x in succ for v in x], np.int32)
     check(mlsim, ptr, idx, res, R, dur, share, prio=rng.integers(-3, 4, size=n).astype(np.int32))
+
+
+def test_bert_bench_launch_sampled(mlsim):
+    """The benchmark's launch: BERT with its 32 links shared on 65536
+    scenarios (a persistent grid taking two rounds of tiles); sampled
+    scenarios from both rounds against the oracle."""
+    w = W.make_config(4, n_scen=65536)
+    dur = w.durations()
+    share = np.zeros(w.n_res, np.uint8)
+    share[W.link_resources(w)] = 1
+    g = mlsim.Graph.from_workload(w)
+    d = dev(dur)
+    mk, fin, st = g.run_share(d, share, want_finish=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(7)
+    scen = np.unique(np.r_[0, 63, 64, w.n_scen - 1, rng.integers(0, w.n_scen, 12)])
+    sub = np.ascontiguousarray(dur[:, scen])
+    omk, ofin, ost = oracle.run_batch_share(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, share=share, prio=w.prio)
+    sel = torch.from_numpy(scen).cuda()
+    assert (ost == 0).all() and (st.cpu().numpy() == 0).all()
+    assert np.array_equal(mk[sel].cpu().numpy(), omk)
+    assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
+    # a second call on the same graph (scratch already allocated) gives the same result
+    mk2, _, _ = g.run_share(d, share)
+    torch.cuda.synchronize()
+    assert torch.equal(mk, mk2)
+    g.close()
