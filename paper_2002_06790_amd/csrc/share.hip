@@ -101,7 +101,12 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       if (a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s] < 1) st |= SIM_ST_BAD_DUR;
     uint32_t span = 0;
     if (!st) {
-      for (int x = 0; x < N; ++x) rc[x] = (uint64_t)(uint32_t)(G.wp_ptr[x + 1] - G.wp_ptr[x]);
+      // {ready 0, count} of every node with two or more predecessors (the
+      // others never read theirs)
+      for (int x = 0; x < N; ++x) {
+        const int np = G.wp_ptr[x + 1] - G.wp_ptr[x];
+        if (np > 1) rc[x] = (uint64_t)(uint32_t)np;
+      }
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
         vt[r] = 0;
@@ -147,46 +152,41 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         return top;
       };
       auto key_of = [](uint32_t t, uint32_t w) -> uint64_t { return ((uint64_t)t << 32) | w; };
-      // a node's predecessor finished (outputs at time t): an op whose count
-      // reaches zero is ready; a barrier passes its ready time to its members
       bool ok = true;
-      auto arrive = [&](int x, uint32_t t) -> uint64_t {  // new {ready, count} of node x
-        const uint64_t o = rc[x];
-        const uint32_t r0 = (uint32_t)(o >> 32);
-        const uint64_t nw = ((uint64_t)(r0 > t ? r0 : t) << 32) | (uint32_t)((uint32_t)o - 1u);
-        rc[x] = nw;
-        return nw;
-      };
       // every successor of an op finished at t, four nodes at a time: their
-      // ids, then their {ready, count} words are requested together (the
+      // ids and predecessor counts, then (nodes with two or more
+      // predecessors) their {ready, count} words are requested together (the
       // nodes of one list are distinct, and a barrier's members are never
-      // in another node's list, so the words are independent)
+      // in another node's list, so the words are independent).  A node with
+      // one predecessor is ready at t without touching its word.
       auto release_all = [&](int e0, int e1, uint32_t t) {
         for (int eb = e0; eb < e1; eb += 4) {
-          int xs[4];
+          int xs[4], np[4];
           uint64_t os[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) xs[j] = eb + j < e1 ? G.ws[eb + j] : -1;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) os[j] = xs[j] >= 0 ? rc[xs[j]] : 0;
+          for (int j = 0; j < 4; ++j) np[j] = xs[j] >= 0 ? G.wp_ptr[xs[j] + 1] - G.wp_ptr[xs[j]] : 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) os[j] = np[j] > 1 ? rc[xs[j]] : 0;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             if (xs[j] < 0) continue;
             const int x = xs[j];
-            const uint32_t r0 = (uint32_t)(os[j] >> 32);
-            const uint32_t v = r0 > t ? r0 : t;
-            const uint32_t left = (uint32_t)os[j] - 1u;
-            rc[x] = ((uint64_t)v << 32) | left;
-            if (left != 0) continue;
+            uint32_t v = t;
+            if (np[j] > 1) {
+              const uint32_t r0 = (uint32_t)(os[j] >> 32);
+              v = r0 > t ? r0 : t;
+              const uint32_t left = (uint32_t)os[j] - 1u;
+              rc[x] = ((uint64_t)v << 32) | left;
+              if (left != 0) continue;
+            }
             if (x < n) {
               ok = ok && push(key_of(v, (uint32_t)(R + x)));
               continue;
             }
-            for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) {  // a barrier's members
-              const int y = G.ws[e];
-              const uint64_t ny = arrive(y, v);
-              if ((uint32_t)ny == 0) ok = ok && push(key_of((uint32_t)(ny >> 32), (uint32_t)(R + y)));
-            }
+            // a barrier's members: the barrier is their only predecessor
+            for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) ok = ok && push(key_of(v, (uint32_t)(R + G.ws[e])));
           }
         }
       };
