@@ -52,7 +52,16 @@ struct ShArgs {
   int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
   int flags_lds;         // the resource flags are copied to LDS after the heap
   int rows_identity;     // compact ids equal the caller's op ids (duration rows)
-  int64_t o_rc, o_rf, o_vt, o_tl, o_k, o_nd, o_mn, o_need, o_op;  // byte offsets in a block's region
+  int64_t o_rc, o_rf, o_ln, o_need, o_op;  // byte offsets in a block's region
+};
+
+// one shared resource's state in one lane: service units per active op
+// since time 0 (vt, as of time tl), the least need of its active ops (mn),
+// its pending finish time (nd) and active count (k); read and written whole
+struct __attribute__((aligned(16))) LinkSt {
+  uint64_t vt, mn;
+  uint32_t tl, nd;
+  int32_t k, pad;
 };
 
 template <class T>
@@ -85,11 +94,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   // per node: ready time (high word) and predecessors not yet finished
   const Lane<uint64_t> rc{(uint64_t *)(blk + a.o_rc) + lane};
   const Lane<uint32_t> rf{(uint32_t *)(blk + a.o_rf) + lane};
-  const Lane<uint64_t> vt{(uint64_t *)(blk + a.o_vt) + lane};
-  const Lane<uint32_t> tl{(uint32_t *)(blk + a.o_tl) + lane};
-  const Lane<int32_t> kk{(int32_t *)(blk + a.o_k) + lane};
-  const Lane<uint32_t> nd{(uint32_t *)(blk + a.o_nd) + lane};
-  const Lane<uint64_t> mn{(uint64_t *)(blk + a.o_mn) + lane};  // least need of the active ops
+  const Lane<LinkSt> lk{(LinkSt *)(blk + a.o_ln) + lane};
   const Lane<uint64_t> need{(uint64_t *)(blk + a.o_need) + lane};  // [R][kShareMax]
   const Lane<int32_t> eop{(int32_t *)(blk + a.o_op) + lane};     // [R][kShareMax]
 
@@ -109,10 +114,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       }
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
-        vt[r] = 0;
-        tl[r] = 0;
-        kk[r] = 0;
-        nd[r] = kNoTime;
+        lk[r] = LinkSt{0, 0, 0, kNoTime, 0, 0};
       }
       int64_t hs = 0;
       auto push = [&](uint64_t key) -> bool {
@@ -190,18 +192,17 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           }
         }
       };
-      auto advance = [&](int r, uint32_t t) {
-        const int k = kk[r];
-        if (k > 0) vt[r] = vt[r] + (uint64_t)(t - tl[r]) * (kShareUnit / (uint64_t)k);
-        tl[r] = t;
+      auto advance = [](LinkSt &L, uint32_t t) {
+        if (L.k > 0) L.vt += (uint64_t)(t - L.tl) * (kShareUnit / (uint64_t)L.k);
+        L.tl = t;
       };
       // the first integer ns at which the resource's next op (the one that
       // needs m units) is done, k > 0 ops active; saturated at 2^31 (a finish
       // there overflows)
-      auto finish_at = [&](int r, int k, uint64_t m) -> uint32_t {
+      auto finish_at = [](const LinkSt &L, int k, uint64_t m) -> uint32_t {
         const uint64_t per_ns = kShareUnit / (uint64_t)k;
-        const uint64_t dt = (m - vt[r] + per_ns - 1) / per_ns;
-        const uint64_t t = (uint64_t)tl[r] + dt;
+        const uint64_t dt = (m - L.vt + per_ns - 1) / per_ns;
+        const uint64_t t = (uint64_t)L.tl + dt;
         return t > kI32Max ? kI32Max + 1u : (uint32_t)t;
       };
       for (int k = 0; k < G.nsrc; ++k) ok = ok && push(key_of(0, (uint32_t)(R + G.src[k])));
@@ -212,14 +213,15 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         const uint32_t t = (uint32_t)(key >> 32), w = (uint32_t)key;
         if (w < (uint32_t)R) {  // a pending finish on shared resource w
           const int r = (int)w;
-          if (kk[r] == 0 || nd[r] != t) continue;  // superseded
+          LinkSt L = lk[r];
+          if (L.k == 0 || L.nd != t) continue;  // superseded
           if (t > kI32Max) {
             st |= SIM_ST_OVERFLOW;
             break;
           }
-          advance(r, t);
-          int k = kk[r];
-          const uint64_t v_now = vt[r];
+          advance(L, t);
+          int k = L.k;
+          const uint64_t v_now = L.vt;
           const int64_t base = (int64_t)r * kShareMax;
           // which active ops have their units (bit i: entry i), and the
           // least need of the others; eight entries requested at a time
@@ -258,15 +260,15 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
             span = t > span ? t : span;
             release_all(G.ws_ptr[c], G.ws_ptr[c + 1], t);
           }
-          kk[r] = k;
+          L.k = k;
           if (k > 0) {
-            mn[r] = m_rest;
-            const uint32_t f = finish_at(r, k, m_rest);
-            nd[r] = f;
-            ok = ok && push(key_of(f, (uint32_t)r));
+            L.mn = m_rest;
+            L.nd = finish_at(L, k, m_rest);
+            ok = ok && push(key_of(L.nd, (uint32_t)r));
           } else {
-            nd[r] = kNoTime;
+            L.nd = kNoTime;
           }
+          lk[r] = L;
           continue;
         }
         const int c = (int)(w - (uint32_t)R);
@@ -278,21 +280,21 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         const int row = orr.x, r = orr.y;
         if (!a.rows_identity) d = a.dur[(int64_t)row * a.ld_dur + s];
         if (flags[r]) {  // joins the resource's active ops at its ready time
-          const int k = kk[r];
+          LinkSt L = lk[r];
+          const int k = L.k;
           if (k == kShareMax) {
             st |= SIM_ST_SHARE_LIMIT;
             break;
           }
-          advance(r, t);
-          const uint64_t nv = vt[r] + (uint64_t)d * kShareUnit;
+          advance(L, t);
+          const uint64_t nv = L.vt + (uint64_t)d * kShareUnit;
           need[(int64_t)r * kShareMax + k] = nv;
           eop[(int64_t)r * kShareMax + k] = c;
-          kk[r] = k + 1;
-          const uint64_t m = k == 0 || nv < mn[r] ? nv : mn[r];
-          mn[r] = m;
-          const uint32_t f = finish_at(r, k + 1, m);
-          nd[r] = f;
-          ok = ok && push(key_of(f, (uint32_t)r));
+          L.k = k + 1;
+          L.mn = k == 0 || nv < L.mn ? nv : L.mn;
+          L.nd = finish_at(L, k + 1, L.mn);
+          lk[r] = L;
+          ok = ok && push(key_of(L.nd, (uint32_t)r));
           continue;
         }
         const uint32_t start = t > rf[r] ? t : rf[r];
@@ -328,16 +330,8 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   off += al(N * 8 * kWave);
   a.o_rf = off;
   off += al(R * 4 * kWave);
-  a.o_vt = off;
-  off += al(R * 8 * kWave);
-  a.o_tl = off;
-  off += al(R * 4 * kWave);
-  a.o_k = off;
-  off += al(R * 4 * kWave);
-  a.o_nd = off;
-  off += al(R * 4 * kWave);
-  a.o_mn = off;
-  off += al(R * 8 * kWave);
+  a.o_ln = off;
+  off += al(R * (int64_t)sizeof(LinkSt) * kWave);
   a.o_need = off;
   off += al(R * kShareMax * 8 * kWave);
   a.o_op = off;
