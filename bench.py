@@ -226,12 +226,12 @@ def main():
     torch.cuda.synchronize()
     sweep_equal = bool(torch.equal(swmk, evmk))
     log(f"sweep variant {sweep_ms:.1f} ms on {sw_n} scenarios, equal to the event replay: {sweep_equal}")
-    # bandwidth sharing on the workload's links (outside the step), on a
-    # slice of up to 65536 scenarios (two wavefronts per CU): every transfer
-    # ready on a link starts at once and the active ones divide its rate
+    # bandwidth sharing on the workload's links (outside the step), on every
+    # scenario: each transfer ready on a link starts at once and the active
+    # ones divide its rate
     share_ms, share_ok = None, None
     links = workloads.link_resources(w)
-    sh_n = min(S, 65536)
+    sh_n = S
     if place is None and links.size:
         sh_dur = dur[:, :sh_n]
         share = np.zeros(w.n_res, np.uint8)

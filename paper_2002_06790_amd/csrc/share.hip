@@ -25,6 +25,7 @@
 // lane-major ([index][64]), so the lanes of a wave touch consecutive words
 // for equal indexes.
 #include <algorithm>
+#include <vector>
 
 #include "sim.hpp"
 
@@ -34,7 +35,7 @@ namespace {
 
 constexpr uint32_t kI32Max = 0x7fffffffu;
 constexpr uint32_t kNoTime = 0xffffffffu;
-constexpr int64_t kShareHeapLds = 119;   // heap positions per lane in LDS: 59.5 KB per wavefront
+constexpr int64_t kShareHeapLds = 72;    // heap positions per lane in LDS: 36 KB per wavefront (four per CU)
 constexpr int64_t kShareFlagsLds = 1024; // resource flags in LDS (4 KB) up to this many resources
 
 struct ShArgs {
@@ -52,6 +53,9 @@ struct ShArgs {
   int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
   int flags_lds;         // the resource flags are copied to LDS after the heap
   int rows_identity;     // compact ids equal the caller's op ids (duration rows)
+  const int32_t *slot_of;  // [n + barriers] ready/count word of a node with two or more predecessors, else -1
+  const int32_t *np_of;    // [n_slots] predecessors of each such node
+  int32_t n_slots;
   int64_t o_rc, o_rf, o_ln, o_need, o_op;  // byte offsets in a block's region
 };
 
@@ -73,7 +77,7 @@ struct Lane {  // element i of a lane-major array
 __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   extern __shared__ uint64_t lds_heap[];
   const int lane = threadIdx.x;
-  const int n = G.n, R = G.R, N = G.n + G.nb;
+  const int n = G.n, R = G.R;
   char *blk = a.scratch + (int64_t)blockIdx.x * a.block_bytes;
   const Lane<uint64_t> heap_g{(uint64_t *)blk + lane};
   // heap position i: in LDS below heap_lds, else in global scratch
@@ -91,7 +95,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
     __syncthreads();
   }
   const int32_t *flags = a.flags_lds ? flags_l : a.share;
-  // per node: ready time (high word) and predecessors not yet finished
+  // per node with two or more predecessors: ready time (high word) and
+  // predecessors not yet finished
   const Lane<uint64_t> rc{(uint64_t *)(blk + a.o_rc) + lane};
   const Lane<uint32_t> rf{(uint32_t *)(blk + a.o_rf) + lane};
   const Lane<LinkSt> lk{(LinkSt *)(blk + a.o_ln) + lane};
@@ -106,12 +111,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       if (a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s] < 1) st |= SIM_ST_BAD_DUR;
     uint32_t span = 0;
     if (!st) {
-      // {ready 0, count} of every node with two or more predecessors (the
-      // others never read theirs)
-      for (int x = 0; x < N; ++x) {
-        const int np = G.wp_ptr[x + 1] - G.wp_ptr[x];
-        if (np > 1) rc[x] = (uint64_t)(uint32_t)np;
-      }
+      // {ready 0, count} of every node with two or more predecessors
+      for (int j = 0; j < a.n_slots; ++j) rc[j] = (uint64_t)(uint32_t)a.np_of[j];
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
         lk[r] = LinkSt{0, 0, 0, kNoTime, 0, 0};
@@ -163,24 +164,24 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       // one predecessor is ready at t without touching its word.
       auto release_all = [&](int e0, int e1, uint32_t t) {
         for (int eb = e0; eb < e1; eb += 4) {
-          int xs[4], np[4];
+          int xs[4], sl[4];
           uint64_t os[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) xs[j] = eb + j < e1 ? G.ws[eb + j] : -1;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) np[j] = xs[j] >= 0 ? G.wp_ptr[xs[j] + 1] - G.wp_ptr[xs[j]] : 0;
+          for (int j = 0; j < 4; ++j) sl[j] = xs[j] >= 0 ? a.slot_of[xs[j]] : -1;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) os[j] = np[j] > 1 ? rc[xs[j]] : 0;
+          for (int j = 0; j < 4; ++j) os[j] = sl[j] >= 0 ? rc[sl[j]] : 0;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             if (xs[j] < 0) continue;
             const int x = xs[j];
             uint32_t v = t;
-            if (np[j] > 1) {
+            if (sl[j] >= 0) {
               const uint32_t r0 = (uint32_t)(os[j] >> 32);
               v = r0 > t ? r0 : t;
               const uint32_t left = (uint32_t)os[j] - 1u;
-              rc[x] = ((uint64_t)v << 32) | left;
+              rc[sl[j]] = ((uint64_t)v << 32) | left;
               if (left != 0) continue;
             }
             if (x < n) {
@@ -321,45 +322,78 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
                  int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
   const DevGraph &G = g->dg;
   const int64_t N = (int64_t)G.n + G.nb, R = G.R;
-  const int64_t cap = 3 * (int64_t)G.n + 1;  // ready ops (n) + two keys per op on a shared resource
   auto al = [](int64_t b) { return (b + 255) & ~(int64_t)255; };
+  // bytes of one block's region for a heap of cap entries per lane
+  auto block_bytes = [&](int64_t cap, int64_t slots, ShArgs *a) {
+    int64_t off = 0;
+    off += al(cap * 8 * kWave);
+    if (a) a->o_rc = off;
+    off += al(std::max<int64_t>(slots, 1) * 8 * kWave);
+    if (a) a->o_rf = off;
+    off += al(R * 4 * kWave);
+    if (a) a->o_ln = off;
+    off += al(R * (int64_t)sizeof(LinkSt) * kWave);
+    if (a) a->o_need = off;
+    off += al(R * kShareMax * 8 * kWave);
+    if (a) a->o_op = off;
+    off += al(R * kShareMax * 4 * kWave);
+    return off;
+  };
+  // first use: the word slots of nodes with two or more predecessors, and
+  // the scratch (resource flags, slot tables, then the block regions, sized
+  // for the largest heap any call can need within the budget)
+  if (!g->share_scratch) {
+    std::vector<int32_t> wp((size_t)N + 1);
+    if (hipMemcpy(wp.data(), G.wp_ptr, wp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess) return SIM_E_HIP;
+    std::vector<int32_t> slot((size_t)N, -1), np;
+    for (int64_t x = 0; x < N; ++x)
+      if (wp[x + 1] - wp[x] > 1) {
+        slot[x] = (int32_t)np.size();
+        np.push_back(wp[x + 1] - wp[x]);
+      }
+    const int64_t head = al(R * 4) + al(N * 4) + al(std::max<size_t>(np.size(), 1) * 4);
+    const int64_t worst = block_bytes(3 * (int64_t)G.n + 1, (int64_t)np.size(), nullptr);
+    const int64_t region = std::max(worst, std::min(kShareScratchBudget, kShareBlocksMax * worst));
+    if (hipMalloc(&g->share_scratch, (size_t)(head + region)) != hipSuccess) {
+      g->share_scratch = nullptr;
+      return SIM_E_NOMEM;
+    }
+    char *b = (char *)g->share_scratch;
+    if (hipMemcpy(b + al(R * 4), slot.data(), slot.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+        (!np.empty() && hipMemcpy(b + al(R * 4) + al(N * 4), np.data(), np.size() * 4, hipMemcpyHostToDevice) !=
+                            hipSuccess)) {
+      (void)hipFree(g->share_scratch);
+      g->share_scratch = nullptr;
+      return SIM_E_HIP;
+    }
+    g->share_head = head;
+    g->share_region = region;
+    g->share_slots = (int32_t)np.size();
+  }
+  // this call's heap: every ready op once, and two keys per op on a shared
+  // resource (its arrival and at most one departure batch)
+  int64_t m_sh = 0;
+  for (int32_t v = 0; v < g->n_ops; ++v) m_sh += share_words[g->h_res[v]] != 0;
+  const int64_t cap = (int64_t)G.n + 2 * m_sh + 1;
   ShArgs a{};
-  int64_t off = 0;
-  off += al(cap * 8 * kWave);
-  a.o_rc = off;
-  off += al(N * 8 * kWave);
-  a.o_rf = off;
-  off += al(R * 4 * kWave);
-  a.o_ln = off;
-  off += al(R * (int64_t)sizeof(LinkSt) * kWave);
-  a.o_need = off;
-  off += al(R * kShareMax * 8 * kWave);
-  a.o_op = off;
-  off += al(R * kShareMax * 4 * kWave);
-  a.block_bytes = off;
+  a.block_bytes = block_bytes(cap, g->share_slots, &a);
   a.heap_cap = cap;
-  // LDS: the heap's top levels, then the resource flags when they are few
+  // LDS: the heap's top positions, then the resource flags when they are few
   a.flags_lds = R <= kShareFlagsLds;
   a.heap_lds = (int)std::min<int64_t>(cap, kShareHeapLds);
   a.rows_identity = g->row_identity;
   const size_t lds = (size_t)a.heap_lds * 8 * kWave + (a.flags_lds ? (size_t)R * 4 : 0);
-  // a persistent grid within the scratch budget, allocated on first use:
-  // the resource flags, then one region per block
-  const int64_t flags_bytes = al(R * 4);
-  if (!g->share_scratch) {
-    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(kShareBlocksMax, kShareScratchBudget / off));
-    if (hipMalloc(&g->share_scratch, (size_t)(flags_bytes + blocks * off)) != hipSuccess) {
-      g->share_scratch = nullptr;
-      return SIM_E_NOMEM;
-    }
-    g->share_blocks = (int32_t)blocks;
-  }
   // the flags travel in stream order as kernel arguments, so the caller's
   // array is no longer read on return
-  int32_t *flags = (int32_t *)g->share_scratch;
+  char *b = (char *)g->share_scratch;
+  int32_t *flags = (int32_t *)b;
   if (int rc = launch_put_words(flags, share_words, (int32_t)R, stream)) return rc;
+  // a persistent grid: as many blocks as the region holds, balanced so the
+  // last round of tiles is not nearly empty
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
-  const int64_t blocks = std::min<int64_t>(tiles, g->share_blocks);
+  const int64_t fit = std::max<int64_t>(1, std::min<int64_t>(kShareBlocksMax, g->share_region / a.block_bytes));
+  const int64_t rounds = (tiles + fit - 1) / fit;
+  const int64_t blocks = std::min((tiles + rounds - 1) / rounds, fit);
   a.n_scen = n_scen;
   a.dur = dur;
   a.ld_dur = ld_dur;
@@ -368,7 +402,10 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   a.ld_fin = ld_fin;
   a.status = status;
   a.share = flags;
-  a.scratch = (char *)g->share_scratch + flags_bytes;
+  a.slot_of = (const int32_t *)(b + al(R * 4));
+  a.np_of = (const int32_t *)(b + al(R * 4) + al(N * 4));
+  a.n_slots = g->share_slots;
+  a.scratch = b + g->share_head;
   k_share<<<dim3((unsigned)blocks), dim3(kWave), lds, stream>>>(G, a);
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }

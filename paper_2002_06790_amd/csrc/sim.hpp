@@ -211,10 +211,12 @@ struct sim_graph {
   // each op by caller id)
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred, h_res;
   size_t scratch_bytes;
-  // bandwidth-sharing replay: its scratch (allocated on first use), the
-  // resource flags of the current call at its start, and its persistent grid
+  // bandwidth-sharing replay: its scratch (allocated on first use): the
+  // resource flags of the current call, the word slots of joining nodes,
+  // then the per-block regions of its persistent grid
   void *share_scratch = nullptr;
-  int32_t share_blocks = 0;
+  int64_t share_head = 0, share_region = 0;  // bytes of flags and slot tables; of block regions
+  int32_t share_slots = 0;                    // nodes with two or more predecessors
 };
 
 namespace mlsim {

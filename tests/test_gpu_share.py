@@ -159,10 +159,10 @@ def test_deep_event_heap(mlsim):
 
 
 def test_bert_bench_launch_sampled(mlsim):
-    """The benchmark's launch: BERT with its 32 links shared on 65536
-    scenarios (a persistent grid taking two rounds of tiles); sampled
-    scenarios from both rounds against the oracle."""
-    w = W.make_config(4, n_scen=65536)
+    """The benchmark's launch: BERT with its 32 links shared on all 262144
+    scenarios (a persistent grid taking several rounds of tiles); sampled
+    scenarios from the first and last rounds against the oracle."""
+    w = W.make_config(4)
     dur = w.durations()
     share = np.zeros(w.n_res, np.uint8)
     share[W.link_resources(w)] = 1
