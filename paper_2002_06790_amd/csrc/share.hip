@@ -20,10 +20,14 @@
 // op, so one key order gives all the tie rules above.  The next finish of a
 // shared resource changes when an op arrives; every change pushes a new key
 // and a popped key is used only if it still equals the resource's current
-// next finish (older keys are skipped).  The heap's top positions live in
-// LDS, the rest and all other per-lane state in global scratch,
-// lane-major ([index][64]), so the lanes of a wave touch consecutive words
-// for equal indexes.
+// next finish (older keys are skipped), so a call's heap holds at most one
+// key per ready op and two per op on a shared resource.  The heap's top 72
+// positions live in LDS (36 KB, four wavefronts per CU), the rest and all
+// other per-lane state in global scratch, lane-major ([index][64]): the
+// {ready time, count} word of each node with two or more predecessors (a
+// node with one predecessor is ready when it finishes and needs none), each
+// resource's free time, each shared resource's 32-byte state record and its
+// active ops.
 #include <algorithm>
 #include <vector>
 
