@@ -14,7 +14,7 @@
 // ready ops keep the (ready time, priority, id) order of the plain replay,
 // and other resources run their queues first in first out as there.
 //
-// Layout.  One scenario per lane.  A lane's event list is a binary heap in
+// Layout.  One scenario per lane.  A lane's event list is a 4-ary heap in
 // global scratch of 64-bit keys (time << 32 | word), word = resource for a
 // pending finish on a shared resource and n_res + compact id for a ready
 // op, so one key order gives all the tie rules above.  The next finish of a
@@ -122,11 +122,13 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         lk[r] = LinkSt{0, 0, 0, kNoTime, 0, 0};
       }
       int64_t hs = 0;
+      // a 4-ary heap: children of position i at 4i + 1 .. 4i + 4, whose keys
+      // are requested together
       auto push = [&](uint64_t key) -> bool {
         if (hs >= a.heap_cap) return false;
         int64_t i = hs++;
         while (i > 0) {
-          const int64_t p = (i - 1) >> 1;
+          const int64_t p = (i - 1) >> 2;
           const uint64_t kp = hget(p);
           if (kp <= key) break;
           hset(i, kp);
@@ -140,17 +142,19 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         const uint64_t last = hget(--hs);
         int64_t i = 0;
         for (;;) {
-          const int64_t l = 2 * i + 1;
+          const int64_t l = 4 * i + 1;
           if (l >= hs) break;
+          uint64_t kc[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) kc[q] = l + q < hs ? hget(l + q) : ~0ull;
           int64_t m = l;
-          uint64_t km = hget(l);
-          if (l + 1 < hs) {
-            const uint64_t kr = hget(l + 1);
-            if (kr < km) {
-              m = l + 1;
-              km = kr;
+          uint64_t km = kc[0];
+#pragma unroll
+          for (int q = 1; q < 4; ++q)
+            if (kc[q] < km) {
+              km = kc[q];
+              m = l + q;
             }
-          }
           if (km >= last) break;
           hset(i, km);
           i = m;
