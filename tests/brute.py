@@ -216,3 +216,75 @@ def all_path_lengths(n, succ_ptr, succ_idx, dur):
         for w in S[v]:
             stack.append((w, L + int(dur[w])))
     return best
+
+
+def tick_sim_share_units(n, n_res, succ_ptr, succ_idx, res, dur, share, unit, prio=None):
+    """One scenario with bandwidth sharing in whole service units, by 1-ns
+    time stepping: finish times (list).
+
+    A shared device delivers ``unit`` service units per ns.  Over each ns
+    its k active ops each receive ``unit // k`` units (the share rounded
+    down, so k ops that do not divide ``unit`` lose the remainder); an op of
+    duration d leaves at the first tick at which it holds d * unit units.
+    At a tick, every op that is done leaves (on shared and exclusive devices
+    alike) before the ops it releases are entered, in (priority, id) order,
+    and before idle exclusive devices start their queue heads; the newly
+    entered ops share the next ns.  Written with plain integers and no
+    event list, independently of the oracle's event-driven replay.
+    """
+    prio = list(range(n)) if prio is None else [int(x) for x in prio]
+    P = preds_of(n, succ_ptr, succ_idx)
+    S = [set() for _ in range(n)]
+    for v in range(n):
+        for u in P[v]:
+            S[u].add(v)
+    cnt = [len(P[v]) for v in range(n)]
+    queue = [deque() for _ in range(n_res)]
+    running = [None] * n_res
+    held = [dict() for _ in range(n_res)]  # shared devices: op -> units received
+    finish = [None] * n
+
+    def enter(ops):
+        for v in sorted(ops, key=lambda v: (prio[v], v)):
+            r = int(res[v])
+            if share[r]:
+                held[r][v] = 0
+            else:
+                queue[r].append(v)
+
+    enter([v for v in range(n) if cnt[v] == 0])
+    done, t = 0, 0
+    limit = int(np.sum(dur)) * 2 + n + 1
+    while done < n:
+        ended = []
+        for r in range(n_res):
+            if running[r] is not None and running[r][1] == t:
+                ended.append(running[r][0])
+                running[r] = None
+            for v in [v for v, got in held[r].items() if got >= int(dur[v]) * unit]:
+                del held[r][v]
+                finish[v] = t
+                ended.append(v)
+        newly = []
+        for v in ended:
+            done += 1
+            for w in S[v]:
+                cnt[w] -= 1
+                if cnt[w] == 0:
+                    newly.append(w)
+        enter(newly)
+        for r in range(n_res):
+            if running[r] is None and queue[r]:
+                v = queue[r].popleft()
+                finish[v] = t + int(dur[v])
+                running[r] = (v, finish[v])
+        for r in range(n_res):
+            k = len(held[r])
+            if k:
+                per_op = unit // k
+                for v in held[r]:
+                    held[r][v] += per_op
+        t += 1
+        if t > limit:
+            raise RuntimeError("tick simulation did not terminate")
+    return finish

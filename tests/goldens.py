@@ -43,4 +43,11 @@ def load(path):
 
 
 def all_goldens():
-    return [load(p) for p in sorted(glob.glob(os.path.join(GOLDEN_DIR, "*.txt")))]
+    """The worked examples of the plain replay (exclusive devices)."""
+    return [load(p) for p in sorted(glob.glob(os.path.join(GOLDEN_DIR, "example_*.txt")))]
+
+
+def share_goldens():
+    """The worked examples of the replay with bandwidth sharing (a "shared"
+    line gives each resource's flag)."""
+    return [load(p) for p in sorted(glob.glob(os.path.join(GOLDEN_DIR, "share_*.txt")))]

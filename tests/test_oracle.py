@@ -1124,6 +1124,76 @@ def test_share_matches_tick_simulation(library=None):
         assert mk[0] == max(tick)
 
 
+def test_share_worked_examples(library=None):
+    """Hand-derived schedules with 17 and 25 ops sharing one link, where the
+    count does not divide the service unit (tests/golden/share_*.txt)."""
+    for g in goldens.share_goldens():
+        ex = g["expect"]
+        mk, fin, st = run_share(g, g["dur"], np.array(ex["shared"], np.uint8), library=library)
+        assert st.tolist() == [0], g["name"]
+        assert fin[:, 0].tolist() == ex["finish"], g["name"]
+        assert mk.tolist() == ex["makespan"], g["name"]
+        tick = brute.tick_sim_share_units(g["n"], g["n_res"], g["succ_ptr"], g["succ_idx"], g["op_res"],
+                                          g["dur"][:, 0], ex["shared"], oracle.SHARE_UNIT, g["prio"])
+        assert tick == ex["finish"], g["name"]
+
+
+def test_share_floor_rule_matches_unit_tick_simulation(library=None):
+    """Above 16 active ops the share per ns is the service unit divided by
+    the count, rounded down: the oracle equals a 1-ns integer tick simulation
+    of that rule exactly, for counts that do not divide the unit (17, 19, 25,
+    61), for counts that do (63, 64), and on random graphs whose links reach
+    more than 16."""
+    U = oracle.SHARE_UNIT
+    rng = np.random.default_rng(45)
+    for k in (17, 19, 25, 61, 63, 64):
+        assert (k >= 63) == (U % k == 0)
+        g = no_edges([0] * k)
+        dur = rng.integers(1, 12, size=(k, 3)).astype(np.int32)
+        _, fin, st = run_share(g, dur, [1], library=library)
+        assert (st == 0).all()
+        for s in range(3):
+            tick = brute.tick_sim_share_units(k, 1, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, s], [1], U)
+            assert list(fin[:, s]) == tick, (k, s)
+        # staggered arrivals: op i becomes ready after a chain of i % 4 exclusive ops
+        n = k + 3
+        preds = [[] for _ in range(n)]
+        for i in range(k):
+            if i % 4:
+                preds[i].append(k + (i % 4) - 1)
+        preds[k + 1].append(k)
+        preds[k + 2].append(k + 1)
+        succ = [[] for _ in range(n)]
+        for v in range(n):
+            for u in preds[v]:
+                succ[u].append(v)
+        gg = dict(n=n, n_res=2, succ_ptr=np.r_[0, np.cumsum([len(x) for x in succ])].astype(np.int64),
+                  succ_idx=np.array([w for x in succ for w in x], np.int32),
+                  op_res=np.array([0] * k + [1] * 3, np.int32), prio=None)
+        dd = rng.integers(1, 9, size=(n, 2)).astype(np.int32)
+        _, fin, st = run_share(gg, dd, [1, 0], library=library)
+        assert (st == 0).all()
+        for s in range(2):
+            tick = brute.tick_sim_share_units(n, 2, gg["succ_ptr"], gg["succ_idx"], gg["op_res"], dd[:, s], [1, 0], U)
+            assert list(fin[:, s]) == tick, (k, s)
+    seen_big = 0
+    for trial in range(12):
+        n = int(rng.integers(30, 60))
+        g = rand_graph(rng, n, 2, 0.02, prio=trial % 2 == 0)
+        g["op_res"] = (rng.random(n) < 0.8).astype(np.int32) ^ 1  # about 80 % on shared device 0
+        dur = rng.integers(1, 6, size=(n, 1)).astype(np.int32)
+        share = np.array([1, 0], np.uint8)
+        mk, fin, st = run_share(g, dur, share, library=library)
+        assert st[0] == 0
+        tick = brute.tick_sim_share_units(n, 2, g["succ_ptr"], g["succ_idx"], g["op_res"], dur[:, 0], share, U,
+                                          g["prio"])
+        assert list(fin[:, 0]) == tick, trial
+        srcs = [v for v in range(n) if g["op_res"][v] == 0 and not any(
+            v in g["succ_idx"][g["succ_ptr"][u]:g["succ_ptr"][u + 1]] for u in range(n))]
+        seen_big += len(srcs) > 16
+    assert seen_big >= 6  # most trials start more than 16 ops at once on the link
+
+
 def test_share_off_or_without_overlap_is_the_plain_replay(library=None):
     rng = np.random.default_rng(43)
     g = rand_graph(rng, 40, 4, 0.1, prio=True)

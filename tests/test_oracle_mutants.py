@@ -96,6 +96,23 @@ MUTANTS = [
      "if (w->cnt[x]-- == g->indeg[x]) heap_push(g, w, x);"),
     ("share-overflow-wraps", "if (f > (int64_t)INT32_MAX) {", "if (0) {"),
     ("share-link-overflow-wraps", "if (lt > INT32_MAX) {", "if (0) {"),
+    # the per-ns share of k active ops rounded other than down (a tuple
+    # plants the same mistake at every listed site)
+    ("share-ceil", ("L->vt += (uint64_t)(t - L->tl) * (ORC_SHARE_UNIT / (uint64_t)L->k);",
+                    "const uint64_t per_ns = ORC_SHARE_UNIT / (uint64_t)L->k;"),
+     ("L->vt += (uint64_t)(t - L->tl) * ((ORC_SHARE_UNIT + (uint64_t)L->k - 1) / (uint64_t)L->k);",
+      "const uint64_t per_ns = (ORC_SHARE_UNIT + (uint64_t)L->k - 1) / (uint64_t)L->k;")),
+    ("share-nearest", ("L->vt += (uint64_t)(t - L->tl) * (ORC_SHARE_UNIT / (uint64_t)L->k);",
+                       "const uint64_t per_ns = ORC_SHARE_UNIT / (uint64_t)L->k;"),
+     ("L->vt += (uint64_t)(t - L->tl) * ((ORC_SHARE_UNIT + (uint64_t)L->k / 2) / (uint64_t)L->k);",
+      "const uint64_t per_ns = (ORC_SHARE_UNIT + (uint64_t)L->k / 2) / (uint64_t)L->k;")),
+    # (a share rounded up only where the next finish is predicted is not a
+    # mistake: the prediction is then early, nothing leaves at it, and the
+    # replay predicts again from there, reaching the same finish times)
+    ("share-ceil-in-advance-only", "L->vt += (uint64_t)(t - L->tl) * (ORC_SHARE_UNIT / (uint64_t)L->k);",
+     "L->vt += (uint64_t)(t - L->tl) * ((ORC_SHARE_UNIT + (uint64_t)L->k - 1) / (uint64_t)L->k);"),
+    ("share-exact-unit-need", "L->need[L->k] = L->vt + (uint64_t)d * ORC_SHARE_UNIT;",
+     "L->need[L->k] = L->vt + (uint64_t)d * (ORC_SHARE_UNIT / 17 * 17);"),
 ]
 
 
@@ -113,9 +130,12 @@ def pins():
 @pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
 def test_pins_catch_planted_mistake(tmp_path, name, orig, mut):
     src = open(SRC).read()
-    assert src.count(orig) == 1, f"mutation site of {name} not found"
+    sites = zip(orig, mut) if isinstance(orig, tuple) else [(orig, mut)]
+    for o, m in sites:
+        assert src.count(o) == 1, f"mutation site of {name} not found"
+        src = src.replace(o, m)
     path = tmp_path / "mutant.c"
-    path.write_text(src.replace(orig, mut))
+    path.write_text(src)
     so = tmp_path / "libmutant.so"
     subprocess.check_call(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-pthread",
                            "-I", os.path.dirname(SRC), str(path), "-o", str(so)])
