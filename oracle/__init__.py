@@ -22,13 +22,40 @@ ST_BAD_DUR, ST_BAD_RES, ST_OVERFLOW, ST_SHARE_LIMIT = 1, 2, 4, 8
 SHARE_MAX, SHARE_UNIT = 64, 2952069120
 
 
-def build() -> str:
-    """Compile ``oracle.c`` with gcc into ``liboracle.so`` (always rebuilds)."""
-    tmp = LIB + ".tmp"
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
+#: sanitizer flags of a checking build (address and undefined-behaviour
+#: sanitizers; any undefined behaviour aborts instead of printing and going on)
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all"]
+
+
+def build(sanitize: bool = False, out: Optional[str] = None) -> str:
+    """Compile ``oracle.c`` with gcc into ``liboracle.so`` (always rebuilds).
+
+    ``sanitize=True`` builds a checking copy with AddressSanitizer and
+    UndefinedBehaviorSanitizer instead (``out``, default
+    ``liboracle_san.so``); a process that loads it must have the sanitizer
+    runtimes preloaded (``sanitizer_env()``).
+    """
+    out = out or (os.path.join(HERE, "liboracle_san.so") if sanitize else LIB)
+    opt = SANITIZE_FLAGS if sanitize else ["-O2"]
+    tmp = out + ".tmp"
+    subprocess.check_call(["gcc", *opt, "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
                            "-pthread", os.path.join(HERE, "oracle.c"), "-o", tmp])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def sanitizer_env(path: str) -> dict:
+    """Environment for a child process whose oracle calls go to the
+    sanitized build at ``path`` (runtimes preloaded, errors fatal)."""
+    rt = [subprocess.check_output(["gcc", f"-print-file-name={name}"], text=True).strip()
+          for name in ("libasan.so", "libubsan.so")]
+    env = dict(os.environ)
+    env["LD_PRELOAD"] = ":".join(rt + ([env["LD_PRELOAD"]] if env.get("LD_PRELOAD") else []))
+    env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=1:halt_on_error=1"
+    env["UBSAN_OPTIONS"] = "halt_on_error=1:print_stacktrace=1"
+    env["ORACLE_LIB"] = path
+    return env
 
 
 _lib = None
@@ -37,6 +64,10 @@ _lib = None
 def lib(path: Optional[str] = None):
     """The loaded oracle library (``path`` loads another build of oracle.c)."""
     global _lib
+    if path is None and _lib is None and os.environ.get("ORACLE_LIB"):
+        path = os.environ["ORACLE_LIB"]  # a checking build (sanitizer_env)
+        _lib = lib(path)
+        return _lib
     if path is not None or _lib is None:
         if path is None and not os.path.exists(LIB):
             build()
