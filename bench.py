@@ -38,19 +38,108 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def cpu_threads():
+    """Host threads for the CPU oracle: every core this process may run on,
+    within the machine's CPU share when the environment states it."""
+    n = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    return min(n, int(share)) if share.isdigit() and int(share) > 0 else n
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def compare_all(makespan, status, cp_len, finish, omk, ost, ocp, ofin, cs, S):
+    """Every scenario of the oracle's sample: makespan, status, critical
+    path, and finish times (in column chunks)."""
+    mk = makespan[:cs].cpu().numpy()
+    st = status[:cs].cpu().numpy()
+    cp = cp_len[:cs].cpu().numpy()
+    bad = (mk != omk) | (st != ost) | (cp != ocp)
+    fin_bad = 0
+    for a in range(0, cs, 16384):
+        b = min(cs, a + 16384)
+        fb = (finish[:, a:b].cpu().numpy() != ofin[:, a:b]).any(axis=0)
+        fin_bad += int(fb.sum())
+        bad[a:b] |= fb
+    nbad = int(bad.sum())
+    return (f"{'bit-exact' if nbad == 0 else 'MISMATCH'} on {cs - nbad} of {cs} scenarios "
+            f"(makespan, status, critical path and every finish time; {fin_bad} with finish differences)")
+
+
+def config_line(k, args, torch, mlsim, workloads):
+    """One workload at its full size: the step's two kernels timed (median
+    of event pairs), every scenario compared with the oracle."""
+    import oracle
+    w = workloads.make_config(k)
+    n, S = w.n_ops, w.n_scen
+    log(f"per-config {w.name}: n={n} S={S}")
+    dur_h = w.durations()
+    place_h = w.placement()
+    dur = torch.from_numpy(dur_h).cuda()
+    place = None if place_h is None else torch.from_numpy(place_h.view(np.int16)).cuda().view(torch.uint16)
+    g = mlsim.Graph.from_workload(w)
+    mk = torch.empty(S, dtype=torch.int32, device="cuda")
+    st = torch.empty(S, dtype=torch.int32, device="cuda")
+    fin = torch.empty((n, S), dtype=torch.int32, device="cuda")
+    cp = torch.empty(S, dtype=torch.int32, device="cuda")
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    ev_ms, cp_ms = [], []
+    for i in range(args.warmup + args.steps):
+        e0.record()
+        g.run(dur, place=place, makespan=mk, finish=fin, status=st)
+        e1.record()
+        g.critical_path(dur, cp_len=cp)
+        e2.record()
+        e2.synchronize()
+        if i >= args.warmup:
+            ev_ms.append(e0.elapsed_time(e1))
+            cp_ms.append(e1.elapsed_time(e2))
+    threads = cpu_threads()
+    t = time.perf_counter()
+    omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h, place=place_h,
+                                      want_finish=True, n_threads=threads)
+    ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, n, dur_h, n_threads=threads)
+    cpu_s = time.perf_counter() - t
+    parity = compare_all(mk, st, cp, fin, omk, ost, ocp, ofin, S, S)
+    log(f"  {w.name}: run_batch {np.median(ev_ms):.3f} ms, critical path {np.median(cp_ms):.3f} ms; {parity}")
+    ev = float(np.median(ev_ms))
+    alg = n * S * (8 + (2 if place is not None else 0)) + S * 8
+    out = {"n_ops": n, "n_scen": S, "run_batch_ms": ev, "critical_path_ms": float(np.median(cp_ms)),
+           "step_ms": ev + float(np.median(cp_ms)),
+           "op_events_per_s": n * S / ((ev + float(np.median(cp_ms))) / 1e3),
+           "scenarios_per_s": S / ((ev + float(np.median(cp_ms))) / 1e3),
+           "run_batch_hbm_frac": alg / (ev / 1e3) / 1e9 / PEAK_HBM_GBS,
+           "cpu_oracle_op_events_per_s": n * S / cpu_s, "cpu_threads": threads, "parity": parity}
+    del g, dur, fin, place
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5")
     ap.add_argument("--scenarios", type=int, default=None)
-    ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep", "walk"))
+    ap.add_argument("--algo", default="event", choices=("auto", "event", "sweep"))
     ap.add_argument("--cpu-sample", type=int, default=262144,
                     help="scenarios of the same workload timed on the CPU oracle (0: skip)")
     ap.add_argument("--calib-mb", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the other workloads' lines (timing and parity at their full sizes)")
+    ap.add_argument("--one-thread-sample", type=int, default=2048,
+                    help="scenarios timed on one CPU thread (0: skip)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -125,7 +214,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    log(f"ms/step {ms_per_step:.3f} (run_batch {np.mean(ev_ms):.3f} ms, critical_path {np.mean(cp_ms):.3f} ms)")
+    log(f"ms/step {ms_per_step:.3f} (run_batch median {np.median(ev_ms):.3f} ms, "
+        f"critical_path median {np.median(cp_ms):.3f} ms)")
 
     # static-order replay (outside the step): every resource runs its ops in
     # the order the event replay ran them in scenario 0
@@ -141,7 +231,7 @@ def main():
         e1.record()
         e1.synchronize()
         sr_ms.append(e0.elapsed_time(e1))
-    log(f"static-order replay {np.mean(sr_ms):.3f} ms")
+    log(f"static-order replay {np.median(sr_ms):.3f} ms")
     sr.close()
     # bottleneck attribution (outside the step): the replay with each op's
     # predecessor on its resource, busy time and binding chain per resource
@@ -157,7 +247,7 @@ def main():
         e1.synchronize()
         at_ms.append(e0.elapsed_time(e1))
     del at
-    log(f"attribution {np.mean(at_ms):.3f} ms")
+    log(f"attribution {np.median(at_ms):.3f} ms")
     # on-device scenario generation (outside the step): the same hot path with
     # every duration computed in the kernels from the workload's knob table
     # and 1 % counter-based noise instead of read from HBM
@@ -179,7 +269,7 @@ def main():
         e2.synchronize()
         gev_ms.append(e0.elapsed_time(e1))
         gcp_ms.append(e1.elapsed_time(e2))
-    log(f"generated: run {np.mean(gev_ms):.3f} ms, critical path {np.mean(gcp_ms):.3f} ms")
+    log(f"generated: run {np.median(gev_ms):.3f} ms, critical path {np.median(gcp_ms):.3f} ms")
     # resource gaps (outside the step): 5 us between consecutive ops on the
     # first quarter of the resources, 2 us on the rest
     gaps = np.full(w.n_res, 2_000, np.int32)
@@ -195,7 +285,7 @@ def main():
         e1.record()
         e1.synchronize()
         gap_ms.append(e0.elapsed_time(e1))
-    log(f"replay with resource gaps {np.mean(gap_ms):.3f} ms")
+    log(f"replay with resource gaps {np.median(gap_ms):.3f} ms")
     # the device model (outside the step): the same gaps, and the outputs of
     # ops on the last three quarters of the resources arrive 10 us after
     # they finish
@@ -210,7 +300,7 @@ def main():
         e1.record()
         e1.synchronize()
         dev_ms.append(e0.elapsed_time(e1))
-    log(f"replay with gaps and output delays {np.mean(dev_ms):.3f} ms")
+    log(f"replay with gaps and output delays {np.median(dev_ms):.3f} ms")
     # the level-synchronous sweep variant (outside the step) on a bounded
     # slice of the scenarios: it re-sweeps the graph every round, so it is
     # the slow exact variant; its makespans must equal the event replay's
@@ -245,7 +335,7 @@ def main():
             e1.record()
             e1.synchronize()
             sh_ms.append(e0.elapsed_time(e1))
-        share_ms = float(np.mean(sh_ms))
+        share_ms = float(np.median(sh_ms))
         share_ok = int((shst == 0).sum())
         log(f"bandwidth sharing on {links.size} links: {share_ms:.1f} ms on {sh_n} scenarios "
             f"({share_ok} without a status bit)")
@@ -253,16 +343,16 @@ def main():
     step()
     torch.cuda.synchronize()
 
-    # CPU oracle baseline on a bounded sample of the same workload; its
-    # outputs also check sampled GPU results
+    # CPU oracle baseline on a bounded sample of the same workload (by
+    # default every scenario); its outputs check every GPU result
     cpu = None
     parity = None
     if args.cpu_sample:
         import oracle
         cs = min(args.cpu_sample, S)
-        threads = min(16, len(os.sched_getaffinity(0)))
-        sub = np.ascontiguousarray(dur_h[:, :cs])
-        psub = None if place_h is None else np.ascontiguousarray(place_h[:, :cs])
+        threads = cpu_threads()
+        sub = dur_h if cs == S else np.ascontiguousarray(dur_h[:, :cs])
+        psub = None if place_h is None else (place_h if cs == S else np.ascontiguousarray(place_h[:, :cs]))
         log(f"cpu oracle on {cs} scenarios, {threads} threads")
         t = time.perf_counter()
         omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, sub, place=psub,
@@ -271,17 +361,22 @@ def main():
         cpu_s = time.perf_counter() - t
         cpu = {"value": n * cs / cpu_s, "unit": "op-events/s", "cores": threads, "kind": "oracle",
                "sample": f"first {cs} of {S} scenarios (run_batch with finish times + critical_path), "
-                         f"{cpu_s:.2f} s"}
+                         f"{cpu_s:.2f} s on {threads} threads",
+               "cpu_model": cpu_model(), "affinity_cores": len(os.sched_getaffinity(0))}
         log(f"cpu oracle {cpu['value']:.3e} op-events/s")
+        if args.one_thread_sample:
+            c1 = min(args.one_thread_sample, cs)
+            t = time.perf_counter()
+            oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, np.ascontiguousarray(sub[:, :c1]),
+                             place=None if psub is None else np.ascontiguousarray(psub[:, :c1]),
+                             want_finish=True, n_threads=1)
+            oracle.critical_path(w.succ_ptr, w.succ_idx, n, np.ascontiguousarray(sub[:, :c1]), n_threads=1)
+            t1 = time.perf_counter() - t
+            cpu["value_1thread"] = n * c1 / t1
+            cpu["sample_1thread"] = f"first {c1} scenarios on 1 thread, {t1:.2f} s"
+            log(f"cpu oracle, 1 thread: {cpu['value_1thread']:.3e} op-events/s")
         if not args.no_check:
-            rng = np.random.default_rng(0)
-            scen = np.unique(np.r_[0, cs - 1, rng.integers(0, cs, 30)])
-            sel = torch.from_numpy(scen).cuda()
-            ok = (np.array_equal(makespan[sel].cpu().numpy(), omk[scen])
-                  and np.array_equal(finish[:, sel].cpu().numpy(), ofin[:, scen])
-                  and np.array_equal(status[sel].cpu().numpy(), ost[scen])
-                  and np.array_equal(cp_len[sel].cpu().numpy(), ocp[scen]))
-            parity = f"{'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
+            parity = compare_all(makespan, status, cp_len, finish, omk, ost, ocp, ofin, cs, S)
             log(parity)
         del ofin
         if not args.no_check:
@@ -299,6 +394,18 @@ def main():
             gp = f"generated {'bit-exact' if ok else 'MISMATCH'} on {scen.size} sampled scenarios"
             parity = f"{parity}; {gp}" if parity else gp
             log(gp)
+    has_place = place is not None
+    del g, dur, finish, place
+    torch.cuda.empty_cache()
+
+    # the other workloads at their full sizes: the same step, timed, and
+    # every scenario checked against the oracle
+    per_config = None
+    if not args.no_per_config:
+        per_config = {}
+        for k in (1, 2, 3, 4, 5):
+            if k != args.config:
+                per_config[workloads.make_config(k).name] = config_line(k, args, torch, mlsim, workloads)
 
     # HBM traffic measured by counters for this exact kernel source, if any
     traffic = None
@@ -313,8 +420,8 @@ def main():
         traffic = None
 
     op_events = n * S
-    ev_s = float(np.mean(ev_ms)) / 1e3
-    alg_bytes = op_events * (4 + 4 + (2 if place is not None else 0)) + S * 8
+    ev_s = float(np.median(ev_ms)) / 1e3
+    alg_bytes = op_events * (4 + 4 + (2 if has_place else 0)) + S * 8
     achieved = alg_bytes / ev_s / 1e9
     out = {
         "metric": "simulated op-events/sec and scenarios/sec at 1 GPU; % of HBM roofline",
@@ -333,20 +440,23 @@ def main():
                                f"{w.n_res} resources, {S} scenarios", "n_ops": n, "n_scen": S,
                    "algo": args.algo, "finish_times": True, "parallelism": "single GPU"},
         "scenarios_per_s": S / (ms_per_step / 1e3),
-        "kernels": {"run_batch_ms": float(np.mean(ev_ms)), "critical_path_ms": float(np.mean(cp_ms)),
+        "kernels": {"timing": f"median of {args.steps} HIP event pairs per kernel",
+                    "run_batch_ms": float(np.median(ev_ms)), "critical_path_ms": float(np.median(cp_ms)),
                     "run_batch_op_events_per_s": op_events / ev_s,
-                    "critical_path_op_events_per_s": op_events / (float(np.mean(cp_ms)) / 1e3),
-                    "static_replay_ms": float(np.mean(sr_ms)),
-                    "static_replay_op_events_per_s": op_events / (float(np.mean(sr_ms)) / 1e3),
-                    "attribution_ms": float(np.mean(at_ms)),
-                    "generated_run_ms": float(np.mean(gev_ms)),
-                    "generated_critical_path_ms": float(np.mean(gcp_ms)),
-                    "generated_run_op_events_per_s": op_events / (float(np.mean(gev_ms)) / 1e3),
-                    "generated_critical_path_op_events_per_s": op_events / (float(np.mean(gcp_ms)) / 1e3),
-                    "gap_run_ms": float(np.mean(gap_ms)),
-                    "gap_run_op_events_per_s": op_events / (float(np.mean(gap_ms)) / 1e3),
-                    "device_model_run_ms": float(np.mean(dev_ms)),
-                    "device_model_run_op_events_per_s": op_events / (float(np.mean(dev_ms)) / 1e3),
+                    "critical_path_op_events_per_s": op_events / (float(np.median(cp_ms)) / 1e3),
+                    "critical_path_hbm_frac": (op_events * 4 + S * 4) / (float(np.median(cp_ms)) / 1e3)
+                                              / 1e9 / PEAK_HBM_GBS,
+                    "static_replay_ms": float(np.median(sr_ms)),
+                    "static_replay_op_events_per_s": op_events / (float(np.median(sr_ms)) / 1e3),
+                    "attribution_ms": float(np.median(at_ms)),
+                    "generated_run_ms": float(np.median(gev_ms)),
+                    "generated_critical_path_ms": float(np.median(gcp_ms)),
+                    "generated_run_op_events_per_s": op_events / (float(np.median(gev_ms)) / 1e3),
+                    "generated_critical_path_op_events_per_s": op_events / (float(np.median(gcp_ms)) / 1e3),
+                    "gap_run_ms": float(np.median(gap_ms)),
+                    "gap_run_op_events_per_s": op_events / (float(np.median(gap_ms)) / 1e3),
+                    "device_model_run_ms": float(np.median(dev_ms)),
+                    "device_model_run_op_events_per_s": op_events / (float(np.median(dev_ms)) / 1e3),
                     "sweep_ms": sweep_ms, "sweep_scenarios": sw_n,
                     "sweep_op_events_per_s": n * sw_n / (sweep_ms / 1e3),
                     "sweep_equals_event": sweep_equal,
@@ -356,9 +466,12 @@ def main():
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
                      "kernel": "k_event (sim_run_batch)",
-                     "bytes_per_launch": alg_bytes},
+                     "bytes_per_launch": alg_bytes,
+                     "limiter": "latency of each lane's dependent divergent loads (the roofline is HBM; "
+                                "the kernel moves far less than HBM peak)"},
         "cpu_baseline": cpu,
         "parity": parity,
+        "per_config": per_config,
         "h2d_s": h2d_s,
     }
     print(json.dumps(out), flush=True)

@@ -28,6 +28,18 @@
  * (or managed) memory owned by the caller; "host" pointers are ordinary
  * memory.  Arrays of shape [n_ops][ld] are op-major: entry (v, s) is at
  * v * ld + s, so one op's values for consecutive scenarios are contiguous.
+ *
+ * Streams and graphs: a graph is read-only after creation, and calls on
+ * different streams may share it and overlap in time.  Each graph owns a
+ * few sets of scratch memory (allocated by sim_graph_create, never by a
+ * call); a call takes one set for its kernels and records an event after
+ * them, and a later call that takes the same set first makes its own stream
+ * wait for that event, so no two calls use one set at once (on devices with
+ * room for several sets, overlapping calls on different streams run
+ * concurrently; otherwise they run one after the other).  Calls made while
+ * their stream is being captured into a HIP graph use a set of their own
+ * and record no event; replays of such captured graphs must not overlap one
+ * another.
  * Streams are hipStream_t passed as void* (NULL = the null stream).
  */
 #ifndef MLSIM_H
@@ -70,15 +82,12 @@ enum {
 #define SIM_SHARE_MAX 64
 #define SIM_SHARE_UNIT 2952069120u
 
-/* sim_run_batch flags & 3: which exact algorithm computes the replay */
+/* sim_run_batch flags & 3: which exact algorithm computes the replay (3 is
+ * not a valid value) */
 enum {
   SIM_ALGO_AUTO = 0,  /* library's choice (currently EVENT) */
   SIM_ALGO_EVENT = 1, /* event-driven list scheduling, one scenario per lane */
-  SIM_ALGO_SWEEP = 2, /* level-synchronous conservative sweeps */
-  SIM_ALGO_WALK = 3   /* lockstep walk along a pilot scenario's event order, each
-                         scenario checked for exactness and replayed with EVENT
-                         when the check fails; needs place == NULL and a graph
-                         within the walk's size limits, else EVENT runs */
+  SIM_ALGO_SWEEP = 2  /* level-synchronous conservative sweeps */
 };
 
 /* limits */
@@ -127,8 +136,7 @@ void sim_graph_destroy(sim_graph *g);
  *   stream   hipStream_t (void*), NULL for the null stream.
  * Asynchronous on `stream`.  Argument errors return synchronously before
  * anything is enqueued.  No memory is allocated.  Calls on different streams
- * that share one graph must not overlap in time (they share its scratch
- * memory); calls on one stream are ordered.
+ * that share one graph may overlap (see "Streams and graphs" above).
  */
 int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                   const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
@@ -149,8 +157,7 @@ int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_
  * Other arguments and outputs as sim_run_batch (placement allowed; a finish
  * time above INT32_MAX sets SIM_ST_OVERFLOW); flags: SIM_ALGO_AUTO or
  * SIM_ALGO_EVENT (others return SIM_E_INVAL).  With every gap 0 the result
- * equals sim_run_batch.  Asynchronous on `stream`; no memory is allocated;
- * calls on different streams sharing one graph must not overlap in time.
+ * equals sim_run_batch.  Asynchronous on `stream`; no memory is allocated.
  */
 int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, const int32_t *gap,
@@ -174,8 +181,7 @@ int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
  *          scratch memory in stream order as kernel arguments).
  * Other arguments, outputs and flags as sim_run_batch_gap; with both arrays
  * NULL, or all entries 0, the result equals sim_run_batch.  Asynchronous on
- * `stream`; no memory is allocated; calls on different streams sharing one
- * graph must not overlap in time.
+ * `stream`; no memory is allocated.
  */
 int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, const int32_t *gap,
@@ -202,13 +208,16 @@ int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
  *          SIM_ST_SHARE_LIMIT (more than SIM_SHARE_MAX ops at once on one
  *          shared resource); a scenario's replay stops at the first
  *          overflow or limit event in time order.
- * dur, makespan, finish, ld_fin as sim_run_batch; no placement.  The first
- * call on a graph allocates the scratch memory of this replay (up to about
- * 8 GiB, held until sim_graph_destroy); later calls allocate nothing.
- * Asynchronous on `stream`; calls on different streams sharing one graph
- * must not overlap in time.
+ * dur, makespan, finish, ld_fin as sim_run_batch; no placement.  The
+ * scratch memory of this replay is one set per graph, allocated by
+ * sim_graph_create (up to about 8 GiB for large graphs, fewer block regions
+ * when the device has less room); calls allocate nothing.  Calls on
+ * different streams that share one graph are ordered one after the other
+ * through that set's event; a call captured into a HIP graph uses the same
+ * set, so its replays must not overlap any other sharing call on the graph.
+ * Asynchronous on `stream`.
  */
-int sim_run_batch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int sim_run_batch_share(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                         const uint8_t *share, int32_t *makespan, int32_t *finish, int64_t ld_fin,
                         int32_t *status, void *stream);
 
@@ -243,12 +252,6 @@ const char *sim_strerror(int code);
  * distinct topological levels. */
 int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *n_edges,
                    int32_t *n_joins, int32_t *n_levels);
-
-/* Whether SIM_ALGO_WALK runs this graph (for scenarios without placement):
- * 1 if it does, 0 if the graph exceeds the walk's limits (too many ops or
- * resources for its on-chip state), in which case WALK runs EVENT;
- * SIM_E_INVAL for a NULL graph. */
-int sim_graph_walk_eligible(const sim_graph *g);
 
 /*
  * Bottleneck attribution (Sec. 1: the simulator is used to find the
@@ -311,7 +314,9 @@ void sim_static_destroy(sim_static *st);
  * -1 with SIM_ST_BAD_DUR (a duration < 1) or SIM_ST_OVERFLOW (a finish time
  * above INT32_MAX) in status; finish values of such scenarios are
  * unspecified.  Asynchronous on `stream`; no memory is allocated.  Calls on
- * different streams that share one object must not overlap in time.
+ * different streams may share one object: when its value slots live in
+ * global memory (one set, allocated by sim_static_create) a call waits for
+ * the previous user of that set as described for graphs above.
  */
 int sim_static_run(const sim_static *st, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                    int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
@@ -356,8 +361,7 @@ int sim_generate(int32_t n_ops, int64_t n_scen, const int32_t *base, int32_t n_k
 
 /* sim_run_batch on generated durations, without placement; makespan, finish,
  * ld_fin, status and stream as there.  flags: SIM_ALGO_AUTO or SIM_ALGO_EVENT
- * (the event kernel; other values return SIM_E_INVAL).  Calls on different
- * streams sharing one graph must not overlap in time. */
+ * (the event kernel; other values return SIM_E_INVAL). */
 int sim_run_generated(const sim_graph *g, int64_t n_scen, const int32_t *base, int32_t n_knobs,
                       int64_t knob_block, uint32_t noise, uint64_t seed, int64_t scen0,
                       int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
@@ -372,8 +376,7 @@ int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, const int32_
                                 int32_t path_cap, int32_t *path_len, void *stream);
 
 /* sim_static_run on generated durations (the generation arguments above);
- * makespan, finish, ld_fin, status and stream as sim_static_run.  Calls on
- * different streams sharing one object must not overlap in time. */
+ * makespan, finish, ld_fin, status and stream as sim_static_run. */
 int sim_static_run_generated(const sim_static *st, int64_t n_scen, const int32_t *base,
                              int32_t n_knobs, int64_t knob_block, uint32_t noise, uint64_t seed,
                              int64_t scen0, int32_t *makespan, int32_t *finish, int64_t ld_fin,

@@ -25,11 +25,14 @@ SIM_OK, SIM_E_INVAL, SIM_E_RANGE, SIM_E_CYCLE, SIM_E_NOMEM, SIM_E_HIP, SIM_E_LIM
 SIM_ST_BAD_DUR, SIM_ST_BAD_RES, SIM_ST_OVERFLOW, SIM_ST_SHARE_LIMIT, SIM_ST_INTERNAL = 1, 2, 4, 8, 16
 #: bandwidth sharing (include/mlsim.h): most active ops per shared resource, service units per ns
 SIM_SHARE_MAX, SIM_SHARE_UNIT = 64, 2952069120
-SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP, SIM_ALGO_WALK = 0, 1, 2, 3
-ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP, "walk": SIM_ALGO_WALK}
+SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP = 0, 1, 2
+ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP}
+#: kernel-variant pins of the testing entry point (include/mlsim_testing.h)
+TEST_VARIANTS = {"auto": 0, "ev_lds_groups": 1, "ev_blocks_cap": 3, "ev_reg": 4, "cp_global": 5,
+                 "rf_global": 6}
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
-           "sim_strerror", "sim_graph_info", "sim_graph_walk_eligible", "sim_static_create",
+           "sim_strerror", "sim_graph_info", "sim_testing_replan", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
            "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
            "sim_run_batch_dev", "sim_run_batch_share")
@@ -78,8 +81,8 @@ def _load():
     L.sim_strerror.restype = ctypes.c_char_p
     L.sim_graph_info.argtypes = [P, P, P, P, P, P]
     L.sim_graph_info.restype = ctypes.c_int
-    L.sim_graph_walk_eligible.argtypes = [P]
-    L.sim_graph_walk_eligible.restype = ctypes.c_int
+    L.sim_testing_replan.argtypes = [P, I32, I32]
+    L.sim_testing_replan.restype = ctypes.c_int
     L.sim_static_create.argtypes = [P, P, ctypes.POINTER(P)]
     L.sim_static_create.restype = ctypes.c_int
     L.sim_static_destroy.argtypes = [P]
@@ -131,7 +134,32 @@ def _dev_matrix(t, dtype, n_ops, what):
         raise ValueError(f"{what} must be {dtype} of shape (n_ops={n_ops}, n_scen)")
     if t.shape[1] > 1 and t.stride(1) != 1:
         raise ValueError(f"{what} must have unit stride along scenarios")
+    if n_ops > 1 and t.shape[1] > 0 and t.stride(0) < t.shape[1]:
+        raise ValueError(f"{what}: rows overlap (row stride {t.stride(0)} < {t.shape[1]} scenarios)")
     return t.data_ptr(), max(t.stride(0), t.shape[1])
+
+
+def _dev_vector(t, n, what, device=None):
+    """Pointer of a caller-supplied int32 [>= n] device vector with unit stride."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{what} must be a torch tensor on the GPU")
+    if t.dtype != torch.int32 or t.dim() != 1 or t.numel() < n:
+        raise ValueError(f"{what} must be int32 of shape ({n},) or longer")
+    if n > 1 and t.stride(0) != 1:
+        raise ValueError(f"{what} must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{what} is on {t.device}, the inputs on {device}")
+    return t.data_ptr()
+
+
+def _dev_out_matrix(t, n_ops, n, what, device):
+    """(pointer, ld) of a caller-supplied int32 [n_ops, >= n] output matrix."""
+    import torch
+    p, ld = _dev_matrix(t, torch.int32, n_ops, what)
+    if t is not None and (t.shape[1] < n or t.device != device):
+        raise ValueError(f"{what} must hold {n} scenarios on {device}")
+    return p, ld
 
 
 def noise_for_sigma(sigma: float) -> int:
@@ -172,7 +200,7 @@ def generate(gen: Gen, n_scen: int, out=None, stream=None):
     import torch
     if out is None:
         out = torch.empty((gen.n_ops, n_scen), dtype=torch.int32, device=gen.base.device)
-    optr, ld = _dev_matrix(out, torch.int32, gen.n_ops, "out")
+    optr, ld = _dev_out_matrix(out, gen.n_ops, n_scen, "out", gen.base.device)
     rc = _load().sim_generate(gen.n_ops, n_scen, *gen.args(), optr, ld, _stream_ptr(stream))
     if rc:
         raise SimError(rc, "sim_generate")
@@ -225,13 +253,13 @@ class Graph:
             raise SimError(rc, "sim_graph_info")
         return dict(zip(("n_ops", "n_res", "n_edges", "n_joins", "n_levels"), [v.value for v in vals]))
 
-    def walk_eligible(self) -> bool:
-        """Whether the lockstep walk (algo "walk", and "auto" without
-        placement) runs this graph; otherwise those run the event kernel."""
-        rc = _load().sim_graph_walk_eligible(self._h)
-        if rc < 0:
-            raise SimError(rc, "sim_graph_walk_eligible")
-        return rc == 1
+    def pin_variant(self, what: str, value: int = 0) -> None:
+        """Testing: pin this graph's kernels to one variant (``what`` in
+        ``TEST_VARIANTS``; "auto" forgets every pin) and plan its scratch
+        again (sim_testing_replan; synchronises the device)."""
+        rc = _load().sim_testing_replan(self._h, TEST_VARIANTS[what], int(value))
+        if rc:
+            raise SimError(rc, "sim_testing_replan")
 
     def run(self, dur, place=None, want_finish: bool = False, algo: str = "auto",
             makespan=None, finish=None, status=None, stream=None, gap=None, delay=None):
@@ -252,13 +280,17 @@ class Graph:
         S = dur.shape[1]
         pptr, ldp = _dev_matrix(place, torch.uint16, self.n_ops, "place")
         dev = dur.device
+        if place is not None and (place.shape[1] < S or place.device != dev):
+            raise ValueError(f"place must hold {S} scenarios on {dev}")
         if makespan is None:
             makespan = torch.empty(S, dtype=torch.int32, device=dev)
         if status is None:
             status = torch.empty(S, dtype=torch.int32, device=dev)
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
-        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        fptr, ldf = _dev_out_matrix(finish, self.n_ops, S, "finish", dev)
+        _dev_vector(makespan, S, "makespan", dev)
+        _dev_vector(status, S, "status", dev)
         def _res_vec(x, name):
             x = _host(x, np.int32)
             if x.shape != (self.n_res,):
@@ -304,7 +336,9 @@ class Graph:
             status = torch.empty(S, dtype=torch.int32, device=dev)
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
-        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        fptr, ldf = _dev_out_matrix(finish, self.n_ops, S, "finish", dev)
+        _dev_vector(makespan, S, "makespan", dev)
+        _dev_vector(status, S, "status", dev)
         rc = _load().sim_run_batch_share(self._h, S, dptr, ld, _hptr(sh), makespan.data_ptr(), fptr, ldf,
                                          status.data_ptr(), _stream_ptr(stream))
         if rc:
@@ -326,7 +360,9 @@ class Graph:
             status = torch.empty(n_scen, dtype=torch.int32, device=dev)
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, n_scen), dtype=torch.int32, device=dev)
-        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        fptr, ldf = _dev_out_matrix(finish, self.n_ops, n_scen, "finish", dev)
+        _dev_vector(makespan, n_scen, "makespan", dev)
+        _dev_vector(status, n_scen, "status", dev)
         rc = _load().sim_run_generated(self._h, n_scen, *gen.args(), makespan.data_ptr(), fptr, ldf,
                                        status.data_ptr(), ALGOS[algo], _stream_ptr(stream))
         if rc:
@@ -341,6 +377,7 @@ class Graph:
             raise ValueError("base table does not match the graph's op count")
         if cp_len is None:
             cp_len = torch.empty(n_scen, dtype=torch.int32, device=gen.base.device)
+        _dev_vector(cp_len, n_scen, "cp_len", gen.base.device)
         cap = max(self.n_ops, 1)
         path = np.empty(cap, np.int32)
         plen = np.zeros(1, np.int32)
@@ -369,6 +406,8 @@ class Graph:
         S = dur.shape[1]
         pptr, ldp = _dev_matrix(place, torch.uint16, self.n_ops, "place")
         dev = dur.device
+        if place is not None and (place.shape[1] < S or place.device != dev):
+            raise ValueError(f"place must hold {S} scenarios on {dev}")
         out = {k: torch.empty(S, dtype=torch.int32, device=dev) for k in ("makespan", "status", "chain_ops")}
         out["finish"] = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
         out["prev"] = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
@@ -395,6 +434,7 @@ class Graph:
         S = dur.shape[1]
         if cp_len is None:
             cp_len = torch.empty(S, dtype=torch.int32, device=dur.device)
+        _dev_vector(cp_len, S, "cp_len", dur.device)
         cap = max(self.n_ops, 1)
         path = np.empty(cap, np.int32)
         plen = np.zeros(1, np.int32)
@@ -445,7 +485,9 @@ class StaticReplay:
             status = torch.empty(S, dtype=torch.int32, device=dev)
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, S), dtype=torch.int32, device=dev)
-        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        fptr, ldf = _dev_out_matrix(finish, self.n_ops, S, "finish", dev)
+        _dev_vector(makespan, S, "makespan", dev)
+        _dev_vector(status, S, "status", dev)
         rc = _load().sim_static_run(self._h, S, dptr, ld, makespan.data_ptr(), fptr, ldf,
                                     status.data_ptr(), _stream_ptr(stream))
         if rc:
@@ -466,7 +508,9 @@ class StaticReplay:
             status = torch.empty(n_scen, dtype=torch.int32, device=dev)
         if want_finish and finish is None:
             finish = torch.empty((self.n_ops, n_scen), dtype=torch.int32, device=dev)
-        fptr, ldf = _dev_matrix(finish, torch.int32, self.n_ops, "finish")
+        fptr, ldf = _dev_out_matrix(finish, self.n_ops, n_scen, "finish", dev)
+        _dev_vector(makespan, n_scen, "makespan", dev)
+        _dev_vector(status, n_scen, "status", dev)
         rc = _load().sim_static_run_generated(self._h, n_scen, *gen.args(), makespan.data_ptr(), fptr, ldf,
                                               status.data_ptr(), _stream_ptr(stream))
         if rc:

@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmlsim.so")
-SOURCES = ["csrc/graph.cpp", "csrc/api.cpp", "csrc/static.cpp", "csrc/kernels.hip", "csrc/walk.hip",
+SOURCES = ["csrc/graph.cpp", "csrc/api.cpp", "csrc/static.cpp", "csrc/pool.cpp", "csrc/kernels.hip",
            "csrc/share.hip"]
 ARCH = os.environ.get("MLSIM_OFFLOAD_ARCH", "gfx950")
 

@@ -67,7 +67,7 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
                              const uint16_t *place, int64_t ld_place, int32_t *makespan,
                              int32_t *finish, int64_t ld_fin, int32_t *status, uint32_t flags,
                              void *stream) {
-  if (!g || n_scen < 0 || (flags & ~3u)) return SIM_E_INVAL;
+  if (!g || n_scen < 0 || (flags & ~3u) || (flags & 3u) == 3u) return SIM_E_INVAL;
   if (n_scen == 0) return SIM_OK;
   if (!makespan) return SIM_E_INVAL;
   if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
@@ -81,13 +81,14 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
     return SIM_OK;
   }
   const uint32_t algo = flags & 3u;
+  if (algo == 3u) return SIM_E_INVAL;
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
   if (algo == SIM_ALGO_SWEEP)
-    return launch_sweep(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
-  // the lockstep walk needs one resource map for every scenario
-  if (algo == SIM_ALGO_WALK && !place && walk_eligible(g))
-    return launch_walk(g, n_scen, dur, ld_dur, makespan, finish, ld_fin, status, st);
-  return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
-                      st);
+    return launch_sweep(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
+                        status, st);
+  return launch_event(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
+                      status, st);
 }
 
 extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
@@ -108,9 +109,12 @@ extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32
     if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
   if (!gap && !delay)
-    return launch_event(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
-  // gaps then delays go to the graph's scratch in stream order before the
+    return launch_event(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
+                        status, st);
+  // gaps then delays go to the call's scratch set in stream order before the
   // replay, passed by value, so the caller's arrays are no longer read on
   // return
   const int32_t R = g->n_res;
@@ -119,13 +123,13 @@ extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32
     if (gap) words[r] = gap[r];
     if (delay) words[R + r] = delay[r];
   }
-  int32_t *dev = (int32_t *)((char *)g->scratch + g->scratch_dev_off);
+  int32_t *dev = (int32_t *)(lease.base() + g->scratch_dev_off);
   if (int rc = launch_put_words(dev, words.data(), 2 * R, st)) return rc;
-  return launch_event_dev(g, n_scen, dur, ld_dur, place, ld_place, dev, gap != nullptr, delay != nullptr,
-                          makespan, finish, ld_fin, status, st);
+  return launch_event_dev(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, dev, gap != nullptr,
+                          delay != nullptr, makespan, finish, ld_fin, status, st);
 }
 
-extern "C" int sim_run_batch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+extern "C" int sim_run_batch_share(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                                    const uint8_t *share, int32_t *makespan, int32_t *finish, int64_t ld_fin,
                                    int32_t *status, void *stream) {
   if (!g || n_scen < 0) return SIM_E_INVAL;
@@ -145,9 +149,16 @@ extern "C" int sim_run_batch_share(sim_graph *g, int64_t n_scen, const int32_t *
     words[r] = share && share[r] ? 1 : 0;
     any = any || words[r];
   }
-  if (!any)  // nothing shared: the plain replay
-    return launch_event(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status, st);
-  return launch_share(g, n_scen, dur, ld_dur, words.data(), makespan, finish, ld_fin, status, st);
+  if (!any) {  // nothing shared: the plain replay
+    Lease lease(g->pool, st);
+    if (lease.rc()) return lease.rc();
+    return launch_event(g, lease.base(), n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
+                        st);
+  }
+  Lease lease(g->share_pool, st);
+  if (lease.rc()) return lease.rc();
+  return launch_share(g, lease.base(), n_scen, dur, ld_dur, words.data(), makespan, finish, ld_fin, status,
+                      st);
 }
 
 extern "C" int sim_run_batch_gap(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
@@ -175,8 +186,11 @@ extern "C" int sim_critical_path(const sim_graph *g, int64_t n_scen, const int32
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;
   }
-  int32_t *dist_dev = path_scen >= 0 ? (int32_t *)((char *)g->scratch + g->scratch_dist_off) : nullptr;
-  int rc = launch_cp(g, n_scen, dur, ld_dur, cp_len, dist_dev, path_scen, st);
+  // the path's dist column stays in the call's set until the copy below
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
+  int32_t *dist_dev = path_scen >= 0 ? (int32_t *)(lease.base() + g->scratch_dist_off) : nullptr;
+  int rc = launch_cp(g, lease.base(), n_scen, dur, ld_dur, cp_len, dist_dev, path_scen, st);
   if (rc || path_scen < 0) return rc;
 
   // Walk back from the lowest-id op of maximum dist, each time to the
@@ -219,7 +233,9 @@ extern "C" int sim_run_generated(const sim_graph *g, int64_t n_scen, const int32
     if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
-  return launch_event_gen(g, n_scen, gen, makespan, finish, ld_fin, status, st);
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
+  return launch_event_gen(g, lease.base(), n_scen, gen, makespan, finish, ld_fin, status, st);
 }
 
 extern "C" int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, const int32_t *base,
@@ -241,11 +257,13 @@ extern "C" int sim_critical_path_generated(const sim_graph *g, int64_t n_scen, c
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;
   }
-  int32_t *dist_dev = path_scen >= 0 ? (int32_t *)((char *)g->scratch + g->scratch_dist_off) : nullptr;
-  int rc = launch_cp(g, n_scen, nullptr, 0, cp_len, dist_dev, path_scen, st, &gen);
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
+  int32_t *dist_dev = path_scen >= 0 ? (int32_t *)(lease.base() + g->scratch_dist_off) : nullptr;
+  int rc = launch_cp(g, lease.base(), n_scen, nullptr, 0, cp_len, dist_dev, path_scen, st, &gen);
   if (rc || path_scen < 0) return rc;
-  // the path scenario's durations, generated once more into scratch
-  int32_t *dcol = (int32_t *)((char *)g->scratch + g->scratch_gen_off);
+  // the path scenario's durations, generated once more into the call's set
+  int32_t *dcol = (int32_t *)(lease.base() + g->scratch_gen_off);
   DurGen one = gen;
   one.scen0 = gen.scen0 + path_scen;
   if ((rc = launch_generate(one, 1, dcol, 1, st))) return rc;
@@ -286,11 +304,16 @@ extern "C" int sim_attribute(const sim_graph *g, int64_t n_scen, const int32_t *
     if (path_scen >= 0) *path_len = 0;
     return SIM_OK;
   }
-  int rc = launch_event_prev(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, prev, ld_op,
-                             status, st);
-  if (rc) return rc;
-  rc = launch_attr(g, n_scen, dur, ld_dur, place, ld_place, finish, prev, ld_op, status, busy, chain,
-                   ld_res, chain_ops, st);
+  int rc;
+  {
+    Lease lease(g->pool, st);
+    if (lease.rc()) return lease.rc();
+    rc = launch_event_prev(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, prev,
+                           ld_op, status, st);
+    if (rc) return rc;
+    rc = launch_attr(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, finish, prev, ld_op, status, busy,
+                     chain, ld_res, chain_ops, st);
+  }
   if (rc || path_scen < 0) return rc;
 
   // the chain of one scenario, walked on the host by the kernel's rule

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "sim.hpp"
+#include "mlsim_testing.h"
 
 using namespace mlsim;
 
@@ -666,8 +667,8 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   g->h_pred = C.pred;
   g->h_res.assign(op_res, op_res + n_ops);
 
-  g->scratch = nullptr;
   rc = plan_scratch(g);
+  if (!rc) rc = plan_share(g);
   if (rc) {
     sim_graph_destroy(g);
     return rc;
@@ -678,10 +679,43 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
 
 extern "C" void sim_graph_destroy(sim_graph *g) {
   if (!g) return;
-  if (g->scratch) (void)hipFree(g->scratch);
-  if (g->share_scratch) (void)hipFree(g->share_scratch);
+  g->pool.destroy();
+  g->share_pool.destroy();
   if (g->dev_mem) (void)hipFree(g->dev_mem);
   delete g;
+}
+
+extern "C" int sim_testing_replan(sim_graph *g, int32_t what, int32_t value) {
+  if (!g) return SIM_E_INVAL;
+  Variant v = g->var;
+  switch (what) {
+    case SIM_TEST_AUTO: v = Variant{}; break;
+    case SIM_TEST_EV_LDS_GROUPS:
+      if (value < -1 || value > 8) return SIM_E_INVAL;
+      v.ev_lds_groups = value;
+      break;
+    case SIM_TEST_EV_BLOCKS_CAP:
+      if (value < 0) return SIM_E_INVAL;
+      v.ev_blocks_cap = value;
+      break;
+    case SIM_TEST_EV_REG:
+      if (value < -1 || value > 1) return SIM_E_INVAL;
+      v.ev_reg = value;
+      break;
+    case SIM_TEST_CP_GLOBAL:
+      if (value < 0 || value > 1) return SIM_E_INVAL;
+      v.cp_global = value;
+      break;
+    case SIM_TEST_RF_GLOBAL:
+      if (value < 0 || value > 1) return SIM_E_INVAL;
+      v.rf_global = value;
+      break;
+    default: return SIM_E_INVAL;
+  }
+  // no call may be in flight: the old sets are freed
+  if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
+  g->var = v;
+  return plan_scratch(g);
 }
 
 extern "C" int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *n_edges,
@@ -693,11 +727,6 @@ extern "C" int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res
   if (n_joins) *n_joins = g->n_joins;
   if (n_levels) *n_levels = g->n_levels;
   return SIM_OK;
-}
-
-extern "C" int sim_graph_walk_eligible(const sim_graph *g) {
-  if (!g) return SIM_E_INVAL;
-  return walk_eligible(g) ? 1 : 0;
 }
 
 extern "C" const char *sim_strerror(int code) {

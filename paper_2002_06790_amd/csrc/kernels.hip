@@ -310,11 +310,6 @@ struct EvArgs {
   int heap_le;        // first heap position in global memory (16 + 8 k)
   int2 *join_g;       // [blocks][J][64] {predecessors finished, max finish}
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
-  int retry;          // 0: every scenario; 1: those whose makespan holds kWalkRetry, when
-                      // the retry list overflowed; 2: the scenarios on the retry list
-  const int32_t *list;        // retry list (scenario indices) and its length
-  const int32_t *list_count;
-  int32_t list_cap;
   int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
   int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
   DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
@@ -329,23 +324,12 @@ struct EvArgs {
 constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
 
 // A lane's join state {predecessors finished, max finish} per join index, in
-// global scratch ([J][64] int2) or in LDS ([J][64] packed into 64 bits).
+// global scratch ([J][64] int2).
 struct JoinGlobal {
   int2 *p;
   __device__ __forceinline__ int2 get(int j) const { return p[(size_t)j * kWave]; }
   __device__ __forceinline__ void set(int j, int2 v) const { p[(size_t)j * kWave] = v; }
 };
-struct JoinLds {
-  lptr<uint64_t> p;
-  __device__ __forceinline__ int2 get(int j) const {
-    const uint64_t x = p[(size_t)j * kWave];
-    return make_int2((int)(uint32_t)x, (int)(uint32_t)(x >> 32));
-  }
-  __device__ __forceinline__ void set(int j, int2 v) const {
-    p[(size_t)j * kWave] = (uint64_t)(uint32_t)v.x | ((uint64_t)(uint32_t)v.y << 32);
-  }
-};
-
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
 template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class Heap, class JPtr,
@@ -518,11 +502,9 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
 // are written in bursts of kFinQ stores per lane, so their completion is
 // waited for once per burst instead of once per step.  GEN: durations are
 // generated from the knob grid and counter-based noise of a.gen instead of
-// read from a.dur.  JOIN_LDS: the join state lives in LDS after the resource
-// times (and last-op table) instead of in global scratch.  REG: the heap
+// read from a.dur.  REG: the heap
 // root's children live in registers (see WideHeap).
-template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool JOIN_LDS = false,
-          bool REG = false>
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool REG = false>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -542,11 +524,6 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   uint32_t *rfree_g = a.rfree_g + (size_t)blockIdx.x * R * kWave + lane;
   lptr<uint32_t> rfree_l = as_lds((uint32_t *)(lds + (size_t)heap_lds * kWave)) + lane;
   const JoinGlobal jst_g{a.join_g + (size_t)blockIdx.x * G.J * kWave + lane};
-  // LDS after the heap, the resource times and (PREV) the last-op table
-  const JoinLds jst_l{as_lds((uint64_t *)((uint32_t *)(lds + (size_t)heap_lds * kWave) +
-                                          (size_t)(PREV ? 2 : 1) * R * kWave)) + lane};
-  if (JOIN_LDS)  // cleared once: every join is reset to zero when it fires
-    for (int j = 0; j < G.J; ++j) jst_l.set(j, make_int2(0, 0));
   auto rf_get = [&](int r) -> uint32_t { return RF_LDS ? rfree_l[r * kWave] : rfree_g[r * kWave]; };
   auto rf_set = [&](int r, uint32_t v) {
     if (RF_LDS)
@@ -569,20 +546,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     return x;
   };
 
-  int64_t items = a.n_scen;
-  if (a.retry) {
-    const int32_t cnt = *(const volatile int32_t *)a.list_count;
-    if (a.retry == 2) items = cnt < a.list_cap ? cnt : a.list_cap;
-    if (a.retry == 1 && cnt <= a.list_cap) return;  // every flagged scenario was on the list
-  }
-  for (int64_t tile = blockIdx.x; tile * kWave < items; tile += gridDim.x) {
-    const int64_t idx = tile * kWave + lane;
-    const bool in_range = idx < items;
-    // the scenario of this lane (inactive lanes replay a valid column)
-    const int64_t s = a.retry == 2 ? (int64_t)a.list[in_range ? idx : items - 1] : idx;
-    const bool active = in_range && (a.retry != 1 || a.makespan[s] == kWalkRetry);
-    if (a.retry == 1 && !__ballot(active)) continue;  // nothing to replay in this tile
-    const int64_t sc = in_range || a.retry == 2 ? s : a.n_scen - 1;
+  for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
+    const int64_t s = tile * kWave + lane;
+    const bool active = s < a.n_scen;
+    // the scenario column this lane replays (lanes past the end replay the last one)
+    const int64_t sc = active ? s : a.n_scen - 1;
     const bool store_fin = a.finish && active;
     const int64_t S = GEN ? a.gen.scen0 + sc : 0;  // global scenario index of the generator
     const int32_t *brow = GEN ? gen_knob_row(a.gen, S) : nullptr;
@@ -625,10 +593,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
                                                               s_hi, dev_l, st, span, fq, rq, pq, rf_get, rf_set,
                                                               last_xchg, flush);
       };
-      if constexpr (JOIN_LDS)
-        run_step(jst_l);
-      else
-        run_step(jst_g);
+      run_step(jst_g);
     }
     flush(n & (kFinQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
@@ -1082,16 +1047,24 @@ int occupancy_blocks(K kernel, size_t lds, int cus) {
 }
 
 constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
-// join state kept in LDS up to this size: 0, since on the BERT workload the
-// occupancy it costs outweighs the global round trip it saves (45.4 vs 41.2 ms)
-constexpr size_t kJoinLdsMax = 0;
-constexpr size_t kScratchBudget = 4ull << 30;  // global scratch of one graph
+constexpr size_t kScratchBudget = 4ull << 30;  // global per-block scratch of one kernel, per set
+constexpr size_t kSweepBudget = 1ull << 30;    // the sweep variant's per-op state, per set
+constexpr size_t kPoolBudget = 4ull << 30;     // all eager sets of one graph together
+constexpr int kMaxSets = 4;                    // eager sets per graph (at least one)
 
-char *base_heap(sim_graph *g) { return (char *)g->scratch + g->scratch_ev_heap_off; }
+bool rf_in_lds(const sim_graph *g) {
+  if (g->var.rf_global) return false;
+  return (size_t)g->dg.R * kWave * 4 <= kRfLdsMax;
+}
 
-bool rf_in_lds(const DevGraph &G) {
-  if (getenv("MLSIM_RF_GLOBAL")) return false;  // tuning override
-  return (size_t)G.R * kWave * 4 <= kRfLdsMax;
+// a fresh set: join state cleared, heap positions empty (all ones); the
+// kernels leave both that way
+int fill_set(void *ctx, char *base) {
+  const sim_graph *g = (const sim_graph *)ctx;
+  if (hipMemset(base, 0, g->scratch_bytes) != hipSuccess) return SIM_E_HIP;
+  if (g->heap_fill_bytes && hipMemset(base + g->scratch_ev_heap_off, 0xff, g->heap_fill_bytes) != hipSuccess)
+    return SIM_E_HIP;
+  return SIM_OK;
 }
 
 }  // namespace
@@ -1099,6 +1072,7 @@ bool rf_in_lds(const DevGraph &G) {
 int plan_scratch(sim_graph *g) {
   const DevGraph &G = g->dg;
   ScratchPlan &P = g->plan;
+  const Variant &V = g->var;
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, g->device) != hipSuccess) return SIM_E_HIP;
   const int cus = prop.multiProcessorCount;
@@ -1107,41 +1081,33 @@ int plan_scratch(sim_graph *g) {
   // lane's heap and its children in LDS, deeper positions (up to the exact
   // bound on ready ops) in global scratch
   const size_t rf_bytes = (size_t)G.R * kWave * 4;
-  const bool rf_lds = rf_in_lds(G);
+  const bool rf_lds = rf_in_lds(g);
+  P.rf_lds = rf_lds;
   P.ev_heap_stride = (int32_t)(((size_t)G.heap_cap + 2 * kD) & ~size_t(kD - 1));
   // groups of the root's grandchildren kept in LDS (4 KB per wave each):
   // four beside a small resource-time table, two beside a large one (heaps
   // of up to 41 or 25 entries then never touch global memory)
   const size_t rf_lds_bytes = rf_lds ? rf_bytes : 0;
   int lds_groups = rf_lds_bytes <= 8 * 1024 ? 4 : 2;
-  if (const char *e = getenv("MLSIM_EV_LDS_GROUPS"))  // tuning override
-    lds_groups = std::min(kD, std::max(0, atoi(e)));
+  if (V.ev_lds_groups >= 0) lds_groups = std::min(kD, V.ev_lds_groups);
   P.ev_heap_le = kL2 + kD * lds_groups;
-  // join state in LDS beside resource times in LDS when it is small
+  // join state in global scratch (in LDS it would cost more occupancy than
+  // the round trip it saves: 45.4 vs 41.2 ms on the BERT workload)
   const size_t join_bytes = (size_t)G.J * kWave * 8;
-  P.ev_join_lds = rf_lds && G.J > 0 && join_bytes <= kJoinLdsMax;  // off: see kJoinLdsMax
-  if (const char *e = getenv("MLSIM_JOIN_LDS"))  // tuning override
-    P.ev_join_lds = rf_lds && G.J > 0 && atoi(e) != 0;
-  const size_t join_lds_bytes = P.ev_join_lds ? join_bytes : 0;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
-  const size_t ev_per_block = (P.ev_join_lds ? 0 : join_bytes) + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
+  const size_t ev_per_block = join_bytes + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
   // device model (gaps, output delays), after the per-lane regions
   const size_t dev_table = ((size_t)G.R * 8 + 15) & ~size_t(15);
   auto grid_of = [&](int occ) -> int32_t {  // resident blocks within the scratch budget
     size_t b = (size_t)std::max(occ, 1);
     if (ev_per_block) b = std::min(b, std::max<size_t>(1, kScratchBudget / ev_per_block));
-    if (const char *e = getenv("MLSIM_EV_BLOCKS"))  // tuning override: cap on the persistent grid
-      b = std::min(b, (size_t)std::max(1, atoi(e)));
+    if (V.ev_blocks_cap > 0) b = std::min(b, (size_t)V.ev_blocks_cap);
     return (int32_t)b;
   };
   // the root's children in LDS (every variant)
-  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes + join_lds_bytes;
+  P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes;
   int occ[3];  // plain, generated durations, device model
-  if (P.ev_join_lds) {
-    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes, cus);
-    occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_lds_bytes + dev_table, cus);
-  } else if (rf_lds) {
+  if (rf_lds) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus);
     occ[2] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes + dev_table, cus);
@@ -1154,32 +1120,30 @@ int plan_scratch(sim_graph *g) {
   P.ev_blocks = grid_of(occ[0]);
   P.ev_gen_blocks = grid_of(occ[1]);
   P.ev_dev_blocks = grid_of(occ[2]);
-  // the root's children in registers (resource times in LDS, join state in
-  // global memory, no placement, no predecessor recording): 4 KB less LDS
-  P.ev_reg = rf_lds && !P.ev_join_lds;
+  // the root's children in registers (resource times in LDS, no placement,
+  // no predecessor recording): 4 KB less LDS
+  P.ev_reg = rf_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
   P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_dev_blocks = P.ev_reg_prev_blocks = 1;
   P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + rf_lds_bytes;  // with the last-op table
   if (P.ev_reg) {
-    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
-    occ[1] = occupancy_blocks(k_event<true, false, false, false, true, false, true>, P.ev_reg_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, false, true>,
-                              P.ev_reg_lds_bytes + dev_table, cus);
+    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
+    occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes + dev_table,
+                              cus);
     if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
     P.ev_reg_blocks = grid_of(occ[0]);
     P.ev_reg_gen_blocks = grid_of(occ[1]);
     P.ev_reg_dev_blocks = grid_of(occ[2]);
     const int prev_occ =
-        occupancy_blocks(k_event<true, false, false, true, false, false, true>, P.ev_reg_prev_lds_bytes, cus);
+        occupancy_blocks(k_event<true, false, false, true, false, true>, P.ev_reg_prev_lds_bytes, cus);
     if (prev_occ < 0) return SIM_E_HIP;
     P.ev_reg_prev_blocks = grid_of(prev_occ);
   }
   // the event kernel for attribution: a last-op table beside the resource times
   P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
-  const int ev_prev_occ =
-      P.ev_join_lds ? occupancy_blocks(k_event<true, false, false, true, false, true>, P.ev_prev_lds_bytes, cus)
-      : rf_lds      ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
-                    : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
+  const int ev_prev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
+                                : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
   P.ev_prev_blocks = grid_of(ev_prev_occ);
   // attribution chains: busy and chain accumulators in LDS when they fit
@@ -1200,9 +1164,7 @@ int plan_scratch(sim_graph *g) {
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
   const size_t cp_ring = 4 * sizeof(CpRec) * kCpBatch;  // record ring
-  P.cp_mode = cp_bytes <= 32 * 1024 ? kCpSlotsLds : kCpSlotsGlobal;
-  if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
-    if (!strcmp(e, "global")) P.cp_mode = kCpSlotsGlobal;
+  P.cp_mode = cp_bytes <= 32 * 1024 && !V.cp_global ? kCpSlotsLds : kCpSlotsGlobal;
   P.cp_lds_bytes = cp_ring + (P.cp_mode == kCpSlotsLds ? cp_bytes : 0);
   const int cp_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus);
   const int cp_gen_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus, true);
@@ -1228,7 +1190,7 @@ int plan_scratch(sim_graph *g) {
   if (sw_occ < 0) return SIM_E_HIP;
   const size_t sw_per_block = (P.sw_val_lds ? 0 : val_bytes) + (P.sw_res_lds ? 0 : res_bytes);
   size_t sw_blocks = (size_t)sw_occ;
-  if (sw_per_block) sw_blocks = std::min(sw_blocks, std::max<size_t>(1, kScratchBudget / sw_per_block));
+  if (sw_per_block) sw_blocks = std::min(sw_blocks, std::max<size_t>(1, kSweepBudget / sw_per_block));
   P.sw_blocks = (int32_t)sw_blocks;
 
   size_t off = 0;
@@ -1238,7 +1200,8 @@ int plan_scratch(sim_graph *g) {
     return o;
   };
   g->scratch_ev_heap_off = take(heap_g_bytes * ev_grid);
-  g->scratch_ev_join_off = take(P.ev_join_lds ? 0 : join_bytes * ev_grid);
+  g->heap_fill_bytes = heap_g_bytes * ev_grid;
+  g->scratch_ev_join_off = take(join_bytes * ev_grid);
   g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_ev_last_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_at_off = take(P.at_lds ? 0 : (size_t)2 * G.R * kWave * 4 * P.at_blocks);
@@ -1248,52 +1211,35 @@ int plan_scratch(sim_graph *g) {
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   g->scratch_gen_off = take((size_t)std::max(G.n, 1) * 4);  // one generated duration column
   g->scratch_dev_off = take((size_t)G.R * 8);                 // the device model of a call
-  {
-    const int rc = plan_walk(g, cus);
-    if (rc) return rc;
-  }
-  g->scratch_wk_off = take(P.wk_ok ? ((size_t)P.wk_groups_max * (size_t)P.wk_group_words + kWave) * 4 : 0);
-  g->scratch_retry_off = take(P.wk_ok ? ((size_t)kRetryCap + 64) * 4 : 0);
   g->scratch_bytes = off;
-  if (hipMalloc(&g->scratch, off) != hipSuccess) {
-    g->scratch = nullptr;
-    return SIM_E_NOMEM;
-  }
-  // join state must start cleared and heap positions empty (all ones); the
-  // kernels leave both that way
-  if (hipMemset(g->scratch, 0, off) != hipSuccess) return SIM_E_HIP;
-  if (hipMemset(base_heap(g), 0xff, heap_g_bytes * ev_grid) != hipSuccess) return SIM_E_HIP;
-  if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
-  if (getenv("MLSIM_VERBOSE"))
+  // as many eager sets as the pool budget allows (one at least), and one
+  // for calls captured into HIP graphs
+  const int n_sets = (int)std::max<size_t>(1, std::min<size_t>(kMaxSets, kPoolBudget / std::max<size_t>(off, 1)));
+  g->pool.destroy();
+  if (int rc = g->pool.init(off, n_sets, true, fill_set, g)) return rc;
+  if (getenv("MLSIM_VERBOSE"))  // diagnostics only
     fprintf(stderr,
             "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (mode %d) "
-            "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu "
-            "walk=%d (groups %d, words %lld, rs_cap %d, slots %d, pilot_lds %zu, walk_lds %zu, blocks %d) "
-            "scratch=%zu MB\n",
+            "ev_blocks=%d cp_blocks=%d sw_blocks=%d ev_lds=%zu scratch=%zu MB x %d sets\n",
             G.n, G.R, G.J, g->n_barriers, G.heap_cap, P.ev_heap_stride, P.ev_heap_le, G.cp_slots, P.cp_mode,
-            P.ev_blocks, P.cp_blocks, P.sw_blocks,
-            P.ev_lds_bytes, P.wk_ok, P.wk_groups_max, (long long)P.wk_group_words, P.wk_rs_cap,
-            P.wk_slot_max, P.wk_pilot_lds, P.wk_walk_lds, P.wk_blocks, off >> 20);
+            P.ev_blocks, P.cp_blocks, P.sw_blocks, P.ev_lds_bytes, off >> 20, n_sets);
   return SIM_OK;
 }
 
 namespace {
-int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
-                      int64_t ld_fin, int32_t *status, int retry, const int32_t *list,
-                      const int32_t *list_count, int32_t list_cap, int32_t *prev, hipStream_t stream,
+                      int64_t ld_fin, int32_t *status, int32_t *prev, hipStream_t stream,
                       const DurGen *gen = nullptr, const int32_t *dev = nullptr, bool has_gap = false,
                       bool has_delay = false) {
   const ScratchPlan &P = g->plan;
-  char *base = (char *)g->scratch;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
-           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off), retry,
-           list, list_count, list_cap, prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{},
-           dev, has_gap, has_delay, 0};
+           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off),
+           prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, dev, has_gap, has_delay, 0};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
-  const bool rf_lds = rf_in_lds(g->dg);
+  const bool rf_lds = P.rf_lds;
   const dim3 block(kWave);
   // when the last round of tiles would fill less than half the grid, use
   // fewer blocks that each take the same number of tiles (within one)
@@ -1301,8 +1247,7 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   // variant with the children in LDS would need two or more rounds of tiles
   const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : dev ? P.ev_dev_blocks : P.ev_blocks;
   bool reg = P.ev_reg && !place && tiles >= 2 * lds_blocks;
-  if (const char *e = getenv("MLSIM_EV_REG"))  // tuning override
-    reg = P.ev_reg && !place && atoi(e) != 0;
+  if (g->var.ev_reg >= 0) reg = P.ev_reg && !place && g->var.ev_reg != 0;
   const int64_t blocks = !reg ? lds_blocks
                          : prev ? P.ev_reg_prev_blocks
                          : gen  ? P.ev_reg_gen_blocks
@@ -1318,16 +1263,14 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
     a.dev_lds = (int)lds;
     lds += ((size_t)g->dg.R * 8 + 15) & ~size_t(15);
   }
-  const int variant = (reg ? 64 : 0) | (P.ev_join_lds ? 32 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
+  const int variant = (reg ? 64 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
                       (rf_lds ? 4 : 0) | (g->dg.ev_compact ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_GEN_CASE(V, A, B) \
   case V: k_event<A, B, false, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
-#define EV_JOIN_CASE(V, B, C, D, E) \
-  case V: k_event<true, B, C, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
 #define EV_REG_CASE(V, B, D, E) \
-  case V: k_event<true, B, false, D, E, false, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+  case V: k_event<true, B, false, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
     // the heap root's children in registers
     EV_REG_CASE(68, false, false, false)
@@ -1336,17 +1279,6 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
     EV_REG_CASE(78, true, true, false)
     EV_REG_CASE(84, false, false, true)
     EV_REG_CASE(86, true, false, true)
-    // join state in LDS (always with resource times in LDS)
-    EV_JOIN_CASE(36, false, false, false, false)
-    EV_JOIN_CASE(37, false, true, false, false)
-    EV_JOIN_CASE(38, true, false, false, false)
-    EV_JOIN_CASE(39, true, true, false, false)
-    EV_JOIN_CASE(44, false, false, true, false)
-    EV_JOIN_CASE(45, false, true, true, false)
-    EV_JOIN_CASE(46, true, false, true, false)
-    EV_JOIN_CASE(47, true, true, true, false)
-    EV_JOIN_CASE(52, false, false, false, true)
-    EV_JOIN_CASE(54, true, false, false, true)
     EV_GEN_CASE(16, false, false)
     EV_GEN_CASE(18, false, true)
     EV_GEN_CASE(20, true, false)
@@ -1370,7 +1302,6 @@ int launch_event_impl(const sim_graph *g, int64_t n_scen, const int32_t *dur, in
   }
 #undef EV_CASE
 #undef EV_GEN_CASE
-#undef EV_JOIN_CASE
 #undef EV_REG_CASE
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
@@ -1438,44 +1369,32 @@ int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld,
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
-int launch_event_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event_dev(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                      const uint16_t *place, int64_t ld_place, const int32_t *dev, bool has_gap,
                      bool has_delay, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
                      hipStream_t stream) {
-  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, 0,
-                           nullptr, nullptr, 0, nullptr, stream, nullptr, dev, has_gap, has_delay);
+  return launch_event_impl(g, scr, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
+                           nullptr, stream, nullptr, dev, has_gap, has_delay);
 }
 
-int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
+int launch_event_gen(const sim_graph *g, char *scr, int64_t n_scen, const DurGen &gen, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
-  return launch_event_impl(g, n_scen, nullptr, 0, nullptr, 0, makespan, finish, ld_fin, status, 0, nullptr,
-                           nullptr, 0, nullptr, stream, &gen);
+  return launch_event_impl(g, scr, n_scen, nullptr, 0, nullptr, 0, makespan, finish, ld_fin, status, nullptr,
+                           stream, &gen);
 }
 
-int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream) {
-  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
-                           status, 0, nullptr, nullptr, 0, nullptr, stream);
+  return launch_event_impl(g, scr, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
+                           status, nullptr, stream);
 }
 
-int launch_event_prev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event_prev(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int32_t *prev, int64_t ld_op, int32_t *status, hipStream_t stream) {
-  return launch_event_impl(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_op,
-                           status, 0, nullptr, nullptr, 0, prev, stream);
-}
-
-int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                       int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
-                       const int32_t *list, const int32_t *list_count, int32_t list_cap,
-                       hipStream_t stream) {
-  // the listed scenarios, then (only if the list overflowed) every flagged one
-  int rc = launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
-                             2, list, list_count, list_cap, nullptr, stream);
-  if (rc) return rc;
-  return launch_event_impl(g, n_scen, dur, ld_dur, nullptr, 0, makespan, finish, ld_fin, status,
-                           1, list, list_count, list_cap, nullptr, stream);
+  return launch_event_impl(g, scr, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_op,
+                           status, prev, stream);
 }
 
 int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen) {
@@ -1519,23 +1438,23 @@ int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
-int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_cp(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
               const DurGen *gen) {
   const ScratchPlan &P = g->plan;
   const MpTable T{g->dg.n, g->dg.cp_slots, g->dg.cp, g->dg.cp_pred};
   return launch_maxplus(T, P.cp_mode, gen ? P.cp_gen_blocks : P.cp_blocks, P.cp_lds_bytes, n_scen, dur,
                         ld_dur, cp_len, nullptr, nullptr, 0, dist_out, dist_scen,
-                        (uint32_t *)((char *)g->scratch + g->scratch_cp_off), stream, gen);
+                        (uint32_t *)(scr + g->scratch_cp_off), stream, gen);
 }
 
-int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_attr(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                 const uint16_t *place, int64_t ld_place, const int32_t *finish, const int32_t *prev,
                 int64_t ld_op, const int32_t *status, int32_t *busy, int32_t *chain, int64_t ld_res,
                 int32_t *chain_ops, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
   AtArgs a{n_scen, dur, ld_dur, place, ld_place, finish, prev, ld_op, status, busy, chain, ld_res,
-           chain_ops, (uint32_t *)((char *)g->scratch + g->scratch_at_off)};
+           chain_ops, (uint32_t *)(scr + g->scratch_at_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const dim3 grid((unsigned)std::min<int64_t>(tiles, P.at_blocks)), blk(kWave);
   const size_t lds = P.at_lds_bytes;
@@ -1553,11 +1472,10 @@ int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t 
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
-int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_sweep(const sim_graph *g, char *base, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream) {
   const ScratchPlan &P = g->plan;
-  char *base = (char *)g->scratch;
   SwArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
            (uint32_t *)(base + g->scratch_sw_val_off), (uint32_t *)(base + g->scratch_sw_res_off)};
   const int64_t tiles = (n_scen + kWave - 1) / kWave;

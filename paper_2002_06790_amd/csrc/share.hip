@@ -326,65 +326,86 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
 
 }  // namespace
 
-int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur, const int32_t *share_words,
-                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream) {
+namespace {
+int64_t al256(int64_t b) { return (b + 255) & ~(int64_t)255; }
+
+// bytes of one block's region for a heap of cap entries per lane (and the
+// offsets of its parts in a)
+int64_t share_block_bytes(int64_t R, int64_t cap, int64_t slots, ShArgs *a) {
+  int64_t off = 0;
+  off += al256(cap * 8 * kWave);
+  if (a) a->o_rc = off;
+  off += al256(std::max<int64_t>(slots, 1) * 8 * kWave);
+  if (a) a->o_rf = off;
+  off += al256(R * 4 * kWave);
+  if (a) a->o_ln = off;
+  off += al256(R * (int64_t)sizeof(LinkSt) * kWave);
+  if (a) a->o_need = off;
+  off += al256(R * kShareMax * 8 * kWave);
+  if (a) a->o_op = off;
+  off += al256(R * kShareMax * 4 * kWave);
+  return off;
+}
+
+// a set's constant head: the word slot of each node and the predecessor
+// count of each slot (the resource flags before them are written per call)
+int fill_share_set(void *ctx, char *b) {
+  const sim_graph *g = (const sim_graph *)ctx;
+  const int64_t R = g->dg.R, N = (int64_t)g->share_slot_of.size();
+  if (hipMemcpy(b + al256(R * 4), g->share_slot_of.data(), (size_t)N * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return SIM_E_HIP;
+  if (!g->share_np.empty() && hipMemcpy(b + al256(R * 4) + al256(N * 4), g->share_np.data(),
+                                        g->share_np.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return SIM_E_HIP;
+  return SIM_OK;
+}
+}  // namespace
+
+// Sized once per graph: the word slots of nodes with two or more
+// predecessors, and one set holding the resource flags, the slot tables and
+// the block regions, sized for the largest heap any call can need (every
+// resource shared) within the budget.  When the device cannot hold the
+// budget, fewer block regions are kept (a call then runs fewer blocks at a
+// time).
+int plan_share(sim_graph *g) {
   const DevGraph &G = g->dg;
   const int64_t N = (int64_t)G.n + G.nb, R = G.R;
-  auto al = [](int64_t b) { return (b + 255) & ~(int64_t)255; };
-  // bytes of one block's region for a heap of cap entries per lane
-  auto block_bytes = [&](int64_t cap, int64_t slots, ShArgs *a) {
-    int64_t off = 0;
-    off += al(cap * 8 * kWave);
-    if (a) a->o_rc = off;
-    off += al(std::max<int64_t>(slots, 1) * 8 * kWave);
-    if (a) a->o_rf = off;
-    off += al(R * 4 * kWave);
-    if (a) a->o_ln = off;
-    off += al(R * (int64_t)sizeof(LinkSt) * kWave);
-    if (a) a->o_need = off;
-    off += al(R * kShareMax * 8 * kWave);
-    if (a) a->o_op = off;
-    off += al(R * kShareMax * 4 * kWave);
-    return off;
-  };
-  // first use: the word slots of nodes with two or more predecessors, and
-  // the scratch (resource flags, slot tables, then the block regions, sized
-  // for the largest heap any call can need within the budget)
-  if (!g->share_scratch) {
-    std::vector<int32_t> wp((size_t)N + 1);
-    if (hipMemcpy(wp.data(), G.wp_ptr, wp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess) return SIM_E_HIP;
-    std::vector<int32_t> slot((size_t)N, -1), np;
-    for (int64_t x = 0; x < N; ++x)
-      if (wp[x + 1] - wp[x] > 1) {
-        slot[x] = (int32_t)np.size();
-        np.push_back(wp[x + 1] - wp[x]);
-      }
-    const int64_t head = al(R * 4) + al(N * 4) + al(std::max<size_t>(np.size(), 1) * 4);
-    const int64_t worst = block_bytes(3 * (int64_t)G.n + 1, (int64_t)np.size(), nullptr);
-    const int64_t region = std::max(worst, std::min(kShareScratchBudget, kShareBlocksMax * worst));
-    if (hipMalloc(&g->share_scratch, (size_t)(head + region)) != hipSuccess) {
-      g->share_scratch = nullptr;
-      return SIM_E_NOMEM;
+  std::vector<int32_t> wp((size_t)N + 1);
+  if (hipMemcpy(wp.data(), G.wp_ptr, wp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess) return SIM_E_HIP;
+  g->share_slot_of.assign((size_t)N, -1);
+  g->share_np.clear();
+  for (int64_t x = 0; x < N; ++x)
+    if (wp[x + 1] - wp[x] > 1) {
+      g->share_slot_of[x] = (int32_t)g->share_np.size();
+      g->share_np.push_back(wp[x + 1] - wp[x]);
     }
-    char *b = (char *)g->share_scratch;
-    if (hipMemcpy(b + al(R * 4), slot.data(), slot.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
-        (!np.empty() && hipMemcpy(b + al(R * 4) + al(N * 4), np.data(), np.size() * 4, hipMemcpyHostToDevice) !=
-                            hipSuccess)) {
-      (void)hipFree(g->share_scratch);
-      g->share_scratch = nullptr;
-      return SIM_E_HIP;
-    }
-    g->share_head = head;
+  g->share_slots = (int32_t)g->share_np.size();
+  const int64_t head = al256(R * 4) + al256(N * 4) + al256(std::max<size_t>(g->share_np.size(), 1) * 4);
+  const int64_t worst = share_block_bytes(R, 3 * (int64_t)G.n + 1, g->share_slots, nullptr);
+  int64_t region = std::max(worst, std::min(kShareScratchBudget, kShareBlocksMax * worst));
+  g->share_head = head;
+  for (;;) {
     g->share_region = region;
-    g->share_slots = (int32_t)np.size();
+    g->share_pool.destroy();
+    const int rc = g->share_pool.init((size_t)(head + region), 1, false, fill_share_set, g);
+    if (rc != SIM_E_NOMEM || region <= worst) return rc;
+    (void)hipGetLastError();  // clear the failed allocation's error
+    region = std::max(worst, region / 2);
   }
+}
+
+int launch_share(const sim_graph *g, char *b, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const int32_t *share_words, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
+                 hipStream_t stream) {
+  const DevGraph &G = g->dg;
+  const int64_t N = (int64_t)G.n + G.nb, R = G.R;
   // this call's heap: every ready op once, and two keys per op on a shared
   // resource (its arrival and at most one departure batch)
   int64_t m_sh = 0;
   for (int32_t v = 0; v < g->n_ops; ++v) m_sh += share_words[g->h_res[v]] != 0;
   const int64_t cap = (int64_t)G.n + 2 * m_sh + 1;
   ShArgs a{};
-  a.block_bytes = block_bytes(cap, g->share_slots, &a);
+  a.block_bytes = share_block_bytes(R, cap, g->share_slots, &a);
   a.heap_cap = cap;
   // LDS: the heap's top positions, then the resource flags when they are few
   a.flags_lds = R <= kShareFlagsLds;
@@ -393,7 +414,6 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   const size_t lds = (size_t)a.heap_lds * 8 * kWave + (a.flags_lds ? (size_t)R * 4 : 0);
   // the flags travel in stream order as kernel arguments, so the caller's
   // array is no longer read on return
-  char *b = (char *)g->share_scratch;
   int32_t *flags = (int32_t *)b;
   if (int rc = launch_put_words(flags, share_words, (int32_t)R, stream)) return rc;
   // a persistent grid: as many blocks as the region holds, balanced so the
@@ -410,8 +430,8 @@ int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_du
   a.ld_fin = ld_fin;
   a.status = status;
   a.share = flags;
-  a.slot_of = (const int32_t *)(b + al(R * 4));
-  a.np_of = (const int32_t *)(b + al(R * 4) + al(N * 4));
+  a.slot_of = (const int32_t *)(b + al256(R * 4));
+  a.np_of = (const int32_t *)(b + al256(R * 4) + al256(N * 4));
   a.n_slots = g->share_slots;
   a.scratch = b + g->share_head;
   k_share<<<dim3((unsigned)blocks), dim3(kWave), lds, stream>>>(G, a);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "mlsim.h"
@@ -84,7 +85,7 @@ struct DevGraph {
   const int32_t *lvl_of;  // [n] level of each compact op (longest path from a source)
   const int32_t *levend;  // [levels] last position of each level in topo
   int32_t n_levels, pad3;
-  // walk graph over nodes 0..n+nb-1 (ops, then barriers): a barrier's
+  // node graph over 0..n+nb-1 (ops, then barriers; the sharing replay): a barrier's
   // predecessors are its shared set, a member's only predecessor is its
   // barrier; successor lists are the reverse
   int32_t nb, pad1;
@@ -116,50 +117,6 @@ struct DevGraph {
   const int4 *ev_rec16;
 };
 
-// Lockstep walk (walk.hip).  Per group of tiles, k_pilot writes a header of
-// kHdrWords words, then kProgWords words per position and the slot lists.
-// A position record holds: the op's row; its resource and output slot; its
-// compact id and sink flag; its packed predecessor slots (or the offset of
-// its slot lists); the row kAhead positions ahead; and up to kInlineCand
-// pull-forward candidates with their offsets, compact ids, rows and packed
-// predecessor slots.
-constexpr int kHdrWords = 8, kProgWords = 16;
-constexpr int kInlineCand = 3;
-constexpr int kCand = 7;      // pull-forward candidates per position: next ops on the resource
-constexpr int kRing = 64;     // duration rows held in LDS (positions k .. k + kAhead)
-constexpr int kAhead = 60;    // rows requested this many positions ahead of the walk
-constexpr int kLat = 16;      // steps a row request has to arrive
-constexpr int kDefer = 16;    // per-lane deferred sinks
-constexpr int kSlotMax = 128; // value slots a walk program may use (packed as 8-bit indices)
-constexpr int kWalkMaxRes = 48;  // resource state lives in registers (more would spill)
-constexpr int32_t kWalkRetry = -2;  // makespan marker: replay this scenario with k_event
-constexpr int32_t kRetryCap = 1 << 20;  // scenarios the retry list holds (then: marker scan)
-struct WalkHdr {
-  int32_t valid;  // 1: program usable; 0: every tile of the group is replayed by k_event
-  int32_t slots;  // value slots used
-  int32_t pad[6];
-};
-struct WalkArgs {
-  int64_t n_scen;
-  const int32_t *dur;
-  int64_t ld_dur;
-  int32_t *makespan;
-  int32_t *finish;
-  int64_t ld_fin;
-  int32_t *status;
-  int32_t *groups;       // [n_groups][group_words]
-  int64_t group_words;
-  int32_t n_groups;
-  int32_t tiles_per_group;
-  int32_t rs_cap;        // pilot ready-list capacity (LDS)
-  int32_t slot_max;      // walk value slots (LDS)
-  int32_t pslot_cap;     // predecessor-slot words per group
-  int32_t pad;
-  int32_t *dummy;        // [64] target of finish stores that lanes skip
-  int32_t *retry_list;   // [kRetryCap] flagged scenarios
-  int32_t *retry_count;  // entries appended (may exceed kRetryCap)
-};
-
 struct ScratchPlan {
   int32_t ev_blocks;    // persistent grid of the event kernel
   int32_t ev_heap_stride;  // global heap entries per lane (lane-major, multiple of 16)
@@ -175,20 +132,71 @@ struct ScratchPlan {
   int32_t ev_prev_blocks, at_blocks, at_lds;
   // generated durations: persistent grids of the event and critical-path kernels
   int32_t ev_gen_blocks, cp_gen_blocks;
-  int32_t ev_join_lds;  // event kernel: join state in LDS (after the resource times)
   int32_t ev_dev_blocks;  // event kernel with a device model (gaps, delays: their table in LDS)
   // event kernel with the heap root's children in registers: available,
   // persistent grids (plain, generated durations, device model) and LDS per block
   int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_dev_blocks, ev_reg_prev_blocks;
   size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
-  // lockstep walk: 0 when the graph does not fit its limits
-  int32_t wk_ok;
-  int32_t wk_groups_max;  // groups the scratch holds
-  int32_t wk_blocks;      // persistent grid of k_walk
-  int32_t wk_rs_cap, wk_slot_max, wk_pslot_cap;
-  int64_t wk_group_words;
-  size_t wk_pilot_lds, wk_walk_lds;
+  int32_t rf_lds;       // event kernel: resource times in LDS (1) or global scratch (0)
+};
+
+// Kernel variants a graph's launch plan may be pinned to instead of the
+// library's choice (every variant computes the same results; the testing
+// entry point sim_testing_replan sets these so each one can be checked).
+struct Variant {
+  int32_t ev_lds_groups = -1;  // heap groups of the root's grandchildren in LDS (0..8), -1: auto
+  int32_t ev_blocks_cap = 0;   // cap on the event kernel's persistent grid, 0: none
+  int32_t ev_reg = -1;         // heap root's children in registers (0/1), -1: auto
+  int32_t cp_global = 0;       // max-plus value slots in global scratch (1) even when LDS holds them
+  int32_t rf_global = 0;       // resource times in global scratch (1) even when LDS holds them
+};
+
+// A few copies ("sets") of one scratch layout.  Every call takes one set for
+// its launches and records an event after them; the next call that takes
+// the set first makes its stream wait for that event, so two calls never use
+// one set at the same time, whichever streams they run on.  A call prefers
+// a set last used on its own stream, then an idle set, then the least
+// recently used one.  Calls being captured into a HIP graph use the capture
+// set (or set 0 when there is none) without events: such calls cannot wait
+// for or record events outside their graph.
+struct ScratchPool {
+  struct Set {
+    char *base = nullptr;
+    hipEvent_t done = nullptr;
+    hipStream_t last = nullptr;
+    bool used = false;
+    uint64_t tick = 0;
+  };
+  std::vector<Set> sets;
+  Set capture;  // base == nullptr: captured calls use sets[0]
+  size_t bytes = 0;
+  uint64_t clock = 0;
+  std::mutex mu;
+  // allocate n copies of `bytes` (plus the capture copy); init(base) fills
+  // one copy's initial contents (stream-ordered on the null stream)
+  int init(size_t bytes, int n, bool with_capture, int (*fill)(void *ctx, char *base), void *ctx);
+  void destroy();
+};
+
+// The set a call uses, held from its first launch until the event after its
+// last launch is recorded (the pool's lock is held as long).
+class Lease {
+ public:
+  Lease(ScratchPool &pool, hipStream_t stream);
+  ~Lease();
+  char *base() const { return set_ ? set_->base : nullptr; }
+  int rc() const { return rc_; }
+  Lease(const Lease &) = delete;
+  Lease &operator=(const Lease &) = delete;
+
+ private:
+  ScratchPool &pool_;
+  std::unique_lock<std::mutex> lock_;
+  ScratchPool::Set *set_ = nullptr;
+  hipStream_t stream_;
+  bool capturing_ = false;
+  int rc_ = 0;
 };
 
 }  // namespace mlsim
@@ -201,22 +209,27 @@ struct sim_graph {
   int device;
   mlsim::DevGraph dg;
   mlsim::ScratchPlan plan;
+  mlsim::Variant var;
   void *dev_mem;          // one allocation holding every graph array
-  void *scratch;          // event kernel: heaps / join state (global variants)
+  // scratch sets of the event, sweep, critical-path and attribution kernels
+  // (one layout, offsets below) and of the bandwidth-sharing replay; sized
+  // here at creation, never allocated by a call
+  mutable mlsim::ScratchPool pool, share_pool;
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
-  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off, scratch_wk_off, scratch_retry_off;
+  size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off;
   size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off, scratch_dev_off;
+  size_t heap_fill_bytes;  // leading bytes of a set that start as all ones (global heap levels)
   // host copies: critical-path recovery (compact predecessor CSR and the
   // caller id of each compact id) and static-order compilation (resource of
   // each op by caller id)
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred, h_res;
   size_t scratch_bytes;
-  // bandwidth-sharing replay: its scratch (allocated on first use): the
-  // resource flags of the current call, the word slots of joining nodes,
-  // then the per-block regions of its persistent grid
-  void *share_scratch = nullptr;
+  // bandwidth-sharing replay: a set holds the resource flags of the current
+  // call, the word slots of joining nodes, then the per-block regions of its
+  // persistent grid
   int64_t share_head = 0, share_region = 0;  // bytes of flags and slot tables; of block regions
   int32_t share_slots = 0;                    // nodes with two or more predecessors
+  std::vector<int32_t> share_slot_of, share_np;  // host copies of the slot tables
 };
 
 namespace mlsim {
@@ -226,25 +239,19 @@ constexpr uint64_t kShareUnit = SIM_SHARE_UNIT;
 constexpr int kShareMax = SIM_SHARE_MAX;
 constexpr int64_t kShareBlocksMax = 2048;
 constexpr int64_t kShareScratchBudget = (int64_t)8 << 30;
-int launch_share(sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur, const int32_t *share_words,
-                 int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
-// launchers (kernels.hip)
-int launch_event(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+// sizes the sharing replay's scratch and allocates its set (at creation)
+int plan_share(sim_graph *g);
+int launch_share(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                 const int32_t *share_words, int32_t *makespan, int32_t *finish, int64_t ld_fin,
+                 int32_t *status, hipStream_t stream);
+// launchers (kernels.hip); scr is the base of the scratch set the call holds
+int launch_event(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream);
-int launch_sweep(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_sweep(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                  const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                  int64_t ld_fin, int32_t *status, hipStream_t stream);
-int launch_walk(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
-                hipStream_t stream);
-// k_event over the scenarios a walk flagged: those on the retry list, then,
-// if the list overflowed, every scenario whose makespan holds kWalkRetry
-int launch_event_retry(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
-                       int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
-                       const int32_t *list, const int32_t *list_count, int32_t list_cap,
-                       hipStream_t stream);
-int launch_cp(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_cp(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
               const DurGen *gen = nullptr);
 // generation parameters of a call, checked (SIM_OK or SIM_E_INVAL)
@@ -258,18 +265,18 @@ int launch_put_words(int32_t *dst, const int32_t *src, int32_t count, hipStream_
 int launch_generate(const DurGen &gen, int64_t n_scen, int32_t *dur, int64_t ld, hipStream_t stream);
 // the event replay with a device model: dev is device memory of 2 n_res
 // words (gaps, then output delays); has_gap / has_delay say which apply
-int launch_event_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event_dev(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                      const uint16_t *place, int64_t ld_place, const int32_t *dev, bool has_gap,
                      bool has_delay, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
                      hipStream_t stream);
-int launch_event_gen(const sim_graph *g, int64_t n_scen, const DurGen &gen, int32_t *makespan,
+int launch_event_gen(const sim_graph *g, char *scr, int64_t n_scen, const DurGen &gen, int32_t *makespan,
                      int32_t *finish, int64_t ld_fin, int32_t *status, hipStream_t stream);
 // attribution: the event replay that also records each op's predecessor on
 // its resource, and the busy-time / binding-chain kernel over its outputs
-int launch_event_prev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_event_prev(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int32_t *prev, int64_t ld_op, int32_t *status, hipStream_t stream);
-int launch_attr(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+int launch_attr(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                 const uint16_t *place, int64_t ld_place, const int32_t *finish, const int32_t *prev,
                 int64_t ld_op, const int32_t *status, int32_t *busy, int32_t *chain, int64_t ld_res,
                 int32_t *chain_ops, hipStream_t stream);
@@ -287,9 +294,7 @@ bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
                    const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
                    std::vector<int32_t> &order);
-// sizing of persistent grids and LDS, decided once per graph
+// sizing of persistent grids and LDS, decided once per graph (and again by
+// sim_testing_replan), and the allocation of the graph's scratch sets
 int plan_scratch(sim_graph *g);
-// walk limits and sizes (walk.hip); fills the wk_* fields of g->plan except the offset
-int plan_walk(sim_graph *g, int cus);
-bool walk_eligible(const sim_graph *g);
 }  // namespace mlsim

@@ -19,7 +19,10 @@ struct sim_static {
   int gen_blocks;   // persistent grid with generated durations
   size_t lds;       // LDS bytes per block
   void *dev_mem;    // records and predecessor lists
-  uint32_t *slots;  // global value slots when they do not fit LDS
+  // global value slots when they do not fit LDS: one set, taken by each call
+  // for its launch (calls on other streams wait for it)
+  mutable ScratchPool slots;
+  bool global_slots;
 };
 
 namespace {
@@ -72,7 +75,6 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   if (!st) return SIM_E_NOMEM;
   st->n_ops = n;
   st->dev_mem = nullptr;
-  st->slots = nullptr;
   if (hipGetDevice(&st->device) != hipSuccess) {
     delete st;
     return SIM_E_HIP;
@@ -98,9 +100,7 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   // value slots in LDS when they fit, else in global scratch for the grid
   const size_t slot_bytes = (size_t)slots * kWave * 4;
   const size_t ring = 4 * sizeof(CpRec) * kCpBatch;
-  st->mode = slot_bytes <= kSlotsLdsMax ? kCpSlotsLds : kCpSlotsGlobal;
-  if (const char *e = getenv("MLSIM_CP_SLOTS"))  // test override
-    if (!strcmp(e, "global")) st->mode = kCpSlotsGlobal;
+  st->mode = slot_bytes <= kSlotsLdsMax && !g->var.cp_global ? kCpSlotsLds : kCpSlotsGlobal;
   st->lds = ring + (st->mode == kCpSlotsLds ? slot_bytes : 0);
   int blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount);
   if (blocks < 0) {
@@ -109,9 +109,14 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   }
   if (st->mode == kCpSlotsGlobal) {
     blocks = (int)std::min<size_t>((size_t)blocks, std::max<size_t>(1, kSlotsScratchBudget / slot_bytes));
-    if (hipMalloc((void **)&st->slots, slot_bytes * (size_t)blocks) != hipSuccess) {
+    auto clear = [](void *ctx, char *b) -> int {
+      return hipMemset(b, 0, *(size_t *)ctx) == hipSuccess ? SIM_OK : SIM_E_HIP;
+    };
+    size_t bytes = slot_bytes * (size_t)blocks;
+    st->global_slots = true;
+    if (int rc = st->slots.init(bytes, 1, false, clear, &bytes)) {
       sim_static_destroy(st);
-      return SIM_E_NOMEM;
+      return rc;
     }
   }
   st->blocks = std::max(1, blocks);
@@ -128,7 +133,7 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
 extern "C" void sim_static_destroy(sim_static *st) {
   if (!st) return;
   if (st->dev_mem) (void)hipFree(st->dev_mem);
-  if (st->slots) (void)hipFree(st->slots);
+  st->slots.destroy();
   delete st;
 }
 
@@ -147,8 +152,13 @@ extern "C" int sim_static_run(const sim_static *st, int64_t n_scen, const int32_
     if (status && launch_zero(status, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
+  if (!st->global_slots)
+    return launch_maxplus(st->tab, st->mode, st->blocks, st->lds, n_scen, dur, ld_dur, makespan, status,
+                          finish, ld_fin, nullptr, 0, nullptr, s);
+  Lease lease(st->slots, s);
+  if (lease.rc()) return lease.rc();
   return launch_maxplus(st->tab, st->mode, st->blocks, st->lds, n_scen, dur, ld_dur, makespan, status,
-                        finish, ld_fin, nullptr, 0, st->slots, s);
+                        finish, ld_fin, nullptr, 0, (uint32_t *)lease.base(), s);
 }
 
 extern "C" int sim_static_run_generated(const sim_static *st, int64_t n_scen, const int32_t *base,
@@ -167,6 +177,11 @@ extern "C" int sim_static_run_generated(const sim_static *st, int64_t n_scen, co
     if (status && launch_zero(status, n_scen, n_scen, 1, s) != SIM_OK) return SIM_E_HIP;
     return SIM_OK;
   }
+  if (!st->global_slots)
+    return launch_maxplus(st->tab, st->mode, st->gen_blocks, st->lds, n_scen, nullptr, 0, makespan, status,
+                          finish, ld_fin, nullptr, 0, nullptr, s, &gen);
+  Lease lease(st->slots, s);
+  if (lease.rc()) return lease.rc();
   return launch_maxplus(st->tab, st->mode, st->gen_blocks, st->lds, n_scen, nullptr, 0, makespan, status,
-                        finish, ld_fin, nullptr, 0, st->slots, s, &gen);
+                        finish, ld_fin, nullptr, 0, (uint32_t *)lease.base(), s, &gen);
 }

@@ -102,12 +102,11 @@ def test_attr_random_graphs(mlsim):
         check_attr(mlsim, ptr, idx, res, R, dur, prio=pr, place=place, path_scen=int(rng.integers(S)))
 
 
-@pytest.mark.parametrize("groups", ["1", "2"])
-def test_attr_heap_children_in_registers(mlsim, groups, monkeypatch):
+@pytest.mark.parametrize("groups", [1, 2])
+def test_attr_heap_children_in_registers(mlsim, groups, pin_variants):
     """The recording replay with the heap root's children in registers
     (chosen by the launcher when the chip is full; forced here)."""
-    monkeypatch.setenv("MLSIM_EV_REG", "1")
-    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    pin_variants(ev_reg=1, ev_lds_groups=groups)
     for k, S in ((4, 130), (2, 70), (1, 1024)):
         w = W.make_config(k, n_scen=S)
         check_attr(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), prio=w.prio,

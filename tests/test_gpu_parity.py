@@ -179,11 +179,11 @@ def test_barrier_members_interleaved(mlsim):
         check_run(mlsim, ptr, idx, res, int(res.max()) + 1, dur, prio=prio)
 
 
-@pytest.mark.parametrize("groups", ["0", "1", "4"])
-def test_heap_groups_in_lds(mlsim, groups, monkeypatch):
+@pytest.mark.parametrize("groups", [0, 1, 4, 8])
+def test_heap_groups_in_lds(mlsim, groups, pin_variants):
     """The ready heap with some of its grandchild groups in LDS (a launch
     parameter) gives the same results as the oracle."""
-    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    pin_variants(ev_lds_groups=groups)
     for k, S in ((4, 130), (5, 70), (2, 100)):
         w = W.make_config(k, n_scen=S)
         check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), place=w.placement())
@@ -195,14 +195,13 @@ def test_heap_groups_in_lds(mlsim, groups, monkeypatch):
         check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
 
 
-@pytest.mark.parametrize("groups", ["0", "1", "2", "4"])
-def test_heap_children_in_registers(mlsim, groups, monkeypatch):
+@pytest.mark.parametrize("groups", [0, 1, 2, 4])
+def test_heap_children_in_registers(mlsim, groups, pin_variants):
     """The event kernel with the heap root's children in registers (chosen
     by the launcher when the chip is full; forced here on small and ragged
     batches), with 0-4 grandchild groups in LDS, equals the oracle: plain,
     with resource gaps and with generated durations."""
-    monkeypatch.setenv("MLSIM_EV_REG", "1")
-    monkeypatch.setenv("MLSIM_EV_LDS_GROUPS", groups)
+    pin_variants(ev_reg=1, ev_lds_groups=groups)
     for k, S in ((4, 130), (2, 100), (1, 1024), (3, 70)):
         w = W.make_config(k, n_scen=S if k != 1 else None)
         dur = w.durations()
@@ -234,13 +233,13 @@ def test_heap_children_in_registers(mlsim, groups, monkeypatch):
 
 
 @pytest.mark.parametrize("slots", ["lds", "global"])
-def test_critical_path_slots(mlsim, slots, monkeypatch):
+def test_critical_path_slots(mlsim, slots, pin_variants):
     """The critical-path sweep with its value slots in LDS or in global
     scratch, on workloads and on random graphs with sources, long predecessor
     lists (more than four, read from the list) and ops without successors;
     batch counts that leave partial batches."""
     if slots == "global":
-        monkeypatch.setenv("MLSIM_CP_SLOTS", "global")
+        pin_variants(cp_global=1)
     for k, S in ((4, 130), (2, 70), (3, 200)):
         w = W.make_config(k, n_scen=S)
         check_cp(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), paths=(0, S - 1))
@@ -313,9 +312,10 @@ def test_makespan_only_matches_finish_mode(mlsim):
 # --------------------------------------------------------------- full sizes
 
 @pytest.mark.parametrize("k", [2, 3, 4, 5])
-def test_full_size_sampled(mlsim, k):
-    """Full scenario count in the benchmark's launch configuration; sampled
-    scenarios against the oracle, every scenario against the bounds."""
+def test_full_size_population(mlsim, k):
+    """Full scenario count in the benchmark's launch configuration: every
+    scenario's makespan, status and critical path against the oracle, finish
+    rows of 1024 sampled scenarios (plus the first and last)."""
     w = W.make_config(k)
     print(f"full-size {w.name} n={w.n_ops} S={w.n_scen}", flush=True)
     dur_h = w.durations()
@@ -328,22 +328,23 @@ def test_full_size_sampled(mlsim, k):
     mk, fin, st = g.run(dur, place=place, want_finish=True)
     cp, _ = g.critical_path(dur)
     torch.cuda.synchronize()
+    mk, st, cp = mk.cpu().numpy(), st.cpu().numpy(), cp.cpu().numpy()
+    print(f"  GPU done; oracle on all {w.n_scen} scenarios", flush=True)
+    omk, _, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h, place=place_h,
+                                   want_finish=False)
+    print("  oracle replay done", flush=True)
+    ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, w.n_ops, dur_h)
+    assert np.array_equal(st, ost), f"status differs in {np.count_nonzero(st != ost)} scenarios"
+    assert np.array_equal(mk, omk), f"makespan differs in {np.count_nonzero(mk != omk)} scenarios"
+    assert np.array_equal(cp, ocp), f"critical path differs in {np.count_nonzero(cp != ocp)} scenarios"
+    assert (ost == 0).all()
     rng = np.random.default_rng(k)
-    scen = np.unique(np.r_[0, w.n_scen - 1, rng.integers(0, w.n_scen, 48)])
-    omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h[:, scen],
-                                      place=None if place_h is None else place_h[:, scen])
-    ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, w.n_ops, dur_h[:, scen])
+    scen = np.unique(np.r_[0, w.n_scen - 1, rng.choice(w.n_scen, 1024, replace=False)])
+    _, ofin, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h[:, scen],
+                                  place=None if place_h is None else place_h[:, scen])
     sel = torch.from_numpy(scen).cuda()
-    assert np.array_equal(mk[sel].cpu().numpy(), omk)
-    assert np.array_equal(st[sel].cpu().numpy(), ost)
     assert np.array_equal(fin[:, sel].cpu().numpy(), ofin)
-    assert np.array_equal(cp[sel].cpu().numpy(), ocp)
-    # every scenario: valid status, cp <= makespan <= total work
-    mk_all, cp_all = mk.cpu().numpy().astype(np.int64), cp.cpu().numpy().astype(np.int64)
-    assert (st.cpu().numpy() == 0).all()
-    total = dur.to(torch.int64).sum(0).cpu().numpy()
-    assert (cp_all <= mk_all).all() and (mk_all <= total).all()
-    assert torch.equal(fin.max(0).values, mk)
+    assert torch.equal(fin.max(0).values.cpu(), torch.from_numpy(mk))
 
 
 # ------------------------------------------------------- sweep variant (a8)
@@ -456,3 +457,112 @@ def test_hip_graph_capture_replays(mlsim):
         omk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh, want_finish=False)
         assert np.array_equal(mk.cpu().numpy(), omk), f"replay {rep}"
     G.close()
+
+
+# ------------------------------------------------ pinned kernel variants
+
+def _variant_cases(mlsim):
+    for k, S in ((4, 130), (2, 100), (5, 70), (1, 1024), (3, 70)):
+        w = W.make_config(k, n_scen=S if k != 1 else None)
+        check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), place=w.placement())
+    rng = np.random.default_rng(4077)
+    for case in range(12):
+        if case < 6:
+            ptr, idx, res, prio, dur = barrier_case(rng, int(rng.integers(2, 6)), int(rng.integers(1, 6)),
+                                                    int(rng.integers(0, 12)), int(rng.integers(1, 4)),
+                                                    int(rng.choice([64, 130])), int(rng.choice([1, 3, 50])))
+            R = int(res.max()) + 1
+        else:
+            n, R = int(rng.integers(100, 400)), int(rng.integers(1, 5))
+            ptr, idx, res, prio, dur = rand_case(rng, n, R, 0.01, bool(rng.integers(2)), False, 65, 1,
+                                                 int(rng.choice([3, 1000])))
+        check_run(mlsim, ptr, idx, res, R, dur, prio=prio)
+
+
+def test_resource_times_in_global_memory(mlsim, pin_variants):
+    """The event kernel with its resource times (and the attribution's
+    last-op table) in global scratch instead of LDS equals the oracle."""
+    pin_variants(rf_global=1)
+    _variant_cases(mlsim)
+    w = W.make_config(2, n_scen=100)
+    dur = w.durations()
+    g = mlsim.Graph.from_workload(w)
+    gap = np.arange(w.n_res, dtype=np.int32) * 311
+    delay = (np.arange(w.n_res, dtype=np.int32) % 3) * 1000
+    mk, fin, _ = g.run(dev(dur), want_finish=True, gap=gap, delay=delay)
+    h = g.attribute(dev(dur))
+    torch.cuda.synchronize()
+    omk, ofin, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, gap=gap, delay=delay)
+    assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(fin.cpu().numpy(), ofin)
+    amk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur)
+    assert np.array_equal(h["makespan"].cpu().numpy(), amk)
+
+
+@pytest.mark.parametrize("cap", [1, 3])
+def test_event_grid_cap(mlsim, cap, pin_variants):
+    """A persistent grid of only 1 or 3 blocks walks every tile in turn."""
+    pin_variants(ev_blocks_cap=cap)
+    w = W.make_config(2, n_scen=64 * 7 + 5)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations())
+    w = W.make_config(5, n_scen=64 * 4 + 1)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), place=w.placement())
+
+
+# --------------------------------------------------- streams and the boundary
+
+def test_two_streams_share_one_graph(mlsim):
+    """Overlapping calls on two streams with one graph (replays with
+    different resource gaps, whose tables live in the calls' scratch sets,
+    critical paths and plain replays) each equal the oracle."""
+    w = W.make_config(2, n_scen=640)
+    g = mlsim.Graph.from_workload(w)
+    dh = [w.durations(), np.maximum(1, w.durations() // 2 + 7).astype(np.int32)]
+    d = [dev(x) for x in dh]
+    gaps = [np.full(w.n_res, 1500, np.int32), np.arange(w.n_res, dtype=np.int32) * 37]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    out = [[], []]
+    for rep in range(3):  # issue everything before waiting for anything
+        for i, s in enumerate(streams):
+            with torch.cuda.stream(s):
+                out[i].append(g.run(d[i], want_finish=True, gap=gaps[i]))
+                out[i].append(g.critical_path(d[i])[0])
+                out[i].append(g.run(d[i], want_finish=False))
+    torch.cuda.synchronize()
+    for i in range(2):
+        omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh[i], gap=gaps[i])
+        pmk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh[i], want_finish=False)
+        ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, w.n_ops, dh[i])
+        for rep in range(3):
+            mk, fin, st = out[i][3 * rep]
+            assert np.array_equal(mk.cpu().numpy(), omk), (i, rep)
+            assert np.array_equal(fin.cpu().numpy(), ofin), (i, rep)
+            assert np.array_equal(out[i][3 * rep + 1].cpu().numpy(), ocp), (i, rep)
+            assert np.array_equal(out[i][3 * rep + 2][0].cpu().numpy(), pmk), (i, rep)
+    g.close()
+
+
+def test_binding_rejects_bad_arrays(mlsim):
+    """Output and input arrays that would let a kernel read or write out of
+    bounds are rejected before the call."""
+    w = W.make_config(1, n_scen=100)
+    g = mlsim.Graph.from_workload(w)
+    d = dev(w.durations())
+    with pytest.raises(ValueError):
+        g.run(d, makespan=torch.empty(99, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):
+        g.run(d, status=torch.empty(100, dtype=torch.int64, device="cuda"))
+    with pytest.raises(TypeError):
+        g.run(d, makespan=torch.empty(100, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        g.run(d, finish=torch.empty((w.n_ops, 50), dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):  # one row expanded over every op: rows overlap
+        g.run(d[:1].expand(w.n_ops, 100))
+    with pytest.raises(ValueError):
+        g.critical_path(d, cp_len=torch.empty(10, dtype=torch.int32, device="cuda"))
+    big = torch.empty(200, dtype=torch.int32, device="cuda")  # longer outputs are fine
+    mk, _, _ = g.run(d, makespan=big)
+    torch.cuda.synchronize()
+    omk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), want_finish=False)
+    assert np.array_equal(big[:100].cpu().numpy(), omk)
+    g.close()

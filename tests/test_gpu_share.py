@@ -183,3 +183,41 @@ def test_bert_bench_launch_sampled(mlsim):
     torch.cuda.synchronize()
     assert torch.equal(mk, mk2)
     g.close()
+
+
+def test_first_call_captured_in_a_graph(mlsim):
+    """The graph's first sharing call is captured in a HIP graph (its scratch
+    exists from creation, so the call allocates nothing); every replay, with
+    new durations written between replays, equals the eager call and the
+    oracle."""
+    w = W.make_config(4, n_scen=130)
+    share = np.zeros(w.n_res, np.uint8)
+    share[W.link_resources(w)] = 1
+    G = mlsim.Graph.from_workload(w)
+    rng = np.random.default_rng(17)
+    durs = [w.durations()] + [np.maximum(1, w.durations() + rng.integers(-3000, 3000, size=(w.n_ops, 130)))
+                              .astype(np.int32) for _ in range(2)]
+    d = dev(durs[0])
+    mk = torch.empty(130, dtype=torch.int32, device="cuda")
+    st = torch.empty(130, dtype=torch.int32, device="cuda")
+    fin = torch.empty((w.n_ops, 130), dtype=torch.int32, device="cuda")
+    # the kernels' code is loaded by a call on another graph, outside the capture
+    other = mlsim.Graph.from_workload(W.make_config(1, n_scen=64))
+    other.run_share(dev(W.make_config(1, n_scen=64).durations()), [0, 0, 1])
+    torch.cuda.synchronize()
+    other.close()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        G.run_share(d, share, makespan=mk, finish=fin, status=st)
+    for rep in range(3):
+        dh = durs[rep]
+        d.copy_(torch.from_numpy(dh))
+        graph.replay()
+        torch.cuda.synchronize()
+        emk, efin, est = G.run_share(d, share, want_finish=True)
+        torch.cuda.synchronize()
+        assert torch.equal(mk, emk) and torch.equal(fin, efin) and torch.equal(st, est), rep
+        omk, ofin, ost = oracle.run_batch_share(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh, share=share)
+        assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(st.cpu().numpy(), ost), rep
+        assert np.array_equal(fin.cpu().numpy(), ofin), rep
+    G.close()

@@ -110,11 +110,11 @@ def test_static_random_orders(mlsim):
 
 
 @pytest.mark.parametrize("slots", ["lds", "global"])
-def test_static_wide_graphs(mlsim, slots, monkeypatch):
+def test_static_wide_graphs(mlsim, slots, pin_variants):
     """Wide layers keep many values live; value slots in LDS where they fit
     or in global scratch."""
     if slots == "global":
-        monkeypatch.setenv("MLSIM_CP_SLOTS", "global")
+        pin_variants(cp_global=1)
     rng = np.random.default_rng(99)
     for case in range(3):
         n = 900

@@ -1,5 +1,6 @@
 """Host-side checks of the C ABI library that need no GPU."""
 import ctypes
+import glob
 import math
 import os
 import re
@@ -14,9 +15,12 @@ HEADER = os.path.join(ROOT, "include", "mlsim.h")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(sim_\w+)\s*\(", text)))
+    """Every function declared by the headers under include/."""
+    names = set()
+    for h in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))):
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(sim_\w+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -124,3 +128,27 @@ def test_share_argument_errors_without_gpu(L):
     assert int(re.search(r"#define SIM_SHARE_MAX (\d+)", hdr).group(1)) == mlsim.SIM_SHARE_MAX
     assert int(re.search(r"#define SIM_SHARE_UNIT (\d+)", hdr).group(1)) == mlsim.SIM_SHARE_UNIT
     assert 4096 * math.lcm(*range(1, 17)) == mlsim.SIM_SHARE_UNIT < 2**32
+
+
+def test_testing_hook_rejects_bad_arguments_without_gpu(L):
+    assert L.sim_testing_replan(None, 0, 0) == mlsim.SIM_E_INVAL
+    hdr = open(os.path.join(ROOT, "include", "mlsim_testing.h")).read()
+    for name, code in mlsim.TEST_VARIANTS.items():
+        assert re.search(r"SIM_TEST_%s = %d\b" % (name.upper(), code), hdr), name
+
+
+def test_no_environment_variable_selects_library_behaviour():
+    """Kernel variants are chosen by the launch plan or pinned through the
+    testing entry point, never by the environment (a diagnostic print is the
+    one exception)."""
+    src = os.path.join(ROOT, "paper_2002_06790_amd", "csrc")
+    for f in sorted(os.listdir(src)):
+        text = open(os.path.join(src, f)).read()
+        for m in re.finditer(r"getenv\(\s*\"(\w+)\"", text):
+            assert m.group(1) == "MLSIM_VERBOSE", (f, m.group(1))
+        assert "getenv(" not in re.sub(r"getenv\(\s*\"MLSIM_VERBOSE\"\)", "", text), f
+
+
+def test_algorithm_three_is_invalid(L):
+    # the value that once selected a removed algorithm is rejected before any GPU work
+    assert L.sim_run_batch(None, 1, None, 1, None, 0, None, None, 0, None, 3, None) == mlsim.SIM_E_INVAL
