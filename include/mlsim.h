@@ -143,6 +143,33 @@ int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_
                   int64_t ld_fin, int32_t *status, uint32_t flags, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * sim_run_batch with the event algorithm, its per-block scratch taken from
+ * one fixed array in the library's static device memory instead of the
+ * graph's scratch sets.  The array holds SIM_NOALLOC_SCRATCH_BYTES per GPU
+ * (the library looks up each device's copy once, when the first graph is
+ * created on it, and every GPU the library runs on keeps it until the
+ * process ends).  The call allocates nothing and clears the part of the
+ * array it uses with a kernel before the replay.
+ *   Arguments and outputs as sim_run_batch; flags SIM_ALGO_AUTO or
+ *   SIM_ALGO_EVENT (others: SIM_E_INVAL).  Results equal sim_run_batch's.
+ *   Returns SIM_E_LIMIT when one block's scratch (the graph's bound on ready
+ *   ops, its joins and, for more resources than LDS holds, its resource
+ *   times, per lane) exceeds the array; more scenarios only take more
+ *   rounds of the persistent grid (fewer blocks run at once than in
+ *   sim_run_batch when the array is smaller than the graph's sets).
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind: calls that overlap in time on one GPU (other streams, other
+ * graphs, other threads) race and their results are undefined.  Calls on
+ * one stream are ordered.  Asynchronous on `stream`.
+ */
+#define SIM_NOALLOC_SCRATCH_BYTES (128u << 20)
+int sim_run_batch_noalloc(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                          const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                          int64_t ld_fin, int32_t *status, uint32_t flags, void *stream);
+
+/*
  * The replay with a gap per resource.  The paper attributes part of its
  * simulator's remaining error to the idle time between consecutive ops on a
  * device, which its loop does not model (Sec. 3).  Here a resource that

@@ -35,7 +35,7 @@ EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critic
            "sim_strerror", "sim_graph_info", "sim_testing_replan", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
            "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
-           "sim_run_batch_dev", "sim_run_batch_share")
+           "sim_run_batch_dev", "sim_run_batch_share", "sim_run_batch_noalloc")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -102,6 +102,8 @@ def _load():
     L.sim_run_batch_gap.restype = ctypes.c_int
     L.sim_run_batch_dev.argtypes = [P, I64, P, I64, P, I64, P, P, P, P, I64, P, U32, P]
     L.sim_run_batch_dev.restype = ctypes.c_int
+    L.sim_run_batch_noalloc.argtypes = [P, I64, P, I64, P, I64, P, P, I64, P, U32, P]
+    L.sim_run_batch_noalloc.restype = ctypes.c_int
     L.sim_run_batch_share.argtypes = [P, I64, P, I64, P, P, P, I64, P, P]
     L.sim_run_batch_share.restype = ctypes.c_int
     L.sim_static_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, P]

@@ -91,6 +91,24 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
                       status, st);
 }
 
+extern "C" int sim_run_batch_noalloc(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                                     const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                                     int64_t ld_fin, int32_t *status, uint32_t flags, void *stream) {
+  if (!g || n_scen < 0 || (flags != SIM_ALGO_AUTO && flags != SIM_ALGO_EVENT)) return SIM_E_INVAL;
+  if (n_scen == 0) return SIM_OK;
+  if (!makespan) return SIM_E_INVAL;
+  if (bad_matrix(dur, ld_dur, n_scen, g->n_ops)) return SIM_E_INVAL;
+  if (place && ld_place < n_scen) return SIM_E_INVAL;
+  if (finish && ld_fin < n_scen) return SIM_E_INVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (g->n_ops == 0) {
+    if (launch_zero(makespan, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    if (status && launch_zero(status, n_scen, n_scen, 1, st) != SIM_OK) return SIM_E_HIP;
+    return SIM_OK;
+  }
+  return launch_event_noalloc(g, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status, st);
+}
+
 extern "C" int sim_run_batch_dev(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                                  const uint16_t *place, int64_t ld_place, const int32_t *gap,
                                  const int32_t *delay, int32_t *makespan, int32_t *finish, int64_t ld_fin,

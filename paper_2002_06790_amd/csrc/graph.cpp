@@ -669,6 +669,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
 
   rc = plan_scratch(g);
   if (!rc) rc = plan_share(g);
+  if (!rc) rc = noalloc_setup(g->device);  // once per device, with it current
   if (rc) {
     sim_graph_destroy(g);
     return rc;

@@ -1227,16 +1227,27 @@ int plan_scratch(sim_graph *g) {
 }
 
 namespace {
+// Per-block scratch of the event kernel outside a graph's scratch sets: the
+// heap's global levels, join state and (when not in LDS) resource times, each
+// indexed by block, for at most max_blocks blocks.
+struct EvScratch {
+  uint64_t *heap;
+  int2 *join;
+  uint32_t *rf;
+  int64_t max_blocks;
+};
+
 int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
                       const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
                       int64_t ld_fin, int32_t *status, int32_t *prev, hipStream_t stream,
                       const DurGen *gen = nullptr, const int32_t *dev = nullptr, bool has_gap = false,
-                      bool has_delay = false) {
+                      bool has_delay = false, const EvScratch *ext = nullptr) {
   const ScratchPlan &P = g->plan;
   EvArgs a{n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
-           (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
-           (int2 *)(base + g->scratch_ev_join_off), (uint32_t *)(base + g->scratch_ev_rf_off),
-           prev, (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, dev, has_gap, has_delay, 0};
+           ext ? ext->heap : (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
+           ext ? ext->join : (int2 *)(base + g->scratch_ev_join_off),
+           ext ? ext->rf : (uint32_t *)(base + g->scratch_ev_rf_off),
+           prev, ext ? nullptr : (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, dev, has_gap, has_delay, 0};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = P.rf_lds;
@@ -1248,11 +1259,12 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
   const int64_t lds_blocks = prev ? P.ev_prev_blocks : gen ? P.ev_gen_blocks : dev ? P.ev_dev_blocks : P.ev_blocks;
   bool reg = P.ev_reg && !place && tiles >= 2 * lds_blocks;
   if (g->var.ev_reg >= 0) reg = P.ev_reg && !place && g->var.ev_reg != 0;
-  const int64_t blocks = !reg ? lds_blocks
-                         : prev ? P.ev_reg_prev_blocks
-                         : gen  ? P.ev_reg_gen_blocks
-                         : dev  ? P.ev_reg_dev_blocks
-                                : P.ev_reg_blocks;
+  int64_t blocks = !reg ? lds_blocks
+                   : prev ? P.ev_reg_prev_blocks
+                   : gen  ? P.ev_reg_gen_blocks
+                   : dev  ? P.ev_reg_dev_blocks
+                          : P.ev_reg_blocks;
+  if (ext) blocks = std::min(blocks, ext->max_blocks);
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
@@ -1395,6 +1407,77 @@ int launch_event_prev(const sim_graph *g, char *scr, int64_t n_scen, const int32
                       int32_t *prev, int64_t ld_op, int32_t *status, hipStream_t stream) {
   return launch_event_impl(g, scr, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_op,
                            status, prev, stream);
+}
+
+// Scratch of the replay variant that allocates nothing
+// (sim_run_batch_noalloc): one array per GPU in the code object's static
+// device memory, held by each GPU the library runs on until the process
+// ends.  In host code `scratch` is a stand-in for the symbol, not a device
+// address: every host use goes through the address hipGetSymbolAddress
+// returned for the device (noalloc_setup), never through the name.
+constexpr size_t kNoAllocBytes = (size_t)SIM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kNoAllocBytes];
+
+namespace {
+std::mutex g_noalloc_mu;
+std::vector<char *> g_noalloc_ptr;  // per device: the array's address, null until looked up
+
+// p[i] = v for i < n (a kernel rather than a memset, so the call can be
+// captured in a graph)
+__global__ __launch_bounds__(256) void k_fill_words(uint32_t *p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = v;
+}
+
+int fill_words(uint32_t *p, int64_t n, uint32_t v, hipStream_t stream) {
+  if (n <= 0) return SIM_OK;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  k_fill_words<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(p, n, v);
+  return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
+}
+
+size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+}  // namespace
+
+int noalloc_setup(int device) {
+  std::lock_guard<std::mutex> lk(g_noalloc_mu);
+  if (device < 0) return SIM_E_HIP;
+  if ((size_t)device >= g_noalloc_ptr.size()) g_noalloc_ptr.resize((size_t)device + 1, nullptr);
+  if (g_noalloc_ptr[device]) return SIM_OK;
+  void *p = nullptr;  // with `device` current (the caller's)
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SIM_E_HIP;
+  g_noalloc_ptr[device] = (char *)p;
+  return SIM_OK;
+}
+
+int launch_event_noalloc(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                         int64_t ld_fin, int32_t *status, hipStream_t stream) {
+  char *base = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_noalloc_mu);
+    if ((size_t)g->device < g_noalloc_ptr.size()) base = g_noalloc_ptr[g->device];
+  }
+  if (!base) return SIM_E_HIP;
+  const ScratchPlan &P = g->plan;
+  const DevGraph &G = g->dg;
+  // one block's region: heap levels in global memory, join state, resource
+  // times when they are not in LDS
+  const size_t heap_b = (size_t)P.ev_heap_stride * kWave * 8, join_b = (size_t)G.J * kWave * 8;
+  const size_t rf_b = P.rf_lds ? 0 : (size_t)G.R * kWave * 4;
+  const size_t per_block = round256(heap_b) + round256(join_b) + round256(rf_b);
+  if (per_block > kNoAllocBytes) return SIM_E_LIMIT;
+  const int64_t cap = (int64_t)(kNoAllocBytes / per_block);
+  const int64_t tiles = (n_scen + kWave - 1) / kWave;
+  const int64_t used = std::min(cap, tiles);  // the grid never exceeds the tiles
+  EvScratch ext{(uint64_t *)base, (int2 *)(base + (size_t)cap * round256(heap_b)),
+                (uint32_t *)(base + (size_t)cap * (round256(heap_b) + round256(join_b))), cap};
+  // the previous call may have used another layout: heap positions start
+  // empty (all ones) and join state cleared, for every block this call runs
+  if (int rc = fill_words((uint32_t *)ext.heap, (int64_t)(used * round256(heap_b) / 4), 0xffffffffu, stream))
+    return rc;
+  if (int rc = fill_words((uint32_t *)ext.join, (int64_t)(used * round256(join_b) / 4), 0u, stream)) return rc;
+  return launch_event_impl(g, nullptr, n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin, status,
+                           nullptr, stream, nullptr, nullptr, false, false, &ext);
 }
 
 int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen) {

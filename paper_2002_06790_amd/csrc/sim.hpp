@@ -294,6 +294,13 @@ bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
                    const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
                    std::vector<int32_t> &order);
+// the replay variant that allocates nothing: the address of the static
+// scratch array on the current device, looked up once per device (at graph
+// creation), and the launch on it
+int noalloc_setup(int device);
+int launch_event_noalloc(const sim_graph *g, int64_t n_scen, const int32_t *dur, int64_t ld_dur,
+                         const uint16_t *place, int64_t ld_place, int32_t *makespan, int32_t *finish,
+                         int64_t ld_fin, int32_t *status, hipStream_t stream);
 // sizing of persistent grids and LDS, decided once per graph (and again by
 // sim_testing_replan), and the allocation of the graph's scratch sets
 int plan_scratch(sim_graph *g);
