@@ -102,6 +102,22 @@ def config_line(k, args, torch, mlsim, workloads):
         if i >= args.warmup:
             ev_ms.append(e0.elapsed_time(e1))
             cp_ms.append(e1.elapsed_time(e2))
+    # the sweep variant on the workloads with wide frontiers it is meant for
+    # (every scenario; its makespans must equal the event replay's)
+    sweep = None
+    if k in (1, 3):
+        smk = torch.empty(S, dtype=torch.int32, device="cuda")
+        g.run(dur, place=place, makespan=smk, algo="sweep")
+        torch.cuda.synchronize()
+        sw_ms = []
+        for _ in range(3):
+            e0.record()
+            g.run(dur, place=place, makespan=smk, algo="sweep")
+            e1.record()
+            e1.synchronize()
+            sw_ms.append(e0.elapsed_time(e1))
+        sweep = {"sweep_ms": float(np.median(sw_ms)), "sweep_equals_event": bool(torch.equal(smk, mk)),
+                 "sweep_op_events_per_s": n * S / (float(np.median(sw_ms)) / 1e3)}
     threads = cpu_threads()
     t = time.perf_counter()
     omk, ofin, ost = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur_h, place=place_h,
@@ -118,6 +134,10 @@ def config_line(k, args, torch, mlsim, workloads):
            "scenarios_per_s": S / ((ev + float(np.median(cp_ms))) / 1e3),
            "run_batch_hbm_frac": alg / (ev / 1e3) / 1e9 / PEAK_HBM_GBS,
            "cpu_oracle_op_events_per_s": n * S / cpu_s, "cpu_threads": threads, "parity": parity}
+    if sweep:
+        out.update(sweep)
+        log(f"  sweep variant {sweep['sweep_ms']:.3f} ms ({sweep['sweep_op_events_per_s']:.3e} op-events/s, "
+            f"CPU oracle {n * S / cpu_s:.3e}); equal to the event replay: {sweep['sweep_equals_event']}")
     del g, dur, fin, place
     torch.cuda.empty_cache()
     return out

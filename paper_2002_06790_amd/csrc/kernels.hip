@@ -626,7 +626,7 @@ struct MpArgs {
 // Each op reads one coalesced duration row (and with FIN writes one finish
 // row); dist of ops that still have unvisited successors lives in value
 // slots.  Software pipeline: while batch t is swept, the duration rows of
-// batches t + 1 and t + 2 and the records of batch t + 3 are in flight.  A
+// batches t + 1 .. t + 3 and the records of batch t + 4 are in flight.  A
 // batch's records arrive in registers (lane i holds words i and 64 + i) and
 // are parked in a four-batch LDS ring; reading a batch back gives its row
 // numbers (for its loads) and its fields (for its sweep) by readlane.  MODE:
@@ -725,31 +725,37 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
       }
 #undef CP_FIELD
     };
-    // One pipeline step: batch t + 2's records (loaded during step t - 1,
-    // before batch t + 1's rows) go to the ring, batch t + 3's records and
-    // batch t + 2's rows go out, then batch t is swept.  Loads complete in
-    // issue order, so waiting for the records leaves batch t + 1's rows in
-    // flight, and waiting for batch t's rows leaves t + 1's and t + 2's.
-    auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&ahead2)[kCpBatch]) {
-      stage_recs(t + 2);
-      load_recs(t + 3);
-      load_rows(t + 2, ahead2);
+    // One pipeline step: batch t + 3's records (loaded during step t - 1,
+    // before batch t + 2's rows) go to the ring, batch t + 4's records and
+    // batch t + 3's rows go out, then batch t is swept.  Loads complete in
+    // issue order, so waiting for the records leaves batch t + 2's rows in
+    // flight, and waiting for batch t's rows leaves those of t + 1 .. t + 3
+    // (48 row loads and a record pair: within the 63 loads a wave can count).
+    auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&ahead3)[kCpBatch]) {
+      stage_recs(t + 3);
+      load_recs(t + 4);
+      load_rows(t + 3, ahead3);
       sweep(t, cur);
     };
-    int32_t da[kCpBatch], db[kCpBatch], dc[kCpBatch];
+    int32_t da[kCpBatch], db[kCpBatch], dc[kCpBatch], dd[kCpBatch];
     load_recs(0);
     stage_recs(0);
     load_recs(1);
     stage_recs(1);
-    load_rows(0, da);
     load_recs(2);
+    stage_recs(2);
+    load_rows(0, da);
     load_rows(1, db);
-    for (int t = 0; t < nbat; t += 3) {
-      step(t, da, dc);
+    load_recs(3);
+    load_rows(2, dc);
+    for (int t = 0; t < nbat; t += 4) {
+      step(t, da, dd);
       if (t + 1 >= nbat) break;
       step(t + 1, db, da);
       if (t + 2 >= nbat) break;
       step(t + 2, dc, db);
+      if (t + 3 >= nbat) break;
+      step(t + 3, dd, dc);
     }
     const int32_t st = bad_dur ? SIM_ST_BAD_DUR : ovf ? SIM_ST_OVERFLOW : 0;
     if (active) {

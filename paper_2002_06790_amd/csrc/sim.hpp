@@ -45,7 +45,7 @@ struct OpRec {
 // batches of kCpBatch plus kCpBatch * kCpAhead more, so a sweep can read
 // records and rows ahead without bounds checks.
 constexpr int kCpBatch = 16;  // ops per batch of the sweep
-constexpr int kCpAhead = 3;   // batches of records read ahead
+constexpr int kCpAhead = 4;   // batches of records read ahead
 constexpr int kCpSlotsGlobal = 0, kCpSlotsLds = 1;  // where the sweep's value slots live
 constexpr int kMpOutNone = 0, kMpOutFinish = 1, kMpOutDist = 2;  // what else the sweep writes
 struct CpRec {
