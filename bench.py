@@ -487,8 +487,10 @@ def main():
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled)",
                      "kernel": "k_event (sim_run_batch)",
                      "bytes_per_launch": alg_bytes,
-                     "limiter": "latency of each lane's dependent divergent loads (the roofline is HBM; "
-                                "the kernel moves far less than HBM peak)"},
+                     "limiter": "the CUs' vector memory address path: every step issues about 6.4 "
+                                "lane-divergent loads and stores (record, duration, heap levels beyond LDS, "
+                                "join state, finish bursts) and the TA units are busy 74% of the launch "
+                                "(profiles/); the roofline axis is HBM bytes, which the kernel does not reach"},
         "cpu_baseline": cpu,
         "parity": parity,
         "per_config": per_config,

@@ -566,3 +566,46 @@ def test_binding_rejects_bad_arrays(mlsim):
     omk, _, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), want_finish=False)
     assert np.array_equal(big[:100].cpu().numpy(), omk)
     g.close()
+
+
+def test_threads_share_one_graph(mlsim):
+    """Four host threads, each with its own stream, call one graph at once
+    (the calls take scratch sets under the graph's lock); every result
+    equals the oracle."""
+    import threading
+    w = W.make_config(3, n_scen=256)
+    g = mlsim.Graph.from_workload(w)
+    dh = [np.maximum(1, w.durations() // (i + 1)).astype(np.int32) for i in range(4)]
+    d = [dev(x) for x in dh]
+    torch.cuda.synchronize()
+    out, errors = [None] * 4, []
+
+    def work(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                res = []
+                for _ in range(5):
+                    res.append(g.run(d[i], want_finish=True, gap=np.full(w.n_res, 100 * i, np.int32)))
+                    res.append(g.critical_path(d[i])[0])
+            s.synchronize()
+            out[i] = res
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    ts = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(4):
+        omk, ofin, _ = oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dh[i],
+                                        gap=np.full(w.n_res, 100 * i, np.int32))
+        ocp, _ = oracle.critical_path(w.succ_ptr, w.succ_idx, w.n_ops, dh[i])
+        for rep in range(5):
+            mk, fin, _ = out[i][2 * rep]
+            assert np.array_equal(mk.cpu().numpy(), omk) and np.array_equal(fin.cpu().numpy(), ofin), (i, rep)
+            assert np.array_equal(out[i][2 * rep + 1].cpu().numpy(), ocp), (i, rep)
+    g.close()
