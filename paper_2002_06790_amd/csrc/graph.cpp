@@ -36,7 +36,7 @@ struct Compiled {
   std::vector<int32_t> ev_rec16;  // [n][4] compact event records (ev_compact)
   std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
-  int32_t J = 0, heap_cap = 0, cp_slots = 0, max_indeg = 0, levels = 0, barriers = 0;
+  int32_t J = 0, heap_cap = 0, cp_slots = 0, cp_n = 0, max_indeg = 0, levels = 0, barriers = 0;
   int64_t m = 0;
 };
 
@@ -447,7 +447,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
 
   // critical-path sweep
   std::vector<int32_t> order;
-  build_maxplus(n, cs, cp, orig_of, C.cp, C.cp_pred, C.cp_slots, order);
+  build_maxplus(n, cs, cp, orig_of, C.cp, C.cp_pred, C.cp_slots, order, C.cp_n);
 
   // compact predecessor CSR (for the sweep variant) and level count
   C.pred_ptr.assign(n + 1, 0);
@@ -487,30 +487,70 @@ namespace mlsim {
 bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
                    const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
-                   std::vector<int32_t> &order) {
-  // the topological order (depth- or breadth-first flavour) that needs fewer
-  // live value slots
-  std::vector<int32_t> o1, o2, s1, s2;
-  if (!kahn(n, succ, true, o1) || !kahn(n, succ, false, o2)) return false;
-  const int32_t n1 = assign_cp_slots(n, succ, pred, o1, s1);
-  const int32_t n2 = assign_cp_slots(n, succ, pred, o2, s2);
-  order = n1 <= n2 ? o1 : o2;
-  const auto &slot = n1 <= n2 ? s1 : s2;
+                   std::vector<int32_t> &order, int32_t &n_sweep) {
+  // A second candidate table: one barrier node for each predecessor set of
+  // two or more ops that two or more ops share.  Its dist is the max over the
+  // set (duration 0), and each op sharing the set takes the barrier as its
+  // only predecessor: the same dist for every op, and the set's values are
+  // dead once the barrier has read them.
+  std::map<std::vector<int32_t>, std::vector<int32_t>> sets;
+  for (int32_t v = 0; v < n; ++v)
+    if (pred[v].size() >= 2) {
+      std::vector<int32_t> key = pred[v];
+      std::sort(key.begin(), key.end());
+      sets[key].push_back(v);
+    }
+  std::vector<std::vector<int32_t>> fpred(pred), fsucc;
+  for (const auto &kv : sets) {
+    if (kv.second.size() < 2) continue;
+    const int32_t b = (int32_t)fpred.size();
+    fpred.push_back(kv.first);
+    for (int32_t v : kv.second) fpred[v].assign(1, b);
+  }
+  const int32_t nf = (int32_t)fpred.size();
+  fsucc.resize(nf);
+  for (int32_t v = 0; v < nf; ++v)
+    for (int32_t p : fpred[v]) fsucc[p].push_back(v);
+  // the candidate (graph, depth- or breadth-first order) that needs the
+  // fewest live value slots; ties keep the table without barriers
+  struct Cand {
+    int32_t nodes;
+    const std::vector<std::vector<int32_t>> *succ, *pred;
+    std::vector<int32_t> order, slot;
+    int32_t live;
+  };
+  std::vector<Cand> cand;
+  for (int f = 0; f < (nf > n ? 2 : 1); ++f)
+    for (int lifo = 1; lifo >= 0; --lifo) {
+      Cand c{f ? nf : n, f ? &fsucc : &succ, f ? &fpred : &pred, {}, {}, 0};
+      if (!kahn(c.nodes, *c.succ, lifo != 0, c.order)) return false;
+      c.live = assign_cp_slots(c.nodes, *c.succ, *c.pred, c.order, c.slot);
+      cand.push_back(std::move(c));
+    }
+  size_t pick = 0;
+  for (size_t i = 1; i < cand.size(); ++i)
+    if (cand[i].live < cand[pick].live) pick = i;
+  const Cand &C = cand[pick];
+  const auto &P = *C.pred;
+  order.clear();
+  for (int32_t v : C.order)
+    if (v < n) order.push_back(v);  // still topological for the ops themselves
+  n_sweep = C.nodes;
   // two more slots: one that always holds 0 (unused inline predecessors
   // read it) and one that ops without successors write (never read)
-  slots = std::min(n1, n2) + 2;
+  slots = C.live + 2;
   const int32_t zslot = slots - 2, sink = slots - 1;
-  const int32_t pad = (n + kCpBatch - 1) / kCpBatch * kCpBatch + kCpBatch * kCpAhead;
+  const int32_t pad = (C.nodes + kCpBatch - 1) / kCpBatch * kCpBatch + kCpBatch * kCpAhead;
   rec.assign(pad, CpRec{n ? row_of[0] : 0, sink, 0, 0, {zslot, zslot, zslot, zslot}});
   plist.clear();
-  for (int32_t k = 0; k < n; ++k) {
-    const int32_t v = order[k];
-    CpRec r{row_of[v], slot[v] >= 0 ? slot[v] : sink, (int32_t)pred[v].size(), (int32_t)plist.size(),
-            {zslot, zslot, zslot, zslot}};
-    if (pred[v].size() <= 4)
-      for (size_t e = 0; e < pred[v].size(); ++e) r.p[e] = slot[pred[v][e]];
+  for (int32_t k = 0; k < C.nodes; ++k) {
+    const int32_t v = C.order[k];
+    CpRec r{v < n ? row_of[v] : -1, C.slot[v] >= 0 ? C.slot[v] : sink, (int32_t)P[v].size(),
+            (int32_t)plist.size(), {zslot, zslot, zslot, zslot}};
+    if (P[v].size() <= 4)
+      for (size_t e = 0; e < P[v].size(); ++e) r.p[e] = C.slot[P[v][e]];
     else
-      for (int32_t p : pred[v]) plist.push_back(slot[p]);
+      for (int32_t p : P[v]) plist.push_back(C.slot[p]);
     rec[k] = r;
   }
   if (plist.empty()) plist.push_back(0);
@@ -625,6 +665,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.nsrc = (int32_t)C.src.size();
   d.heap_cap = C.heap_cap;
   d.cp_slots = C.cp_slots;
+  d.cp_n = C.cp_n;
   d.max_indeg = C.max_indeg;
   d.ops = (const OpRec *)(base + o_ops);
   d.succ = (const int32_t *)(base + o_succ);

@@ -620,22 +620,25 @@ struct MpArgs {
 
 // Max-plus sweep, one scenario per lane: dist(v) = d(v) + max over v's
 // predecessors in the table of their dist, in one topological order shared by
-// the whole wave, in batches of kCpBatch ops.  With the DAG's predecessors
+// the whole wave, in batches of kCpBatch records.  With the DAG's predecessors
 // this is the longest path (critical path); with each op's previous op on its
 // device added it is the static-order replay, whose dist is the finish time.
-// Each op reads one coalesced duration row (and with FIN writes one finish
-// row); dist of ops that still have unvisited successors lives in value
-// slots.  Software pipeline: while batch t is swept, the duration rows of
-// batches t + 1 .. t + 3 and the records of batch t + 4 are in flight.  A
-// batch's records arrive in registers (lane i holds words i and 64 + i) and
-// are parked in a four-batch LDS ring; reading a batch back gives its row
-// numbers (for its loads) and its fields (for its sweep) by readlane.  MODE:
-// where the value slots live (kCpSlotsLds or kCpSlotsGlobal); OUT: what
-// besides the per-scenario result is written (kMpOutFinish: every op's dist
-// as finish rows; kMpOutDist: every op's dist for one scenario).  GEN: a
-// batch's "rows" are base durations of the lane's knob, and the sweep turns
-// them into durations with the counter-based noise of a.gen.
-template <int MODE, int OUT, bool GEN = false>
+// A record is an op or a barrier node (row -1: duration 0, so its dist is the
+// max over a predecessor set that several ops share, and those ops read it
+// instead of the whole set).  Each op reads one coalesced duration row (and
+// with FIN writes one finish row); dist of records that still have unvisited
+// successors lives in value slots.  Software pipeline: while batch t is
+// swept, the duration rows of batches t + 1 .. t + 3 and the records of batch
+// t + 4 are in flight.  A batch's records arrive in two registers (lane i
+// holds words i and 64 + i) and stay there until the batch is swept; a field
+// is read by readlane, first the rows (for the batch's loads), later the rest
+// (for its sweep).  MODE: where the value slots live (kCpSlotsLds or
+// kCpSlotsGlobal); OUT: what besides the per-scenario result is written
+// (kMpOutFinish: every op's dist as finish rows; kMpOutDist: every op's dist
+// for one scenario).  GEN: a batch's "rows" are base durations of the lane's
+// knob, and the sweep turns them into durations with the counter-based noise
+// of a.gen.  BAR: the table holds barrier records.
+template <int MODE, int OUT, bool GEN, bool BAR>
 __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   extern __shared__ uint32_t lds32[];
   const int lane = threadIdx.x;
@@ -643,10 +646,10 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
   constexpr int kRecWords = (int)(sizeof(CpRec) / 4);  // 8
   constexpr int kBatchWords = kCpBatch * kRecWords;    // 128: two words per lane
   static_assert(kBatchWords == 2 * kWave, "a batch of records is two words per lane");
+  static_assert(kCpAhead == 4, "the pipeline below holds records four batches ahead");
   const int32_t *recw = (const int32_t *)T.rec;
   const cptr<int32_t> cp_pred = as_const(T.pred);
-  int32_t *ring = (int32_t *)lds32;  // [4][kBatchWords]
-  uint32_t *slots = MODE == kCpSlotsLds ? lds32 + 4 * kBatchWords + lane
+  uint32_t *slots = MODE == kCpSlotsLds ? lds32 + lane
                                         : a.slots_g + (size_t)blockIdx.x * T.slots * kWave + lane;
   auto sget = [&](int i) -> uint32_t { return slots[(size_t)i * kWave]; };
   auto sset = [&](int i, uint32_t x) { slots[(size_t)i * kWave] = x; };
@@ -660,36 +663,36 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
     const int64_t S = GEN ? a.gen.scen0 + sc : 0;  // global scenario index of the generator
     const int32_t *brow = GEN ? gen_knob_row(a.gen, S) : nullptr;
     const uint32_t s_lo = (uint32_t)S, s_hi = (uint32_t)((uint64_t)S >> 32);
+    // The scenario is flagged at the end of its tile: a duration below 1
+    // makes dmin < 1; a dist above INT32_MAX makes mx > INT32_MAX (the first
+    // such dist is a sum of two terms <= INT32_MAX, so it does not wrap, and
+    // mx never decreases).  A flagged scenario's dist values are unspecified,
+    // so nothing is clamped on the way.
     uint32_t mx = 0;
-    bool bad_dur = false, ovf = false;
-    int32_t rx0, rx1;  // records of one batch in flight
-    auto load_recs = [&](int t) {
-      rx0 = recw[(size_t)t * kBatchWords + lane];
-      rx1 = recw[(size_t)t * kBatchWords + kWave + lane];
+    int32_t dmin = 1;
+    struct Recs {
+      int32_t w0, w1;  // lane i: words i and 64 + i of a batch's records
     };
-    auto stage_recs = [&](int t) {
-      ring[(t & 3) * kBatchWords + lane] = rx0;
-      ring[(t & 3) * kBatchWords + kWave + lane] = rx1;
+    auto load_recs = [&](int t) -> Recs {
+      return Recs{recw[(size_t)t * kBatchWords + lane], recw[(size_t)t * kBatchWords + kWave + lane]};
     };
-    // rows of batch t, whose records are in the ring
-    auto load_rows = [&](int t, int32_t (&dv)[kCpBatch]) {
-      const int32_t y0 = ring[(t & 3) * kBatchWords + lane];
-      const int32_t y1 = ring[(t & 3) * kBatchWords + kWave + lane];
+    // rows of one batch (a barrier's row -1 reads row 0, which its sweep ignores)
+    auto load_rows = [&](const Recs &r, int32_t (&dv)[kCpBatch]) {
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
         const int w = u * kRecWords;  // word of the batch holding the row
-        const uint32_t row = (uint32_t)__builtin_amdgcn_readlane(w < kWave ? y0 : y1, w & (kWave - 1));
-        dv[u] = GEN ? brow[row] : a.dur[(uint64_t)row * (uint64_t)a.ld_dur + sc];  // rows are never negative
+        const int32_t row = __builtin_amdgcn_readlane(w < kWave ? r.w0 : r.w1, w & (kWave - 1));
+        const uint32_t rr = BAR && row < 0 ? 0u : (uint32_t)row;
+        dv[u] = GEN ? brow[rr] : a.dur[(uint64_t)rr * (uint64_t)a.ld_dur + sc];
       }
     };
-    auto sweep = [&](int t, const int32_t (&dv)[kCpBatch]) {
-      // the batch's records back in registers (lane i: words i and 64 + i), fields by readlane
-      const int32_t y0 = ring[(t & 3) * kBatchWords + lane];
-      const int32_t y1 = ring[(t & 3) * kBatchWords + kWave + lane];
-#define CP_FIELD(u, f) __builtin_amdgcn_readlane(((u) * kRecWords + (f)) < kWave ? y0 : y1, ((u) * kRecWords + (f)) & (kWave - 1))
+    auto sweep = [&](int t, const Recs &r, const int32_t (&dv)[kCpBatch]) {
+#define CP_FIELD(u, f) __builtin_amdgcn_readlane(((u) * kRecWords + (f)) < kWave ? r.w0 : r.w1, ((u) * kRecWords + (f)) & (kWave - 1))
 #pragma unroll
       for (int u = 0; u < kCpBatch; ++u) {
-        if (t * kCpBatch + u >= n) break;
+        // padding records (row of op 0, no predecessors, the sink slot) are
+        // harmless to sweep unless they would write op 0's row
+        if (OUT != kMpOutNone && t * kCpBatch + u >= n) break;
         const int np = CP_FIELD(u, 2);
         uint32_t best;
         if (__builtin_expect(np <= 4, 1)) {  // unused entries name the slot that holds 0
@@ -707,47 +710,48 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
             best = x > best ? x : best;
           }
         }
+        // A barrier's row -1 read op 0's durations (row 0, and op 0's noise
+        // counter when generated), so dmin sees nothing that op 0 does not;
+        // then a barrier adds 0 and writes no row.  No branch: a barrier's
+        // dist never exceeds mx, the max of its predecessors' dist.
+        const int32_t row = BAR || GEN || OUT != kMpOutNone ? CP_FIELD(u, 0) : 0;
+        const int32_t keep = BAR ? ~(row >> 31) : -1;  // all ones for an op, 0 for a barrier
         int32_t d = dv[u];
-        if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)CP_FIELD(u, 0), a.gen.key0, a.gen.key1, a.gen.noise);
-        if (d < 1) {
-          bad_dur = true;
-          d = 1;
-        }
-        uint32_t dist = best + (uint32_t)d;  // both terms <= INT32_MAX: no uint32 wrap
-        if (dist > kI32Max) {
-          ovf = true;
-          dist = kI32Max;
-        }
+        if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)(row & keep), a.gen.key0, a.gen.key1, a.gen.noise);
+        dmin = d < dmin ? d : dmin;
+        const uint32_t dist = best + (uint32_t)(d & keep);
         sset(CP_FIELD(u, 1), dist);
         mx = dist > mx ? dist : mx;
-        if (OUT == kMpOutFinish && active) a.finish[(int64_t)CP_FIELD(u, 0) * a.ld_fin + s] = (int32_t)dist;
-        if (OUT == kMpOutDist && want_dist) a.dist_out[CP_FIELD(u, 0)] = (int32_t)dist;
+        if (OUT == kMpOutFinish && active && keep) a.finish[(int64_t)row * a.ld_fin + s] = (int32_t)dist;
+        if (OUT == kMpOutDist && want_dist && keep) a.dist_out[row] = (int32_t)dist;
       }
 #undef CP_FIELD
     };
-    // One pipeline step: batch t + 3's records (loaded during step t - 1,
-    // before batch t + 2's rows) go to the ring, batch t + 4's records and
-    // batch t + 3's rows go out, then batch t is swept.  Loads complete in
-    // issue order, so waiting for the records leaves batch t + 2's rows in
-    // flight, and waiting for batch t's rows leaves those of t + 1 .. t + 3
-    // (48 row loads and a record pair: within the 63 loads a wave can count).
+    // One pipeline step: the records of batch t + 3 (loaded during step
+    // t - 1, before batch t + 2's rows) give batch t + 3's rows; batch t + 4's
+    // records go out; then batch t is swept.  Loads complete in issue order,
+    // so waiting for the records leaves batch t + 2's rows in flight, and
+    // waiting for batch t's rows leaves those of t + 1 .. t + 3 (48 row loads
+    // and a record pair: within the 63 loads a wave can count).  r0 .. r2
+    // hold the records of batches t .. t + 2, rx those of t + 3.
+    Recs r0, r1, r2, rx;
     auto step = [&](int t, const int32_t (&cur)[kCpBatch], int32_t (&ahead3)[kCpBatch]) {
-      stage_recs(t + 3);
-      load_recs(t + 4);
-      load_rows(t + 3, ahead3);
-      sweep(t, cur);
+      const Recs r3 = rx;
+      rx = load_recs(t + 4);
+      load_rows(r3, ahead3);
+      sweep(t, r0, cur);
+      r0 = r1;
+      r1 = r2;
+      r2 = r3;
     };
     int32_t da[kCpBatch], db[kCpBatch], dc[kCpBatch], dd[kCpBatch];
-    load_recs(0);
-    stage_recs(0);
-    load_recs(1);
-    stage_recs(1);
-    load_recs(2);
-    stage_recs(2);
-    load_rows(0, da);
-    load_rows(1, db);
-    load_recs(3);
-    load_rows(2, dc);
+    r0 = load_recs(0);
+    r1 = load_recs(1);
+    r2 = load_recs(2);
+    load_rows(r0, da);
+    load_rows(r1, db);
+    rx = load_recs(3);
+    load_rows(r2, dc);
     for (int t = 0; t < nbat; t += 4) {
       step(t, da, dd);
       if (t + 1 >= nbat) break;
@@ -757,7 +761,7 @@ __global__ __launch_bounds__(kWave) void k_maxplus(MpTable T, MpArgs a) {
       if (t + 3 >= nbat) break;
       step(t + 3, dd, dc);
     }
-    const int32_t st = bad_dur ? SIM_ST_BAD_DUR : ovf ? SIM_ST_OVERFLOW : 0;
+    const int32_t st = dmin < 1 ? SIM_ST_BAD_DUR : mx > kI32Max ? SIM_ST_OVERFLOW : 0;
     if (active) {
       a.out[s] = st ? -1 : (int32_t)mx;
       if (a.status) a.status[s] = st;
@@ -1169,11 +1173,11 @@ int plan_scratch(sim_graph *g) {
 
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
-  const size_t cp_ring = 4 * sizeof(CpRec) * kCpBatch;  // record ring
   P.cp_mode = cp_bytes <= 32 * 1024 && !V.cp_global ? kCpSlotsLds : kCpSlotsGlobal;
-  P.cp_lds_bytes = cp_ring + (P.cp_mode == kCpSlotsLds ? cp_bytes : 0);
-  const int cp_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus);
-  const int cp_gen_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus, true);
+  P.cp_lds_bytes = P.cp_mode == kCpSlotsLds ? cp_bytes : 0;
+  const bool cp_bar = G.cp_n > G.n;
+  const int cp_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus, false, cp_bar);
+  const int cp_gen_occ = maxplus_occupancy(P.cp_mode, false, P.cp_lds_bytes, cus, true, cp_bar);
   if (cp_occ < 0 || cp_gen_occ < 0) return SIM_E_HIP;
   size_t cp_blocks = (size_t)cp_occ;
   if (P.cp_mode == kCpSlotsGlobal && cp_bytes)
@@ -1486,44 +1490,49 @@ int launch_event_noalloc(const sim_graph *g, int64_t n_scen, const int32_t *dur,
                            nullptr, stream, nullptr, nullptr, false, false, &ext);
 }
 
-int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen) {
-  if (gen) {
-    if (mode == kCpSlotsLds)
-      return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutFinish, true>, lds, cus)
-                 : occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutNone, true>, lds, cus);
-    return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutFinish, true>, lds, cus)
-               : occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutNone, true>, lds, cus);
+namespace {
+
+using MpKernel = void (*)(MpTable, MpArgs);
+
+template <int M, int O>
+MpKernel mp_kernel_of(bool gen, bool bar) {
+  if (gen) return bar ? k_maxplus<M, O, true, true> : k_maxplus<M, O, true, false>;
+  return bar ? k_maxplus<M, O, false, true> : k_maxplus<M, O, false, false>;
+}
+
+// the sweep instance for a slot placement, what it writes, generated
+// durations and whether the table holds barrier records
+MpKernel mp_kernel(int mode, int out, bool gen, bool bar) {
+  if (mode == kCpSlotsLds) {
+    if (out == kMpOutFinish) return mp_kernel_of<kCpSlotsLds, kMpOutFinish>(gen, bar);
+    if (out == kMpOutDist) return mp_kernel_of<kCpSlotsLds, kMpOutDist>(gen, bar);
+    return mp_kernel_of<kCpSlotsLds, kMpOutNone>(gen, bar);
   }
-  if (mode == kCpSlotsLds)
-    return fin ? occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutFinish>, lds, cus)
-               : occupancy_blocks(k_maxplus<kCpSlotsLds, kMpOutNone>, lds, cus);
-  return fin ? occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutFinish>, lds, cus)
-             : occupancy_blocks(k_maxplus<kCpSlotsGlobal, kMpOutNone>, lds, cus);
+  if (out == kMpOutFinish) return mp_kernel_of<kCpSlotsGlobal, kMpOutFinish>(gen, bar);
+  if (out == kMpOutDist) return mp_kernel_of<kCpSlotsGlobal, kMpOutDist>(gen, bar);
+  return mp_kernel_of<kCpSlotsGlobal, kMpOutNone>(gen, bar);
+}
+
+}  // namespace
+
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen, bool bar) {
+  return occupancy_blocks(mp_kernel(mode, fin ? kMpOutFinish : kMpOutNone, gen, bar), lds, cus);
 }
 
 int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
                    const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
                    int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
                    uint32_t *slots_g, hipStream_t stream, const DurGen *gen) {
+  MpTable t = T;
   MpArgs a{n_scen, dur, ld_dur, out, status, finish, ld_fin, dist_out, dist_scen, slots_g, DurGen{}};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const dim3 grid((unsigned)std::min<int64_t>(tiles, max_blocks)), blk(kWave);
   const int out_kind = finish ? kMpOutFinish : dist_out ? kMpOutDist : kMpOutNone;
-#define MP_CASE(M, O) \
-  if (mode == M && out_kind == O) {                                  \
-    if (gen)                                                         \
-      k_maxplus<M, O, true><<<grid, blk, lds, stream>>>(T, a);       \
-    else                                                             \
-      k_maxplus<M, O><<<grid, blk, lds, stream>>>(T, a);             \
-  }
-  MP_CASE(kCpSlotsLds, kMpOutNone)
-  MP_CASE(kCpSlotsLds, kMpOutFinish)
-  MP_CASE(kCpSlotsLds, kMpOutDist)
-  MP_CASE(kCpSlotsGlobal, kMpOutNone)
-  MP_CASE(kCpSlotsGlobal, kMpOutFinish)
-  MP_CASE(kCpSlotsGlobal, kMpOutDist)
-#undef MP_CASE
+  void *args[] = {&t, &a};
+  if (hipLaunchKernel((const void *)mp_kernel(mode, out_kind, gen != nullptr, T.bar != 0), grid, blk, args, lds,
+                      stream) != hipSuccess)
+    return SIM_E_HIP;
   return hipGetLastError() == hipSuccess ? SIM_OK : SIM_E_HIP;
 }
 
@@ -1531,7 +1540,7 @@ int launch_cp(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *dur,
               int32_t *cp_len, int32_t *dist_out, int64_t dist_scen, hipStream_t stream,
               const DurGen *gen) {
   const ScratchPlan &P = g->plan;
-  const MpTable T{g->dg.n, g->dg.cp_slots, g->dg.cp, g->dg.cp_pred};
+  const MpTable T{g->dg.cp_n, g->dg.cp_slots, g->dg.cp, g->dg.cp_pred, g->dg.cp_n > g->dg.n};
   return launch_maxplus(T, P.cp_mode, gen ? P.cp_gen_blocks : P.cp_blocks, P.cp_lds_bytes, n_scen, dur,
                         ld_dur, cp_len, nullptr, nullptr, 0, dist_out, dist_scen,
                         (uint32_t *)(scr + g->scratch_cp_off), stream, gen);

@@ -40,7 +40,8 @@ struct OpRec {
   int32_t j1;
 };
 
-// Per position of the critical-path sweep order (32 bytes).  The table is
+// Per position of the critical-path sweep order (32 bytes): an op, or a
+// barrier node standing for a predecessor set that several ops share.  The table is
 // padded with empty records (row 0, no slot, no predecessors) to whole
 // batches of kCpBatch plus kCpBatch * kCpAhead more, so a sweep can read
 // records and rows ahead without bounds checks.
@@ -49,7 +50,7 @@ constexpr int kCpAhead = 4;   // batches of records read ahead
 constexpr int kCpSlotsGlobal = 0, kCpSlotsLds = 1;  // where the sweep's value slots live
 constexpr int kMpOutNone = 0, kMpOutFinish = 1, kMpOutDist = 2;  // what else the sweep writes
 struct CpRec {
-  int32_t orig;   // row of dur
+  int32_t orig;   // row of dur; -1 for a barrier node (duration 0, no row of its own)
   int32_t slot;   // slot receiving dist(v) (ops without successors: slot cp_slots - 1)
   int32_t npred;
   int32_t pbeg;   // predecessor slots in cp_pred[pbeg, pbeg + npred) when npred > 4
@@ -60,10 +61,11 @@ struct CpRec {
 // Device view of a max-plus sweep table (critical path or static-order
 // replay): records in sweep order and the long predecessor lists.
 struct MpTable {
-  int32_t n;      // ops
+  int32_t n;      // records swept (ops and barrier nodes)
   int32_t slots;  // value slots (live values + the zero slot + the sink slot)
   const CpRec *rec;
   const int32_t *pred;
+  int32_t bar;    // 1 when some records are barrier nodes
 };
 
 // Device view of a compiled graph (plain pointers, passed by value).
@@ -72,7 +74,7 @@ struct DevGraph {
   int32_t heap_cap;       // bound on simultaneously ready ops (>= DAG width)
   int32_t cp_slots;       // value slots of the critical-path sweep (live values + 2)
   int32_t max_indeg;
-  int32_t pad0;
+  int32_t cp_n;           // records of the critical-path sweep (ops and its barrier nodes)
   const OpRec *ops;       // [n + barriers + 1]
   const int32_t *succ;    // pairs {successor id, its join index, kJoinNone or kJoinSibling}
   const int32_t *jneed;   // [J] predecessors a join waits for
@@ -282,18 +284,20 @@ int launch_attr(const sim_graph *g, char *scr, int64_t n_scen, const int32_t *du
                 int32_t *chain_ops, hipStream_t stream);
 // the max-plus sweep on any table: blocks resident per launch for a slot mode
 // and LDS size, and the launch itself (finish != null writes finish rows)
-int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen = false);
+int maxplus_occupancy(int mode, bool fin, size_t lds, int cus, bool gen, bool bar);
 int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64_t n_scen,
                    const int32_t *dur, int64_t ld_dur, int32_t *out, int32_t *status,
                    int32_t *finish, int64_t ld_fin, int32_t *dist_out, int64_t dist_scen,
                    uint32_t *slots_g, hipStream_t stream, const DurGen *gen = nullptr);
 // Records of a max-plus sweep over ops 0..n-1 (duration row of op v:
-// row_of[v]) with the given successor and predecessor lists: a topological
-// order, its value slots and the padded records.  False on a cycle.
+// row_of[v]) with the given successor and predecessor lists, possibly with
+// barrier nodes for shared predecessor sets: the ops in a topological order,
+// the value slots, the number of records swept (ops and barriers) and the
+// padded records.  False on a cycle.
 bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
                    const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
-                   std::vector<int32_t> &order);
+                   std::vector<int32_t> &order, int32_t &n_sweep);
 // the replay variant that allocates nothing: the address of the static
 // scratch array on the current device, looked up once per device (at graph
 // creation), and the launch on it

@@ -68,8 +68,8 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   for (int32_t v = 0; v < n; ++v) rows[v] = v;
   std::vector<CpRec> rec;
   std::vector<int32_t> plist;
-  int32_t slots = 0;
-  if (!build_maxplus(n, succ, pred, rows, rec, plist, slots, sweep_order)) return SIM_E_CYCLE;
+  int32_t slots = 0, n_sweep = 0;
+  if (!build_maxplus(n, succ, pred, rows, rec, plist, slots, sweep_order, n_sweep)) return SIM_E_CYCLE;
 
   sim_static *st = new (std::nothrow) sim_static();
   if (!st) return SIM_E_NOMEM;
@@ -96,13 +96,12 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
     sim_static_destroy(st);
     return SIM_E_HIP;
   }
-  st->tab = MpTable{n, slots, (const CpRec *)base, (const int32_t *)(base + pl_off)};
+  st->tab = MpTable{n_sweep, slots, (const CpRec *)base, (const int32_t *)(base + pl_off), n_sweep > n};
   // value slots in LDS when they fit, else in global scratch for the grid
   const size_t slot_bytes = (size_t)slots * kWave * 4;
-  const size_t ring = 4 * sizeof(CpRec) * kCpBatch;
   st->mode = slot_bytes <= kSlotsLdsMax && !g->var.cp_global ? kCpSlotsLds : kCpSlotsGlobal;
-  st->lds = ring + (st->mode == kCpSlotsLds ? slot_bytes : 0);
-  int blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount);
+  st->lds = st->mode == kCpSlotsLds ? slot_bytes : 0;
+  int blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount, false, st->tab.bar != 0);
   if (blocks < 0) {
     sim_static_destroy(st);
     return SIM_E_HIP;
@@ -120,7 +119,7 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
     }
   }
   st->blocks = std::max(1, blocks);
-  const int gen_blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount, true);
+  const int gen_blocks = maxplus_occupancy(st->mode, true, st->lds, prop.multiProcessorCount, true, st->tab.bar != 0);
   if (gen_blocks < 0) {
     sim_static_destroy(st);
     return SIM_E_HIP;
