@@ -12,6 +12,7 @@
 #include <map>
 #include <new>
 #include <numeric>
+#include <queue>
 #include <vector>
 
 #include "sim.hpp"
@@ -166,6 +167,59 @@ int32_t assign_cp_slots(int32_t n, const std::vector<std::vector<int32_t>> &succ
     }
   }
   return nslots;
+}
+
+// A topological order that keeps few values live: among the ready nodes,
+// visit the one that ends the most live values (predecessors whose last
+// unvisited successor it is), less one if its own value will be live;
+// ties go to the smaller tie key.  Scores only grow while a node waits
+// (a predecessor reaching its last unvisited successor adds one to that
+// successor), so each change pushes a fresh heap entry and stale entries are
+// skipped: O((nodes + edges) log nodes).
+void greedy_order(int32_t n, const std::vector<std::vector<int32_t>> &succ,
+                  const std::vector<std::vector<int32_t>> &pred, const std::vector<int64_t> &tie,
+                  std::vector<int32_t> &order) {
+  std::vector<int32_t> cnt(n), rem(n), score(n);
+  std::vector<char> done(n, 0);
+  for (int32_t v = 0; v < n; ++v) {
+    cnt[v] = (int32_t)pred[v].size();
+    rem[v] = (int32_t)succ[v].size();
+    score[v] = succ[v].empty() ? 0 : -1;
+  }
+  for (int32_t v = 0; v < n; ++v)
+    for (int32_t p : pred[v])
+      if (rem[p] == 1) ++score[v];
+  struct Entry {
+    int32_t score;
+    int64_t tie;
+    int32_t v;
+    bool operator<(const Entry &o) const {  // max-heap: higher score, then smaller tie
+      return score != o.score ? score < o.score : tie > o.tie;
+    }
+  };
+  std::priority_queue<Entry> heap;
+  for (int32_t v = 0; v < n; ++v)
+    if (cnt[v] == 0) heap.push({score[v], tie[v], v});
+  order.clear();
+  order.reserve(n);
+  while (!heap.empty()) {
+    const Entry e = heap.top();
+    heap.pop();
+    if (done[e.v] || e.score != score[e.v]) continue;
+    const int32_t v = e.v;
+    done[v] = 1;
+    order.push_back(v);
+    for (int32_t p : pred[v])
+      if (--rem[p] == 1)
+        for (int32_t q : succ[p])
+          if (!done[q]) {
+            ++score[q];
+            if (cnt[q] == 0) heap.push({score[q], tie[q], q});
+            break;
+          }
+    for (int32_t w : succ[v])
+      if (--cnt[w] == 0) heap.push({score[w], tie[w], w});
+  }
 }
 
 int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_idx,
@@ -447,7 +501,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
 
   // critical-path sweep
   std::vector<int32_t> order;
-  build_maxplus(n, cs, cp, orig_of, C.cp, C.cp_pred, C.cp_slots, order, C.cp_n);
+  build_maxplus(n, cs, cp, {}, {}, orig_of, C.cp, C.cp_pred, C.cp_slots, order, C.cp_n);
 
   // compact predecessor CSR (for the sweep variant) and level count
   C.pred_ptr.assign(n + 1, 0);
@@ -485,45 +539,60 @@ size_t bytes_of(const std::vector<T> &v) {
 namespace mlsim {
 
 bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
-                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
+                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &extra,
+                   const std::vector<int64_t> &tie, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
                    std::vector<int32_t> &order, int32_t &n_sweep) {
-  // A second candidate table: one barrier node for each predecessor set of
-  // two or more ops that two or more ops share.  Its dist is the max over the
-  // set (duration 0), and each op sharing the set takes the barrier as its
-  // only predecessor: the same dist for every op, and the set's values are
-  // dead once the barrier has read them.
+  // A second candidate table: one barrier node for each predecessor set (two
+  // or more ops, not counting an op's extra predecessor) that two or more
+  // ops share.  Its dist is the max over the set (duration 0), and each op
+  // sharing the set takes the barrier (and its extra predecessor) instead:
+  // the same dist for every op, and the set's values are dead once the
+  // barrier has read them.
+  auto extra_of = [&](int32_t v) { return extra.empty() ? -1 : extra[v]; };
   std::map<std::vector<int32_t>, std::vector<int32_t>> sets;
-  for (int32_t v = 0; v < n; ++v)
-    if (pred[v].size() >= 2) {
-      std::vector<int32_t> key = pred[v];
-      std::sort(key.begin(), key.end());
-      sets[key].push_back(v);
-    }
+  for (int32_t v = 0; v < n; ++v) {
+    std::vector<int32_t> key;
+    for (int32_t p : pred[v])
+      if (p != extra_of(v)) key.push_back(p);
+    if (key.size() < 2) continue;
+    std::sort(key.begin(), key.end());
+    sets[key].push_back(v);
+  }
   std::vector<std::vector<int32_t>> fpred(pred), fsucc;
   for (const auto &kv : sets) {
     if (kv.second.size() < 2) continue;
     const int32_t b = (int32_t)fpred.size();
     fpred.push_back(kv.first);
-    for (int32_t v : kv.second) fpred[v].assign(1, b);
+    for (int32_t v : kv.second) {
+      fpred[v].assign(1, b);
+      if (extra_of(v) >= 0) fpred[v].push_back(extra_of(v));
+    }
   }
   const int32_t nf = (int32_t)fpred.size();
   fsucc.resize(nf);
   for (int32_t v = 0; v < nf; ++v)
     for (int32_t p : fpred[v]) fsucc[p].push_back(v);
-  // the candidate (graph, depth- or breadth-first order) that needs the
-  // fewest live value slots; ties keep the table without barriers
+  // the candidate (graph; depth-first, breadth-first or greedy order) that
+  // needs the fewest live value slots; ties keep the earlier candidate
   struct Cand {
     int32_t nodes;
     const std::vector<std::vector<int32_t>> *succ, *pred;
     std::vector<int32_t> order, slot;
     int32_t live;
   };
+  std::vector<int64_t> key(nf);  // greedy ties: the given key (else the id), barriers first
+  for (int32_t v = 0; v < nf; ++v) key[v] = v >= n ? -1 : tie.empty() ? v : tie[v];
   std::vector<Cand> cand;
   for (int f = 0; f < (nf > n ? 2 : 1); ++f)
-    for (int lifo = 1; lifo >= 0; --lifo) {
+    for (int how = 0; how < 3; ++how) {
       Cand c{f ? nf : n, f ? &fsucc : &succ, f ? &fpred : &pred, {}, {}, 0};
-      if (!kahn(c.nodes, *c.succ, lifo != 0, c.order)) return false;
+      if (how < 2) {
+        if (!kahn(c.nodes, *c.succ, how == 0, c.order)) return false;
+      } else {
+        greedy_order(c.nodes, *c.succ, *c.pred, key, c.order);
+        if ((int32_t)c.order.size() != c.nodes) return false;
+      }
       c.live = assign_cp_slots(c.nodes, *c.succ, *c.pred, c.order, c.slot);
       cand.push_back(std::move(c));
     }

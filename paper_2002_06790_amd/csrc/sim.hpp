@@ -293,9 +293,13 @@ int launch_maxplus(const MpTable &T, int mode, int max_blocks, size_t lds, int64
 // row_of[v]) with the given successor and predecessor lists, possibly with
 // barrier nodes for shared predecessor sets: the ops in a topological order,
 // the value slots, the number of records swept (ops and barriers) and the
-// padded records.  False on a cycle.
+// padded records.  extra (empty, or one entry per op): a predecessor of v
+// that is left out when predecessor sets are compared, or -1; tie (empty, or
+// one key per op): the order preferred among equally good ready ops.  False
+// on a cycle.
 bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
-                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &row_of,
+                   const std::vector<std::vector<int32_t>> &pred, const std::vector<int32_t> &extra,
+                   const std::vector<int64_t> &tie, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
                    std::vector<int32_t> &order, int32_t &n_sweep);
 // the replay variant that allocates nothing: the address of the static

@@ -53,11 +53,19 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
     const int32_t v = g->h_orig_of[c];
     for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k) pred[v].push_back(g->h_orig_of[g->h_pred[k]]);
   }
-  std::vector<int32_t> last(g->n_res, -1);
+  // extra[v]: the device predecessor when it is not already a DAG
+  // predecessor (the sweep table compares predecessor sets without it);
+  // pos[v]: v's place in the given order, which the sweep order prefers
+  // among equally good choices
+  std::vector<int32_t> last(g->n_res, -1), extra(n, -1);
+  std::vector<int64_t> pos(n);
   for (int32_t k = 0; k < n; ++k) {
     const int32_t v = order[k], r = g->h_res[v];
-    if (last[r] >= 0 && std::find(pred[v].begin(), pred[v].end(), last[r]) == pred[v].end())
+    pos[v] = k;
+    if (last[r] >= 0 && std::find(pred[v].begin(), pred[v].end(), last[r]) == pred[v].end()) {
       pred[v].push_back(last[r]);
+      extra[v] = last[r];
+    }
     last[r] = v;
   }
   for (int32_t v = 0; v < n; ++v) {
@@ -69,7 +77,7 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   std::vector<CpRec> rec;
   std::vector<int32_t> plist;
   int32_t slots = 0, n_sweep = 0;
-  if (!build_maxplus(n, succ, pred, rows, rec, plist, slots, sweep_order, n_sweep)) return SIM_E_CYCLE;
+  if (!build_maxplus(n, succ, pred, extra, pos, rows, rec, plist, slots, sweep_order, n_sweep)) return SIM_E_CYCLE;
 
   sim_static *st = new (std::nothrow) sim_static();
   if (!st) return SIM_E_NOMEM;
