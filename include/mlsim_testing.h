@@ -4,10 +4,11 @@
  *
  * The library picks, once per graph, where each kernel keeps its per-lane
  * state (LDS, registers or global scratch) and how many blocks its
- * persistent grids hold.  Every choice computes the same results; this call
- * pins a graph to one of them so that a test can check each variant against
- * the oracle.  No environment variable or other hidden state selects a
- * variant.
+ * persistent grids hold.  Every choice computes the same results;
+ * sim_testing_replan pins a graph to one of them so that a test can check
+ * each variant against the oracle.  No environment variable or other hidden
+ * state selects a variant.  sim_testing_sweep_table returns the max-plus
+ * sweep table built for a graph, for CPU tests of the table builder.
  */
 #ifndef MLSIM_TESTING_H
 #define MLSIM_TESTING_H
@@ -41,6 +42,30 @@ enum {
  * a value out of range, or the allocation's error.
  */
 int sim_testing_replan(sim_graph *g, int32_t what, int32_t value);
+
+/*
+ * The max-plus sweep table the library builds, on the host only (no device
+ * is used), so that a test can evaluate it on the CPU and compare the result
+ * with an independent replay.  The graph arguments are those of
+ * sim_graph_create.  order NULL: the critical-path table (sim_critical_path);
+ * otherwise a permutation of the op ids whose restriction to each resource
+ * is that resource's run order: the table of sim_static_create.
+ * Outputs (host): *n_rec records in sweep order, each 8 int32 in rec
+ * [rec_cap][8]: {row, slot, npred, pbeg, p0, p1, p2, p3} -- row: the op
+ * (its dist is its finish time or path length), -1 for a barrier record
+ * (duration 0); slot: the value slot receiving the record's dist; the
+ * predecessor slots are p0..p(npred-1) when npred <= 4, else plist[pbeg ..
+ * pbeg + npred); unused p entries name slot *slots - 2, which holds 0; a
+ * record whose value nothing reads writes slot *slots - 1.  *plist_len
+ * entries go to plist [plist_cap].  Returns SIM_OK; the argument errors of
+ * sim_graph_create and sim_static_create (SIM_E_INVAL, SIM_E_RANGE,
+ * SIM_E_CYCLE, SIM_E_LIMIT); or SIM_E_LIMIT when rec_cap or plist_cap is too
+ * small, after writing *n_rec and *plist_len.
+ */
+int sim_testing_sweep_table(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                            const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                            const int32_t *order, int32_t *n_rec, int32_t *slots, int32_t *rec,
+                            int64_t rec_cap, int32_t *plist, int64_t plist_cap, int64_t *plist_len);
 
 #ifdef __cplusplus
 }

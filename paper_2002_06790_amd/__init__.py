@@ -35,7 +35,7 @@ EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critic
            "sim_strerror", "sim_graph_info", "sim_testing_replan", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
            "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
-           "sim_run_batch_dev", "sim_run_batch_share", "sim_run_batch_noalloc")
+           "sim_run_batch_dev", "sim_run_batch_share", "sim_run_batch_noalloc", "sim_testing_sweep_table")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -108,6 +108,8 @@ def _load():
     L.sim_run_batch_share.restype = ctypes.c_int
     L.sim_static_run_generated.argtypes = [P, I64, P, I32, I64, U32, U64, I64, P, P, I64, P, P]
     L.sim_static_run_generated.restype = ctypes.c_int
+    L.sim_testing_sweep_table.argtypes = [I32, I32, P, P, P, P, P, P, P, P, I64, P, I64, P]
+    L.sim_testing_sweep_table.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -115,6 +117,39 @@ def _load():
 def lib():
     """The loaded ctypes library (raises if it is not built)."""
     return _load()
+
+
+def sweep_table(succ_ptr, succ_idx, op_res, n_res: int, prio=None, order=None):
+    """The max-plus sweep table the library builds for a graph, on the host
+    only (sim_testing_sweep_table): the critical-path table, or with
+    ``order`` (a permutation of the op ids) the static-order replay's.
+    Returns ``(rec int32 [n_rec, 8], plist int32, slots)``; the fields of a
+    record are {row, slot, npred, pbeg, p0, p1, p2, p3} (row -1: a barrier
+    record)."""
+    L = _load()
+    ptr = _host(succ_ptr, np.int64)
+    idx = _host(succ_idx, np.int32)
+    res = _host(op_res, np.int32)
+    pr = _host(prio, np.int32)
+    od = _host(order, np.int32)
+    n = int(ptr.size - 1)
+    if res.size != n or (pr is not None and pr.size != n) or (od is not None and od.size != n):
+        raise ValueError("op_res, prio and order need one entry per op")
+    n_rec, slots, plen = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+    rec = np.zeros((0, 8), np.int32)
+    plist = np.zeros(0, np.int32)
+    for _ in range(2):  # sizes first, then the table
+        rc = L.sim_testing_sweep_table(n, int(n_res), _hptr(ptr), _hptr(idx), _hptr(res), _hptr(pr), _hptr(od),
+                                       ctypes.byref(n_rec), ctypes.byref(slots), _hptr(rec) if rec.size else None,
+                                       rec.shape[0], _hptr(plist) if plist.size else None, plist.size,
+                                       ctypes.byref(plen))
+        if rc == SIM_OK:
+            return rec[:n_rec.value].copy(), plist[:plen.value].copy(), slots.value
+        if rc != SIM_E_LIMIT or (rec.shape[0] >= n_rec.value and plist.size >= plen.value):
+            raise SimError(rc, "sim_testing_sweep_table")
+        rec = np.zeros((n_rec.value, 8), np.int32)
+        plist = np.zeros(max(plen.value, 1), np.int32)
+    raise SimError(SIM_E_LIMIT, "sim_testing_sweep_table")
 
 
 def _host(a, dt):

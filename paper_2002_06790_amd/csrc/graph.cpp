@@ -629,11 +629,11 @@ bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
 }  // namespace mlsim
 
 
-extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
-                                const int32_t *succ_idx, const int32_t *op_res,
-                                const int32_t *prio, sim_graph **out) {
-  if (!out) return SIM_E_INVAL;
-  *out = nullptr;
+namespace {
+
+// The argument checks of sim_graph_create.
+int check_graph_args(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr, const int32_t *succ_idx,
+                     const int32_t *op_res) {
   if (n_ops < 0 || n_res < 1) return SIM_E_INVAL;
   if (n_ops > SIM_MAX_OPS || n_res > SIM_MAX_RES) return SIM_E_LIMIT;
   if (n_ops > 0 && (!succ_ptr || !op_res)) return SIM_E_INVAL;
@@ -648,6 +648,17 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
     for (int32_t v = 0; v < n_ops; ++v)
       if (op_res[v] < 0 || op_res[v] >= n_res) return SIM_E_RANGE;
   }
+  return SIM_OK;
+}
+
+}  // namespace
+
+extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                                const int32_t *succ_idx, const int32_t *op_res,
+                                const int32_t *prio, sim_graph **out) {
+  if (!out) return SIM_E_INVAL;
+  *out = nullptr;
+  if (int rc = check_graph_args(n_ops, n_res, succ_ptr, succ_idx, op_res)) return rc;
   Compiled C;
   int rc;
   try {
@@ -851,4 +862,45 @@ extern "C" const char *sim_strerror(int code) {
     case SIM_E_LIMIT: return "graph exceeds a library limit";
     default: return "unknown error";
   }
+}
+
+extern "C" int sim_testing_sweep_table(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                                       const int32_t *succ_idx, const int32_t *op_res,
+                                       const int32_t *prio, const int32_t *order, int32_t *n_rec,
+                                       int32_t *slots, int32_t *rec, int64_t rec_cap, int32_t *plist,
+                                       int64_t plist_cap, int64_t *plist_len) {
+  if (!n_rec || !slots || !plist_len || rec_cap < 0 || plist_cap < 0) return SIM_E_INVAL;
+  if ((rec_cap > 0 && !rec) || (plist_cap > 0 && !plist)) return SIM_E_INVAL;
+  if (int rc = check_graph_args(n_ops, n_res, succ_ptr, succ_idx, op_res)) return rc;
+  std::vector<CpRec> table;
+  std::vector<int32_t> pl;
+  int32_t ns = 0, sl = 0;
+  try {
+    Compiled C;
+    if (int rc = compile(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, C)) return rc;
+    if (!order) {
+      table = std::move(C.cp);
+      pl = std::move(C.cp_pred);
+      ns = C.cp_n;
+      sl = C.cp_slots;
+    } else {
+      std::vector<int32_t> orig_of(n_ops);
+      for (int32_t c = 0; c < n_ops; ++c) orig_of[c] = C.ops[c].orig;
+      const std::vector<int32_t> res(op_res, op_res + n_ops);
+      if (int rc = static_table(n_ops, orig_of, C.pred_ptr, C.pred, res, order, table, pl, sl, ns)) return rc;
+    }
+  } catch (const std::bad_alloc &) {
+    return SIM_E_NOMEM;
+  }
+  *n_rec = ns;
+  *slots = sl;
+  *plist_len = (int64_t)pl.size();
+  if (ns > rec_cap || (int64_t)pl.size() > plist_cap) return SIM_E_LIMIT;
+  for (int32_t k = 0; k < ns; ++k) {
+    const CpRec &r = table[k];
+    const int32_t w[8] = {r.orig, r.slot, r.npred, r.pbeg, r.p[0], r.p[1], r.p[2], r.p[3]};
+    std::memcpy(rec + 8 * (size_t)k, w, sizeof w);
+  }
+  if (!pl.empty()) std::memcpy(plist, pl.data(), pl.size() * 4);
+  return SIM_OK;
 }

@@ -302,6 +302,13 @@ bool build_maxplus(int32_t n, const std::vector<std::vector<int32_t>> &succ,
                    const std::vector<int64_t> &tie, const std::vector<int32_t> &row_of,
                    std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots,
                    std::vector<int32_t> &order, int32_t &n_sweep);
+// The static-order replay's sweep table for `order` (a permutation of the
+// caller's op ids) over a compiled graph's host view: compact predecessor
+// CSR, compact -> caller ids, each caller id's resource.  SIM_E_INVAL for a
+// bad order, SIM_E_CYCLE when the order contradicts the DAG.
+int static_table(int32_t n, const std::vector<int32_t> &orig_of, const std::vector<int32_t> &pred_ptr,
+                 const std::vector<int32_t> &pred_c, const std::vector<int32_t> &res, const int32_t *order,
+                 std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots, int32_t &n_sweep);
 // the replay variant that allocates nothing: the address of the static
 // scratch array on the current device, looked up once per device (at graph
 // creation), and the launch on it

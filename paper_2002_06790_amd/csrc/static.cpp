@@ -32,11 +32,11 @@ constexpr size_t kSlotsScratchBudget = 1ull << 30;
 
 }  // namespace
 
-extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_static **out) {
-  if (!out) return SIM_E_INVAL;
-  *out = nullptr;
-  if (!g) return SIM_E_INVAL;
-  const int32_t n = g->n_ops;
+namespace mlsim {
+
+int static_table(int32_t n, const std::vector<int32_t> &orig_of, const std::vector<int32_t> &pred_ptr,
+                 const std::vector<int32_t> &pred_c, const std::vector<int32_t> &res, const int32_t *order,
+                 std::vector<CpRec> &rec, std::vector<int32_t> &plist, int32_t &slots, int32_t &n_sweep) {
   if (n > 0 && !order) return SIM_E_INVAL;
   // the order names every op once
   std::vector<char> seen(n, 0);
@@ -50,17 +50,18 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   // it) and the previous op on the device in the given order
   std::vector<std::vector<int32_t>> pred(n), succ(n);
   for (int32_t c = 0; c < n; ++c) {
-    const int32_t v = g->h_orig_of[c];
-    for (int32_t k = g->h_pred_ptr[c]; k < g->h_pred_ptr[c + 1]; ++k) pred[v].push_back(g->h_orig_of[g->h_pred[k]]);
+    const int32_t v = orig_of[c];
+    for (int32_t k = pred_ptr[c]; k < pred_ptr[c + 1]; ++k) pred[v].push_back(orig_of[pred_c[k]]);
   }
   // extra[v]: the device predecessor when it is not already a DAG
   // predecessor (the sweep table compares predecessor sets without it);
   // pos[v]: v's place in the given order, which the sweep order prefers
   // among equally good choices
-  std::vector<int32_t> last(g->n_res, -1), extra(n, -1);
+  std::vector<int32_t> last, extra(n, -1);
   std::vector<int64_t> pos(n);
   for (int32_t k = 0; k < n; ++k) {
-    const int32_t v = order[k], r = g->h_res[v];
+    const int32_t v = order[k], r = res[v];
+    if (r >= (int32_t)last.size()) last.resize(r + 1, -1);
     pos[v] = k;
     if (last[r] >= 0 && std::find(pred[v].begin(), pred[v].end(), last[r]) == pred[v].end()) {
       pred[v].push_back(last[r]);
@@ -74,10 +75,26 @@ extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_s
   }
   std::vector<int32_t> rows(n), sweep_order;
   for (int32_t v = 0; v < n; ++v) rows[v] = v;
+  if (!build_maxplus(n, succ, pred, extra, pos, rows, rec, plist, slots, sweep_order, n_sweep)) return SIM_E_CYCLE;
+  return SIM_OK;
+}
+
+}  // namespace mlsim
+
+extern "C" int sim_static_create(const sim_graph *g, const int32_t *order, sim_static **out) {
+  if (!out) return SIM_E_INVAL;
+  *out = nullptr;
+  if (!g) return SIM_E_INVAL;
+  const int32_t n = g->n_ops;
   std::vector<CpRec> rec;
   std::vector<int32_t> plist;
   int32_t slots = 0, n_sweep = 0;
-  if (!build_maxplus(n, succ, pred, extra, pos, rows, rec, plist, slots, sweep_order, n_sweep)) return SIM_E_CYCLE;
+  try {
+    if (int rc = static_table(n, g->h_orig_of, g->h_pred_ptr, g->h_pred, g->h_res, order, rec, plist, slots, n_sweep))
+      return rc;
+  } catch (const std::bad_alloc &) {
+    return SIM_E_NOMEM;
+  }
 
   sim_static *st = new (std::nothrow) sim_static();
   if (!st) return SIM_E_NOMEM;
