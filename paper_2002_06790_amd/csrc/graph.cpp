@@ -33,7 +33,7 @@ struct Compiled {
   // {predecessors needed, word released} per join, source words
   std::vector<OpRec> ev_ops;
   std::vector<int32_t> ev_succ, jinfo, ev_src;
-  int32_t pk_sh = 0, pk_join = 0, pk_jn = 0, pk_jb = 0, pk_rb = 0, ev_compact = 0;
+  int32_t pk_sh = 0, pk_join = 0, pk_jn = 0, pk_jb = 0, pk_rb = 0, ev_compact = 0, pk_rkey = 0;
   std::vector<int32_t> ev_rec16;  // [n][4] compact event records (ev_compact)
   std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
@@ -441,13 +441,16 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     while ((1ll << rb) < (int64_t)R) ++rb;
     bool ident = true;  // caller ids equal compact ids: the duration row is the id
     for (int32_t c = 0; c < n && ident; ++c) ident = orig_of[c] == c;
-    // compact records: identity rows, self-contained join entries, and id,
-    // resource and join field in one word
-    const bool compact = ident && jn && rb + jb < 32 && (int64_t)n <= (1ll << (32 - rb - jb));
+    // compact records: identity rows, self-contained join entries, and id
+    // and join field in one word; the resource too when it fits (rkey),
+    // else the replay reads it by row (it needs none with a placement)
+    const bool compact = ident && jn && jb < 32 && (int64_t)n <= (1ll << (32 - jb));
+    const bool rkey = compact && rb + jb < 32 && (int64_t)n <= (1ll << (32 - rb - jb));
     const bool pack = compact || (jb > 0 && jb < 32 && (int64_t)n <= (1ll << (32 - jb)));
-    if (!compact) rb = 0;
+    if (!rkey) rb = 0;
     if (!pack) jb = 0;
     C.ev_compact = compact;
+    C.pk_rkey = rkey;
     C.pk_jb = jb;
     C.pk_rb = rb;
     C.pk_sh = rb + jb;
@@ -457,7 +460,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
       if (!pack || c < 0 || c >= n) return c;
       const OpRec &r = C.ops[c];
       const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)r.j0 : jnone;
-      const uint32_t res = compact ? (uint32_t)r.res << jb : 0u;
+      const uint32_t res = rkey ? (uint32_t)r.res << jb : 0u;
       return (int32_t)(((uint32_t)c << (rb + jb)) | res | jf);
     };
     auto entry = [&](int32_t &x, int32_t &y) {
@@ -774,6 +777,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   d.pk_jb = C.pk_jb;
   d.pk_rmask = (int32_t)((1u << C.pk_rb) - 1u);
   d.ev_compact = C.ev_compact;
+  d.pk_rkey = C.pk_rkey;
   d.ev_rec16 = (const int4 *)(base + o_rec16);
   d.lvl_of = (const int32_t *)(base + o_lvl);
   d.levend = (const int32_t *)(base + o_levend);

@@ -363,7 +363,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   int rp = 0;
   if (ROW_ID) {
     d = GEN ? brow[c] : a.dur[(int64_t)c * a.ld_dur + sc];
-    if (PLACE) rp = a.place[(int64_t)c * a.ld_place + sc];
+    if (PLACE)
+      rp = a.place[(int64_t)c * a.ld_place + sc];
+    else if (!G.pk_rkey)
+      rp = G.row_res[c];  // the key word has no room for the resource
   }
   // the first successor's join state, when the key word names the join:
   // read together with the record instead of after it
@@ -384,7 +387,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     if (PLACE) rp = a.place[(int64_t)row * a.ld_place + sc];
   }
   if (GEN) d = gen_duration(d, s_lo, s_hi, (uint32_t)row, a.gen.key0, a.gen.key1, a.gen.noise);
-  int r = PLACE ? rp : ROW_ID ? (int)((low >> G.pk_jb) & (uint32_t)G.pk_rmask) : r0.y;
+  int r = PLACE ? rp : !ROW_ID ? r0.y : G.pk_rkey ? (int)((low >> G.pk_jb) & (uint32_t)G.pk_rmask) : rp;
   if (PLACE && r >= R) {
     st |= SIM_ST_BAD_RES;
     r = 0;
@@ -497,7 +500,8 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
 // the outer loop is wave-uniform.  ROW_ID: the caller's op ids equal the
 // compact ids, so the duration row is known as soon as the op is popped, and
 // the graph has compact records (one 16-byte load per step; the resource
-// comes from the key word).
+// comes from the key word, or when it has no room from a load by row issued
+// with the record).
 // PLACE: resources come from the per-scenario placement matrix.  Finish times
 // are written in bursts of kFinQ stores per lane, so their completion is
 // waited for once per burst instead of once per step.  GEN: durations are
@@ -1048,11 +1052,11 @@ __global__ __launch_bounds__(kWave) void k_sweep(DevGraph G, SwArgs a) {
 }
 
 template <class K>
-int occupancy_blocks(K kernel, size_t lds, int cus) {
+int occupancy_blocks(K kernel, size_t lds, int cus, bool strict = false) {
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kWave, lds) != hipSuccess)
     return -1;
-  if (per_cu < 1) per_cu = 1;
+  if (per_cu < 1) per_cu = strict ? 0 : 1;  // strict: 0 when the LDS does not fit one block
   return per_cu * cus;
 }
 
@@ -1156,6 +1160,33 @@ int plan_scratch(sim_graph *g) {
                                 : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
   P.ev_prev_blocks = grid_of(ev_prev_occ);
+  // A call with few tiles (fewer than the grids below hold) keeps the whole
+  // third heap level in LDS: heaps of up to 73 entries then never touch
+  // global memory.  Not planned when a test pins the LDS groups.
+  P.ev_wide_le = kL2 + kD * kD;
+  P.ev_wide_lds_bytes = (size_t)(P.ev_wide_le - kL1) * kWave * 8 + rf_lds_bytes;
+  P.ev_wide_blocks = P.ev_wide_gen_blocks = P.ev_wide_dev_blocks = P.ev_wide_prev_blocks = 0;
+  if (V.ev_lds_groups < 0 && lds_groups < kD) {
+    const size_t wl = P.ev_wide_lds_bytes;
+    int wo[4];
+    if (rf_lds) {
+      wo[0] = occupancy_blocks(k_event<true, false, false, false>, wl, cus, true);
+      wo[1] = occupancy_blocks(k_event<true, false, false, false, true>, wl, cus, true);
+      wo[2] = occupancy_blocks(k_event<true, false, false, false>, wl + dev_table, cus, true);
+      wo[3] = occupancy_blocks(k_event<true, false, false, true>, wl + rf_lds_bytes, cus, true);
+    } else {
+      wo[0] = occupancy_blocks(k_event<false, false, false, false>, wl, cus, true);
+      wo[1] = occupancy_blocks(k_event<false, false, false, false, true>, wl, cus, true);
+      wo[2] = occupancy_blocks(k_event<false, false, false, false>, wl + dev_table, cus, true);
+      wo[3] = occupancy_blocks(k_event<false, false, false, true>, wl, cus, true);
+    }
+    if (wo[0] < 0 || wo[1] < 0 || wo[2] < 0 || wo[3] < 0) return SIM_E_HIP;
+    auto wide_grid = [&](int occ) { return occ > 0 ? grid_of(occ) : 0; };  // 0: not available
+    P.ev_wide_blocks = wide_grid(wo[0]);
+    P.ev_wide_gen_blocks = wide_grid(wo[1]);
+    P.ev_wide_dev_blocks = wide_grid(wo[2]);
+    P.ev_wide_prev_blocks = wide_grid(wo[3]);
+  }
   // attribution chains: busy and chain accumulators in LDS when they fit
   const size_t at_bytes = (size_t)2 * G.R * kWave * 4;
   P.at_lds = at_bytes <= 64 * 1024;
@@ -1169,7 +1200,8 @@ int plan_scratch(sim_graph *g) {
   // scratch for the largest persistent grid of any event variant
   const int32_t ev_grid = std::max({P.ev_blocks, P.ev_gen_blocks, P.ev_dev_blocks, P.ev_prev_blocks,
                                     P.ev_reg_blocks, P.ev_reg_gen_blocks, P.ev_reg_dev_blocks,
-                                    P.ev_reg_prev_blocks});
+                                    P.ev_reg_prev_blocks, P.ev_wide_blocks, P.ev_wide_gen_blocks,
+                                    P.ev_wide_dev_blocks, P.ev_wide_prev_blocks});
 
   // critical path: slots in LDS when they fit, else in global scratch
   const size_t cp_bytes = (size_t)G.cp_slots * kWave * 4;
@@ -1274,13 +1306,24 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
                    : gen  ? P.ev_reg_gen_blocks
                    : dev  ? P.ev_reg_dev_blocks
                           : P.ev_reg_blocks;
+  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
+                   : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
+  if (!reg && !ext) {  // few tiles: the whole third heap level in LDS
+    const int64_t wide = prev ? P.ev_wide_prev_blocks
+                         : gen ? P.ev_wide_gen_blocks
+                         : dev ? P.ev_wide_dev_blocks
+                               : P.ev_wide_blocks;
+    if (tiles <= wide) {
+      blocks = wide;
+      a.heap_le = P.ev_wide_le;
+      lds = P.ev_wide_lds_bytes + (prev && rf_lds ? (size_t)g->dg.R * kWave * 4 : 0);
+    }
+  }
   if (ext) blocks = std::min(blocks, ext->max_blocks);
   const int64_t rounds = (tiles + blocks - 1) / blocks;
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
-  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
-                   : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
   if (dev) {  // the device-model table after the per-lane regions
     a.dev_lds = (int)lds;
     lds += ((size_t)g->dg.R * 8 + 15) & ~size_t(15);

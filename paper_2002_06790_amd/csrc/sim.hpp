@@ -103,7 +103,7 @@ struct DevGraph {
   // event kernel: ready-list key words (low 32 bits of a key) are
   // (compact id << pk_sh) | (resource << pk_jb) | join index of the op's
   // first successor entry (pk_jb bits, all ones: not a join), with
-  // pk_sh = resource bits + pk_jb (resource bits only with ev_compact);
+  // pk_sh = resource bits + pk_jb (resource bits only with pk_rkey);
   // records, successor entries and sources hold such words for the ops they
   // release directly, and jinfo[j] = {predecessors needed, word released}
   // per join.  With pk_jn a join entry {x, y} itself holds x = the word
@@ -115,7 +115,8 @@ struct DevGraph {
   int32_t pk_sh, pk_join, pk_jn, pk_jb, pk_rmask;
   // compact event records (identity rows): 16 bytes per op, entries 0 and 1
   // (see kRecNoSucc, kRecMore); the op's resource comes from its key word
-  int32_t ev_compact, pad2;
+  // with pk_rkey, else from row_res
+  int32_t ev_compact, pk_rkey;
   const int4 *ev_rec16;
 };
 
@@ -141,6 +142,12 @@ struct ScratchPlan {
   size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   int32_t rf_lds;       // event kernel: resource times in LDS (1) or global scratch (0)
+  // event kernel with the heap's whole third level in LDS (heap_le
+  // ev_wide_le), for calls whose tiles all fit these grids (plain, generated
+  // durations, device model, recording predecessors; 0: not planned) and
+  // LDS per block (plus the last-op table when recording predecessors)
+  int32_t ev_wide_le, ev_wide_blocks, ev_wide_gen_blocks, ev_wide_dev_blocks, ev_wide_prev_blocks;
+  size_t ev_wide_lds_bytes;
 };
 
 // Kernel variants a graph's launch plan may be pinned to instead of the

@@ -80,6 +80,25 @@ def test_workload_parity(mlsim, k, S):
     check_cp(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur, paths=(0, dur.shape[1] - 1))
 
 
+def test_compact_records_resource_by_row(mlsim):
+    """Graphs whose key word holds the op id and first join but has no room
+    for the resource (random-layered: 20000 ops, 14894 joins, 100 resources;
+    a random DAG on 1000 resources): without a placement the replay reads
+    each op's resource by row, with one it uses the placement."""
+    w = W.make_config(5, n_scen=130)
+    dur = w.durations()
+    print("random-layered without placement", flush=True)
+    check_run(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, dur)
+    rng = np.random.default_rng(31337)
+    n, R = 3000, 1000
+    ptr, idx, res, _ = W.random_dag(n, R, 0.002, rng, with_prio=False)
+    dur = W.random_durations(n, 100, 1, 1000, rng)
+    print("random DAG on 1000 resources", flush=True)
+    check_run(mlsim, ptr, idx, res, R, dur)
+    place = rng.integers(0, R, size=(n, 100)).astype(np.uint16)
+    check_run(mlsim, ptr, idx, res, R, dur, place=place)
+
+
 def test_bert_all_knobs(mlsim):
     """Sampled scenarios of every strategy knob of the BERT workload."""
     w = W.make_config(4)
