@@ -72,6 +72,15 @@ struct __attribute__((aligned(16))) LinkSt {
   int32_t k, pad;
 };
 
+// Read-only tables read at wave-uniform indices: through the constant
+// address space such reads become scalar loads.
+template <class T>
+using cptr = const __attribute__((address_space(4))) T *;
+template <class T>
+__device__ __forceinline__ cptr<T> as_const(const T *p) {
+  return (cptr<T>)p;
+}
+
 template <class T>
 struct Lane {  // element i of a lane-major array
   T *p;
@@ -110,13 +119,38 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
     if (s >= a.n_scen) continue;
+    // any duration below 1 flags the scenario before its replay starts:
+    // the whole column, sixteen rows requested at a time (coalesced across
+    // the wave; row ids are uniform, read as scalars)
     uint32_t st = 0;
-    for (int c = 0; c < n; ++c)
-      if (a.dur[(int64_t)G.ops[c].orig * a.ld_dur + s] < 1) st |= SIM_ST_BAD_DUR;
+    {
+      const cptr<OpRec> ops = as_const(G.ops);
+      int32_t dmin = 1;
+      for (int c0 = 0; c0 < n; c0 += 16) {
+        int32_t x[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int c = c0 + j < n ? c0 + j : n - 1;
+          const int row = a.rows_identity ? c : ops[c].orig;
+          x[j] = a.dur[(int64_t)row * a.ld_dur + s];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) dmin = x[j] < dmin ? x[j] : dmin;
+      }
+      if (dmin < 1) st |= SIM_ST_BAD_DUR;
+    }
     uint32_t span = 0;
     if (!st) {
       // {ready 0, count} of every node with two or more predecessors
-      for (int j = 0; j < a.n_slots; ++j) rc[j] = (uint64_t)(uint32_t)a.np_of[j];
+      const cptr<int32_t> np_of = as_const(a.np_of);
+      for (int j0 = 0; j0 < a.n_slots; j0 += 8) {
+        uint64_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (uint64_t)(uint32_t)np_of[j0 + j < a.n_slots ? j0 + j : j0];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (j0 + j < a.n_slots) rc[j0 + j] = v[j];
+      }
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
         lk[r] = LinkSt{0, 0, 0, kNoTime, 0, 0};
