@@ -17,7 +17,9 @@
 // Layout.  One scenario per lane.  A lane's event list is a 4-ary heap in
 // global scratch of 64-bit keys (time << 32 | word), word = resource for a
 // pending finish on a shared resource and n_res + compact id for a ready
-// op, so one key order gives all the tie rules above.  The next finish of a
+// op (with the op's resource in the low bits below the id when it fits, so
+// a popped op's resource state is requested together with its record), so
+// one key order gives all the tie rules above.  The next finish of a
 // shared resource changes when an op arrives; every change pushes a new key
 // and a popped key is used only if it still equals the resource's current
 // next finish (older keys are skipped), so a call's heap holds at most one
@@ -29,6 +31,7 @@
 // resource's free time, each shared resource's 32-byte state record and its
 // active ops.
 #include <algorithm>
+#include <cstring>
 #include <vector>
 
 #include "sim.hpp"
@@ -57,10 +60,26 @@ struct ShArgs {
   int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
   int flags_lds;         // the resource flags are copied to LDS after the heap
   int rows_identity;     // compact ids equal the caller's op ids (duration rows)
-  const int32_t *slot_of;  // [n + barriers] ready/count word of a node with two or more predecessors, else -1
-  const int32_t *np_of;    // [n_slots] predecessors of each such node
+  const int32_t *np_of;  // [n_slots] predecessors of each node with two or more
+  const struct ShRec *rec;  // [n] per op
+  const int2 *sent;      // successor entries of every op (see ShRec)
+  const int32_t *mword;  // key words of barrier members, indexed like the node successor lists
+  const int32_t *srcw;   // [nsrc] key words of the sources
+  int kres, rb;          // ready-op key words hold the resource in their low rb bits
   int32_t n_slots;
   int64_t o_rc, o_rf, o_ln, o_need, o_op;  // byte offsets in a block's region
+};
+
+// One op of the sharing replay (32 bytes): its duration row, its resource,
+// and its successor entries {key word of the node, the node's ready/count
+// word slot or -1}, the first two inline (kShNone: none) and all of them at
+// sent[eb ...].  A node's key word is n_res + (id << rb | resource) for an op
+// (n_res + id when the resource does not fit), or -(x + 1) for a barrier
+// node x, whose members' key words are mword[ws_ptr[x] .. ws_ptr[x + 1]).
+constexpr int32_t kShNone = INT32_MIN;
+struct __attribute__((aligned(16))) ShRec {
+  int32_t orig, res, eb, ne;
+  int32_t w0, s0, w1, s1;
 };
 
 // one shared resource's state in one lane: service units per active op
@@ -198,41 +217,45 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       };
       auto key_of = [](uint32_t t, uint32_t w) -> uint64_t { return ((uint64_t)t << 32) | w; };
       bool ok = true;
-      // every successor of an op finished at t, four nodes at a time: their
-      // ids and predecessor counts, then (nodes with two or more
-      // predecessors) their {ready, count} words are requested together (the
-      // nodes of one list are distinct, and a barrier's members are never
-      // in another node's list, so the words are independent).  A node with
-      // one predecessor is ready at t without touching its word.
-      auto release_all = [&](int e0, int e1, uint32_t t) {
-        for (int eb = e0; eb < e1; eb += 4) {
-          int xs[4], sl[4];
+      // a successor entry {key word w, word slot sl} of an op finished (or
+      // whose outputs arrive) at t, sl's word already read (os): count the
+      // predecessor and, when it was the last, push the node's key (a
+      // barrier pushes its members: it is their only predecessor).  A node
+      // with one predecessor is ready at t without touching a word.
+      auto fire = [&](int32_t w, int32_t sl, uint64_t os, uint32_t t) {
+        if (w == kShNone) return;
+        uint32_t v = t;
+        if (sl >= 0) {
+          const uint32_t r0 = (uint32_t)(os >> 32);
+          v = r0 > t ? r0 : t;
+          const uint32_t left = (uint32_t)os - 1u;
+          rc[sl] = ((uint64_t)v << 32) | left;
+          if (left != 0) return;
+        }
+        if (w >= 0) {
+          ok = ok && push(key_of(v, (uint32_t)w));
+          return;
+        }
+        const int x = -w - 1;
+        for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) ok = ok && push(key_of(v, (uint32_t)a.mword[e]));
+      };
+      // every successor of an op (record halves A {row, resource, first
+      // entry, entries} and B {entries 0 and 1}) at t: the words of the
+      // inline entries requested together, the others four entries at a time
+      // (the nodes of one list are distinct, so the words are independent)
+      auto release_op = [&](const int4 A, const int4 B, uint32_t t) {
+        const uint64_t o0 = B.y >= 0 ? rc[B.y] : 0, o1 = B.w >= 0 ? rc[B.w] : 0;
+        fire(B.x, B.y, o0, t);
+        fire(B.z, B.w, o1, t);
+        for (int e = 2; e < A.w; e += 4) {
+          int2 en[4];
           uint64_t os[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) xs[j] = eb + j < e1 ? G.ws[eb + j] : -1;
+          for (int j = 0; j < 4; ++j) en[j] = e + j < A.w ? a.sent[A.z + e + j] : make_int2(kShNone, -1);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) sl[j] = xs[j] >= 0 ? a.slot_of[xs[j]] : -1;
+          for (int j = 0; j < 4; ++j) os[j] = en[j].y >= 0 ? rc[en[j].y] : 0;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) os[j] = sl[j] >= 0 ? rc[sl[j]] : 0;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (xs[j] < 0) continue;
-            const int x = xs[j];
-            uint32_t v = t;
-            if (sl[j] >= 0) {
-              const uint32_t r0 = (uint32_t)(os[j] >> 32);
-              v = r0 > t ? r0 : t;
-              const uint32_t left = (uint32_t)os[j] - 1u;
-              rc[sl[j]] = ((uint64_t)v << 32) | left;
-              if (left != 0) continue;
-            }
-            if (x < n) {
-              ok = ok && push(key_of(v, (uint32_t)(R + x)));
-              continue;
-            }
-            // a barrier's members: the barrier is their only predecessor
-            for (int e = G.ws_ptr[x]; e < G.ws_ptr[x + 1]; ++e) ok = ok && push(key_of(v, (uint32_t)(R + G.ws[e])));
-          }
+          for (int j = 0; j < 4; ++j) fire(en[j].x, en[j].y, os[j], t);
         }
       };
       auto advance = [](LinkSt &L, uint32_t t) {
@@ -248,7 +271,9 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         const uint64_t t = (uint64_t)L.tl + dt;
         return t > kI32Max ? kI32Max + 1u : (uint32_t)t;
       };
-      for (int k = 0; k < G.nsrc; ++k) ok = ok && push(key_of(0, (uint32_t)(R + G.src[k])));
+      const int4 *rec4 = (const int4 *)a.rec;
+      const uint32_t rmask = (1u << a.rb) - 1u;
+      for (int k = 0; k < G.nsrc; ++k) ok = ok && push(key_of(0, (uint32_t)a.srcw[k]));
       // every iteration pops one key and the keys pushed are bounded by the
       // heap capacity, so the loop ends; the guard only bounds it explicitly
       for (int64_t it = 0; hs > 0 && ok && it <= a.heap_cap; ++it) {
@@ -267,8 +292,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           const uint64_t v_now = L.vt;
           const int64_t base = (int64_t)r * kShareMax;
           // which active ops have their units (bit i: entry i), and the
-          // least need of the others; eight entries requested at a time
-          // (entries from k on are in bounds and ignored)
+          // least need of the others; eight entries (and their ops)
+          // requested at a time (entries from k on are in bounds and ignored)
           uint64_t gone = 0, m_rest = ~0ull;
           for (int i0 = 0; i0 < k; i0 += 8) {
             uint64_t x[8];
@@ -298,10 +323,10 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
               eop[base + i] = eop[base + k - 1];
             }
             --k;
-            const int2 orr = *(const int2 *)&G.ops[c];
-            if (a.finish) a.finish[(int64_t)orr.x * a.ld_fin + s] = (int32_t)t;
+            const int4 A = rec4[2 * c], B = rec4[2 * c + 1];
+            if (a.finish) a.finish[(int64_t)A.x * a.ld_fin + s] = (int32_t)t;
             span = t > span ? t : span;
-            release_all(G.ws_ptr[c], G.ws_ptr[c + 1], t);
+            release_op(A, B, t);
           }
           L.k = k;
           if (k > 0) {
@@ -314,16 +339,23 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           lk[r] = L;
           continue;
         }
-        const int c = (int)(w - (uint32_t)R);
-        // the op's row and resource, its successor range and (identity
-        // rows) its duration, all requested before the first is used
-        const int2 orr = *(const int2 *)&G.ops[c];
-        const int e0 = G.ws_ptr[c], e1 = G.ws_ptr[c + 1];
+        // a ready op: its record, its duration and (the resource named by
+        // the key word) the resource's state, all requested before the first
+        // is used
+        const uint32_t u = w - (uint32_t)R;
+        const int c = a.kres ? (int)(u >> a.rb) : (int)u;
+        const int4 A = rec4[2 * c], B = rec4[2 * c + 1];
         int32_t d = a.rows_identity ? a.dur[(int64_t)c * a.ld_dur + s] : 0;
-        const int row = orr.x, r = orr.y;
-        if (!a.rows_identity) d = a.dur[(int64_t)row * a.ld_dur + s];
-        if (flags[r]) {  // joins the resource's active ops at its ready time
-          LinkSt L = lk[r];
+        const int r = a.kres ? (int)(u & rmask) : A.y;
+        const bool shr = flags[r] != 0;
+        LinkSt L;
+        uint32_t rfree = 0;
+        if (shr)
+          L = lk[r];
+        else
+          rfree = rf[r];
+        if (!a.rows_identity) d = a.dur[(int64_t)A.x * a.ld_dur + s];
+        if (shr) {  // joins the resource's active ops at its ready time
           const int k = L.k;
           if (k == kShareMax) {
             st |= SIM_ST_SHARE_LIMIT;
@@ -340,7 +372,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           ok = ok && push(key_of(L.nd, (uint32_t)r));
           continue;
         }
-        const uint32_t start = t > rf[r] ? t : rf[r];
+        const uint32_t start = t > rfree ? t : rfree;
         const uint32_t f = start + (uint32_t)d;  // both terms <= INT32_MAX
         if (f > kI32Max) {
           st |= SIM_ST_OVERFLOW;
@@ -348,8 +380,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         }
         rf[r] = f;
         span = f > span ? f : span;
-        if (a.finish) a.finish[(int64_t)row * a.ld_fin + s] = (int32_t)f;
-        release_all(e0, e1, f);
+        if (a.finish) a.finish[(int64_t)A.x * a.ld_fin + s] = (int32_t)f;
+        release_op(A, B, f);
       }
       if (!ok) st |= SIM_ST_INTERNAL;
     }
@@ -381,40 +413,88 @@ int64_t share_block_bytes(int64_t R, int64_t cap, int64_t slots, ShArgs *a) {
   return off;
 }
 
-// a set's constant head: the word slot of each node and the predecessor
-// count of each slot (the resource flags before them are written per call)
+// a set's constant head after the resource flags: the graph tables
 int fill_share_set(void *ctx, char *b) {
   const sim_graph *g = (const sim_graph *)ctx;
-  const int64_t R = g->dg.R, N = (int64_t)g->share_slot_of.size();
-  if (hipMemcpy(b + al256(R * 4), g->share_slot_of.data(), (size_t)N * 4, hipMemcpyHostToDevice) != hipSuccess)
-    return SIM_E_HIP;
-  if (!g->share_np.empty() && hipMemcpy(b + al256(R * 4) + al256(N * 4), g->share_np.data(),
-                                        g->share_np.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+  const int64_t R = g->dg.R;
+  if (!g->share_tables.empty() && hipMemcpy(b + al256(R * 4), g->share_tables.data(), g->share_tables.size(),
+                                            hipMemcpyHostToDevice) != hipSuccess)
     return SIM_E_HIP;
   return SIM_OK;
 }
 }  // namespace
 
-// Sized once per graph: the word slots of nodes with two or more
-// predecessors, and one set holding the resource flags, the slot tables and
-// the block regions, sized for the largest heap any call can need (every
-// resource shared) within the budget.  When the device cannot hold the
-// budget, fewer block regions are kept (a call then runs fewer blocks at a
-// time).
+// Sized once per graph: the tables of the replay (the predecessor count of
+// each node with two or more predecessors, per op its record and successor
+// entries, the key words of barrier members and of sources), and one set
+// holding the resource flags, the tables and the block regions, sized for
+// the largest heap any call can need (every resource shared) within the
+// budget.  When the device cannot hold the budget, fewer block regions are
+// kept (a call then runs fewer blocks at a time).
 int plan_share(sim_graph *g) {
   const DevGraph &G = g->dg;
-  const int64_t N = (int64_t)G.n + G.nb, R = G.R;
-  std::vector<int32_t> wp((size_t)N + 1);
-  if (hipMemcpy(wp.data(), G.wp_ptr, wp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess) return SIM_E_HIP;
-  g->share_slot_of.assign((size_t)N, -1);
-  g->share_np.clear();
+  const int64_t n = G.n, N = (int64_t)G.n + G.nb, R = G.R;
+  std::vector<int32_t> wp((size_t)N + 1), wsp((size_t)N + 1), src((size_t)G.nsrc);
+  if (hipMemcpy(wp.data(), G.wp_ptr, wp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(wsp.data(), G.ws_ptr, wsp.size() * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      (G.nsrc && hipMemcpy(src.data(), G.src, src.size() * 4, hipMemcpyDeviceToHost) != hipSuccess))
+    return SIM_E_HIP;
+  std::vector<int32_t> ws((size_t)wsp[N]);
+  if (!ws.empty() && hipMemcpy(ws.data(), G.ws, ws.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return SIM_E_HIP;
+  // word slot of each node with two or more predecessors, and their counts
+  std::vector<int32_t> slot_of((size_t)N, -1), np;
   for (int64_t x = 0; x < N; ++x)
     if (wp[x + 1] - wp[x] > 1) {
-      g->share_slot_of[x] = (int32_t)g->share_np.size();
-      g->share_np.push_back(wp[x + 1] - wp[x]);
+      slot_of[x] = (int32_t)np.size();
+      np.push_back(wp[x + 1] - wp[x]);
     }
-  g->share_slots = (int32_t)g->share_np.size();
-  const int64_t head = al256(R * 4) + al256(N * 4) + al256(std::max<size_t>(g->share_np.size(), 1) * 4);
+  g->share_slots = (int32_t)np.size();
+  // key word of a ready op: n_res + (id << rb | resource) when that fits 32
+  // bits, else n_res + id; a barrier node x is named -(x + 1)
+  int32_t rb = 0;
+  while ((1ll << rb) < R) ++rb;
+  const bool kres = R + ((int64_t)n << rb) <= (int64_t)UINT32_MAX;
+  g->share_kres = kres;
+  g->share_rb = kres ? rb : 0;
+  auto res_of = [&](int64_t c) { return g->h_res[g->h_orig_of[c]]; };
+  auto word = [&](int64_t x) -> int32_t {
+    if (x >= n) return (int32_t)(-(x + 1));
+    return (int32_t)(uint32_t)(R + (kres ? ((uint64_t)x << rb | (uint64_t)res_of(x)) : (uint64_t)x));
+  };
+  std::vector<ShRec> rec((size_t)n);
+  std::vector<int2> sent;
+  for (int64_t c = 0; c < n; ++c) {
+    ShRec r{g->h_orig_of[c], res_of(c), (int32_t)sent.size(), wsp[c + 1] - wsp[c], kShNone, -1, kShNone, -1};
+    for (int32_t e = wsp[c]; e < wsp[c + 1]; ++e) sent.push_back(make_int2(word(ws[e]), slot_of[ws[e]]));
+    if (r.ne > 0) r.w0 = sent[r.eb].x, r.s0 = sent[r.eb].y;
+    if (r.ne > 1) r.w1 = sent[r.eb + 1].x, r.s1 = sent[r.eb + 1].y;
+    rec[c] = r;
+  }
+  std::vector<int32_t> mword(ws.size(), 0), srcw(src.size());
+  for (int64_t x = n; x < N; ++x)  // barrier members (ops)
+    for (int32_t e = wsp[x]; e < wsp[x + 1]; ++e) mword[e] = word(ws[e]);
+  for (size_t k = 0; k < src.size(); ++k) srcw[k] = word(src[k]);
+  // the tables, each 256-byte aligned, after the flags
+  auto place = [](int64_t &off, int64_t bytes) {
+    const int64_t o = off;
+    off += al256(std::max<int64_t>(bytes, 4));
+    return o;
+  };
+  int64_t off = 0;
+  g->share_o_np = place(off, (int64_t)np.size() * 4);
+  g->share_o_rec = place(off, (int64_t)rec.size() * (int64_t)sizeof(ShRec));
+  g->share_o_sent = place(off, (int64_t)sent.size() * 8);
+  g->share_o_mword = place(off, (int64_t)mword.size() * 4);
+  g->share_o_srcw = place(off, (int64_t)srcw.size() * 4);
+  g->share_tables.assign((size_t)off, 0);
+  char *t = g->share_tables.data();
+  if (!np.empty()) std::memcpy(t + g->share_o_np, np.data(), np.size() * 4);
+  if (!rec.empty()) std::memcpy(t + g->share_o_rec, rec.data(), rec.size() * sizeof(ShRec));
+  if (!sent.empty()) std::memcpy(t + g->share_o_sent, sent.data(), sent.size() * 8);
+  if (!mword.empty()) std::memcpy(t + g->share_o_mword, mword.data(), mword.size() * 4);
+  if (!srcw.empty()) std::memcpy(t + g->share_o_srcw, srcw.data(), srcw.size() * 4);
+  const int64_t head = al256(R * 4) + off;
   const int64_t worst = share_block_bytes(R, 3 * (int64_t)G.n + 1, g->share_slots, nullptr);
   int64_t region = std::max(worst, std::min(kShareScratchBudget, kShareBlocksMax * worst));
   g->share_head = head;
@@ -432,7 +512,7 @@ int launch_share(const sim_graph *g, char *b, int64_t n_scen, const int32_t *dur
                  const int32_t *share_words, int32_t *makespan, int32_t *finish, int64_t ld_fin, int32_t *status,
                  hipStream_t stream) {
   const DevGraph &G = g->dg;
-  const int64_t N = (int64_t)G.n + G.nb, R = G.R;
+  const int64_t R = G.R;
   // this call's heap: every ready op once, and two keys per op on a shared
   // resource (its arrival and at most one departure batch)
   int64_t m_sh = 0;
@@ -464,8 +544,14 @@ int launch_share(const sim_graph *g, char *b, int64_t n_scen, const int32_t *dur
   a.ld_fin = ld_fin;
   a.status = status;
   a.share = flags;
-  a.slot_of = (const int32_t *)(b + al256(R * 4));
-  a.np_of = (const int32_t *)(b + al256(R * 4) + al256(N * 4));
+  const char *tab = b + al256(R * 4);
+  a.np_of = (const int32_t *)(tab + g->share_o_np);
+  a.rec = (const ShRec *)(tab + g->share_o_rec);
+  a.sent = (const int2 *)(tab + g->share_o_sent);
+  a.mword = (const int32_t *)(tab + g->share_o_mword);
+  a.srcw = (const int32_t *)(tab + g->share_o_srcw);
+  a.kres = g->share_kres;
+  a.rb = g->share_rb;
   a.n_slots = g->share_slots;
   a.scratch = b + g->share_head;
   k_share<<<dim3((unsigned)blocks), dim3(kWave), lds, stream>>>(G, a);

@@ -234,11 +234,13 @@ struct sim_graph {
   std::vector<int32_t> h_orig_of, h_pred_ptr, h_pred, h_res;
   size_t scratch_bytes;
   // bandwidth-sharing replay: a set holds the resource flags of the current
-  // call, the word slots of joining nodes, then the per-block regions of its
-  // persistent grid
-  int64_t share_head = 0, share_region = 0;  // bytes of flags and slot tables; of block regions
+  // call, the graph tables below (constant), then the per-block regions of
+  // its persistent grid
+  int64_t share_head = 0, share_region = 0;  // bytes of flags and tables; of block regions
   int32_t share_slots = 0;                    // nodes with two or more predecessors
-  std::vector<int32_t> share_slot_of, share_np;  // host copies of the slot tables
+  int32_t share_kres = 0, share_rb = 0;       // ready-op key words hold the resource (rb bits)
+  std::vector<char> share_tables;             // host copy of the tables (after the flags)
+  int64_t share_o_np = 0, share_o_rec = 0, share_o_sent = 0, share_o_mword = 0, share_o_srcw = 0;
 };
 
 namespace mlsim {
