@@ -23,8 +23,8 @@
 // shared resource changes when an op arrives; every change pushes a new key
 // and a popped key is used only if it still equals the resource's current
 // next finish (older keys are skipped), so a call's heap holds at most one
-// key per ready op and two per op on a shared resource.  The heap's top 72
-// positions live in LDS (36 KB, four wavefronts per CU), the rest and all
+// key per ready op and two per op on a shared resource.  The heap's top
+// three levels (21 positions, 10.5 KB) live in LDS, the rest and all
 // other per-lane state in global scratch, lane-major ([index][64]): the
 // {ready time, count} word of each node with two or more predecessors (a
 // node with one predecessor is ready when it finishes and needs none), each
@@ -42,7 +42,7 @@ namespace {
 
 constexpr uint32_t kI32Max = 0x7fffffffu;
 constexpr uint32_t kNoTime = 0xffffffffu;
-constexpr int64_t kShareHeapLds = 72;    // heap positions per lane in LDS: 36 KB per wavefront (four per CU)
+constexpr int64_t kShareHeapLds = 21;    // heap positions per lane in LDS: the top three levels (10.5 KB per wavefront)
 constexpr int64_t kShareFlagsLds = 1024; // resource flags in LDS (4 KB) up to this many resources
 
 struct ShArgs {
@@ -56,7 +56,8 @@ struct ShArgs {
   const int32_t *share;  // [R] 0 / 1
   char *scratch;         // per block: the regions below, lane-major
   int64_t block_bytes;
-  int64_t heap_cap;      // heap entries per lane
+  int64_t heap_cap;      // heap entries per lane (keys present at once)
+  int64_t max_keys;      // keys pushed over a whole replay (bounds its pops)
   int heap_lds;          // heap positions per lane kept in LDS (the top of the heap)
   int flags_lds;         // the resource flags are copied to LDS after the heap
   int rows_identity;     // compact ids equal the caller's op ids (duration rows)
@@ -274,9 +275,9 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       const int4 *rec4 = (const int4 *)a.rec;
       const uint32_t rmask = (1u << a.rb) - 1u;
       for (int k = 0; k < G.nsrc; ++k) ok = ok && push(key_of(0, (uint32_t)a.srcw[k]));
-      // every iteration pops one key and the keys pushed are bounded by the
-      // heap capacity, so the loop ends; the guard only bounds it explicitly
-      for (int64_t it = 0; hs > 0 && ok && it <= a.heap_cap; ++it) {
+      // every iteration pops one key and a replay pushes at most max_keys,
+      // so the loop ends; the guard only bounds it explicitly
+      for (int64_t it = 0; hs > 0 && ok && it <= a.max_keys; ++it) {
         const uint64_t key = pop();
         const uint32_t t = (uint32_t)(key >> 32), w = (uint32_t)key;
         if (w < (uint32_t)R) {  // a pending finish on shared resource w
@@ -495,7 +496,7 @@ int plan_share(sim_graph *g) {
   if (!mword.empty()) std::memcpy(t + g->share_o_mword, mword.data(), mword.size() * 4);
   if (!srcw.empty()) std::memcpy(t + g->share_o_srcw, srcw.data(), srcw.size() * 4);
   const int64_t head = al256(R * 4) + off;
-  const int64_t worst = share_block_bytes(R, 3 * (int64_t)G.n + 1, g->share_slots, nullptr);
+  const int64_t worst = share_block_bytes(R, (int64_t)G.heap_cap + 2 * (int64_t)G.n + 1, g->share_slots, nullptr);
   int64_t region = std::max(worst, std::min(kShareScratchBudget, kShareBlocksMax * worst));
   g->share_head = head;
   for (;;) {
@@ -513,14 +514,17 @@ int launch_share(const sim_graph *g, char *b, int64_t n_scen, const int32_t *dur
                  hipStream_t stream) {
   const DevGraph &G = g->dg;
   const int64_t R = G.R;
-  // this call's heap: every ready op once, and two keys per op on a shared
-  // resource (its arrival and at most one departure batch)
+  // this call's heap: the ready ops not yet popped, which form an antichain
+  // (a path between two of them would pass an unfinished predecessor), so
+  // at most the minimum path cover of the DAG, plus two keys per op on a
+  // shared resource (its arrival and at most one departure batch)
   int64_t m_sh = 0;
   for (int32_t v = 0; v < g->n_ops; ++v) m_sh += share_words[g->h_res[v]] != 0;
-  const int64_t cap = (int64_t)G.n + 2 * m_sh + 1;
+  const int64_t cap = (int64_t)G.heap_cap + 2 * m_sh + 1;
   ShArgs a{};
   a.block_bytes = share_block_bytes(R, cap, g->share_slots, &a);
   a.heap_cap = cap;
+  a.max_keys = (int64_t)G.n + 2 * m_sh + 1;
   // LDS: the heap's top positions, then the resource flags when they are few
   a.flags_lds = R <= kShareFlagsLds;
   a.heap_lds = (int)std::min<int64_t>(cap, kShareHeapLds);
