@@ -312,6 +312,7 @@ struct EvArgs {
   uint32_t *rfree_g;  // [blocks][R][64] when resource times are not in LDS
   int32_t *prev;      // [n_ops][ld_fin] (PREV): the op that ran before each op on its resource, -1: none
   int32_t *last_g;    // [blocks][R][64] (PREV, resource times not in LDS): last op run per resource
+  int last16;         // PREV with resource times in LDS: the last-op table holds 16-bit rows (0xffff: none)
   DurGen gen;         // GEN: durations generated from a knob grid and counter-based noise
   // device model, or null: [2R] words, each resource's idle time between
   // consecutive ops (gap) and then the time from an op's finish until its
@@ -536,11 +537,17 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       rfree_g[r * kWave] = v;
   };
   // PREV: the last op (row) each resource ran, next to the resource times
+  // (in 16 bits when every row fits: half the LDS)
   lptr<int32_t> last_l = as_lds((int32_t *)(lds + (size_t)heap_lds * kWave) + (size_t)R * kWave) + lane;
+  lptr<uint16_t> last_h = as_lds((uint16_t *)(lds + (size_t)heap_lds * kWave) + (size_t)2 * R * kWave) + lane;
   int32_t *last_g = PREV && !RF_LDS ? a.last_g + (size_t)blockIdx.x * R * kWave + lane : nullptr;
   auto last_xchg = [&](int r, int32_t row) -> int32_t {
     int32_t x;
-    if (RF_LDS) {
+    if (RF_LDS && a.last16) {
+      const uint32_t h = last_h[r * kWave];
+      x = h == 0xffffu ? -1 : (int32_t)h;
+      last_h[r * kWave] = (uint16_t)row;
+    } else if (RF_LDS) {
       x = last_l[r * kWave];
       last_l[r * kWave] = row;
     } else {
@@ -562,7 +569,9 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     for (int r = 0; r < R; ++r) rf_set(r, 0);
     if (PREV)
       for (int r = 0; r < R; ++r) {
-        if (RF_LDS)
+        if (RF_LDS && a.last16)
+          last_h[r * kWave] = 0xffffu;
+        else if (RF_LDS)
           last_l[r * kWave] = -1;
         else
           last_g[r * kWave] = -1;
@@ -1139,7 +1148,10 @@ int plan_scratch(sim_graph *g) {
   P.ev_reg = rf_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
   P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_dev_blocks = P.ev_reg_prev_blocks = 1;
-  P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + rf_lds_bytes;  // with the last-op table
+  // the last-op table of attribution: 16-bit rows when every row fits
+  P.ev_last16 = G.n < 0xffff;
+  const size_t last_lds_bytes = P.ev_last16 ? rf_lds_bytes / 2 : rf_lds_bytes;
+  P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + last_lds_bytes;  // with the last-op table
   if (P.ev_reg) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
@@ -1155,7 +1167,7 @@ int plan_scratch(sim_graph *g) {
     P.ev_reg_prev_blocks = grid_of(prev_occ);
   }
   // the event kernel for attribution: a last-op table beside the resource times
-  P.ev_prev_lds_bytes = P.ev_lds_bytes + rf_lds_bytes;
+  P.ev_prev_lds_bytes = P.ev_lds_bytes + last_lds_bytes;
   const int ev_prev_occ = rf_lds ? occupancy_blocks(k_event<true, false, false, true>, P.ev_prev_lds_bytes, cus)
                                 : occupancy_blocks(k_event<false, false, false, true>, P.ev_prev_lds_bytes, cus);
   if (ev_prev_occ < 0) return SIM_E_HIP;
@@ -1173,7 +1185,7 @@ int plan_scratch(sim_graph *g) {
       wo[0] = occupancy_blocks(k_event<true, false, false, false>, wl, cus, true);
       wo[1] = occupancy_blocks(k_event<true, false, false, false, true>, wl, cus, true);
       wo[2] = occupancy_blocks(k_event<true, false, false, false>, wl + dev_table, cus, true);
-      wo[3] = occupancy_blocks(k_event<true, false, false, true>, wl + rf_lds_bytes, cus, true);
+      wo[3] = occupancy_blocks(k_event<true, false, false, true>, wl + last_lds_bytes, cus, true);
     } else {
       wo[0] = occupancy_blocks(k_event<false, false, false, false>, wl, cus, true);
       wo[1] = occupancy_blocks(k_event<false, false, false, false, true>, wl, cus, true);
@@ -1289,7 +1301,8 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
            ext ? ext->heap : (uint64_t *)(base + g->scratch_ev_heap_off), P.ev_heap_stride, P.ev_heap_le,
            ext ? ext->join : (int2 *)(base + g->scratch_ev_join_off),
            ext ? ext->rf : (uint32_t *)(base + g->scratch_ev_rf_off),
-           prev, ext ? nullptr : (int32_t *)(base + g->scratch_ev_last_off), DurGen{}, dev, has_gap, has_delay, 0};
+           prev, ext ? nullptr : (int32_t *)(base + g->scratch_ev_last_off), P.ev_last16, DurGen{}, dev, has_gap,
+           has_delay, 0};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = P.rf_lds;
@@ -1316,7 +1329,7 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
     if (tiles <= wide) {
       blocks = wide;
       a.heap_le = P.ev_wide_le;
-      lds = P.ev_wide_lds_bytes + (prev && rf_lds ? (size_t)g->dg.R * kWave * 4 : 0);
+      lds = P.ev_wide_lds_bytes + (prev && rf_lds ? (size_t)g->dg.R * kWave * (P.ev_last16 ? 2 : 4) : 0);
     }
   }
   if (ext) blocks = std::min(blocks, ext->max_blocks);

@@ -142,6 +142,7 @@ struct ScratchPlan {
   size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   int32_t rf_lds;       // event kernel: resource times in LDS (1) or global scratch (0)
+  int32_t ev_last16;    // attribution's last-op table in 16-bit rows (every row below 0xffff)
   // event kernel with the heap's whole third level in LDS (heap_le
   // ev_wide_le), for calls whose tiles all fit these grids (plain, generated
   // durations, device model, recording predecessors; 0: not planned) and

@@ -119,6 +119,28 @@ def test_attr_heap_children_in_registers(mlsim, groups, pin_variants):
         check_attr(mlsim, ptr, idx, res, R, dur, prio=pr, path_scen=int(rng.integers(S)))
 
 
+def test_attr_wide_rows(mlsim):
+    """A graph with more ops than 16-bit rows can name (70000): the last-op
+    table keeps 32-bit rows; checked against the oracle on a few scenarios."""
+    rng = np.random.default_rng(65536)
+    n, R = 70000, 8
+    # op v > 0 takes one or two predecessors among the 64 ops before it
+    v = np.repeat(np.arange(1, n), 2)
+    u = v - rng.integers(1, 65, size=v.size)
+    keep = (u >= 0) & ((np.arange(v.size) % 2 == 0) | (rng.random(v.size) < 0.5))
+    u, v = u[keep], v[keep]
+    order = np.lexsort((v, u))
+    u, v = u[order], v[order]
+    ptr = np.zeros(n + 1, np.int64)
+    np.add.at(ptr, u + 1, 1)
+    ptr = np.cumsum(ptr)
+    idx = v.astype(np.int32)
+    res = rng.integers(0, R, size=n).astype(np.int32)
+    dur = W.random_durations(n, 70, 1, 1000, rng)
+    print(f"attribution on {n} ops", flush=True)
+    check_attr(mlsim, ptr, idx, res, R, dur, path_scen=3)
+
+
 def test_attr_status_and_empty(mlsim):
     ptr = np.array([0, 1, 2, 2], np.int64)
     idx = np.array([1, 2], np.int32)
