@@ -322,7 +322,10 @@ struct EvArgs {
   int dev_lds;             // byte offset of the device-model table in LDS (when dev is set)
 };
 
-constexpr int kFinQ = 8;                 // finish times buffered per lane before a store burst
+// finish times buffered per lane before a store burst: sixteen where the
+// registers allow it without costing occupancy (the register-children
+// variants, which run two wavefronts per SIMD anyway), else eight
+constexpr int kFinQ = 8, kFinQWide = 16;
 
 // A lane's join state {predecessors finished, max finish} per join index, in
 // global scratch ([J][64] int2).
@@ -334,14 +337,14 @@ struct JoinGlobal {
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
 template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class Heap, class JPtr,
-          class RfGet, class RfSet, class LastXchg, class Flush>
+          class RfGet, class RfSet, class LastXchg, class Flush, int FQ>
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, Heap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
                                            uint32_t s_hi, lptr<const int32_t> dev_l, uint32_t &st,
                                            uint32_t &span,
-                                           int32_t (&fq)[kFinQ], int32_t (&rq)[kFinQ],
-                                           int32_t (&pq)[kFinQ], RfGet rf_get, RfSet rf_set,
+                                           int32_t (&fq)[FQ], int32_t (&rq)[FQ],
+                                           int32_t (&pq)[FQ], RfGet rf_get, RfSet rf_set,
                                            LastXchg last_xchg, Flush flush) {
   const int R = G.R;
   const int2 *succ = (const int2 *)G.ev_succ;
@@ -443,15 +446,15 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   }
   js0 = settle(js0);
   ji0 = settle(ji0);
-  const int qs = it & (kFinQ - 1);  // wave-uniform
+  const int qs = it & (FQ - 1);  // wave-uniform
 #pragma unroll
-  for (int k = 0; k < kFinQ; ++k)
+  for (int k = 0; k < FQ; ++k)
     if (k == qs) {
       fq[k] = (int32_t)fin;
       rq[k] = row;
       if (PREV) pq[k] = before;
     }
-  if (qs == kFinQ - 1) flush(kFinQ);
+  if (qs == FQ - 1) flush(FQ);
   bool hole = true;  // the root was popped and is not yet replaced
   auto release = [&](uint32_t t, int w) {
     const uint64_t nk = make_key(t, w);
@@ -504,7 +507,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
 // comes from the key word, or when it has no room from a load by row issued
 // with the record).
 // PLACE: resources come from the per-scenario placement matrix.  Finish times
-// are written in bursts of kFinQ stores per lane, so their completion is
+// are written in bursts of kFinQ (or kFinQWide) stores per lane, so their completion is
 // waited for once per burst instead of once per step.  GEN: durations are
 // generated from the knob grid and counter-based noise of a.gen instead of
 // read from a.dur.  REG: the heap
@@ -584,10 +587,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.ev_src[k]));
     uint32_t st = 0, span = 0;
-    int32_t fq[kFinQ], rq[kFinQ], pq[kFinQ];  // buffered finish times, their rows, previous ops
+    constexpr int kQ = REG && !PREV ? kFinQWide : kFinQ;
+    int32_t fq[kQ], rq[kQ], pq[kQ];  // buffered finish times, their rows, previous ops
     auto flush = [&](int cnt) {
 #pragma unroll
-      for (int k = 0; k < kFinQ; ++k)
+      for (int k = 0; k < kQ; ++k)
         if (k < cnt && store_fin) {
           a.finish[(int64_t)rq[k] * a.ld_fin + s] = fq[k];
           if (PREV) a.prev[(int64_t)rq[k] * a.ld_fin + s] = pq[k];
@@ -608,7 +612,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       };
       run_step(jst_g);
     }
-    flush(n & (kFinQ - 1));
+    flush(n & (kQ - 1));
     if (st & (SIM_ST_BAD_DUR | SIM_ST_BAD_RES)) st &= ~(uint32_t)SIM_ST_OVERFLOW;
     if (active) {
       a.makespan[s] = st ? -1 : (int32_t)span;
