@@ -323,8 +323,9 @@ struct EvArgs {
 };
 
 // finish times buffered per lane before a store burst: sixteen where the
-// registers allow it without costing occupancy (the register-children
-// variants, which run two wavefronts per SIMD anyway), else eight
+// registers allow it without costing occupancy and it measured faster (the
+// register-children variants, which run two wavefronts per SIMD anyway,
+// with loaded durations), else eight
 constexpr int kFinQ = 8, kFinQWide = 16;
 
 // A lane's join state {predecessors finished, max finish} per join index, in
@@ -587,7 +588,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.ev_src[k]));
     uint32_t st = 0, span = 0;
-    constexpr int kQ = REG && !PREV ? kFinQWide : kFinQ;
+    constexpr int kQ = REG && !PREV && !GEN ? kFinQWide : kFinQ;
     int32_t fq[kQ], rq[kQ], pq[kQ];  // buffered finish times, their rows, previous ops
     auto flush = [&](int cnt) {
 #pragma unroll
