@@ -31,7 +31,9 @@ enum {
                                  -1: auto (registers when the chip is full) */
   SIM_TEST_CP_GLOBAL = 5,     /* value 0/1: the max-plus sweeps' value slots in global scratch (1) even
                                  when LDS holds them (static-order replays created afterwards too) */
-  SIM_TEST_RF_GLOBAL = 6      /* value 0/1: the event kernel's resource times in global scratch (1) */
+  SIM_TEST_RF_GLOBAL = 6,     /* value 0/1: the event kernel's resource times in global scratch (1) */
+  SIM_TEST_SHARE_KEY_ID = 7   /* value 0/1: the sharing replay's ready-op key words hold only the op id
+                                 (1), as for graphs whose ids and resources do not fit 32 bits together */
 };
 
 /*

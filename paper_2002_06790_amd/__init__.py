@@ -29,7 +29,7 @@ SIM_ALGO_AUTO, SIM_ALGO_EVENT, SIM_ALGO_SWEEP = 0, 1, 2
 ALGOS = {"auto": SIM_ALGO_AUTO, "event": SIM_ALGO_EVENT, "sweep": SIM_ALGO_SWEEP}
 #: kernel-variant pins of the testing entry point (include/mlsim_testing.h)
 TEST_VARIANTS = {"auto": 0, "ev_lds_groups": 1, "ev_blocks_cap": 3, "ev_reg": 4, "cp_global": 5,
-                 "rf_global": 6}
+                 "rf_global": 6, "share_key_id": 7}
 
 EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critical_path",
            "sim_strerror", "sim_graph_info", "sim_testing_replan", "sim_static_create",

@@ -836,12 +836,18 @@ extern "C" int sim_testing_replan(sim_graph *g, int32_t what, int32_t value) {
       if (value < 0 || value > 1) return SIM_E_INVAL;
       v.rf_global = value;
       break;
+    case SIM_TEST_SHARE_KEY_ID:
+      if (value < 0 || value > 1) return SIM_E_INVAL;
+      v.share_key_id = value;
+      break;
     default: return SIM_E_INVAL;
   }
   // no call may be in flight: the old sets are freed
   if (hipDeviceSynchronize() != hipSuccess) return SIM_E_HIP;
+  const bool share_again = v.share_key_id != g->var.share_key_id;
   g->var = v;
-  return plan_scratch(g);
+  if (int rc = plan_scratch(g)) return rc;
+  return share_again ? plan_share(g) : SIM_OK;
 }
 
 extern "C" int sim_graph_info(const sim_graph *g, int32_t *n_ops, int32_t *n_res, int64_t *n_edges,

@@ -455,7 +455,7 @@ int plan_share(sim_graph *g) {
   // bits, else n_res + id; a barrier node x is named -(x + 1)
   int32_t rb = 0;
   while ((1ll << rb) < R) ++rb;
-  const bool kres = R + ((int64_t)n << rb) <= (int64_t)UINT32_MAX;
+  const bool kres = R + ((int64_t)n << rb) <= (int64_t)UINT32_MAX && !g->var.share_key_id;
   g->share_kres = kres;
   g->share_rb = kres ? rb : 0;
   auto res_of = [&](int64_t c) { return g->h_res[g->h_orig_of[c]]; };

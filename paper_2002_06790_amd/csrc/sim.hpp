@@ -160,6 +160,7 @@ struct Variant {
   int32_t ev_reg = -1;         // heap root's children in registers (0/1), -1: auto
   int32_t cp_global = 0;       // max-plus value slots in global scratch (1) even when LDS holds them
   int32_t rf_global = 0;       // resource times in global scratch (1) even when LDS holds them
+  int32_t share_key_id = 0;    // sharing replay: ready-op key words without the resource (1)
 };
 
 // A few copies ("sets") of one scratch layout.  Every call takes one set for

@@ -92,6 +92,25 @@ def test_workload_parity(mlsim, k, S):
     assert (ost == 0).all()
 
 
+def test_key_words_without_the_resource(mlsim, pin_variants):
+    """Ready-op key words holding only the op id (the layout for graphs whose
+    ids and resources do not fit 32 bits together; pinned here): the
+    resource then comes from the op's record, with the same results."""
+    pin_variants(share_key_id=1)
+    for k, S in ((4, 130), (2, 70)):
+        w = W.make_config(k, n_scen=S)
+        share = np.zeros(w.n_res, np.uint8)
+        share[W.link_resources(w)] = 1
+        print(f"share workload {w.name} S={S}, id-only key words", flush=True)
+        check(mlsim, w.succ_ptr, w.succ_idx, w.op_res, w.n_res, w.durations(), share, prio=w.prio)
+    rng = np.random.default_rng(63)
+    for n, R, p in ((60, 3, 0.1), (200, 6, 0.05)):
+        ptr, idx, res, prio = W.random_dag(n, R, p, rng, with_prio=True, dup_edges=True)
+        share = (rng.random(R) < 0.5).astype(np.uint8)
+        share[0] = 1
+        check(mlsim, ptr, idx, res, R, W.random_durations(n, 97, 1, 5000, rng), share, prio=prio)
+
+
 def test_nothing_shared_is_the_plain_replay(mlsim):
     w = W.make_config(4, n_scen=256)
     dur = dev(w.durations())
