@@ -490,7 +490,7 @@ def main():
                      "bytes_per_launch": alg_bytes,
                      "limiter": "the CUs' vector memory address path: every step issues about 6.4 "
                                 "lane-divergent loads and stores (record, duration, heap levels beyond LDS, "
-                                "join state, finish bursts) and the TA units are busy 74% of the launch "
+                                "join state, finish bursts) and the TA units are busy 66% of the launch "
                                 "(profiles/); the roofline axis is HBM bytes, which the kernel does not reach"},
         "cpu_baseline": cpu,
         "parity": parity,

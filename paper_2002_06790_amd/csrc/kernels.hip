@@ -448,13 +448,23 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   js0 = settle(js0);
   ji0 = settle(ji0);
   const int qs = it & (FQ - 1);  // wave-uniform
+  if (!PLACE && !GEN) {
+    // one indexed register move per array (the index is in a scalar register);
+    // the placement and generated-duration kernels keep the compare chain,
+    // which times faster there
+    const int q = __builtin_amdgcn_readfirstlane(qs);
+    fq[q] = (int32_t)fin;
+    rq[q] = row;
+    if (PREV) pq[q] = before;
+  } else {
 #pragma unroll
-  for (int k = 0; k < FQ; ++k)
-    if (k == qs) {
-      fq[k] = (int32_t)fin;
-      rq[k] = row;
-      if (PREV) pq[k] = before;
-    }
+    for (int k = 0; k < FQ; ++k)
+      if (k == qs) {
+        fq[k] = (int32_t)fin;
+        rq[k] = row;
+        if (PREV) pq[k] = before;
+      }
+  }
   if (qs == FQ - 1) flush(FQ);
   bool hole = true;  // the root was popped and is not yet replaced
   auto release = [&](uint32_t t, int w) {
