@@ -8,7 +8,8 @@
  * sim_testing_replan pins a graph to one of them so that a test can check
  * each variant against the oracle.  No environment variable or other hidden
  * state selects a variant.  sim_testing_sweep_table returns the max-plus
- * sweep table built for a graph, for CPU tests of the table builder.
+ * sweep table built for a graph, for CPU tests of the table builder, and
+ * sim_testing_join_slots the event replay's join state slots.
  */
 #ifndef MLSIM_TESTING_H
 #define MLSIM_TESTING_H
@@ -68,6 +69,23 @@ int sim_testing_sweep_table(int32_t n_ops, int32_t n_res, const int64_t *succ_pt
                             const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
                             const int32_t *order, int32_t *n_rec, int32_t *slots, int32_t *rec,
                             int64_t rec_cap, int32_t *plist, int64_t plist_cap, int64_t *plist_len);
+
+/*
+ * The join state slots of the event replay (sim_run_batch and the calls
+ * built on it), on the host only.  An op whose predecessors, after removing
+ * edges implied by longer paths, number two or more waits on a join: a
+ * {predecessors finished, latest finish} word per lane, which the replay
+ * updates when each of those predecessors finishes and clears when the last
+ * one does.  Ops with the same predecessor set share one join.  Joins whose
+ * words are never needed at the same time in any scenario may share a slot
+ * (the replay's scratch then holds fewer words).  The graph arguments are
+ * those of sim_graph_create.  Outputs (host): slot_of [n_ops]: the slot of
+ * the join each op waits on, -1 for an op without one; *n_slots: the number
+ * of slots.  Returns SIM_OK or the argument errors of sim_graph_create.
+ */
+int sim_testing_join_slots(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                           const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                           int32_t *slot_of, int32_t *n_slots);
 
 #ifdef __cplusplus
 }

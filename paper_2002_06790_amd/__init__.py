@@ -35,7 +35,8 @@ EXPORTS = ("sim_graph_create", "sim_graph_destroy", "sim_run_batch", "sim_critic
            "sim_strerror", "sim_graph_info", "sim_testing_replan", "sim_static_create",
            "sim_static_destroy", "sim_static_run", "sim_attribute", "sim_generate", "sim_run_generated",
            "sim_critical_path_generated", "sim_run_batch_gap", "sim_static_run_generated",
-           "sim_run_batch_dev", "sim_run_batch_share", "sim_run_batch_noalloc", "sim_testing_sweep_table")
+           "sim_run_batch_dev", "sim_run_batch_share", "sim_run_batch_noalloc", "sim_testing_sweep_table",
+           "sim_testing_join_slots")
 
 #: generator limits (include/mlsim.h): largest base duration, noise bound
 SIM_GEN_BASE_MAX, SIM_GEN_NOISE_MAX = 1 << 24, 1 << 20
@@ -110,6 +111,8 @@ def _load():
     L.sim_static_run_generated.restype = ctypes.c_int
     L.sim_testing_sweep_table.argtypes = [I32, I32, P, P, P, P, P, P, P, P, I64, P, I64, P]
     L.sim_testing_sweep_table.restype = ctypes.c_int
+    L.sim_testing_join_slots.argtypes = [I32, I32, P, P, P, P, P, P]
+    L.sim_testing_join_slots.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -150,6 +153,27 @@ def sweep_table(succ_ptr, succ_idx, op_res, n_res: int, prio=None, order=None):
         rec = np.zeros((n_rec.value, 8), np.int32)
         plist = np.zeros(max(plen.value, 1), np.int32)
     raise SimError(SIM_E_LIMIT, "sim_testing_sweep_table")
+
+
+def join_slots(succ_ptr, succ_idx, op_res, n_res: int, prio=None):
+    """The event replay's join state slots for a graph, on the host only
+    (sim_testing_join_slots).  Returns ``(slot_of int32 [n_ops], n_slots)``:
+    the slot of the join each op waits on (-1: none)."""
+    L = _load()
+    ptr = _host(succ_ptr, np.int64)
+    idx = _host(succ_idx, np.int32)
+    res = _host(op_res, np.int32)
+    pr = _host(prio, np.int32)
+    n = int(ptr.size - 1)
+    if res.size != n or (pr is not None and pr.size != n):
+        raise ValueError("op_res and prio need one entry per op")
+    slot_of = np.full(max(n, 1), -2, np.int32)
+    n_slots = ctypes.c_int32()
+    rc = L.sim_testing_join_slots(n, int(n_res), _hptr(ptr), _hptr(idx), _hptr(res), _hptr(pr),
+                                  _hptr(slot_of), ctypes.byref(n_slots))
+    if rc != SIM_OK:
+        raise SimError(rc, "sim_testing_join_slots")
+    return slot_of[:n].copy(), n_slots.value
 
 
 def _host(a, dt):

@@ -37,7 +37,9 @@ struct Compiled {
   std::vector<int32_t> ev_rec16;  // [n][4] compact event records (ev_compact)
   std::vector<int32_t> wp_ptr, wp, ws_ptr, ws;  // walk: predecessors / successors, barriers as nodes
   std::vector<CpRec> cp;
-  int32_t J = 0, heap_cap = 0, cp_slots = 0, cp_n = 0, max_indeg = 0, levels = 0, barriers = 0;
+  std::vector<int32_t> jslot;    // [J] join state slot of each join (the event kernel's join index)
+  std::vector<int32_t> join_of;  // [n] the join a compact op waits on (its own or its barrier's), -1
+  int32_t J = 0, JS = 0, heap_cap = 0, cp_slots = 0, cp_n = 0, max_indeg = 0, levels = 0, barriers = 0;
   int64_t m = 0;
 };
 
@@ -110,6 +112,78 @@ int32_t min_path_cover(int32_t n, const std::vector<std::vector<int32_t>> &adj) 
     }
   }
   return n - matched;
+}
+
+// Join state slots of the event replay.  A join's state {predecessors
+// finished, latest finish} is live from the completion of its first
+// predecessor until that of its last one, which clears it.  Join k may take
+// over the slot of join j when j's node is an ancestor-or-self of every
+// predecessor of k: each predecessor of k then completes after j's node was
+// released, hence after j's last predecessor cleared j's state, so the two
+// are never open together, whatever the durations.  (Siblings of one op
+// never qualify: neither is an ancestor of their common predecessor.)  Joins
+// are visited in a topological order of the walk graph (nodes 0..N-1, preds
+// / succs as CSR) and take the lowest slot whose latest holder qualifies,
+// else a new one.  Ancestor sets (bitsets over join ids) are kept only while
+// a successor of their node is unvisited; when they would need more than
+// kJoinSlotBudget bytes, every join keeps a slot of its own.
+constexpr size_t kJoinSlotBudget = size_t(256) << 20;
+
+int32_t assign_join_slots(int32_t N, const std::vector<int32_t> &p_ptr, const std::vector<int32_t> &p,
+                          const std::vector<int32_t> &s_ptr, const std::vector<int32_t> &s,
+                          const std::vector<int32_t> &jid, int32_t J, std::vector<int32_t> &slot) {
+  slot.resize(J);
+  std::iota(slot.begin(), slot.end(), 0);
+  if (J <= 1) return J;
+  const size_t W = ((size_t)J + 63) / 64;
+  std::vector<int32_t> cnt(N), left(N), order;
+  order.reserve(N);
+  for (int32_t x = 0; x < N; ++x) {
+    cnt[x] = p_ptr[x + 1] - p_ptr[x];
+    left[x] = s_ptr[x + 1] - s_ptr[x];
+    if (cnt[x] == 0) order.push_back(x);
+  }
+  std::vector<std::vector<uint64_t>> anc(N);
+  std::vector<int32_t> holder;  // per slot: its latest join
+  std::vector<uint64_t> ca(W);
+  size_t live = 0;
+  for (size_t h = 0; h < order.size(); ++h) {
+    const int32_t x = order[h];
+    std::vector<uint64_t> a(W, 0);
+    std::fill(ca.begin(), ca.end(), ~0ull);
+    for (int32_t e = p_ptr[x]; e < p_ptr[x + 1]; ++e) {
+      const std::vector<uint64_t> &b = anc[p[e]];
+      for (size_t w = 0; w < W; ++w) {
+        a[w] |= b[w];
+        ca[w] &= b[w];
+      }
+    }
+    for (int32_t e = p_ptr[x]; e < p_ptr[x + 1]; ++e)
+      if (--left[p[e]] == 0) {
+        std::vector<uint64_t>().swap(anc[p[e]]);
+        live -= W * 8;
+      }
+    const int32_t j = jid[x];
+    if (j >= 0) {
+      size_t k = 0;
+      while (k < holder.size() && !(ca[(size_t)holder[k] / 64] >> (holder[k] % 64) & 1)) ++k;
+      if (k == holder.size()) holder.push_back(j);
+      holder[k] = j;
+      slot[j] = (int32_t)k;
+      a[(size_t)j / 64] |= 1ull << (j % 64);
+    }
+    if (left[x] > 0) {
+      anc[x].swap(a);
+      live += W * 8;
+      if (live > kJoinSlotBudget) {
+        std::iota(slot.begin(), slot.end(), 0);
+        return J;
+      }
+    }
+    for (int32_t e = s_ptr[x]; e < s_ptr[x + 1]; ++e)
+      if (--cnt[s[e]] == 0) order.push_back(s[e]);
+  }
+  return (int32_t)holder.size();
 }
 
 // Kahn's algorithm; lifo = depth-first flavour.  Returns false on a cycle.
@@ -364,8 +438,9 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     C.ws_ptr[N] = (int32_t)C.ws.size();
   }
 
-  // joins: ops still counting two or more predecessors, in topological order
-  // (concurrently pending joins get nearby indices), then the barriers
+  // joins: ops still counting two or more predecessors, in topological
+  // order, then the barriers; their state slots may be shared (see
+  // assign_join_slots)
   std::vector<int32_t> join(n + nb, -1);  // kJoinNone for plain successors
   C.J = 0;
   C.jneed.clear();
@@ -381,6 +456,10 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     C.jneed.push_back(bneed[b]);
     C.jtarget.push_back(bmem[b][0]);
   }
+  C.join_of.assign(join.begin(), join.begin() + n);
+  for (int32_t b = 0; b < nb; ++b)
+    for (int32_t w : bmem[b]) C.join_of[w] = join[n + b];
+  C.JS = assign_join_slots(n + nb, C.wp_ptr, C.wp, C.ws_ptr, C.ws, join, C.J, C.jslot);
   C.max_indeg = 0;
   for (int32_t c = 0; c < n; ++c) C.max_indeg = std::max(C.max_indeg, (int32_t)cp[c].size());
 
@@ -433,11 +512,18 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     // A join entry can carry everything its firing needs: the word of the op
     // it releases and, beside the join index, the number of predecessors it
     // waits for (when they fit 16 and 15 bits), so no per-join table is read.
-    bool jn = C.J <= 65536;
+    // The join field of an entry and of a key word is the join's state slot;
+    // without self-contained entries it also indexes the per-join table, so
+    // every join then keeps a slot of its own.
+    bool jn = C.JS <= 65536;
     for (int32_t j = 0; j < C.J && jn; ++j) jn = C.jneed[j] < 32768;
+    if (!jn) {
+      std::iota(C.jslot.begin(), C.jslot.end(), 0);
+      C.JS = C.J;
+    }
     C.pk_jn = jn;
     int32_t jb = 0, rb = 0;
-    while ((1ll << jb) < (int64_t)C.J + 1) ++jb;
+    while ((1ll << jb) < (int64_t)C.JS + 1) ++jb;
     while ((1ll << rb) < (int64_t)R) ++rb;
     bool ident = true;  // caller ids equal compact ids: the duration row is the id
     for (int32_t c = 0; c < n && ident; ++c) ident = orig_of[c] == c;
@@ -459,7 +545,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     auto word = [&](int32_t c) -> int32_t {  // c: a compact op id (never a barrier)
       if (!pack || c < 0 || c >= n) return c;
       const OpRec &r = C.ops[c];
-      const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)r.j0 : jnone;
+      const uint32_t jf = r.nsucc > 0 && r.j0 >= 0 ? (uint32_t)C.jslot[r.j0] : jnone;
       const uint32_t res = rkey ? (uint32_t)r.res << jb : 0u;
       return (int32_t)(((uint32_t)c << (rb + jb)) | res | jf);
     };
@@ -468,7 +554,7 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
         x = word(x);  // released directly (or a sibling)
       } else if (jn) {
         x = word(C.jtarget[y]);
-        y = (int32_t)((uint32_t)y | ((uint32_t)C.jneed[y] << 16));
+        y = (int32_t)((uint32_t)C.jslot[y] | ((uint32_t)C.jneed[y] << 16));
       }
     };
     C.ev_ops = C.ops;
@@ -744,7 +830,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
   DevGraph &d = g->dg;
   d.n = n_ops;
   d.R = n_res;
-  d.J = C.J;
+  d.J = C.JS;
   d.nsrc = (int32_t)C.src.size();
   d.heap_cap = C.heap_cap;
   d.cp_slots = C.cp_slots;
@@ -872,6 +958,25 @@ extern "C" const char *sim_strerror(int code) {
     case SIM_E_LIMIT: return "graph exceeds a library limit";
     default: return "unknown error";
   }
+}
+
+extern "C" int sim_testing_join_slots(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,
+                                      const int32_t *succ_idx, const int32_t *op_res, const int32_t *prio,
+                                      int32_t *slot_of, int32_t *n_slots) {
+  if (!n_slots || (n_ops > 0 && !slot_of)) return SIM_E_INVAL;
+  if (int rc = check_graph_args(n_ops, n_res, succ_ptr, succ_idx, op_res)) return rc;
+  try {
+    Compiled C;
+    if (int rc = compile(n_ops, n_res, succ_ptr, succ_idx, op_res, prio, C)) return rc;
+    for (int32_t c = 0; c < n_ops; ++c) {
+      const int32_t j = C.join_of[c];
+      slot_of[C.ops[c].orig] = j < 0 ? -1 : C.jslot[j];
+    }
+    *n_slots = C.JS;
+  } catch (const std::bad_alloc &) {
+    return SIM_E_NOMEM;
+  }
+  return SIM_OK;
 }
 
 extern "C" int sim_testing_sweep_table(int32_t n_ops, int32_t n_res, const int64_t *succ_ptr,

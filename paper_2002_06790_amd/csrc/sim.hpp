@@ -70,14 +70,14 @@ struct MpTable {
 
 // Device view of a compiled graph (plain pointers, passed by value).
 struct DevGraph {
-  int32_t n, R, J, nsrc;  // n real ops (barriers follow them), J joins
+  int32_t n, R, J, nsrc;  // n real ops (barriers follow them), J join state slots
   int32_t heap_cap;       // bound on simultaneously ready ops (>= DAG width)
   int32_t cp_slots;       // value slots of the critical-path sweep (live values + 2)
   int32_t max_indeg;
   int32_t cp_n;           // records of the critical-path sweep (ops and its barrier nodes)
   const OpRec *ops;       // [n + barriers + 1]
   const int32_t *succ;    // pairs {successor id, its join index, kJoinNone or kJoinSibling}
-  const int32_t *jneed;   // [J] predecessors a join waits for
+  const int32_t *jneed;   // [joins] predecessors a join waits for
   const int32_t *src;     // [nsrc] compact ids of sources
   const CpRec *cp;        // [round_up(n, kCpBatch) + kCpBatch * kCpAhead]
   const int32_t *cp_pred; // predecessor slot lists of the critical-path sweep
@@ -107,7 +107,9 @@ struct DevGraph {
   // records, successor entries and sources hold such words for the ops they
   // release directly, and jinfo[j] = {predecessors needed, word released}
   // per join.  With pk_jn a join entry {x, y} itself holds x = the word
-  // released and y = join index | predecessors needed << 16.
+  // released and y = join index | predecessors needed << 16, and the join
+  // index is a join state slot, which joins never open together may share
+  // (without pk_jn each join has its own).
   const OpRec *ev_ops;     // [n + barriers + 1]
   const int32_t *ev_succ;  // pairs {word or barrier id, join index / kJoinNone / kJoinSibling}
   const int2 *jinfo;       // [J]
