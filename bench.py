@@ -59,10 +59,11 @@ def cpu_model():
 def launch_step(torch, g, dur, place, algo, mk, fin, st, cp, side, go, done, mid=None):
     """One step of the hot path: the replay on the current stream and the
     critical path (which reads the same durations and nothing the replay
-    writes) on stream ``side``, launched after the replay so that its blocks
-    take the compute units the replay's persistent grid leaves idle as its
-    last tiles finish.  The current stream waits for both; ``mid`` (an
-    event) is recorded on it when the replay ends."""
+    writes) on stream ``side``, launched after the replay, so that the two
+    kernels share the chip: the critical path streams coalesced rows while
+    the replay is bound by divergent accesses per compute unit.  The current
+    stream waits for both; ``mid`` (an event) is recorded on it when the
+    replay ends."""
     main = torch.cuda.current_stream()
     go.record(main)
     g.run(dur, place=place, algo=algo, makespan=mk, finish=fin, status=st)
@@ -501,7 +502,7 @@ def main():
         "scenarios_per_s": S / (ms_per_step / 1e3),
         "kernels": {"timing": f"median of {args.steps} HIP event pairs per kernel",
                     "step": "sim_run_batch on the main stream; sim_critical_path on a second stream, "
-                            "launched after it and running in the compute units its last tiles free",
+                            "launched after it, the two kernels sharing the chip",
                     "run_batch_ms": float(np.median(ev_ms)), "critical_path_ms": float(np.median(cp_ms)),
                     "step_after_run_batch_ms": float(np.median(tail_ms)),
                     "run_batch_op_events_per_s": op_events / ev_s,
