@@ -25,11 +25,13 @@
 // next finish (older keys are skipped), so a call's heap holds at most one
 // key per ready op and two per op on a shared resource.  The heap's top
 // three levels (21 positions, 10.5 KB) live in LDS, the rest and all
-// other per-lane state in global scratch, lane-major ([index][64]): the
-// {ready time, count} word of each node with two or more predecessors (a
-// node with one predecessor is ready when it finishes and needs none), each
-// resource's free time, each shared resource's 32-byte state record and its
-// active ops.
+// other per-lane state in global scratch.  A lane walks its heap and
+// scans a resource's active ops, so those two lie contiguous per lane
+// (each child group, each run of active ops one segment); the state read
+// at one index per event lies lane-major ([index][64]): the {ready time,
+// count} word of each node with two or more predecessors (a node with one
+// predecessor is ready when it finishes and needs none), each resource's
+// free time and each shared resource's 32-byte state record.
 #include <algorithm>
 #include <cstring>
 #include <vector>
@@ -54,7 +56,7 @@ struct ShArgs {
   int64_t ld_fin;
   int32_t *status;
   const int32_t *share;  // [R] 0 / 1
-  char *scratch;         // per block: the regions below, lane-major
+  char *scratch;         // per block: the regions below
   int64_t block_bytes;
   int64_t heap_cap;      // heap entries per lane (keys present at once)
   int64_t max_keys;      // keys pushed over a whole replay (bounds its pops)
@@ -133,8 +135,11 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   const Lane<uint64_t> rc{(uint64_t *)(blk + a.o_rc) + lane};
   const Lane<uint32_t> rf{(uint32_t *)(blk + a.o_rf) + lane};
   const Lane<LinkSt> lk{(LinkSt *)(blk + a.o_ln) + lane};
-  const Lane<uint64_t> need{(uint64_t *)(blk + a.o_need) + lane};  // [R][kShareMax]
-  const Lane<int32_t> eop{(int32_t *)(blk + a.o_op) + lane};     // [R][kShareMax]
+  // each shared resource's active ops: the service units each needs and its
+  // compact id, [R][kShareMax] contiguous per lane (a departure scans a
+  // resource's entries in order)
+  uint64_t *const need = (uint64_t *)(blk + a.o_need) + (int64_t)lane * R * kShareMax;
+  int32_t *const eop = (int32_t *)(blk + a.o_op) + (int64_t)lane * R * kShareMax;
 
   for (int64_t tile = blockIdx.x; tile * kWave < a.n_scen; tile += gridDim.x) {
     const int64_t s = tile * kWave + lane;
@@ -198,9 +203,19 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         for (;;) {
           const int64_t l = 4 * i + 1;
           if (l >= hs) break;
+          // the four children requested together (indices clamped into the
+          // LDS part or the lane's region; positions from hs on are empty)
           uint64_t kc[4];
+          if (l < HL) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) kc[q] = l + q < hs ? hget(l + q) : ~0ull;
+            for (int q = 0; q < 4; ++q) kc[q] = lds_heap[(l + q < HL ? l + q : HL - 1) * kWave + lane];
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) kc[q] = heap_g[l + q < a.heap_cap ? l + q : a.heap_cap - 1];
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (l + q >= hs) kc[q] = ~0ull;
           int64_t m = l;
           uint64_t km = kc[0];
 #pragma unroll
@@ -244,17 +259,23 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       // entry, entries} and B {entries 0 and 1}) at t: the words of the
       // inline entries requested together, the others four entries at a time
       // (the nodes of one list are distinct, so the words are independent)
+      // (every load below reads a valid index, clamped where the entry is
+      // absent, and its value is discarded afterwards: conditional loads
+      // would each wait for their data before the next is issued)
       auto release_op = [&](const int4 A, const int4 B, uint32_t t) {
-        const uint64_t o0 = B.y >= 0 ? rc[B.y] : 0, o1 = B.w >= 0 ? rc[B.w] : 0;
+        const uint64_t o0 = rc[B.y >= 0 ? B.y : 0], o1 = rc[B.w >= 0 ? B.w : 0];
         fire(B.x, B.y, o0, t);
         fire(B.z, B.w, o1, t);
         for (int e = 2; e < A.w; e += 4) {
           int2 en[4];
           uint64_t os[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) en[j] = e + j < A.w ? a.sent[A.z + e + j] : make_int2(kShNone, -1);
+          for (int j = 0; j < 4; ++j) en[j] = a.sent[A.z + (e + j < A.w ? e + j : e)];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) os[j] = en[j].y >= 0 ? rc[en[j].y] : 0;
+          for (int j = 0; j < 4; ++j)
+            if (e + j >= A.w) en[j] = make_int2(kShNone, -1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) os[j] = rc[en[j].y >= 0 ? en[j].y : 0];
 #pragma unroll
           for (int j = 0; j < 4; ++j) fire(en[j].x, en[j].y, os[j], t);
         }
