@@ -20,18 +20,20 @@
 // op (with the op's resource in the low bits below the id when it fits, so
 // a popped op's resource state is requested together with its record), so
 // one key order gives all the tie rules above.  The next finish of a
-// shared resource changes when an op arrives; every change pushes a new key
-// and a popped key is used only if it still equals the resource's current
-// next finish (older keys are skipped), so a call's heap holds at most one
-// key per ready op and two per op on a shared resource.  The heap's top
-// three levels (21 positions, 10.5 KB) live in LDS, the rest and all
-// other per-lane state in global scratch.  A lane walks its heap and
-// scans a resource's active ops, so those two lie contiguous per lane
-// (each child group, each run of active ops one segment); the state read
-// at one index per event lies lane-major ([index][64]): the {ready time,
-// count} word of each node with two or more predecessors (a node with one
-// predecessor is ready when it finishes and needs none), each resource's
-// free time and each shared resource's 32-byte state record.
+// shared resource changes when an op arrives or leaves.  The heap holds one
+// current key per busy shared resource, whose time (pk) is at most its next
+// finish: a departure, or an arrival that moves the next finish earlier,
+// pushes a new key (an older one is then skipped when popped); an arrival
+// that moves it later pushes nothing, and when the held key comes up before
+// the finish it is pushed again at the finish.  So a call's heap holds at
+// most one key per ready op and two per op on a shared resource.  The
+// heap's top three levels (21 positions, 10.5 KB) live in LDS, the rest and
+// all other per-lane state in global scratch, lane-major ([index][64]),
+// except each shared resource's active ops, which a departure scans in
+// order and so lie contiguous per lane: the {ready time, count} word of
+// each node with two or more predecessors (a node with one predecessor is
+// ready when it finishes and needs none), each resource's free time, each
+// shared resource's 32-byte state record and its active ops.
 #include <algorithm>
 #include <cstring>
 #include <vector>
@@ -87,11 +89,13 @@ struct __attribute__((aligned(16))) ShRec {
 
 // one shared resource's state in one lane: service units per active op
 // since time 0 (vt, as of time tl), the least need of its active ops (mn),
-// its pending finish time (nd) and active count (k); read and written whole
+// its pending finish time (nd), active count (k) and the time of the key
+// the heap holds for it (pk <= nd; kNoTime: none); read and written whole
 struct __attribute__((aligned(16))) LinkSt {
   uint64_t vt, mn;
   uint32_t tl, nd;
-  int32_t k, pad;
+  int32_t k;
+  uint32_t pk;
 };
 
 // Read-only tables read at wave-uniform indices: through the constant
@@ -178,7 +182,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       }
       for (int r = 0; r < R; ++r) {
         rf[r] = 0;
-        lk[r] = LinkSt{0, 0, 0, kNoTime, 0, 0};
+        lk[r] = LinkSt{0, 0, 0, kNoTime, 0, kNoTime};
       }
       int64_t hs = 0;
       // a 4-ary heap: children of position i at 4i + 1 .. 4i + 4, whose keys
@@ -304,7 +308,13 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         if (w < (uint32_t)R) {  // a pending finish on shared resource w
           const int r = (int)w;
           LinkSt L = lk[r];
-          if (L.k == 0 || L.nd != t) continue;  // superseded
+          if (L.k == 0 || L.pk != t) continue;  // superseded
+          if (L.nd != t) {  // arrivals since moved the next finish later: key it now
+            L.pk = L.nd;
+            ok = ok && push(key_of(L.nd, (uint32_t)r));
+            lk[r] = L;
+            continue;
+          }
           if (t > kI32Max) {
             st |= SIM_ST_OVERFLOW;
             break;
@@ -353,10 +363,10 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           L.k = k;
           if (k > 0) {
             L.mn = m_rest;
-            L.nd = finish_at(L, k, m_rest);
+            L.nd = L.pk = finish_at(L, k, m_rest);
             ok = ok && push(key_of(L.nd, (uint32_t)r));
           } else {
-            L.nd = kNoTime;
+            L.nd = L.pk = kNoTime;
           }
           lk[r] = L;
           continue;
@@ -390,8 +400,13 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           L.k = k + 1;
           L.mn = k == 0 || nv < L.mn ? nv : L.mn;
           L.nd = finish_at(L, k + 1, L.mn);
+          // a new key only when the next finish moved earlier than the key
+          // held; a later one is keyed when the held key comes up
+          if (L.nd < L.pk) {
+            L.pk = L.nd;
+            ok = ok && push(key_of(L.nd, (uint32_t)r));
+          }
           lk[r] = L;
-          ok = ok && push(key_of(L.nd, (uint32_t)r));
           continue;
         }
         const uint32_t start = t > rfree ? t : rfree;
