@@ -205,13 +205,14 @@ __device__ __forceinline__ void heap_push(H &h, int &end, uint64_t x) {
 // step's duration and record loads, so a sift-down costs no round trip of
 // its own unless it goes deeper than the root's grandchildren.
 struct HeapAhead {
+  bool eager;       // the last element is requested with the look-ahead (else when a pop needs it)
   uint64_t m1;      // smallest child of the root (kEmpty if none)
   int q1;           // its position
   int c2;           // first child of q1 (>= end: none)
   uint64_t v2[kD];  // that group (valid if c2 < end)
   uint64_t m2;      // its minimum
   int q2;           // the minimum's index in the group
-  uint64_t last;    // the last element when it sits in global memory
+  uint64_t last;    // the last element when it sits in global memory (eager)
 };
 
 template <bool DEEP, class H>
@@ -224,7 +225,7 @@ __device__ __forceinline__ void heap_look_ahead(const H &h, int end, HeapAhead &
   A.last = kEmpty;
   if (DEEP) {
     if (A.c2 < end && A.c2 >= h.le) h.global_group(A.c2, A.v2);
-    if (end - 1 >= h.le) A.last = h.g[end - 1 - h.le];
+    if (A.eager && end - 1 >= h.le) A.last = h.g[end - 1 - h.le];
   }
   if (A.c2 < end && A.c2 < h.le) h.lds_group(A.c2, A.v2);
 }
@@ -241,7 +242,7 @@ __device__ __forceinline__ void heap_settle_ahead(HeapAhead &A) {
 #pragma unroll
   for (int k = 0; k < kD; ++k) v[k] = A.v2[k] = DEEP ? settle(A.v2[k]) : A.v2[k];
   min_group(v, A.m2, A.q2);
-  if (DEEP) A.last = settle(A.last);
+  if (DEEP && A.eager) A.last = settle(A.last);
 }
 
 // Replace the root by x (the first op a step releases), using the look-ahead.
@@ -277,7 +278,7 @@ __device__ __forceinline__ void heap_pop_root(H &h, int &end, HeapAhead &A) {
     x = h.l[(lp - H::kLB) * kWave];
     h.l[(lp - H::kLB) * kWave] = kEmpty;
   } else {
-    x = A.last;
+    x = A.eager ? A.last : settle(h.g[lp - h.le]);
     h.g[lp - h.le] = kEmpty;
   }
   if (lp < kL2) {  // a child of the root left: rescan them (no grandchildren remain)
@@ -337,7 +338,7 @@ struct JoinGlobal {
 };
 // One replay step of k_event (see there).  DEEP: some lane's heap reaches
 // global memory, so the step reads its heap ahead.
-template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, class Heap, class JPtr,
+template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, bool LAZY, class Heap, class JPtr,
           class RfGet, class RfSet, class LastXchg, class Flush, int FQ>
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, Heap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
@@ -382,7 +383,12 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     js0 = jst.get(jf);
     if (!G.pk_jn) ji0 = G.jinfo[jf];
   }
+  // LAZY: the heap's last element is read when a pop needs it instead of
+  // with the look-ahead (most steps release an op and pop nothing, so the
+  // early load is mostly wasted address work; it measured faster only in
+  // the register-children kernel with loaded durations and no device model)
   HeapAhead A;
+  A.eager = !LAZY;
   heap_look_ahead<DEEP>(heap, end, A);
   // keep the scheduler from sinking these loads below the first use of d
   __builtin_amdgcn_sched_barrier(0);
@@ -522,8 +528,9 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
 // waited for once per burst instead of once per step.  GEN: durations are
 // generated from the knob grid and counter-based noise of a.gen instead of
 // read from a.dur.  REG: the heap
-// root's children live in registers (see WideHeap).
-template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool REG = false>
+// root's children live in registers (see WideHeap).  LAZY: the heap's last
+// element is read only by steps that pop (see event_step).
+template <bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN = false, bool REG = false, bool LAZY = false>
 __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
@@ -613,11 +620,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       if (end <= kRoot) break;  // unreachable for a DAG: some op is always ready
       auto run_step = [&](auto jp) {
         if (__ballot(end > heap.le))
-          event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
+          event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN, LAZY>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
                                                              dev_l, st, span, fq, rq, pq, rf_get, rf_set,
                                                              last_xchg, flush);
         else
-          event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN>(G, a, heap, end, jp, it, s, sc, brow, s_lo,
+          event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN, LAZY>(G, a, heap, end, jp, it, s, sc, brow, s_lo,
                                                               s_hi, dev_l, st, span, fq, rq, pq, rf_get, rf_set,
                                                               last_xchg, flush);
       };
@@ -1168,7 +1175,7 @@ int plan_scratch(sim_graph *g) {
   const size_t last_lds_bytes = P.ev_last16 ? rf_lds_bytes / 2 : rf_lds_bytes;
   P.ev_reg_prev_lds_bytes = P.ev_reg_lds_bytes + last_lds_bytes;  // with the last-op table
   if (P.ev_reg) {
-    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
+    occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
     occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes + dev_table,
                               cus);
@@ -1356,7 +1363,7 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
     a.dev_lds = (int)lds;
     lds += ((size_t)g->dg.R * 8 + 15) & ~size_t(15);
   }
-  const int variant = (reg ? 64 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
+  const int variant = (reg && !gen && !prev && !dev ? 128 : 0) | (reg ? 64 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
                       (rf_lds ? 4 : 0) | (g->dg.ev_compact ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \
   case V: k_event<A, B, C, D><<<grid, block, lds, stream>>>(g->dg, a); break;
@@ -1365,7 +1372,10 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
 #define EV_REG_CASE(V, B, D, E) \
   case V: k_event<true, B, false, D, E, true><<<grid, block, lds, stream>>>(g->dg, a); break;
   switch (variant) {
-    // the heap root's children in registers
+    // the heap root's children in registers (loaded durations, no device
+    // model: the heap's last element read only when a pop needs it)
+    case 196: k_event<true, false, false, false, false, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
+    case 198: k_event<true, true, false, false, false, true, true><<<grid, block, lds, stream>>>(g->dg, a); break;
     EV_REG_CASE(68, false, false, false)
     EV_REG_CASE(70, true, false, false)
     EV_REG_CASE(76, false, true, false)
