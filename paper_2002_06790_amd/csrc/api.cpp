@@ -82,11 +82,14 @@ extern "C" int sim_run_batch(const sim_graph *g, int64_t n_scen, const int32_t *
   }
   const uint32_t algo = flags & 3u;
   if (algo == 3u) return SIM_E_INVAL;
-  Lease lease(g->pool, st);
-  if (lease.rc()) return lease.rc();
-  if (algo == SIM_ALGO_SWEEP)
+  if (algo == SIM_ALGO_SWEEP) {
+    Lease lease(g->sweep_pool, st);
+    if (lease.rc()) return lease.rc();
     return launch_sweep(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
                         status, st);
+  }
+  Lease lease(g->pool, st);
+  if (lease.rc()) return lease.rc();
   return launch_event(g, lease.base(), n_scen, dur, ld_dur, place, ld_place, makespan, finish, ld_fin,
                       status, st);
 }

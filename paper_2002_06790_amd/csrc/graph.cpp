@@ -892,6 +892,7 @@ extern "C" int sim_graph_create(int32_t n_ops, int32_t n_res, const int64_t *suc
 extern "C" void sim_graph_destroy(sim_graph *g) {
   if (!g) return;
   g->pool.destroy();
+  g->sweep_pool.destroy();
   g->share_pool.destroy();
   if (g->dev_mem) (void)hipFree(g->dev_mem);
   delete g;

@@ -1093,7 +1093,7 @@ int occupancy_blocks(K kernel, size_t lds, int cus, bool strict = false) {
 
 constexpr size_t kRfLdsMax = 32 * 1024;        // resource times kept in LDS up to this size
 constexpr size_t kScratchBudget = 4ull << 30;  // global per-block scratch of one kernel, per set
-constexpr size_t kSweepBudget = 1ull << 30;    // the sweep variant's per-op state, per set
+constexpr size_t kSweepBudget = 3ull << 30;    // the sweep variant's per-op state, per set of its own
 constexpr size_t kPoolBudget = 4ull << 30;     // all eager sets of one graph together
 constexpr int kMaxSets = 4;                    // eager sets per graph (at least one)
 
@@ -1264,10 +1264,14 @@ int plan_scratch(sim_graph *g) {
     sw_occ = P.sw_res_lds ? occupancy_blocks(k_sweep<false, true>, P.sw_lds_bytes, cus)
                           : occupancy_blocks(k_sweep<false, false>, P.sw_lds_bytes, cus);
   if (sw_occ < 0) return SIM_E_HIP;
-  const size_t sw_per_block = (P.sw_val_lds ? 0 : val_bytes) + (P.sw_res_lds ? 0 : res_bytes);
+  // the sweep's global state lives in sets of its own (one eager, one for
+  // captures), as many blocks as kSweepBudget holds: it is latency-bound, so
+  // its speed follows the resident blocks
+  const size_t sw_val_blk = P.sw_val_lds ? 0 : (val_bytes + 255) & ~size_t(255);
+  const size_t sw_res_blk = P.sw_res_lds ? 0 : (res_bytes + 255) & ~size_t(255);
+  const size_t sw_per_block = sw_val_blk + sw_res_blk;
   size_t sw_blocks = (size_t)sw_occ;
   if (sw_per_block) sw_blocks = std::min(sw_blocks, std::max<size_t>(1, kSweepBudget / sw_per_block));
-  P.sw_blocks = (int32_t)sw_blocks;
 
   size_t off = 0;
   auto take = [&](size_t b) {
@@ -1281,8 +1285,6 @@ int plan_scratch(sim_graph *g) {
   g->scratch_ev_rf_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_ev_last_off = take(rf_lds ? 0 : rf_bytes * ev_grid);
   g->scratch_at_off = take(P.at_lds ? 0 : (size_t)2 * G.R * kWave * 4 * P.at_blocks);
-  g->scratch_sw_val_off = take(P.sw_val_lds ? 0 : val_bytes * P.sw_blocks);
-  g->scratch_sw_res_off = take(P.sw_res_lds ? 0 : res_bytes * P.sw_blocks);
   g->scratch_cp_off = take(P.cp_mode == kCpSlotsGlobal ? cp_bytes * P.cp_blocks : 0);
   g->scratch_dist_off = take((size_t)std::max(G.n, 1) * 4);
   g->scratch_gen_off = take((size_t)std::max(G.n, 1) * 4);  // one generated duration column
@@ -1293,6 +1295,21 @@ int plan_scratch(sim_graph *g) {
   const int n_sets = (int)std::max<size_t>(1, std::min<size_t>(kMaxSets, kPoolBudget / std::max<size_t>(off, 1)));
   g->pool.destroy();
   if (int rc = g->pool.init(off, n_sets, true, fill_set, g)) return rc;
+  // the sweep's sets (the kernel initialises its state per tile): fewer
+  // blocks when the memory is not there
+  for (;;) {
+    P.sw_blocks = (int32_t)sw_blocks;
+    g->scratch_sw_val_off = 0;
+    g->scratch_sw_res_off = sw_val_blk * sw_blocks;
+    g->sweep_pool.destroy();
+    const int rc = g->sweep_pool.init(sw_per_block * sw_blocks, 1, true, nullptr, nullptr);
+    if (rc != SIM_E_NOMEM || sw_blocks <= 1) {
+      if (rc) return rc;
+      break;
+    }
+    (void)hipGetLastError();  // clear the failed allocation's error
+    sw_blocks = std::max<size_t>(1, sw_blocks / 2);
+  }
   if (getenv("MLSIM_VERBOSE"))  // diagnostics only
     fprintf(stderr,
             "[mlsim] n=%d R=%d J=%d (barriers %d) heap_cap=%d (stride %d, lds end %d) cp_slots=%d (mode %d) "

@@ -224,10 +224,12 @@ struct sim_graph {
   mlsim::ScratchPlan plan;
   mlsim::Variant var;
   void *dev_mem;          // one allocation holding every graph array
-  // scratch sets of the event, sweep, critical-path and attribution kernels
-  // (one layout, offsets below) and of the bandwidth-sharing replay; sized
-  // here at creation, never allocated by a call
-  mutable mlsim::ScratchPool pool, share_pool;
+  // scratch sets of the event, critical-path and attribution kernels (one
+  // layout, offsets below), of the sweep variant (its per-op and
+  // per-resource state, offsets below within its own sets) and of the
+  // bandwidth-sharing replay; sized here at creation, never allocated by a
+  // call
+  mutable mlsim::ScratchPool pool, sweep_pool, share_pool;
   size_t scratch_ev_heap_off, scratch_ev_join_off, scratch_ev_rf_off, scratch_cp_off;
   size_t scratch_sw_val_off, scratch_sw_res_off, scratch_dist_off;
   size_t scratch_ev_last_off, scratch_at_off, scratch_gen_off, scratch_dev_off;
