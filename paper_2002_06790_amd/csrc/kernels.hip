@@ -201,7 +201,7 @@ __device__ __forceinline__ void heap_push(H &h, int &end, uint64_t x) {
 
 // What one replay step reads of its heap before it knows the new key: the
 // smallest child of the root, that child's own child group and, when it sits
-// in global memory, the last element.  The global loads go out with the
+// in global memory and the kernel is not LAZY, the last element.  The global loads go out with the
 // step's duration and record loads, so a sift-down costs no round trip of
 // its own unless it goes deeper than the root's grandchildren.
 struct HeapAhead {
