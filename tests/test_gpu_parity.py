@@ -561,6 +561,35 @@ def test_two_streams_share_one_graph(mlsim):
     g.close()
 
 
+def test_two_streams_sweep_beside_event(mlsim):
+    """The sweep variant keeps its state in scratch sets of its own: sweeps
+    and event replays issued on two streams at once, over one graph, each
+    equal the oracle."""
+    w = W.make_config(3, n_scen=640)
+    g = mlsim.Graph.from_workload(w)
+    dh = [w.durations(), np.maximum(1, w.durations() // 3 + 11).astype(np.int32)]
+    d = [dev(x) for x in dh]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    out = [[], []]
+    for rep in range(2):  # issue everything before waiting for anything
+        for i, s in enumerate(streams):
+            with torch.cuda.stream(s):
+                out[i].append(g.run(d[i], algo="sweep", want_finish=True))
+                out[i].append(g.run(d[1 - i], algo="event", want_finish=True))
+    torch.cuda.synchronize()
+    ref = [oracle.run_batch(w.succ_ptr, w.succ_idx, w.op_res, w.n_res, x, prio=w.prio) for x in dh]
+    for i in range(2):
+        for rep in range(2):
+            for k, src in ((0, i), (1, 1 - i)):
+                mk, fin, st = out[i][2 * rep + k]
+                omk, ofin, ost = ref[src]
+                assert np.array_equal(mk.cpu().numpy(), omk), (i, rep, k)
+                assert np.array_equal(st.cpu().numpy(), ost), (i, rep, k)
+                assert np.array_equal(fin.cpu().numpy(), ofin), (i, rep, k)
+    g.close()
+
+
 def test_binding_rejects_bad_arrays(mlsim):
     """Output and input arrays that would let a kernel read or write out of
     bounds are rejected before the call."""
