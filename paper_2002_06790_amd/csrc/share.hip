@@ -107,6 +107,15 @@ __device__ __forceinline__ cptr<T> as_const(const T *p) {
   return (cptr<T>)p;
 }
 
+// A loaded value consumed by an empty asm: a load in one branch of an
+// LDS-or-global choice then differs from the other branch's, so the two are
+// not merged into one generic-address (flat) load through a selected pointer.
+template <class T>
+__device__ __forceinline__ T sh_settle(T v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 template <class T>
 struct Lane {  // element i of a lane-major array
   T *p;
@@ -121,19 +130,26 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
   const Lane<uint64_t> heap_g{(uint64_t *)blk + lane};
   // heap position i: in LDS below heap_lds, else in global scratch
   const int64_t HL = a.heap_lds;
-  auto hget = [&](int64_t i) -> uint64_t { return i < HL ? lds_heap[i * kWave + lane] : heap_g[i]; };
+  // (each branch keeps its own instruction: LDS or global, never flat)
+  auto hget = [&](int64_t i) -> uint64_t {
+    if (i < HL) return lds_heap[i * kWave + lane];
+    return sh_settle(heap_g[i]);
+  };
   auto hset = [&](int64_t i, uint64_t v) {
-    if (i < HL)
+    if (i < HL) {
       lds_heap[i * kWave + lane] = v;
-    else
+    } else {
       heap_g[i] = v;
+      asm volatile("" ::: "memory");
+    }
   };
   int32_t *flags_l = (int32_t *)(lds_heap + HL * kWave);
   if (a.flags_lds) {
     for (int r = lane; r < R; r += kWave) flags_l[r] = a.share[r];
     __syncthreads();
   }
-  const int32_t *flags = a.flags_lds ? flags_l : a.share;
+  // resource r shared?  (the LDS copy or the argument, each by its own load)
+  auto shared_res = [&](int r) -> bool { return (a.flags_lds ? flags_l[r] : sh_settle(a.share[r])) != 0; };
   // per node with two or more predecessors: ready time (high word) and
   // predecessors not yet finished
   const Lane<uint64_t> rc{(uint64_t *)(blk + a.o_rc) + lane};
@@ -216,6 +232,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q) kc[q] = heap_g[l + q < a.heap_cap ? l + q : a.heap_cap - 1];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) kc[q] = sh_settle(kc[q]);
           }
 #pragma unroll
           for (int q = 0; q < 4; ++q)
@@ -379,7 +397,7 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         const int4 A = rec4[2 * c], B = rec4[2 * c + 1];
         int32_t d = a.rows_identity ? a.dur[(int64_t)c * a.ld_dur + s] : 0;
         const int r = a.kres ? (int)(u & rmask) : A.y;
-        const bool shr = flags[r] != 0;
+        const bool shr = shared_res(r);
         LinkSt L;
         uint32_t rfree = 0;
         if (shr)
