@@ -1170,6 +1170,8 @@ int plan_scratch(sim_graph *g) {
   P.ev_reg = rf_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
   P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_dev_blocks = P.ev_reg_prev_blocks = 1;
+  P.ev_reg_dev_le = P.ev_heap_le;
+  P.ev_reg_dev_lds_bytes = P.ev_reg_lds_bytes;
   // the last-op table of attribution: 16-bit rows when every row fits
   P.ev_last16 = G.n < 0xffff;
   const size_t last_lds_bytes = P.ev_last16 ? rf_lds_bytes / 2 : rf_lds_bytes;
@@ -1180,6 +1182,19 @@ int plan_scratch(sim_graph *g) {
     occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes + dev_table,
                               cus);
     if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
+    // device model: when its table costs a wavefront per CU, keep one heap
+    // group fewer in LDS instead (measured faster on the BERT workload:
+    // two rounds of full CUs against three of lighter ones)
+    if (occ[2] < occ[0] && P.ev_heap_le > kL2 && V.ev_lds_groups < 0) {
+      const size_t fewer = P.ev_reg_lds_bytes - (size_t)kD * kWave * 8;
+      const int o = occupancy_blocks(k_event<true, false, false, false, false, true>, fewer + dev_table, cus);
+      if (o < 0) return SIM_E_HIP;
+      if (o > occ[2]) {
+        occ[2] = o;
+        P.ev_reg_dev_le = P.ev_heap_le - kD;
+        P.ev_reg_dev_lds_bytes = fewer;
+      }
+    }
     P.ev_reg_blocks = grid_of(occ[0]);
     P.ev_reg_gen_blocks = grid_of(occ[1]);
     P.ev_reg_dev_blocks = grid_of(occ[2]);
@@ -1358,8 +1373,9 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
                    : gen  ? P.ev_reg_gen_blocks
                    : dev  ? P.ev_reg_dev_blocks
                           : P.ev_reg_blocks;
-  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
+  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : dev && !gen ? P.ev_reg_dev_lds_bytes : P.ev_reg_lds_bytes)
                    : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
+  if (reg && dev && !prev && !gen) a.heap_le = P.ev_reg_dev_le;
   if (!reg && !ext) {  // few tiles: the whole third heap level in LDS
     const int64_t wide = prev ? P.ev_wide_prev_blocks
                          : gen ? P.ev_wide_gen_blocks
