@@ -482,33 +482,109 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
       heap_push(heap, end, nk);
     }
   };
-  for (int e = 0; e < nsucc; ++e) {
-    const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);  // {successor, join}
-    if (sw.y < 0) {  // a plain successor, or the next member of a barrier
-      release(sw.y == kJoinSibling ? ready : out, sw.x);
-      continue;
+  if (!PLACE) {
+    for (int e = 0; e < nsucc; ++e) {
+      const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);  // {successor, join}
+      if (sw.y < 0) {  // a plain successor, or the next member of a barrier
+        release(sw.y == kJoinSibling ? ready : out, sw.x);
+        continue;
+      }
+      // the join's state {predecessors finished, max finish} (already read for
+      // the first entry when the key named it) and {predecessors needed, word
+      // of the op released} (in the entry itself, or in the join table)
+      const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
+      int2 js, ji;
+      if (e == 0 && G.pk_join) {
+        js = js0;
+        ji = ji0;
+      } else {
+        js = settle(jst.get(j));
+        if (!G.pk_jn) ji = settle(G.jinfo[j]);
+      }
+      if (G.pk_jn) ji = make_int2((int)((uint32_t)sw.y >> 16), sw.x);
+      const uint32_t rdy = (uint32_t)js.y > out ? (uint32_t)js.y : out;
+      if (js.x + 1 < ji.x) {
+        jst.set(j, make_int2(js.x + 1, (int)rdy));
+        continue;
+      }
+      jst.set(j, make_int2(0, 0));  // leave the join state clean
+      // the join's op, or for a barrier its first member (the others follow it)
+      release(rdy, ji.y);
     }
-    // the join's state {predecessors finished, max finish} (already read for
-    // the first entry when the key named it) and {predecessors needed, word
-    // of the op released} (in the entry itself, or in the join table)
-    const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
-    int2 js, ji;
-    if (e == 0 && G.pk_join) {
-      js = js0;
-      ji = ji0;
-    } else {
-      js = settle(jst.get(j));
-      if (!G.pk_jn) ji = settle(G.jinfo[j]);
+  } else {
+    // one successor entry {successor, join} with its join's state js
+    // {predecessors finished, max finish} and ji {predecessors needed, word of
+    // the op released} (from the entry itself, or from the join table)
+    auto handle = [&](int2 sw, int2 js, int2 ji) {
+      if (sw.y < 0) {  // a plain successor, or the next member of a barrier
+        release(sw.y == kJoinSibling ? ready : out, sw.x);
+        return;
+      }
+      const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
+      if (G.pk_jn) ji = make_int2((int)((uint32_t)sw.y >> 16), sw.x);
+      const uint32_t rdy = (uint32_t)js.y > out ? (uint32_t)js.y : out;
+      if (js.x + 1 < ji.x) {
+        jst.set(j, make_int2(js.x + 1, (int)rdy));
+        return;
+      }
+      jst.set(j, make_int2(0, 0));  // leave the join state clean
+      // the join's op, or for a barrier its first member (the others follow it)
+      release(rdy, ji.y);
+    };
+    // entry e from e0 (the join state of its join already read with the
+    // record when the key named it), e1 (unless the record points to the
+    // list) or the successor list
+    auto one = [&](int e) {
+      const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);
+      int2 js = js0, ji = ji0;
+      if (sw.y >= 0 && !(e == 0 && G.pk_join)) {
+        const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
+        js = settle(jst.get(j));
+        if (!G.pk_jn) ji = settle(G.jinfo[j]);
+      }
+      handle(sw, js, ji);
+    };
+    // The placement kernels issue the first four entries' loads together and
+    // then their joins' states together (two round trips instead of one per
+    // join; their ops release two or three joins each, and at one wavefront
+    // per CU the extra loads of absent entries, issued at clamped valid
+    // indices and discarded, cost little).  The successors of one op are
+    // distinct nodes whose joins never share a slot, so none of these loads
+    // can see a store of the same group.  (The other kernels take one entry
+    // at a time, which needs fewer registers and no wasted loads.)
+    constexpr int kC = 4;
+    int e = 0;
+    if (__ballot(nsucc > 0)) {  // some lane has entries: the list is not empty
+      int2 sw[kC], js[kC], ji[kC];
+#pragma unroll
+      for (int k = 0; k < kC; ++k) {
+        const bool listed = k < nsucc && !(k == 0 || (k == 1 && !more));
+        const int2 m = succ[listed ? sbeg + k : 0];
+        sw[k] = k == 0 ? e0 : k == 1 && !more ? e1 : m;
+      }
+#pragma unroll
+      for (int k = 0; k < kC; ++k) sw[k] = settle(sw[k]);
+#pragma unroll
+      for (int k = 0; k < kC; ++k) {
+        const bool first = k == 0 && G.pk_join;
+        const bool joined = k < nsucc && sw[k].y >= 0 && !first;
+        const int j = joined ? (G.pk_jn ? (sw[k].y & 0xffff) : sw[k].y) : 0;
+        const int2 vs = G.J > 0 ? jst.get(j) : make_int2(0, 0);
+        const int2 vi = G.J > 0 && !G.pk_jn ? G.jinfo[j] : make_int2(0, 0);
+        js[k] = first ? js0 : vs;
+        ji[k] = first ? ji0 : vi;
+      }
+#pragma unroll
+      for (int k = 0; k < kC; ++k) {
+        js[k] = settle(js[k]);
+        ji[k] = settle(ji[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < kC; ++k)
+        if (k < nsucc) handle(sw[k], js[k], ji[k]);
+      e = kC;
     }
-    if (G.pk_jn) ji = make_int2((int)((uint32_t)sw.y >> 16), sw.x);
-    const uint32_t rdy = (uint32_t)js.y > out ? (uint32_t)js.y : out;
-    if (js.x + 1 < ji.x) {
-      jst.set(j, make_int2(js.x + 1, (int)rdy));
-      continue;
-    }
-    jst.set(j, make_int2(0, 0));  // leave the join state clean
-    // the join's op, or for a barrier its first member (the others follow it)
-    release(rdy, ji.y);
+    for (; e < nsucc; ++e) one(e);
   }
   if (hole) heap_pop_root(heap, end, A);
 }
