@@ -126,8 +126,10 @@ int32_t min_path_cover(int32_t n, const std::vector<std::vector<int32_t>> &adj) 
 // / succs as CSR) and take the lowest slot whose latest holder qualifies,
 // else a new one.  Ancestor sets (bitsets over join ids) are kept only while
 // a successor of their node is unvisited; when they would need more than
-// kJoinSlotBudget bytes, every join keeps a slot of its own.
+// kJoinSlotBudget bytes, every join keeps a slot of its own.  Only the
+// first kJoinSlotScan slots are tried for each join (a bound on the time).
 constexpr size_t kJoinSlotBudget = size_t(256) << 20;
+constexpr size_t kJoinSlotScan = 4096;
 
 int32_t assign_join_slots(int32_t N, const std::vector<int32_t> &p_ptr, const std::vector<int32_t> &p,
                           const std::vector<int32_t> &s_ptr, const std::vector<int32_t> &s,
@@ -165,8 +167,10 @@ int32_t assign_join_slots(int32_t N, const std::vector<int32_t> &p_ptr, const st
       }
     const int32_t j = jid[x];
     if (j >= 0) {
+      const size_t scan = std::min(holder.size(), kJoinSlotScan);
       size_t k = 0;
-      while (k < holder.size() && !(ca[(size_t)holder[k] / 64] >> (holder[k] % 64) & 1)) ++k;
+      while (k < scan && !(ca[(size_t)holder[k] / 64] >> (holder[k] % 64) & 1)) ++k;
+      if (k == scan) k = holder.size();
       if (k == holder.size()) holder.push_back(j);
       holder[k] = j;
       slot[j] = (int32_t)k;
