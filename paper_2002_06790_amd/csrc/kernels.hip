@@ -325,8 +325,8 @@ struct EvArgs {
 
 // finish times buffered per lane before a store burst: sixteen where the
 // registers allow it without costing occupancy and it measured faster (the
-// register-children variants, which run two wavefronts per SIMD anyway,
-// with loaded durations), else eight
+// register-children variants with loaded durations, also those recording
+// predecessors: at most two wavefronts per SIMD either way), else eight
 constexpr int kFinQ = 8, kFinQWide = 16;
 
 // A lane's join state {predecessors finished, max finish} per join index, in
@@ -681,7 +681,7 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
     int end = kRoot;  // one past the last heap position
     for (int k = 0; k < G.nsrc; ++k) heap_push(heap, end, make_key(0, G.ev_src[k]));
     uint32_t st = 0, span = 0;
-    constexpr int kQ = REG && !PREV && !GEN ? kFinQWide : kFinQ;
+    constexpr int kQ = REG && !GEN ? kFinQWide : kFinQ;
     int32_t fq[kQ], rq[kQ], pq[kQ];  // buffered finish times, their rows, previous ops
     auto flush = [&](int cnt) {
 #pragma unroll
