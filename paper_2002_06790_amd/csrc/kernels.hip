@@ -471,7 +471,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
         if (PREV) pq[k] = before;
       }
   }
-  if (qs == FQ - 1) flush(FQ);
+  // a full burst goes out here, or for the placement kernels at the end of
+  // the step (one counter covers loads and stores, so the loads of their
+  // successor groups would wait behind it; the others measured faster here)
+  if (!PLACE && qs == FQ - 1) flush(FQ);
   bool hole = true;  // the root was popped and is not yet replaced
   auto release = [&](uint32_t t, int w) {
     const uint64_t nk = make_key(t, w);
@@ -587,6 +590,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     for (; e < nsucc; ++e) one(e);
   }
   if (hole) heap_pop_root(heap, end, A);
+  if (PLACE && qs == FQ - 1) flush(FQ);
 }
 
 // Event-driven list scheduling, one scenario per lane (the paper's replay
