@@ -216,8 +216,8 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
         hset(i, key);
         return true;
       };
-      auto pop = [&]() -> uint64_t {
-        const uint64_t top = hget(0);
+      // remove the minimum (the caller read it): the last key sifted down
+      auto pop_rest = [&]() {
         const uint64_t last = hget(--hs);
         int64_t i = 0;
         for (;;) {
@@ -251,7 +251,6 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           i = m;
         }
         if (hs > 0) hset(i, last);
-        return top;
       };
       auto key_of = [](uint32_t t, uint32_t w) -> uint64_t { return ((uint64_t)t << 32) | w; };
       bool ok = true;
@@ -321,11 +320,39 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
       // every iteration pops one key and a replay pushes at most max_keys,
       // so the loop ends; the guard only bounds it explicitly
       for (int64_t it = 0; hs > 0 && ok && it <= a.max_keys; ++it) {
-        const uint64_t key = pop();
+        const uint64_t key = hget(0);
         const uint32_t t = (uint32_t)(key >> 32), w = (uint32_t)key;
-        if (w < (uint32_t)R) {  // a pending finish on shared resource w
-          const int r = (int)w;
-          LinkSt L = lk[r];
+        // The event's loads go out before the minimum is removed from the
+        // heap (they read nothing the heap holds), so their round trip
+        // overlaps the sift-down's: for a pending finish the resource's
+        // state, for a ready op its record, its duration and (when the key
+        // word names the resource) the resource's state.
+        const bool lnk = w < (uint32_t)R;
+        const uint32_t u = w - (uint32_t)R;
+        const int c = lnk ? 0 : a.kres ? (int)(u >> a.rb) : (int)u;
+        int4 A = make_int4(0, 0, 0, 0), B = A;
+        int32_t d = 0;
+        int r = lnk ? (int)w : 0;
+        bool shr = lnk;
+        LinkSt L{};
+        uint32_t rfree = 0;
+        if (lnk) {
+          L = lk[r];
+        } else {
+          A = rec4[2 * c];
+          B = rec4[2 * c + 1];
+          if (a.rows_identity) d = a.dur[(int64_t)c * a.ld_dur + s];
+          if (a.kres) {
+            r = (int)(u & rmask);
+            shr = shared_res(r);
+            if (shr)
+              L = lk[r];
+            else
+              rfree = rf[r];
+          }
+        }
+        pop_rest();
+        if (lnk) {  // a pending finish on shared resource r
           if (L.k == 0 || L.pk != t) continue;  // superseded
           if (L.nd != t) {  // arrivals since moved the next finish later: key it now
             L.pk = L.nd;
@@ -389,21 +416,16 @@ __global__ __launch_bounds__(kWave) void k_share(DevGraph G, ShArgs a) {
           lk[r] = L;
           continue;
         }
-        // a ready op: its record, its duration and (the resource named by
-        // the key word) the resource's state, all requested before the first
-        // is used
-        const uint32_t u = w - (uint32_t)R;
-        const int c = a.kres ? (int)(u >> a.rb) : (int)u;
-        const int4 A = rec4[2 * c], B = rec4[2 * c + 1];
-        int32_t d = a.rows_identity ? a.dur[(int64_t)c * a.ld_dur + s] : 0;
-        const int r = a.kres ? (int)(u & rmask) : A.y;
-        const bool shr = shared_res(r);
-        LinkSt L;
-        uint32_t rfree = 0;
-        if (shr)
-          L = lk[r];
-        else
-          rfree = rf[r];
+        // a ready op (its resource from the record when the key word has
+        // no room for it)
+        if (!a.kres) {
+          r = A.y;
+          shr = shared_res(r);
+          if (shr)
+            L = lk[r];
+          else
+            rfree = rf[r];
+        }
         if (!a.rows_identity) d = a.dur[(int64_t)A.x * a.ld_dur + s];
         if (shr) {  // joins the resource's active ops at its ready time
           const int k = L.k;
