@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "philox.hpp"
 #include "regarr.hpp"
@@ -534,43 +535,40 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
       // the join's op, or for a barrier its first member (the others follow it)
       release(rdy, ji.y);
     };
-    // entry e from e0 (the join state of its join already read with the
-    // record when the key named it), e1 (unless the record points to the
-    // list) or the successor list
-    auto one = [&](int e) {
-      const int2 sw = e == 0 ? e0 : e == 1 && !more ? e1 : settle(succ[sbeg + e]);
-      int2 js = js0, ji = ji0;
-      if (sw.y >= 0 && !(e == 0 && G.pk_join)) {
-        const int j = G.pk_jn ? (sw.y & 0xffff) : sw.y;
-        js = settle(jst.get(j));
-        if (!G.pk_jn) ji = settle(G.jinfo[j]);
-      }
-      handle(sw, js, ji);
-    };
-    // The placement kernels issue the first four entries' loads together and
-    // then their joins' states together (two round trips instead of one per
-    // join; their ops release two or three joins each, and at one wavefront
-    // per CU the extra loads of absent entries, issued at clamped valid
-    // indices and discarded, cost little).  The successors of one op are
-    // distinct nodes whose joins never share a slot, so none of these loads
-    // can see a store of the same group.  (The other kernels take one entry
-    // at a time, which needs fewer registers and no wasted loads.)
-    constexpr int kC = 4;
-    int e = 0;
-    if (__ballot(nsucc > 0)) {  // some lane has entries: the list is not empty
-      int2 sw[kC], js[kC], ji[kC];
+    // The placement kernels take an op's first kC entries as one chunk: the
+    // chunk's entries requested together, then their joins' states together,
+    // two round trips in all instead of two per join.  Their ops release two
+    // or three joins each, but the lanes of a wavefront pop different ops
+    // and every lane waits for the one with the most entries (on random
+    // layered graphs the largest of 64 lanes' counts is about eight: 4 and
+    // 4 + 4 entries measured 10 % slower than 8, 12 and 16 slower too).
+    // Entries beyond the chunk, rare, follow kC1 at a time.  Absent entries
+    // load from clamped valid indices (one address, or one lane-major row,
+    // across lanes) and are discarded; at one wavefront per CU they cost
+    // little.  The successors of one op are distinct nodes whose joins never
+    // share a slot, so none of these loads can see a store of the same op.
+    // (The other kernels take one entry at a time, which needs fewer
+    // registers and no wasted loads.)  The first chunk holds the inline
+    // entries: e0 (its join's state already read with the record when the
+    // key named it) and e1 (unless the record points to the list).
+    constexpr int kC = 8, kC1 = 1;
+    auto chunk = [&](auto first_tag, auto size_tag, int base) {
+      constexpr bool F = decltype(first_tag)::value;
+      constexpr int C = decltype(size_tag)::value;
+      int2 sw[C], js[C], ji[C];
 #pragma unroll
-      for (int k = 0; k < kC; ++k) {
-        const bool listed = k < nsucc && !(k == 0 || (k == 1 && !more));
-        const int2 m = succ[listed ? sbeg + k : 0];
-        sw[k] = k == 0 ? e0 : k == 1 && !more ? e1 : m;
+      for (int k = 0; k < C; ++k) {
+        const int e = base + k;
+        const bool inl = F && (k == 0 || (k == 1 && !more));
+        const int2 m = succ[e < nsucc && !inl ? sbeg + e : 0];
+        sw[k] = !F ? m : k == 0 ? e0 : k == 1 && !more ? e1 : m;
       }
 #pragma unroll
-      for (int k = 0; k < kC; ++k) sw[k] = settle(sw[k]);
+      for (int k = 0; k < C; ++k) sw[k] = settle(sw[k]);
 #pragma unroll
-      for (int k = 0; k < kC; ++k) {
-        const bool first = k == 0 && G.pk_join;
-        const bool joined = k < nsucc && sw[k].y >= 0 && !first;
+      for (int k = 0; k < C; ++k) {
+        const bool first = F && k == 0 && G.pk_join;
+        const bool joined = base + k < nsucc && sw[k].y >= 0 && !first;
         const int j = joined ? (G.pk_jn ? (sw[k].y & 0xffff) : sw[k].y) : 0;
         const int2 vs = G.J > 0 ? jst.get(j) : make_int2(0, 0);
         const int2 vi = G.J > 0 && !G.pk_jn ? G.jinfo[j] : make_int2(0, 0);
@@ -578,16 +576,19 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
         ji[k] = first ? ji0 : vi;
       }
 #pragma unroll
-      for (int k = 0; k < kC; ++k) {
+      for (int k = 0; k < C; ++k) {
         js[k] = settle(js[k]);
         ji[k] = settle(ji[k]);
       }
 #pragma unroll
-      for (int k = 0; k < kC; ++k)
-        if (k < nsucc) handle(sw[k], js[k], ji[k]);
-      e = kC;
+      for (int k = 0; k < C; ++k)
+        if (base + k < nsucc) handle(sw[k], js[k], ji[k]);
+    };
+    if (__ballot(nsucc > 0)) {  // some lane has entries
+      chunk(std::true_type{}, std::integral_constant<int, kC>{}, 0);
+      for (int base = kC; __ballot(base < nsucc); base += kC1)
+        chunk(std::false_type{}, std::integral_constant<int, kC1>{}, base);
     }
-    for (; e < nsucc; ++e) one(e);
   }
   if (hole) heap_pop_root(heap, end, A);
   if (PLACE && qs == FQ - 1) flush(FQ);
