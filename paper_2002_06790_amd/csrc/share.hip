@@ -48,6 +48,10 @@ constexpr uint32_t kI32Max = 0x7fffffffu;
 constexpr uint32_t kNoTime = 0xffffffffu;
 constexpr int64_t kShareHeapLds = 21;    // heap positions per lane in LDS: the top three levels (10.5 KB per wavefront)
 constexpr int64_t kShareFlagsLds = 1024; // resource flags in LDS (4 KB) up to this many resources
+// a pop reads a child group 4i + 1 .. 4i + 4 from LDS when it starts there,
+// so no group may straddle the end of the LDS part (a smaller heap, whose
+// positions from its capacity on are all empty, needs no such care)
+static_assert(kShareHeapLds % 4 == 1, "the LDS part of the heap must end at a child group boundary");
 
 struct ShArgs {
   int64_t n_scen;
