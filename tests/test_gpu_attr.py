@@ -86,6 +86,22 @@ def test_attr_workloads(mlsim, k, S):
                place=w.placement(), path_scen=S - 1)
 
 
+def test_attr_placement_wide_fanout(mlsim):
+    """Attribution under a placement on layered graphs whose ops have up to
+    24 successors (the placement replay's grouped successor entries, with
+    predecessor recording)."""
+    from test_gpu_parity import wide_layered
+    rng = np.random.default_rng(1618)
+    for case, (levels, width, max_in) in enumerate([(6, 24, 12), (5, 20, 20)]):
+        ptr, idx = wide_layered(rng, levels, width, max_in)
+        n, R, S = levels * width, int(rng.integers(2, 9)), 70
+        print(f"case {case}: n={n} R={R} S={S} max out-degree {np.diff(ptr).max()}", flush=True)
+        res = rng.integers(0, R, size=n).astype(np.int32)
+        dur = W.random_durations(n, S, 1, int(rng.choice([3, 5000])), rng)
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16)
+        check_attr(mlsim, ptr, idx, res, R, dur, place=place, path_scen=S - 1)
+
+
 def test_attr_random_graphs(mlsim):
     """Random DAGs with priorities, repeated edges, placement and small
     duration ranges (many equal times, so the tie rules matter)."""

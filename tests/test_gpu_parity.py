@@ -129,6 +129,43 @@ def test_random_graphs(mlsim):
         check_cp(mlsim, ptr, idx, res, R, dur, paths=(0,))
 
 
+def wide_layered(rng, levels, width, max_in):
+    """Levels of `width` ops, each op past the first fed by 1..max_in distinct
+    ops of the previous level: out-degrees up to `width`, every edge direct
+    (a layered graph has no longer path between consecutive levels), mixing
+    joins with ops of one predecessor.  Returns (succ_ptr, succ_idx)."""
+    succ = [[] for _ in range(levels * width)]
+    for L in range(1, levels):
+        for v in range(L * width, (L + 1) * width):
+            k = int(rng.integers(1, max_in + 1))
+            for u in rng.choice(width, size=k, replace=False):
+                succ[(L - 1) * width + int(u)].append(v)
+    ptr = np.zeros(len(succ) + 1, np.int64)
+    ptr[1:] = np.cumsum([len(x) for x in succ])
+    idx = np.array([x for l in succ for x in l], np.int32)
+    return ptr, idx
+
+
+def test_placement_wide_fanout(mlsim):
+    """Ops with up to 24 successors under a placement: the placement replay
+    takes an op's first eight entries as one group and the rest one at a
+    time, so lanes whose ops have 0, 1, 2, 8, 9 and many more successors
+    (joins and ops with a single predecessor among them) meet in one
+    wavefront.  Ragged scenario count; priorities on every other case."""
+    rng = np.random.default_rng(2411)
+    for case, (levels, width, max_in) in enumerate([(6, 24, 12), (12, 16, 8), (4, 24, 24), (9, 12, 9)]):
+        ptr, idx = wide_layered(rng, levels, width, max_in)
+        n, R, S = levels * width, int(rng.integers(2, 9)), 131
+        deg = np.diff(ptr)
+        print(f"case {case}: n={n} R={R} S={S} max out-degree {deg.max()}", flush=True)
+        assert deg.max() > 8
+        res = rng.integers(0, R, size=n).astype(np.int32)
+        pr = rng.integers(-3, 4, size=n).astype(np.int32) if case % 2 else None
+        dur = W.random_durations(n, S, 1, 5000, rng)
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16)
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr, place=place)
+
+
 def test_random_with_placement(mlsim):
     rng = np.random.default_rng(7)
     for _ in range(10):
