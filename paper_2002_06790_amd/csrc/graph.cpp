@@ -406,6 +406,29 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
     const auto &mem = bmem[b];
     for (size_t i = 0; i + 1 < mem.size(); ++i) es[mem[i]].insert(es[mem[i]].begin(), mem[i + 1]);
   }
+  // Fans: the successors of an op p whose only predecessor is p share p's
+  // output time as their ready time, so they too can be chained: p releases
+  // the first, and popping member i releases member i + 1 (the pop order is
+  // unchanged by the argument above).  Chained only where p has more than two
+  // entries (two are held in its record, the rest read one after another
+  // from the successor list) and only members whose own list is at most one
+  // plain entry, so each member still holds its entries in its record and
+  // its key word still names its first join (it has none).
+  std::vector<std::vector<int32_t>> fans;
+  auto is_join = [&](int32_t x) { return x >= n || need[x] >= 2; };
+  for (int32_t p = 0; p < n; ++p) {
+    if (es[p].size() <= 2) continue;
+    std::vector<int32_t> mem;
+    for (int32_t w : es[p])
+      if (w < n && need[w] == 1 && cp[w].size() == 1 && es[w].size() <= 1 && (es[w].empty() || !is_join(es[w][0])))
+        mem.push_back(w);
+    if (mem.size() < 2) continue;
+    std::vector<int32_t> keep;
+    std::set_difference(es[p].begin(), es[p].end(), mem.begin() + 1, mem.end(), std::back_inserter(keep));
+    es[p].swap(keep);
+    for (size_t i = 0; i + 1 < mem.size(); ++i) es[mem[i]].insert(es[mem[i]].begin(), mem[i + 1]);
+    fans.push_back(std::move(mem));
+  }
 
   // Walk graph (pull model): node ids are the compact ops 0..n-1 and the
   // barriers n..n+nb-1.  A barrier's predecessors are its shared set; each
@@ -471,10 +494,12 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   C.ops.resize(n + nb + 1);
   C.succ.clear();
   int32_t e = 0;
-  // sibling entries: the first entry of a barrier member that has a next one
+  // sibling entries: the first entry of a barrier or fan member that has a next one
   std::vector<uint8_t> has_sib(n, 0);
   for (int32_t b = 0; b < nb; ++b)
     for (size_t i = 0; i + 1 < bmem[b].size(); ++i) has_sib[bmem[b][i]] = 1;
+  for (const auto &mem : fans)
+    for (size_t i = 0; i + 1 < mem.size(); ++i) has_sib[mem[i]] = 1;
   for (int32_t c = 0; c < n + nb; ++c) {
     std::vector<int32_t> lst = c < n ? es[c] : std::vector<int32_t>{bmem[c - n][0]};
     std::vector<int32_t> jl(lst.size());
