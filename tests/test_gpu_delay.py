@@ -98,6 +98,63 @@ def test_zero_delays_equal_plain_and_gap_replay(mlsim):
     g.close()
 
 
+def fan_graph(rng, n_src, width):
+    """Sources each releasing a fan of 2..width ops whose only predecessor
+    it is, each fan op with no successor or one that has a single
+    predecessor (the ops the library may chain), a few fan ops that also
+    join two fans (not chained), and one sink joining everything left
+    open.  Returns (succ_ptr, succ_idx, n)."""
+    succ, n = [], 0
+
+    def new():
+        nonlocal n
+        succ.append([])
+        n += 1
+        return n - 1
+
+    srcs = [new() for _ in range(n_src)]
+    fans = []
+    for u in srcs:
+        fan = [new() for _ in range(int(rng.integers(2, width + 1)))]
+        succ[u].extend(fan)
+        for v in fan:
+            if rng.integers(2):
+                succ[v].append(new())
+        fans.append(fan)
+    for a, b in zip(fans, fans[1:]):  # a join of two fans' last ops
+        j = new()
+        succ[a[-1]].append(j)
+        succ[b[-1]].append(j)
+    sink = new()
+    for v in range(n - 1):
+        if not succ[v]:
+            succ[v].append(sink)
+    ptr = np.zeros(n + 1, np.int64)
+    ptr[1:] = np.cumsum([len(x) for x in succ])
+    return ptr, np.array([x for l in succ for x in l], np.int32), n
+
+
+def test_fans_with_delays(mlsim):
+    """Fans of ops with one predecessor: chained members release each other
+    at the source's output time (its finish plus its resource's delay),
+    whatever their own resources and priorities; with and without gaps and a
+    placement."""
+    rng = np.random.default_rng(31)
+    for case in range(6):
+        ptr, idx, n = fan_graph(rng, int(rng.integers(1, 6)), int(rng.choice([3, 8, 13])))
+        R, S = int(rng.integers(2, 7)), 131
+        res = rng.integers(0, R, size=n).astype(np.int32)
+        prio = rng.integers(-3, 4, size=n).astype(np.int32) if case % 2 else None
+        dur = W.random_durations(n, S, 1, int(rng.choice([4, 5000])), rng)
+        delay = rng.integers(0, 6000, size=R).astype(np.int32)
+        gap = rng.integers(0, 2000, size=R).astype(np.int32) if case % 3 == 0 else None
+        place = rng.integers(0, R, size=(n, S)).astype(np.uint16) if case % 3 == 1 else None
+        print(f"fans case {case}: n={n} R={R} prio={prio is not None} gap={gap is not None} "
+              f"place={place is not None}", flush=True)
+        check(mlsim, ptr, idx, res, R, dur, None, None, prio=prio, place=place)
+        check(mlsim, ptr, idx, res, R, dur, gap, delay, prio=prio, place=place)
+
+
 def test_random_graphs_many_resources(mlsim):
     """Barriers of ops sharing predecessors, resource tables too large for
     LDS, priorities, duplicate edges, ragged tiles."""
