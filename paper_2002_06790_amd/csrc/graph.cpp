@@ -409,22 +409,27 @@ int compile(int32_t n, int32_t R, const int64_t *succ_ptr, const int32_t *succ_i
   // Fans: the successors of an op p whose only predecessor is p share p's
   // output time as their ready time, so they too can be chained: p releases
   // the first, and popping member i releases member i + 1 (the pop order is
-  // unchanged by the argument above).  Chained only where p has more than two
-  // entries (two are held in its record, the rest read one after another
-  // from the successor list) and only members whose own list is at most one
-  // plain entry, so each member still holds its entries in its record and
-  // its key word still names its first join (it has none).
+  // unchanged by the argument above; members are chained in compact-id
+  // order, which is their key order).  Chained only where p has more than
+  // two entries (two are held in its record, the rest read one after
+  // another from the successor list) and only members whose own list is at
+  // most one entry, so each member still holds its entries in its record.
+  // (A member's join then follows its sibling entry, so its state is read
+  // after the record instead of with it: one round trip in the member's
+  // step against the list reads saved in p's.)
   std::vector<std::vector<int32_t>> fans;
-  auto is_join = [&](int32_t x) { return x >= n || need[x] >= 2; };
   for (int32_t p = 0; p < n; ++p) {
     if (es[p].size() <= 2) continue;
     std::vector<int32_t> mem;
     for (int32_t w : es[p])
-      if (w < n && need[w] == 1 && cp[w].size() == 1 && es[w].size() <= 1 && (es[w].empty() || !is_join(es[w][0])))
+      if (w < n && need[w] == 1 && cp[w].size() == 1 && es[w].size() <= 1)
         mem.push_back(w);
     if (mem.size() < 2) continue;
+    std::sort(mem.begin(), mem.end());
+    // (order kept: p may be a barrier member whose sibling entry comes first)
     std::vector<int32_t> keep;
-    std::set_difference(es[p].begin(), es[p].end(), mem.begin() + 1, mem.end(), std::back_inserter(keep));
+    for (int32_t x : es[p])
+      if (x == mem[0] || !std::binary_search(mem.begin() + 1, mem.end(), x)) keep.push_back(x);
     es[p].swap(keep);
     for (size_t i = 0; i + 1 < mem.size(); ++i) es[mem[i]].insert(es[mem[i]].begin(), mem[i + 1]);
     fans.push_back(std::move(mem));

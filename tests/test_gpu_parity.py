@@ -166,6 +166,51 @@ def test_placement_wide_fanout(mlsim):
         check_run(mlsim, ptr, idx, res, R, dur, prio=pr, place=place)
 
 
+def test_barrier_member_with_fan(mlsim):
+    """Ops sharing a predecessor set (barrier members: each but the last
+    releases the next through a sibling entry, first in its list) whose own
+    successors form a fan of ops with a single predecessor (chained too).
+    Ids are laid out so that the fan's ids fall below and above the next
+    member's, with and without priorities, gaps and delays."""
+    rng = np.random.default_rng(77)
+    for case in range(8):
+        k = int(rng.integers(3, 7))  # fan size of the first member
+        # ids: fan ops, then the sources and the members (or the reverse)
+        low_fans = case % 2 == 0
+        nf, nm = k + 2, 3
+        fan_ids = list(range(nf)) if low_fans else list(range(2 + nm, 2 + nm + nf))
+        base = nf if low_fans else 0
+        a, b = base, base + 1
+        mem = [base + 2 + i for i in range(nm)]
+        n = nf + 2 + nm
+        succ = [[] for _ in range(n)]
+        for m in mem:
+            succ[a].append(m)
+            succ[b].append(m)
+        succ[mem[0]] = fan_ids[:k]                  # the fan
+        succ[mem[1]] = fan_ids[k:]                  # two more ops with one predecessor
+        for f in fan_ids[:k:2]:                     # some fan ops also feed one of those (a join)
+            succ[f].append(fan_ids[-1])
+        ptr = np.zeros(n + 1, np.int64)
+        ptr[1:] = np.cumsum([len(x) for x in succ])
+        idx = np.array([x for l in succ for x in l], np.int32)
+        R = int(rng.integers(1, 4))
+        res = rng.integers(0, R, size=n).astype(np.int32)
+        pr = rng.integers(-2, 3, size=n).astype(np.int32) if case % 4 >= 2 else None
+        dur = W.random_durations(n, 67, 1, int(rng.choice([3, 900])), rng)
+        print(f"case {case}: n={n} fan {k} low ids {low_fans} prio {pr is not None}", flush=True)
+        check_run(mlsim, ptr, idx, res, R, dur, prio=pr)
+        g = mlsim.Graph(ptr, idx, res, R, prio=pr)
+        gap = rng.integers(0, 50, size=R).astype(np.int32)
+        delay = rng.integers(0, 50, size=R).astype(np.int32)
+        mk, fin, st = g.run(dev(dur), want_finish=True, gap=gap, delay=delay)
+        torch.cuda.synchronize()
+        omk, ofin, ost = oracle.run_batch(ptr, idx, res, R, dur, prio=pr, gap=gap, delay=delay)
+        assert np.array_equal(st.cpu().numpy(), ost) and np.array_equal(mk.cpu().numpy(), omk)
+        assert np.array_equal(fin.cpu().numpy(), ofin)
+        g.close()
+
+
 def test_random_with_placement(mlsim):
     rng = np.random.default_rng(7)
     for _ in range(10):
