@@ -20,7 +20,8 @@ constexpr int kWave = 64;  // CDNA wavefront width: one scenario per lane
 // barrier instead of each counting the predecessors itself; a barrier has no
 // duration or resource.  When it completes it releases its first member
 // (lowest compact id); each member then releases the next one, at the same
-// ready time, through a sibling entry (join index kJoinSibling).
+// ready time, through a sibling entry (join index kJoinSibling).  The ops
+// whose only predecessor is one op (a fan) may be chained the same way.
 
 // join index of a successor entry: a join counter, or one of these
 constexpr int32_t kJoinNone = -1;     // released at the op's finish time
