@@ -321,7 +321,6 @@ struct EvArgs {
   // outputs reach its successors (output delay)
   const int32_t *dev;
   int dev_gap, dev_delay;  // which of the two halves apply (uniform)
-  int dev_lds;             // byte offset of the device-model table in LDS (when dev is set)
 };
 
 // finish times buffered per lane before a store burst: sixteen where the
@@ -344,7 +343,7 @@ template <bool DEEP, bool RF_LDS, bool ROW_ID, bool PLACE, bool PREV, bool GEN, 
 __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, Heap &heap,
                                            int &end, JPtr jst, int it, int64_t s,
                                            int64_t sc, const int32_t *brow, uint32_t s_lo,
-                                           uint32_t s_hi, lptr<const int32_t> dev_l, uint32_t &st,
+                                           uint32_t s_hi, uint32_t &st,
                                            uint32_t &span,
                                            int32_t (&fq)[FQ], int32_t (&rq)[FQ],
                                            int32_t (&pq)[FQ], RfGet rf_get, RfSet rf_set,
@@ -404,6 +403,11 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
     st |= SIM_ST_BAD_RES;
     r = 0;
   }
+  // the device model's gap and delay of the resource: a small table read
+  // from global memory (cached), requested before the duration is used
+  int32_t gapv = 0, dlyv = 0;
+  if (a.dev_gap) gapv = a.dev[r];
+  if (a.dev_delay) dlyv = a.dev[R + r];
   if (d < 1) {
     st |= SIM_ST_BAD_DUR;
     d = 1;
@@ -420,11 +424,11 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   // saturated at 2^31, which still makes any later finish overflow)
   uint32_t avail = fin, out = fin;
   if (a.dev_gap) {
-    const uint32_t x = fin + (uint32_t)dev_l[r];
+    const uint32_t x = fin + (uint32_t)gapv;
     avail = x < kI32Max + 1u ? x : kI32Max + 1u;
   }
   if (a.dev_delay) {
-    const uint32_t x = fin + (uint32_t)dev_l[R + r];
+    const uint32_t x = fin + (uint32_t)dlyv;
     out = x < kI32Max + 1u ? x : kI32Max + 1u;
   }
   rf_set(r, avail);
@@ -616,13 +620,6 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
   extern __shared__ uint64_t lds[];
   const int lane = threadIdx.x;
   const int n = G.n, R = G.R;
-  // device model (one table per wave, after every per-lane region)
-  const lptr<int32_t> dev_w = as_lds((int32_t *)((char *)lds + a.dev_lds));
-  if (a.dev) {
-    for (int r = lane; r < 2 * R; r += kWave) dev_w[r] = a.dev[r];
-    __syncthreads();
-  }
-  const lptr<const int32_t> dev_l = (lptr<const int32_t>)dev_w;
   WideHeap<REG> heap;
   heap.l = as_lds(lds) + lane;
   heap.g = a.heap_g + ((size_t)blockIdx.x * kWave + lane) * a.heap_stride;
@@ -702,11 +699,11 @@ __global__ __launch_bounds__(kWave) void k_event(DevGraph G, EvArgs a) {
       auto run_step = [&](auto jp) {
         if (__ballot(end > heap.le))
           event_step<true, RF_LDS, ROW_ID, PLACE, PREV, GEN, LAZY>(G, a, heap, end, jp, it, s, sc, brow, s_lo, s_hi,
-                                                             dev_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                             st, span, fq, rq, pq, rf_get, rf_set,
                                                              last_xchg, flush);
         else
           event_step<false, RF_LDS, ROW_ID, PLACE, PREV, GEN, LAZY>(G, a, heap, end, jp, it, s, sc, brow, s_lo,
-                                                              s_hi, dev_l, st, span, fq, rq, pq, rf_get, rf_set,
+                                                              s_hi, st, span, fq, rq, pq, rf_get, rf_set,
                                                               last_xchg, flush);
       };
       run_step(jst_g);
@@ -1222,8 +1219,6 @@ int plan_scratch(sim_graph *g) {
   const size_t join_bytes = (size_t)G.J * kWave * 8;
   const size_t heap_g_bytes = (size_t)P.ev_heap_stride * kWave * 8;
   const size_t ev_per_block = join_bytes + heap_g_bytes + (rf_lds ? 0 : rf_bytes);
-  // device model (gaps, output delays), after the per-lane regions
-  const size_t dev_table = ((size_t)G.R * 8 + 15) & ~size_t(15);
   auto grid_of = [&](int occ) -> int32_t {  // resident blocks within the scratch budget
     size_t b = (size_t)std::max(occ, 1);
     if (ev_per_block) b = std::min(b, std::max<size_t>(1, kScratchBudget / ev_per_block));
@@ -1232,15 +1227,15 @@ int plan_scratch(sim_graph *g) {
   };
   // the root's children in LDS (every variant)
   P.ev_lds_bytes = (size_t)(P.ev_heap_le - kL1) * kWave * 8 + rf_lds_bytes;
-  int occ[3];  // plain, generated durations, device model
+  int occ[3];  // plain, generated durations, device model (its table is read from global memory)
   if (rf_lds) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false>, P.ev_lds_bytes + dev_table, cus);
+    occ[2] = occ[0];
   } else {
     occ[0] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<false, false, false, false, true>, P.ev_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<false, false, false, false>, P.ev_lds_bytes + dev_table, cus);
+    occ[2] = occ[0];
   }
   if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
   P.ev_blocks = grid_of(occ[0]);
@@ -1251,8 +1246,6 @@ int plan_scratch(sim_graph *g) {
   P.ev_reg = rf_lds;
   P.ev_reg_lds_bytes = (size_t)(P.ev_heap_le - kL2) * kWave * 8 + rf_lds_bytes;
   P.ev_reg_blocks = P.ev_reg_gen_blocks = P.ev_reg_dev_blocks = P.ev_reg_prev_blocks = 1;
-  P.ev_reg_dev_le = P.ev_heap_le;
-  P.ev_reg_dev_lds_bytes = P.ev_reg_lds_bytes;
   // the last-op table of attribution: 16-bit rows when every row fits
   P.ev_last16 = G.n < 0xffff;
   const size_t last_lds_bytes = P.ev_last16 ? rf_lds_bytes / 2 : rf_lds_bytes;
@@ -1260,22 +1253,8 @@ int plan_scratch(sim_graph *g) {
   if (P.ev_reg) {
     occ[0] = occupancy_blocks(k_event<true, false, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
     occ[1] = occupancy_blocks(k_event<true, false, false, false, true, true>, P.ev_reg_lds_bytes, cus);
-    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes + dev_table,
-                              cus);
+    occ[2] = occupancy_blocks(k_event<true, false, false, false, false, true>, P.ev_reg_lds_bytes, cus);
     if (occ[0] < 0 || occ[1] < 0 || occ[2] < 0) return SIM_E_HIP;
-    // device model: when its table costs a wavefront per CU, keep one heap
-    // group fewer in LDS instead (measured faster on the BERT workload:
-    // two rounds of full CUs against three of lighter ones)
-    if (occ[2] < occ[0] && P.ev_heap_le > kL2 && V.ev_lds_groups < 0) {
-      const size_t fewer = P.ev_reg_lds_bytes - (size_t)kD * kWave * 8;
-      const int o = occupancy_blocks(k_event<true, false, false, false, false, true>, fewer + dev_table, cus);
-      if (o < 0) return SIM_E_HIP;
-      if (o > occ[2]) {
-        occ[2] = o;
-        P.ev_reg_dev_le = P.ev_heap_le - kD;
-        P.ev_reg_dev_lds_bytes = fewer;
-      }
-    }
     P.ev_reg_blocks = grid_of(occ[0]);
     P.ev_reg_gen_blocks = grid_of(occ[1]);
     P.ev_reg_dev_blocks = grid_of(occ[2]);
@@ -1302,12 +1281,12 @@ int plan_scratch(sim_graph *g) {
     if (rf_lds) {
       wo[0] = occupancy_blocks(k_event<true, false, false, false>, wl, cus, true);
       wo[1] = occupancy_blocks(k_event<true, false, false, false, true>, wl, cus, true);
-      wo[2] = occupancy_blocks(k_event<true, false, false, false>, wl + dev_table, cus, true);
+      wo[2] = wo[0];
       wo[3] = occupancy_blocks(k_event<true, false, false, true>, wl + last_lds_bytes, cus, true);
     } else {
       wo[0] = occupancy_blocks(k_event<false, false, false, false>, wl, cus, true);
       wo[1] = occupancy_blocks(k_event<false, false, false, false, true>, wl, cus, true);
-      wo[2] = occupancy_blocks(k_event<false, false, false, false>, wl + dev_table, cus, true);
+      wo[2] = wo[0];
       wo[3] = occupancy_blocks(k_event<false, false, false, true>, wl, cus, true);
     }
     if (wo[0] < 0 || wo[1] < 0 || wo[2] < 0 || wo[3] < 0) return SIM_E_HIP;
@@ -1437,7 +1416,7 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
            ext ? ext->join : (int2 *)(base + g->scratch_ev_join_off),
            ext ? ext->rf : (uint32_t *)(base + g->scratch_ev_rf_off),
            prev, ext ? nullptr : (int32_t *)(base + g->scratch_ev_last_off), P.ev_last16, DurGen{}, dev, has_gap,
-           has_delay, 0};
+           has_delay};
   if (gen) a.gen = *gen;
   const int64_t tiles = (n_scen + kWave - 1) / kWave;
   const bool rf_lds = P.rf_lds;
@@ -1454,9 +1433,8 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
                    : gen  ? P.ev_reg_gen_blocks
                    : dev  ? P.ev_reg_dev_blocks
                           : P.ev_reg_blocks;
-  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : dev && !gen ? P.ev_reg_dev_lds_bytes : P.ev_reg_lds_bytes)
+  size_t lds = reg ? (prev ? P.ev_reg_prev_lds_bytes : P.ev_reg_lds_bytes)
                    : (prev ? P.ev_prev_lds_bytes : P.ev_lds_bytes);
-  if (reg && dev && !prev && !gen) a.heap_le = P.ev_reg_dev_le;
   if (!reg && !ext) {  // few tiles: the whole third heap level in LDS
     const int64_t wide = prev ? P.ev_wide_prev_blocks
                          : gen ? P.ev_wide_gen_blocks
@@ -1473,10 +1451,6 @@ int launch_event_impl(const sim_graph *g, char *base, int64_t n_scen, const int3
   const int64_t tail = tiles - (rounds - 1) * blocks;
   const dim3 grid((unsigned)(2 * tail >= blocks ? std::min<int64_t>(tiles, blocks)
                                                 : (tiles + rounds - 1) / rounds));
-  if (dev) {  // the device-model table after the per-lane regions
-    a.dev_lds = (int)lds;
-    lds += ((size_t)g->dg.R * 8 + 15) & ~size_t(15);
-  }
   const int variant = (reg && !gen && !prev && !dev ? 128 : 0) | (reg ? 64 : 0) | (gen ? 16 : 0) | (prev ? 8 : 0) |
                       (rf_lds ? 4 : 0) | (g->dg.ev_compact ? 2 : 0) | (place ? 1 : 0);
 #define EV_CASE(V, A, B, C, D) \

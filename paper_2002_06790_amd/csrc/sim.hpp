@@ -143,10 +143,6 @@ struct ScratchPlan {
   // persistent grids (plain, generated durations, device model) and LDS per block
   int32_t ev_reg, ev_reg_blocks, ev_reg_gen_blocks, ev_reg_dev_blocks, ev_reg_prev_blocks;
   size_t ev_reg_lds_bytes, ev_reg_prev_lds_bytes;
-  // that kernel with a device model: one LDS heap group fewer when the
-  // model's table would otherwise cost a resident wavefront per CU
-  int32_t ev_reg_dev_le;
-  size_t ev_reg_dev_lds_bytes;
   size_t ev_prev_lds_bytes, at_lds_bytes;
   int32_t rf_lds;       // event kernel: resource times in LDS (1) or global scratch (0)
   int32_t ev_last16;    // attribution's last-op table in 16-bit rows (every row below 0xffff)
