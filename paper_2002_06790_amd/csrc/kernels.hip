@@ -351,6 +351,10 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   const int R = G.R;
   const int2 *succ = (const int2 *)G.ev_succ;
   const int4 *rec4 = (const int4 *)G.ev_ops;
+  // the step's loads go out at a raised wave priority (lowered once they
+  // are issued), so with several wavefronts per SIMD the one starting a
+  // step gets its requests in flight before others issue arithmetic
+  __builtin_amdgcn_s_setprio(2);
   const uint64_t key = heap.root;
   const uint32_t low = (uint32_t)key;  // key word: compact id, maybe resource and first join
   const int c = (int)(low >> G.pk_sh);
@@ -392,6 +396,7 @@ __device__ __forceinline__ void event_step(const DevGraph &G, const EvArgs &a, H
   heap_look_ahead<DEEP>(heap, end, A);
   // keep the scheduler from sinking these loads below the first use of d
   __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(0);
   const int32_t row = ROW_ID ? c : r0.x;
   if (!ROW_ID) {
     d = GEN ? brow[row] : a.dur[(int64_t)row * a.ld_dur + sc];
